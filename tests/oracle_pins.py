@@ -1,0 +1,387 @@
+"""Pins of the CPU oracle to facts that do not come from the oracle itself.
+
+Every pin is a plain function taking the loaded oracle library (a ctypes
+handle).  ``test_oracle_pins.py`` runs them against the real oracle;
+``test_oracle_mutants.py`` runs them against copies of the oracle with a
+planted mistake and requires that at least one pin fails for each.
+
+Sources of truth used here: closed forms (cosines of constructed angles,
+the logistic function), hand-worked examples (``golden/worked_examples.json``),
+invariants that follow from the equations (row sums, shift invariance,
+permutation equivariance), brute-force enumeration on tiny inputs, and
+special cases that reduce to a library routine (numpy stable argsort,
+torch.softmax in float64 on the CPU).
+"""
+
+from __future__ import annotations
+
+import itertools
+import json
+import math
+import os
+
+import numpy as np
+
+import oracle as O
+
+GOLDEN = json.load(open(os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                                     "worked_examples.json")))
+
+
+def _rot(d, rng):
+    q, _ = np.linalg.qr(rng.standard_normal((d, d)))
+    return q
+
+
+# ------------------------------------------------------------------ Eq. M --
+
+def pin_cosine_known_angles(lib):
+    """Sec. 4.3, equation for M.  Anchors and visual tokens lie in a rotated
+    plane at known angles with arbitrary positive lengths, so
+    M[i][j] = cos(alpha_i - beta_j) exactly."""
+    rng = np.random.default_rng(11)
+    d, nt, nv = 24, 5, 9
+    R = _rot(d, rng)
+    e1, e2 = R[0], R[1]
+    alpha = rng.uniform(-math.pi, math.pi, nt)
+    beta = rng.uniform(-math.pi, math.pi, nv)
+    ra = rng.uniform(0.1, 20.0, nt)
+    rb = rng.uniform(0.1, 20.0, nv)
+    A = (ra[:, None] * (np.cos(alpha)[:, None] * e1 + np.sin(alpha)[:, None] * e2))
+    V = (rb[:, None] * (np.cos(beta)[:, None] * e1 + np.sin(beta)[:, None] * e2))
+    M = O.cosine(A, V, lib=lib)
+    want = np.cos(alpha[:, None] - beta[None, :])
+    assert M.shape == (nt, nv)
+    assert np.max(np.abs(M - want)) < 1e-12
+
+
+def pin_cosine_zero_rule_and_bounds(lib):
+    """Zero vectors give 0 (reading of the equation for M); |M| <= 1; M is
+    unchanged by positive row scaling and flips sign with the visual token."""
+    rng = np.random.default_rng(12)
+    A = rng.standard_normal((4, 16))
+    V = rng.standard_normal((7, 16))
+    A[2] = 0.0
+    V[5] = 0.0
+    M = O.cosine(A, V, lib=lib)
+    assert np.all(M[2] == 0.0) and np.all(M[:, 5] == 0.0)
+    assert np.all(np.abs(M) <= 1.0 + 1e-15)
+    M2 = O.cosine(A * rng.uniform(0.5, 3.0, (4, 1)), V * rng.uniform(0.01, 9.0, (7, 1)), lib=lib)
+    assert np.max(np.abs(M2 - M)) < 1e-13
+    M3 = O.cosine(A, -V, lib=lib)
+    assert np.max(np.abs(M3 + M)) < 1e-15
+    # parallel vectors have cosine 1
+    M4 = O.cosine(V[:1] * 3.0, V[:1] * 0.25, lib=lib)
+    assert abs(M4[0, 0] - 1.0) < 1e-14
+
+
+# -------------------------------------------------------------- Eq. M-hat --
+
+def pin_center_worked_example(lib):
+    g = GOLDEN["center"]
+    out = O.center(np.array(g["M"]), lib=lib)
+    assert np.array_equal(out, np.array(g["Mhat"]))
+
+
+def pin_center_row_properties(lib):
+    """Each row of M-hat sums to zero and differs from M by a per-row
+    constant (together these fix M-hat = M - row mean)."""
+    rng = np.random.default_rng(13)
+    M = rng.uniform(-1, 1, (6, 11))
+    Mh = O.center(M, lib=lib)
+    assert np.max(np.abs(Mh.sum(axis=1))) < 1e-13
+    diff = M - Mh
+    assert np.max(np.abs(diff - diff[:, :1])) < 1e-14
+
+
+# ------------------------------------------------------------------ Eq. p --
+
+def pin_maxpool_worked_example(lib):
+    g = GOLDEN["maxpool"]
+    p = O.maxpool(np.array(g["Mhat"]), lib=lib)
+    assert np.array_equal(p, np.array(g["p"]))
+
+
+def pin_maxpool_properties(lib):
+    rng = np.random.default_rng(14)
+    Mh = rng.standard_normal((7, 13))
+    p = O.maxpool(Mh, lib=lib)
+    assert p.shape == (13,)
+    assert np.all(p[None, :] >= Mh)
+    assert all(p[j] in Mh[:, j] for j in range(13))
+
+
+# ---------------------------------------------------------------- top-k ----
+
+def _brute_topk(score, k):
+    """Enumerate every size-k subset; keep the largest score sum, breaking
+    ties by the lexicographically smallest index tuple.  Integer scores keep
+    the sums exact."""
+    best, best_sum = None, None
+    for comb in itertools.combinations(range(len(score)), k):
+        s = sum(score[c] for c in comb)
+        if best is None or s > best_sum or (s == best_sum and comb < best):
+            best, best_sum = comb, s
+    return np.array(best, np.int32)
+
+
+def pin_topk_bruteforce(lib):
+    rng = np.random.default_rng(15)
+    for trial in range(60):
+        n = int(rng.integers(1, 11))
+        k = int(rng.integers(1, n + 1))
+        score = rng.integers(-3, 4, n).astype(np.float64)  # many ties
+        got = O.topk(score, k, lib=lib)
+        assert np.array_equal(got, _brute_topk(list(score), k)), (score, k, got)
+
+
+def pin_topk_library_and_edges(lib):
+    """Stable argsort of -score (numpy) is the same total order; k = n is the
+    identity; +0 and -0 tie; output strictly increasing with exactly k."""
+    rng = np.random.default_rng(16)
+    for _ in range(20):
+        n = int(rng.integers(1, 300))
+        k = int(rng.integers(1, n + 1))
+        score = np.round(rng.standard_normal(n), 1)
+        got = O.topk(score, k, lib=lib)
+        want = np.sort(np.argsort(-score, kind="stable")[:k])
+        assert np.array_equal(got, want)
+        assert got.shape == (k,) and np.all(np.diff(got) > 0)
+    s = rng.standard_normal(17)
+    assert np.array_equal(O.topk(s, 17, lib=lib), np.arange(17))
+    z = np.array([1.0, -0.0, 0.0, -0.0, -1.0])
+    assert np.array_equal(O.topk(z, 2, lib=lib), [0, 1])
+    assert np.array_equal(O.topk(z, 3, lib=lib), [0, 1, 2])
+
+
+# ----------------------------------------------------- nearest centroid ----
+
+def pin_assign_constructed(lib):
+    """Sec. 4.3, last paragraph.  Each pruned token is a positive multiple of
+    one centroid plus a small perturbation, so its nearest centroid is known
+    by construction.  Decoy centroids with 100x the norm and a moderate
+    cosine (0.5) would win under an unnormalised dot product."""
+    rng = np.random.default_rng(17)
+    d, n1 = 64, 6
+    R = _rot(d, rng)
+    cents = R[:n1] * rng.uniform(0.5, 2.0, (n1, 1))
+    nv = 40
+    vis = np.zeros((nv, d))
+    kept = np.sort(rng.choice(nv, n1, replace=False)).astype(np.int32)
+    for s, j in enumerate(kept):
+        vis[j] = cents[s]
+    # make the last two centroids huge decoys
+    vis[kept[-1]] = 100.0 * R[n1 + 0]
+    vis[kept[-2]] = 100.0 * R[n1 + 1]
+    want = {}
+    for j in range(nv):
+        if j in kept:
+            continue
+        s = int(rng.integers(0, n1 - 2))
+        u = R[s] * rng.uniform(0.1, 5.0)
+        # a component towards a decoy: cosine to the decoy ~0.5, to its own ~0.85
+        u = u + 0.55 * np.linalg.norm(u) * R[n1 + 0] + 0.01 * rng.standard_normal(d)
+        vis[j] = u
+        want[j] = s
+    a, b1, b2 = O.assign(vis, kept, lib=lib)
+    for j, s in want.items():
+        assert a[j] == s, (j, a[j], s)
+        assert b1[j] > b2[j]
+    for s, j in enumerate(kept):
+        assert a[j] == s
+
+
+def pin_assign_twins_and_ties(lib):
+    """An exact copy of a kept token has cosine 1 to it (the maximum);
+    two identical centroids tie and the lower slot wins."""
+    rng = np.random.default_rng(18)
+    d = 32
+    vis = rng.standard_normal((8, d))
+    vis[6] = vis[2]          # twin of kept token 2
+    vis[4] = vis[1]          # kept tokens 1 and 4 are identical centroids
+    vis[7] = vis[1] * 2.0    # parallel to both -> tie -> lower slot (token 1)
+    kept = np.array([1, 2, 4, 5], np.int32)
+    a, b1, _ = O.assign(vis, kept, lib=lib)
+    assert a[6] == 1 and abs(b1[6] - 1.0) < 1e-14
+    assert a[7] == 0
+    assert list(a[kept]) == [0, 1, 2, 3]
+
+
+def pin_assign_subset_rows(lib):
+    rng = np.random.default_rng(19)
+    vis = rng.standard_normal((30, 16))
+    kept = np.array([0, 3, 9, 20, 29], np.int32)
+    full, f1, f2 = O.assign(vis, kept, lib=lib)
+    rows = np.array([28, 1, 7, 3], np.int32)
+    sub, s1, s2 = O.assign(vis, kept, rows, lib=lib)
+    assert np.array_equal(sub, full[rows])
+    assert np.array_equal(s1, f1[rows]) and np.array_equal(s2, f2[rows])
+
+
+# ----------------------------------------------------------------- merge ---
+
+def pin_merge_reading(lib):
+    """Pinned only to the reading (unweighted mean of centroid and members);
+    a centroid with no members is unchanged bit for bit."""
+    g = GOLDEN["merge"]
+    out = O.merge(np.array(g["vis"]), np.array(g["kept"]), np.array(g["assign"]), lib=lib)
+    assert np.array_equal(out, np.array(g["merged"]))
+    rng = np.random.default_rng(20)
+    vis = rng.standard_normal((9, 12))
+    vis[5] = vis[1]
+    kept = np.array([1, 3, 7], np.int32)
+    asg = np.array([0, 0, 0, 1, 1, 0, 2, 2, 2], np.int32)   # 1 absorbs its twin 5 and 0, 2
+    out = O.merge(vis, kept, asg, lib=lib)
+    assert np.array_equal(out[2], (vis[7] + vis[6] + vis[8]) / 3.0)
+    asg2 = np.array([1, 0, 1, 1, 1, 0, 1, 2, 1], np.int32)
+    out2 = O.merge(vis, kept, asg2, lib=lib)
+    assert np.array_equal(out2[2], vis[7])                  # no members: unchanged
+    assert np.array_equal(out2[0], vis[1])                  # absorbing an exact twin
+
+
+# ------------------------------------------------------- softmax / Eq. v ---
+
+def pin_attention_two_keys(lib):
+    g = GOLDEN["two_key_softmax"]
+    A = O.attention(np.array(g["q"]), np.array(g["k"]), lib=lib)
+    e = math.e
+    assert abs(A[0, 0] - e / (1 + e)) < 1e-15 and abs(A[0, 1] - 1 / (1 + e)) < 1e-15
+
+
+def pin_attention_invariants(lib):
+    """Rows sum to 1; adding one vector to every key shifts each row's
+    logits by a constant and leaves the row unchanged; Q = 0 is uniform."""
+    rng = np.random.default_rng(21)
+    q = rng.standard_normal((5, 16)) * 2
+    k = rng.standard_normal((23, 16)) * 2
+    A = O.attention(q, k, lib=lib)
+    assert np.max(np.abs(A.sum(1) - 1.0)) < 1e-14 and np.all(A > 0)
+    w = rng.standard_normal(16) * 3
+    A2 = O.attention(q, k + w[None, :], lib=lib)
+    assert np.max(np.abs(A2 - A)) < 1e-12
+    U = O.attention(np.zeros((3, 16)), k, lib=lib)
+    assert np.max(np.abs(U - 1.0 / 23)) < 1e-16
+
+
+def pin_attention_library(lib):
+    """Special case reducing to a library routine: torch.softmax in float64
+    on the CPU over q k^T / sqrt(hd)."""
+    import torch
+    rng = np.random.default_rng(22)
+    q = rng.standard_normal((7, 32))
+    k = rng.standard_normal((19, 32))
+    want = torch.softmax(torch.from_numpy(q) @ torch.from_numpy(k).T / math.sqrt(32), dim=-1).numpy()
+    A = O.attention(q, k, lib=lib)
+    assert np.max(np.abs(A - want)) < 1e-14
+
+
+def _torch_all_head_mean(q, k):
+    """FastV-style importance: attention averaged over every head and every
+    text row, computed independently with torch (float64, CPU)."""
+    import torch
+    Q = torch.from_numpy(q)
+    K = torch.from_numpy(k)
+    A = torch.softmax(Q @ K.transpose(1, 2).contiguous() / math.sqrt(q.shape[-1]), dim=-1)
+    return A.mean(dim=(0, 1)).numpy()
+
+
+def pin_head_aware_all_heads_baseline(lib):
+    """Sec. 4.4: with V = every head the head-aware score is the all-head
+    aggregation of attention-based pruning (the paper's 'All Attention
+    Heads' configuration)."""
+    rng = np.random.default_rng(23)
+    H, nt, n, hd = 6, 9, 31, 16
+    q = rng.standard_normal((H, nt, hd)) * 1.5
+    k = rng.standard_normal((H, n, hd)) * 1.5
+    v = O.head_aware_score(q, k, list(range(H)), lib=lib)
+    assert np.max(np.abs(v - _torch_all_head_mean(q, k))) < 1e-15
+
+
+def pin_head_aware_subset(lib):
+    """Only the listed heads are read; one head gives that head's column
+    mean; the order of the list does not matter; v sums to 1; permuting
+    the keys permutes v."""
+    import torch
+    rng = np.random.default_rng(24)
+    H, nt, n, hd = 5, 6, 17, 8
+    q = rng.standard_normal((H, nt, hd)) * 2
+    k = rng.standard_normal((H, n, hd)) * 2
+    v = O.head_aware_score(q, k, [3, 1], lib=lib)
+    assert abs(v.sum() - 1.0) < 1e-14
+    k2 = k.copy()
+    k2[0] = rng.standard_normal((n, hd))
+    k2[4] = 0.0
+    assert np.array_equal(O.head_aware_score(q, k2, [3, 1], lib=lib), v)
+    assert np.max(np.abs(O.head_aware_score(q, k, [1, 3], lib=lib) - v)) < 1e-16
+    one = O.head_aware_score(q, k, [2], lib=lib)
+    A2 = torch.softmax(torch.from_numpy(q[2]) @ torch.from_numpy(k[2]).T / math.sqrt(hd), -1)
+    assert np.max(np.abs(one - A2.mean(0).numpy())) < 1e-15
+    two = _torch_all_head_mean(q[[1, 3]], k[[1, 3]])
+    assert np.max(np.abs(v - two)) < 1e-15
+    perm = rng.permutation(n)
+    vp = O.head_aware_score(q, k[:, perm], [3, 1], lib=lib)
+    assert np.max(np.abs(vp - v[perm])) < 1e-15
+
+
+def pin_head_aware_topk(lib):
+    rng = np.random.default_rng(25)
+    B, H, nt, n, hd = 2, 4, 5, 12, 8
+    q = rng.standard_normal((B, H, nt, hd))
+    k = rng.standard_normal((B, H, n, hd))
+    heads = np.array([[0, 2], [3, 1]], np.int32)
+    kept, v = O.head_aware(q, k, heads, 5, lib=lib)
+    for b in range(B):
+        assert np.array_equal(kept[b], np.sort(np.argsort(-v[b], kind="stable")[:5]))
+
+
+# ---------------------------------------------------------------- gather ---
+
+def pin_gather_bytes(lib):
+    rng = np.random.default_rng(26)
+    src = rng.integers(0, 255, (3, 4, 11, 16), dtype=np.uint8)
+    idx = np.stack([np.sort(rng.choice(11, 5, replace=False)) for _ in range(3)]).astype(np.int32)
+    out = O.gather(src, idx, lib=lib)
+    want = np.stack([src[b][:, idx[b]] for b in range(3)])
+    assert np.array_equal(out, want)
+    h = rng.standard_normal((2, 9, 6)).astype(np.float32)
+    idx2 = np.array([[0, 4, 8], [1, 2, 3]], np.int32)
+    assert np.array_equal(O.gather(h, idx2, lib=lib), np.stack([h[0][[0, 4, 8]], h[1][[1, 2, 3]]]))
+
+
+# ------------------------------------------------------- stage A end to end
+
+def pin_dedup_axes(lib):
+    g = GOLDEN["dedup_axes"]
+    A = np.array(g["anchors"])[None]
+    V = np.array(g["vis"])[None]
+    r = 1.0 / math.sqrt(2.0)
+    want_p = np.array([1 - (1 + r) / 5, 0.8, -0.2, -0.2, r - (1 + r) / 5])
+    for n1, key in ((2, "kept_top2"), (3, "kept_top3"), (4, "kept_top4")):
+        res = O.dedup(A, V, n1, lib=lib)
+        assert np.max(np.abs(res["p"][0] - want_p)) < 1e-15
+        assert np.array_equal(res["kept"][0], g[key])
+
+
+def pin_dedup_twins(lib):
+    """Exact twins get bit-identical p; if the higher twin is kept the lower
+    one is too; a pruned twin whose twin is kept is absorbed by it."""
+    rng = np.random.default_rng(27)
+    B, nv, d, nt = 1, 40, 24, 6
+    vis = rng.standard_normal((B, nv, d))
+    pairs = [(2, 30), (5, 6), (11, 39), (17, 18)]
+    for a, b in pairs:
+        vis[0, b] = vis[0, a]
+    anchors = rng.standard_normal((B, nt, d))
+    res = O.dedup(anchors, vis, 20, lib=lib)
+    kept = set(res["kept"][0].tolist())
+    for a, b in pairs:
+        assert res["p"][0, a] == res["p"][0, b]
+        if b in kept:
+            assert a in kept
+        if a in kept and b not in kept:
+            slot = list(res["kept"][0]).index(a)
+            assert res["assign"][0, b] == slot
+    assert len(kept) == 20 and np.all(np.diff(res["kept"][0]) > 0)
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_") and callable(v)]
