@@ -1,0 +1,174 @@
+/*
+ * provip.h -- C ABI of the ProViP pruning hot path on AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The method (Ma et al., "Not All Attention Heads Contribute to Critical
+ * Visual Token Selection: Head-Aware Pruning Matters More") prunes visual
+ * tokens in two places:
+ *   - before the LLM (Sec. 4.3): text-guided cosine similarity, row
+ *     centring, max-pooling, top-N_1, and aggregation of every pruned token
+ *     into its nearest retained token          -> pv_prune_dedup
+ *   - inside the LLM at a pruning layer (Sec. 4.4): the softmax attention of
+ *     the text-query rows over the visual keys, averaged over a given subset
+ *     of heads and over the rows, then top-N_2   -> pv_prune_head_aware
+ *   - pruned tokens leave all later computation (Sec. 4.1): order-preserving
+ *     compaction of hidden-state and K/V rows     -> pv_prune_gather
+ *
+ * Conventions shared by every call
+ *   - Tensor pointers are DEVICE memory owned by the caller, row-major and
+ *     contiguous unless strides are passed.  Device pointers must be 16-byte
+ *     aligned.  The library keeps no pointer after a call returns.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  Every call checks
+ *     its arguments on the host first; on an error nothing is enqueued and a
+ *     negative pv_status is returned.  Otherwise all work is enqueued on
+ *     `stream` and the call returns PV_OK without synchronising.
+ *   - `workspace` is caller-owned device scratch of at least the size the
+ *     matching *_workspace_bytes query returns.  Its contents on entry do not
+ *     matter; two calls that use one workspace must not overlap in time.
+ *   - Scores are float32.  Index outputs are int32 token indices local to the
+ *     span passed in, strictly increasing within a sample.
+ *   - Ties between equal scores go to the lower token index; -0 and +0 are
+ *     equal.  Inputs must be finite (NaN/Inf give unspecified selections).
+ *   - Results are deterministic: two calls on the same inputs return the same
+ *     bits (no floating-point atomics; every reduction has a fixed order).
+ */
+#ifndef PROVIP_H
+#define PROVIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PV_OK = 0,
+    PV_ERR_NULL = -1,      /* a required pointer is NULL                      */
+    PV_ERR_SHAPE = -2,     /* a size is <= 0, too large, or not a multiple the
+                              kernels need (see each call)                     */
+    PV_ERR_BUDGET = -3,    /* budget < 1 or budget > number of tokens          */
+    PV_ERR_HEADS = -4,     /* head list empty, out of range or repeated        */
+    PV_ERR_DTYPE = -5,     /* dtype is not PV_F32 or PV_BF16                   */
+    PV_ERR_WORKSPACE = -6, /* workspace NULL or smaller than the query         */
+    PV_ERR_HIP = -7,       /* a kernel launch failed                            */
+    PV_ERR_ALIGN = -8      /* a pointer, row size or stride is not 16-byte
+                              aligned                                          */
+} pv_status;
+
+typedef enum { PV_F32 = 0, PV_BF16 = 1 } pv_dtype;
+
+/* Size limits checked by the calls. */
+#define PV_MAX_TOKENS 16384   /* visual tokens per sample (Nv, N)            */
+#define PV_MAX_TEXT 1024      /* text rows per sample (Nt)                   */
+#define PV_MAX_DIM 16384      /* embedding width d                           */
+#define PV_MAX_HEAD_DIM 256   /* head width hd                               */
+#define PV_MAX_HEAD_LIST 512  /* B * n_heads entries of one head-aware call   */
+
+/* Static string for a pv_status value (never NULL). */
+const char *pv_status_string(int status);
+
+/* ABI version, (major << 16) | minor. */
+int pv_version(void);
+
+/* -------------------------------------------------------------------------
+ * Pruning before the LLM (Sec. 4.3).
+ *
+ * Per sample b (all B samples independent):
+ *   M[i][j]  = cos(anchors[b][i], vis[b][j])         (equation for M; a pair
+ *              with a zero-norm vector has M = 0)
+ *   Mh[i][j] = M[i][j] - mean_k M[i][k]              (equation for M-hat)
+ *   p[j]     = max_i Mh[i][j]                        (equation for p)
+ *   kept     = the `budget` tokens with the highest p (ties: lower index),
+ *              written in ascending index order
+ *   assign[j]= slot s in [0, budget) of the kept token nearest to token j by
+ *              cosine (ties: lower slot); a kept token gets its own slot
+ *   merged[s]= mean of vis[kept[s]] and every pruned token assigned to s
+ *              (the paper gives no aggregation formula; this is the unweighted
+ *              mean of the centroid and its members)
+ *
+ * vis      [B][Nv][d]      dtype        visual embeddings (connector output)
+ * anchors  [B][Nt][d]      dtype        embeddings of the critical text tokens
+ * kept     [B][budget]     int32 out    required
+ * score    [B][Nv]         float32 out  p, may be NULL
+ * assign   [B][Nv]         int32 out    may be NULL
+ * merged   [B][budget][d]  dtype out    may be NULL (then no merge is run)
+ * Sizes: 1 <= Nv <= PV_MAX_TOKENS, 1 <= Nt <= PV_MAX_TEXT,
+ *        64 <= d <= PV_MAX_DIM with d % 64 == 0, 1 <= budget <= Nv.
+ * ---------------------------------------------------------------------- */
+size_t pv_dedup_workspace_bytes(int B, int Nv, int Nt, int d, int budget, int dtype);
+
+int pv_prune_dedup(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
+                   int dtype, int budget, int32_t *kept, float *score, int32_t *assign,
+                   void *merged, void *workspace, size_t workspace_bytes, void *stream);
+
+/* -------------------------------------------------------------------------
+ * Head-aware pruning at a pruning layer (Sec. 4.4, equations for S^vis and v).
+ *
+ * Per sample b, with V_b = heads_host[b*n_heads .. b*n_heads + n_heads):
+ *   A_h[i][j] = softmax_j( q[b][h][i] . k[b][h][j] / sqrt(hd) )  over the N
+ *               visual keys passed in (each row sums to 1)
+ *   v[j]      = (1/|V_b|) sum_{h in V_b} (1/Nt) sum_i A_h[i][j]
+ *   kept      = the `budget` tokens with the highest v (ties: lower index),
+ *               ascending.
+ * Passing every head 0..H-1 gives the all-head aggregation the paper uses at
+ * its middle pruning layer.
+ *
+ * q          [B][H][Nt][hd]  dtype      text-query rows at the pruning layer
+ * k          [B][H][N][hd]   dtype      keys of the N visual tokens
+ * heads_host [B][n_heads]    int32      HOST memory; distinct ids in [0, H)
+ * kept       [B][budget]     int32 out  required
+ * score      [B][N]          float32 out  v, may be NULL
+ * Sizes: 1 <= N <= PV_MAX_TOKENS, 1 <= Nt <= PV_MAX_TEXT, hd % 32 == 0,
+ *        32 <= hd <= PV_MAX_HEAD_DIM, 1 <= n_heads <= H,
+ *        B * n_heads <= PV_MAX_HEAD_LIST, 1 <= budget <= N.
+ * ---------------------------------------------------------------------- */
+size_t pv_head_aware_workspace_bytes(int B, int H, int Nt, int N, int hd, int n_heads,
+                                     int budget, int dtype);
+
+int pv_prune_head_aware(const void *q, const void *k, const int32_t *heads_host, int n_heads,
+                        int B, int H, int Nt, int N, int hd, int dtype, int budget,
+                        int32_t *kept, float *score, void *workspace, size_t workspace_bytes,
+                        void *stream);
+
+/* -------------------------------------------------------------------------
+ * Order-preserving row compaction (Sec. 4.1: pruned tokens are excluded from
+ * all later computation):
+ *   dst + b*dst_batch_stride + g*dst_group_stride + r*dst_row_stride
+ *     <- row_bytes bytes at
+ *   src + b*src_batch_stride + g*src_group_stride + idx[b*k + r]*src_row_stride
+ * for b < B, g < groups, r < k.  Use groups = 1 for hidden states [B][N][D]
+ * and groups = H for K/V caches [B][H][N][hd].  All strides are in bytes.
+ * A pure byte copy: bit-exact.  idx is DEVICE memory [B][k]; an index outside
+ * [0, n_src) yields a zero-filled destination row (never an out-of-bounds
+ * read).  row_bytes and every stride must be multiples of 16.
+ * ---------------------------------------------------------------------- */
+int pv_prune_gather(const void *src, void *dst, const int32_t *idx, int B, int n_src, int k,
+                    int groups, int64_t row_bytes, int64_t src_batch_stride,
+                    int64_t src_group_stride, int64_t src_row_stride, int64_t dst_batch_stride,
+                    int64_t dst_group_stride, int64_t dst_row_stride, void *stream);
+
+/* -------------------------------------------------------------------------
+ * Timed variants, for profiling.  Same arguments and results as the calls
+ * above, plus an array of hipEvent_t handles: events[i] is recorded on
+ * `stream` just before the i-th kernel the call launches and events[n] just
+ * after the last one, for n = min(n_events - 1, number of kernels).  The
+ * number of kernels a call launches is returned through *n_kernels (may be
+ * NULL).  Passing n_events = 0 records nothing.
+ * ---------------------------------------------------------------------- */
+int pv_prune_dedup_timed(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
+                         int dtype, int budget, int32_t *kept, float *score, int32_t *assign,
+                         void *merged, void *workspace, size_t workspace_bytes, void *stream,
+                         void *const *events, int n_events, int *n_kernels);
+
+int pv_prune_head_aware_timed(const void *q, const void *k, const int32_t *heads_host,
+                              int n_heads, int B, int H, int Nt, int N, int hd, int dtype,
+                              int budget, int32_t *kept, float *score, void *workspace,
+                              size_t workspace_bytes, void *stream, void *const *events,
+                              int n_events, int *n_kernels);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PROVIP_H */

@@ -1,0 +1,48 @@
+// Host-side launchers of the ProViP kernels (internal to libprovip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pv {
+
+// Element types of the inputs (values of pv_dtype).
+constexpr int kF32 = 0;
+constexpr int kBF16 = 1;
+
+// Tile shapes of the row x row MFMA product, smallest first.
+enum TileCfg { TILE_16 = 0, TILE_32 = 1, TILE_64 = 2, TILE_128 = 3, N_TILE_CFG = 4 };
+int tile_size(int cfg);  // BM == BN of a config
+
+constexpr int kMaxHeadArgs = 512;
+struct HeadArgs {
+    int32_t h[kMaxHeadArgs];
+};
+
+// ---- pruning before the LLM (Sec. 4.3)
+hipError_t launch_cos_tile(int dt, int cfg, const void *vis, const void *anchors, int B, int Nv,
+                           int Nt, int d, float *M, float *invn, float *rowsum, unsigned *counters,
+                           int n_counters, hipStream_t st);
+hipError_t launch_center_select(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
+                                float *p, int budget, int32_t *kept, int32_t *pruned,
+                                int32_t *slot_of, unsigned *counters, hipStream_t st);
+hipError_t launch_gram_assign(int dt, int cfg, const void *vis, int B, int Nv, int d,
+                              const int32_t *kept, int N1, const int32_t *pruned, int Mp,
+                              const float *invn, float *best_val, int32_t *best_slot,
+                              int32_t *assign, unsigned *counters, hipStream_t st);
+hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept, int N1,
+                        const int32_t *assign, void *merged, hipStream_t st);
+
+// ---- head-aware pruning (Sec. 4.4)
+hipError_t launch_score_partial(int dt, const void *q, const void *k, const HeadArgs &heads,
+                                int B, int H, int Nt, int N, int hd, int n_heads, float *partial,
+                                hipStream_t st);
+hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,
+                               float *v, int budget, int32_t *kept, hipStream_t st);
+
+// ---- compaction (Sec. 4.1)
+hipError_t launch_gather(const void *src, void *dst, const int32_t *idx, int B, int n_src, int k,
+                         int groups, int64_t row_bytes, int64_t sb, int64_t sg, int64_t sr,
+                         int64_t db, int64_t dg, int64_t dr, hipStream_t st);
+
+}  // namespace pv

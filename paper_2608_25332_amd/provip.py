@@ -1,0 +1,234 @@
+"""ctypes binding of libprovip (the C ABI in include/provip.h).
+
+Argument marshalling only: torch tensors supply device memory and the
+current HIP stream; every step of the computation runs in the HIP kernels of
+libprovip.so.  If the library is not built this module raises on first use;
+there is no fallback path.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import torch
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libprovip.so")
+
+PV_OK = 0
+PV_F32 = 0
+PV_BF16 = 1
+
+STATUS = {
+    0: "PV_OK", -1: "PV_ERR_NULL", -2: "PV_ERR_SHAPE", -3: "PV_ERR_BUDGET", -4: "PV_ERR_HEADS",
+    -5: "PV_ERR_DTYPE", -6: "PV_ERR_WORKSPACE", -7: "PV_ERR_HIP", -8: "PV_ERR_ALIGN",
+}
+
+_lib = None
+
+_vp = ctypes.c_void_p
+_i = ctypes.c_int
+_i64 = ctypes.c_int64
+_sz = ctypes.c_size_t
+
+
+class ProvipError(RuntimeError):
+    def __init__(self, fn: str, status: int, lib=None):
+        msg = lib.pv_status_string(status).decode() if lib is not None else ""
+        super().__init__(f"{fn} failed: {STATUS.get(status, status)} ({msg})")
+        self.status = status
+
+
+def load(path: str = LIB_PATH):
+    """Load libprovip.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libprovip.so is not built ({path}); run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    lib.pv_status_string.argtypes = [_i]
+    lib.pv_status_string.restype = ctypes.c_char_p
+    lib.pv_version.argtypes = []
+    lib.pv_version.restype = _i
+    lib.pv_dedup_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i]
+    lib.pv_dedup_workspace_bytes.restype = _sz
+    ded = [_vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.pv_prune_dedup.argtypes = ded
+    lib.pv_prune_dedup.restype = _i
+    lib.pv_prune_dedup_timed.argtypes = ded + [ctypes.POINTER(_vp), _i, ctypes.POINTER(_i)]
+    lib.pv_prune_dedup_timed.restype = _i
+    lib.pv_head_aware_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i, _i]
+    lib.pv_head_aware_workspace_bytes.restype = _sz
+    ha = [_vp, _vp, ctypes.POINTER(ctypes.c_int32), _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp,
+          _vp, _sz, _vp]
+    lib.pv_prune_head_aware.argtypes = ha
+    lib.pv_prune_head_aware.restype = _i
+    lib.pv_prune_head_aware_timed.argtypes = ha + [ctypes.POINTER(_vp), _i, ctypes.POINTER(_i)]
+    lib.pv_prune_head_aware_timed.restype = _i
+    lib.pv_prune_gather.argtypes = [_vp, _vp, _vp, _i, _i, _i, _i, _i64, _i64, _i64, _i64, _i64,
+                                    _i64, _i64, _vp]
+    lib.pv_prune_gather.restype = _i
+    _lib = lib
+    return lib
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return PV_BF16
+    if t.dtype == torch.float32:
+        return PV_F32
+    raise TypeError(f"unsupported dtype {t.dtype}; use bfloat16 or float32")
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(device: torch.device):
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def _check(fn: str, rc: int, lib):
+    if rc != PV_OK:
+        raise ProvipError(fn, rc, lib)
+
+
+def _contig(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _events_array(events: Optional[Sequence]):
+    if not events:
+        return None, 0
+    arr = (_vp * len(events))(*[e.cuda_event if hasattr(e, "cuda_event") else e for e in events])
+    return arr, len(events)
+
+
+# ----------------------------------------------------------------------------
+def pv_dedup_workspace_bytes(B: int, Nv: int, Nt: int, d: int, budget: int, dtype: int) -> int:
+    return int(load().pv_dedup_workspace_bytes(B, Nv, Nt, d, budget, dtype))
+
+
+def pv_prune_dedup(vis: torch.Tensor, anchors: torch.Tensor, budget: int, *,
+                   want_score: bool = True, want_assign: bool = True, want_merged: bool = True,
+                   out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None,
+                   events: Optional[Sequence] = None):
+    """Pruning before the LLM.  vis [B, Nv, d], anchors [B, Nt, d] (same dtype).
+    Returns dict(kept [B,budget] int32, score [B,Nv] f32 | None,
+    assign [B,Nv] int32 | None, merged [B,budget,d] | None, n_kernels)."""
+    lib = load()
+    _contig(vis, "vis")
+    _contig(anchors, "anchors")
+    B, Nv, d = vis.shape
+    Bt, Nt, dt_ = anchors.shape
+    if Bt != B or dt_ != d or anchors.dtype != vis.dtype:
+        raise ValueError("anchors must be [B, Nt, d] with the dtype of vis")
+    code = _dtype_code(vis)
+    dev = vis.device
+    o = out if out is not None else {}
+    kept = o.get("kept")
+    if kept is None:
+        kept = torch.empty((B, budget), dtype=torch.int32, device=dev)
+    score = o.get("score") if want_score else None
+    if want_score and score is None:
+        score = torch.empty((B, Nv), dtype=torch.float32, device=dev)
+    assign = o.get("assign") if want_assign else None
+    if want_assign and assign is None:
+        assign = torch.empty((B, Nv), dtype=torch.int32, device=dev)
+    merged = o.get("merged") if want_merged else None
+    if want_merged and merged is None:
+        merged = torch.empty((B, budget, d), dtype=vis.dtype, device=dev)
+    nbytes = lib.pv_dedup_workspace_bytes(B, Nv, Nt, d, budget, code)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    ev, nev = _events_array(events)
+    nk = _i(0)
+    rc = lib.pv_prune_dedup_timed(vis.data_ptr(), anchors.data_ptr(), B, Nv, Nt, d, code,
+                                  int(budget), kept.data_ptr(), _ptr(score), _ptr(assign),
+                                  _ptr(merged), workspace.data_ptr(), workspace.numel(),
+                                  _stream(dev), ev, nev, ctypes.byref(nk))
+    _check("pv_prune_dedup", rc, lib)
+    return {"kept": kept, "score": score, "assign": assign, "merged": merged,
+            "n_kernels": nk.value, "workspace": workspace}
+
+
+def pv_head_aware_workspace_bytes(B: int, H: int, Nt: int, N: int, hd: int, n_heads: int,
+                                  budget: int, dtype: int) -> int:
+    return int(load().pv_head_aware_workspace_bytes(B, H, Nt, N, hd, n_heads, budget, dtype))
+
+
+def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
+                        want_score: bool = True, out: Optional[dict] = None,
+                        workspace: Optional[torch.Tensor] = None,
+                        events: Optional[Sequence] = None):
+    """Head-aware pruning.  q [B,H,Nt,hd], k [B,H,N,hd] (same dtype), heads: host
+    int sequence [B, n_heads].  Returns dict(kept [B,budget] int32,
+    score [B,N] f32 | None, n_kernels)."""
+    import numpy as np
+
+    lib = load()
+    _contig(q, "q")
+    _contig(k, "k")
+    B, H, Nt, hd = q.shape
+    Bk, Hk, N, hdk = k.shape
+    if (Bk, Hk, hdk) != (B, H, hd) or k.dtype != q.dtype:
+        raise ValueError("k must be [B, H, N, hd] with the dtype of q")
+    hs = np.ascontiguousarray(np.asarray(heads, dtype=np.int32).reshape(B, -1))
+    n_heads = hs.shape[1]
+    code = _dtype_code(q)
+    dev = q.device
+    o = out if out is not None else {}
+    kept = o.get("kept")
+    if kept is None:
+        kept = torch.empty((B, budget), dtype=torch.int32, device=dev)
+    score = o.get("score") if want_score else None
+    if want_score and score is None:
+        score = torch.empty((B, N), dtype=torch.float32, device=dev)
+    nbytes = lib.pv_head_aware_workspace_bytes(B, H, Nt, N, hd, n_heads, budget, code)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    ev, nev = _events_array(events)
+    nk = _i(0)
+    rc = lib.pv_prune_head_aware_timed(q.data_ptr(), k.data_ptr(),
+                                       hs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n_heads,
+                                       B, H, Nt, N, hd, code, int(budget), kept.data_ptr(),
+                                       _ptr(score), workspace.data_ptr(), workspace.numel(),
+                                       _stream(dev), ev, nev, ctypes.byref(nk))
+    _check("pv_prune_head_aware", rc, lib)
+    return {"kept": kept, "score": score, "n_kernels": nk.value, "workspace": workspace}
+
+
+def pv_prune_gather(src: torch.Tensor, idx: torch.Tensor, *, out: Optional[torch.Tensor] = None):
+    """Order-preserving compaction of rows.  src [B, N, ...] (groups = 1) or
+    [B, G, N, hd] with grouped=4-D (K/V caches); idx [B, k] int32 device.
+    Returns dst [B, k, ...] / [B, G, k, hd]."""
+    lib = load()
+    _contig(src, "src")
+    _contig(idx, "idx")
+    if idx.dtype != torch.int32:
+        raise TypeError("idx must be int32")
+    B, k = idx.shape
+    if src.dim() == 4:
+        _, G, n, hd = src.shape
+        row_bytes = hd * src.element_size()
+        shape = (B, G, k, hd)
+    else:
+        G, n = 1, src.shape[1]
+        row_bytes = int(torch.tensor(src.shape[2:]).prod().item()) * src.element_size() \
+            if src.dim() > 2 else src.element_size()
+        shape = (B, k) + tuple(src.shape[2:])
+    if out is None:
+        out = torch.empty(shape, dtype=src.dtype, device=src.device)
+    sb, sg, sr = n * G * row_bytes, n * row_bytes, row_bytes
+    db, dg, dr = k * G * row_bytes, k * row_bytes, row_bytes
+    rc = lib.pv_prune_gather(src.data_ptr(), out.data_ptr(), idx.data_ptr(), B, n, k, G,
+                             row_bytes, sb, sg, sr, db, dg, dr, _stream(src.device))
+    _check("pv_prune_gather", rc, lib)
+    return out

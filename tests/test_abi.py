@@ -1,0 +1,133 @@
+"""The C ABI without a GPU: the library loads, exports every entry point
+declared in include/provip.h, and rejects bad arguments on the host before
+anything is enqueued (these calls never reach a kernel launch)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "provip.h")
+
+
+def _declared():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(pv_[a-z_0-9]+)\s*\(", txt)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2608_25332_amd import provip
+    return provip.load()
+
+
+def test_header_declares_the_three_calls():
+    names = _declared()
+    for n in ("pv_prune_dedup", "pv_prune_head_aware", "pv_prune_gather",
+              "pv_dedup_workspace_bytes", "pv_head_aware_workspace_bytes", "pv_status_string"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+def test_exported_c_symbols_are_declared():
+    """Every unmangled symbol the library exports is part of the header."""
+    import shutil
+    import subprocess
+    from paper_2608_25332_amd import provip
+    if shutil.which("nm") is None:
+        pytest.skip("nm not available")
+    out = subprocess.run(["nm", "-D", "--defined-only", provip.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    names = [l.split()[-1] for l in out.splitlines() if l.strip()]
+    c_names = [n for n in names if not n.startswith("_Z") and not n.startswith("__")]
+    assert set(c_names) <= set(_declared()), set(c_names) - set(_declared())
+
+
+def test_status_strings(lib):
+    for s in range(-8, 1):
+        assert len(lib.pv_status_string(s)) > 0
+    assert lib.pv_status_string(-99) == b"unknown status"
+    assert lib.pv_version() >> 16 == 1
+
+
+FAKE = 0x100000  # never dereferenced: every call below fails validation first
+
+
+def _dedup(lib, vis=FAKE, anc=FAKE, B=1, Nv=64, Nt=16, d=256, dt=1, budget=32, kept=FAKE,
+           ws=FAKE, wsb=1 << 40):
+    return lib.pv_prune_dedup(vis, anc, B, Nv, Nt, d, dt, budget, kept, None, None, None, ws,
+                              wsb, None)
+
+
+def test_dedup_validation(lib):
+    assert _dedup(lib, vis=None) == -1
+    assert _dedup(lib, kept=None) == -1
+    assert _dedup(lib, dt=7) == -5
+    assert _dedup(lib, Nv=0) == -2
+    assert _dedup(lib, d=100) == -2
+    assert _dedup(lib, d=32) == -2
+    assert _dedup(lib, Nt=0) == -2
+    assert _dedup(lib, Nv=20000) == -2
+    assert _dedup(lib, budget=0) == -3
+    assert _dedup(lib, budget=65) == -3
+    assert _dedup(lib, ws=None) == -6
+    assert _dedup(lib, wsb=16) == -6
+    assert _dedup(lib, vis=FAKE + 4) == -8
+
+
+def test_dedup_workspace_query(lib):
+    a = lib.pv_dedup_workspace_bytes(1, 576, 64, 4096, 192, 1)
+    b = lib.pv_dedup_workspace_bytes(16, 576, 64, 4096, 192, 1)
+    assert 0 < a < b
+    assert lib.pv_dedup_workspace_bytes(1, 576, 64, 4096, 0, 1) == 0
+    assert lib.pv_dedup_workspace_bytes(1, 576, 64, 4096, 577, 1) == 0
+
+
+def _heads(lib, heads, B=1, H=4, Nt=16, N=32, hd=64, dt=1, budget=8, q=FAKE, k=FAKE, kept=FAKE,
+           ws=FAKE, wsb=1 << 40):
+    hs = np.ascontiguousarray(np.asarray(heads, np.int32).reshape(B, -1))
+    return lib.pv_prune_head_aware(q, k, hs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                   hs.shape[1], B, H, Nt, N, hd, dt, budget, kept, None, ws, wsb,
+                                   None)
+
+
+def test_head_aware_validation(lib):
+    assert _heads(lib, [1], q=None) == -1
+    assert _heads(lib, [4]) == -4          # out of range
+    assert _heads(lib, [-1]) == -4
+    assert _heads(lib, [1, 1]) == -4       # repeated
+    assert _heads(lib, [0, 1, 2, 3, 0]) == -4  # more heads than H
+    assert _heads(lib, [1], hd=48) == -2
+    assert _heads(lib, [1], hd=512) == -2
+    assert _heads(lib, [1], N=0) == -2
+    assert _heads(lib, [1], budget=0) == -3
+    assert _heads(lib, [1], budget=33) == -3
+    assert _heads(lib, [1], dt=3) == -5
+    assert _heads(lib, [1], ws=None) == -6
+    assert _heads(lib, [1], wsb=8) == -6
+    assert _heads(lib, [1], q=FAKE + 8) == -8
+    assert _heads(lib, [[0], [1], [4]], B=3) == -4   # a later sample is checked too
+
+
+def test_gather_validation(lib):
+    g = lib.pv_prune_gather
+    args = dict(src=FAKE, dst=FAKE, idx=FAKE, B=1, n=8, k=4, G=1, rb=256)
+
+    def call(**kw):
+        a = {**args, **kw}
+        return g(a["src"], a["dst"], a["idx"], a["B"], a["n"], a["k"], a["G"], a["rb"],
+                 a["rb"] * a["n"], a["rb"] * a["n"], a["rb"], a["rb"] * a["k"], a["rb"] * a["k"],
+                 a["rb"], None)
+    assert call(src=None) == -1
+    assert call(idx=None) == -1
+    assert call(k=0) == -2
+    assert call(rb=8) == -2
+    assert call(rb=40) == -8
+    assert call(dst=FAKE + 2) == -8

@@ -1,0 +1,331 @@
+"""HIP path vs the CPU oracle, element by element, on the seeded workloads.
+
+All calls go through the C ABI (ctypes binding).  Tiny and LLaVA-1.5 sizes
+are checked in full; at the larger sizes the oracle is run on whole samples
+for the scores and selections and on sampled rows / slots for the
+nearest-centroid assignment and the merge (each decision is computed by the
+oracle one by one, with the GPU's own kept list and assignment as input).
+"""
+
+from __future__ import annotations
+
+import functools
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_25332_amd import workloads as W
+from parity_util import (TOL, check_assign_rows, check_kept, check_merged, rel_err, to_dev,
+                         to_host)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_25332_amd import provip
+    provip.load()
+
+
+@functools.lru_cache(maxsize=None)
+def workload(wid: int, with_kv: bool = True):
+    return W.make_workload(wid, with_kv=with_kv)
+
+
+def run_dedup(vis_np, anc_np, dtype, budget):
+    from paper_2608_25332_amd import provip
+    vis = to_dev(vis_np, dtype)
+    anc = to_dev(anc_np, dtype)
+    r = provip.pv_prune_dedup(vis, anc, budget)
+    torch.cuda.synchronize()
+    return {k: (to_host(v) if hasattr(v, "cpu") else v) for k, v in r.items() if k != "workspace"}
+
+
+# --------------------------------------------------------------- dedup ------
+
+FULL_SAMPLES = {1: None, 2: None, 3: [0, 7, 15], 4: [0, 3], 5: [0, 1]}
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_dedup_parity(wid):
+    w = workload(wid, with_kv=False)
+    dt = w.dtype
+    _say(f"[dedup] workload {wid} {w.spec.name} B={w.spec.B} Nv={w.spec.Nv} d={w.spec.d}")
+    g = run_dedup(w.vis, w.anchors, dt, w.N1)
+    B, Nv = w.spec.B, w.spec.Nv
+    samples = FULL_SAMPLES[wid] or list(range(B))
+    rng = np.random.default_rng(100 + wid)
+    exempt = 0
+    for b in range(B):
+        kept = g["kept"][b]
+        assert np.all(np.diff(kept) > 0) and kept.shape == (w.N1,)
+        # kept tokens are their own centroids; every token has a valid slot
+        assert np.array_equal(g["assign"][b][kept], np.arange(w.N1))
+        assert g["assign"][b].min() >= 0 and g["assign"][b].max() < w.N1
+    for b in samples:
+        M = oracle.cosine(w.anchors[b], w.vis[b])
+        p = oracle.maxpool(oracle.center(M))
+        assert rel_err(g["score"][b], p) <= TOL[dt], rel_err(g["score"][b], p)
+        exempt += check_kept(g["kept"][b], p, w.N1, dt)
+        kept = g["kept"][b]
+        pruned = np.setdiff1d(np.arange(Nv), kept)
+        rows = pruned if Nv <= 576 else np.sort(rng.choice(pruned, 48, replace=False))
+        check_assign_rows(g["assign"][b], w.vis[b], kept, rows, dt)
+        slots = np.arange(w.N1) if Nv <= 576 else np.sort(rng.choice(w.N1, 16, replace=False))
+        check_merged(g["merged"][b], w.vis[b], kept, g["assign"][b], slots, dt)
+    _say(f"[dedup] workload {wid}: ok, {exempt} near-tie tokens exempt")
+
+
+def test_dedup_tiny_exact_against_full_oracle():
+    w = workload(1, with_kv=False)
+    g = run_dedup(w.vis, w.anchors, "f32", w.N1)
+    ref = oracle.dedup(w.anchors, w.vis, w.N1)
+    assert np.array_equal(g["kept"], ref["kept"])
+    assert np.array_equal(g["assign"], ref["assign"])
+    assert rel_err(g["merged"], ref["merged"]) <= 1e-5
+
+
+def test_dedup_twins_on_gpu():
+    """Planted exact duplicates: bit-identical p; if the higher twin is kept
+    the lower one is too; a pruned twin of a kept token is absorbed by it."""
+    w = workload(1, with_kv=False)
+    for dt in ("f32", "bf16"):
+        vis = w.vis if dt == "f32" else W.bf16_round(w.vis)
+        anc = w.anchors if dt == "f32" else W.bf16_round(w.anchors)
+        g = run_dedup(vis, anc, dt, w.N1)
+        kept = set(g["kept"][0].tolist())
+        for a, b in w.dup_pairs:
+            assert g["score"][0, a] == g["score"][0, b], (dt, a, b)
+            if b in kept:
+                assert a in kept
+            if a in kept and b not in kept:
+                assert g["assign"][0, b] == list(g["kept"][0]).index(a)
+
+
+def test_dedup_deterministic():
+    w = workload(2, with_kv=False)
+    a = run_dedup(w.vis, w.anchors, "bf16", w.N1)
+    b = run_dedup(w.vis, w.anchors, "bf16", w.N1)
+    for k in ("kept", "score", "assign", "merged"):
+        assert np.array_equal(a[k], b[k]), k
+
+
+DEDUP_EDGE = [
+    # (B, Nv, Nt, d, budget, dtype)
+    (1, 17, 1, 64, 5, "f32"),
+    (2, 33, 3, 128, 33, "bf16"),     # budget == Nv: identity, nothing pruned
+    (3, 70, 20, 192, 1, "bf16"),     # budget == 1
+    (1, 300, 37, 256, 129, "bf16"),  # ragged everywhere
+    (2, 1000, 130, 320, 333, "bf16"),
+    (1, 5, 2, 64, 4, "f32"),
+]
+
+
+@pytest.mark.parametrize("B,Nv,Nt,d,budget,dt", DEDUP_EDGE)
+def test_dedup_edges(B, Nv, Nt, d, budget, dt):
+    _say(f"[dedup-edge] B={B} Nv={Nv} Nt={Nt} d={d} budget={budget} {dt}")
+    rng = np.random.default_rng(Nv * 7 + Nt)
+    vis = rng.standard_normal((B, Nv, d)).astype(np.float32)
+    anc = rng.standard_normal((B, Nt, d)).astype(np.float32)
+    if dt == "bf16":
+        vis, anc = W.bf16_round(vis), W.bf16_round(anc)
+    g = run_dedup(vis, anc, dt, budget)
+    for b in range(B):
+        p = oracle.maxpool(oracle.center(oracle.cosine(anc[b], vis[b])))
+        assert rel_err(g["score"][b], p) <= TOL[dt]
+        check_kept(g["kept"][b], p, budget, dt)
+        kept = g["kept"][b]
+        pruned = np.setdiff1d(np.arange(Nv), kept)
+        if len(pruned):
+            check_assign_rows(g["assign"][b], vis[b], kept, pruned, dt)
+        check_merged(g["merged"][b], vis[b], kept, g["assign"][b], np.arange(budget), dt)
+        if budget == Nv:
+            assert np.array_equal(kept, np.arange(Nv))
+            assert np.array_equal(g["merged"][b], vis[b])
+
+
+def test_dedup_zero_vectors():
+    """A zero visual token or anchor has cosine 0 to everything."""
+    rng = np.random.default_rng(5)
+    vis = rng.standard_normal((1, 40, 64)).astype(np.float32)
+    anc = rng.standard_normal((1, 4, 64)).astype(np.float32)
+    vis[0, 7] = 0.0
+    anc[0, 2] = 0.0
+    g = run_dedup(vis, anc, "f32", 10)
+    p = oracle.maxpool(oracle.center(oracle.cosine(anc[0], vis[0])))
+    assert rel_err(g["score"][0], p) <= 1e-5
+    check_kept(g["kept"][0], p, 10, "f32")
+
+
+# ----------------------------------------------------------- head-aware -----
+
+def _subset_keys(w, n, seed):
+    rng = np.random.default_rng(seed)
+    idx = np.stack([np.sort(rng.choice(w.spec.Nv, n, replace=False)) for _ in range(w.spec.B)])
+    k = np.stack([w.k_full[b][:, idx[b]] for b in range(w.spec.B)])
+    return np.ascontiguousarray(k)
+
+
+def run_head(q_np, k_np, heads, dtype, budget):
+    from paper_2608_25332_amd import provip
+    q = to_dev(q_np, dtype)
+    k = to_dev(k_np, dtype)
+    r = provip.pv_prune_head_aware(q, k, heads, budget)
+    torch.cuda.synchronize()
+    return to_host(r["kept"]), to_host(r["score"])
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_head_aware_parity(wid):
+    w = workload(wid)
+    dt = w.dtype
+    _say(f"[head-aware] workload {wid} heads={w.heads.tolist()[:2]}")
+    k1 = _subset_keys(w, w.N1, 200 + wid)
+    kept, v = run_head(w.q, k1, w.heads, dt, w.N2)
+    ref_kept, ref_v = oracle.head_aware(w.q, k1, w.heads, w.N2)
+    assert rel_err(v, ref_v) <= TOL[dt], rel_err(v, ref_v)
+    for b in range(w.spec.B):
+        check_kept(kept[b], ref_v[b], w.N2, dt)
+        assert abs(float(np.sum(v[b], dtype=np.float64)) - 1.0) < 1e-4
+
+
+@pytest.mark.parametrize("wid", [2, 4])
+def test_head_aware_all_heads(wid):
+    """Every head selected: the all-head aggregation of the middle layer."""
+    w = workload(wid)
+    k1 = _subset_keys(w, w.N1, 300 + wid)
+    heads = np.tile(np.arange(w.spec.H, dtype=np.int32), (w.spec.B, 1))
+    kept, v = run_head(w.q, k1, heads, w.dtype, w.N2)
+    ref_kept, ref_v = oracle.head_aware(w.q, k1, heads, w.N2)
+    assert rel_err(v, ref_v) <= TOL[w.dtype]
+    for b in range(w.spec.B):
+        check_kept(kept[b], ref_v[b], w.N2, w.dtype)
+
+
+HEAD_EDGE = [
+    # (B, H, Nt, N, hd, heads per sample, budget, dtype)
+    (1, 2, 1, 1, 32, 1, 1, "f32"),
+    (1, 3, 1, 15, 64, 2, 15, "bf16"),
+    (2, 4, 17, 17, 64, 3, 5, "bf16"),
+    (3, 8, 33, 100, 128, 8, 40, "bf16"),
+    (1, 4, 16, 64, 256, 2, 16, "bf16"),
+    (2, 4, 5, 50, 96, 1, 7, "f32"),
+    (1, 2, 200, 2000, 128, 2, 600, "bf16"),
+]
+
+
+@pytest.mark.parametrize("B,H,Nt,N,hd,nh,budget,dt", HEAD_EDGE)
+def test_head_aware_edges(B, H, Nt, N, hd, nh, budget, dt):
+    _say(f"[head-edge] B={B} H={H} Nt={Nt} N={N} hd={hd} nh={nh} budget={budget} {dt}")
+    rng = np.random.default_rng(B * 1000 + N)
+    q = (rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32)
+    k = (rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32)
+    if dt == "bf16":
+        q, k = W.bf16_round(q), W.bf16_round(k)
+    heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+    kept, v = run_head(q, k, heads, dt, budget)
+    _, ref_v = oracle.head_aware(q, k, heads, budget)
+    assert rel_err(v, ref_v) <= TOL[dt]
+    for b in range(B):
+        check_kept(kept[b], ref_v[b], budget, dt)
+
+
+def test_head_aware_duplicate_keys_tie():
+    """Exact duplicate keys get bit-identical v, and the lower index wins."""
+    rng = np.random.default_rng(9)
+    q = rng.standard_normal((1, 2, 8, 64)).astype(np.float32)
+    k = rng.standard_normal((1, 2, 40, 64)).astype(np.float32)
+    k[:, :, 30] = k[:, :, 4]
+    k[:, :, 4] *= 3.0   # make token 4 (and its twin 30) important
+    k[:, :, 30] = k[:, :, 4]
+    kept, v = run_head(q, k, [[0, 1]], "f32", 1)
+    assert v[0, 4] == v[0, 30]
+    if v[0].argmax() in (4, 30):
+        assert kept[0].tolist() == [4]
+
+
+# --------------------------------------------------------------- gather -----
+
+def test_gather_bit_exact():
+    from paper_2608_25332_amd import provip
+    rng = np.random.default_rng(3)
+    B, H, N, hd, D, k = 2, 8, 300, 128, 4096, 97
+    hid = torch.from_numpy(rng.standard_normal((B, N, D)).astype(np.float32)).to("cuda:0").bfloat16()
+    kv = torch.from_numpy(rng.standard_normal((B, H, N, hd)).astype(np.float32)).to("cuda:0").bfloat16()
+    idx_np = np.stack([np.sort(rng.choice(N, k, replace=False)) for _ in range(B)]).astype(np.int32)
+    idx = torch.from_numpy(idx_np).to("cuda:0")
+    oh = provip.pv_prune_gather(hid, idx)
+    ok = provip.pv_prune_gather(kv, idx)
+    torch.cuda.synchronize()
+    hb = hid.view(torch.int16).cpu().numpy()
+    kb = kv.view(torch.int16).cpu().numpy()
+    assert np.array_equal(oh.view(torch.int16).cpu().numpy(), oracle.gather(hb, idx_np))
+    assert np.array_equal(ok.view(torch.int16).cpu().numpy(), oracle.gather(kb, idx_np))
+
+
+def test_gather_out_of_range_rows_are_zero():
+    from paper_2608_25332_amd import provip
+    src = torch.arange(4 * 8, dtype=torch.float32, device="cuda:0").reshape(1, 8, 4) + 1
+    idx = torch.tensor([[0, 9, -1, 7]], dtype=torch.int32, device="cuda:0")
+    out = provip.pv_prune_gather(src, idx).cpu().numpy()
+    s = src.cpu().numpy()
+    assert np.array_equal(out[0, 0], s[0, 0]) and np.array_equal(out[0, 3], s[0, 7])
+    assert np.all(out[0, 1] == 0) and np.all(out[0, 2] == 0)
+
+
+# ------------------------------------------------------------- pipeline -----
+
+@pytest.mark.parametrize("wid", [1, 2])
+def test_pipeline_against_oracle(wid):
+    """The step bench.py times: dedup -> K/V of the kept tokens -> head-aware
+    -> compaction of hidden (merged), K and V."""
+    from paper_2608_25332_amd import provip
+    w = workload(wid)
+    dt = w.dtype
+    vis, anc = to_dev(w.vis, dt), to_dev(w.anchors, dt)
+    q, kf, vf = to_dev(w.q, dt), to_dev(w.k_full, dt), to_dev(w.v_full, dt)
+    r = provip.pv_prune_dedup(vis, anc, w.N1)
+    k1 = provip.pv_prune_gather(kf, r["kept"])
+    v1 = provip.pv_prune_gather(vf, r["kept"])
+    h = provip.pv_prune_head_aware(q, k1, w.heads, w.N2)
+    hid2 = provip.pv_prune_gather(r["merged"], h["kept"])
+    k2 = provip.pv_prune_gather(k1, h["kept"])
+    v2 = provip.pv_prune_gather(v1, h["kept"])
+    torch.cuda.synchronize()
+    ref = oracle.dedup(w.anchors, w.vis, w.N1)
+    kept1 = to_host(r["kept"])
+    for b in range(w.spec.B):
+        check_kept(kept1[b], ref["p"][b], w.N1, dt)
+    k1_ref = np.stack([w.k_full[b][:, kept1[b]] for b in range(w.spec.B)])
+    assert np.array_equal(to_host(k1), k1_ref)
+    _, v_ref = oracle.head_aware(w.q, k1_ref, w.heads, w.N2)
+    kept2 = to_host(h["kept"])
+    for b in range(w.spec.B):
+        check_kept(kept2[b], v_ref[b], w.N2, dt)
+    assert np.array_equal(to_host(hid2), oracle.gather(to_host(r["merged"]), kept2))
+    assert np.array_equal(to_host(k2), oracle.gather(k1_ref, kept2))
+    v1_ref = np.stack([w.v_full[b][:, kept1[b]] for b in range(w.spec.B)])
+    assert np.array_equal(to_host(v2), oracle.gather(v1_ref, kept2))
+
+
+def test_abi_errors_on_gpu():
+    from paper_2608_25332_amd import provip
+    x = torch.zeros((1, 64, 256), device="cuda:0")
+    with pytest.raises(provip.ProvipError) as e:
+        provip.pv_prune_dedup(x, x[:, :16], 65)
+    assert e.value.status == -3
+    q = torch.zeros((1, 4, 16, 64), device="cuda:0")
+    with pytest.raises(provip.ProvipError) as e:
+        provip.pv_prune_head_aware(q, q, [[1, 1]], 4)
+    assert e.value.status == -4
