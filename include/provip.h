@@ -149,23 +149,46 @@ int pv_prune_gather(const void *src, void *dst, const int32_t *idx, int B, int n
                     int64_t dst_group_stride, int64_t dst_row_stride, void *stream);
 
 /* -------------------------------------------------------------------------
+ * The same compaction for up to PV_MAX_GATHER tensors that share one index
+ * list (typically the hidden states, K and V of one pruning step), in a
+ * single kernel launch.  Each descriptor has the meaning of the arguments of
+ * pv_prune_gather; idx, B and k are common to all.  Errors as above; nothing
+ * is enqueued if any descriptor is invalid.
+ * ---------------------------------------------------------------------- */
+#define PV_MAX_GATHER 4
+
+typedef struct pv_gather_desc {
+    const void *src;
+    void *dst;
+    int n_src;
+    int groups;
+    int64_t row_bytes;
+    int64_t src_batch_stride, src_group_stride, src_row_stride;
+    int64_t dst_batch_stride, dst_group_stride, dst_row_stride;
+} pv_gather_desc;
+
+int pv_prune_gather_batch(const pv_gather_desc *descs, int n_desc, const int32_t *idx, int B,
+                          int k, void *stream);
+
+/* -------------------------------------------------------------------------
  * Timed variants, for profiling.  Same arguments and results as the calls
  * above, plus an array of hipEvent_t handles: events[i] is recorded on
  * `stream` just before the i-th kernel the call launches and events[n] just
  * after the last one, for n = min(n_events - 1, number of kernels).  The
- * number of kernels a call launches is returned through *n_kernels (may be
- * NULL).  Passing n_events = 0 records nothing.
+ * number of kernels a call launches is returned through *n_kernels and their
+ * names (static strings, at most n_events - 1 of them) through names; both
+ * may be NULL.  Passing n_events = 0 records nothing.
  * ---------------------------------------------------------------------- */
 int pv_prune_dedup_timed(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
                          int dtype, int budget, int32_t *kept, float *score, int32_t *assign,
                          void *merged, void *workspace, size_t workspace_bytes, void *stream,
-                         void *const *events, int n_events, int *n_kernels);
+                         void *const *events, int n_events, int *n_kernels, const char **names);
 
 int pv_prune_head_aware_timed(const void *q, const void *k, const int32_t *heads_host,
                               int n_heads, int B, int H, int Nt, int N, int hd, int dtype,
                               int budget, int32_t *kept, float *score, void *workspace,
                               size_t workspace_bytes, void *stream, void *const *events,
-                              int n_events, int *n_kernels);
+                              int n_events, int *n_kernels, const char **names);
 
 #ifdef __cplusplus
 }

@@ -35,10 +35,14 @@ bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 struct Trace {
     void *const *ev;
     int n_ev;
+    const char **names;
     int launched = 0;
     hipStream_t st;
-    void before() {
-        if (ev && launched < n_ev - 1) (void)hipEventRecord((hipEvent_t)ev[launched], st);
+    void before(const char *name) {
+        if (ev && launched < n_ev - 1) {
+            (void)hipEventRecord((hipEvent_t)ev[launched], st);
+            if (names) names[launched] = name;
+        }
     }
     void after_all() {
         if (ev && launched >= 1 && n_ev >= 1) {
@@ -48,41 +52,46 @@ struct Trace {
     }
 };
 
-// Pick the largest square tile whose grid still gives >= ~1 workgroup per CU
-// (256 CUs); fall back to the smallest tile.
-int pick_tile(int rows_m, int rows_n, int B) {
-    for (int cfg = pv::TILE_128; cfg > pv::TILE_16; --cfg) {
-        const int t = pv::tile_size(cfg);
-        const long long wgs = (long long)((rows_m + t - 1) / t) * ((rows_n + t - 1) / t) * B;
-        if (wgs >= 240) return cfg;
-    }
+long long n_tiles(int rows_m, int rows_n, int B, int t) {
+    return (long long)((rows_m + t - 1) / t) * ((rows_n + t - 1) / t) * B;
+}
+
+// Streaming tiles: the largest square tile whose grid still gives about one
+// workgroup per CU (256 CUs); the smallest tile otherwise.
+int pick_stream_tile(int rows_m, int rows_n, int B) {
+    for (int cfg = pv::TILE_64; cfg > pv::TILE_16; --cfg)
+        if (n_tiles(rows_m, rows_n, B, pv::tile_size(cfg)) >= 240) return cfg;
     return pv::TILE_16;
+}
+
+// The Gram switches to LDS-staged 128x128 tiles once those alone fill the
+// chip: it is then compute-heavy enough for MFMA throughput to matter.
+int pick_gram_tile(int Mp, int N1, int B) {
+    if (n_tiles(Mp, N1, B, 128) >= 240) return pv::TILE_128;
+    return pick_stream_tile(Mp, N1, B);
 }
 
 struct DedupPlan {
     int cos_cfg, njt;
     int gram_cfg, ntm, ntn, Mp;
-    int n_counters;
     // workspace
     float *M, *invn, *rowsum, *p;
     int32_t *pruned, *assign;
     float *best_val;
     int32_t *best_slot;
-    unsigned *counters;
     size_t bytes;
 };
 
 DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int budget, bool want_p, bool want_assign) {
     DedupPlan P;
-    P.cos_cfg = pick_tile(Nv, Nt, B);
+    P.cos_cfg = pick_stream_tile(Nv, Nt, B);
     const int t1 = pv::tile_size(P.cos_cfg);
     P.njt = (Nv + t1 - 1) / t1;
     P.Mp = Nv - budget;
-    P.gram_cfg = pick_tile(P.Mp > 0 ? P.Mp : 1, budget, B);
+    P.gram_cfg = pick_gram_tile(P.Mp > 0 ? P.Mp : 1, budget, B);
     const int t4 = pv::tile_size(P.gram_cfg);
     P.ntm = (P.Mp + t4 - 1) / t4;
     P.ntn = (budget + t4 - 1) / t4;
-    P.n_counters = B + B * P.ntm;
     Carve c(ws);
     P.M = c.take<float>((size_t)B * Nt * Nv);
     P.invn = c.take<float>((size_t)B * Nv);
@@ -92,7 +101,6 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int budget, bool want_p, b
     P.assign = want_assign ? c.take<int32_t>((size_t)B * Nv) : nullptr;
     P.best_val = c.take<float>((size_t)B * P.ntn * (P.Mp > 0 ? P.Mp : 1));
     P.best_slot = c.take<int32_t>((size_t)B * P.ntn * (P.Mp > 0 ? P.Mp : 1));
-    P.counters = c.take<unsigned>((size_t)P.n_counters);
     P.bytes = c.off + kAlign;
     return P;
 }
@@ -111,7 +119,7 @@ int check_dedup(const void *vis, const void *anchors, int B, int Nv, int Nt, int
 int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int d, int dtype,
                int budget, int32_t *kept, float *score, int32_t *assign, void *merged,
                void *workspace, size_t ws_bytes, void *stream, void *const *events, int n_events,
-               int *n_kernels) {
+               int *n_kernels, const char **names) {
     int rc = check_dedup(vis, anchors, B, Nv, Nt, d, dtype, budget, kept);
     if (rc != PV_OK) return rc;
     const bool need_assign = assign != nullptr || merged != nullptr;
@@ -128,33 +136,34 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     int32_t *asg = assign ? assign : P.assign;
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
     hipStream_t st = (hipStream_t)stream;
-    Trace tr{events, n_events, 0, st};
-    hipError_t e;
-
-    tr.before();
-    e = pv::launch_cos_tile(dt, P.cos_cfg, vis, anchors, B, Nv, Nt, d, P.M, P.invn, P.rowsum,
-                            P.counters, P.n_counters, st);
-    if (e != hipSuccess) return PV_ERR_HIP;
-    ++tr.launched;
-
-    tr.before();
-    e = pv::launch_center_select(P.M, P.rowsum, P.njt, B, Nt, Nv, p, budget, kept, P.pruned,
-                                 need_assign ? asg : nullptr, P.counters, st);
-    if (e != hipSuccess) return PV_ERR_HIP;
-    ++tr.launched;
-
-    if (need_assign && P.Mp > 0) {
-        tr.before();
-        e = pv::launch_gram_assign(dt, P.gram_cfg, vis, B, Nv, d, kept, budget, P.pruned, P.Mp,
-                                   P.invn, P.best_val, P.best_slot, asg, P.counters + B, st);
-        if (e != hipSuccess) return PV_ERR_HIP;
+    Trace tr{events, n_events, names, 0, st};
+    auto step = [&](hipError_t err) {
         ++tr.launched;
+        return err == hipSuccess;
+    };
+    tr.before("cos_stream");
+    if (!step(pv::launch_cos_tile(dt, P.cos_cfg, vis, anchors, B, Nv, Nt, d, P.M, P.invn, P.rowsum, st)))
+        return PV_ERR_HIP;
+    tr.before("center");
+    if (!step(pv::launch_center(P.M, P.rowsum, P.njt, B, Nt, Nv, p, st))) return PV_ERR_HIP;
+    tr.before("select");
+    if (!step(pv::launch_select(p, B, Nv, budget, kept, P.pruned, need_assign ? asg : nullptr, st)))
+        return PV_ERR_HIP;
+    if (need_assign && P.Mp > 0) {
+        tr.before(P.gram_cfg == pv::TILE_128 ? "gram_tile" : "gram_stream");
+        if (!step(pv::launch_gram(dt, P.gram_cfg, vis, B, Nv, d, kept, budget, P.pruned, P.Mp,
+                                  P.invn, P.best_val, P.best_slot, asg, st)))
+            return PV_ERR_HIP;
+        if (P.ntn > 1) {
+            tr.before("gram_finish");
+            if (!step(pv::launch_gram_finish(P.best_val, P.best_slot, B, P.ntn, P.Mp, Nv, P.pruned,
+                                             asg, st)))
+                return PV_ERR_HIP;
+        }
     }
     if (merged) {
-        tr.before();
-        e = pv::launch_merge(dt, vis, B, Nv, d, kept, budget, asg, merged, st);
-        if (e != hipSuccess) return PV_ERR_HIP;
-        ++tr.launched;
+        tr.before("merge");
+        if (!step(pv::launch_merge(dt, vis, B, Nv, d, budget, asg, merged, st))) return PV_ERR_HIP;
     }
     tr.after_all();
     if (n_kernels) *n_kernels = tr.launched;
@@ -201,7 +210,8 @@ int check_head(const void *q, const void *k, const int32_t *heads, int n_heads, 
 
 int head_impl(const void *q, const void *k, const int32_t *heads, int n_heads, int B, int H, int Nt,
               int N, int hd, int dtype, int budget, int32_t *kept, float *score, void *workspace,
-              size_t ws_bytes, void *stream, void *const *events, int n_events, int *n_kernels) {
+              size_t ws_bytes, void *stream, void *const *events, int n_events, int *n_kernels,
+              const char **names) {
     int rc = check_head(q, k, heads, n_heads, B, H, Nt, N, hd, dtype, budget, kept);
     if (rc != PV_OK) return rc;
     HeadPlan P0 = plan_head(nullptr, B, Nt, N, n_heads, score == nullptr);
@@ -213,17 +223,17 @@ int head_impl(const void *q, const void *k, const int32_t *heads, int n_heads, i
     float *v = score ? score : P.v;
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
     hipStream_t st = (hipStream_t)stream;
-    Trace tr{events, n_events, 0, st};
+    Trace tr{events, n_events, names, 0, st};
 
     pv::HeadArgs ha;
     memset(&ha, 0, sizeof(ha));
     memcpy(ha.h, heads, sizeof(int32_t) * (size_t)B * n_heads);
 
-    tr.before();
+    tr.before("score_partial");
     if (pv::launch_score_partial(dt, q, k, ha, B, H, Nt, N, hd, n_heads, P.partial, st) != hipSuccess)
         return PV_ERR_HIP;
     ++tr.launched;
-    tr.before();
+    tr.before("score_select");
     const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
     if (pv::launch_score_select(P.partial, B, n_heads * P.nrb, N, inv_norm, v, budget, kept, st) !=
         hipSuccess)
@@ -265,16 +275,16 @@ PV_API int pv_prune_dedup(const void *vis, const void *anchors, int B, int Nv, i
                           int dtype, int budget, int32_t *kept, float *score, int32_t *assign,
                           void *merged, void *workspace, size_t workspace_bytes, void *stream) {
     return dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, budget, kept, score, assign, merged,
-                      workspace, workspace_bytes, stream, nullptr, 0, nullptr);
+                      workspace, workspace_bytes, stream, nullptr, 0, nullptr, nullptr);
 }
 
 PV_API int pv_prune_dedup_timed(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
                                 int dtype, int budget, int32_t *kept, float *score,
                                 int32_t *assign, void *merged, void *workspace,
                                 size_t workspace_bytes, void *stream, void *const *events,
-                                int n_events, int *n_kernels) {
+                                int n_events, int *n_kernels, const char **names) {
     return dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, budget, kept, score, assign, merged,
-                      workspace, workspace_bytes, stream, events, n_events, n_kernels);
+                      workspace, workspace_bytes, stream, events, n_events, n_kernels, names);
 }
 
 PV_API size_t pv_head_aware_workspace_bytes(int B, int H, int Nt, int N, int hd, int n_heads,
@@ -292,16 +302,70 @@ PV_API int pv_prune_head_aware(const void *q, const void *k, const int32_t *head
                                int32_t *kept, float *score, void *workspace, size_t workspace_bytes,
                                void *stream) {
     return head_impl(q, k, heads_host, n_heads, B, H, Nt, N, hd, dtype, budget, kept, score,
-                     workspace, workspace_bytes, stream, nullptr, 0, nullptr);
+                     workspace, workspace_bytes, stream, nullptr, 0, nullptr, nullptr);
 }
 
 PV_API int pv_prune_head_aware_timed(const void *q, const void *k, const int32_t *heads_host,
                                      int n_heads, int B, int H, int Nt, int N, int hd, int dtype,
                                      int budget, int32_t *kept, float *score, void *workspace,
                                      size_t workspace_bytes, void *stream, void *const *events,
-                                     int n_events, int *n_kernels) {
+                                     int n_events, int *n_kernels, const char **names) {
     return head_impl(q, k, heads_host, n_heads, B, H, Nt, N, hd, dtype, budget, kept, score,
-                     workspace, workspace_bytes, stream, events, n_events, n_kernels);
+                     workspace, workspace_bytes, stream, events, n_events, n_kernels, names);
+}
+
+namespace {
+
+int fill_desc(const pv_gather_desc &in, int B, int k, pv::GatherDesc &out, int64_t *blocks) {
+    if (!in.src || !in.dst) return PV_ERR_NULL;
+    if (in.n_src < 1 || in.groups < 1 || in.row_bytes < 16) return PV_ERR_SHAPE;
+    if (!aligned16(in.src) || !aligned16(in.dst) || in.row_bytes % 16 || in.src_batch_stride % 16 ||
+        in.src_group_stride % 16 || in.src_row_stride % 16 || in.dst_batch_stride % 16 ||
+        in.dst_group_stride % 16 || in.dst_row_stride % 16)
+        return PV_ERR_ALIGN;
+    const int64_t cpr = in.row_bytes / 16;
+    const int64_t per_plane = cpr * k;  // 16-byte pieces of one plane
+    if (per_plane > 0x3FFFFFFF) return PV_ERR_SHAPE;
+    const int64_t span = 256 * pv::kGatherIT;
+    const int64_t bpp = (per_plane + span - 1) / span;
+    out.src = (const char *)in.src;
+    out.dst = (char *)in.dst;
+    out.n_src = in.n_src;
+    out.groups = in.groups;
+    out.cpr = (int)cpr;
+    out.bpp = (int)bpp;
+    out.sb = in.src_batch_stride;
+    out.sg = in.src_group_stride;
+    out.sr = in.src_row_stride;
+    out.db = in.dst_batch_stride;
+    out.dg = in.dst_group_stride;
+    out.dr = in.dst_row_stride;
+    *blocks = (int64_t)B * in.groups * bpp;
+    return PV_OK;
+}
+
+}  // namespace
+
+PV_API int pv_prune_gather_batch(const pv_gather_desc *descs, int n_desc, const int32_t *idx, int B,
+                                 int k, void *stream) {
+    if (!descs || !idx) return PV_ERR_NULL;
+    if (n_desc < 1 || n_desc > PV_MAX_GATHER || B < 1 || k < 1) return PV_ERR_SHAPE;
+    if (!aligned16(idx)) return PV_ERR_ALIGN;
+    pv::GatherArgs ga;
+    memset(&ga, 0, sizeof(ga));
+    ga.n = n_desc;
+    int64_t run = 0;
+    for (int t = 0; t < n_desc; ++t) {
+        int64_t blocks = 0;
+        const int rc = fill_desc(descs[t], B, k, ga.d[t], &blocks);
+        if (rc != PV_OK) return rc;
+        ga.bstart[t] = (int)run;
+        run += blocks;
+        if (run > 0x7FFFFFFF) return PV_ERR_SHAPE;
+    }
+    ga.bstart[n_desc] = (int)run;
+    if (pv::launch_gather(ga, idx, B, k, (hipStream_t)stream) != hipSuccess) return PV_ERR_HIP;
+    return PV_OK;
 }
 
 PV_API int pv_prune_gather(const void *src, void *dst, const int32_t *idx, int B, int n_src, int k,
@@ -310,16 +374,17 @@ PV_API int pv_prune_gather(const void *src, void *dst, const int32_t *idx, int B
                            int64_t dst_batch_stride, int64_t dst_group_stride,
                            int64_t dst_row_stride, void *stream) {
     if (!src || !dst || !idx) return PV_ERR_NULL;
-    if (B < 1 || B > 65535 || n_src < 1 || k < 1 || groups < 1 || groups > 65535 || row_bytes < 16)
-        return PV_ERR_SHAPE;
-    if ((row_bytes / 16) * (long long)k > 0x7FFFFFFFLL) return PV_ERR_SHAPE;
-    if (!aligned16(src) || !aligned16(dst) || !aligned16(idx) || row_bytes % 16 ||
-        src_batch_stride % 16 || src_group_stride % 16 || src_row_stride % 16 ||
-        dst_batch_stride % 16 || dst_group_stride % 16 || dst_row_stride % 16)
-        return PV_ERR_ALIGN;
-    if (pv::launch_gather(src, dst, idx, B, n_src, k, groups, row_bytes, src_batch_stride,
-                          src_group_stride, src_row_stride, dst_batch_stride, dst_group_stride,
-                          dst_row_stride, (hipStream_t)stream) != hipSuccess)
-        return PV_ERR_HIP;
-    return PV_OK;
+    pv_gather_desc d;
+    d.src = src;
+    d.dst = dst;
+    d.n_src = n_src;
+    d.groups = groups;
+    d.row_bytes = row_bytes;
+    d.src_batch_stride = src_batch_stride;
+    d.src_group_stride = src_group_stride;
+    d.src_row_stride = src_row_stride;
+    d.dst_batch_stride = dst_batch_stride;
+    d.dst_group_stride = dst_group_stride;
+    d.dst_row_stride = dst_row_stride;
+    return pv_prune_gather_batch(&d, 1, idx, B, k, stream);
 }

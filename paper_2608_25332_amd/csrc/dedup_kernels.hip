@@ -3,14 +3,22 @@
 // nearest-centroid assignment of the pruned tokens and their aggregation.
 //
 // Kernel sequence of one call (all on the caller's stream):
-//   cos_tile      anchors x vis on MFMA, norms fused; writes cosines, the
-//                 inverse norms of the visual tokens and per-tile row sums
-//   center_select p[j] = max_i (M[i][j] - mean_i); the last workgroup of a
-//                 sample runs the top-N_1 radix select
-//   gram_assign   pruned x kept cosine Gram on MFMA with a fused row argmax;
-//                 the last workgroup of a row tile reduces across column tiles
+//   cos_stream    anchors x vis on MFMA (streaming tiles, norms fused);
+//                 writes the cosines, the inverse norms of the visual tokens
+//                 and per-tile row sums
+//   center        p[j] = max_i (M[i][j] - mean_i)
+//   select        top-N_1 radix select, one workgroup per sample
+//   gram_*        pruned x kept cosine Gram on MFMA with a fused row argmax
+//                 per column tile (streaming tiles at small sizes, LDS-staged
+//                 128x128 tiles when the Gram is large enough to be
+//                 MFMA-bound)
+//   gram_finish   best column tile per pruned row -> assignment
 //   merge         centroid <- mean of itself and its members
+// Workgroups never wait on or signal each other: every cross-workgroup
+// dependency is a kernel boundary, so no kernel needs a device-wide fence
+// (on this chip a device-scope fence writes back and invalidates the L2).
 #include "pv_launch.h"
+#include "pv_stream_tile.h"
 #include "pv_tile_gemm.h"
 
 #include <math.h>
@@ -19,66 +27,71 @@ namespace pv {
 
 int tile_size(int cfg) { return 16 << cfg; }
 
-// ----------------------------------------------------------------------------
-// cos_tile: grid (Nv tiles, Nt tiles, B).
-// ----------------------------------------------------------------------------
-template <int DT, int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(64 * WM * WN) void cos_tile_kernel(
-    const char *__restrict__ vis, const char *__restrict__ anchors, int Nv, int Nt, int d_bytes,
-    float *__restrict__ M, float *__restrict__ invn_vis, float *__restrict__ rowsum,
-    unsigned *__restrict__ counters, int n_counters) {
-    using G = TileGemm<DT, BM, BN, WM, WN>;
-    __shared__ __attribute__((aligned(16))) char lds[G::LDS_BYTES];
-    __shared__ float rowss[G::ROWS];
-    __shared__ float rowinv[G::ROWS];
-    __shared__ float red[WN][BM];
+// Waves and unroll depth of a streaming tile: enough 16-byte loads in flight
+// per workgroup to cover memory latency within ~128 VGPRs of fragments.
+template <int T> struct StreamCfg;
+template <> struct StreamCfg<16> { static constexpr int NW = 8, U = 8; };
+template <> struct StreamCfg<32> { static constexpr int NW = 4, U = 4; };
+template <> struct StreamCfg<64> { static constexpr int NW = 4, U = 2; };
 
-    const int jt = blockIdx.x, it = blockIdx.y, b = blockIdx.z;
-    const int njt = gridDim.x;
+// ----------------------------------------------------------------------------
+// cos_stream: 1-D grid over (sample, vis tile, anchor tile) in XCD order.
+// ----------------------------------------------------------------------------
+template <int DT, int T>
+__global__ __launch_bounds__(64 * StreamCfg<T>::NW) void cos_stream_kernel(
+    const char *__restrict__ vis, const char *__restrict__ anchors, int B, int Nv, int Nt,
+    int d_bytes, int njt, int nit, float *__restrict__ M, float *__restrict__ invn_vis,
+    float *__restrict__ rowsum) {
+    constexpr int NW = StreamCfg<T>::NW, U = StreamCfg<T>::U;
+    using S = StreamTile<DT, T, T, NW, U>;
+    constexpr int F = T / 16;
+    __shared__ float red[S::RED_FLOATS];
+
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / WN, wn = wave % WN;
+    const int total = B * njt * nit;
+    const int tile = xcd_tile(blockIdx.x, total);
+    const int it = tile % nit;
+    const int jt = (tile / nit) % njt;
+    const int b = tile / (nit * njt);
 
-    // Later kernels of this call count finished workgroups in `counters`.
-    if (jt == 0 && it == 0 && b == 0)
-        for (int e = tid; e < n_counters; e += G::NT) counters[e] = 0u;
-
-    const int i0 = it * BM, j0 = jt * BN;
-    const char *abase = anchors + (size_t)b * Nt * d_bytes;
-    const char *vbase = vis + (size_t)b * Nv * d_bytes;
-    auto row_ptr = [&](int r) -> const char * {
-        if (r < BM) return abase + (size_t)min(i0 + r, Nt - 1) * d_bytes;
-        return vbase + (size_t)min(j0 + r - BM, Nv - 1) * d_bytes;
-    };
-
-    f32x4_t acc[G::FM][G::FN];
-    float ss[G::PPT];
-    G::template run<true>(row_ptr, d_bytes / G::CHUNK, lds, acc, ss);
-    G::reduce_rows(ss, rowss);
-    __syncthreads();
-    for (int r = tid; r < G::ROWS; r += G::NT) {
-        float s = rowss[r];
-        rowinv[r] = (s > 0.f) ? 1.0f / sqrtf(s) : 0.f;
-    }
-    __syncthreads();
-
-    if (it == 0) {
-        for (int c = tid; c < BN; c += G::NT)
-            if (j0 + c < Nv) invn_vis[(size_t)b * Nv + j0 + c] = rowinv[BM + c];
-    }
-
+    const int i0 = it * T, j0 = jt * T;
+    const int koff = (lane >> 4) * 16;
+    const char *abase = anchors + (size_t)b * Nt * d_bytes + koff;
+    const char *vbase = vis + (size_t)b * Nv * d_bytes + koff;
+    const char *rp[2 * F];
 #pragma unroll
-    for (int fm = 0; fm < G::FM; ++fm) {
+    for (int f = 0; f < F; ++f) {
+        rp[f] = abase + (size_t)min(i0 + f * 16 + (lane & 15), Nt - 1) * d_bytes;
+        rp[F + f] = vbase + (size_t)min(j0 + f * 16 + (lane & 15), Nv - 1) * d_bytes;
+    }
+    f32x4_t acc[F][F];
+    float ss[2 * F];
+    S::template run<true>(rp, d_bytes / 64, acc, ss);
+    S::template reduce<true>(acc, ss, red);
+    if (wave != 0) return;
+
+    float inv[2 * F];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = wm * G::SUB_M + fm * 16 + (lane >> 4) * 4 + i;
-            const int gi = i0 + r;
-            const float ia = rowinv[r];
+    for (int q = 0; q < 2 * F; ++q) inv[q] = (ss[q] > 0.f) ? 1.0f / sqrtf(ss[q]) : 0.f;
+    if (it == 0 && lane < 16) {
+#pragma unroll
+        for (int f = 0; f < F; ++f) {
+            const int j = j0 + f * 16 + lane;
+            if (j < Nv) invn_vis[(size_t)b * Nv + j] = inv[F + f];
+        }
+    }
+#pragma unroll
+    for (int fm = 0; fm < F; ++fm) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int rl = (lane >> 4) * 4 + e;  // row inside the 16-row block
+            const int gi = i0 + fm * 16 + rl;
+            const float ia = __shfl(inv[fm], rl, 64);
             float rs = 0.f;
 #pragma unroll
-            for (int fn = 0; fn < G::FN; ++fn) {
-                const int c = wn * G::SUB_N + fn * 16 + (lane & 15);
-                const int gj = j0 + c;
-                const float cs = acc[fm][fn][i] * ia * rowinv[BM + c];
+            for (int fn = 0; fn < F; ++fn) {
+                const int gj = j0 + fn * 16 + (lane & 15);
+                const float cs = acc[fm][fn][e] * ia * inv[F + fn];
                 if (gj < Nv) {
                     rs += cs;
                     if (gi < Nt) M[((size_t)b * Nt + gi) * Nv + gj] = cs;
@@ -88,85 +101,198 @@ __global__ __launch_bounds__(64 * WM * WN) void cos_tile_kernel(
             rs += __shfl_xor(rs, 2, 64);
             rs += __shfl_xor(rs, 4, 64);
             rs += __shfl_xor(rs, 8, 64);
-            if ((lane & 15) == 0) red[wn][r] = rs;
+            if ((lane & 15) == 0 && gi < Nt) rowsum[((size_t)b * njt + jt) * Nt + gi] = rs;
         }
-    }
-    __syncthreads();
-    for (int r = tid; r < BM; r += G::NT) {
-        float s = 0.f;
-#pragma unroll
-        for (int w = 0; w < WN; ++w) s += red[w][r];
-        if (i0 + r < Nt) rowsum[((size_t)b * njt + jt) * Nt + i0 + r] = s;
     }
 }
 
 // ----------------------------------------------------------------------------
-// center_select: grid (ceil(Nv / 256), B), 256 threads.
+// center: grid (ceil(Nv / 64), B), 256 threads; 4 threads per token.
 // ----------------------------------------------------------------------------
-constexpr int kSelNT = 256;
+constexpr int kCenNT = 256;
+constexpr int kCenTok = 64;
 
-__global__ __launch_bounds__(kSelNT) void center_select_kernel(
-    const float *__restrict__ M, const float *__restrict__ rowsum, int njt, int Nt, int Nv,
-    float *__restrict__ p, int budget, int32_t *__restrict__ kept, int32_t *__restrict__ pruned,
-    int32_t *__restrict__ slot_of, unsigned *__restrict__ counters) {
+__global__ __launch_bounds__(kCenNT) void center_kernel(const float *__restrict__ M,
+                                                        const float *__restrict__ rowsum, int njt,
+                                                        int Nt, int Nv, float *__restrict__ p) {
     extern __shared__ float mu[];  // [Nt]
-    __shared__ TopkSmem sm;
-    __shared__ int is_last;
+    __shared__ float part[4][kCenTok];
     const int b = blockIdx.y, tid = threadIdx.x;
-    const int j = blockIdx.x * kSelNT + tid;
-
-    // Row means of M over all Nv tokens, from the per-tile partial sums.
-    for (int i = tid; i < Nt; i += kSelNT) {
+    // Row means of M over all Nv tokens, from the per-tile partial sums
+    // (added in tile order).
+    for (int i = tid; i < Nt; i += kCenNT) {
+        const float *rs = rowsum + (size_t)b * njt * Nt + i;
         float s = 0.f;
-        for (int t = 0; t < njt; ++t) s += rowsum[((size_t)b * njt + t) * Nt + i];
+#pragma unroll 8
+        for (int t = 0; t < njt; ++t) s += rs[(size_t)t * Nt];
         mu[i] = s / (float)Nv;
     }
     __syncthreads();
+    const int jl = tid & (kCenTok - 1), g = tid / kCenTok;
+    const int j = blockIdx.x * kCenTok + jl;
+    float m = -INFINITY;
     if (j < Nv) {
         const float *col = M + (size_t)b * Nt * Nv + j;
-        float m = col[0] - mu[0];
-        for (int i = 1; i < Nt; ++i) m = fmaxf(m, col[(size_t)i * Nv] - mu[i]);
-        p[(size_t)b * Nv + j] = m;
+#pragma unroll 4
+        for (int i = g; i < Nt; i += 4) m = fmaxf(m, col[(size_t)i * Nv] - mu[i]);
     }
-
-    // The last workgroup of this sample selects the top `budget` tokens.
-    __threadfence();
+    part[g][jl] = m;
     __syncthreads();
-    if (tid == 0) is_last = (atomicAdd(&counters[b], 1u) == gridDim.x - 1);
-    __syncthreads();
-    if (!is_last) return;
-    __threadfence();
-    block_topk<kSelNT>(p + (size_t)b * Nv, Nv, budget, kept + (size_t)b * budget,
-                       pruned ? pruned + (size_t)b * (Nv - budget) : nullptr,
-                       slot_of ? slot_of + (size_t)b * Nv : nullptr, sm);
+    if (g == 0 && j < Nv)
+        p[(size_t)b * Nv + j] = fmaxf(fmaxf(part[0][jl], part[1][jl]), fmaxf(part[2][jl], part[3][jl]));
 }
 
 // ----------------------------------------------------------------------------
-// gram_assign: grid (N1 tiles, Mp tiles, B).  A rows = pruned tokens, B rows =
-// kept tokens.  Each workgroup finds, for each of its pruned rows, the best
-// (cosine, slot) within its column tile; ordering (higher cosine, then lower
-// slot) is a total order, so the maximum does not depend on reduction order.
+// select: grid (B), 256 threads; top-`budget` of p with its complement list
+// and the slot of every kept token.  Keys are staged in LDS up to kStageKeys.
+// ----------------------------------------------------------------------------
+constexpr int kSelNT = 256;
+constexpr int kStageKeys = 8192;
+
+__global__ __launch_bounds__(kSelNT) void select_kernel(const float *__restrict__ p, int Nv,
+                                                        int budget, int32_t *__restrict__ kept,
+                                                        int32_t *__restrict__ pruned,
+                                                        int32_t *__restrict__ slot_of) {
+    extern __shared__ uint32_t keys[];  // [Nv] when staged
+    __shared__ TopkSmem sm;
+    const int b = blockIdx.x;
+    block_topk<kSelNT>(p + (size_t)b * Nv, Nv, budget, kept + (size_t)b * budget,
+                       pruned ? pruned + (size_t)b * (Nv - budget) : nullptr,
+                       slot_of ? slot_of + (size_t)b * Nv : nullptr, sm,
+                       Nv <= kStageKeys ? keys : nullptr);
+}
+
+// ----------------------------------------------------------------------------
+// Nearest centroid: best (cosine, slot) of every pruned row.  Ordering by
+// higher cosine, then lower slot, is a total order, so the maximum does not
+// depend on the order in which candidates are combined.
 // ----------------------------------------------------------------------------
 __device__ __forceinline__ bool better(float v, int s, float bv, int bs) {
     return v > bv || (v == bv && s < bs);
 }
 
+// gram_finish: grid (ceil(Mp / 256), B).  Best column tile of every pruned
+// row, combined in tile order with the total order above.
+constexpr int kFinNT = 256;
+
+__global__ __launch_bounds__(kFinNT) void gram_finish_kernel(const float *__restrict__ best_val,
+                                                             const int32_t *__restrict__ best_slot,
+                                                             int ntn, int Mp, int Nv,
+                                                             const int32_t *__restrict__ pruned,
+                                                             int32_t *__restrict__ assign) {
+    const int b = blockIdx.y;
+    const int m = blockIdx.x * kFinNT + threadIdx.x;
+    if (m >= Mp) return;
+    float bv = -INFINITY;
+    int bs = 0x7FFFFFFF;
+    for (int t = 0; t < ntn; ++t) {
+        const float v = best_val[((size_t)b * ntn + t) * Mp + m];
+        const int s = best_slot[((size_t)b * ntn + t) * Mp + m];
+        if (better(v, s, bv, bs)) {
+            bv = v;
+            bs = s;
+        }
+    }
+    assign[(size_t)b * Nv + pruned[(size_t)b * Mp + m]] = bs;
+}
+
+// gram_stream: 1-D grid over (sample, pruned-row tile, kept-column tile).
+template <int DT, int T>
+__global__ __launch_bounds__(64 * StreamCfg<T>::NW) void gram_stream_kernel(
+    const char *__restrict__ vis, int B, int Nv, int d_bytes, const int32_t *__restrict__ kept,
+    int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn,
+    const float *__restrict__ invn, float *__restrict__ best_val,
+    int32_t *__restrict__ best_slot, int32_t *__restrict__ assign) {
+    constexpr int NW = StreamCfg<T>::NW, U = StreamCfg<T>::U;
+    using S = StreamTile<DT, T, T, NW, U>;
+    constexpr int F = T / 16;
+    __shared__ float red[S::RED_FLOATS];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int total = B * ntm * ntn;
+    const int tile = xcd_tile(blockIdx.x, total);
+    const int nt = tile % ntn;
+    const int mt = (tile / ntn) % ntm;
+    const int b = tile / (ntn * ntm);
+    const int m0 = mt * T, n0 = nt * T;
+    const int32_t *pr = pruned + (size_t)b * Mp;
+    const int32_t *kp = kept + (size_t)b * N1;
+    const int koff = (lane >> 4) * 16;
+    const char *vbase = vis + (size_t)b * Nv * d_bytes + koff;
+
+    const char *rp[2 * F];
+    float inv[2 * F];
+#pragma unroll
+    for (int f = 0; f < F; ++f) {
+        const int ta = pr[min(m0 + f * 16 + (lane & 15), Mp - 1)];
+        const int tb = kp[min(n0 + f * 16 + (lane & 15), N1 - 1)];
+        rp[f] = vbase + (size_t)ta * d_bytes;
+        rp[F + f] = vbase + (size_t)tb * d_bytes;
+        inv[f] = invn[(size_t)b * Nv + ta];
+        inv[F + f] = invn[(size_t)b * Nv + tb];
+    }
+    f32x4_t acc[F][F];
+    float ss[2 * F];
+    S::template run<false>(rp, d_bytes / 64, acc, ss);
+    S::template reduce<false>(acc, ss, red);
+
+    if (wave == 0) {
+#pragma unroll
+        for (int fm = 0; fm < F; ++fm) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int rl = (lane >> 4) * 4 + e;
+                const float ia = __shfl(inv[fm], rl, 64);
+                float bv = -INFINITY;
+                int bs = 0x7FFFFFFF;
+#pragma unroll
+                for (int fn = 0; fn < F; ++fn) {
+                    const int slot = n0 + fn * 16 + (lane & 15);
+                    const float cs = acc[fm][fn][e] * ia * inv[F + fn];
+                    if (slot < N1 && better(cs, slot, bv, bs)) {
+                        bv = cs;
+                        bs = slot;
+                    }
+                }
+#pragma unroll
+                for (int off = 1; off < 16; off <<= 1) {
+                    const float ov = __shfl_xor(bv, off, 64);
+                    const int os = __shfl_xor(bs, off, 64);
+                    if (better(ov, os, bv, bs)) {
+                        bv = ov;
+                        bs = os;
+                    }
+                }
+                const int m = m0 + fm * 16 + rl;
+                if ((lane & 15) == 0 && m < Mp) {
+                    if (ntn == 1) {
+                        assign[(size_t)b * Nv + pr[m]] = bs;
+                    } else {
+                        best_val[((size_t)b * ntn + nt) * Mp + m] = bv;
+                        best_slot[((size_t)b * ntn + nt) * Mp + m] = bs;
+                    }
+                }
+            }
+        }
+    }
+}
+
+// gram_tile: LDS-staged 128 x 128 tiles for the large, MFMA-bound Grams.
+// grid (N1 tiles, Mp tiles, B).
 template <int DT, int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(64 * WM * WN) void gram_assign_kernel(
+__global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
     const char *__restrict__ vis, int Nv, int d_bytes, const int32_t *__restrict__ kept, int N1,
     const int32_t *__restrict__ pruned, int Mp, const float *__restrict__ invn,
-    float *__restrict__ best_val, int32_t *__restrict__ best_slot, int32_t *__restrict__ assign,
-    unsigned *__restrict__ counters) {
+    float *__restrict__ best_val, int32_t *__restrict__ best_slot, int32_t *__restrict__ assign) {
     using G = TileGemm<DT, BM, BN, WM, WN>;
     __shared__ __attribute__((aligned(16))) char lds[G::LDS_BYTES];
     __shared__ int32_t rowtok[G::ROWS];
     __shared__ float rowinv[G::ROWS];
     __shared__ float red_v[WN][BM];
     __shared__ int red_s[WN][BM];
-    __shared__ int is_last;
 
     const int nt = blockIdx.x, mt = blockIdx.y, b = blockIdx.z;
-    const int ntn = gridDim.x, ntm = gridDim.y;
+    const int ntn = gridDim.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
     const int m0 = mt * BM, n0 = nt * BN;
@@ -174,7 +300,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_assign_kernel(
     const int32_t *kp = kept + (size_t)b * N1;
 
     for (int r = tid; r < G::ROWS; r += G::NT) {
-        int tok = (r < BM) ? pr[min(m0 + r, Mp - 1)] : kp[min(n0 + r - BM, N1 - 1)];
+        const int tok = (r < BM) ? pr[min(m0 + r, Mp - 1)] : kp[min(n0 + r - BM, N1 - 1)];
         rowtok[r] = tok;
         rowinv[r] = invn[(size_t)b * Nv + tok];
     }
@@ -206,8 +332,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_assign_kernel(
             }
 #pragma unroll
             for (int off = 1; off < 16; off <<= 1) {
-                float ov = __shfl_xor(bv, off, 64);
-                int os = __shfl_xor(bs, off, 64);
+                const float ov = __shfl_xor(bv, off, 64);
+                const int os = __shfl_xor(bs, off, 64);
                 if (better(ov, os, bv, bs)) {
                     bv = ov;
                     bs = os;
@@ -239,39 +365,19 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_assign_kernel(
             }
         }
     }
-    if (ntn == 1) return;
-
-    // The last column tile of this row tile reduces across column tiles.
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) is_last = (atomicAdd(&counters[(size_t)b * ntm + mt], 1u) == (unsigned)ntn - 1);
-    __syncthreads();
-    if (!is_last) return;
-    __threadfence();
-    for (int r = tid; r < BM; r += G::NT) {
-        const int m = m0 + r;
-        if (m >= Mp) continue;
-        float bv = -INFINITY;
-        int bs = 0x7FFFFFFF;
-        for (int t = 0; t < ntn; ++t) {
-            float v = best_val[((size_t)b * ntn + t) * Mp + m];
-            int s = best_slot[((size_t)b * ntn + t) * Mp + m];
-            if (better(v, s, bv, bs)) {
-                bv = v;
-                bs = s;
-            }
-        }
-        assign[(size_t)b * Nv + rowtok[r]] = bs;
-    }
 }
 
 // ----------------------------------------------------------------------------
-// merge: grid (N1, B), 256 threads.  Members of slot s are found by scanning
-// the assignment 64 tokens at a time with a wave ballot, in ascending token
-// order, so the fp32 sums have a fixed order.
+// merge: grid (N1, B), 256 threads.  The members of slot s (the tokens whose
+// assignment is s, the kept token itself included) are collected in
+// ascending token order by one wave with ballots over the assignment (staged
+// in LDS when it fits), then all threads add the member rows in that order
+// (fp32), four rows in flight at a time.
 // ----------------------------------------------------------------------------
 constexpr int kMergeNT = 256;
-constexpr int kMergeCPT = 4;  // 16-byte chunks per thread per pass
+constexpr int kMergeCPT = 4;      // 16-byte chunks per thread per pass
+constexpr int kMergeList = 4096;  // members held in LDS per round; also the
+                                  // largest assignment staged in LDS
 
 template <int DT>
 __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict__ vis, int Nv,
@@ -279,12 +385,22 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
                                                          const int32_t *__restrict__ assign,
                                                          int N1, char *__restrict__ merged) {
     constexpr int EPC = (DT == kBF16) ? 8 : 4;  // elements per 16-byte chunk
+    __shared__ int list[kMergeList];
+    __shared__ int staged[kMergeList];
+    __shared__ int s_count, s_next;
     const int s = blockIdx.x, b = blockIdx.y;
     const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nchunk = d_bytes / 16;
     const int32_t *as = assign + (size_t)b * Nv;
     const char *vb = vis + (size_t)b * Nv * d_bytes;
     char *out = merged + ((size_t)b * N1 + s) * d_bytes;
+    const bool stage = Nv <= kMergeList;
+    if (stage) {
+        for (int j = tid; j < Nv; j += kMergeNT) staged[j] = as[j];
+        __syncthreads();
+    }
+    const int *src = stage ? (const int *)staged : (const int *)as;
 
     for (int cbase = 0; cbase < nchunk; cbase += kMergeNT * kMergeCPT) {
         float acc[kMergeCPT][EPC];
@@ -292,57 +408,78 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
         for (int t = 0; t < kMergeCPT; ++t)
 #pragma unroll
             for (int e = 0; e < EPC; ++e) acc[t][e] = 0.f;
-        int count = 0;
-        for (int base = 0; base < Nv; base += 64) {
-            const int jj = base + lane;
-            const int a = (jj < Nv) ? as[jj] : -1;
-            unsigned long long mask = __ballot(a == s);
-            while (mask) {
-                const int bit = __ffsll((long long)mask) - 1;
-                mask &= mask - 1ull;
-                const char *row = vb + (size_t)(base + bit) * d_bytes;
-                ++count;
+        int scan_from = 0, total = 0;
+        while (true) {
+            if (wave == 0) {
+                // collect up to kMergeList members from token scan_from on
+                int cnt = 0, pos = scan_from;
+                while (pos < Nv) {
+                    const int a0 = (pos + lane < Nv) ? src[pos + lane] : -1;
+                    const unsigned long long mk = __ballot(a0 == s);
+                    const int nb = __popcll(mk);
+                    if (cnt + nb > kMergeList) break;
+                    if (a0 == s) list[cnt + __popcll(mk & ((1ull << lane) - 1ull))] = pos + lane;
+                    cnt += nb;
+                    pos += 64;
+                }
+                if (lane == 0) {
+                    s_count = cnt;
+                    s_next = pos;
+                }
+            }
+            __syncthreads();
+            const int cnt = s_count;
+            scan_from = s_next;
+            total += cnt;
+            for (int m = 0; m < cnt; m += 4) {
+                uint4 v[4][kMergeCPT];
 #pragma unroll
-                for (int t = 0; t < kMergeCPT; ++t) {
-                    const int c = cbase + tid + t * kMergeNT;
-                    if (c < nchunk) {
-                        uint4 v = ld16(row + (size_t)c * 16);
-                        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+                for (int u = 0; u < 4; ++u) {
+                    const char *row = vb + (size_t)list[min(m + u, cnt - 1)] * d_bytes;
+#pragma unroll
+                    for (int t = 0; t < kMergeCPT; ++t) {
+                        const int c = min(cbase + tid + t * kMergeNT, nchunk - 1);
+                        v[u][t] = ld16(row + (size_t)c * 16);
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    if (m + u >= cnt) break;
+#pragma unroll
+                    for (int t = 0; t < kMergeCPT; ++t) {
+                        const uint32_t w4[4] = {v[u][t].x, v[u][t].y, v[u][t].z, v[u][t].w};
                         if (DT == kBF16) {
 #pragma unroll
                             for (int q = 0; q < 4; ++q) {
-                                acc[t][2 * q] += __uint_as_float(w[q] << 16);
-                                acc[t][2 * q + 1] += __uint_as_float(w[q] & 0xFFFF0000u);
+                                acc[t][2 * q] += __uint_as_float(w4[q] << 16);
+                                acc[t][2 * q + 1] += __uint_as_float(w4[q] & 0xFFFF0000u);
                             }
                         } else {
 #pragma unroll
-                            for (int q = 0; q < 4; ++q) acc[t][q] += __uint_as_float(w[q]);
+                            for (int q = 0; q < 4; ++q) acc[t][q] += __uint_as_float(w4[q]);
                         }
                     }
                 }
             }
+            __syncthreads();
+            if (scan_from >= Nv) break;
         }
-        const float cnt = (float)count;
+        const float cnt = (float)total;
 #pragma unroll
         for (int t = 0; t < kMergeCPT; ++t) {
             const int c = cbase + tid + t * kMergeNT;
             if (c >= nchunk) continue;
-            uint4 v;
-            uint32_t w[4];
+            uint32_t w4[4];
             if (DT == kBF16) {
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
-                    w[q] = f32_to_bf16_rne(acc[t][2 * q] / cnt) |
-                           (f32_to_bf16_rne(acc[t][2 * q + 1] / cnt) << 16);
+                    w4[q] = f32_to_bf16_rne(acc[t][2 * q] / cnt) |
+                            (f32_to_bf16_rne(acc[t][2 * q + 1] / cnt) << 16);
             } else {
 #pragma unroll
-                for (int q = 0; q < 4; ++q) w[q] = __float_as_uint(acc[t][q] / cnt);
+                for (int q = 0; q < 4; ++q) w4[q] = __float_as_uint(acc[t][q] / cnt);
             }
-            v.x = w[0];
-            v.y = w[1];
-            v.z = w[2];
-            v.w = w[3];
-            st16(out + (size_t)c * 16, v);
+            st16(out + (size_t)c * 16, uint4{w4[0], w4[1], w4[2], w4[3]});
         }
     }
 }
@@ -350,94 +487,107 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
 // ----------------------------------------------------------------------------
 // launchers
 // ----------------------------------------------------------------------------
-template <int DT, int BM, int BN, int WM, int WN>
-static hipError_t cos_tile_go(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
-                              float *M, float *invn, float *rowsum, unsigned *counters,
-                              int n_counters, hipStream_t st) {
+template <int DT, int T>
+static hipError_t cos_go(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
+                         float *M, float *invn, float *rowsum, hipStream_t st) {
     const int esz = (DT == kBF16) ? 2 : 4;
-    dim3 grid((Nv + BN - 1) / BN, (Nt + BM - 1) / BM, B);
-    hipLaunchKernelGGL((cos_tile_kernel<DT, BM, BN, WM, WN>), grid, dim3(64 * WM * WN), 0, st,
-                       (const char *)vis, (const char *)anchors, Nv, Nt, d * esz, M, invn, rowsum,
-                       counters, n_counters);
+    const int njt = (Nv + T - 1) / T, nit = (Nt + T - 1) / T;
+    hipLaunchKernelGGL((cos_stream_kernel<DT, T>), dim3(B * njt * nit),
+                       dim3(64 * StreamCfg<T>::NW), 0, st, (const char *)vis, (const char *)anchors,
+                       B, Nv, Nt, d * esz, njt, nit, M, invn, rowsum);
     return hipGetLastError();
 }
 
 template <int DT>
-static hipError_t cos_tile_dt(int cfg, const void *vis, const void *anchors, int B, int Nv, int Nt,
-                              int d, float *M, float *invn, float *rowsum, unsigned *counters,
-                              int n_counters, hipStream_t st) {
+static hipError_t cos_dt(int cfg, const void *vis, const void *anchors, int B, int Nv, int Nt,
+                         int d, float *M, float *invn, float *rowsum, hipStream_t st) {
     switch (cfg) {
-        case TILE_16:
-            return cos_tile_go<DT, 16, 16, 1, 1>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, counters, n_counters, st);
-        case TILE_32:
-            return cos_tile_go<DT, 32, 32, 2, 2>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, counters, n_counters, st);
-        case TILE_64:
-            return cos_tile_go<DT, 64, 64, 2, 2>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, counters, n_counters, st);
-        case TILE_128:
-            return cos_tile_go<DT, 128, 128, 2, 2>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, counters, n_counters, st);
+        case TILE_16: return cos_go<DT, 16>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
+        case TILE_32: return cos_go<DT, 32>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
+        case TILE_64: return cos_go<DT, 64>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
     }
     return hipErrorInvalidValue;
 }
 
 hipError_t launch_cos_tile(int dt, int cfg, const void *vis, const void *anchors, int B, int Nv,
-                           int Nt, int d, float *M, float *invn, float *rowsum, unsigned *counters,
-                           int n_counters, hipStream_t st) {
-    if (dt == kBF16)
-        return cos_tile_dt<kBF16>(cfg, vis, anchors, B, Nv, Nt, d, M, invn, rowsum, counters, n_counters, st);
-    return cos_tile_dt<kF32>(cfg, vis, anchors, B, Nv, Nt, d, M, invn, rowsum, counters, n_counters, st);
+                           int Nt, int d, float *M, float *invn, float *rowsum, hipStream_t st) {
+    if (dt == kBF16) return cos_dt<kBF16>(cfg, vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
+    return cos_dt<kF32>(cfg, vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
 }
 
-hipError_t launch_center_select(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
-                                float *p, int budget, int32_t *kept, int32_t *pruned,
-                                int32_t *slot_of, unsigned *counters, hipStream_t st) {
-    dim3 grid((Nv + kSelNT - 1) / kSelNT, B);
-    hipLaunchKernelGGL(center_select_kernel, grid, dim3(kSelNT), Nt * sizeof(float), st, M, rowsum,
-                       njt, Nt, Nv, p, budget, kept, pruned, slot_of, counters);
+hipError_t launch_center(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
+                         float *p, hipStream_t st) {
+    dim3 grid((Nv + kCenTok - 1) / kCenTok, B);
+    hipLaunchKernelGGL(center_kernel, grid, dim3(kCenNT), (size_t)Nt * sizeof(float), st, M, rowsum,
+                       njt, Nt, Nv, p);
     return hipGetLastError();
 }
 
-template <int DT, int BM, int BN, int WM, int WN>
-static hipError_t gram_go(const void *vis, int B, int Nv, int d, const int32_t *kept, int N1,
-                          const int32_t *pruned, int Mp, const float *invn, float *best_val,
-                          int32_t *best_slot, int32_t *assign, unsigned *counters, hipStream_t st) {
+hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kept, int32_t *pruned,
+                         int32_t *slot_of, hipStream_t st) {
+    const size_t lds = (Nv <= kStageKeys) ? (size_t)Nv * sizeof(uint32_t) : 0;
+    hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelNT), lds, st, p, Nv, budget, kept, pruned,
+                       slot_of);
+    return hipGetLastError();
+}
+
+template <int DT, int T>
+static hipError_t gram_stream_go(const void *vis, int B, int Nv, int d, const int32_t *kept,
+                                 int N1, const int32_t *pruned, int Mp, const float *invn,
+                                 float *best_val, int32_t *best_slot, int32_t *assign,
+                                 hipStream_t st) {
     const int esz = (DT == kBF16) ? 2 : 4;
-    dim3 grid((N1 + BN - 1) / BN, (Mp + BM - 1) / BM, B);
-    hipLaunchKernelGGL((gram_assign_kernel<DT, BM, BN, WM, WN>), grid, dim3(64 * WM * WN), 0, st,
+    const int ntm = (Mp + T - 1) / T, ntn = (N1 + T - 1) / T;
+    hipLaunchKernelGGL((gram_stream_kernel<DT, T>), dim3(B * ntm * ntn),
+                       dim3(64 * StreamCfg<T>::NW), 0, st, (const char *)vis, B, Nv, d * esz,
+                       kept, N1, pruned, Mp, ntm, ntn, invn, best_val, best_slot, assign);
+    return hipGetLastError();
+}
+
+template <int DT>
+static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int32_t *kept, int N1,
+                               const int32_t *pruned, int Mp, const float *invn, float *best_val,
+                               int32_t *best_slot, int32_t *assign, hipStream_t st) {
+    const int esz = (DT == kBF16) ? 2 : 4;
+    dim3 grid((N1 + 127) / 128, (Mp + 127) / 128, B);
+    hipLaunchKernelGGL((gram_tile_kernel<DT, 128, 128, 2, 2>), grid, dim3(256), 0, st,
                        (const char *)vis, Nv, d * esz, kept, N1, pruned, Mp, invn, best_val,
-                       best_slot, assign, counters);
+                       best_slot, assign);
     return hipGetLastError();
 }
 
 template <int DT>
 static hipError_t gram_dt(int cfg, const void *vis, int B, int Nv, int d, const int32_t *kept,
                           int N1, const int32_t *pruned, int Mp, const float *invn,
-                          float *best_val, int32_t *best_slot, int32_t *assign,
-                          unsigned *counters, hipStream_t st) {
+                          float *best_val, int32_t *best_slot, int32_t *assign, hipStream_t st) {
     switch (cfg) {
-        case TILE_16:
-            return gram_go<DT, 16, 16, 1, 1>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, counters, st);
-        case TILE_32:
-            return gram_go<DT, 32, 32, 2, 2>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, counters, st);
-        case TILE_64:
-            return gram_go<DT, 64, 64, 2, 2>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, counters, st);
-        case TILE_128:
-            return gram_go<DT, 128, 128, 2, 2>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, counters, st);
+        case TILE_16: return gram_stream_go<DT, 16>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
+        case TILE_32: return gram_stream_go<DT, 32>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
+        case TILE_64: return gram_stream_go<DT, 64>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
+        case TILE_128: return gram_tile_go<DT>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
     }
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_gram_assign(int dt, int cfg, const void *vis, int B, int Nv, int d,
-                              const int32_t *kept, int N1, const int32_t *pruned, int Mp,
-                              const float *invn, float *best_val, int32_t *best_slot,
-                              int32_t *assign, unsigned *counters, hipStream_t st) {
+hipError_t launch_gram(int dt, int cfg, const void *vis, int B, int Nv, int d, const int32_t *kept,
+                       int N1, const int32_t *pruned, int Mp, const float *invn, float *best_val,
+                       int32_t *best_slot, int32_t *assign, hipStream_t st) {
     if (dt == kBF16)
-        return gram_dt<kBF16>(cfg, vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, counters, st);
-    return gram_dt<kF32>(cfg, vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, counters, st);
+        return gram_dt<kBF16>(cfg, vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
+    return gram_dt<kF32>(cfg, vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
 }
 
-hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept, int N1,
+hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, int B, int ntn,
+                              int Mp, int Nv, const int32_t *pruned, int32_t *assign,
+                              hipStream_t st) {
+    dim3 grid((Mp + kFinNT - 1) / kFinNT, B);
+    hipLaunchKernelGGL(gram_finish_kernel, grid, dim3(kFinNT), 0, st, best_val, best_slot, ntn, Mp,
+                       Nv, pruned, assign);
+    return hipGetLastError();
+}
+
+hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
                         const int32_t *assign, void *merged, hipStream_t st) {
-    (void)kept;
     dim3 grid(N1, B);
     if (dt == kBF16)
         hipLaunchKernelGGL(merge_kernel<kBF16>, grid, dim3(kMergeNT), 0, st, (const char *)vis, Nv,

@@ -8,11 +8,12 @@
 //
 // score_partial (grid: 16-row blocks x selected heads x B) keeps the 16 query
 // rows of its block in registers as MFMA fragments and streams the head's
-// keys straight from HBM/L2 twice: pass 1 builds each row's running max and
-// exp-sum, pass 2 recomputes the logits, normalises them and sums the 16 rows
-// of every column.  Only the selected heads are ever read and the attention
-// map is never written out.  score_select (one workgroup per sample) adds the
-// per-(head, row-block) column sums in a fixed order and runs the top-N_2.
+// keys from HBM/L2.  When a wave's share of the keys is at most MAXB blocks of
+// 16 the logits stay in registers between the row statistics and the column
+// sums (one pass over K); otherwise the logits are recomputed in a second
+// pass.  Only the selected heads are ever read and the attention map is never
+// written out.  score_select (one workgroup per sample) adds the per-(head,
+// row-block) column sums in a fixed order and runs the top-N_2.
 #include "pv_launch.h"
 #include "pv_device.h"
 
@@ -30,6 +31,19 @@ __device__ __forceinline__ void lse_merge(float &m, float &l, float m2, float l2
 }
 
 template <int DT, int NKS>
+__device__ __forceinline__ f32x4_t qk_block(const uint4 (&qf)[NKS], const char *kb, int col, int N,
+                                            int hd_bytes, int koff) {
+    const char *kr = kb + (size_t)min(col, N - 1) * hd_bytes + koff;
+    uint4 kf[NKS];
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) kf[s] = ld16(kr + s * 64);
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) acc = mma16<DT>(qf[s], kf[s], acc);
+    return acc;
+}
+
+template <int DT, int NKS, int MAXB>
 __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads, int H, int Nt, int N,
     int hd_bytes, int n_heads, float scale_log2e, float *__restrict__ partial) {
@@ -37,7 +51,10 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     __shared__ float row_m[16], row_il[16];
     const int rb = blockIdx.x, hi = blockIdx.y, b = blockIdx.z;
     const int nrb = gridDim.x;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    // uniform wave index: the block guards around the MFMAs become scalar
+    // branches (an MFMA does not honour the execution mask)
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int h = heads.h[b * n_heads + hi];
     const char *qb = q + ((size_t)b * H + h) * Nt * hd_bytes;
     const char *kb = k + ((size_t)b * H + h) * N * hd_bytes;
@@ -58,15 +75,43 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         m[i] = -INFINITY;
         l[i] = 0.f;
     }
-    for (int blk = wave; blk < nblk; blk += 4) {
-        const int col = blk * 16 + (lane & 15);
-        const char *kr = kb + (size_t)min(col, N - 1) * hd_bytes + koff;
-        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    f32x4_t keep[MAXB > 0 ? MAXB : 1];
+    if (MAXB > 0) {
+        // all key fragments of this wave's blocks in flight at once (rows past
+        // the end are clamped to the last key), then the MFMAs
+        uint4 kf[MAXB > 0 ? MAXB : 1][NKS];
 #pragma unroll
-        for (int s = 0; s < NKS; ++s) acc = mma16<DT>(qf[s], ld16(kr + s * 64), acc);
-        if (col < N) {
+        for (int bi = 0; bi < MAXB; ++bi) {
+            const int col = min((wave + 4 * bi) * 16 + (lane & 15), N - 1);
+            const char *kr = kb + (size_t)col * hd_bytes + koff;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) lse_merge(m[i], l[i], acc[i] * scale_log2e, 1.f);
+            for (int s2 = 0; s2 < NKS; ++s2) kf[bi][s2] = ld16(kr + s2 * 64);
+        }
+#pragma unroll
+        for (int bi = 0; bi < MAXB; ++bi) {
+            if (wave + 4 * bi < nblk) {
+                f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int s2 = 0; s2 < NKS; ++s2) acc = mma16<DT>(qf[s2], kf[bi][s2], acc);
+                keep[bi] = acc;
+            }
+        }
+#pragma unroll
+        for (int bi = 0; bi < MAXB; ++bi) {
+            const int blk = wave + 4 * bi;
+            if (blk < nblk && blk * 16 + (lane & 15) < N) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) lse_merge(m[i], l[i], keep[bi][i] * scale_log2e, 1.f);
+            }
+        }
+    } else {
+        for (int blk = wave; blk < nblk; blk += 4) {
+            const int col = blk * 16 + (lane & 15);
+            const f32x4_t acc = qk_block<DT, NKS>(qf, kb, col, N, hd_bytes, koff);
+            if (col < N) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) lse_merge(m[i], l[i], acc[i] * scale_log2e, 1.f);
+            }
         }
     }
     // combine the 16 lanes that hold the same rows, then the 4 waves
@@ -74,8 +119,8 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     for (int off = 1; off < 16; off <<= 1) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            float m2 = __shfl_xor(m[i], off, 64);
-            float l2 = __shfl_xor(l[i], off, 64);
+            const float m2 = __shfl_xor(m[i], off, 64);
+            const float l2 = __shfl_xor(l[i], off, 64);
             lse_merge(m[i], l[i], m2, l2);
         }
     }
@@ -104,50 +149,82 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     }
     float *out = partial + (((size_t)b * n_heads + hi) * nrb + rb) * N;
     // pass 2: normalised probabilities, summed over the 16 rows of each column
-    for (int blk = wave; blk < nblk; blk += 4) {
-        const int col = blk * 16 + (lane & 15);
-        const char *kr = kb + (size_t)min(col, N - 1) * hd_bytes + koff;
-        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < NKS; ++s) acc = mma16<DT>(qf[s], ld16(kr + s * 64), acc);
+    auto emit = [&](const f32x4_t &acc, int col) {
         float cs = 0.f;
 #pragma unroll
         for (int i = 0; i < 4; ++i) cs += exp2f(acc[i] * scale_log2e - rm[i]) * ril[i];
         cs += __shfl_xor(cs, 16, 64);
         cs += __shfl_xor(cs, 32, 64);
         if (lane < 16 && col < N) out[col] = cs;
+    };
+    if (MAXB > 0) {
+#pragma unroll
+        for (int bi = 0; bi < MAXB; ++bi) {
+            const int blk = wave + 4 * bi;
+            if (blk < nblk) emit(keep[bi], blk * 16 + (lane & 15));
+        }
+    } else {
+        for (int blk = wave; blk < nblk; blk += 4) {
+            const int col = blk * 16 + (lane & 15);
+            emit(qk_block<DT, NKS>(qf, kb, col, N, hd_bytes, koff), col);
+        }
     }
 }
 
 constexpr int kSelectNT = 256;
+constexpr int kSelectStage = 8192;
 
 __global__ __launch_bounds__(kSelectNT) void score_select_kernel(const float *__restrict__ partial,
                                                                  int nparts, int N, float inv_norm,
                                                                  float *__restrict__ v, int budget,
                                                                  int32_t *__restrict__ kept) {
+    extern __shared__ uint32_t keys[];  // [N] when staged
     __shared__ TopkSmem sm;
     const int b = blockIdx.x, tid = threadIdx.x;
     const float *pb = partial + (size_t)b * nparts * N;
     float *vb = v + (size_t)b * N;
+    const bool stage = N <= kSelectStage;
     for (int j = tid; j < N; j += kSelectNT) {
         float s = 0.f;
+#pragma unroll 4
         for (int t = 0; t < nparts; ++t) s += pb[(size_t)t * N + j];
         vb[j] = s * inv_norm;
     }
-    __threadfence_block();
-    __syncthreads();
-    block_topk<kSelectNT>(vb, N, budget, kept + (size_t)b * budget, nullptr, nullptr, sm);
+    // block_topk stages v[j] in LDS with the same thread-to-j mapping, so
+    // every thread reads back only what it wrote itself
+    block_topk<kSelectNT>(vb, N, budget, kept + (size_t)b * budget, nullptr, nullptr, sm,
+                          stage ? keys : nullptr);
 }
 
-template <int DT, int NKS>
+template <int DT, int NKS, int MAXB>
 static hipError_t score_go(const void *q, const void *k, const HeadArgs &heads, int B, int H,
                            int Nt, int N, int hd_bytes, int n_heads, float scale_log2e,
                            float *partial, hipStream_t st) {
     dim3 grid((Nt + 15) / 16, n_heads, B);
-    hipLaunchKernelGGL((score_partial_kernel<DT, NKS>), grid, dim3(kScoreNT), 0, st,
+    hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXB>), grid, dim3(kScoreNT), 0, st,
                        (const char *)q, (const char *)k, heads, H, Nt, N, hd_bytes, n_heads,
                        scale_log2e, partial);
     return hipGetLastError();
+}
+
+// Key blocks per wave held in registers: the smallest of 1, 2, 4, 8 that
+// covers the wave's share, while the fragments stay within 32 x 16 bytes per
+// lane; otherwise the two-pass form (MAXB = 0).
+template <int DT, int NKS>
+static hipError_t score_nks(const void *q, const void *k, const HeadArgs &heads, int B, int H,
+                            int Nt, int N, int hd_bytes, int n_heads, float sl2e, float *partial,
+                            hipStream_t st) {
+    const int bpw = ((N + 15) / 16 + 3) / 4;
+#define PV_MAXB_CASE(mb)                                                                           \
+    if (bpw <= mb && mb * NKS <= 32)                                                               \
+        return score_go<DT, NKS, (mb * NKS <= 32 ? mb : 0)>(q, k, heads, B, H, Nt, N, hd_bytes,    \
+                                                            n_heads, sl2e, partial, st);
+    PV_MAXB_CASE(1)
+    PV_MAXB_CASE(2)
+    PV_MAXB_CASE(4)
+    PV_MAXB_CASE(8)
+#undef PV_MAXB_CASE
+    return score_go<DT, NKS, 0>(q, k, heads, B, H, Nt, N, hd_bytes, n_heads, sl2e, partial, st);
 }
 
 template <int DT>
@@ -156,7 +233,7 @@ static hipError_t score_dt(int nks, const void *q, const void *k, const HeadArgs
                            float *partial, hipStream_t st) {
 #define PV_NKS_CASE(n) \
     case n:            \
-        return score_go<DT, n>(q, k, heads, B, H, Nt, N, hd_bytes, n_heads, sl2e, partial, st);
+        return score_nks<DT, n>(q, k, heads, B, H, Nt, N, hd_bytes, n_heads, sl2e, partial, st);
     switch (nks) {
         PV_NKS_CASE(1)
         PV_NKS_CASE(2)
@@ -188,7 +265,8 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const Head
 
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,
                                float *v, int budget, int32_t *kept, hipStream_t st) {
-    hipLaunchKernelGGL(score_select_kernel, dim3(B), dim3(kSelectNT), 0, st, partial, nparts, N,
+    const size_t lds = (N <= kSelectStage) ? (size_t)N * sizeof(uint32_t) : 0;
+    hipLaunchKernelGGL(score_select_kernel, dim3(B), dim3(kSelectNT), lds, st, partial, nparts, N,
                        inv_norm, v, budget, kept);
     return hipGetLastError();
 }

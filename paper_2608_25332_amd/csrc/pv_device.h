@@ -115,6 +115,16 @@ __device__ __forceinline__ int block_excl_scan(int x, int *wsum, int *total) {
     return before + inc - x;
 }
 
+// Workgroups are dispatched to the 8 XCDs of the chip round-robin by linear
+// id.  Map linear id L to a tile index so that every XCD receives one
+// contiguous run of tiles: tiles that share operand rows then share that
+// XCD's L2 instead of each fetching the rows from memory.
+__device__ __forceinline__ int xcd_tile(int L, int total) {
+    const int x = L & 7, q = L >> 3;
+    const int base = total >> 3, rem = total & 7;
+    return x * base + (x < rem ? x : rem) + q;
+}
+
 struct TopkSmem {
     int hist[256];
     int wsum[16];
@@ -129,33 +139,39 @@ struct TopkSmem {
 //   slot_of[j]       position of j in kept, or -1 (if slot_of != nullptr).
 // Radix select over the order-preserving keys (four 8-bit digits, most
 // significant first) finds the k-th largest key T; the keys above T and the
-// first (k - #above) keys equal to T in index order are kept.  Scores are read
-// from global memory (they stay in cache) so n is not bounded by LDS.
+// first (k - #above) keys equal to T in index order are kept.  When `lds_keys`
+// is given (room for n keys) the keys are staged there once; otherwise every
+// pass re-reads the scores from global memory (cache resident).
 template <int NT>
 __device__ void block_topk(const float *score, int n, int k, int32_t *kept, int32_t *rest,
-                           int32_t *slot_of, TopkSmem &sm) {
+                           int32_t *slot_of, TopkSmem &sm, uint32_t *lds_keys) {
     const int tid = threadIdx.x;
+    if (lds_keys) {
+        for (int j = tid; j < n; j += NT) lds_keys[j] = order_key(score[j]);
+        __syncthreads();
+    }
+    auto key_of = [&](int j) -> uint32_t { return lds_keys ? lds_keys[j] : order_key(score[j]); };
     uint32_t prefix = 0u, mask = 0u;
     int kr = k;  // rank still to be found inside the current prefix group
     for (int shift = 24; shift >= 0; shift -= 8) {
         for (int e = tid; e < 256; e += NT) sm.hist[e] = 0;
         __syncthreads();
         for (int j = tid; j < n; j += NT) {
-            uint32_t key = order_key(score[j]);
+            const uint32_t key = key_of(j);
             if ((key & mask) == prefix) atomicAdd(&sm.hist[(key >> shift) & 255u], 1);
         }
         __syncthreads();
         if (tid < 64) {
-            // lane owns bins 4*lane .. 4*lane+3; count of keys in higher bins
-            int h0 = sm.hist[4 * tid], h1 = sm.hist[4 * tid + 1];
-            int h2 = sm.hist[4 * tid + 2], h3 = sm.hist[4 * tid + 3];
-            int mine = h0 + h1 + h2 + h3;
-            // suffix sum over lanes: reverse lane order, inclusive scan
-            int rev = __shfl(mine, 63 - tid, 64);
-            int inc = wave_incl_scan(rev);
-            int suffix_incl = __shfl(inc, 63 - tid, 64);  // sum over lanes >= tid
-            int above = suffix_incl - mine;                // keys in bins > 4*tid+3
-            int ge3 = above + h3, ge2 = ge3 + h2, ge1 = ge2 + h1, ge0 = ge1 + h0;
+            // lane owns bins 4*lane .. 4*lane+3
+            const int h0 = sm.hist[4 * tid], h1 = sm.hist[4 * tid + 1];
+            const int h2 = sm.hist[4 * tid + 2], h3 = sm.hist[4 * tid + 3];
+            const int mine = h0 + h1 + h2 + h3;
+            // suffix sum over lanes: reverse the lane order, inclusive scan
+            const int rev = __shfl(mine, 63 - tid, 64);
+            const int inc = wave_incl_scan(rev);
+            const int suffix_incl = __shfl(inc, 63 - tid, 64);  // sum over lanes >= tid
+            const int above = suffix_incl - mine;                // keys in bins > 4*tid+3
+            const int ge3 = above + h3, ge2 = ge3 + h2, ge1 = ge2 + h1, ge0 = ge1 + h0;
             int dsel = -1, gt = 0;
             if (above < kr && kr <= ge3) { dsel = 3; gt = above; }
             else if (ge3 < kr && kr <= ge2) { dsel = 2; gt = ge3; }
@@ -176,13 +192,13 @@ __device__ void block_topk(const float *score, int n, int k, int32_t *kept, int3
     int carry_eq = 0, carry_keep = 0;
     for (int base = 0; base < n; base += NT) {
         const int j = base + tid;
-        uint32_t key = (j < n) ? order_key(score[j]) : 0u;
-        int is_gt = (j < n) && key > T;
-        int is_eq = (j < n) && key == T;
+        const uint32_t key = (j < n) ? key_of(j) : 0u;
+        const int is_gt = (j < n) && key > T;
+        const int is_eq = (j < n) && key == T;
         int tot_eq, tot_keep;
-        int eq_before = block_excl_scan<NT>(is_eq, sm.wsum, &tot_eq) + carry_eq;
-        int keep = is_gt || (is_eq && eq_before < kr);
-        int pos = block_excl_scan<NT>(keep, sm.wsum, &tot_keep) + carry_keep;
+        const int eq_before = block_excl_scan<NT>(is_eq, sm.wsum, &tot_eq) + carry_eq;
+        const int keep = is_gt || (is_eq && eq_before < kr);
+        const int pos = block_excl_scan<NT>(keep, sm.wsum, &tot_keep) + carry_keep;
         if (j < n) {
             if (keep) {
                 kept[pos] = j;

@@ -21,16 +21,18 @@ struct HeadArgs {
 
 // ---- pruning before the LLM (Sec. 4.3)
 hipError_t launch_cos_tile(int dt, int cfg, const void *vis, const void *anchors, int B, int Nv,
-                           int Nt, int d, float *M, float *invn, float *rowsum, unsigned *counters,
-                           int n_counters, hipStream_t st);
-hipError_t launch_center_select(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
-                                float *p, int budget, int32_t *kept, int32_t *pruned,
-                                int32_t *slot_of, unsigned *counters, hipStream_t st);
-hipError_t launch_gram_assign(int dt, int cfg, const void *vis, int B, int Nv, int d,
-                              const int32_t *kept, int N1, const int32_t *pruned, int Mp,
-                              const float *invn, float *best_val, int32_t *best_slot,
-                              int32_t *assign, unsigned *counters, hipStream_t st);
-hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept, int N1,
+                           int Nt, int d, float *M, float *invn, float *rowsum, hipStream_t st);
+hipError_t launch_center(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
+                         float *p, hipStream_t st);
+hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kept, int32_t *pruned,
+                         int32_t *slot_of, hipStream_t st);
+hipError_t launch_gram(int dt, int cfg, const void *vis, int B, int Nv, int d, const int32_t *kept,
+                       int N1, const int32_t *pruned, int Mp, const float *invn, float *best_val,
+                       int32_t *best_slot, int32_t *assign, hipStream_t st);
+hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, int B, int ntn,
+                              int Mp, int Nv, const int32_t *pruned, int32_t *assign,
+                              hipStream_t st);
+hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
                         const int32_t *assign, void *merged, hipStream_t st);
 
 // ---- head-aware pruning (Sec. 4.4)
@@ -41,8 +43,20 @@ hipError_t launch_score_select(const float *partial, int B, int nparts, int N, f
                                float *v, int budget, int32_t *kept, hipStream_t st);
 
 // ---- compaction (Sec. 4.1)
-hipError_t launch_gather(const void *src, void *dst, const int32_t *idx, int B, int n_src, int k,
-                         int groups, int64_t row_bytes, int64_t sb, int64_t sg, int64_t sr,
-                         int64_t db, int64_t dg, int64_t dr, hipStream_t st);
+constexpr int kMaxGather = 4;
+constexpr int kGatherIT = 4;  // 16-byte pieces per thread
+struct GatherDesc {
+    const char *src;
+    char *dst;
+    int n_src, groups, cpr;  // cpr: 16-byte pieces per row
+    int bpp;                 // workgroups per plane (sample x head group)
+    int64_t sb, sg, sr, db, dg, dr;
+};
+struct GatherArgs {
+    GatherDesc d[kMaxGather];
+    int bstart[kMaxGather + 1];  // first workgroup of each tensor; bstart[n] = total
+    int n;
+};
+hipError_t launch_gather(const GatherArgs &ga, const int32_t *idx, int B, int k, hipStream_t st);
 
 }  // namespace pv

@@ -34,6 +34,16 @@ _i64 = ctypes.c_int64
 _sz = ctypes.c_size_t
 
 
+PV_MAX_GATHER = 4
+
+
+class GatherDesc(ctypes.Structure):
+    """pv_gather_desc of include/provip.h."""
+    _fields_ = [("src", _vp), ("dst", _vp), ("n_src", _i), ("groups", _i), ("row_bytes", _i64),
+                ("src_batch_stride", _i64), ("src_group_stride", _i64), ("src_row_stride", _i64),
+                ("dst_batch_stride", _i64), ("dst_group_stride", _i64), ("dst_row_stride", _i64)]
+
+
 class ProvipError(RuntimeError):
     def __init__(self, fn: str, status: int, lib=None):
         msg = lib.pv_status_string(status).decode() if lib is not None else ""
@@ -58,7 +68,8 @@ def load(path: str = LIB_PATH):
     ded = [_vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _vp, _sz, _vp]
     lib.pv_prune_dedup.argtypes = ded
     lib.pv_prune_dedup.restype = _i
-    lib.pv_prune_dedup_timed.argtypes = ded + [ctypes.POINTER(_vp), _i, ctypes.POINTER(_i)]
+    names_t = ctypes.POINTER(ctypes.c_char_p)
+    lib.pv_prune_dedup_timed.argtypes = ded + [ctypes.POINTER(_vp), _i, ctypes.POINTER(_i), names_t]
     lib.pv_prune_dedup_timed.restype = _i
     lib.pv_head_aware_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i, _i]
     lib.pv_head_aware_workspace_bytes.restype = _sz
@@ -66,11 +77,13 @@ def load(path: str = LIB_PATH):
           _vp, _sz, _vp]
     lib.pv_prune_head_aware.argtypes = ha
     lib.pv_prune_head_aware.restype = _i
-    lib.pv_prune_head_aware_timed.argtypes = ha + [ctypes.POINTER(_vp), _i, ctypes.POINTER(_i)]
+    lib.pv_prune_head_aware_timed.argtypes = ha + [ctypes.POINTER(_vp), _i, ctypes.POINTER(_i), names_t]
     lib.pv_prune_head_aware_timed.restype = _i
     lib.pv_prune_gather.argtypes = [_vp, _vp, _vp, _i, _i, _i, _i, _i64, _i64, _i64, _i64, _i64,
                                     _i64, _i64, _vp]
     lib.pv_prune_gather.restype = _i
+    lib.pv_prune_gather_batch.argtypes = [ctypes.POINTER(GatherDesc), _i, _vp, _i, _i, _vp]
+    lib.pv_prune_gather_batch.restype = _i
     _lib = lib
     return lib
 
@@ -105,10 +118,17 @@ def _contig(t: torch.Tensor, name: str) -> torch.Tensor:
 
 
 def _events_array(events: Optional[Sequence]):
+    """(event handle array, count, kernel-name array) for the *_timed calls."""
     if not events:
-        return None, 0
+        return None, 0, None
     arr = (_vp * len(events))(*[e.cuda_event if hasattr(e, "cuda_event") else e for e in events])
-    return arr, len(events)
+    return arr, len(events), (ctypes.c_char_p * len(events))()
+
+
+def _names(names_arr, n: int):
+    if names_arr is None:
+        return []
+    return [names_arr[i].decode() for i in range(n) if names_arr[i] is not None]
 
 
 # ----------------------------------------------------------------------------
@@ -148,15 +168,16 @@ def pv_prune_dedup(vis: torch.Tensor, anchors: torch.Tensor, budget: int, *,
     nbytes = lib.pv_dedup_workspace_bytes(B, Nv, Nt, d, budget, code)
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
-    ev, nev = _events_array(events)
+    ev, nev, nm = _events_array(events)
     nk = _i(0)
     rc = lib.pv_prune_dedup_timed(vis.data_ptr(), anchors.data_ptr(), B, Nv, Nt, d, code,
                                   int(budget), kept.data_ptr(), _ptr(score), _ptr(assign),
                                   _ptr(merged), workspace.data_ptr(), workspace.numel(),
-                                  _stream(dev), ev, nev, ctypes.byref(nk))
+                                  _stream(dev), ev, nev, ctypes.byref(nk), nm)
     _check("pv_prune_dedup", rc, lib)
     return {"kept": kept, "score": score, "assign": assign, "merged": merged,
-            "n_kernels": nk.value, "workspace": workspace}
+            "n_kernels": nk.value, "kernel_names": _names(nm, min(nk.value, max(nev - 1, 0))),
+            "workspace": workspace}
 
 
 def pv_head_aware_workspace_bytes(B: int, H: int, Nt: int, N: int, hd: int, n_heads: int,
@@ -194,20 +215,34 @@ def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
     nbytes = lib.pv_head_aware_workspace_bytes(B, H, Nt, N, hd, n_heads, budget, code)
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
-    ev, nev = _events_array(events)
+    ev, nev, nm = _events_array(events)
     nk = _i(0)
     rc = lib.pv_prune_head_aware_timed(q.data_ptr(), k.data_ptr(),
                                        hs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n_heads,
                                        B, H, Nt, N, hd, code, int(budget), kept.data_ptr(),
                                        _ptr(score), workspace.data_ptr(), workspace.numel(),
-                                       _stream(dev), ev, nev, ctypes.byref(nk))
+                                       _stream(dev), ev, nev, ctypes.byref(nk), nm)
     _check("pv_prune_head_aware", rc, lib)
-    return {"kept": kept, "score": score, "n_kernels": nk.value, "workspace": workspace}
+    return {"kept": kept, "score": score, "n_kernels": nk.value,
+            "kernel_names": _names(nm, min(nk.value, max(nev - 1, 0))), "workspace": workspace}
+
+
+def _gather_geometry(src: torch.Tensor, B: int, k: int):
+    """(groups, n_src, row_bytes, out_shape) of a contiguous [B, N, ...] or
+    [B, G, N, hd] tensor (4-D tensors are K/V caches with G head groups)."""
+    if src.dim() == 4:
+        _, G, n, hd = src.shape
+        return G, n, hd * src.element_size(), (B, G, k, hd)
+    G, n = 1, src.shape[1]
+    per_row = 1
+    for x in src.shape[2:]:
+        per_row *= int(x)
+    return G, n, per_row * src.element_size(), (B, k) + tuple(src.shape[2:])
 
 
 def pv_prune_gather(src: torch.Tensor, idx: torch.Tensor, *, out: Optional[torch.Tensor] = None):
     """Order-preserving compaction of rows.  src [B, N, ...] (groups = 1) or
-    [B, G, N, hd] with grouped=4-D (K/V caches); idx [B, k] int32 device.
+    [B, G, N, hd] (K/V caches, G head groups); idx [B, k] int32 device.
     Returns dst [B, k, ...] / [B, G, k, hd]."""
     lib = load()
     _contig(src, "src")
@@ -215,15 +250,7 @@ def pv_prune_gather(src: torch.Tensor, idx: torch.Tensor, *, out: Optional[torch
     if idx.dtype != torch.int32:
         raise TypeError("idx must be int32")
     B, k = idx.shape
-    if src.dim() == 4:
-        _, G, n, hd = src.shape
-        row_bytes = hd * src.element_size()
-        shape = (B, G, k, hd)
-    else:
-        G, n = 1, src.shape[1]
-        row_bytes = int(torch.tensor(src.shape[2:]).prod().item()) * src.element_size() \
-            if src.dim() > 2 else src.element_size()
-        shape = (B, k) + tuple(src.shape[2:])
+    G, n, row_bytes, shape = _gather_geometry(src, B, k)
     if out is None:
         out = torch.empty(shape, dtype=src.dtype, device=src.device)
     sb, sg, sr = n * G * row_bytes, n * row_bytes, row_bytes
@@ -232,3 +259,29 @@ def pv_prune_gather(src: torch.Tensor, idx: torch.Tensor, *, out: Optional[torch
                              row_bytes, sb, sg, sr, db, dg, dr, _stream(src.device))
     _check("pv_prune_gather", rc, lib)
     return out
+
+
+def pv_prune_gather_batch(srcs: Sequence[torch.Tensor], idx: torch.Tensor, *,
+                          outs: Optional[Sequence[torch.Tensor]] = None):
+    """pv_prune_gather of up to PV_MAX_GATHER tensors sharing idx, in one launch."""
+    lib = load()
+    _contig(idx, "idx")
+    if idx.dtype != torch.int32:
+        raise TypeError("idx must be int32")
+    B, k = idx.shape
+    if not 1 <= len(srcs) <= PV_MAX_GATHER:
+        raise ValueError(f"1..{PV_MAX_GATHER} tensors per batch")
+    descs = (GatherDesc * len(srcs))()
+    res = []
+    for t, src in enumerate(srcs):
+        _contig(src, "src")
+        G, n, row_bytes, shape = _gather_geometry(src, B, k)
+        out = outs[t] if outs is not None else torch.empty(shape, dtype=src.dtype, device=src.device)
+        d = descs[t]
+        d.src, d.dst, d.n_src, d.groups, d.row_bytes = src.data_ptr(), out.data_ptr(), n, G, row_bytes
+        d.src_batch_stride, d.src_group_stride, d.src_row_stride = n * G * row_bytes, n * row_bytes, row_bytes
+        d.dst_batch_stride, d.dst_group_stride, d.dst_row_stride = k * G * row_bytes, k * row_bytes, row_bytes
+        res.append(out)
+    rc = lib.pv_prune_gather_batch(descs, len(srcs), idx.data_ptr(), B, k, _stream(idx.device))
+    _check("pv_prune_gather_batch", rc, lib)
+    return res

@@ -131,3 +131,24 @@ def test_gather_validation(lib):
     assert call(rb=8) == -2
     assert call(rb=40) == -8
     assert call(dst=FAKE + 2) == -8
+
+
+def test_gather_batch_validation(lib):
+    from paper_2608_25332_amd import provip
+    d = (provip.GatherDesc * 2)()
+    for t in range(2):
+        d[t].src, d[t].dst, d[t].n_src, d[t].groups, d[t].row_bytes = FAKE, FAKE, 8, 1, 256
+        d[t].src_batch_stride = d[t].src_group_stride = 8 * 256
+        d[t].src_row_stride = d[t].dst_row_stride = 256
+        d[t].dst_batch_stride = d[t].dst_group_stride = 4 * 256
+    g = lib.pv_prune_gather_batch
+    assert g(None, 2, FAKE, 1, 4, None) == -1
+    assert g(d, 0, FAKE, 1, 4, None) == -2
+    assert g(d, 5, FAKE, 1, 4, None) == -2
+    assert g(d, 2, FAKE, 1, 0, None) == -2
+    assert g(d, 2, FAKE + 4, 1, 4, None) == -8
+    d[1].row_bytes = 40
+    assert g(d, 2, FAKE, 1, 4, None) == -8
+    d[1].row_bytes = 256
+    d[1].dst = None
+    assert g(d, 2, FAKE, 1, 4, None) == -1

@@ -129,6 +129,12 @@ DEDUP_EDGE = [
     (1, 300, 37, 256, 129, "bf16"),  # ragged everywhere
     (2, 1000, 130, 320, 333, "bf16"),
     (1, 5, 2, 64, 4, "f32"),
+    # k ranges that are not a multiple of the unroll depth (wave slices with
+    # 0 or 1 windows): regression cases for masked-off MFMA blocks
+    (1, 40, 4, 128, 1, "bf16"),
+    (1, 40, 4, 192, 1, "bf16"),
+    (1, 40, 4, 256, 3, "bf16"),
+    (2, 40, 4, 320, 7, "f32"),
 ]
 
 
@@ -141,6 +147,9 @@ def test_dedup_edges(B, Nv, Nt, d, budget, dt):
     if dt == "bf16":
         vis, anc = W.bf16_round(vis), W.bf16_round(anc)
     g = run_dedup(vis, anc, dt, budget)
+    g2 = run_dedup(vis, anc, dt, budget)
+    for key in ("kept", "score", "assign", "merged"):
+        assert np.array_equal(g[key], g2[key]), f"two calls differ in {key}"
     for b in range(B):
         p = oracle.maxpool(oracle.center(oracle.cosine(anc[b], vis[b])))
         assert rel_err(g["score"][b], p) <= TOL[dt]
@@ -274,6 +283,23 @@ def test_gather_bit_exact():
     assert np.array_equal(ok.view(torch.int16).cpu().numpy(), oracle.gather(kb, idx_np))
 
 
+def test_gather_batch_bit_exact():
+    """Hidden, K and V (different row sizes) in one launch."""
+    from paper_2608_25332_amd import provip
+    rng = np.random.default_rng(4)
+    B, H, N, hd, D, k = 3, 4, 77, 64, 512, 31
+    hid = torch.from_numpy(rng.standard_normal((B, N, D)).astype(np.float32)).to("cuda:0")
+    kk = torch.from_numpy(rng.standard_normal((B, H, N, hd)).astype(np.float32)).to("cuda:0").bfloat16()
+    vv = torch.from_numpy(rng.standard_normal((B, H, N, hd)).astype(np.float32)).to("cuda:0").bfloat16()
+    idx_np = np.stack([np.sort(rng.choice(N, k, replace=False)) for _ in range(B)]).astype(np.int32)
+    idx = torch.from_numpy(idx_np).to("cuda:0")
+    oh, ok, ov = provip.pv_prune_gather_batch([hid, kk, vv], idx)
+    torch.cuda.synchronize()
+    assert np.array_equal(oh.cpu().numpy(), oracle.gather(hid.cpu().numpy(), idx_np))
+    assert np.array_equal(ok.view(torch.int16).cpu().numpy(), oracle.gather(kk.view(torch.int16).cpu().numpy(), idx_np))
+    assert np.array_equal(ov.view(torch.int16).cpu().numpy(), oracle.gather(vv.view(torch.int16).cpu().numpy(), idx_np))
+
+
 def test_gather_out_of_range_rows_are_zero():
     from paper_2608_25332_amd import provip
     src = torch.arange(4 * 8, dtype=torch.float32, device="cuda:0").reshape(1, 8, 4) + 1
@@ -296,12 +322,9 @@ def test_pipeline_against_oracle(wid):
     vis, anc = to_dev(w.vis, dt), to_dev(w.anchors, dt)
     q, kf, vf = to_dev(w.q, dt), to_dev(w.k_full, dt), to_dev(w.v_full, dt)
     r = provip.pv_prune_dedup(vis, anc, w.N1)
-    k1 = provip.pv_prune_gather(kf, r["kept"])
-    v1 = provip.pv_prune_gather(vf, r["kept"])
+    k1, v1 = provip.pv_prune_gather_batch([kf, vf], r["kept"])
     h = provip.pv_prune_head_aware(q, k1, w.heads, w.N2)
-    hid2 = provip.pv_prune_gather(r["merged"], h["kept"])
-    k2 = provip.pv_prune_gather(k1, h["kept"])
-    v2 = provip.pv_prune_gather(v1, h["kept"])
+    hid2, k2, v2 = provip.pv_prune_gather_batch([r["merged"], k1, v1], h["kept"])
     torch.cuda.synchronize()
     ref = oracle.dedup(w.anchors, w.vis, w.N1)
     kept1 = to_host(r["kept"])
