@@ -132,6 +132,22 @@ int pv_prune_head_aware(const void *q, const void *k, const int32_t *heads_host,
                         void *stream);
 
 /* -------------------------------------------------------------------------
+ * The retention rule of both stages on its own (Sec. 4.3: keep the N_1
+ * tokens with the highest p; Sec. 4.4: keep the N_2 tokens with the highest
+ * v), for callers that compute their own scores.  Per sample b: the k
+ * highest of scores[b][0..n) (ties: lower index), written ascending; the
+ * kernel is the one both pruning calls above run.
+ *
+ * scores   [B][n]     float32     finite scores
+ * kept     [B][k]     int32 out   required
+ * rest     [B][n-k]   int32 out   the other indices, ascending; may be NULL
+ * slot_of  [B][n]     int32 out   position of j in kept, or -1; may be NULL
+ * Sizes: 1 <= B <= 65535, 1 <= n <= PV_MAX_TOKENS, 1 <= k <= n.
+ * ---------------------------------------------------------------------- */
+int pv_select_topk(const float *scores, int B, int n, int k, int32_t *kept, int32_t *rest,
+                   int32_t *slot_of, void *stream);
+
+/* -------------------------------------------------------------------------
  * Order-preserving row compaction (Sec. 4.1: pruned tokens are excluded from
  * all later computation):
  *   dst + b*dst_batch_stride + g*dst_group_stride + r*dst_row_stride

@@ -56,51 +56,59 @@ long long n_tiles(int rows_m, int rows_n, int B, int t) {
     return (long long)((rows_m + t - 1) / t) * ((rows_n + t - 1) / t) * B;
 }
 
-// Streaming tiles: the largest square tile whose grid still gives about one
-// workgroup per CU (256 CUs); the smallest tile otherwise.
-int pick_stream_tile(int rows_m, int rows_n, int B) {
-    for (int cfg = pv::TILE_64; cfg > pv::TILE_16; --cfg)
-        if (n_tiles(rows_m, rows_n, B, pv::tile_size(cfg)) >= 240) return cfg;
-    return pv::TILE_16;
-}
-
-// The Gram switches to LDS-staged 128x128 tiles once those alone fill the
-// chip: it is then compute-heavy enough for MFMA throughput to matter.
-int pick_gram_tile(int Mp, int N1, int B) {
-    if (n_tiles(Mp, N1, B, 128) >= 240) return pv::TILE_128;
-    return pick_stream_tile(Mp, N1, B);
+// k slices of a split-k product: about one workgroup per CU (256 CUs), at
+// least two 128-byte chunks in every slice.
+int pick_slices(long long tiles, int nchunks) {
+    long long ks = (250 + tiles - 1) / tiles;
+    const long long max_ks = nchunks / 2 > 1 ? nchunks / 2 : 1;
+    if (ks > max_ks) ks = max_ks;
+    if (ks < 1) ks = 1;
+    return (int)ks;
 }
 
 struct DedupPlan {
-    int cos_cfg, njt;
-    int gram_cfg, ntm, ntn, Mp;
+    int nch;                       // 128-byte k chunks per row
+    int ks_cos, njt;               // cosine: k slices, token tiles of the row sums
+    int Mp;
+    bool gram_big;                 // LDS-staged 128x128 full-k tiles
+    int ks_gram, ntn;              // split-k slices (small) / column tiles (big)
     // workspace
-    float *M, *invn, *rowsum, *p;
-    int32_t *pruned, *assign;
-    float *best_val;
-    int32_t *best_slot;
+    float *cpart, *ssv, *ssa, *M, *rowsum, *invn, *p, *gpart, *best_val;
+    int32_t *pruned, *assign, *best_slot;
     size_t bytes;
 };
 
-DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int budget, bool want_p, bool want_assign) {
+DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget, bool want_p,
+                     bool want_assign) {
     DedupPlan P;
-    P.cos_cfg = pick_stream_tile(Nv, Nt, B);
-    const int t1 = pv::tile_size(P.cos_cfg);
-    P.njt = (Nv + t1 - 1) / t1;
+    P.nch = d * esz / 128;
+    const int T = pv::kSplitTile;
+    P.ks_cos = pick_slices(n_tiles(Nv, Nt, B, T), P.nch);
+    P.njt = pv::cos_row_tiles(Nv);
     P.Mp = Nv - budget;
-    P.gram_cfg = pick_gram_tile(P.Mp > 0 ? P.Mp : 1, budget, B);
-    const int t4 = pv::tile_size(P.gram_cfg);
-    P.ntm = (P.Mp + t4 - 1) / t4;
-    P.ntn = (budget + t4 - 1) / t4;
+    const int Mp1 = P.Mp > 0 ? P.Mp : 1;
+    P.gram_big = n_tiles(Mp1, budget, B, 128) >= 240;
+    P.ks_gram = P.gram_big ? 1 : pick_slices(n_tiles(Mp1, budget, B, T), P.nch);
+    P.ntn = P.gram_big ? (budget + 127) / 128 : 1;
     Carve c(ws);
+    P.cpart = c.take<float>((size_t)P.ks_cos * B * Nt * Nv);
+    P.ssv = c.take<float>((size_t)P.ks_cos * B * Nv);
+    P.ssa = c.take<float>((size_t)P.ks_cos * B * Nt);
     P.M = c.take<float>((size_t)B * Nt * Nv);
-    P.invn = c.take<float>((size_t)B * Nv);
     P.rowsum = c.take<float>((size_t)B * P.njt * Nt);
+    P.invn = c.take<float>((size_t)B * Nv);
     P.p = want_p ? c.take<float>((size_t)B * Nv) : nullptr;
-    P.pruned = c.take<int32_t>((size_t)B * (P.Mp > 0 ? P.Mp : 1));
+    P.pruned = c.take<int32_t>((size_t)B * Mp1);
     P.assign = want_assign ? c.take<int32_t>((size_t)B * Nv) : nullptr;
-    P.best_val = c.take<float>((size_t)B * P.ntn * (P.Mp > 0 ? P.Mp : 1));
-    P.best_slot = c.take<int32_t>((size_t)B * P.ntn * (P.Mp > 0 ? P.Mp : 1));
+    if (P.gram_big) {
+        P.gpart = nullptr;
+        P.best_val = c.take<float>((size_t)B * P.ntn * Mp1);
+        P.best_slot = c.take<int32_t>((size_t)B * P.ntn * Mp1);
+    } else {
+        P.gpart = c.take<float>((size_t)P.ks_gram * B * Mp1 * budget);
+        P.best_val = nullptr;
+        P.best_slot = nullptr;
+    }
     P.bytes = c.off + kAlign;
     return P;
 }
@@ -123,7 +131,9 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     int rc = check_dedup(vis, anchors, B, Nv, Nt, d, dtype, budget, kept);
     if (rc != PV_OK) return rc;
     const bool need_assign = assign != nullptr || merged != nullptr;
-    DedupPlan P0 = plan_dedup(nullptr, B, Nv, Nt, budget, score == nullptr, need_assign && !assign);
+    const int esz = (dtype == PV_BF16) ? 2 : 4;
+    DedupPlan P0 = plan_dedup(nullptr, B, Nv, Nt, d, esz, budget, score == nullptr,
+                              need_assign && !assign);
     if (!workspace) return PV_ERR_WORKSPACE;
     if (ws_bytes < P0.bytes) return PV_ERR_WORKSPACE;
     for (const void *p : {vis, anchors, (const void *)kept, (const void *)score,
@@ -131,7 +141,8 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
         if (p && !aligned16(p)) return PV_ERR_ALIGN;
     // carve from a 256-aligned start
     char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
-    DedupPlan P = plan_dedup(wsa, B, Nv, Nt, budget, score == nullptr, need_assign && !assign);
+    DedupPlan P = plan_dedup(wsa, B, Nv, Nt, d, esz, budget, score == nullptr,
+                             need_assign && !assign);
     float *p = score ? score : P.p;
     int32_t *asg = assign ? assign : P.assign;
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
@@ -141,8 +152,13 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
         ++tr.launched;
         return err == hipSuccess;
     };
-    tr.before("cos_stream");
-    if (!step(pv::launch_cos_tile(dt, P.cos_cfg, vis, anchors, B, Nv, Nt, d, P.M, P.invn, P.rowsum, st)))
+    tr.before("cos_partial");
+    if (!step(pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart, P.ssv,
+                                     P.ssa, st)))
+        return PV_ERR_HIP;
+    tr.before("cos_reduce");
+    if (!step(pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M, P.rowsum,
+                                    P.invn, st)))
         return PV_ERR_HIP;
     tr.before("center");
     if (!step(pv::launch_center(P.M, P.rowsum, P.njt, B, Nt, Nv, p, st))) return PV_ERR_HIP;
@@ -150,14 +166,25 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     if (!step(pv::launch_select(p, B, Nv, budget, kept, P.pruned, need_assign ? asg : nullptr, st)))
         return PV_ERR_HIP;
     if (need_assign && P.Mp > 0) {
-        tr.before(P.gram_cfg == pv::TILE_128 ? "gram_tile" : "gram_stream");
-        if (!step(pv::launch_gram(dt, P.gram_cfg, vis, B, Nv, d, kept, budget, P.pruned, P.Mp,
-                                  P.invn, P.best_val, P.best_slot, asg, st)))
-            return PV_ERR_HIP;
-        if (P.ntn > 1) {
-            tr.before("gram_finish");
-            if (!step(pv::launch_gram_finish(P.best_val, P.best_slot, B, P.ntn, P.Mp, Nv, P.pruned,
-                                             asg, st)))
+        if (P.gram_big) {
+            tr.before("gram_tile");
+            if (!step(pv::launch_gram_tile(dt, vis, B, Nv, d, kept, budget, P.pruned, P.Mp, P.invn,
+                                           P.best_val, P.best_slot, asg, st)))
+                return PV_ERR_HIP;
+            if (P.ntn > 1) {
+                tr.before("gram_finish");
+                if (!step(pv::launch_gram_finish(P.best_val, P.best_slot, B, P.ntn, P.Mp, Nv,
+                                                 P.pruned, asg, st)))
+                    return PV_ERR_HIP;
+            }
+        } else {
+            tr.before("gram_partial");
+            if (!step(pv::launch_gram_partial(dt, vis, B, Nv, d, kept, budget, P.pruned, P.Mp,
+                                              P.ks_gram, P.gpart, st)))
+                return PV_ERR_HIP;
+            tr.before("gram_reduce");
+            if (!step(pv::launch_gram_reduce(P.gpart, B, P.Mp, budget, Nv, P.ks_gram, P.invn,
+                                             P.pruned, kept, asg, st)))
                 return PV_ERR_HIP;
         }
     }
@@ -264,11 +291,10 @@ PV_API const char *pv_status_string(int status) {
 PV_API int pv_version(void) { return (1 << 16) | 0; }
 
 PV_API size_t pv_dedup_workspace_bytes(int B, int Nv, int Nt, int d, int budget, int dtype) {
-    (void)d;
-    (void)dtype;
-    if (B < 1 || Nv < 1 || Nt < 1 || budget < 1 || budget > Nv) return 0;
+    if (B < 1 || Nv < 1 || Nt < 1 || d < 64 || budget < 1 || budget > Nv) return 0;
+    if (dtype != PV_F32 && dtype != PV_BF16) return 0;
     // sized for the case that needs the most: no score or assign output
-    return plan_dedup(nullptr, B, Nv, Nt, budget, true, true).bytes;
+    return plan_dedup(nullptr, B, Nv, Nt, d, dtype == PV_BF16 ? 2 : 4, budget, true, true).bytes;
 }
 
 PV_API int pv_prune_dedup(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
@@ -345,6 +371,19 @@ int fill_desc(const pv_gather_desc &in, int B, int k, pv::GatherDesc &out, int64
 }
 
 }  // namespace
+
+PV_API int pv_select_topk(const float *scores, int B, int n, int k, int32_t *kept, int32_t *rest,
+                          int32_t *slot_of, void *stream) {
+    if (!scores || !kept) return PV_ERR_NULL;
+    if (B < 1 || B > 65535 || n < 1 || n > PV_MAX_TOKENS) return PV_ERR_SHAPE;
+    if (k < 1 || k > n) return PV_ERR_BUDGET;
+    if (!aligned16(scores) || !aligned16(kept) || (rest && !aligned16(rest)) ||
+        (slot_of && !aligned16(slot_of)))
+        return PV_ERR_ALIGN;
+    if (pv::launch_select(scores, B, n, k, kept, rest, slot_of, (hipStream_t)stream) != hipSuccess)
+        return PV_ERR_HIP;
+    return PV_OK;
+}
 
 PV_API int pv_prune_gather_batch(const pv_gather_desc *descs, int n_desc, const int32_t *idx, int B,
                                  int k, void *stream) {

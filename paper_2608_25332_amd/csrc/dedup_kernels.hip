@@ -3,107 +3,134 @@
 // nearest-centroid assignment of the pruned tokens and their aggregation.
 //
 // Kernel sequence of one call (all on the caller's stream):
-//   cos_stream    anchors x vis on MFMA (streaming tiles, norms fused);
-//                 writes the cosines, the inverse norms of the visual tokens
-//                 and per-tile row sums
-//   center        p[j] = max_i (M[i][j] - mean_i)
+//   cos_partial   anchors x vis on MFMA, split over k: partial dot products
+//                 and partial sums of squares
+//   cos_reduce    adds the k slices: cosines M, per-tile row sums, inverse
+//                 norms of the visual tokens
+//   center        p[j] = max_i (M[i][j] - mean_i)  (folded into select when
+//                 one sample's M is small)
 //   select        top-N_1 radix select, one workgroup per sample
-//   gram_*        pruned x kept cosine Gram on MFMA with a fused row argmax
-//                 per column tile (streaming tiles at small sizes, LDS-staged
-//                 128x128 tiles when the Gram is large enough to be
-//                 MFMA-bound)
-//   gram_finish   best column tile per pruned row -> assignment
+//   gram_partial  pruned x kept Gram on MFMA, split over k
+//   gram_reduce   adds the k slices, cosine, row argmax -> assignment
+//     (large Grams instead: gram_tile, LDS-staged 128x128 full-k tiles with a
+//      fused argmax per column tile, then gram_finish across column tiles)
 //   merge         centroid <- mean of itself and its members
 // Workgroups never wait on or signal each other: every cross-workgroup
 // dependency is a kernel boundary, so no kernel needs a device-wide fence
 // (on this chip a device-scope fence writes back and invalidates the L2).
 #include "pv_launch.h"
-#include "pv_stream_tile.h"
 #include "pv_tile_gemm.h"
 
 #include <math.h>
 
 namespace pv {
 
-int tile_size(int cfg) { return 16 << cfg; }
-
-// Waves and unroll depth of a streaming tile: enough 16-byte loads in flight
-// per workgroup to cover memory latency within ~128 VGPRs of fragments.
-template <int T> struct StreamCfg;
-template <> struct StreamCfg<16> { static constexpr int NW = 8, U = 8; };
-template <> struct StreamCfg<32> { static constexpr int NW = 4, U = 4; };
-template <> struct StreamCfg<64> { static constexpr int NW = 4, U = 2; };
-
 // ----------------------------------------------------------------------------
-// cos_stream: 1-D grid over (sample, vis tile, anchor tile) in XCD order.
+// Split-k products (the cosine, and the Grams that are too small to fill the
+// chip with full-k tiles).
+//
+// A workgroup owns a 64 x 64 output tile and one k slice of its rows (LDS-
+// staged, see pv_tile_gemm.h); the k slices are added in slice order by the
+// reduce kernels.  Slicing k spreads a B=1 problem over every CU while each
+// CU fetches only a few tens of KB; the price is KS fp32 partial tiles, which
+// stay in L2.
 // ----------------------------------------------------------------------------
-template <int DT, int T>
-__global__ __launch_bounds__(64 * StreamCfg<T>::NW) void cos_stream_kernel(
+constexpr int kPT = 64;  // tile edge of the split-k products
+template <int DT>
+using PTile = TileGemm<DT, kPT, kPT, 2, 2, 2>;
+
+// cos_partial: 1-D grid over (sample, k slice, anchor tile, token tile) in XCD
+// order (token tiles of one anchor tile and slice are adjacent: they share the
+// anchor rows).  Writes partial dot products part[ks][b][Nt][Nv] and partial
+// sums of squares of the token rows ssv[ks][b][Nv] and anchor rows
+// ssa[ks][b][Nt].
+template <int DT>
+__global__ __launch_bounds__(256) void cos_partial_kernel(
     const char *__restrict__ vis, const char *__restrict__ anchors, int B, int Nv, int Nt,
-    int d_bytes, int njt, int nit, float *__restrict__ M, float *__restrict__ invn_vis,
-    float *__restrict__ rowsum) {
-    constexpr int NW = StreamCfg<T>::NW, U = StreamCfg<T>::U;
-    using S = StreamTile<DT, T, T, NW, U>;
-    constexpr int F = T / 16;
-    __shared__ float red[S::RED_FLOATS];
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int total = B * njt * nit;
+    int d_bytes, int njt, int nit, int KS, float *__restrict__ part, float *__restrict__ ssv,
+    float *__restrict__ ssa) {
+    using G = PTile<DT>;
+    __shared__ __attribute__((aligned(16))) char lds[G::LDS_BYTES];
+    __shared__ float rowss[G::ROWS];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / 2, wn = wave % 2;
+    const int total = B * KS * nit * njt;
     const int tile = xcd_tile(blockIdx.x, total);
-    const int it = tile % nit;
-    const int jt = (tile / nit) % njt;
-    const int b = tile / (nit * njt);
-
-    const int i0 = it * T, j0 = jt * T;
-    const int koff = (lane >> 4) * 16;
-    const char *abase = anchors + (size_t)b * Nt * d_bytes + koff;
-    const char *vbase = vis + (size_t)b * Nv * d_bytes + koff;
-    const char *rp[2 * F];
+    const int jt = tile % njt;
+    const int it = (tile / njt) % nit;
+    const int ks = (tile / (njt * nit)) % KS;
+    const int b = tile / (njt * nit * KS);
+    const int i0 = it * kPT, j0 = jt * kPT;
+    const char *abase = anchors + (size_t)b * Nt * d_bytes;
+    const char *vbase = vis + (size_t)b * Nv * d_bytes;
+    auto row_ptr = [&](int r) -> const char * {
+        if (r < kPT) return abase + (size_t)min(i0 + r, Nt - 1) * d_bytes;
+        return vbase + (size_t)min(j0 + r - kPT, Nv - 1) * d_bytes;
+    };
+    const int nch = d_bytes / G::CHUNK;
+    const int c0 = (int)(((long long)nch * ks) / KS), c1 = (int)(((long long)nch * (ks + 1)) / KS);
+    f32x4_t acc[G::FM][G::FN];
+    float ss[G::PPT];
+    G::template run<true>(row_ptr, c0, c1, lds, acc, ss);
+    G::reduce_rows(ss, rowss);
+    const size_t kb = (size_t)ks * B + b;
+    float *pb = part + kb * Nt * Nv;
 #pragma unroll
-    for (int f = 0; f < F; ++f) {
-        rp[f] = abase + (size_t)min(i0 + f * 16 + (lane & 15), Nt - 1) * d_bytes;
-        rp[F + f] = vbase + (size_t)min(j0 + f * 16 + (lane & 15), Nv - 1) * d_bytes;
-    }
-    f32x4_t acc[F][F];
-    float ss[2 * F];
-    S::template run<true>(rp, d_bytes / 64, acc, ss);
-    S::template reduce<true>(acc, ss, red);
-    if (wave != 0) return;
-
-    float inv[2 * F];
+    for (int fm = 0; fm < G::FM; ++fm)
 #pragma unroll
-    for (int q = 0; q < 2 * F; ++q) inv[q] = (ss[q] > 0.f) ? 1.0f / sqrtf(ss[q]) : 0.f;
-    if (it == 0 && lane < 16) {
+        for (int fn = 0; fn < G::FN; ++fn) {
+            const int j = j0 + wn * G::SUB_N + fn * 16 + (lane & 15);
 #pragma unroll
-        for (int f = 0; f < F; ++f) {
-            const int j = j0 + f * 16 + lane;
-            if (j < Nv) invn_vis[(size_t)b * Nv + j] = inv[F + f];
-        }
-    }
-#pragma unroll
-    for (int fm = 0; fm < F; ++fm) {
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const int rl = (lane >> 4) * 4 + e;  // row inside the 16-row block
-            const int gi = i0 + fm * 16 + rl;
-            const float ia = __shfl(inv[fm], rl, 64);
-            float rs = 0.f;
-#pragma unroll
-            for (int fn = 0; fn < F; ++fn) {
-                const int gj = j0 + fn * 16 + (lane & 15);
-                const float cs = acc[fm][fn][e] * ia * inv[F + fn];
-                if (gj < Nv) {
-                    rs += cs;
-                    if (gi < Nt) M[((size_t)b * Nt + gi) * Nv + gj] = cs;
-                }
+            for (int e = 0; e < 4; ++e) {
+                const int i = i0 + wm * G::SUB_M + fm * 16 + (lane >> 4) * 4 + e;
+                if (i < Nt && j < Nv) pb[(size_t)i * Nv + j] = acc[fm][fn][e];
             }
-            rs += __shfl_xor(rs, 1, 64);
-            rs += __shfl_xor(rs, 2, 64);
-            rs += __shfl_xor(rs, 4, 64);
-            rs += __shfl_xor(rs, 8, 64);
-            if ((lane & 15) == 0 && gi < Nt) rowsum[((size_t)b * njt + jt) * Nt + gi] = rs;
         }
+    __syncthreads();
+    if (tid < kPT) {
+        if (jt == 0 && i0 + tid < Nt) ssa[kb * Nt + i0 + tid] = rowss[tid];
+    } else if (tid < 2 * kPT) {
+        const int j = j0 + tid - kPT;
+        if (it == 0 && j < Nv) ssv[kb * Nv + j] = rowss[tid];
     }
+}
+
+// cos_reduce: grid (ceil(Nv / 64), ceil(Nt / 4), B), 256 threads, one output
+// per thread (wave = anchor row, lane = token).  Adds the k slices in slice
+// order, forms cos = dot / (|a| |v|) (0 for a zero vector), writes
+// M[b][Nt][Nv], the row sums of M over this workgroup's 64 tokens
+// rowsum[b][Nv/64][Nt] and (first row group) the inverse token norms.
+constexpr int kRedTok = 64, kRedRows = 4;
+
+__global__ __launch_bounds__(256) void cos_reduce_kernel(
+    const float *__restrict__ part, const float *__restrict__ ssv, const float *__restrict__ ssa,
+    int B, int Nv, int Nt, int KS, float *__restrict__ M, float *__restrict__ rowsum,
+    float *__restrict__ invn_vis) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int jt = blockIdx.x, b = blockIdx.z;
+    const int njt = gridDim.x;
+    const int i = blockIdx.y * kRedRows + wave;
+    const int j = jt * kRedTok + lane;
+    const int jc = min(j, Nv - 1), ic = min(i, Nt - 1);
+    float sv = 0.f, sa = 0.f, dot = 0.f;
+#pragma unroll 8
+    for (int ks = 0; ks < KS; ++ks) {
+        const size_t kb = (size_t)ks * B + b;
+        sv += ssv[kb * Nv + jc];
+        sa += ssa[kb * Nt + ic];
+        dot += part[(kb * Nt + ic) * Nv + jc];
+    }
+    const float inv_v = (sv > 0.f) ? 1.0f / sqrtf(sv) : 0.f;
+    const float inv_a = (sa > 0.f) ? 1.0f / sqrtf(sa) : 0.f;
+    if (blockIdx.y == 0 && wave == 0 && j < Nv) invn_vis[(size_t)b * Nv + j] = inv_v;
+    const float cs = dot * inv_a * inv_v;
+    if (i < Nt && j < Nv) M[((size_t)b * Nt + i) * Nv + j] = cs;
+    float rs = (j < Nv) ? cs : 0.f;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) rs += __shfl_xor(rs, off, 64);
+    if (lane == 0 && i < Nt) rowsum[((size_t)b * njt + jt) * Nt + i] = rs;
 }
 
 // ----------------------------------------------------------------------------
@@ -143,23 +170,24 @@ __global__ __launch_bounds__(kCenNT) void center_kernel(const float *__restrict_
 }
 
 // ----------------------------------------------------------------------------
-// select: grid (B), 256 threads; top-`budget` of p with its complement list
-// and the slot of every kept token.  Keys are staged in LDS up to kStageKeys.
+// select: grid (B), NT threads; top-`budget` of p with its complement list and
+// the slot of every kept token.  Each thread holds EMAX keys in registers.
 // ----------------------------------------------------------------------------
-constexpr int kSelNT = 256;
-constexpr int kStageKeys = 8192;
-
-__global__ __launch_bounds__(kSelNT) void select_kernel(const float *__restrict__ p, int Nv,
-                                                        int budget, int32_t *__restrict__ kept,
-                                                        int32_t *__restrict__ pruned,
-                                                        int32_t *__restrict__ slot_of) {
-    extern __shared__ uint32_t keys[];  // [Nv] when staged
+template <int NT, int EMAX>
+__global__ __launch_bounds__(NT) void select_kernel(const float *__restrict__ p, int Nv,
+                                                    int budget, int32_t *__restrict__ kept,
+                                                    int32_t *__restrict__ pruned,
+                                                    int32_t *__restrict__ slot_of) {
     __shared__ TopkSmem sm;
     const int b = blockIdx.x;
-    block_topk<kSelNT>(p + (size_t)b * Nv, Nv, budget, kept + (size_t)b * budget,
-                       pruned ? pruned + (size_t)b * (Nv - budget) : nullptr,
-                       slot_of ? slot_of + (size_t)b * Nv : nullptr, sm,
-                       Nv <= kStageKeys ? keys : nullptr);
+    const float *pb = p + (size_t)b * Nv;
+    const int E = topk_per_thread(Nv, NT), j0 = threadIdx.x * E;
+    uint32_t key[EMAX];
+#pragma unroll
+    for (int e = 0; e < EMAX; ++e) key[e] = (e < E && j0 + e < Nv) ? order_key(pb[j0 + e]) : 0u;
+    block_topk<NT, EMAX>(key, Nv, budget, kept + (size_t)b * budget,
+                         pruned ? pruned + (size_t)b * (Nv - budget) : nullptr,
+                         slot_of ? slot_of + (size_t)b * Nv : nullptr, sm);
 }
 
 // ----------------------------------------------------------------------------
@@ -196,85 +224,88 @@ __global__ __launch_bounds__(kFinNT) void gram_finish_kernel(const float *__rest
     assign[(size_t)b * Nv + pruned[(size_t)b * Mp + m]] = bs;
 }
 
-// gram_stream: 1-D grid over (sample, pruned-row tile, kept-column tile).
-template <int DT, int T>
-__global__ __launch_bounds__(64 * StreamCfg<T>::NW) void gram_stream_kernel(
+// gram_partial: 1-D grid over (sample, k slice, kept tile, pruned tile) in
+// XCD order (pruned tiles of one kept tile and slice are adjacent: they share
+// the kept rows).  Writes partial dot products part[ks][b][Mp][N1].
+template <int DT>
+__global__ __launch_bounds__(256) void gram_partial_kernel(
     const char *__restrict__ vis, int B, int Nv, int d_bytes, const int32_t *__restrict__ kept,
-    int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn,
-    const float *__restrict__ invn, float *__restrict__ best_val,
-    int32_t *__restrict__ best_slot, int32_t *__restrict__ assign) {
-    constexpr int NW = StreamCfg<T>::NW, U = StreamCfg<T>::U;
-    using S = StreamTile<DT, T, T, NW, U>;
-    constexpr int F = T / 16;
-    __shared__ float red[S::RED_FLOATS];
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int total = B * ntm * ntn;
+    int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn, int KS,
+    float *__restrict__ part) {
+    using G = PTile<DT>;
+    __shared__ __attribute__((aligned(16))) char lds[G::LDS_BYTES];
+    __shared__ int32_t rowtok[G::ROWS];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / 2, wn = wave % 2;
+    const int total = B * KS * ntn * ntm;
     const int tile = xcd_tile(blockIdx.x, total);
-    const int nt = tile % ntn;
-    const int mt = (tile / ntn) % ntm;
-    const int b = tile / (ntn * ntm);
-    const int m0 = mt * T, n0 = nt * T;
+    const int mt = tile % ntm;
+    const int nt = (tile / ntm) % ntn;
+    const int ks = (tile / (ntm * ntn)) % KS;
+    const int b = tile / (ntm * ntn * KS);
+    const int m0 = mt * kPT, n0 = nt * kPT;
     const int32_t *pr = pruned + (size_t)b * Mp;
     const int32_t *kp = kept + (size_t)b * N1;
-    const int koff = (lane >> 4) * 16;
-    const char *vbase = vis + (size_t)b * Nv * d_bytes + koff;
-
-    const char *rp[2 * F];
-    float inv[2 * F];
+    for (int r = tid; r < G::ROWS; r += G::NT)
+        rowtok[r] = (r < kPT) ? pr[min(m0 + r, Mp - 1)] : kp[min(n0 + r - kPT, N1 - 1)];
+    __syncthreads();
+    const char *vbase = vis + (size_t)b * Nv * d_bytes;
+    auto row_ptr = [&](int r) -> const char * { return vbase + (size_t)rowtok[r] * d_bytes; };
+    const int nch = d_bytes / G::CHUNK;
+    const int c0 = (int)(((long long)nch * ks) / KS), c1 = (int)(((long long)nch * (ks + 1)) / KS);
+    f32x4_t acc[G::FM][G::FN];
+    float ss[G::PPT];
+    G::template run<false>(row_ptr, c0, c1, lds, acc, ss);
+    float *pb = part + ((size_t)ks * B + b) * Mp * N1;
 #pragma unroll
-    for (int f = 0; f < F; ++f) {
-        const int ta = pr[min(m0 + f * 16 + (lane & 15), Mp - 1)];
-        const int tb = kp[min(n0 + f * 16 + (lane & 15), N1 - 1)];
-        rp[f] = vbase + (size_t)ta * d_bytes;
-        rp[F + f] = vbase + (size_t)tb * d_bytes;
-        inv[f] = invn[(size_t)b * Nv + ta];
-        inv[F + f] = invn[(size_t)b * Nv + tb];
-    }
-    f32x4_t acc[F][F];
-    float ss[2 * F];
-    S::template run<false>(rp, d_bytes / 64, acc, ss);
-    S::template reduce<false>(acc, ss, red);
-
-    if (wave == 0) {
+    for (int fm = 0; fm < G::FM; ++fm)
 #pragma unroll
-        for (int fm = 0; fm < F; ++fm) {
+        for (int fn = 0; fn < G::FN; ++fn) {
+            const int n = n0 + wn * G::SUB_N + fn * 16 + (lane & 15);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const int rl = (lane >> 4) * 4 + e;
-                const float ia = __shfl(inv[fm], rl, 64);
-                float bv = -INFINITY;
-                int bs = 0x7FFFFFFF;
-#pragma unroll
-                for (int fn = 0; fn < F; ++fn) {
-                    const int slot = n0 + fn * 16 + (lane & 15);
-                    const float cs = acc[fm][fn][e] * ia * inv[F + fn];
-                    if (slot < N1 && better(cs, slot, bv, bs)) {
-                        bv = cs;
-                        bs = slot;
-                    }
-                }
-#pragma unroll
-                for (int off = 1; off < 16; off <<= 1) {
-                    const float ov = __shfl_xor(bv, off, 64);
-                    const int os = __shfl_xor(bs, off, 64);
-                    if (better(ov, os, bv, bs)) {
-                        bv = ov;
-                        bs = os;
-                    }
-                }
-                const int m = m0 + fm * 16 + rl;
-                if ((lane & 15) == 0 && m < Mp) {
-                    if (ntn == 1) {
-                        assign[(size_t)b * Nv + pr[m]] = bs;
-                    } else {
-                        best_val[((size_t)b * ntn + nt) * Mp + m] = bv;
-                        best_slot[((size_t)b * ntn + nt) * Mp + m] = bs;
-                    }
-                }
+                const int m = m0 + wm * G::SUB_M + fm * 16 + (lane >> 4) * 4 + e;
+                if (m < Mp && n < N1) pb[(size_t)m * N1 + n] = acc[fm][fn][e];
             }
         }
+}
+
+// gram_reduce: grid (ceil(Mp / 2), B), 128 threads, one wave per pruned row.
+// Adds the k slices in slice order, forms the cosine to every kept token and
+// writes the slot of the best one (higher cosine, then lower slot).
+__global__ __launch_bounds__(128) void gram_reduce_kernel(
+    const float *__restrict__ part, int B, int Mp, int N1, int Nv, int KS,
+    const float *__restrict__ invn, const int32_t *__restrict__ pruned,
+    const int32_t *__restrict__ kept, int32_t *__restrict__ assign) {
+    const int lane = threadIdx.x & 63;
+    const int m = blockIdx.x * 2 + (threadIdx.x >> 6);
+    const int b = blockIdx.y;
+    if (m >= Mp) return;
+    const int tok = pruned[(size_t)b * Mp + m];
+    const float ia = invn[(size_t)b * Nv + tok];
+    float bv = -INFINITY;
+    int bs = 0x7FFFFFFF;
+    for (int n = lane; n < N1; n += 64) {
+        float dot = 0.f;
+#pragma unroll 8
+        for (int ks = 0; ks < KS; ++ks) dot += part[(((size_t)ks * B + b) * Mp + m) * N1 + n];
+        const float cs = dot * ia * invn[(size_t)b * Nv + kept[(size_t)b * N1 + n]];
+        if (better(cs, n, bv, bs)) {
+            bv = cs;
+            bs = n;
+        }
     }
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const float ov = __shfl_xor(bv, off, 64);
+        const int os = __shfl_xor(bs, off, 64);
+        if (better(ov, os, bv, bs)) {
+            bv = ov;
+            bs = os;
+        }
+    }
+    if (lane == 0) assign[(size_t)b * Nv + tok] = bs;
 }
 
 // gram_tile: LDS-staged 128 x 128 tiles for the large, MFMA-bound Grams.
@@ -284,7 +315,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
     const char *__restrict__ vis, int Nv, int d_bytes, const int32_t *__restrict__ kept, int N1,
     const int32_t *__restrict__ pruned, int Mp, const float *__restrict__ invn,
     float *__restrict__ best_val, int32_t *__restrict__ best_slot, int32_t *__restrict__ assign) {
-    using G = TileGemm<DT, BM, BN, WM, WN>;
+    using G = TileGemm<DT, BM, BN, WM, WN, 1>;
     __shared__ __attribute__((aligned(16))) char lds[G::LDS_BYTES];
     __shared__ int32_t rowtok[G::ROWS];
     __shared__ float rowinv[G::ROWS];
@@ -310,7 +341,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
 
     f32x4_t acc[G::FM][G::FN];
     float ss[G::PPT];
-    G::template run<false>(row_ptr, d_bytes / G::CHUNK, lds, acc, ss);
+    G::template run<false>(row_ptr, 0, d_bytes / G::CHUNK, lds, acc, ss);
 
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
@@ -487,33 +518,29 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
 // ----------------------------------------------------------------------------
 // launchers
 // ----------------------------------------------------------------------------
-template <int DT, int T>
-static hipError_t cos_go(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
-                         float *M, float *invn, float *rowsum, hipStream_t st) {
-    const int esz = (DT == kBF16) ? 2 : 4;
-    const int njt = (Nv + T - 1) / T, nit = (Nt + T - 1) / T;
-    hipLaunchKernelGGL((cos_stream_kernel<DT, T>), dim3(B * njt * nit),
-                       dim3(64 * StreamCfg<T>::NW), 0, st, (const char *)vis, (const char *)anchors,
-                       B, Nv, Nt, d * esz, njt, nit, M, invn, rowsum);
+hipError_t launch_cos_partial(int dt, const void *vis, const void *anchors, int B, int Nv, int Nt,
+                              int d, int KS, float *part, float *ssv, float *ssa, hipStream_t st) {
+    const int esz = (dt == kBF16) ? 2 : 4;
+    const int njt = (Nv + kPT - 1) / kPT, nit = (Nt + kPT - 1) / kPT;
+    const dim3 grid(B * KS * nit * njt), block(256);
+    if (dt == kBF16)
+        hipLaunchKernelGGL(cos_partial_kernel<kBF16>, grid, block, 0, st, (const char *)vis,
+                           (const char *)anchors, B, Nv, Nt, d * esz, njt, nit, KS, part, ssv, ssa);
+    else
+        hipLaunchKernelGGL(cos_partial_kernel<kF32>, grid, block, 0, st, (const char *)vis,
+                           (const char *)anchors, B, Nv, Nt, d * esz, njt, nit, KS, part, ssv, ssa);
     return hipGetLastError();
 }
 
-template <int DT>
-static hipError_t cos_dt(int cfg, const void *vis, const void *anchors, int B, int Nv, int Nt,
-                         int d, float *M, float *invn, float *rowsum, hipStream_t st) {
-    switch (cfg) {
-        case TILE_16: return cos_go<DT, 16>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
-        case TILE_32: return cos_go<DT, 32>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
-        case TILE_64: return cos_go<DT, 64>(vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
-    }
-    return hipErrorInvalidValue;
+hipError_t launch_cos_reduce(const float *part, const float *ssv, const float *ssa, int B, int Nv,
+                             int Nt, int KS, float *M, float *rowsum, float *invn, hipStream_t st) {
+    dim3 grid((Nv + kRedTok - 1) / kRedTok, (Nt + kRedRows - 1) / kRedRows, B);
+    hipLaunchKernelGGL(cos_reduce_kernel, grid, dim3(256), 0, st, part, ssv, ssa, B, Nv, Nt, KS, M,
+                       rowsum, invn);
+    return hipGetLastError();
 }
 
-hipError_t launch_cos_tile(int dt, int cfg, const void *vis, const void *anchors, int B, int Nv,
-                           int Nt, int d, float *M, float *invn, float *rowsum, hipStream_t st) {
-    if (dt == kBF16) return cos_dt<kBF16>(cfg, vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
-    return cos_dt<kF32>(cfg, vis, anchors, B, Nv, Nt, d, M, invn, rowsum, st);
-}
+int cos_row_tiles(int Nv) { return (Nv + kRedTok - 1) / kRedTok; }
 
 hipError_t launch_center(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
                          float *p, hipStream_t st) {
@@ -525,22 +552,17 @@ hipError_t launch_center(const float *M, const float *rowsum, int njt, int B, in
 
 hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kept, int32_t *pruned,
                          int32_t *slot_of, hipStream_t st) {
-    const size_t lds = (Nv <= kStageKeys) ? (size_t)Nv * sizeof(uint32_t) : 0;
-    hipLaunchKernelGGL(select_kernel, dim3(B), dim3(kSelNT), lds, st, p, Nv, budget, kept, pruned,
-                       slot_of);
-    return hipGetLastError();
-}
-
-template <int DT, int T>
-static hipError_t gram_stream_go(const void *vis, int B, int Nv, int d, const int32_t *kept,
-                                 int N1, const int32_t *pruned, int Mp, const float *invn,
-                                 float *best_val, int32_t *best_slot, int32_t *assign,
-                                 hipStream_t st) {
-    const int esz = (DT == kBF16) ? 2 : 4;
-    const int ntm = (Mp + T - 1) / T, ntn = (N1 + T - 1) / T;
-    hipLaunchKernelGGL((gram_stream_kernel<DT, T>), dim3(B * ntm * ntn),
-                       dim3(64 * StreamCfg<T>::NW), 0, st, (const char *)vis, B, Nv, d * esz,
-                       kept, N1, pruned, Mp, ntm, ntn, invn, best_val, best_slot, assign);
+    if (Nv <= 256 * 4)
+        hipLaunchKernelGGL((select_kernel<256, 4>), dim3(B), dim3(256), 0, st, p, Nv, budget, kept,
+                           pruned, slot_of);
+    else if (Nv <= 512 * 8)
+        hipLaunchKernelGGL((select_kernel<512, 8>), dim3(B), dim3(512), 0, st, p, Nv, budget, kept,
+                           pruned, slot_of);
+    else if (Nv <= 1024 * 16)
+        hipLaunchKernelGGL((select_kernel<1024, 16>), dim3(B), dim3(1024), 0, st, p, Nv, budget,
+                           kept, pruned, slot_of);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 
@@ -556,25 +578,36 @@ static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int3
     return hipGetLastError();
 }
 
-template <int DT>
-static hipError_t gram_dt(int cfg, const void *vis, int B, int Nv, int d, const int32_t *kept,
-                          int N1, const int32_t *pruned, int Mp, const float *invn,
-                          float *best_val, int32_t *best_slot, int32_t *assign, hipStream_t st) {
-    switch (cfg) {
-        case TILE_16: return gram_stream_go<DT, 16>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
-        case TILE_32: return gram_stream_go<DT, 32>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
-        case TILE_64: return gram_stream_go<DT, 64>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
-        case TILE_128: return gram_tile_go<DT>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
-    }
-    return hipErrorInvalidValue;
+hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
+                               int N1, const int32_t *pruned, int Mp, int KS, float *part,
+                               hipStream_t st) {
+    const int esz = (dt == kBF16) ? 2 : 4;
+    const int ntm = (Mp + kPT - 1) / kPT, ntn = (N1 + kPT - 1) / kPT;
+    const dim3 grid(B * KS * ntm * ntn), block(256);
+    if (dt == kBF16)
+        hipLaunchKernelGGL(gram_partial_kernel<kBF16>, grid, block, 0, st, (const char *)vis, B, Nv,
+                           d * esz, kept, N1, pruned, Mp, ntm, ntn, KS, part);
+    else
+        hipLaunchKernelGGL(gram_partial_kernel<kF32>, grid, block, 0, st, (const char *)vis, B, Nv,
+                           d * esz, kept, N1, pruned, Mp, ntm, ntn, KS, part);
+    return hipGetLastError();
 }
 
-hipError_t launch_gram(int dt, int cfg, const void *vis, int B, int Nv, int d, const int32_t *kept,
-                       int N1, const int32_t *pruned, int Mp, const float *invn, float *best_val,
-                       int32_t *best_slot, int32_t *assign, hipStream_t st) {
+hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, int KS,
+                              const float *invn, const int32_t *pruned, const int32_t *kept,
+                              int32_t *assign, hipStream_t st) {
+    dim3 grid((Mp + 1) / 2, B);
+    hipLaunchKernelGGL(gram_reduce_kernel, grid, dim3(128), 0, st, part, B, Mp, N1, Nv, KS, invn,
+                       pruned, kept, assign);
+    return hipGetLastError();
+}
+
+hipError_t launch_gram_tile(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
+                            int N1, const int32_t *pruned, int Mp, const float *invn,
+                            float *best_val, int32_t *best_slot, int32_t *assign, hipStream_t st) {
     if (dt == kBF16)
-        return gram_dt<kBF16>(cfg, vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
-    return gram_dt<kF32>(cfg, vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
+        return gram_tile_go<kBF16>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
+    return gram_tile_go<kF32>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
 }
 
 hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, int B, int ntn,

@@ -171,29 +171,30 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     }
 }
 
-constexpr int kSelectNT = 256;
-constexpr int kSelectStage = 8192;
-
-__global__ __launch_bounds__(kSelectNT) void score_select_kernel(const float *__restrict__ partial,
-                                                                 int nparts, int N, float inv_norm,
-                                                                 float *__restrict__ v, int budget,
-                                                                 int32_t *__restrict__ kept) {
-    extern __shared__ uint32_t keys[];  // [N] when staged
+template <int NT, int EMAX>
+__global__ __launch_bounds__(NT) void score_select_kernel(const float *__restrict__ partial,
+                                                          int nparts, int N, float inv_norm,
+                                                          float *__restrict__ v, int budget,
+                                                          int32_t *__restrict__ kept) {
     __shared__ TopkSmem sm;
-    const int b = blockIdx.x, tid = threadIdx.x;
+    const int b = blockIdx.x;
     const float *pb = partial + (size_t)b * nparts * N;
     float *vb = v + (size_t)b * N;
-    const bool stage = N <= kSelectStage;
-    for (int j = tid; j < N; j += kSelectNT) {
-        float s = 0.f;
-#pragma unroll 4
-        for (int t = 0; t < nparts; ++t) s += pb[(size_t)t * N + j];
-        vb[j] = s * inv_norm;
+    const int E = topk_per_thread(N, NT), j0 = threadIdx.x * E;
+    uint32_t key[EMAX];
+#pragma unroll
+    for (int e = 0; e < EMAX; ++e) {
+        const int j = j0 + e;
+        key[e] = 0u;
+        if (e < E && j < N) {
+            float s = 0.f;
+            for (int t = 0; t < nparts; ++t) s += pb[(size_t)t * N + j];
+            s *= inv_norm;
+            vb[j] = s;
+            key[e] = order_key(s);
+        }
     }
-    // block_topk stages v[j] in LDS with the same thread-to-j mapping, so
-    // every thread reads back only what it wrote itself
-    block_topk<kSelectNT>(vb, N, budget, kept + (size_t)b * budget, nullptr, nullptr, sm,
-                          stage ? keys : nullptr);
+    block_topk<NT, EMAX>(key, N, budget, kept + (size_t)b * budget, nullptr, nullptr, sm);
 }
 
 template <int DT, int NKS, int MAXB>
@@ -265,9 +266,17 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const Head
 
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,
                                float *v, int budget, int32_t *kept, hipStream_t st) {
-    const size_t lds = (N <= kSelectStage) ? (size_t)N * sizeof(uint32_t) : 0;
-    hipLaunchKernelGGL(score_select_kernel, dim3(B), dim3(kSelectNT), lds, st, partial, nparts, N,
-                       inv_norm, v, budget, kept);
+    if (N <= 256 * 4)
+        hipLaunchKernelGGL((score_select_kernel<256, 4>), dim3(B), dim3(256), 0, st, partial,
+                           nparts, N, inv_norm, v, budget, kept);
+    else if (N <= 512 * 8)
+        hipLaunchKernelGGL((score_select_kernel<512, 8>), dim3(B), dim3(512), 0, st, partial,
+                           nparts, N, inv_norm, v, budget, kept);
+    else if (N <= 1024 * 16)
+        hipLaunchKernelGGL((score_select_kernel<1024, 16>), dim3(B), dim3(1024), 0, st, partial,
+                           nparts, N, inv_norm, v, budget, kept);
+    else
+        return hipErrorInvalidValue;
     return hipGetLastError();
 }
 

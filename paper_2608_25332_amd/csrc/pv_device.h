@@ -126,89 +126,151 @@ __device__ __forceinline__ int xcd_tile(int L, int total) {
 }
 
 struct TopkSmem {
-    int hist[256];
+    int hist[2][256];
     int wsum[16];
-    uint32_t digit;
-    int remaining;
+    uint32_t wlo[16], whi[16];
+    int sel[2][3];  // digit, rank still to find, keys in the digit's bin
 };
 
-// Deterministic top-k of n float scores by one block of NT threads: keeps the
-// k highest scores, lower index first among equal scores, and writes
+// Number of keys each thread owns in block_topk: ceil(n / NT).
+__host__ __device__ constexpr int topk_per_thread(int n, int NT) { return (n + NT - 1) / NT; }
+
+// Deterministic top-k of n keys by one block of NT threads: keeps the k
+// largest keys, lower index first among equal keys, and writes
 //   kept[0..k)       the kept indices, ascending,
 //   rest[0..n-k)     the other indices, ascending (if rest != nullptr),
 //   slot_of[j]       position of j in kept, or -1 (if slot_of != nullptr).
-// Radix select over the order-preserving keys (four 8-bit digits, most
-// significant first) finds the k-th largest key T; the keys above T and the
-// first (k - #above) keys equal to T in index order are kept.  When `lds_keys`
-// is given (room for n keys) the keys are staged there once; otherwise every
-// pass re-reads the scores from global memory (cache resident).
-template <int NT>
-__device__ void block_topk(const float *score, int n, int k, int32_t *kept, int32_t *rest,
-                           int32_t *slot_of, TopkSmem &sm, uint32_t *lds_keys) {
-    const int tid = threadIdx.x;
-    if (lds_keys) {
-        for (int j = tid; j < n; j += NT) lds_keys[j] = order_key(score[j]);
-        __syncthreads();
-    }
-    auto key_of = [&](int j) -> uint32_t { return lds_keys ? lds_keys[j] : order_key(score[j]); };
-    uint32_t prefix = 0u, mask = 0u;
-    int kr = k;  // rank still to be found inside the current prefix group
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        for (int e = tid; e < 256; e += NT) sm.hist[e] = 0;
-        __syncthreads();
-        for (int j = tid; j < n; j += NT) {
-            const uint32_t key = key_of(j);
-            if ((key & mask) == prefix) atomicAdd(&sm.hist[(key >> shift) & 255u], 1);
+// Thread t owns the E = ceil(n / NT) <= EMAX consecutive indices starting at
+// t * E and passes their keys in key[] (entries past n are ignored).  The keys
+// are order-preserving images of the scores (order_key), so comparing keys
+// compares scores.
+//
+// Radix select, most significant digit first, but starting just below the
+// bits that every key shares (found from the block's min and max key): close
+// scores share their sign and exponent bits, and starting there would pile
+// every key into one bin.  Each pass histograms the 8-bit digit of the keys
+// that still match the prefix found so far and picks the bin that holds the
+// rank still sought.  The search stops as soon as that bin is kept whole (its
+// count equals the rank sought) or the key is fully resolved; the kept set is
+// then every key whose resolved prefix is greater, plus the first `rank`
+// keys, in index order, whose prefix is equal.  One packed block scan places
+// every index.  k must satisfy 1 <= k <= n.
+template <int NT, int EMAX>
+__device__ __forceinline__ void block_topk(const uint32_t (&key)[EMAX], int n, int k,
+                                           int32_t *kept, int32_t *rest, int32_t *slot_of,
+                                           TopkSmem &sm) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    constexpr int NW = NT / 64;
+    const int E = topk_per_thread(n, NT);
+    const int j0 = tid * E;
+
+    // block min and max key
+    uint32_t lo = 0xFFFFFFFFu, hi = 0u;
+#pragma unroll
+    for (int e = 0; e < EMAX; ++e) {
+        if (e < E && j0 + e < n) {
+            lo = min(lo, key[e]);
+            hi = max(hi, key[e]);
         }
-        __syncthreads();
-        if (tid < 64) {
-            // lane owns bins 4*lane .. 4*lane+3
-            const int h0 = sm.hist[4 * tid], h1 = sm.hist[4 * tid + 1];
-            const int h2 = sm.hist[4 * tid + 2], h3 = sm.hist[4 * tid + 3];
-            const int mine = h0 + h1 + h2 + h3;
-            // suffix sum over lanes: reverse the lane order, inclusive scan
-            const int rev = __shfl(mine, 63 - tid, 64);
-            const int inc = wave_incl_scan(rev);
-            const int suffix_incl = __shfl(inc, 63 - tid, 64);  // sum over lanes >= tid
-            const int above = suffix_incl - mine;                // keys in bins > 4*tid+3
-            const int ge3 = above + h3, ge2 = ge3 + h2, ge1 = ge2 + h1, ge0 = ge1 + h0;
-            int dsel = -1, gt = 0;
-            if (above < kr && kr <= ge3) { dsel = 3; gt = above; }
-            else if (ge3 < kr && kr <= ge2) { dsel = 2; gt = ge3; }
-            else if (ge2 < kr && kr <= ge1) { dsel = 1; gt = ge2; }
-            else if (ge1 < kr && kr <= ge0) { dsel = 0; gt = ge1; }
-            if (dsel >= 0) {
-                sm.digit = (uint32_t)(4 * tid + dsel);
-                sm.remaining = kr - gt;
-            }
-        }
-        __syncthreads();
-        prefix |= sm.digit << shift;
-        mask |= 0xFFu << shift;
-        kr = sm.remaining;
-        __syncthreads();
     }
-    const uint32_t T = prefix;  // key of the k-th largest score
-    int carry_eq = 0, carry_keep = 0;
-    for (int base = 0; base < n; base += NT) {
-        const int j = base + tid;
-        const uint32_t key = (j < n) ? key_of(j) : 0u;
-        const int is_gt = (j < n) && key > T;
-        const int is_eq = (j < n) && key == T;
-        int tot_eq, tot_keep;
-        const int eq_before = block_excl_scan<NT>(is_eq, sm.wsum, &tot_eq) + carry_eq;
-        const int keep = is_gt || (is_eq && eq_before < kr);
-        const int pos = block_excl_scan<NT>(keep, sm.wsum, &tot_keep) + carry_keep;
-        if (j < n) {
-            if (keep) {
-                kept[pos] = j;
-            } else if (rest) {
-                rest[j - pos] = j;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        lo = min(lo, (uint32_t)__shfl_xor((int)lo, off, 64));
+        hi = max(hi, (uint32_t)__shfl_xor((int)hi, off, 64));
+    }
+    if (lane == 0) {
+        sm.wlo[wave] = lo;
+        sm.whi[wave] = hi;
+    }
+    for (int e = tid; e < 256; e += NT) sm.hist[0][e] = 0;
+    __syncthreads();
+    lo = sm.wlo[0];
+    hi = sm.whi[0];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) {
+        lo = min(lo, sm.wlo[w]);
+        hi = max(hi, sm.whi[w]);
+    }
+
+    // prefix/mask: the bits resolved so far; kr: rank still sought among the
+    // keys that match the prefix
+    uint32_t prefix = hi, mask = 0xFFFFFFFFu;
+    int kr = k;
+    const uint32_t diff = lo ^ hi;
+    if (diff != 0u) {
+        const int top = 31 - __clz(diff);  // highest bit where keys differ
+        mask = (top == 31) ? 0u : ~((2u << top) - 1u);
+        prefix = hi & mask;
+        int shift = top - 7 > 0 ? top - 7 : 0;
+        int cur = 0;
+        while (true) {
+#pragma unroll
+            for (int e = 0; e < EMAX; ++e) {
+                if (e < E && j0 + e < n && (key[e] & mask) == prefix)
+                    atomicAdd(&sm.hist[cur][(key[e] >> shift) & 255u], 1);
             }
+            __syncthreads();
+            for (int e = tid; e < 256; e += NT) sm.hist[cur ^ 1][e] = 0;
+            if (wave == 0) {
+                // lane owns bins 4*lane .. 4*lane+3; find the bin holding rank kr
+                // counted from the top
+                const int h0 = sm.hist[cur][4 * lane], h1 = sm.hist[cur][4 * lane + 1];
+                const int h2 = sm.hist[cur][4 * lane + 2], h3 = sm.hist[cur][4 * lane + 3];
+                const int mine = h0 + h1 + h2 + h3;
+                const int rev = __shfl(mine, 63 - lane, 64);
+                const int inc = wave_incl_scan(rev);
+                const int suffix_incl = __shfl(inc, 63 - lane, 64);  // lanes >= this one
+                const int above = suffix_incl - mine;                 // bins > 4*lane+3
+                const int ge3 = above + h3, ge2 = ge3 + h2, ge1 = ge2 + h1, ge0 = ge1 + h0;
+                int dsel = -1, gt = 0, cnt = 0;
+                if (above < kr && kr <= ge3) { dsel = 3; gt = above; cnt = h3; }
+                else if (ge3 < kr && kr <= ge2) { dsel = 2; gt = ge3; cnt = h2; }
+                else if (ge2 < kr && kr <= ge1) { dsel = 1; gt = ge2; cnt = h1; }
+                else if (ge1 < kr && kr <= ge0) { dsel = 0; gt = ge1; cnt = h0; }
+                if (dsel >= 0) {
+                    sm.sel[cur][0] = 4 * lane + dsel;
+                    sm.sel[cur][1] = kr - gt;
+                    sm.sel[cur][2] = cnt;
+                }
+            }
+            __syncthreads();
+            const uint32_t digit = (uint32_t)sm.sel[cur][0];
+            const int cnt = sm.sel[cur][2];
+            kr = sm.sel[cur][1];
+            prefix = (prefix & ~(0xFFu << shift)) | (digit << shift);
+            mask |= 0xFFu << shift;
+            if (cnt == kr || shift == 0) break;
+            shift = shift >= 8 ? shift - 8 : 0;
+            cur ^= 1;
+        }
+    }
+
+    // keep: prefix greater, or prefix equal and among the first kr such keys
+    int n_gt = 0, n_eq = 0;
+#pragma unroll
+    for (int e = 0; e < EMAX; ++e) {
+        if (e < E && j0 + e < n) {
+            const uint32_t m = key[e] & mask;
+            n_gt += m > prefix;
+            n_eq += m == prefix;
+        }
+    }
+    int total;
+    const int before = block_excl_scan<NT>(n_gt | (n_eq << 16), sm.wsum, &total);
+    int gt_before = before & 0xFFFF, eq_before = before >> 16;
+#pragma unroll
+    for (int e = 0; e < EMAX; ++e) {
+        const int j = j0 + e;
+        if (e < E && j < n) {
+            const uint32_t m = key[e] & mask;
+            const int pos = gt_before + min(eq_before, kr);
+            const bool keep = m > prefix || (m == prefix && eq_before < kr);
+            if (keep) kept[pos] = j;
+            else if (rest) rest[j - pos] = j;
             if (slot_of) slot_of[j] = keep ? pos : -1;
+            gt_before += m > prefix;
+            eq_before += m == prefix;
         }
-        carry_eq += tot_eq;
-        carry_keep += tot_keep;
     }
 }
 

@@ -10,25 +10,31 @@ namespace pv {
 constexpr int kF32 = 0;
 constexpr int kBF16 = 1;
 
-// Tile shapes of the row x row MFMA product, smallest first.
-enum TileCfg { TILE_16 = 0, TILE_32 = 1, TILE_64 = 2, TILE_128 = 3, N_TILE_CFG = 4 };
-int tile_size(int cfg);  // BM == BN of a config
-
 constexpr int kMaxHeadArgs = 512;
 struct HeadArgs {
     int32_t h[kMaxHeadArgs];
 };
 
 // ---- pruning before the LLM (Sec. 4.3)
-hipError_t launch_cos_tile(int dt, int cfg, const void *vis, const void *anchors, int B, int Nv,
-                           int Nt, int d, float *M, float *invn, float *rowsum, hipStream_t st);
+constexpr int kSplitTile = 64;  // tile edge of the split-k products
+int cos_row_tiles(int Nv);      // token tiles of the row sums written by cos_reduce
+hipError_t launch_cos_partial(int dt, const void *vis, const void *anchors, int B, int Nv, int Nt,
+                              int d, int KS, float *part, float *ssv, float *ssa, hipStream_t st);
+hipError_t launch_cos_reduce(const float *part, const float *ssv, const float *ssa, int B, int Nv,
+                             int Nt, int KS, float *M, float *rowsum, float *invn, hipStream_t st);
 hipError_t launch_center(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
                          float *p, hipStream_t st);
 hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kept, int32_t *pruned,
                          int32_t *slot_of, hipStream_t st);
-hipError_t launch_gram(int dt, int cfg, const void *vis, int B, int Nv, int d, const int32_t *kept,
-                       int N1, const int32_t *pruned, int Mp, const float *invn, float *best_val,
-                       int32_t *best_slot, int32_t *assign, hipStream_t st);
+hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
+                               int N1, const int32_t *pruned, int Mp, int KS, float *part,
+                               hipStream_t st);
+hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, int KS,
+                              const float *invn, const int32_t *pruned, const int32_t *kept,
+                              int32_t *assign, hipStream_t st);
+hipError_t launch_gram_tile(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
+                            int N1, const int32_t *pruned, int Mp, const float *invn,
+                            float *best_val, int32_t *best_slot, int32_t *assign, hipStream_t st);
 hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, int B, int ntn,
                               int Mp, int Nv, const int32_t *pruned, int32_t *assign,
                               hipStream_t st);

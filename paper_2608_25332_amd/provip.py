@@ -84,6 +84,8 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_gather.restype = _i
     lib.pv_prune_gather_batch.argtypes = [ctypes.POINTER(GatherDesc), _i, _vp, _i, _i, _vp]
     lib.pv_prune_gather_batch.restype = _i
+    lib.pv_select_topk.argtypes = [_vp, _i, _i, _i, _vp, _vp, _vp, _vp]
+    lib.pv_select_topk.restype = _i
     _lib = lib
     return lib
 
@@ -259,6 +261,39 @@ def pv_prune_gather(src: torch.Tensor, idx: torch.Tensor, *, out: Optional[torch
                              row_bytes, sb, sg, sr, db, dg, dr, _stream(src.device))
     _check("pv_prune_gather", rc, lib)
     return out
+
+
+def pv_select_topk(scores: torch.Tensor, k: int, *, want_rest: bool = False,
+                   want_slot: bool = False, out: Optional[dict] = None):
+    """Top-k of float32 scores [B, n] (or [n]); ties go to the lower index.
+    Returns dict(kept [B,k] int32 ascending, rest [B,n-k] | None,
+    slot_of [B,n] | None), shaped like the input's batch."""
+    lib = load()
+    _contig(scores, "scores")
+    if scores.dtype != torch.float32:
+        raise TypeError("scores must be float32")
+    flat = scores.dim() == 1
+    s2 = scores.view(1, -1) if flat else scores
+    B, n = s2.shape
+    dev = scores.device
+    o = out if out is not None else {}
+
+    def buf(name, want, shape):
+        if not want:
+            return None
+        t = o.get(name)
+        return t if t is not None else torch.empty(shape, dtype=torch.int32, device=dev)
+
+    kept = buf("kept", True, (B, k))
+    rest = buf("rest", want_rest, (B, n - k))
+    slot = buf("slot_of", want_slot, (B, n))
+    rc = lib.pv_select_topk(s2.data_ptr(), B, n, int(k), kept.data_ptr(), _ptr(rest), _ptr(slot),
+                            _stream(dev))
+    _check("pv_select_topk", rc, lib)
+    res = {"kept": kept, "rest": rest, "slot_of": slot}
+    if flat:
+        res = {key: (v.view(-1) if v is not None else None) for key, v in res.items()}
+    return res
 
 
 def pv_prune_gather_batch(srcs: Sequence[torch.Tensor], idx: torch.Tensor, *,

@@ -152,3 +152,17 @@ def test_gather_batch_validation(lib):
     d[1].row_bytes = 256
     d[1].dst = None
     assert g(d, 2, FAKE, 1, 4, None) == -1
+
+
+def test_select_topk_validation(lib):
+    t = lib.pv_select_topk
+    assert t(None, 1, 8, 4, FAKE, None, None, None) == -1
+    assert t(FAKE, 1, 8, 4, None, None, None, None) == -1
+    assert t(FAKE, 0, 8, 4, FAKE, None, None, None) == -2
+    assert t(FAKE, 1, 0, 1, FAKE, None, None, None) == -2
+    assert t(FAKE, 1, 16385, 4, FAKE, None, None, None) == -2
+    assert t(FAKE, 1, 8, 0, FAKE, None, None, None) == -3
+    assert t(FAKE, 1, 8, 9, FAKE, None, None, None) == -3
+    assert t(FAKE + 4, 1, 8, 4, FAKE, None, None, None) == -8
+    assert t(FAKE, 1, 8, 4, FAKE, FAKE + 8, None, None) == -8
+    assert t(FAKE, 1, 8, 4, FAKE, None, FAKE + 12, None) == -8
