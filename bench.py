@@ -13,11 +13,12 @@ workload (B=1, 576 visual tokens, d=4096, 32 heads x 128, 64 text rows,
 
 Inputs are seeded synthetic tensors already resident in HBM.  The timed
 region replays the step captured as one HIP graph K times between two HIP
-events (the step is launch-bound at this size).  A second, eager pass over
-the same steps records a HIP event pair around every kernel (through the
-*_timed entry points) for the per-kernel breakdown and the roofline of the
-dominant kernel.  The CPU oracle is timed on a bounded sample of the same
-workload on the host.
+events (the step is launch-bound at this size).  Then every kernel of the
+step is launched back to back between two HIP events on the library's
+stream (the *_timed entry points with reps > 1) for its average duration,
+which gives the per-kernel and per-stage roofline positions and the
+roofline of the dominant kernel.  The CPU oracle is timed on a bounded
+sample of the same workload on the host.
 
 Prints one JSON line.
 """
@@ -26,7 +27,6 @@ from __future__ import annotations
 
 import argparse
 import json
-import math
 import os
 import sys
 import time
@@ -50,15 +50,19 @@ def parse():
     ap.add_argument("--workload", type=int, default=2, help="workload id (2 = LLaVA-1.5-7B)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="budget of the CPU-oracle baseline leg (0 disables it)")
-    ap.add_argument("--eager-steps", type=int, default=200)
+    ap.add_argument("--kernel-reps", type=int, default=20,
+                    help="back-to-back launches of each kernel per timing sample")
+    ap.add_argument("--kernel-iters", type=int, default=10, help="timing samples per kernel")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--split", action="store_true",
+                    help="time the step with the merge branch on a second stream")
     return ap.parse_args()
 
 
 class Step:
     """Buffers and the kernel sequence of one step (all preallocated)."""
 
-    def __init__(self, w, dev):
+    def __init__(self, w, dev, split=False):
         import torch
 
         from paper_2608_25332_amd import provip
@@ -97,57 +101,47 @@ class Step:
         self.ws2 = torch.empty(provip.pv_head_aware_workspace_bytes(B, H, s.Nt, N1, hd,
                                                                     self.heads.shape[1], N2, code),
                                dtype=torch.uint8, device=dev)
+        # second stream (default priority) and the fork/join events of the
+        # two-stream step; torch creates a HIP event on its first record
+        self.split = split
+        self.side = torch.cuda.Stream(dev)
+        self.ev_sel = torch.cuda.Event()
+        self.ev_done = torch.cuda.Event()
+        self.ev_sel.record()
+        self.ev_done.record()
+        torch.cuda.synchronize()
 
-    def run(self, ev=None):
-        """Enqueue one step.  With ev (a list of torch events) every kernel is
-        bracketed: returns the list of (name, start_event, end_event)."""
-        pv = self.pv
-        marks = []
-        n1 = Step.DEDUP_EVENTS
-        e1 = ev[:n1] if ev else None
-        r = pv.pv_prune_dedup(self.vis, self.anc, self.w.N1, out=self.o1, workspace=self.ws1,
-                              events=e1)
-        if ev:
-            for i, nm in enumerate(r["kernel_names"]):
-                marks.append((nm, ev[i], ev[i + 1]))
-        base = n1
-        seq = [
-            ("gather_kv1", lambda: pv.pv_prune_gather_batch([self.kf, self.vf], self.o1["kept"],
-                                                            outs=[self.k1, self.v1])),
-        ]
-        for nm, fn in seq:
-            if ev:
-                ev[base].record()
-            fn()
-            if ev:
-                ev[base + 1].record()
-                marks.append((nm, ev[base], ev[base + 1]))
-                base += 2
-        e2 = ev[base:base + Step.HEAD_EVENTS] if ev else None
-        h = pv.pv_prune_head_aware(self.q, self.k1, self.heads, self.w.N2, out=self.o2,
-                                   workspace=self.ws2, events=e2)
-        if ev:
-            for i, nm in enumerate(h["kernel_names"]):
-                marks.append((nm, ev[base + i], ev[base + i + 1]))
-            base += Step.HEAD_EVENTS
-        seq = [
-            ("gather_hkv2", lambda: pv.pv_prune_gather_batch(
-                [self.o1["merged"], self.k1, self.v1], self.o2["kept"],
-                outs=[self.hid2, self.k2, self.v2])),
-        ]
-        for nm, fn in seq:
-            if ev:
-                ev[base].record()
-            fn()
-            if ev:
-                ev[base + 1].record()
-                marks.append((nm, ev[base], ev[base + 1]))
-                base += 2
-        return marks
+    def gather_kv1(self):
+        self.pv.pv_prune_gather_batch([self.kf, self.vf], self.o1["kept"], outs=[self.k1, self.v1])
+
+    def gather_hkv2(self):
+        self.pv.pv_prune_gather_batch([self.o1["merged"], self.k1, self.v1], self.o2["kept"],
+                                      outs=[self.hid2, self.k2, self.v2])
+
+    def run(self):
+        """Enqueue one step on the current stream.  With self.split the
+        nearest-centroid and merge kernels run on a second stream, overlapped
+        with the K/V gather and the head-aware score (they meet again before
+        the final gather, which needs the merged rows)."""
+        pv, w = self.pv, self.w
+        if self.split:
+            cur = self.torch.cuda.current_stream()
+            pv.pv_prune_dedup(self.vis, self.anc, w.N1, out=self.o1, workspace=self.ws1,
+                              split=(self.side, self.ev_sel, self.ev_done))
+            self.gather_kv1()
+            pv.pv_prune_head_aware(self.q, self.k1, self.heads, w.N2, out=self.o2,
+                                   workspace=self.ws2)
+            cur.wait_event(self.ev_done)
+            self.gather_hkv2()
+        else:
+            pv.pv_prune_dedup(self.vis, self.anc, w.N1, out=self.o1, workspace=self.ws1)
+            self.gather_kv1()
+            pv.pv_prune_head_aware(self.q, self.k1, self.heads, w.N2, out=self.o2,
+                                   workspace=self.ws2)
+            self.gather_hkv2()
 
     DEDUP_EVENTS = 8   # up to 7 kernels + 1
     HEAD_EVENTS = 4    # up to 3 kernels + 1
-    N_EVENTS = DEDUP_EVENTS + 2 + HEAD_EVENTS + 2
 
     def snapshot(self):
         return {k: v.clone() for k, v in [("kept1", self.o1["kept"]), ("assign", self.o1["assign"]),
@@ -156,40 +150,169 @@ class Step:
                                           ("k2", self.k2), ("v2", self.v2)]}
 
 
-DEDUP_KERNELS = ("cos_stream", "center", "select", "gram_stream", "gram_tile", "gram_finish",
-                 "merge")
+# kernel -> the stage of the hot path it belongs to
+STAGE_OF = {
+    "cos_partial": "cosine", "cos_reduce": "cosine", "center": "cosine",
+    "select": "select", "gram_partial": "gram", "gram_reduce": "gram", "gram_tile": "gram",
+    "gram_finish": "gram", "merge": "merge", "gather_kv1": "kv_of_kept",
+    "score_partial": "head_aware", "score_select": "head_aware", "gather_hkv2": "gather",
+}
 
 
 def algorithmic(w):
-    """Algorithmic HBM bytes and flops per kernel per launch (one batch): the
-    bytes a kernel must move at least (its inputs read once, its outputs
-    written once) and the flops its step defines."""
+    """Algorithmic HBM bytes and flops per launch (one batch), per kernel and
+    per stage: the bytes a step must move at least (its inputs read once,
+    its outputs written once) and the flops it defines.  Split-k partial
+    sums are an implementation choice and are not counted."""
     s = w.spec
     B, Nv, d, Nt, H, hd, N1, N2 = s.B, s.Nv, s.d, s.Nt, s.H, s.hd, w.N1, w.N2
     nh = w.heads.shape[1]
     e = 2 if w.dtype == "bf16" else 4
     Mp = Nv - N1
-    gram = dict(bytes=B * Nv * d * e, flops=2.0 * B * Mp * N1 * d)
-    return {
-        # cosine: read the visual tokens and the anchors once, write M
-        "cos_stream": dict(bytes=B * (Nv + Nt) * d * e + B * Nt * Nv * 4, flops=2.0 * B * Nt * Nv * d),
+    gram_flops = 2.0 * B * Mp * N1 * d
+    kern = {
+        # cosine products: read the visual tokens and the anchors once
+        "cos_partial": dict(bytes=B * (Nv + Nt) * d * e, flops=2.0 * B * Nt * Nv * d),
+        # cosines: write M and the inverse token norms
+        "cos_reduce": dict(bytes=B * (Nt * Nv + Nv) * 4, flops=3.0 * B * Nt * Nv),
         # centring + max-pool: read M, write p
         "center": dict(bytes=B * (Nt * Nv + Nv) * 4, flops=2.0 * B * Nt * Nv),
         # top-N1: read p, write kept / pruned / slots
         "select": dict(bytes=B * Nv * 4 * 3, flops=0.0),
         # Gram: read every visual token once (pruned rows and kept rows)
-        "gram_stream": gram, "gram_tile": gram,
+        "gram_partial": dict(bytes=B * Nv * d * e, flops=gram_flops),
+        "gram_tile": dict(bytes=B * Nv * d * e, flops=gram_flops),
+        # argmax: read the inverse norms, write the assignment
+        "gram_reduce": dict(bytes=B * Nv * 4 * 2, flops=1.0 * B * Mp * N1),
         "gram_finish": dict(bytes=B * Mp * 4 * 2, flops=0.0),
         # merge: read every visual token once, write the N1 centroids
         "merge": dict(bytes=B * (Nv + N1) * d * e, flops=1.0 * B * Nv * d),
         # read + write the K and V rows of the N1 kept tokens
         "gather_kv1": dict(bytes=2 * 2 * B * H * N1 * hd * e, flops=0.0),
         # score: Q and K of the selected heads only
-        "score_partial": dict(bytes=B * nh * (Nt + N1) * hd * e, flops=2.0 * 2 * B * nh * Nt * N1 * hd),
-        "score_select": dict(bytes=B * N1 * 4, flops=0.0),
+        "score_partial": dict(bytes=B * nh * (Nt + N1) * hd * e,
+                              flops=2.0 * 2 * B * nh * Nt * N1 * hd),
+        "score_select": dict(bytes=B * N1 * 4 * 2, flops=0.0),
         # read + write the hidden, K and V rows of the N2 kept tokens
         "gather_hkv2": dict(bytes=2 * B * N2 * (d + 2 * H * hd) * e, flops=0.0),
     }
+    stage = {
+        "cosine": dict(bytes=B * (Nv + Nt) * d * e + B * Nv * 4, flops=2.0 * B * Nt * Nv * d),
+        "select": kern["select"],
+        "gram": dict(bytes=B * Nv * d * e + B * Nv * 4, flops=gram_flops),
+        "merge": kern["merge"],
+        "kv_of_kept": kern["gather_kv1"],
+        "head_aware": dict(bytes=B * nh * (Nt + N1) * hd * e + B * N2 * 4,
+                           flops=kern["score_partial"]["flops"]),
+        "gather": kern["gather_hkv2"],
+    }
+    return kern, stage
+
+
+def roof(a, sec):
+    """Roofline position of work a (bytes, flops) done in sec seconds: bound
+    by MFMA when its arithmetic intensity is above the bf16 ridge, else HBM."""
+    ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    ai = a["flops"] / a["bytes"] if a["bytes"] else float("inf")
+    if ai >= ridge:
+        r = {"bound": "mfma", "achieved": a["flops"] / sec / 1e12, "peak": BF16_PEAK_TFLOPS,
+             "unit": "TFLOP/s"}
+    else:
+        r = {"bound": "hbm", "achieved": a["bytes"] / sec / 1e9, "peak": HBM_PEAK_GBS,
+             "unit": "GB/s"}
+    r["frac"] = r["achieved"] / r["peak"]
+    return r
+
+
+def sleep_cycles_for(torch, ms):
+    """Argument of torch.cuda._sleep that keeps the GPU busy for about ms."""
+    a = torch.cuda.Event(enable_timing=True)
+    z = torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(1000)
+    a.record()
+    torch.cuda._sleep(1_000_000)
+    z.record()
+    torch.cuda.synchronize()
+    per_ms = 1_000_000 / max(a.elapsed_time(z), 1e-3)
+    return int(per_ms * ms)
+
+
+def kernel_times(torch, step, reps, iters):
+    """Average duration of every kernel of the step: the kernels of each call
+    are launched reps times back to back between two HIP events recorded on
+    the stream the library launches on (the current stream).  A spin kernel
+    queued first keeps the GPU behind the host, so the launches run back to
+    back rather than at the host's pace."""
+    pv = step.pv
+    per = {}
+    hold = sleep_cycles_for(torch, 4.0 + 0.05 * reps * 11)
+    for _ in range(iters):
+        e1 = [torch.cuda.Event(enable_timing=True) for _ in range(Step.DEDUP_EVENTS)]
+        e2 = [torch.cuda.Event(enable_timing=True) for _ in range(Step.HEAD_EVENTS)]
+        g1 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        g2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        for e in e1 + e2 + g1 + g2:  # torch creates the HIP event on first record
+            e.record()
+        torch.cuda.synchronize()
+        torch.cuda._sleep(hold)
+        r1 = pv.pv_prune_dedup(step.vis, step.anc, step.w.N1, out=step.o1, workspace=step.ws1,
+                               events=e1, reps=reps)
+        g1[0].record()
+        for _ in range(reps):
+            step.gather_kv1()
+        g1[1].record()
+        r2 = pv.pv_prune_head_aware(step.q, step.k1, step.heads, step.w.N2, out=step.o2,
+                                    workspace=step.ws2, events=e2, reps=reps)
+        g2[0].record()
+        for _ in range(reps):
+            step.gather_hkv2()
+        g2[1].record()
+        torch.cuda.synchronize()
+        marks = [(nm, e1[i], e1[i + 1]) for i, nm in enumerate(r1["kernel_names"])]
+        marks += [("gather_kv1", g1[0], g1[1])]
+        marks += [(nm, e2[i], e2[i + 1]) for i, nm in enumerate(r2["kernel_names"])]
+        marks += [("gather_hkv2", g2[0], g2[1])]
+        for nm, a, b in marks:
+            per.setdefault(nm, []).append(a.elapsed_time(b) * 1000.0 / reps)
+    return {k: float(np.median(v)) for k, v in per.items()}
+
+
+def csrc_digest():
+    """Digest of the library sources: counter figures taken from a build with
+    another digest no longer describe the kernels."""
+    import hashlib
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, "paper_2608_25332_amd", "csrc")
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload, kernel):
+    """HBM bytes per launch of `kernel` from the committed PMC summary of this
+    workload (FETCH_SIZE and WRITE_SIZE, scaled by a copy kernel of known
+    size), or None when there is none or the sources changed since."""
+    path = os.path.join(ROOT, "profiles", f"pmc_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    txt = open(path).read()
+    i = txt.find("```json")
+    if i < 0:
+        return None
+    j = txt.find("```", i + 7)
+    try:
+        rec = json.loads(txt[i + 7:j])
+    except ValueError:
+        return None
+    if rec.get("csrc_digest") != csrc_digest():
+        return None
+    k = rec.get("kernels", {}).get(kernel)
+    if not k:
+        return None
+    return float(k["fetch_bytes"]) + float(k["write_bytes"])
 
 
 def graph_time_us(torch, fn, reps=300):
@@ -285,7 +408,7 @@ def main():
     torch.cuda.set_device(dev)
     w = W.make_workload(args.workload)
     s = w.spec
-    step = Step(w, dev)
+    step = Step(w, dev, split=args.split)
     stream = torch.cuda.current_stream(dev)
 
     # eager reference outputs
@@ -332,63 +455,46 @@ def main():
     ms_total = t_start.elapsed_time(t_end)
     ms_per_step = ms_total / args.steps
 
-    # ---- eager pass with an event pair around every kernel
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(Step.N_EVENTS)]
-           for _ in range(args.eager_steps)]
-    for row in evs:          # torch creates the HIP event on first record
-        for e in row:
-            e.record()
-    torch.cuda.synchronize()
-    all_marks = []
-    e_start = torch.cuda.Event(enable_timing=True)
-    e_end = torch.cuda.Event(enable_timing=True)
-    e_start.record()
-    for i in range(args.eager_steps):
-        # keep the GPU behind the host so each event is stamped when the GPU
-        # reaches it, not while it waits for the next launch
-        torch.cuda._sleep(2_000_000)
-        all_marks.append(step.run(evs[i]))
-    e_end.record()
-    torch.cuda.synchronize()
-    per = {}
-    for marks in all_marks:
-        for nm, a, b in marks:
-            per.setdefault(nm, []).append(a.elapsed_time(b) * 1000.0)
-    kern_us = {k: float(np.mean(v)) for k, v in per.items()}
-    kern_p50 = {k: float(np.median(v)) for k, v in per.items()}
-    stage_us = {
-        "dedup": sum(kern_us[k] for k in DEDUP_KERNELS if k in kern_us),
-        "kv_of_kept": kern_us["gather_kv1"],
-        "head_aware": kern_us["score_partial"] + kern_us["score_select"],
-        "gather": kern_us["gather_hkv2"],
-    }
+    # ---- per-kernel durations (each kernel launched back to back between events)
+    kern_us = kernel_times(torch, step, args.kernel_reps, args.kernel_iters)
     breakdown = stage_breakdown(torch, step)
+
+    def other():
+        step.split = not args.split
+        try:
+            step.run()
+        finally:
+            step.split = args.split
+    breakdown["step_two_streams" if not args.split else "step_single_stream"] = graph_time_us(
+        torch, other)
     step.run()
     torch.cuda.synchronize()
-    # last replay/eager output still matches
+    # the outputs after all of the above still match the first eager step
     snap = step.snapshot()
     for k in ref:
         if not torch.equal(ref[k], snap[k]):
             raise RuntimeError(f"benchmark output drifted in {k}")
 
-    alg = algorithmic(w)
+    alg_k, alg_s = algorithmic(w)
+    kernels = {}
+    for k, us in kern_us.items():
+        r = roof(alg_k[k], us * 1e-6)
+        kernels[k] = {"us": us, "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"],
+                      "frac": r["frac"]}
+    stage_us = {}
+    for k, us in kern_us.items():
+        stage_us[STAGE_OF[k]] = stage_us.get(STAGE_OF[k], 0.0) + us
+    stages = {}
+    for st_name, us in stage_us.items():
+        r = roof(alg_s[st_name], us * 1e-6)
+        stages[st_name] = {"us": us, "bound": r["bound"], "achieved": r["achieved"],
+                           "unit": r["unit"], "frac": r["frac"]}
     dom = max(kern_us, key=lambda k: kern_us[k])
-    a = alg[dom]
-    sec = kern_us[dom] * 1e-6
-    ai = a["flops"] / a["bytes"] if a["bytes"] else float("inf")
-    ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
-    if ai >= ridge:
-        roof = {"bound": "mfma", "achieved": a["flops"] / sec / 1e12, "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s"}
-    else:
-        roof = {"bound": "hbm", "achieved": a["bytes"] / sec / 1e9, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s"}
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = None
-    roof["kernel"] = dom
-    roof["kernel_us"] = kern_us[dom]
-    roof["algorithmic_bytes"] = a["bytes"]
-    roof["algorithmic_flops"] = a["flops"]
+    a = alg_k[dom]
+    rf = roof(a, kern_us[dom] * 1e-6)
+    traffic = load_traffic(s.name, dom)
+    rf.update({"traffic": traffic, "kernel": dom, "kernel_us": kern_us[dom],
+               "algorithmic_bytes": a["bytes"], "algorithmic_flops": a["flops"]})
 
     toks = s.B * s.Nv
     value = toks / (ms_per_step * 1e-3)
@@ -407,13 +513,15 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "B": s.B, "Nv": s.Nv, "d": s.d, "H": s.H, "hd": s.hd,
                    "Nt": s.Nt, "heads_per_sample": int(w.heads.shape[1]), "N1": w.N1, "N2": w.N2,
-                   "timing": "hip-graph replay of the full step" if graph is not None else "eager"},
-        "latency_us": {"pipeline": ms_per_step * 1000.0,
-                       "pipeline_eager_evented": e_start.elapsed_time(e_end) * 1000.0 / args.eager_steps,
-                       "stages_eager": stage_us, "kernels_eager_mean": kern_us,
-                       "kernels_eager_p50": kern_p50,
-                       "stages_graph_replay": breakdown},
-        "roofline": roof,
+                   "timing": ("hip-graph replay of the full step" +
+                              (", merge branch on a second stream" if args.split else "")
+                              if graph is not None else "eager")},
+        "latency_us": {"pipeline": ms_per_step * 1000.0, "kernels": kern_us,
+                       "stages": stage_us, "calls_graph_replay": breakdown},
+        "roofline": rf,
+        "roofline_kernels": kernels,
+        "roofline_stages": stages,
+        "csrc_digest": csrc_digest(),
     }
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)

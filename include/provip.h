@@ -103,6 +103,31 @@ int pv_prune_dedup(const void *vis, const void *anchors, int B, int Nv, int Nt, 
                    void *merged, void *workspace, size_t workspace_bytes, void *stream);
 
 /* -------------------------------------------------------------------------
+ * pv_prune_dedup on two streams.  In Sec. 4.3 the retained set depends only
+ * on the cosine scores; the aggregation of the pruned tokens into their
+ * nearest retained token comes after it and nothing else in the step needs
+ * it until the kept rows are gathered.  This variant lets that aggregation
+ * overlap later work on `stream` (e.g. the layers up to the pruning layer,
+ * or pv_prune_head_aware):
+ *   - the cosine, centring, max-pool and top-N_1 kernels run on `stream`;
+ *     then `selected` is recorded on `stream`;
+ *   - `merge_stream` waits for `selected`; the nearest-centroid and merge
+ *     kernels run on `merge_stream`; then `merged_done` is recorded there.
+ * kept and score are ordered on `stream` as usual; assign and merged are
+ * ready only once `merged_done` has completed (make the consumer's stream
+ * wait for it).  Until then the call still reads `workspace`, `vis` and
+ * `kept`: a later call must not reuse that workspace, nor overwrite vis or
+ * kept, before `merged_done`.  selected and merged_done are hipEvent_t
+ * handles owned by the caller; merge_stream is a hipStream_t (it may equal
+ * stream).  Results are bit-identical to pv_prune_dedup.  Errors as
+ * pv_prune_dedup, plus PV_ERR_NULL if merge_stream or an event is NULL.
+ * ---------------------------------------------------------------------- */
+int pv_prune_dedup_split(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
+                         int dtype, int budget, int32_t *kept, float *score, int32_t *assign,
+                         void *merged, void *workspace, size_t workspace_bytes, void *stream,
+                         void *merge_stream, void *selected, void *merged_done);
+
+/* -------------------------------------------------------------------------
  * Head-aware pruning at a pruning layer (Sec. 4.4, equations for S^vis and v).
  *
  * Per sample b, with V_b = heads_host[b*n_heads .. b*n_heads + n_heads):
@@ -190,21 +215,27 @@ int pv_prune_gather_batch(const pv_gather_desc *descs, int n_desc, const int32_t
  * Timed variants, for profiling.  Same arguments and results as the calls
  * above, plus an array of hipEvent_t handles: events[i] is recorded on
  * `stream` just before the i-th kernel the call launches and events[n] just
- * after the last one, for n = min(n_events - 1, number of kernels).  The
- * number of kernels a call launches is returned through *n_kernels and their
- * names (static strings, at most n_events - 1 of them) through names; both
- * may be NULL.  Passing n_events = 0 records nothing.
+ * after the last one, for n = min(n_events - 1, number of kernels).  With
+ * reps > 1 every kernel is launched reps times back to back between its two
+ * events (the results are unchanged: no kernel reads what it writes), so
+ * that elapsed(events[i], events[i+1]) / reps is the kernel's average
+ * duration in a stream of its own launches.  The number of kernels a call
+ * launches is returned through *n_kernels and their names (static strings,
+ * at most n_events - 1 of them) through names; both may be NULL.  Passing
+ * n_events = 0 records nothing.  reps < 1 gives PV_ERR_SHAPE; a NULL handle
+ * among events[0 .. n_events) gives PV_ERR_NULL (nothing is enqueued).
  * ---------------------------------------------------------------------- */
 int pv_prune_dedup_timed(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
                          int dtype, int budget, int32_t *kept, float *score, int32_t *assign,
                          void *merged, void *workspace, size_t workspace_bytes, void *stream,
-                         void *const *events, int n_events, int *n_kernels, const char **names);
+                         void *const *events, int n_events, int reps, int *n_kernels,
+                         const char **names);
 
 int pv_prune_head_aware_timed(const void *q, const void *k, const int32_t *heads_host,
                               int n_heads, int B, int H, int Nt, int N, int hd, int dtype,
                               int budget, int32_t *kept, float *score, void *workspace,
                               size_t workspace_bytes, void *stream, void *const *events,
-                              int n_events, int *n_kernels, const char **names);
+                              int n_events, int reps, int *n_kernels, const char **names);
 
 #ifdef __cplusplus
 }

@@ -31,24 +31,40 @@ struct Carve {
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
-// Records events[i] before kernel i and events[n] after the last kernel.
+// Launches the kernels of one call.  With events, events[i] is recorded
+// before kernel i and events[n] after the last one; with reps > 1 every
+// kernel is launched reps times back to back between its two events (the
+// kernels are idempotent: none reads what it writes).
 struct Trace {
     void *const *ev;
     int n_ev;
     const char **names;
-    int launched = 0;
+    int reps;
     hipStream_t st;
-    void before(const char *name) {
+    int launched = 0;
+    // every handle a call may record must exist (checked before any launch)
+    bool handles_ok() const {
+        for (int i = 0; ev && i < n_ev; ++i)
+            if (!ev[i]) return false;
+        return true;
+    }
+    template <typename F>
+    bool launch(const char *name, F f) {
         if (ev && launched < n_ev - 1) {
-            (void)hipEventRecord((hipEvent_t)ev[launched], st);
+            if (hipEventRecord((hipEvent_t)ev[launched], st) != hipSuccess) return false;
             if (names) names[launched] = name;
         }
+        for (int r = 0; r < reps; ++r)
+            if (f() != hipSuccess) return false;
+        ++launched;
+        return true;
     }
-    void after_all() {
+    bool after_all() {
         if (ev && launched >= 1 && n_ev >= 1) {
             int i = launched < n_ev - 1 ? launched : n_ev - 1;
-            (void)hipEventRecord((hipEvent_t)ev[i], st);
+            return hipEventRecord((hipEvent_t)ev[i], st) == hipSuccess;
         }
+        return true;
     }
 };
 
@@ -124,10 +140,20 @@ int check_dedup(const void *vis, const void *anchors, int B, int Nv, int Nt, int
     return PV_OK;
 }
 
+// Second stream of pv_prune_dedup_split: the assignment and merge kernels run
+// there, after `selected` (recorded on the main stream once the kept list
+// exists); `merged_done` is recorded there after the last of them.
+struct Fork {
+    hipStream_t stream;
+    hipEvent_t selected;
+    hipEvent_t merged_done;
+};
+
 int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int d, int dtype,
                int budget, int32_t *kept, float *score, int32_t *assign, void *merged,
                void *workspace, size_t ws_bytes, void *stream, void *const *events, int n_events,
-               int *n_kernels, const char **names) {
+               int reps, int *n_kernels, const char **names, const Fork *fork = nullptr) {
+    if (reps < 1) return PV_ERR_SHAPE;
     int rc = check_dedup(vis, anchors, B, Nv, Nt, d, dtype, budget, kept);
     if (rc != PV_OK) return rc;
     const bool need_assign = assign != nullptr || merged != nullptr;
@@ -147,52 +173,69 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     int32_t *asg = assign ? assign : P.assign;
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
     hipStream_t st = (hipStream_t)stream;
-    Trace tr{events, n_events, names, 0, st};
-    auto step = [&](hipError_t err) {
-        ++tr.launched;
-        return err == hipSuccess;
-    };
-    tr.before("cos_partial");
-    if (!step(pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart, P.ssv,
-                                     P.ssa, st)))
+    Trace tr{events, n_events, names, reps, st};
+    if (!tr.handles_ok()) return PV_ERR_NULL;
+    if (!tr.launch("cos_partial", [&] {
+            return pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart, P.ssv,
+                                          P.ssa, st);
+        }))
         return PV_ERR_HIP;
-    tr.before("cos_reduce");
-    if (!step(pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M, P.rowsum,
-                                    P.invn, st)))
+    if (!tr.launch("cos_reduce", [&] {
+            return pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M, P.rowsum,
+                                         P.invn, st);
+        }))
         return PV_ERR_HIP;
-    tr.before("center");
-    if (!step(pv::launch_center(P.M, P.rowsum, P.njt, B, Nt, Nv, p, st))) return PV_ERR_HIP;
-    tr.before("select");
-    if (!step(pv::launch_select(p, B, Nv, budget, kept, P.pruned, need_assign ? asg : nullptr, st)))
+    if (!tr.launch("center", [&] {
+            return pv::launch_center(P.M, P.rowsum, P.njt, B, Nt, Nv, p, st);
+        }))
         return PV_ERR_HIP;
+    if (!tr.launch("select", [&] {
+            return pv::launch_select(p, B, Nv, budget, kept, P.pruned, need_assign ? asg : nullptr,
+                                     st);
+        }))
+        return PV_ERR_HIP;
+    hipStream_t sm = st;  // stream of the assignment and merge kernels
+    if (fork) {
+        if (hipEventRecord(fork->selected, st) != hipSuccess ||
+            hipStreamWaitEvent(fork->stream, fork->selected, 0) != hipSuccess)
+            return PV_ERR_HIP;
+        sm = fork->stream;
+    }
     if (need_assign && P.Mp > 0) {
         if (P.gram_big) {
-            tr.before("gram_tile");
-            if (!step(pv::launch_gram_tile(dt, vis, B, Nv, d, kept, budget, P.pruned, P.Mp, P.invn,
-                                           P.best_val, P.best_slot, asg, st)))
+            if (!tr.launch("gram_tile", [&] {
+                    return pv::launch_gram_tile(dt, vis, B, Nv, d, kept, budget, P.pruned, P.Mp,
+                                                P.invn, P.best_val, P.best_slot, asg, sm);
+                }))
                 return PV_ERR_HIP;
             if (P.ntn > 1) {
-                tr.before("gram_finish");
-                if (!step(pv::launch_gram_finish(P.best_val, P.best_slot, B, P.ntn, P.Mp, Nv,
-                                                 P.pruned, asg, st)))
+                if (!tr.launch("gram_finish", [&] {
+                        return pv::launch_gram_finish(P.best_val, P.best_slot, B, P.ntn, P.Mp, Nv,
+                                                      P.pruned, asg, sm);
+                    }))
                     return PV_ERR_HIP;
             }
         } else {
-            tr.before("gram_partial");
-            if (!step(pv::launch_gram_partial(dt, vis, B, Nv, d, kept, budget, P.pruned, P.Mp,
-                                              P.ks_gram, P.gpart, st)))
+            if (!tr.launch("gram_partial", [&] {
+                    return pv::launch_gram_partial(dt, vis, B, Nv, d, kept, budget, P.pruned, P.Mp,
+                                                   P.ks_gram, P.gpart, sm);
+                }))
                 return PV_ERR_HIP;
-            tr.before("gram_reduce");
-            if (!step(pv::launch_gram_reduce(P.gpart, B, P.Mp, budget, Nv, P.ks_gram, P.invn,
-                                             P.pruned, kept, asg, st)))
+            if (!tr.launch("gram_reduce", [&] {
+                    return pv::launch_gram_reduce(P.gpart, B, P.Mp, budget, Nv, P.ks_gram, P.invn,
+                                                  P.pruned, kept, asg, sm);
+                }))
                 return PV_ERR_HIP;
         }
     }
     if (merged) {
-        tr.before("merge");
-        if (!step(pv::launch_merge(dt, vis, B, Nv, d, budget, asg, merged, st))) return PV_ERR_HIP;
+        if (!tr.launch("merge", [&] {
+                return pv::launch_merge(dt, vis, B, Nv, d, budget, asg, merged, sm);
+            }))
+            return PV_ERR_HIP;
     }
-    tr.after_all();
+    if (fork && hipEventRecord(fork->merged_done, sm) != hipSuccess) return PV_ERR_HIP;
+    if (!tr.after_all()) return PV_ERR_HIP;
     if (n_kernels) *n_kernels = tr.launched;
     return PV_OK;
 }
@@ -237,8 +280,9 @@ int check_head(const void *q, const void *k, const int32_t *heads, int n_heads, 
 
 int head_impl(const void *q, const void *k, const int32_t *heads, int n_heads, int B, int H, int Nt,
               int N, int hd, int dtype, int budget, int32_t *kept, float *score, void *workspace,
-              size_t ws_bytes, void *stream, void *const *events, int n_events, int *n_kernels,
-              const char **names) {
+              size_t ws_bytes, void *stream, void *const *events, int n_events, int reps,
+              int *n_kernels, const char **names) {
+    if (reps < 1) return PV_ERR_SHAPE;
     int rc = check_head(q, k, heads, n_heads, B, H, Nt, N, hd, dtype, budget, kept);
     if (rc != PV_OK) return rc;
     HeadPlan P0 = plan_head(nullptr, B, Nt, N, n_heads, score == nullptr);
@@ -250,23 +294,24 @@ int head_impl(const void *q, const void *k, const int32_t *heads, int n_heads, i
     float *v = score ? score : P.v;
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
     hipStream_t st = (hipStream_t)stream;
-    Trace tr{events, n_events, names, 0, st};
+    Trace tr{events, n_events, names, reps, st};
+    if (!tr.handles_ok()) return PV_ERR_NULL;
 
     pv::HeadArgs ha;
     memset(&ha, 0, sizeof(ha));
     memcpy(ha.h, heads, sizeof(int32_t) * (size_t)B * n_heads);
 
-    tr.before("score_partial");
-    if (pv::launch_score_partial(dt, q, k, ha, B, H, Nt, N, hd, n_heads, P.partial, st) != hipSuccess)
+    if (!tr.launch("score_partial", [&] {
+            return pv::launch_score_partial(dt, q, k, ha, B, H, Nt, N, hd, n_heads, P.partial, st);
+        }))
         return PV_ERR_HIP;
-    ++tr.launched;
-    tr.before("score_select");
     const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
-    if (pv::launch_score_select(P.partial, B, n_heads * P.nrb, N, inv_norm, v, budget, kept, st) !=
-        hipSuccess)
+    if (!tr.launch("score_select", [&] {
+            return pv::launch_score_select(P.partial, B, n_heads * P.nrb, N, inv_norm, v, budget,
+                                           kept, st);
+        }))
         return PV_ERR_HIP;
-    ++tr.launched;
-    tr.after_all();
+    if (!tr.after_all()) return PV_ERR_HIP;
     if (n_kernels) *n_kernels = tr.launched;
     return PV_OK;
 }
@@ -301,16 +346,27 @@ PV_API int pv_prune_dedup(const void *vis, const void *anchors, int B, int Nv, i
                           int dtype, int budget, int32_t *kept, float *score, int32_t *assign,
                           void *merged, void *workspace, size_t workspace_bytes, void *stream) {
     return dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, budget, kept, score, assign, merged,
-                      workspace, workspace_bytes, stream, nullptr, 0, nullptr, nullptr);
+                      workspace, workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr);
 }
 
 PV_API int pv_prune_dedup_timed(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
                                 int dtype, int budget, int32_t *kept, float *score,
                                 int32_t *assign, void *merged, void *workspace,
                                 size_t workspace_bytes, void *stream, void *const *events,
-                                int n_events, int *n_kernels, const char **names) {
+                                int n_events, int reps, int *n_kernels, const char **names) {
     return dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, budget, kept, score, assign, merged,
-                      workspace, workspace_bytes, stream, events, n_events, n_kernels, names);
+                      workspace, workspace_bytes, stream, events, n_events, reps, n_kernels, names);
+}
+
+PV_API int pv_prune_dedup_split(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
+                                int dtype, int budget, int32_t *kept, float *score,
+                                int32_t *assign, void *merged, void *workspace,
+                                size_t workspace_bytes, void *stream, void *merge_stream,
+                                void *selected, void *merged_done) {
+    if (!merge_stream || !selected || !merged_done) return PV_ERR_NULL;
+    const Fork f{(hipStream_t)merge_stream, (hipEvent_t)selected, (hipEvent_t)merged_done};
+    return dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, budget, kept, score, assign, merged,
+                      workspace, workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr, &f);
 }
 
 PV_API size_t pv_head_aware_workspace_bytes(int B, int H, int Nt, int N, int hd, int n_heads,
@@ -328,16 +384,16 @@ PV_API int pv_prune_head_aware(const void *q, const void *k, const int32_t *head
                                int32_t *kept, float *score, void *workspace, size_t workspace_bytes,
                                void *stream) {
     return head_impl(q, k, heads_host, n_heads, B, H, Nt, N, hd, dtype, budget, kept, score,
-                     workspace, workspace_bytes, stream, nullptr, 0, nullptr, nullptr);
+                     workspace, workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr);
 }
 
 PV_API int pv_prune_head_aware_timed(const void *q, const void *k, const int32_t *heads_host,
                                      int n_heads, int B, int H, int Nt, int N, int hd, int dtype,
                                      int budget, int32_t *kept, float *score, void *workspace,
                                      size_t workspace_bytes, void *stream, void *const *events,
-                                     int n_events, int *n_kernels, const char **names) {
+                                     int n_events, int reps, int *n_kernels, const char **names) {
     return head_impl(q, k, heads_host, n_heads, B, H, Nt, N, hd, dtype, budget, kept, score,
-                     workspace, workspace_bytes, stream, events, n_events, n_kernels, names);
+                     workspace, workspace_bytes, stream, events, n_events, reps, n_kernels, names);
 }
 
 namespace {

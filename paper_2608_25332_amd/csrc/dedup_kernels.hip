@@ -101,7 +101,7 @@ __global__ __launch_bounds__(256) void cos_partial_kernel(
 // order, forms cos = dot / (|a| |v|) (0 for a zero vector), writes
 // M[b][Nt][Nv], the row sums of M over this workgroup's 64 tokens
 // rowsum[b][Nv/64][Nt] and (first row group) the inverse token norms.
-constexpr int kRedTok = 64, kRedRows = 4;
+constexpr int kRedTok = 64, kRedRows = 4, kRedU = 16;
 
 __global__ __launch_bounds__(256) void cos_reduce_kernel(
     const float *__restrict__ part, const float *__restrict__ ssv, const float *__restrict__ ssa,
@@ -114,13 +114,26 @@ __global__ __launch_bounds__(256) void cos_reduce_kernel(
     const int i = blockIdx.y * kRedRows + wave;
     const int j = jt * kRedTok + lane;
     const int jc = min(j, Nv - 1), ic = min(i, Nt - 1);
+    // slices in blocks of kRedU with clamped (always valid) addresses, so a
+    // block's loads are all in flight at once; added in slice order
     float sv = 0.f, sa = 0.f, dot = 0.f;
-#pragma unroll 8
-    for (int ks = 0; ks < KS; ++ks) {
-        const size_t kb = (size_t)ks * B + b;
-        sv += ssv[kb * Nv + jc];
-        sa += ssa[kb * Nt + ic];
-        dot += part[(kb * Nt + ic) * Nv + jc];
+    for (int ks0 = 0; ks0 < KS; ks0 += kRedU) {
+        float v[kRedU], a[kRedU], p[kRedU];
+#pragma unroll
+        for (int u = 0; u < kRedU; ++u) {
+            const size_t kb = (size_t)min(ks0 + u, KS - 1) * B + b;
+            v[u] = ssv[kb * Nv + jc];
+            a[u] = ssa[kb * Nt + ic];
+            p[u] = part[(kb * Nt + ic) * Nv + jc];
+        }
+#pragma unroll
+        for (int u = 0; u < kRedU; ++u) {
+            if (ks0 + u < KS) {
+                sv += v[u];
+                sa += a[u];
+                dot += p[u];
+            }
+        }
     }
     const float inv_v = (sv > 0.f) ? 1.0f / sqrtf(sv) : 0.f;
     const float inv_a = (sa > 0.f) ? 1.0f / sqrtf(sa) : 0.f;
@@ -274,26 +287,56 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(
 // gram_reduce: grid (ceil(Mp / 2), B), 128 threads, one wave per pruned row.
 // Adds the k slices in slice order, forms the cosine to every kept token and
 // writes the slot of the best one (higher cosine, then lower slot).
+constexpr int kGramU = 16;
+
 __global__ __launch_bounds__(128) void gram_reduce_kernel(
     const float *__restrict__ part, int B, int Mp, int N1, int Nv, int KS,
     const float *__restrict__ invn, const int32_t *__restrict__ pruned,
     const int32_t *__restrict__ kept, int32_t *__restrict__ assign) {
+    constexpr int CPL = 4;  // columns per lane per pass
     const int lane = threadIdx.x & 63;
-    const int m = blockIdx.x * 2 + (threadIdx.x >> 6);
+    const int m = blockIdx.x * 2 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int b = blockIdx.y;
     if (m >= Mp) return;
     const int tok = pruned[(size_t)b * Mp + m];
     const float ia = invn[(size_t)b * Nv + tok];
+    const size_t kstride = (size_t)B * Mp * N1;
+    const float *prow = part + ((size_t)b * Mp + m) * N1;
     float bv = -INFINITY;
     int bs = 0x7FFFFFFF;
-    for (int n = lane; n < N1; n += 64) {
-        float dot = 0.f;
-#pragma unroll 8
-        for (int ks = 0; ks < KS; ++ks) dot += part[(((size_t)ks * B + b) * Mp + m) * N1 + n];
-        const float cs = dot * ia * invn[(size_t)b * Nv + kept[(size_t)b * N1 + n]];
-        if (better(cs, n, bv, bs)) {
-            bv = cs;
-            bs = n;
+    for (int n0 = 0; n0 < N1; n0 += 64 * CPL) {
+        int nc[CPL];
+        float kin[CPL], dot[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            nc[c] = min(n0 + c * 64 + lane, N1 - 1);
+            kin[c] = invn[(size_t)b * Nv + kept[(size_t)b * N1 + nc[c]]];
+            dot[c] = 0.f;
+        }
+        // slices in blocks of kGramU with clamped addresses: every load of a
+        // block is in flight at once; added in slice order
+        for (int ks0 = 0; ks0 < KS; ks0 += kGramU) {
+            float v[kGramU][CPL];
+#pragma unroll
+            for (int u = 0; u < kGramU; ++u)
+#pragma unroll
+                for (int c = 0; c < CPL; ++c)
+                    v[u][c] = prow[(size_t)min(ks0 + u, KS - 1) * kstride + nc[c]];
+#pragma unroll
+            for (int u = 0; u < kGramU; ++u)
+                if (ks0 + u < KS) {
+#pragma unroll
+                    for (int c = 0; c < CPL; ++c) dot[c] += v[u][c];
+                }
+        }
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const int n = n0 + c * 64 + lane;
+            const float cs = dot[c] * ia * kin[c];
+            if (n < N1 && better(cs, n, bv, bs)) {
+                bv = cs;
+                bs = n;
+            }
         }
     }
 #pragma unroll
@@ -399,16 +442,20 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
 }
 
 // ----------------------------------------------------------------------------
-// merge: grid (N1, B), 256 threads.  The members of slot s (the tokens whose
-// assignment is s, the kept token itself included) are collected in
-// ascending token order by one wave with ballots over the assignment (staged
-// in LDS when it fits), then all threads add the member rows in that order
-// (fp32), four rows in flight at a time.
+// merge: grid (ceil(d_bytes / 1024), N1, B), 256 threads.  A workgroup owns
+// one slot s and one 1 KB column block (16 bytes per lane).  The members of s
+// (the tokens whose assignment is s, the kept token itself included) are
+// listed in ascending token order with one block scan per round of 4096
+// tokens; the four waves then take every fourth member, so a slot with many
+// members keeps 4 x kMergeU rows in flight instead of a serial chain, and the
+// column split spreads one slot's bytes over several CUs.  Each wave adds its
+// members in list order (fp32) and the four partial sums are combined in wave
+// order, so the result does not depend on timing.
 // ----------------------------------------------------------------------------
 constexpr int kMergeNT = 256;
-constexpr int kMergeCPT = 4;      // 16-byte chunks per thread per pass
-constexpr int kMergeList = 4096;  // members held in LDS per round; also the
-                                  // largest assignment staged in LDS
+constexpr int kMergeRound = 4096;                  // tokens listed per round
+constexpr int kMergeTPT = kMergeRound / kMergeNT;  // tokens per thread per round
+constexpr int kMergeU = 8;                         // member rows in flight per wave
 
 template <int DT>
 __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict__ vis, int Nv,
@@ -416,102 +463,84 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
                                                          const int32_t *__restrict__ assign,
                                                          int N1, char *__restrict__ merged) {
     constexpr int EPC = (DT == kBF16) ? 8 : 4;  // elements per 16-byte chunk
-    __shared__ int list[kMergeList];
-    __shared__ int staged[kMergeList];
-    __shared__ int s_count, s_next;
-    const int s = blockIdx.x, b = blockIdx.y;
+    constexpr int NW = kMergeNT / 64;
+    __shared__ int list[kMergeRound];
+    __shared__ int wsum[NW];
+    __shared__ float part[NW][EPC][64];
+    const int s = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int nchunk = d_bytes / 16;
+    const int nchunk = d_bytes >> 4;
+    const int c = blockIdx.x * 64 + lane;
+    const char *col = vis + (size_t)b * Nv * d_bytes + (size_t)min(c, nchunk - 1) * 16;
     const int32_t *as = assign + (size_t)b * Nv;
-    const char *vb = vis + (size_t)b * Nv * d_bytes;
-    char *out = merged + ((size_t)b * N1 + s) * d_bytes;
-    const bool stage = Nv <= kMergeList;
-    if (stage) {
-        for (int j = tid; j < Nv; j += kMergeNT) staged[j] = as[j];
-        __syncthreads();
-    }
-    const int *src = stage ? (const int *)staged : (const int *)as;
 
-    for (int cbase = 0; cbase < nchunk; cbase += kMergeNT * kMergeCPT) {
-        float acc[kMergeCPT][EPC];
+    float acc[EPC];
 #pragma unroll
-        for (int t = 0; t < kMergeCPT; ++t)
+    for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
+    int total = 0;
+    for (int r0 = 0; r0 < Nv; r0 += kMergeRound) {
+        const int rend = min(r0 + kMergeRound, Nv);
+        const int tpt = (rend - r0 + kMergeNT - 1) / kMergeNT;  // uniform
+        const int t0 = r0 + tid * tpt;
+        int a[kMergeTPT];
 #pragma unroll
-            for (int e = 0; e < EPC; ++e) acc[t][e] = 0.f;
-        int scan_from = 0, total = 0;
-        while (true) {
-            if (wave == 0) {
-                // collect up to kMergeList members from token scan_from on
-                int cnt = 0, pos = scan_from;
-                while (pos < Nv) {
-                    const int a0 = (pos + lane < Nv) ? src[pos + lane] : -1;
-                    const unsigned long long mk = __ballot(a0 == s);
-                    const int nb = __popcll(mk);
-                    if (cnt + nb > kMergeList) break;
-                    if (a0 == s) list[cnt + __popcll(mk & ((1ull << lane) - 1ull))] = pos + lane;
-                    cnt += nb;
-                    pos += 64;
-                }
-                if (lane == 0) {
-                    s_count = cnt;
-                    s_next = pos;
-                }
-            }
-            __syncthreads();
-            const int cnt = s_count;
-            scan_from = s_next;
-            total += cnt;
-            for (int m = 0; m < cnt; m += 4) {
-                uint4 v[4][kMergeCPT];
+        for (int e = 0; e < kMergeTPT; ++e)
+            if (e < tpt) a[e] = as[min(t0 + e, rend - 1)];
+        int mine = 0;
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const char *row = vb + (size_t)list[min(m + u, cnt - 1)] * d_bytes;
+        for (int e = 0; e < kMergeTPT; ++e) mine += (e < tpt && t0 + e < rend && a[e] == s);
+        int cnt;
+        int w = block_excl_scan<kMergeNT>(mine, wsum, &cnt);
 #pragma unroll
-                    for (int t = 0; t < kMergeCPT; ++t) {
-                        const int c = min(cbase + tid + t * kMergeNT, nchunk - 1);
-                        v[u][t] = ld16(row + (size_t)c * 16);
+        for (int e = 0; e < kMergeTPT; ++e)
+            if (e < tpt && t0 + e < rend && a[e] == s) list[w++] = t0 + e;
+        __syncthreads();
+        for (int m0 = wave; m0 < cnt; m0 += NW * kMergeU) {
+            uint4 v[kMergeU];
+#pragma unroll
+            for (int u = 0; u < kMergeU; ++u)
+                v[u] = ld16(col + (size_t)list[min(m0 + u * NW, cnt - 1)] * d_bytes);
+#pragma unroll
+            for (int u = 0; u < kMergeU; ++u) {
+                if (m0 + u * NW >= cnt) break;
+                const uint32_t w4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+                if (DT == kBF16) {
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        acc[2 * q] += __uint_as_float(w4[q] << 16);
+                        acc[2 * q + 1] += __uint_as_float(w4[q] & 0xFFFF0000u);
                     }
-                }
+                } else {
 #pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    if (m + u >= cnt) break;
-#pragma unroll
-                    for (int t = 0; t < kMergeCPT; ++t) {
-                        const uint32_t w4[4] = {v[u][t].x, v[u][t].y, v[u][t].z, v[u][t].w};
-                        if (DT == kBF16) {
-#pragma unroll
-                            for (int q = 0; q < 4; ++q) {
-                                acc[t][2 * q] += __uint_as_float(w4[q] << 16);
-                                acc[t][2 * q + 1] += __uint_as_float(w4[q] & 0xFFFF0000u);
-                            }
-                        } else {
-#pragma unroll
-                            for (int q = 0; q < 4; ++q) acc[t][q] += __uint_as_float(w4[q]);
-                        }
-                    }
+                    for (int q = 0; q < 4; ++q) acc[q] += __uint_as_float(w4[q]);
                 }
             }
-            __syncthreads();
-            if (scan_from >= Nv) break;
         }
-        const float cnt = (float)total;
+        total += cnt;
+        __syncthreads();  // the list is rewritten by the next round
+    }
+    if (wave > 0) {
 #pragma unroll
-        for (int t = 0; t < kMergeCPT; ++t) {
-            const int c = cbase + tid + t * kMergeNT;
-            if (c >= nchunk) continue;
-            uint32_t w4[4];
-            if (DT == kBF16) {
+        for (int e = 0; e < EPC; ++e) part[wave][e][lane] = acc[e];
+    }
+    __syncthreads();
+    if (wave == 0 && c < nchunk) {
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    w4[q] = f32_to_bf16_rne(acc[t][2 * q] / cnt) |
-                            (f32_to_bf16_rne(acc[t][2 * q + 1] / cnt) << 16);
-            } else {
+        for (int w2 = 1; w2 < NW; ++w2)
 #pragma unroll
-                for (int q = 0; q < 4; ++q) w4[q] = __float_as_uint(acc[t][q] / cnt);
-            }
-            st16(out + (size_t)c * 16, uint4{w4[0], w4[1], w4[2], w4[3]});
+            for (int e = 0; e < EPC; ++e) acc[e] += part[w2][e][lane];
+        const float cntf = (float)total;
+        uint32_t w4[4];
+        if (DT == kBF16) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                w4[q] = f32_to_bf16_rne(acc[2 * q] / cntf) | (f32_to_bf16_rne(acc[2 * q + 1] / cntf) << 16);
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) w4[q] = __float_as_uint(acc[q] / cntf);
         }
+        st16(merged + ((size_t)b * N1 + s) * d_bytes + (size_t)c * 16, uint4{w4[0], w4[1], w4[2], w4[3]});
     }
 }
 
@@ -621,7 +650,8 @@ hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, i
 
 hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
                         const int32_t *assign, void *merged, hipStream_t st) {
-    dim3 grid(N1, B);
+    const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
+    const dim3 grid((d_bytes / 16 + 63) / 64, N1, B);
     if (dt == kBF16)
         hipLaunchKernelGGL(merge_kernel<kBF16>, grid, dim3(kMergeNT), 0, st, (const char *)vis, Nv,
                            d * 2, assign, N1, (char *)merged);

@@ -8,11 +8,11 @@
 //
 // score_partial (grid: 16-row blocks x selected heads x B) keeps the 16 query
 // rows of its block in registers as MFMA fragments and streams the head's
-// keys from HBM/L2.  When a wave's share of the keys is at most MAXB blocks of
-// 16 the logits stay in registers between the row statistics and the column
-// sums (one pass over K); otherwise the logits are recomputed in a second
-// pass.  Only the selected heads are ever read and the attention map is never
-// written out.  score_select (one workgroup per sample) adds the per-(head,
+// keys from HBM/L2 through LDS, 64 keys per chunk.  When the chunks number at
+// most MAXC the logits stay in registers between the row statistics and the
+// column sums (one pass over K); otherwise the keys are streamed again in a
+// second pass.  Only the selected heads are ever read and the attention map
+// is never written out.  score_select (one workgroup per sample) adds the per-(head,
 // row-block) column sums in a fixed order and runs the top-N_2.
 #include "pv_launch.h"
 #include "pv_device.h"
@@ -30,23 +30,28 @@ __device__ __forceinline__ void lse_merge(float &m, float &l, float m2, float l2
     m = mn;
 }
 
-template <int DT, int NKS>
-__device__ __forceinline__ f32x4_t qk_block(const uint4 (&qf)[NKS], const char *kb, int col, int N,
-                                            int hd_bytes, int koff) {
-    const char *kr = kb + (size_t)min(col, N - 1) * hd_bytes + koff;
-    uint4 kf[NKS];
-#pragma unroll
-    for (int s = 0; s < NKS; ++s) kf[s] = ld16(kr + s * 64);
-    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < NKS; ++s) acc = mma16<DT>(qf[s], kf[s], acc);
-    return acc;
-}
+// Key rows are staged through LDS 64 at a time (one 16-key block per wave)
+// with row-major 16-byte loads: 4*NKS consecutive lanes read one key row, the
+// access pattern that moves the most bytes per clock into a CU.  The MFMA
+// fragments are then read from LDS.
+constexpr int kScoreCK = 64;  // keys per staged chunk
 
-template <int DT, int NKS, int MAXB>
+template <int NKS>
+struct ScoreStage {
+    static constexpr int RB = 64 * NKS;     // bytes of one key row
+    static constexpr int STRIDE = RB + 16;  // LDS bytes per staged row (16-byte pad)
+    static constexpr int PPR = RB / 16;     // 16-byte pieces per row
+    static constexpr int PPT = kScoreCK * PPR / kScoreNT;  // pieces per thread per chunk
+    static constexpr int LDS = kScoreCK * STRIDE;
+    static_assert(kScoreCK * PPR % kScoreNT == 0, "chunk must fill the loaders evenly");
+};
+
+template <int DT, int NKS, int MAXC>
 __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads, int H, int Nt, int N,
-    int hd_bytes, int n_heads, float scale_log2e, float *__restrict__ partial) {
+    int n_heads, float scale_log2e, float *__restrict__ partial) {
+    using S = ScoreStage<NKS>;
+    __shared__ __attribute__((aligned(16))) char kst[S::LDS];
     __shared__ float sm_m[4][16], sm_l[4][16];
     __shared__ float row_m[16], row_il[16];
     const int rb = blockIdx.x, hi = blockIdx.y, b = blockIdx.z;
@@ -56,64 +61,70 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     // branches (an MFMA does not honour the execution mask)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int h = heads.h[b * n_heads + hi];
-    const char *qb = q + ((size_t)b * H + h) * Nt * hd_bytes;
-    const char *kb = k + ((size_t)b * H + h) * N * hd_bytes;
+    const char *qb = q + ((size_t)b * H + h) * Nt * S::RB;
+    const char *kb = k + ((size_t)b * H + h) * N * S::RB;
     const int koff = (lane >> 4) * 16;
 
     uint4 qf[NKS];
     {
-        const char *qr = qb + (size_t)min(rb * 16 + (lane & 15), Nt - 1) * hd_bytes + koff;
+        const char *qr = qb + (size_t)min(rb * 16 + (lane & 15), Nt - 1) * S::RB + koff;
 #pragma unroll
         for (int s = 0; s < NKS; ++s) qf[s] = ld16(qr + s * 64);
     }
-    const int nblk = (N + 15) / 16;
+    const int nch = (N + kScoreCK - 1) / kScoreCK;
 
-    // pass 1: running (max, sum of exp) of the logits, per lane and row
+    int srow[S::PPT], scol[S::PPT];
+#pragma unroll
+    for (int p = 0; p < S::PPT; ++p) {
+        const int qq = tid + kScoreNT * p;
+        srow[p] = qq / S::PPR;
+        scol[p] = (qq % S::PPR) * 16;
+    }
+    // one pass over the keys: stage chunk ch (the next one is in flight while
+    // this one is multiplied) and hand this wave's 16x16 logit block to body
+    auto sweep = [&](auto body) {
+        uint4 buf[S::PPT];
+        auto fetch = [&](int ch) {
+#pragma unroll
+            for (int p = 0; p < S::PPT; ++p) {
+                const int row = min(ch * kScoreCK + srow[p], N - 1);  // past the end: last key
+                buf[p] = ld16(kb + (size_t)row * S::RB + scol[p]);
+            }
+        };
+        fetch(0);
+        for (int ch = 0; ch < nch; ++ch) {
+            __syncthreads();  // the previous chunk's fragment reads are done
+#pragma unroll
+            for (int p = 0; p < S::PPT; ++p) st16(kst + srow[p] * S::STRIDE + scol[p], buf[p]);
+            __syncthreads();
+            if (ch + 1 < nch) fetch(ch + 1);
+            const char *fr = kst + (wave * 16 + (lane & 15)) * S::STRIDE + koff;
+            f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < NKS; ++s) acc = mma16<DT>(qf[s], ld16(fr + s * 64), acc);
+            body(ch, acc);
+        }
+    };
+
+    // pass 1: running (max, sum of exp) of the logits, per lane and row; with
+    // MAXC > 0 the logit blocks also stay in registers for pass 2
     float m[4], l[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         m[i] = -INFINITY;
         l[i] = 0.f;
     }
-    f32x4_t keep[MAXB > 0 ? MAXB : 1];
-    if (MAXB > 0) {
-        // all key fragments of this wave's blocks in flight at once (rows past
-        // the end are clamped to the last key), then the MFMAs
-        uint4 kf[MAXB > 0 ? MAXB : 1][NKS];
+    f32x4_t keep[MAXC > 0 ? MAXC : 1];
+    sweep([&](int ch, const f32x4_t &acc) {
+        if (MAXC > 0) {
 #pragma unroll
-        for (int bi = 0; bi < MAXB; ++bi) {
-            const int col = min((wave + 4 * bi) * 16 + (lane & 15), N - 1);
-            const char *kr = kb + (size_t)col * hd_bytes + koff;
-#pragma unroll
-            for (int s2 = 0; s2 < NKS; ++s2) kf[bi][s2] = ld16(kr + s2 * 64);
+            for (int c = 0; c < (MAXC > 0 ? MAXC : 1); ++c) keep[c] = (c == ch) ? acc : keep[c];
         }
+        if (ch * kScoreCK + wave * 16 + (lane & 15) < N) {
 #pragma unroll
-        for (int bi = 0; bi < MAXB; ++bi) {
-            if (wave + 4 * bi < nblk) {
-                f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int s2 = 0; s2 < NKS; ++s2) acc = mma16<DT>(qf[s2], kf[bi][s2], acc);
-                keep[bi] = acc;
-            }
+            for (int i = 0; i < 4; ++i) lse_merge(m[i], l[i], acc[i] * scale_log2e, 1.f);
         }
-#pragma unroll
-        for (int bi = 0; bi < MAXB; ++bi) {
-            const int blk = wave + 4 * bi;
-            if (blk < nblk && blk * 16 + (lane & 15) < N) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) lse_merge(m[i], l[i], keep[bi][i] * scale_log2e, 1.f);
-            }
-        }
-    } else {
-        for (int blk = wave; blk < nblk; blk += 4) {
-            const int col = blk * 16 + (lane & 15);
-            const f32x4_t acc = qk_block<DT, NKS>(qf, kb, col, N, hd_bytes, koff);
-            if (col < N) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) lse_merge(m[i], l[i], acc[i] * scale_log2e, 1.f);
-            }
-        }
-    }
+    });
     // combine the 16 lanes that hold the same rows, then the 4 waves
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) {
@@ -157,19 +168,18 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         cs += __shfl_xor(cs, 32, 64);
         if (lane < 16 && col < N) out[col] = cs;
     };
-    if (MAXB > 0) {
+    if (MAXC > 0) {
 #pragma unroll
-        for (int bi = 0; bi < MAXB; ++bi) {
-            const int blk = wave + 4 * bi;
-            if (blk < nblk) emit(keep[bi], blk * 16 + (lane & 15));
-        }
+        for (int c = 0; c < (MAXC > 0 ? MAXC : 1); ++c)
+            if (c < nch) emit(keep[c], c * kScoreCK + wave * 16 + (lane & 15));
     } else {
-        for (int blk = wave; blk < nblk; blk += 4) {
-            const int col = blk * 16 + (lane & 15);
-            emit(qk_block<DT, NKS>(qf, kb, col, N, hd_bytes, koff), col);
-        }
+        sweep([&](int ch, const f32x4_t &acc) {
+            emit(acc, ch * kScoreCK + wave * 16 + (lane & 15));
+        });
     }
 }
+
+constexpr int kSelU = 16;
 
 template <int NT, int EMAX>
 __global__ __launch_bounds__(NT) void score_select_kernel(const float *__restrict__ partial,
@@ -187,8 +197,17 @@ __global__ __launch_bounds__(NT) void score_select_kernel(const float *__restric
         const int j = j0 + e;
         key[e] = 0u;
         if (e < E && j < N) {
+            // partials in blocks of kSelU with clamped addresses (all loads of a
+            // block in flight), added in part order
             float s = 0.f;
-            for (int t = 0; t < nparts; ++t) s += pb[(size_t)t * N + j];
+            for (int t0 = 0; t0 < nparts; t0 += kSelU) {
+                float v[kSelU];
+#pragma unroll
+                for (int u = 0; u < kSelU; ++u) v[u] = pb[(size_t)min(t0 + u, nparts - 1) * N + j];
+#pragma unroll
+                for (int u = 0; u < kSelU; ++u)
+                    if (t0 + u < nparts) s += v[u];
+            }
             s *= inv_norm;
             vb[j] = s;
             key[e] = order_key(s);
@@ -197,44 +216,50 @@ __global__ __launch_bounds__(NT) void score_select_kernel(const float *__restric
     block_topk<NT, EMAX>(key, N, budget, kept + (size_t)b * budget, nullptr, nullptr, sm);
 }
 
-template <int DT, int NKS, int MAXB>
+template <int DT, int NKS, int MAXC>
 static hipError_t score_go(const void *q, const void *k, const HeadArgs &heads, int B, int H,
-                           int Nt, int N, int hd_bytes, int n_heads, float scale_log2e,
-                           float *partial, hipStream_t st) {
+                           int Nt, int N, int n_heads, float scale_log2e, float *partial,
+                           hipStream_t st) {
     dim3 grid((Nt + 15) / 16, n_heads, B);
-    hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXB>), grid, dim3(kScoreNT), 0, st,
-                       (const char *)q, (const char *)k, heads, H, Nt, N, hd_bytes, n_heads,
-                       scale_log2e, partial);
+    hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC>), grid, dim3(kScoreNT), 0, st,
+                       (const char *)q, (const char *)k, heads, H, Nt, N, n_heads, scale_log2e,
+                       partial);
     return hipGetLastError();
 }
 
-// Key blocks per wave held in registers: the smallest of 1, 2, 4, 8 that
-// covers the wave's share, while the fragments stay within 32 x 16 bytes per
-// lane; otherwise the two-pass form (MAXB = 0).
+// Logit blocks held in registers between the two passes: the smallest of 1,
+// 2, 4, 8, 16 chunks that covers the keys, within a register budget that
+// shrinks as the head width grows; otherwise the keys are streamed twice
+// (MAXC = 0).
+template <int NKS>
+constexpr int score_maxc_cap() { return NKS <= 4 ? 16 : (NKS <= 8 ? 8 : 4); }
+
 template <int DT, int NKS>
 static hipError_t score_nks(const void *q, const void *k, const HeadArgs &heads, int B, int H,
-                            int Nt, int N, int hd_bytes, int n_heads, float sl2e, float *partial,
+                            int Nt, int N, int n_heads, float sl2e, float *partial,
                             hipStream_t st) {
-    const int bpw = ((N + 15) / 16 + 3) / 4;
-#define PV_MAXB_CASE(mb)                                                                           \
-    if (bpw <= mb && mb * NKS <= 32)                                                               \
-        return score_go<DT, NKS, (mb * NKS <= 32 ? mb : 0)>(q, k, heads, B, H, Nt, N, hd_bytes,    \
-                                                            n_heads, sl2e, partial, st);
-    PV_MAXB_CASE(1)
-    PV_MAXB_CASE(2)
-    PV_MAXB_CASE(4)
-    PV_MAXB_CASE(8)
-#undef PV_MAXB_CASE
-    return score_go<DT, NKS, 0>(q, k, heads, B, H, Nt, N, hd_bytes, n_heads, sl2e, partial, st);
+    const int nch = (N + kScoreCK - 1) / kScoreCK;
+    constexpr int cap = score_maxc_cap<NKS>();
+#define PV_MAXC_CASE(mc)                                                                           \
+    if (nch <= mc && mc <= cap)                                                                    \
+        return score_go<DT, NKS, (mc <= cap ? mc : 0)>(q, k, heads, B, H, Nt, N, n_heads, sl2e,   \
+                                                       partial, st);
+    PV_MAXC_CASE(1)
+    PV_MAXC_CASE(2)
+    PV_MAXC_CASE(4)
+    PV_MAXC_CASE(8)
+    PV_MAXC_CASE(16)
+#undef PV_MAXC_CASE
+    return score_go<DT, NKS, 0>(q, k, heads, B, H, Nt, N, n_heads, sl2e, partial, st);
 }
 
 template <int DT>
 static hipError_t score_dt(int nks, const void *q, const void *k, const HeadArgs &heads, int B,
-                           int H, int Nt, int N, int hd_bytes, int n_heads, float sl2e,
+                           int H, int Nt, int N, int n_heads, float sl2e,
                            float *partial, hipStream_t st) {
 #define PV_NKS_CASE(n) \
     case n:            \
-        return score_nks<DT, n>(q, k, heads, B, H, Nt, N, hd_bytes, n_heads, sl2e, partial, st);
+        return score_nks<DT, n>(q, k, heads, B, H, Nt, N, n_heads, sl2e, partial, st);
     switch (nks) {
         PV_NKS_CASE(1)
         PV_NKS_CASE(2)
@@ -260,8 +285,8 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const Head
     const int hd_bytes = hd * esz;
     const int nks = hd_bytes / 64;
     const float sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
-    if (dt == kBF16) return score_dt<kBF16>(nks, q, k, heads, B, H, Nt, N, hd_bytes, n_heads, sl2e, partial, st);
-    return score_dt<kF32>(nks, q, k, heads, B, H, Nt, N, hd_bytes, n_heads, sl2e, partial, st);
+    if (dt == kBF16) return score_dt<kBF16>(nks, q, k, heads, B, H, Nt, N, n_heads, sl2e, partial, st);
+    return score_dt<kF32>(nks, q, k, heads, B, H, Nt, N, n_heads, sl2e, partial, st);
 }
 
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,

@@ -69,15 +69,19 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_dedup.argtypes = ded
     lib.pv_prune_dedup.restype = _i
     names_t = ctypes.POINTER(ctypes.c_char_p)
-    lib.pv_prune_dedup_timed.argtypes = ded + [ctypes.POINTER(_vp), _i, ctypes.POINTER(_i), names_t]
+    lib.pv_prune_dedup_timed.argtypes = ded + [ctypes.POINTER(_vp), _i, _i, ctypes.POINTER(_i),
+                                              names_t]
     lib.pv_prune_dedup_timed.restype = _i
+    lib.pv_prune_dedup_split.argtypes = ded + [_vp, _vp, _vp]
+    lib.pv_prune_dedup_split.restype = _i
     lib.pv_head_aware_workspace_bytes.argtypes = [_i, _i, _i, _i, _i, _i, _i, _i]
     lib.pv_head_aware_workspace_bytes.restype = _sz
     ha = [_vp, _vp, ctypes.POINTER(ctypes.c_int32), _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp,
           _vp, _sz, _vp]
     lib.pv_prune_head_aware.argtypes = ha
     lib.pv_prune_head_aware.restype = _i
-    lib.pv_prune_head_aware_timed.argtypes = ha + [ctypes.POINTER(_vp), _i, ctypes.POINTER(_i), names_t]
+    lib.pv_prune_head_aware_timed.argtypes = ha + [ctypes.POINTER(_vp), _i, _i,
+                                                   ctypes.POINTER(_i), names_t]
     lib.pv_prune_head_aware_timed.restype = _i
     lib.pv_prune_gather.argtypes = [_vp, _vp, _vp, _i, _i, _i, _i, _i64, _i64, _i64, _i64, _i64,
                                     _i64, _i64, _vp]
@@ -141,10 +145,14 @@ def pv_dedup_workspace_bytes(B: int, Nv: int, Nt: int, d: int, budget: int, dtyp
 def pv_prune_dedup(vis: torch.Tensor, anchors: torch.Tensor, budget: int, *,
                    want_score: bool = True, want_assign: bool = True, want_merged: bool = True,
                    out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None,
-                   events: Optional[Sequence] = None):
+                   events: Optional[Sequence] = None, reps: int = 1, split=None):
     """Pruning before the LLM.  vis [B, Nv, d], anchors [B, Nt, d] (same dtype).
     Returns dict(kept [B,budget] int32, score [B,Nv] f32 | None,
-    assign [B,Nv] int32 | None, merged [B,budget,d] | None, n_kernels)."""
+    assign [B,Nv] int32 | None, merged [B,budget,d] | None, n_kernels).
+    events / reps: see pv_prune_dedup_timed (profiling only).
+    split = (merge_stream, selected, merged_done) (a torch stream and two torch
+    events, already recorded once so that their HIP events exist): runs
+    pv_prune_dedup_split; assign and merged are ready after merged_done."""
     lib = load()
     _contig(vis, "vis")
     _contig(anchors, "anchors")
@@ -170,12 +178,24 @@ def pv_prune_dedup(vis: torch.Tensor, anchors: torch.Tensor, budget: int, *,
     nbytes = lib.pv_dedup_workspace_bytes(B, Nv, Nt, d, budget, code)
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    if split is not None:
+        if events:
+            raise ValueError("events and split cannot be combined")
+        merge_stream, selected, merged_done = split
+        rc = lib.pv_prune_dedup_split(vis.data_ptr(), anchors.data_ptr(), B, Nv, Nt, d, code,
+                                      int(budget), kept.data_ptr(), _ptr(score), _ptr(assign),
+                                      _ptr(merged), workspace.data_ptr(), workspace.numel(),
+                                      _stream(dev), merge_stream.cuda_stream,
+                                      selected.cuda_event, merged_done.cuda_event)
+        _check("pv_prune_dedup_split", rc, lib)
+        return {"kept": kept, "score": score, "assign": assign, "merged": merged,
+                "n_kernels": None, "kernel_names": [], "workspace": workspace}
     ev, nev, nm = _events_array(events)
     nk = _i(0)
     rc = lib.pv_prune_dedup_timed(vis.data_ptr(), anchors.data_ptr(), B, Nv, Nt, d, code,
                                   int(budget), kept.data_ptr(), _ptr(score), _ptr(assign),
                                   _ptr(merged), workspace.data_ptr(), workspace.numel(),
-                                  _stream(dev), ev, nev, ctypes.byref(nk), nm)
+                                  _stream(dev), ev, nev, int(reps), ctypes.byref(nk), nm)
     _check("pv_prune_dedup", rc, lib)
     return {"kept": kept, "score": score, "assign": assign, "merged": merged,
             "n_kernels": nk.value, "kernel_names": _names(nm, min(nk.value, max(nev - 1, 0))),
@@ -190,10 +210,11 @@ def pv_head_aware_workspace_bytes(B: int, H: int, Nt: int, N: int, hd: int, n_he
 def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
                         want_score: bool = True, out: Optional[dict] = None,
                         workspace: Optional[torch.Tensor] = None,
-                        events: Optional[Sequence] = None):
+                        events: Optional[Sequence] = None, reps: int = 1):
     """Head-aware pruning.  q [B,H,Nt,hd], k [B,H,N,hd] (same dtype), heads: host
     int sequence [B, n_heads].  Returns dict(kept [B,budget] int32,
-    score [B,N] f32 | None, n_kernels)."""
+    score [B,N] f32 | None, n_kernels).  events / reps: see
+    pv_prune_head_aware_timed (profiling only)."""
     import numpy as np
 
     lib = load()
@@ -223,7 +244,7 @@ def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
                                        hs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n_heads,
                                        B, H, Nt, N, hd, code, int(budget), kept.data_ptr(),
                                        _ptr(score), workspace.data_ptr(), workspace.numel(),
-                                       _stream(dev), ev, nev, ctypes.byref(nk), nm)
+                                       _stream(dev), ev, nev, int(reps), ctypes.byref(nk), nm)
     _check("pv_prune_head_aware", rc, lib)
     return {"kept": kept, "score": score, "n_kernels": nk.value,
             "kernel_names": _names(nm, min(nk.value, max(nev - 1, 0))), "workspace": workspace}

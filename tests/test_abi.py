@@ -166,3 +166,33 @@ def test_select_topk_validation(lib):
     assert t(FAKE + 4, 1, 8, 4, FAKE, None, None, None) == -8
     assert t(FAKE, 1, 8, 4, FAKE, FAKE + 8, None, None) == -8
     assert t(FAKE, 1, 8, 4, FAKE, None, FAKE + 12, None) == -8
+
+
+def test_timed_reps_validation(lib):
+    # reps < 1 is rejected before anything is enqueued
+    rc = lib.pv_prune_dedup_timed(FAKE, FAKE, 1, 64, 16, 256, 1, 32, FAKE, None, None, None, FAKE,
+                                  1 << 40, None, None, 0, 0, None, None)
+    assert rc == -2
+    hs = np.zeros((1, 1), np.int32)
+    rc = lib.pv_prune_head_aware_timed(FAKE, FAKE, hs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                       1, 1, 4, 16, 32, 64, 1, 8, FAKE, None, FAKE, 1 << 40, None,
+                                       None, 0, 0, None, None)
+    assert rc == -2
+
+
+def test_timed_null_event_handle(lib):
+    evs = (ctypes.c_void_p * 3)(FAKE, None, FAKE)
+    rc = lib.pv_prune_dedup_timed(FAKE, FAKE, 1, 64, 16, 256, 1, 32, FAKE, None, None, None, FAKE,
+                                  1 << 40, None, evs, 3, 1, None, None)
+    assert rc == -1
+
+
+def test_dedup_split_validation(lib):
+    s = lib.pv_prune_dedup_split
+    args = [FAKE, FAKE, 1, 64, 16, 256, 1, 32, FAKE, None, None, None, FAKE, 1 << 40, None]
+    assert s(*args, None, FAKE, FAKE) == -1
+    assert s(*args, FAKE, None, FAKE) == -1
+    assert s(*args, FAKE, FAKE, None) == -1
+    bad = list(args)
+    bad[7] = 0  # budget
+    assert s(*bad, FAKE, FAKE, FAKE) == -3

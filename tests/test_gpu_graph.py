@@ -1,6 +1,6 @@
 """The pruning step captured in a HIP graph: every replay, with eager work
 and synchronisations in between, must reproduce the eager result bit for
-bit (the library clears its counters with a kernel, never a memset node)."""
+bit (the library records no memset node and keeps no state between calls)."""
 import numpy as np
 import pytest
 
@@ -8,7 +8,8 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 
-def test_graph_replays_match_eager():
+@pytest.mark.parametrize("split", [True, False])
+def test_graph_replays_match_eager(split):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     import bench
@@ -16,7 +17,7 @@ def test_graph_replays_match_eager():
 
     dev = torch.device("cuda:0")
     w = W.make_workload(2)
-    step = bench.Step(w, dev)
+    step = bench.Step(w, dev, split=split)
     step.run()
     torch.cuda.synchronize()
     ref = step.snapshot()

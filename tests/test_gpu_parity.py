@@ -121,6 +121,55 @@ def test_dedup_deterministic():
         assert np.array_equal(a[k], b[k]), k
 
 
+def test_timed_reps_leave_results_unchanged():
+    """The profiling variants with every kernel launched several times give
+    the results of one launch (no kernel reads what it writes)."""
+    from paper_2608_25332_amd import provip
+    w = workload(2)
+    vis, anc = to_dev(w.vis, "bf16"), to_dev(w.anchors, "bf16")
+    a = provip.pv_prune_dedup(vis, anc, w.N1)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(8)]
+    for e in ev:  # torch creates the HIP event on its first record
+        e.record()
+    b = provip.pv_prune_dedup(vis, anc, w.N1, events=ev, reps=3)
+    torch.cuda.synchronize()
+    assert b["n_kernels"] == len(b["kernel_names"]) >= 5
+    for k in ("kept", "score", "assign", "merged"):
+        assert torch.equal(a[k], b[k]), k
+    q, kf = to_dev(w.q, "bf16"), to_dev(w.k_full, "bf16")
+    k1 = provip.pv_prune_gather(kf, a["kept"])
+    h1 = provip.pv_prune_head_aware(q, k1, w.heads, w.N2)
+    ev2 = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in ev2:
+        e.record()
+    h2 = provip.pv_prune_head_aware(q, k1, w.heads, w.N2, events=ev2, reps=4)
+    torch.cuda.synchronize()
+    assert h2["kernel_names"] == ["score_partial", "score_select"]
+    for k in ("kept", "score"):
+        assert torch.equal(h1[k], h2[k]), k
+
+
+@pytest.mark.parametrize("wid", [1, 2, 4])
+def test_dedup_split_matches_single_stream(wid):
+    """pv_prune_dedup_split (merge branch on a second stream) gives the bits
+    of pv_prune_dedup once merged_done has completed."""
+    from paper_2608_25332_amd import provip
+    w = workload(wid, with_kv=False)
+    dt = w.dtype
+    vis, anc = to_dev(w.vis, dt), to_dev(w.anchors, dt)
+    a = provip.pv_prune_dedup(vis, anc, w.N1)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    sel, done = torch.cuda.Event(), torch.cuda.Event()
+    sel.record()
+    done.record()
+    b = provip.pv_prune_dedup(vis, anc, w.N1, split=(side, sel, done))
+    torch.cuda.current_stream().wait_event(done)
+    torch.cuda.synchronize()
+    for k in ("kept", "score", "assign", "merged"):
+        assert torch.equal(a[k], b[k]), k
+
+
 DEDUP_EDGE = [
     # (B, Nv, Nt, d, budget, dtype)
     (1, 17, 1, 64, 5, "f32"),
@@ -230,7 +279,12 @@ HEAD_EDGE = [
     (3, 8, 33, 100, 128, 8, 40, "bf16"),
     (1, 4, 16, 64, 256, 2, 16, "bf16"),
     (2, 4, 5, 50, 96, 1, 7, "f32"),
-    (1, 2, 200, 2000, 128, 2, 600, "bf16"),
+    (1, 2, 200, 2000, 128, 2, 600, "bf16"),   # keys streamed twice
+    (1, 2, 20, 600, 256, 1, 100, "bf16"),     # wide head, streamed twice
+    (1, 2, 16, 130, 256, 2, 30, "f32"),       # widest head, logits kept
+    (1, 2, 16, 300, 256, 1, 30, "f32"),       # widest head, streamed twice
+    (2, 3, 40, 70, 160, 2, 9, "bf16"),
+    (1, 2, 33, 257, 224, 2, 64, "f32"),
 ]
 
 
