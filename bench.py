@@ -54,6 +54,10 @@ def parse():
                     help="back-to-back launches of each kernel per timing sample")
     ap.add_argument("--kernel-iters", type=int, default=10, help="timing samples per kernel")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="counter-collection pass: `steps` eager steps, then a copy kernel of "
+                         "known size (--calib-mib) to scale the counters; no timing")
+    ap.add_argument("--calib-mib", type=int, default=256)
     ap.add_argument("--split", action="store_true",
                     help="time the step with the merge branch on a second stream")
     return ap.parse_args()
@@ -242,19 +246,24 @@ def kernel_times(torch, step, reps, iters):
     are launched reps times back to back between two HIP events recorded on
     the stream the library launches on (the current stream).  A spin kernel
     queued first keeps the GPU behind the host, so the launches run back to
-    back rather than at the host's pace."""
+    back rather than at the host's pace; a sample whose spin had already
+    ended when the host finished enqueuing is taken again with a longer
+    spin."""
     pv = step.pv
     per = {}
-    hold = sleep_cycles_for(torch, 4.0 + 0.05 * reps * 11)
-    for _ in range(iters):
+    hold_ms = 4.0
+    done = 0
+    while done < iters:
         e1 = [torch.cuda.Event(enable_timing=True) for _ in range(Step.DEDUP_EVENTS)]
         e2 = [torch.cuda.Event(enable_timing=True) for _ in range(Step.HEAD_EVENTS)]
         g1 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         g2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-        for e in e1 + e2 + g1 + g2:  # torch creates the HIP event on first record
+        spun = torch.cuda.Event()
+        for e in e1 + e2 + g1 + g2 + [spun]:  # torch creates the HIP event on first record
             e.record()
         torch.cuda.synchronize()
-        torch.cuda._sleep(hold)
+        torch.cuda._sleep(sleep_cycles_for(torch, hold_ms))
+        spun.record()
         r1 = pv.pv_prune_dedup(step.vis, step.anc, step.w.N1, out=step.o1, workspace=step.ws1,
                                events=e1, reps=reps)
         g1[0].record()
@@ -267,7 +276,14 @@ def kernel_times(torch, step, reps, iters):
         for _ in range(reps):
             step.gather_hkv2()
         g2[1].record()
+        starved = spun.query()
         torch.cuda.synchronize()
+        if starved:
+            hold_ms *= 2
+            if hold_ms > 1000:
+                raise RuntimeError("host cannot keep ahead of the GPU for the kernel timing")
+            continue
+        done += 1
         marks = [(nm, e1[i], e1[i + 1]) for i, nm in enumerate(r1["kernel_names"])]
         marks += [("gather_kv1", g1[0], g1[1])]
         marks += [(nm, e2[i], e2[i + 1]) for i, nm in enumerate(r2["kernel_names"])]
@@ -415,6 +431,23 @@ def main():
     step.run()
     torch.cuda.synchronize()
     ref = step.snapshot()
+
+    if args.pmc_pass:
+        # every dispatch of a library kernel here runs in the step's own
+        # sequence (no graph, no back-to-back repeats)
+        for _ in range(args.steps):
+            step.run()
+        torch.cuda.synchronize()
+        n = args.calib_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty(n, dtype=torch.uint8, device=dev)
+        src.fill_(1)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"pmc_pass": s.name, "steps": args.steps, "calib_bytes": n,
+                          "csrc_digest": csrc_digest()}), flush=True)
+        return
 
     # ---- headline: graph replay
     use_graph = not args.no_graph
