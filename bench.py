@@ -144,7 +144,7 @@ class Step:
                                    workspace=self.ws2)
             self.gather_hkv2()
 
-    DEDUP_EVENTS = 8   # up to 7 kernels + 1
+    DEDUP_EVENTS = 9   # up to 8 kernels + 1
     HEAD_EVENTS = 4    # up to 3 kernels + 1
 
     def snapshot(self):
@@ -158,7 +158,7 @@ class Step:
 STAGE_OF = {
     "cos_partial": "cosine", "cos_reduce": "cosine", "center": "cosine",
     "select": "select", "gram_partial": "gram", "gram_reduce": "gram", "gram_tile": "gram",
-    "gram_finish": "gram", "merge": "merge", "gather_kv1": "kv_of_kept",
+    "gram_finish": "gram", "bucket": "merge", "merge": "merge", "gather_kv1": "kv_of_kept",
     "score_partial": "head_aware", "score_select": "head_aware", "gather_hkv2": "gather",
 }
 
@@ -189,6 +189,8 @@ def algorithmic(w):
         # argmax: read the inverse norms, write the assignment
         "gram_reduce": dict(bytes=B * Nv * 4 * 2, flops=1.0 * B * Mp * N1),
         "gram_finish": dict(bytes=B * Mp * 4 * 2, flops=0.0),
+        # member lists: read the assignment, write the lists
+        "bucket": dict(bytes=B * (Nv * 4 * 2 + N1 * 8), flops=0.0),
         # merge: read every visual token once, write the N1 centroids
         "merge": dict(bytes=B * (Nv + N1) * d * e, flops=1.0 * B * Nv * d),
         # read + write the K and V rows of the N1 kept tokens

@@ -89,13 +89,14 @@ struct DedupPlan {
     bool gram_big;                 // LDS-staged 128x128 full-k tiles
     int ks_gram, ntn;              // split-k slices (small) / column tiles (big)
     // workspace
+    bool lists;                    // merge reads bucketed member lists
     float *cpart, *ssv, *ssa, *M, *rowsum, *invn, *p, *gpart, *best_val;
-    int32_t *pruned, *assign, *best_slot;
+    int32_t *pruned, *assign, *best_slot, *mcount, *mstart, *mlist;
     size_t bytes;
 };
 
 DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget, bool want_p,
-                     bool want_assign) {
+                     bool want_assign, bool want_merged) {
     DedupPlan P;
     P.nch = d * esz / 128;
     const int T = pv::kSplitTile;
@@ -124,6 +125,15 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
         P.gpart = c.take<float>((size_t)P.ks_gram * B * Mp1 * budget);
         P.best_val = nullptr;
         P.best_slot = nullptr;
+    }
+    P.lists = want_merged && pv::merge_uses_lists(budget, d * esz);
+    if (P.lists) {
+        const int ngroups = (budget + pv::kBucketSlotsPerGroup - 1) / pv::kBucketSlotsPerGroup;
+        P.mcount = c.take<int32_t>((size_t)B * budget);
+        P.mstart = c.take<int32_t>((size_t)B * budget);
+        P.mlist = c.take<int32_t>((size_t)B * ngroups * Nv);
+    } else {
+        P.mcount = P.mstart = P.mlist = nullptr;
     }
     P.bytes = c.off + kAlign;
     return P;
@@ -159,7 +169,7 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     const bool need_assign = assign != nullptr || merged != nullptr;
     const int esz = (dtype == PV_BF16) ? 2 : 4;
     DedupPlan P0 = plan_dedup(nullptr, B, Nv, Nt, d, esz, budget, score == nullptr,
-                              need_assign && !assign);
+                              need_assign && !assign, merged != nullptr);
     if (!workspace) return PV_ERR_WORKSPACE;
     if (ws_bytes < P0.bytes) return PV_ERR_WORKSPACE;
     for (const void *p : {vis, anchors, (const void *)kept, (const void *)score,
@@ -168,7 +178,7 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     // carve from a 256-aligned start
     char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
     DedupPlan P = plan_dedup(wsa, B, Nv, Nt, d, esz, budget, score == nullptr,
-                             need_assign && !assign);
+                             need_assign && !assign, merged != nullptr);
     float *p = score ? score : P.p;
     int32_t *asg = assign ? assign : P.assign;
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
@@ -228,7 +238,17 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
                 return PV_ERR_HIP;
         }
     }
-    if (merged) {
+    if (merged && P.lists) {
+        if (!tr.launch("bucket", [&] {
+                return pv::launch_bucket(asg, B, Nv, budget, P.mcount, P.mstart, P.mlist, sm);
+            }))
+            return PV_ERR_HIP;
+        if (!tr.launch("merge", [&] {
+                return pv::launch_merge_csr(dt, vis, B, Nv, d, budget, P.mcount, P.mstart, P.mlist,
+                                            merged, sm);
+            }))
+            return PV_ERR_HIP;
+    } else if (merged) {
         if (!tr.launch("merge", [&] {
                 return pv::launch_merge(dt, vis, B, Nv, d, budget, asg, merged, sm);
             }))
@@ -339,7 +359,7 @@ PV_API size_t pv_dedup_workspace_bytes(int B, int Nv, int Nt, int d, int budget,
     if (B < 1 || Nv < 1 || Nt < 1 || d < 64 || budget < 1 || budget > Nv) return 0;
     if (dtype != PV_F32 && dtype != PV_BF16) return 0;
     // sized for the case that needs the most: no score or assign output
-    return plan_dedup(nullptr, B, Nv, Nt, d, dtype == PV_BF16 ? 2 : 4, budget, true, true).bytes;
+    return plan_dedup(nullptr, B, Nv, Nt, d, dtype == PV_BF16 ? 2 : 4, budget, true, true, true).bytes;
 }
 
 PV_API int pv_prune_dedup(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,

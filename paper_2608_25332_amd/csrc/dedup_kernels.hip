@@ -457,6 +457,53 @@ constexpr int kMergeRound = 4096;                  // tokens listed per round
 constexpr int kMergeTPT = kMergeRound / kMergeNT;  // tokens per thread per round
 constexpr int kMergeU = 8;                         // member rows in flight per wave
 
+// Adds the elements of one 16-byte chunk to acc (fp32).
+template <int DT>
+__device__ __forceinline__ void add16(float (&acc)[DT == kBF16 ? 8 : 4], uint4 v) {
+    const uint32_t w4[4] = {v.x, v.y, v.z, v.w};
+    if (DT == kBF16) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            acc[2 * q] += __uint_as_float(w4[q] << 16);
+            acc[2 * q + 1] += __uint_as_float(w4[q] & 0xFFFF0000u);
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[q] += __uint_as_float(w4[q]);
+    }
+}
+
+// Combines the waves' partial sums in wave order, divides by the member count
+// and stores this lane's 16-byte chunk of the output row.
+template <int DT, int NW>
+__device__ __forceinline__ void merge_finish(float (&acc)[DT == kBF16 ? 8 : 4],
+                                             float (&part)[NW][DT == kBF16 ? 8 : 4][64], int wave,
+                                             int lane, int c, int nchunk, int total, char *out) {
+    constexpr int EPC = (DT == kBF16) ? 8 : 4;
+    if (wave > 0) {
+#pragma unroll
+        for (int e = 0; e < EPC; ++e) part[wave][e][lane] = acc[e];
+    }
+    __syncthreads();
+    if (wave == 0 && c < nchunk) {
+#pragma unroll
+        for (int w2 = 1; w2 < NW; ++w2)
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) acc[e] += part[w2][e][lane];
+        const float cntf = (float)total;
+        uint32_t w4[4];
+        if (DT == kBF16) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                w4[q] = f32_to_bf16_rne(acc[2 * q] / cntf) | (f32_to_bf16_rne(acc[2 * q + 1] / cntf) << 16);
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) w4[q] = __float_as_uint(acc[q] / cntf);
+        }
+        st16(out + (size_t)c * 16, uint4{w4[0], w4[1], w4[2], w4[3]});
+    }
+}
+
 template <int DT>
 __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict__ vis, int Nv,
                                                          int d_bytes,
@@ -504,44 +551,167 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
 #pragma unroll
             for (int u = 0; u < kMergeU; ++u) {
                 if (m0 + u * NW >= cnt) break;
-                const uint32_t w4[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
-                if (DT == kBF16) {
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) {
-                        acc[2 * q] += __uint_as_float(w4[q] << 16);
-                        acc[2 * q + 1] += __uint_as_float(w4[q] & 0xFFFF0000u);
-                    }
-                } else {
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) acc[q] += __uint_as_float(w4[q]);
-                }
+                add16<DT>(acc, v[u]);
             }
         }
         total += cnt;
         __syncthreads();  // the list is rewritten by the next round
     }
-    if (wave > 0) {
+    merge_finish<DT, NW>(acc, part, wave, lane, c, nchunk, total,
+                         merged + ((size_t)b * N1 + s) * d_bytes);
+}
+
+// ----------------------------------------------------------------------------
+// Member lists for large inputs, where every merge workgroup scanning the whole
+// assignment would cost more than the rows it adds.
+//
+// bucket: grid (ceil(N1 / 256), B), 512 threads.  Lists the members of the
+// 256 slots [256 g, 256 g + 256) in ascending token order: mcount[b][s],
+// mstart[b][s] (offset in the sample's list region) and the lists themselves
+// in mlist[b][g * Nv ...].  The assignment is staged in LDS; the eight waves
+// take eight consecutive token segments and sweep them twice, 64 tokens per
+// step: per-slot counts, then placement at offsets that keep the segments in
+// order.  Within a step, the lanes that hold the same slot are found with one
+// ballot per bit of the slot offset (the lanes whose offsets agree on every
+// bit), so a step costs the same whatever the number of distinct slots in it;
+// the lowest such lane updates the wave's counter of that slot.
+// ----------------------------------------------------------------------------
+constexpr int kBucketBits = 8;
+constexpr int kBucketSlots = 1 << kBucketBits;
+static_assert(kBucketSlots == kBucketSlotsPerGroup, "slots per bucket group");
+constexpr int kBucketNT = 512;
+constexpr int kBucketW = kBucketNT / 64;
+
+// Lanes whose value v agrees with this lane's on the low kBucketBits bits,
+// among the lanes in `act`.
+__device__ __forceinline__ unsigned long long same_slot_lanes(int v, unsigned long long act) {
+    unsigned long long same = act;
 #pragma unroll
-        for (int e = 0; e < EPC; ++e) part[wave][e][lane] = acc[e];
+    for (int bit = 0; bit < kBucketBits; ++bit) {
+        const bool on = (v >> bit) & 1;
+        const unsigned long long ones = __ballot(on);
+        same &= on ? ones : ~ones;
+    }
+    return same;
+}
+
+__global__ __launch_bounds__(kBucketNT) void bucket_kernel(const int32_t *__restrict__ assign,
+                                                           int Nv, int N1,
+                                                           int32_t *__restrict__ mcount,
+                                                           int32_t *__restrict__ mstart,
+                                                           int32_t *__restrict__ mlist) {
+    extern __shared__ int32_t sa[];  // [Nv] the sample's assignment
+    __shared__ int cur[kBucketW][kBucketSlots];
+    __shared__ int wsum[kBucketW];
+    const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int ngroups = gridDim.x;
+    const int s0 = g * kBucketSlots;
+    const int32_t *as = assign + (size_t)b * Nv;
+    int32_t *lst = mlist + ((size_t)b * ngroups + g) * Nv;
+    const unsigned long long lt = (1ull << lane) - 1ull;
+
+    for (int e = lane; e < kBucketSlots; e += 64) cur[wave][e] = 0;
+    // stage: eight loads per thread in flight per round
+    for (int j0 = 0; j0 < Nv; j0 += kBucketNT * 8) {
+        int v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = as[min(j0 + u * kBucketNT + tid, Nv - 1)];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            if (j0 + u * kBucketNT + tid < Nv) sa[j0 + u * kBucketNT + tid] = v[u];
     }
     __syncthreads();
-    if (wave == 0 && c < nchunk) {
-#pragma unroll
-        for (int w2 = 1; w2 < NW; ++w2)
-#pragma unroll
-            for (int e = 0; e < EPC; ++e) acc[e] += part[w2][e][lane];
-        const float cntf = (float)total;
-        uint32_t w4[4];
-        if (DT == kBF16) {
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                w4[q] = f32_to_bf16_rne(acc[2 * q] / cntf) | (f32_to_bf16_rne(acc[2 * q + 1] / cntf) << 16);
-        } else {
-#pragma unroll
-            for (int q = 0; q < 4; ++q) w4[q] = __float_as_uint(acc[q] / cntf);
-        }
-        st16(merged + ((size_t)b * N1 + s) * d_bytes + (size_t)c * 16, uint4{w4[0], w4[1], w4[2], w4[3]});
+    // this wave's token segment [t0, t1), whole 64-token steps
+    const int seg = ((Nv + kBucketW - 1) / kBucketW + 63) / 64 * 64;
+    const int t0 = min(wave * seg, Nv), t1 = min(t0 + seg, Nv);
+    int *wc = cur[wave];
+
+    // pass 1: this wave's count of every slot
+    for (int c0 = t0; c0 < t1; c0 += 64) {
+        const int j = c0 + lane;
+        const int v = (j < t1) ? sa[j] - s0 : -1;
+        const bool rel = v >= 0 && v < kBucketSlots;
+        const unsigned long long same = same_slot_lanes(v, __ballot(rel));
+        if (rel && (same & lt) == 0ull) wc[v] += __popcll(same);
     }
+    __syncthreads();
+    // slot totals and offsets; then each wave's first position per slot
+    int tot = 0;
+    if (tid < kBucketSlots) {
+#pragma unroll
+        for (int w = 0; w < kBucketW; ++w) tot += cur[w][tid];
+    }
+    int all;
+    const int base = block_excl_scan<kBucketNT>(tot, wsum, &all);
+    if (tid < kBucketSlots) {
+        if (s0 + tid < N1) {
+            mcount[(size_t)b * N1 + s0 + tid] = tot;
+            mstart[(size_t)b * N1 + s0 + tid] = g * Nv + base;
+        }
+        int run = base;
+#pragma unroll
+        for (int w = 0; w < kBucketW; ++w) {
+            const int c = cur[w][tid];
+            cur[w][tid] = run;
+            run += c;
+        }
+    }
+    __syncthreads();
+    // pass 2: placement in token order
+    for (int c0 = t0; c0 < t1; c0 += 64) {
+        const int j = c0 + lane;
+        const int v = (j < t1) ? sa[j] - s0 : -1;
+        const bool rel = v >= 0 && v < kBucketSlots;
+        const unsigned long long same = same_slot_lanes(v, __ballot(rel));
+        if (rel) {
+            lst[wc[v] + __popcll(same & lt)] = j;
+            if ((same & lt) == 0ull) wc[v] += __popcll(same);
+        }
+    }
+}
+
+// merge_csr: as merge, with the member list read from the bucket output.
+template <int DT>
+__global__ __launch_bounds__(kMergeNT) void merge_csr_kernel(
+    const char *__restrict__ vis, int Nv, int d_bytes, const int32_t *__restrict__ mcount,
+    const int32_t *__restrict__ mstart, const int32_t *__restrict__ mlist, int N1, int ngroups,
+    char *__restrict__ merged) {
+    constexpr int EPC = (DT == kBF16) ? 8 : 4;
+    constexpr int NW = kMergeNT / 64;
+    __shared__ int list[kMergeRound];
+    __shared__ float part[NW][EPC][64];
+    const int s = blockIdx.y, b = blockIdx.z;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int nchunk = d_bytes >> 4;
+    const int c = blockIdx.x * 64 + lane;
+    const char *col = vis + (size_t)b * Nv * d_bytes + (size_t)min(c, nchunk - 1) * 16;
+    const int total = mcount[(size_t)b * N1 + s];
+    const int32_t *src = mlist + (size_t)b * ngroups * Nv + mstart[(size_t)b * N1 + s];
+
+    float acc[EPC];
+#pragma unroll
+    for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
+    for (int r0 = 0; r0 < total; r0 += kMergeRound) {
+        const int cnt = min(kMergeRound, total - r0);
+        for (int m = tid; m < cnt; m += kMergeNT) list[m] = src[r0 + m];
+        __syncthreads();
+        for (int m0 = wave; m0 < cnt; m0 += NW * kMergeU) {
+            uint4 v[kMergeU];
+#pragma unroll
+            for (int u = 0; u < kMergeU; ++u)
+                v[u] = ld16(col + (size_t)list[min(m0 + u * NW, cnt - 1)] * d_bytes);
+#pragma unroll
+            for (int u = 0; u < kMergeU; ++u) {
+                if (m0 + u * NW >= cnt) break;
+                add16<DT>(acc, v[u]);
+            }
+        }
+        __syncthreads();  // the list is rewritten by the next round
+    }
+    merge_finish<DT, NW>(acc, part, wave, lane, c, nchunk, total,
+                         merged + ((size_t)b * N1 + s) * d_bytes);
 }
 
 // ----------------------------------------------------------------------------
@@ -645,6 +815,29 @@ hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, i
     dim3 grid((Mp + kFinNT - 1) / kFinNT, B);
     hipLaunchKernelGGL(gram_finish_kernel, grid, dim3(kFinNT), 0, st, best_val, best_slot, ntn, Mp,
                        Nv, pruned, assign);
+    return hipGetLastError();
+}
+
+hipError_t launch_bucket(const int32_t *assign, int B, int Nv, int N1, int32_t *mcount,
+                         int32_t *mstart, int32_t *mlist, hipStream_t st) {
+    const dim3 grid((N1 + kBucketSlots - 1) / kBucketSlots, B);
+    hipLaunchKernelGGL(bucket_kernel, grid, dim3(kBucketNT), (size_t)Nv * sizeof(int32_t), st,
+                       assign, Nv, N1, mcount, mstart, mlist);
+    return hipGetLastError();
+}
+
+hipError_t launch_merge_csr(int dt, const void *vis, int B, int Nv, int d, int N1,
+                            const int32_t *mcount, const int32_t *mstart, const int32_t *mlist,
+                            void *merged, hipStream_t st) {
+    const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
+    const int ngroups = (N1 + kBucketSlots - 1) / kBucketSlots;
+    const dim3 grid((d_bytes / 16 + 63) / 64, N1, B);
+    if (dt == kBF16)
+        hipLaunchKernelGGL(merge_csr_kernel<kBF16>, grid, dim3(kMergeNT), 0, st, (const char *)vis,
+                           Nv, d_bytes, mcount, mstart, mlist, N1, ngroups, (char *)merged);
+    else
+        hipLaunchKernelGGL(merge_csr_kernel<kF32>, grid, dim3(kMergeNT), 0, st, (const char *)vis,
+                           Nv, d_bytes, mcount, mstart, mlist, N1, ngroups, (char *)merged);
     return hipGetLastError();
 }
 

@@ -38,6 +38,17 @@ hipError_t launch_gram_tile(int dt, const void *vis, int B, int Nv, int d, const
 hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, int B, int ntn,
                               int Mp, int Nv, const int32_t *pruned, int32_t *assign,
                               hipStream_t st);
+constexpr int kBucketSlotsPerGroup = 256;  // slots whose member lists one workgroup builds
+hipError_t launch_bucket(const int32_t *assign, int B, int Nv, int N1, int32_t *mcount,
+                         int32_t *mstart, int32_t *mlist, hipStream_t st);
+hipError_t launch_merge_csr(int dt, const void *vis, int B, int Nv, int d, int N1,
+                            const int32_t *mcount, const int32_t *mstart, const int32_t *mlist,
+                            void *merged, hipStream_t st);
+// Whether the merge reads member lists built by the bucket kernel (large
+// inputs) instead of scanning the assignment in every workgroup.
+inline bool merge_uses_lists(int N1, int d_bytes) {
+    return (long long)((d_bytes / 16 + 63) / 64) * N1 * 4 > d_bytes;
+}
 hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
                         const int32_t *assign, void *merged, hipStream_t st);
 

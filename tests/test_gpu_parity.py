@@ -184,6 +184,9 @@ DEDUP_EDGE = [
     (1, 40, 4, 192, 1, "bf16"),
     (1, 40, 4, 256, 3, "bf16"),
     (2, 40, 4, 320, 7, "f32"),
+    # merge through bucketed member lists (narrow rows, many slots)
+    (1, 1000, 8, 64, 70, "bf16"),
+    (2, 700, 5, 128, 200, "f32"),
 ]
 
 
@@ -211,6 +214,22 @@ def test_dedup_edges(B, Nv, Nt, d, budget, dt):
         if budget == Nv:
             assert np.array_equal(kept, np.arange(Nv))
             assert np.array_equal(g["merged"][b], vis[b])
+
+
+def test_dedup_one_slot_takes_almost_everything():
+    """Identical visual tokens: every pruned token ties on cosine 1 and goes
+    to slot 0 (lowest slot), whose member list then exceeds one 4096-entry
+    round of the merge."""
+    rng = np.random.default_rng(9)
+    row = W.bf16_round(rng.standard_normal(64).astype(np.float32))
+    vis = np.ascontiguousarray(np.broadcast_to(row, (1, 5000, 64)), np.float32)
+    anc = W.bf16_round(rng.standard_normal((1, 3, 64)).astype(np.float32))
+    g = run_dedup(vis, anc, "bf16", 40)
+    assert np.array_equal(g["kept"][0], np.arange(40))
+    want = np.zeros(5000, np.int32)
+    want[:40] = np.arange(40)
+    assert np.array_equal(g["assign"][0], want)
+    check_merged(g["merged"][0], vis[0], g["kept"][0], g["assign"][0], np.arange(40), "bf16")
 
 
 def test_dedup_zero_vectors():
