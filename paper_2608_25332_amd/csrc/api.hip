@@ -86,7 +86,7 @@ struct DedupPlan {
     int nch;                       // 128-byte k chunks per row
     int ks_cos, njt;               // cosine: k slices, token tiles of the row sums
     int Mp;
-    bool gram_big;                 // LDS-staged 128x128 full-k tiles
+    bool gram_big;                 // full-k 256x128 tiles (operands streamed into LDS)
     int ks_gram, ntn;              // split-k slices (small) / column tiles (big)
     // workspace
     bool lists;                    // merge reads bucketed member lists
@@ -104,9 +104,10 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
     P.njt = pv::cos_row_tiles(Nv);
     P.Mp = Nv - budget;
     const int Mp1 = P.Mp > 0 ? P.Mp : 1;
-    P.gram_big = n_tiles(Mp1, budget, B, 128) >= 240;
+    P.gram_big = (long long)((Mp1 + pv::kGramTileM - 1) / pv::kGramTileM) *
+                     ((budget + pv::kGramTileN - 1) / pv::kGramTileN) * B >= 128;
     P.ks_gram = P.gram_big ? 1 : pick_slices(n_tiles(Mp1, budget, B, T), P.nch);
-    P.ntn = P.gram_big ? (budget + 127) / 128 : 1;
+    P.ntn = P.gram_big ? (budget + pv::kGramTileN - 1) / pv::kGramTileN : 1;
     Carve c(ws);
     P.cpart = c.take<float>((size_t)P.ks_cos * B * Nt * Nv);
     P.ssv = c.take<float>((size_t)P.ks_cos * B * Nv);

@@ -20,6 +20,7 @@
 // (on this chip a device-scope fence writes back and invalidates the L2).
 #include "pv_launch.h"
 #include "pv_tile_gemm.h"
+#include "pv_tile_lds.h"
 
 #include <math.h>
 
@@ -351,22 +352,25 @@ __global__ __launch_bounds__(128) void gram_reduce_kernel(
     if (lane == 0) assign[(size_t)b * Nv + tok] = bs;
 }
 
-// gram_tile: LDS-staged 128 x 128 tiles for the large, MFMA-bound Grams.
-// grid (N1 tiles, Mp tiles, B).
-template <int DT, int BM, int BN, int WM, int WN>
+// gram_tile: the large, MFMA-bound Grams.  1-D grid over (sample, pruned
+// tile, kept tile) in XCD order (the kept tiles of one pruned tile are
+// adjacent, so they share its rows in one L2); 256 x 128 tiles with the
+// operands streamed straight into LDS (TileGemmLds), eight waves of 64 x 64.
+// Writes the best (cosine, slot) of every pruned row within this kept tile,
+// or the slot itself when there is only one kept tile.
+template <int DT, int BM, int BN, int WM, int WN, int NS>
 __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
     const char *__restrict__ vis, int Nv, int d_bytes, const int32_t *__restrict__ kept, int N1,
-    const int32_t *__restrict__ pruned, int Mp, const float *__restrict__ invn,
+    const int32_t *__restrict__ pruned, int Mp, const float *__restrict__ invn, int ntm, int ntn,
     float *__restrict__ best_val, int32_t *__restrict__ best_slot, int32_t *__restrict__ assign) {
-    using G = TileGemm<DT, BM, BN, WM, WN, 1>;
-    __shared__ __attribute__((aligned(16))) char lds[G::LDS_BYTES];
+    using G = TileGemmLds<DT, BM, BN, WM, WN, NS>;
     __shared__ int32_t rowtok[G::ROWS];
     __shared__ float rowinv[G::ROWS];
     __shared__ float red_v[WN][BM];
     __shared__ int red_s[WN][BM];
 
-    const int nt = blockIdx.x, mt = blockIdx.y, b = blockIdx.z;
-    const int ntn = gridDim.x;
+    const int L = xcd_tile(blockIdx.x, gridDim.x);
+    const int nt = L % ntn, mt = (L / ntn) % ntm, b = L / (ntn * ntm);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
     const int m0 = mt * BM, n0 = nt * BN;
@@ -383,8 +387,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
     auto row_ptr = [&](int r) -> const char * { return vbase + (size_t)rowtok[r] * d_bytes; };
 
     f32x4_t acc[G::FM][G::FN];
-    float ss[G::PPT];
-    G::template run<false>(row_ptr, 0, d_bytes / G::CHUNK, lds, acc, ss);
+    float ssa[G::FM], ssb[G::FN];
+    G::template run<false>(row_ptr, 0, d_bytes / G::CHUNK, acc, ssa, ssb);
 
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
@@ -770,10 +774,10 @@ static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int3
                                const int32_t *pruned, int Mp, const float *invn, float *best_val,
                                int32_t *best_slot, int32_t *assign, hipStream_t st) {
     const int esz = (DT == kBF16) ? 2 : 4;
-    dim3 grid((N1 + 127) / 128, (Mp + 127) / 128, B);
-    hipLaunchKernelGGL((gram_tile_kernel<DT, 128, 128, 2, 2>), grid, dim3(256), 0, st,
-                       (const char *)vis, Nv, d * esz, kept, N1, pruned, Mp, invn, best_val,
-                       best_slot, assign);
+    const int ntm = (Mp + kGramTileM - 1) / kGramTileM, ntn = (N1 + kGramTileN - 1) / kGramTileN;
+    hipLaunchKernelGGL((gram_tile_kernel<DT, kGramTileM, kGramTileN, 4, 2, 2>),
+                       dim3(B * ntm * ntn), dim3(512), 0, st, (const char *)vis, Nv, d * esz, kept,
+                       N1, pruned, Mp, invn, ntm, ntn, best_val, best_slot, assign);
     return hipGetLastError();
 }
 

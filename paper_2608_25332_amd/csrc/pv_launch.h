@@ -32,6 +32,8 @@ hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, co
 hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, int KS,
                               const float *invn, const int32_t *pruned, const int32_t *kept,
                               int32_t *assign, hipStream_t st);
+// Tile of the full-k Gram (pruned rows x kept rows) used for large inputs.
+constexpr int kGramTileM = 256, kGramTileN = 128;
 hipError_t launch_gram_tile(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                             int N1, const int32_t *pruned, int Mp, const float *invn,
                             float *best_val, int32_t *best_slot, int32_t *assign, hipStream_t st);

@@ -1,0 +1,194 @@
+// "Row x row" tile product on the matrix cores with operands streamed straight
+// into LDS (gfx950 global_load_lds_dwordx4).
+//
+// Same contract as TileGemm: C[m][n] = dot(A_row(m), B_row(n)) over a range
+// of 128-byte k chunks, rows addressed through a per-row pointer.  The
+// difference is the load path.  A direct-to-LDS load writes the 16 bytes of
+// lane i to LDS byte 16 * i of the instruction's 1 KB block without passing
+// through registers; on this chip one CU then sustains several times the
+// bytes per second that register loads reach, and the loads of the next
+// NSTAGE - 1 chunks stay in flight while the current one is multiplied.
+//
+// LDS layout of one stage: row r's 128-byte chunk occupies bytes
+// [128 r, 128 r + 128), its eight 16-byte pieces stored at slot
+// piece ^ (r & 7).  Because the destination of each lane is fixed, the
+// swizzle is applied on the global side: the lane that fills slot s of row r
+// loads piece s ^ (r & 7).  The fragment reads (16 rows at one piece) then
+// spread over the LDS banks.
+//
+// Ordering.  Before a stage is read, every wave waits for its own loads of
+// that stage (vmcnt), then all waves meet at a bare barrier: a __syncthreads
+// fence would also wait for the younger loads still in flight.  The fragment
+// reads are issued as inline assembly: the compiler cannot tell that they do
+// not touch the stages still being filled and would otherwise drain every
+// load in flight before each read.  Their completion is awaited explicitly
+// (lds_wait) and every fragment is tied to that wait before the MFMAs use it.
+#pragma once
+
+#include "pv_device.h"
+
+namespace pv {
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maximum).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier without a memory fence (see the ordering note above).
+__device__ __forceinline__ void bare_barrier() {
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef unsigned lds_u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 lds_read16(const char *p) {
+    lds_u32x4_t r;
+    const unsigned addr = (unsigned)(uintptr_t)p;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr) : "memory");
+    return uint4{r.x, r.y, r.z, r.w};
+}
+__device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Ties a fragment to the preceding lds_wait(): volatile asm statements keep
+// their order, so no use of the value can be scheduled before the wait.
+__device__ __forceinline__ void lds_after_wait(uint4 &v) {
+    lds_u32x4_t r = {v.x, v.y, v.z, v.w};
+    asm volatile("" : "+v"(r));
+    v = uint4{r.x, r.y, r.z, r.w};
+}
+
+template <int DT, int BM, int BN, int WM, int WN, int NSTAGE>
+struct TileGemmLds {
+    static constexpr int NT = 64 * WM * WN;
+    static constexpr int NW = WM * WN;
+    static constexpr int ROWS = BM + BN;
+    static constexpr int CHUNK = 128;
+    static constexpr int STAGE_BYTES = ROWS * CHUNK;
+    static constexpr int LDS_BYTES = NSTAGE * STAGE_BYTES;
+    static constexpr int IPW = ROWS * 8 / 64 / NW;  // load instructions per wave per stage
+    static constexpr int SUB_M = BM / WM, SUB_N = BN / WN;
+    static constexpr int FM = SUB_M / 16, FN = SUB_N / 16;
+    static_assert(ROWS * 8 % (64 * NW) == 0, "stage rows must split evenly over the waves");
+    static_assert(SUB_M % 16 == 0 && SUB_N % 16 == 0, "wave tile must be 16-aligned");
+    static_assert(NSTAGE >= 2 && NSTAGE <= 4, "two to four stages");
+    static_assert(IPW * (NSTAGE - 1) < 64, "loads in flight exceed the wait counter");
+
+    // Multiply chunks [c_begin, c_end) into acc.  row_ptr(r) is the global byte
+    // address of staged row r (r < BM: A rows, r >= BM: B rows); every row
+    // must be valid (clamp past-the-end rows in the caller).  With WANT_SS,
+    // ssa[fm] / ssb[fn] receive this lane's partial sums of squares of the A
+    // rows (waves with wn == 0) and B rows (waves with wm == 0) it reads; see
+    // row_sumsq.  Must be called by every thread of the workgroup.
+    template <bool WANT_SS, typename RowPtr>
+    __device__ __forceinline__ static void run(RowPtr row_ptr, int c_begin, int c_end,
+                                               f32x4_t (&acc)[FM][FN], float (&ssa)[FM],
+                                               float (&ssb)[FN]) {
+        __shared__ __attribute__((aligned(16))) char st0[STAGE_BYTES];
+        __shared__ __attribute__((aligned(16))) char st1[STAGE_BYTES];
+        __shared__ __attribute__((aligned(16))) char st2[NSTAGE > 2 ? STAGE_BYTES : 16];
+        __shared__ __attribute__((aligned(16))) char st3[NSTAGE > 3 ? STAGE_BYTES : 16];
+        auto stage = [&](int j) -> char * { return j == 0 ? st0 : j == 1 ? st1 : j == 2 ? st2 : st3; };
+
+        const int lane = threadIdx.x & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int wm = wave / WN, wn = wave % WN;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+            ssa[i] = 0.f;
+#pragma unroll
+            for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) ssb[j] = 0.f;
+        const int nc = c_end - c_begin;
+        if (nc <= 0) return;
+
+        // this lane's source row and piece for each of its IPW instructions
+        const char *src[IPW];
+#pragma unroll
+        for (int q = 0; q < IPW; ++q) {
+            const int pos = (wave * IPW + q) * 64 + lane;  // 16-byte slot in the stage
+            const int r = pos >> 3, slot = pos & 7;
+            src[q] = row_ptr(r) + (size_t)c_begin * CHUNK + ((slot ^ (r & 7)) << 4);
+        }
+        // chunk i (relative to c_begin) goes to stage i % NSTAGE
+        auto issue = [&](int i, int j) {
+            char *dst = stage(j) + wave * IPW * 1024;
+#pragma unroll
+            for (int q = 0; q < IPW; ++q)
+                __builtin_amdgcn_global_load_lds(src[q] + (size_t)i * CHUNK,
+                                                 (lds_void_t *)(dst + q * 1024), 16, 0, 0);
+        };
+#pragma unroll
+        for (int p = 0; p < NSTAGE - 1; ++p)
+            if (p < nc) issue(p, p);
+
+        const int a_row = wm * SUB_M + (lane & 15);
+        const int b_row = BM + wn * SUB_N + (lane & 15);
+        const int kq = lane >> 4;  // 16-byte quarter of the 64-byte window
+        for (int i0 = 0; i0 < nc; i0 += NSTAGE) {
+#pragma unroll
+            for (int j = 0; j < NSTAGE; ++j) {
+                const int i = i0 + j;
+                if (i >= nc) break;
+                // this wave's loads of chunk i are done once at most the loads
+                // of the younger chunks already issued are outstanding
+                if (i + NSTAGE - 1 <= nc) wait_vmcnt<IPW * (NSTAGE - 2)>();
+                else wait_vmcnt<0>();
+                bare_barrier();  // all of chunk i is in LDS; chunk i - 1 has been read
+                if (i + NSTAGE - 1 < nc) issue(i + NSTAGE - 1, (j + NSTAGE - 1) % NSTAGE);
+                const char *sp = stage(j);
+#pragma unroll
+                for (int s = 0; s < 2; ++s) {
+                    const int piece = s * 4 + kq;
+                    uint4 af[FM], bfr[FN];
+#pragma unroll
+                    for (int f = 0; f < FM; ++f) {
+                        const int r = a_row + f * 16;
+                        af[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
+                    }
+#pragma unroll
+                    for (int f = 0; f < FN; ++f) {
+                        const int r = b_row + f * 16;
+                        bfr[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
+                    }
+                    lds_wait();
+#pragma unroll
+                    for (int f = 0; f < FM; ++f) lds_after_wait(af[f]);
+#pragma unroll
+                    for (int f = 0; f < FN; ++f) lds_after_wait(bfr[f]);
+                    if (WANT_SS) {
+                        if (wn == 0) {
+#pragma unroll
+                            for (int f = 0; f < FM; ++f) ssa[f] += sumsq16<DT>(af[f]);
+                        }
+                        if (wm == 0) {
+#pragma unroll
+                            for (int f = 0; f < FN; ++f) ssb[f] += sumsq16<DT>(bfr[f]);
+                        }
+                    }
+#pragma unroll
+                    for (int f = 0; f < FM; ++f)
+#pragma unroll
+                        for (int g = 0; g < FN; ++g) acc[f][g] = mma16<DT>(af[f], bfr[g], acc[f][g]);
+                }
+            }
+        }
+        bare_barrier();  // the stages may be reused by a later call
+    }
+
+    // Sum of squares of row (lane & 15) of a fragment block: combines the four
+    // 16-byte quarters held by lanes l, l+16, l+32, l+48 in a fixed order.
+    __device__ __forceinline__ static float row_sumsq(float partial) {
+        partial += __shfl_xor(partial, 16, 64);
+        partial += __shfl_xor(partial, 32, 64);
+        return partial;
+    }
+};
+
+}  // namespace pv

@@ -184,6 +184,10 @@ DEDUP_EDGE = [
     (1, 40, 4, 192, 1, "bf16"),
     (1, 40, 4, 256, 3, "bf16"),
     (2, 40, 4, 320, 7, "f32"),
+    # full-k Gram tiles: one kept tile (slot written directly), and two kept
+    # tiles in fp32 (per-tile candidates merged by gram_finish)
+    (128, 300, 4, 64, 100, "bf16"),
+    (64, 600, 4, 128, 200, "f32"),
     # merge through bucketed member lists (narrow rows, many slots)
     (1, 1000, 8, 64, 70, "bf16"),
     (2, 700, 5, 128, 200, "f32"),
