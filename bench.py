@@ -156,7 +156,7 @@ class Step:
 
 # kernel -> the stage of the hot path it belongs to
 STAGE_OF = {
-    "cos_partial": "cosine", "cos_reduce": "cosine", "center": "cosine",
+    "cos_full": "cosine", "cos_partial": "cosine", "cos_reduce": "cosine", "center": "cosine",
     "select": "select", "gram_partial": "gram", "gram_reduce": "gram", "gram_tile": "gram",
     "gram_finish": "gram", "bucket": "merge", "merge": "merge", "gather_kv1": "kv_of_kept",
     "score_partial": "head_aware", "score_select": "head_aware", "gather_hkv2": "gather",
@@ -177,6 +177,9 @@ def algorithmic(w):
     kern = {
         # cosine products: read the visual tokens and the anchors once
         "cos_partial": dict(bytes=B * (Nv + Nt) * d * e, flops=2.0 * B * Nt * Nv * d),
+        # one-pass cosine: read the visual tokens and anchors, write M and norms
+        "cos_full": dict(bytes=B * (Nv + Nt) * d * e + B * (Nt * Nv + Nv) * 4,
+                         flops=2.0 * B * Nt * Nv * d),
         # cosines: write M and the inverse token norms
         "cos_reduce": dict(bytes=B * (Nt * Nv + Nv) * 4, flops=3.0 * B * Nt * Nv),
         # centring + max-pool: read M, write p

@@ -72,11 +72,11 @@ long long n_tiles(int rows_m, int rows_n, int B, int t) {
     return (long long)((rows_m + t - 1) / t) * ((rows_n + t - 1) / t) * B;
 }
 
-// k slices of a split-k product: about one workgroup per CU (256 CUs), at
-// least two 128-byte chunks in every slice.
+// k slices of a split-k product: about three workgroups per CU (256 CUs; three
+// 48 KB LDS rings fit one CU), at least four 128-byte chunks in every slice.
 int pick_slices(long long tiles, int nchunks) {
-    long long ks = (250 + tiles - 1) / tiles;
-    const long long max_ks = nchunks / 2 > 1 ? nchunks / 2 : 1;
+    long long ks = (768 + tiles / 2) / tiles;
+    const long long max_ks = nchunks / 4 > 1 ? nchunks / 4 : 1;
     if (ks > max_ks) ks = max_ks;
     if (ks < 1) ks = 1;
     return (int)ks;
@@ -84,6 +84,7 @@ int pick_slices(long long tiles, int nchunks) {
 
 struct DedupPlan {
     int nch;                       // 128-byte k chunks per row
+    bool cos_full;                 // cosine in one full-k pass (small inputs)
     int ks_cos, njt;               // cosine: k slices, token tiles of the row sums
     int Mp;
     bool gram_big;                 // full-k 256x128 tiles (operands streamed into LDS)
@@ -101,7 +102,8 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
     P.nch = d * esz / 128;
     const int T = pv::kSplitTile;
     P.ks_cos = pick_slices(n_tiles(Nv, Nt, B, T), P.nch);
-    P.njt = pv::cos_row_tiles(Nv);
+    P.cos_full = pv::cos_use_full(B, Nv, Nt, d * esz);
+    P.njt = P.cos_full ? pv::cos_full_row_tiles(Nv) : pv::cos_row_tiles(Nv);
     P.Mp = Nv - budget;
     const int Mp1 = P.Mp > 0 ? P.Mp : 1;
     P.gram_big = (long long)((Mp1 + pv::kGramTileM - 1) / pv::kGramTileM) *
@@ -109,9 +111,13 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
     P.ks_gram = P.gram_big ? 1 : pick_slices(n_tiles(Mp1, budget, B, T), P.nch);
     P.ntn = P.gram_big ? (budget + pv::kGramTileN - 1) / pv::kGramTileN : 1;
     Carve c(ws);
-    P.cpart = c.take<float>((size_t)P.ks_cos * B * Nt * Nv);
-    P.ssv = c.take<float>((size_t)P.ks_cos * B * Nv);
-    P.ssa = c.take<float>((size_t)P.ks_cos * B * Nt);
+    if (P.cos_full) {
+        P.cpart = P.ssv = P.ssa = nullptr;
+    } else {
+        P.cpart = c.take<float>((size_t)P.ks_cos * B * Nt * Nv);
+        P.ssv = c.take<float>((size_t)P.ks_cos * B * Nv);
+        P.ssa = c.take<float>((size_t)P.ks_cos * B * Nt);
+    }
     P.M = c.take<float>((size_t)B * Nt * Nv);
     P.rowsum = c.take<float>((size_t)B * P.njt * Nt);
     P.invn = c.take<float>((size_t)B * Nv);
@@ -186,16 +192,24 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     hipStream_t st = (hipStream_t)stream;
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
-    if (!tr.launch("cos_partial", [&] {
-            return pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart, P.ssv,
-                                          P.ssa, st);
-        }))
-        return PV_ERR_HIP;
-    if (!tr.launch("cos_reduce", [&] {
-            return pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M, P.rowsum,
-                                         P.invn, st);
-        }))
-        return PV_ERR_HIP;
+    if (P.cos_full) {
+        if (!tr.launch("cos_full", [&] {
+                return pv::launch_cos_full(dt, vis, anchors, B, Nv, Nt, d, P.M, P.rowsum, P.invn,
+                                           st);
+            }))
+            return PV_ERR_HIP;
+    } else {
+        if (!tr.launch("cos_partial", [&] {
+                return pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart,
+                                              P.ssv, P.ssa, st);
+            }))
+            return PV_ERR_HIP;
+        if (!tr.launch("cos_reduce", [&] {
+                return pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M,
+                                             P.rowsum, P.invn, st);
+            }))
+            return PV_ERR_HIP;
+    }
     if (!tr.launch("center", [&] {
             return pv::launch_center(P.M, P.rowsum, P.njt, B, Nt, Nv, p, st);
         }))

@@ -19,7 +19,6 @@
 // dependency is a kernel boundary, so no kernel needs a device-wide fence
 // (on this chip a device-scope fence writes back and invalidates the L2).
 #include "pv_launch.h"
-#include "pv_tile_gemm.h"
 #include "pv_tile_lds.h"
 
 #include <math.h>
@@ -30,29 +29,27 @@ namespace pv {
 // Split-k products (the cosine, and the Grams that are too small to fill the
 // chip with full-k tiles).
 //
-// A workgroup owns a 64 x 64 output tile and one k slice of its rows (LDS-
-// staged, see pv_tile_gemm.h); the k slices are added in slice order by the
+// A workgroup owns a 64 x 64 output tile and one k slice of its rows (streamed
+// into LDS, see pv_tile_lds.h); the k slices are added in slice order by the
 // reduce kernels.  Slicing k spreads a B=1 problem over every CU while each
 // CU fetches only a few tens of KB; the price is KS fp32 partial tiles, which
 // stay in L2.
 // ----------------------------------------------------------------------------
 constexpr int kPT = 64;  // tile edge of the split-k products
-template <int DT>
-using PTile = TileGemm<DT, kPT, kPT, 2, 2, 2>;
+template <int DT, int NS>
+using PTile = TileGemmLds<DT, kPT, kPT, 2, 2, NS>;
 
 // cos_partial: 1-D grid over (sample, k slice, anchor tile, token tile) in XCD
 // order (token tiles of one anchor tile and slice are adjacent: they share the
 // anchor rows).  Writes partial dot products part[ks][b][Nt][Nv] and partial
 // sums of squares of the token rows ssv[ks][b][Nv] and anchor rows
 // ssa[ks][b][Nt].
-template <int DT>
+template <int DT, int NS>
 __global__ __launch_bounds__(256) void cos_partial_kernel(
     const char *__restrict__ vis, const char *__restrict__ anchors, int B, int Nv, int Nt,
     int d_bytes, int njt, int nit, int KS, float *__restrict__ part, float *__restrict__ ssv,
     float *__restrict__ ssa) {
-    using G = PTile<DT>;
-    __shared__ __attribute__((aligned(16))) char lds[G::LDS_BYTES];
-    __shared__ float rowss[G::ROWS];
+    using G = PTile<DT, NS>;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / 2, wn = wave % 2;
@@ -72,9 +69,8 @@ __global__ __launch_bounds__(256) void cos_partial_kernel(
     const int nch = d_bytes / G::CHUNK;
     const int c0 = (int)(((long long)nch * ks) / KS), c1 = (int)(((long long)nch * (ks + 1)) / KS);
     f32x4_t acc[G::FM][G::FN];
-    float ss[G::PPT];
-    G::template run<true>(row_ptr, c0, c1, lds, acc, ss);
-    G::reduce_rows(ss, rowss);
+    float sa[G::FM], sb[G::FN];
+    G::template run<true>(row_ptr, c0, c1, acc, sa, sb);
     const size_t kb = (size_t)ks * B + b;
     float *pb = part + kb * Nt * Nv;
 #pragma unroll
@@ -88,12 +84,23 @@ __global__ __launch_bounds__(256) void cos_partial_kernel(
                 if (i < Nt && j < Nv) pb[(size_t)i * Nv + j] = acc[fm][fn][e];
             }
         }
-    __syncthreads();
-    if (tid < kPT) {
-        if (jt == 0 && i0 + tid < Nt) ssa[kb * Nt + i0 + tid] = rowss[tid];
-    } else if (tid < 2 * kPT) {
-        const int j = j0 + tid - kPT;
-        if (it == 0 && j < Nv) ssv[kb * Nv + j] = rowss[tid];
+    // sums of squares: anchor rows from the waves of the first column, token
+    // rows from the waves of the first row (each row read by exactly one)
+    if (wn == 0 && jt == 0) {
+#pragma unroll
+        for (int f = 0; f < G::FM; ++f) {
+            const float v = G::row_sumsq(sa[f]);
+            const int i = i0 + wm * G::SUB_M + f * 16 + (lane & 15);
+            if (lane < 16 && i < Nt) ssa[kb * Nt + i] = v;
+        }
+    }
+    if (wm == 0 && it == 0) {
+#pragma unroll
+        for (int f = 0; f < G::FN; ++f) {
+            const float v = G::row_sumsq(sb[f]);
+            const int j = j0 + wn * G::SUB_N + f * 16 + (lane & 15);
+            if (lane < 16 && j < Nv) ssv[kb * Nv + j] = v;
+        }
     }
 }
 
@@ -148,6 +155,118 @@ __global__ __launch_bounds__(256) void cos_reduce_kernel(
 }
 
 // ----------------------------------------------------------------------------
+// cos_full: the cosine for small inputs (one sample of LLaVA-1.5 size), where
+// a split-k pass plus its reduction costs two launches for a few MB.  1-D grid
+// over (sample, anchor tile, token tile) of 16 x 16 tiles in XCD order, 512
+// threads.  Each workgroup computes its tile of M over the whole k range: the
+// eight waves take an eighth of k each and stream their part of the 32 rows
+// straight into their own LDS ring, so the k loop needs no barrier.  The wave
+// results are added in wave order; the tile then writes M, its per-anchor row
+// sums over its 16 tokens (rowsum[b][token tile][Nt]) and, for the first anchor
+// tile, the inverse token norms.
+// ----------------------------------------------------------------------------
+constexpr int kFT = 16;   // tile edge
+
+template <int DT, int NW, int kFNS>
+__global__ __launch_bounds__(64 * NW) void cos_full_kernel(
+    const char *__restrict__ vis, const char *__restrict__ anchors, int Nv, int Nt, int d_bytes,
+    int nit, int njt, float *__restrict__ M, float *__restrict__ rowsum,
+    float *__restrict__ invn_vis) {
+    constexpr int ROWS = 2 * kFT, STAGE = ROWS * 128, IPW = STAGE / 1024;
+    __shared__ __attribute__((aligned(16))) char ring[NW][kFNS][STAGE];
+    __shared__ float accb[NW][kFT][kFT];
+    __shared__ float ssab[NW][kFT], ssvb[NW][kFT];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int L = xcd_tile(blockIdx.x, gridDim.x);
+    const int jt = L % njt, it = (L / njt) % nit, b = L / (njt * nit);
+    const int i0 = it * kFT, j0 = jt * kFT;
+    const char *abase = anchors + (size_t)b * Nt * d_bytes;
+    const char *vbase = vis + (size_t)b * Nv * d_bytes;
+    const int nch = d_bytes / 128;
+    const int c0 = nch * wave / NW, c1 = nch * (wave + 1) / NW;
+    const int nc = c1 - c0;
+
+    // this lane's row and piece for each of the IPW loads of a chunk
+    const char *src[IPW];
+#pragma unroll
+    for (int q = 0; q < IPW; ++q) {
+        const int pos = q * 64 + lane;
+        const int r = pos >> 3, slot = pos & 7;
+        const char *row = (r < kFT) ? abase + (size_t)min(i0 + r, Nt - 1) * d_bytes
+                                    : vbase + (size_t)min(j0 + r - kFT, Nv - 1) * d_bytes;
+        src[q] = row + (size_t)c0 * 128 + ((slot ^ (r & 7)) << 4);
+    }
+    auto issue = [&](int i) {
+        char *dst = ring[wave][i % kFNS];
+#pragma unroll
+        for (int q = 0; q < IPW; ++q)
+            __builtin_amdgcn_global_load_lds(src[q] + (size_t)i * 128, (lds_void_t *)(dst + q * 1024),
+                                             16, 0, 0);
+    };
+#pragma unroll
+    for (int pp = 0; pp < kFNS - 1; ++pp)
+        if (pp < nc) issue(pp);
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    float sa = 0.f, sv = 0.f;
+    const int kq = lane >> 4, ra = lane & 15, rv = kFT + (lane & 15);
+    for (int i = 0; i < nc; ++i) {
+        if (i + kFNS - 1 <= nc) wait_vmcnt<IPW * (kFNS - 2)>();
+        else wait_vmcnt<0>();
+        if (i + kFNS - 1 < nc) issue(i + kFNS - 1);
+        const char *sp = ring[wave][i % kFNS];
+        uint4 a[2], v[2];
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {  // both 64-byte windows of the chunk, one wait
+            const int piece = s2 * 4 + kq;
+            a[s2] = lds_read16(sp + ra * 128 + ((piece ^ (ra & 7)) << 4));
+            v[s2] = lds_read16(sp + rv * 128 + ((piece ^ (rv & 7)) << 4));
+        }
+        lds_wait();
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+            lds_after_wait(a[s2]);
+            lds_after_wait(v[s2]);
+            sa += sumsq16<DT>(a[s2]);
+            sv += sumsq16<DT>(v[s2]);
+            acc = mma16<DT>(a[s2], v[s2], acc);
+        }
+    }
+    // the four quarters of each row's sum of squares, in a fixed order
+    sa += __shfl_xor(sa, 16, 64);
+    sa += __shfl_xor(sa, 32, 64);
+    sv += __shfl_xor(sv, 16, 64);
+    sv += __shfl_xor(sv, 32, 64);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) accb[wave][4 * kq + e][lane & 15] = acc[e];
+    if (lane < kFT) {
+        ssab[wave][lane] = sa;
+        ssvb[wave][lane] = sv;
+    }
+    __syncthreads();
+    if (tid >= kFT * kFT) return;  // no barrier follows
+    // one output per thread: anchor ii, token jj; waves added in order
+    const int ii = tid >> 4, jj = tid & 15;
+    float dot = 0.f, a2 = 0.f, v2 = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+        dot += accb[w][ii][jj];
+        a2 += ssab[w][ii];
+        v2 += ssvb[w][jj];
+    }
+    const float inv_a = (a2 > 0.f) ? 1.0f / sqrtf(a2) : 0.f;
+    const float inv_v = (v2 > 0.f) ? 1.0f / sqrtf(v2) : 0.f;
+    const int i = i0 + ii, j = j0 + jj;
+    const float cs = dot * inv_a * inv_v;
+    if (i < Nt && j < Nv) M[((size_t)b * Nt + i) * Nv + j] = cs;
+    if (it == 0 && ii == 0 && j < Nv) invn_vis[(size_t)b * Nv + j] = inv_v;
+    float rs = (j < Nv) ? cs : 0.f;
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) rs += __shfl_xor(rs, off, 64);
+    if (jj == 0 && i < Nt) rowsum[((size_t)b * njt + jt) * Nt + i] = rs;
+}
+
+// ----------------------------------------------------------------------------
 // center: grid (ceil(Nv / 64), B), 256 threads; 4 threads per token.
 // ----------------------------------------------------------------------------
 constexpr int kCenNT = 256;
@@ -164,8 +283,14 @@ __global__ __launch_bounds__(kCenNT) void center_kernel(const float *__restrict_
     for (int i = tid; i < Nt; i += kCenNT) {
         const float *rs = rowsum + (size_t)b * njt * Nt + i;
         float s = 0.f;
-#pragma unroll 8
-        for (int t = 0; t < njt; ++t) s += rs[(size_t)t * Nt];
+        for (int t0 = 0; t0 < njt; t0 += 16) {
+            float v[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) v[u] = rs[(size_t)min(t0 + u, njt - 1) * Nt];
+#pragma unroll
+            for (int u = 0; u < 16; ++u)
+                if (t0 + u < njt) s += v[u];
+        }
         mu[i] = s / (float)Nv;
     }
     __syncthreads();
@@ -241,13 +366,12 @@ __global__ __launch_bounds__(kFinNT) void gram_finish_kernel(const float *__rest
 // gram_partial: 1-D grid over (sample, k slice, kept tile, pruned tile) in
 // XCD order (pruned tiles of one kept tile and slice are adjacent: they share
 // the kept rows).  Writes partial dot products part[ks][b][Mp][N1].
-template <int DT>
+template <int DT, int NS>
 __global__ __launch_bounds__(256) void gram_partial_kernel(
     const char *__restrict__ vis, int B, int Nv, int d_bytes, const int32_t *__restrict__ kept,
     int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn, int KS,
     float *__restrict__ part) {
-    using G = PTile<DT>;
-    __shared__ __attribute__((aligned(16))) char lds[G::LDS_BYTES];
+    using G = PTile<DT, NS>;
     __shared__ int32_t rowtok[G::ROWS];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -269,8 +393,8 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(
     const int nch = d_bytes / G::CHUNK;
     const int c0 = (int)(((long long)nch * ks) / KS), c1 = (int)(((long long)nch * (ks + 1)) / KS);
     f32x4_t acc[G::FM][G::FN];
-    float ss[G::PPT];
-    G::template run<false>(row_ptr, c0, c1, lds, acc, ss);
+    float sa[G::FM], sb[G::FN];
+    G::template run<false>(row_ptr, c0, c1, acc, sa, sb);
     float *pb = part + ((size_t)ks * B + b) * Mp * N1;
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm)
@@ -721,17 +845,30 @@ __global__ __launch_bounds__(kMergeNT) void merge_csr_kernel(
 // ----------------------------------------------------------------------------
 // launchers
 // ----------------------------------------------------------------------------
+// Ring depth of the split-k tiles: three 16 KB stages.  Measured: a deeper
+// ring costs more (fewer workgroups fit a CU) than the extra loads in flight
+// gain.
+constexpr int kSplitNS = 3;
+
+template <int DT, int NS>
+static void cos_partial_go(dim3 grid, const void *vis, const void *anchors, int B, int Nv, int Nt,
+                           int d_bytes, int njt, int nit, int KS, float *part, float *ssv,
+                           float *ssa, hipStream_t st) {
+    hipLaunchKernelGGL((cos_partial_kernel<DT, NS>), grid, dim3(256), 0, st, (const char *)vis,
+                       (const char *)anchors, B, Nv, Nt, d_bytes, njt, nit, KS, part, ssv, ssa);
+}
+
 hipError_t launch_cos_partial(int dt, const void *vis, const void *anchors, int B, int Nv, int Nt,
                               int d, int KS, float *part, float *ssv, float *ssa, hipStream_t st) {
-    const int esz = (dt == kBF16) ? 2 : 4;
+    const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
     const int njt = (Nv + kPT - 1) / kPT, nit = (Nt + kPT - 1) / kPT;
-    const dim3 grid(B * KS * nit * njt), block(256);
+    const dim3 grid(B * KS * nit * njt);
     if (dt == kBF16)
-        hipLaunchKernelGGL(cos_partial_kernel<kBF16>, grid, block, 0, st, (const char *)vis,
-                           (const char *)anchors, B, Nv, Nt, d * esz, njt, nit, KS, part, ssv, ssa);
+        cos_partial_go<kBF16, kSplitNS>(grid, vis, anchors, B, Nv, Nt, d_bytes, njt, nit, KS, part,
+                                        ssv, ssa, st);
     else
-        hipLaunchKernelGGL(cos_partial_kernel<kF32>, grid, block, 0, st, (const char *)vis,
-                           (const char *)anchors, B, Nv, Nt, d * esz, njt, nit, KS, part, ssv, ssa);
+        cos_partial_go<kF32, kSplitNS>(grid, vis, anchors, B, Nv, Nt, d_bytes, njt, nit, KS, part,
+                                       ssv, ssa, st);
     return hipGetLastError();
 }
 
@@ -744,6 +881,24 @@ hipError_t launch_cos_reduce(const float *part, const float *ssv, const float *s
 }
 
 int cos_row_tiles(int Nv) { return (Nv + kRedTok - 1) / kRedTok; }
+int cos_full_row_tiles(int Nv) { return (Nv + kFT - 1) / kFT; }
+constexpr int kFullW = 8, kFullNS = 2;  // waves (k slices) and ring stages of cos_full
+
+hipError_t launch_cos_full(int dt, const void *vis, const void *anchors, int B, int Nv, int Nt,
+                           int d, float *M, float *rowsum, float *invn, hipStream_t st) {
+    const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
+    const int nit = (Nt + kFT - 1) / kFT, njt = (Nv + kFT - 1) / kFT;
+    const dim3 grid(B * nit * njt);
+    if (dt == kBF16)
+        hipLaunchKernelGGL((cos_full_kernel<kBF16, kFullW, kFullNS>), grid, dim3(64 * kFullW), 0, st,
+                           (const char *)vis, (const char *)anchors, Nv, Nt, d_bytes, nit, njt, M,
+                           rowsum, invn);
+    else
+        hipLaunchKernelGGL((cos_full_kernel<kF32, kFullW, kFullNS>), grid, dim3(64 * kFullW), 0, st,
+                           (const char *)vis, (const char *)anchors, Nv, Nt, d_bytes, nit, njt, M,
+                           rowsum, invn);
+    return hipGetLastError();
+}
 
 hipError_t launch_center(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
                          float *p, hipStream_t st) {
@@ -781,18 +936,26 @@ static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int3
     return hipGetLastError();
 }
 
+template <int DT, int NS>
+static void gram_partial_go(dim3 grid, const void *vis, int B, int Nv, int d_bytes,
+                            const int32_t *kept, int N1, const int32_t *pruned, int Mp, int ntm,
+                            int ntn, int KS, float *part, hipStream_t st) {
+    hipLaunchKernelGGL((gram_partial_kernel<DT, NS>), grid, dim3(256), 0, st, (const char *)vis, B,
+                       Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS, part);
+}
+
 hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                                int N1, const int32_t *pruned, int Mp, int KS, float *part,
                                hipStream_t st) {
-    const int esz = (dt == kBF16) ? 2 : 4;
+    const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
     const int ntm = (Mp + kPT - 1) / kPT, ntn = (N1 + kPT - 1) / kPT;
-    const dim3 grid(B * KS * ntm * ntn), block(256);
+    const dim3 grid(B * KS * ntm * ntn);
     if (dt == kBF16)
-        hipLaunchKernelGGL(gram_partial_kernel<kBF16>, grid, block, 0, st, (const char *)vis, B, Nv,
-                           d * esz, kept, N1, pruned, Mp, ntm, ntn, KS, part);
+        gram_partial_go<kBF16, kSplitNS>(grid, vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn,
+                                         KS, part, st);
     else
-        hipLaunchKernelGGL(gram_partial_kernel<kF32>, grid, block, 0, st, (const char *)vis, B, Nv,
-                           d * esz, kept, N1, pruned, Mp, ntm, ntn, KS, part);
+        gram_partial_go<kF32, kSplitNS>(grid, vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn,
+                                        KS, part, st);
     return hipGetLastError();
 }
 

@@ -18,6 +18,16 @@ struct HeadArgs {
 // ---- pruning before the LLM (Sec. 4.3)
 constexpr int kSplitTile = 64;  // tile edge of the split-k products
 int cos_row_tiles(int Nv);      // token tiles of the row sums written by cos_reduce
+int cos_full_row_tiles(int Nv); // token tiles of the row sums written by cos_full
+// Whether the cosine runs as one full-k pass over 16 x 16 tiles (small inputs:
+// the rows it re-reads, one copy per tile row and column, stay under 48 MB).
+inline bool cos_use_full(int B, int Nv, int Nt, int d_bytes) {
+    const double reread = (double)B * d_bytes *
+                          ((double)((Nt + 15) / 16) * Nv + (double)((Nv + 15) / 16) * Nt);
+    return reread <= 48.0 * (1 << 20);
+}
+hipError_t launch_cos_full(int dt, const void *vis, const void *anchors, int B, int Nv, int Nt,
+                           int d, float *M, float *rowsum, float *invn, hipStream_t st);
 hipError_t launch_cos_partial(int dt, const void *vis, const void *anchors, int B, int Nv, int Nt,
                               int d, int KS, float *part, float *ssv, float *ssa, hipStream_t st);
 hipError_t launch_cos_reduce(const float *part, const float *ssv, const float *ssa, int B, int Nv,

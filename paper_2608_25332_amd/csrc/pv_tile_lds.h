@@ -16,6 +16,8 @@
 // loads piece s ^ (r & 7).  The fragment reads (16 rows at one piece) then
 // spread over the LDS banks.
 //
+// The stages form one ring; chunk i of the range goes to stage i % NSTAGE.
+//
 // Ordering.  Before a stage is read, every wave waits for its own loads of
 // that stage (vmcnt), then all waves meet at a bare barrier: a __syncthreads
 // fence would also wait for the younger loads still in flight.  The fragment
@@ -75,7 +77,7 @@ struct TileGemmLds {
     static constexpr int FM = SUB_M / 16, FN = SUB_N / 16;
     static_assert(ROWS * 8 % (64 * NW) == 0, "stage rows must split evenly over the waves");
     static_assert(SUB_M % 16 == 0 && SUB_N % 16 == 0, "wave tile must be 16-aligned");
-    static_assert(NSTAGE >= 2 && NSTAGE <= 4, "two to four stages");
+    static_assert(NSTAGE >= 2, "at least double buffering");
     static_assert(IPW * (NSTAGE - 1) < 64, "loads in flight exceed the wait counter");
 
     // Multiply chunks [c_begin, c_end) into acc.  row_ptr(r) is the global byte
@@ -88,12 +90,7 @@ struct TileGemmLds {
     __device__ __forceinline__ static void run(RowPtr row_ptr, int c_begin, int c_end,
                                                f32x4_t (&acc)[FM][FN], float (&ssa)[FM],
                                                float (&ssb)[FN]) {
-        __shared__ __attribute__((aligned(16))) char st0[STAGE_BYTES];
-        __shared__ __attribute__((aligned(16))) char st1[STAGE_BYTES];
-        __shared__ __attribute__((aligned(16))) char st2[NSTAGE > 2 ? STAGE_BYTES : 16];
-        __shared__ __attribute__((aligned(16))) char st3[NSTAGE > 3 ? STAGE_BYTES : 16];
-        auto stage = [&](int j) -> char * { return j == 0 ? st0 : j == 1 ? st1 : j == 2 ? st2 : st3; };
-
+        __shared__ __attribute__((aligned(16))) char ring[NSTAGE][STAGE_BYTES];
         const int lane = threadIdx.x & 63;
         const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
         const int wm = wave / WN, wn = wave % WN;
@@ -117,8 +114,8 @@ struct TileGemmLds {
             src[q] = row_ptr(r) + (size_t)c_begin * CHUNK + ((slot ^ (r & 7)) << 4);
         }
         // chunk i (relative to c_begin) goes to stage i % NSTAGE
-        auto issue = [&](int i, int j) {
-            char *dst = stage(j) + wave * IPW * 1024;
+        auto issue = [&](int i) {
+            char *dst = ring[i % NSTAGE] + wave * IPW * 1024;
 #pragma unroll
             for (int q = 0; q < IPW; ++q)
                 __builtin_amdgcn_global_load_lds(src[q] + (size_t)i * CHUNK,
@@ -126,57 +123,52 @@ struct TileGemmLds {
         };
 #pragma unroll
         for (int p = 0; p < NSTAGE - 1; ++p)
-            if (p < nc) issue(p, p);
+            if (p < nc) issue(p);
 
         const int a_row = wm * SUB_M + (lane & 15);
         const int b_row = BM + wn * SUB_N + (lane & 15);
         const int kq = lane >> 4;  // 16-byte quarter of the 64-byte window
-        for (int i0 = 0; i0 < nc; i0 += NSTAGE) {
+        for (int i = 0; i < nc; ++i) {
+            // this wave's loads of chunk i are done once at most the loads of
+            // the younger chunks already issued are outstanding
+            if (i + NSTAGE - 1 <= nc) wait_vmcnt<IPW * (NSTAGE - 2)>();
+            else wait_vmcnt<0>();
+            bare_barrier();  // all of chunk i is in LDS; chunk i - 1 has been read
+            if (i + NSTAGE - 1 < nc) issue(i + NSTAGE - 1);
+            const char *sp = ring[i % NSTAGE];
 #pragma unroll
-            for (int j = 0; j < NSTAGE; ++j) {
-                const int i = i0 + j;
-                if (i >= nc) break;
-                // this wave's loads of chunk i are done once at most the loads
-                // of the younger chunks already issued are outstanding
-                if (i + NSTAGE - 1 <= nc) wait_vmcnt<IPW * (NSTAGE - 2)>();
-                else wait_vmcnt<0>();
-                bare_barrier();  // all of chunk i is in LDS; chunk i - 1 has been read
-                if (i + NSTAGE - 1 < nc) issue(i + NSTAGE - 1, (j + NSTAGE - 1) % NSTAGE);
-                const char *sp = stage(j);
+            for (int s = 0; s < 2; ++s) {
+                const int piece = s * 4 + kq;
+                uint4 af[FM], bfr[FN];
 #pragma unroll
-                for (int s = 0; s < 2; ++s) {
-                    const int piece = s * 4 + kq;
-                    uint4 af[FM], bfr[FN];
-#pragma unroll
-                    for (int f = 0; f < FM; ++f) {
-                        const int r = a_row + f * 16;
-                        af[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
-                    }
-#pragma unroll
-                    for (int f = 0; f < FN; ++f) {
-                        const int r = b_row + f * 16;
-                        bfr[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
-                    }
-                    lds_wait();
-#pragma unroll
-                    for (int f = 0; f < FM; ++f) lds_after_wait(af[f]);
-#pragma unroll
-                    for (int f = 0; f < FN; ++f) lds_after_wait(bfr[f]);
-                    if (WANT_SS) {
-                        if (wn == 0) {
-#pragma unroll
-                            for (int f = 0; f < FM; ++f) ssa[f] += sumsq16<DT>(af[f]);
-                        }
-                        if (wm == 0) {
-#pragma unroll
-                            for (int f = 0; f < FN; ++f) ssb[f] += sumsq16<DT>(bfr[f]);
-                        }
-                    }
-#pragma unroll
-                    for (int f = 0; f < FM; ++f)
-#pragma unroll
-                        for (int g = 0; g < FN; ++g) acc[f][g] = mma16<DT>(af[f], bfr[g], acc[f][g]);
+                for (int f = 0; f < FM; ++f) {
+                    const int r = a_row + f * 16;
+                    af[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
                 }
+#pragma unroll
+                for (int f = 0; f < FN; ++f) {
+                    const int r = b_row + f * 16;
+                    bfr[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
+                }
+                lds_wait();
+#pragma unroll
+                for (int f = 0; f < FM; ++f) lds_after_wait(af[f]);
+#pragma unroll
+                for (int f = 0; f < FN; ++f) lds_after_wait(bfr[f]);
+                if (WANT_SS) {
+                    if (wn == 0) {
+#pragma unroll
+                        for (int f = 0; f < FM; ++f) ssa[f] += sumsq16<DT>(af[f]);
+                    }
+                    if (wm == 0) {
+#pragma unroll
+                        for (int f = 0; f < FN; ++f) ssb[f] += sumsq16<DT>(bfr[f]);
+                    }
+                }
+#pragma unroll
+                for (int f = 0; f < FM; ++f)
+#pragma unroll
+                    for (int g = 0; g < FN; ++g) acc[f][g] = mma16<DT>(af[f], bfr[g], acc[f][g]);
             }
         }
         bare_barrier();  // the stages may be reused by a later call

@@ -184,6 +184,9 @@ DEDUP_EDGE = [
     (1, 40, 4, 192, 1, "bf16"),
     (1, 40, 4, 256, 3, "bf16"),
     (2, 40, 4, 320, 7, "f32"),
+    # split-k cosine (batches too large for the full-k small-input pass)
+    (64, 200, 33, 1024, 70, "bf16"),
+    (48, 150, 5, 2048, 40, "f32"),
     # full-k Gram tiles: one kept tile (slot written directly), and two kept
     # tiles in fp32 (per-tile candidates merged by gram_finish)
     (128, 300, 4, 64, 100, "bf16"),
