@@ -133,7 +133,7 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
         P.best_val = nullptr;
         P.best_slot = nullptr;
     }
-    P.lists = want_merged && pv::merge_uses_lists(budget, d * esz);
+    P.lists = want_merged && pv::merge_uses_lists(B, budget, d * esz);
     if (P.lists) {
         const int ngroups = (budget + pv::kBucketSlotsPerGroup - 1) / pv::kBucketSlotsPerGroup;
         P.mcount = c.take<int32_t>((size_t)B * budget);

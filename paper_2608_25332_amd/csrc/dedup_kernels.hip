@@ -799,47 +799,80 @@ __global__ __launch_bounds__(kBucketNT) void bucket_kernel(const int32_t *__rest
     }
 }
 
-// merge_csr: as merge, with the member list read from the bucket output.
-template <int DT>
+// merge_csr: as merge, with the member list read from the bucket output and
+// CPL 16-byte chunks per lane (a column block of 64 * CPL chunks): every
+// workgroup keeps CPL x kMergeU x 4 member chunks in flight per lane group.
+// The list entries are read where they are (they are the same for every lane
+// of a wave), so the chain per workgroup is count/offset, list, rows.
+template <int DT, int CPL>
 __global__ __launch_bounds__(kMergeNT) void merge_csr_kernel(
     const char *__restrict__ vis, int Nv, int d_bytes, const int32_t *__restrict__ mcount,
     const int32_t *__restrict__ mstart, const int32_t *__restrict__ mlist, int N1, int ngroups,
     char *__restrict__ merged) {
     constexpr int EPC = (DT == kBF16) ? 8 : 4;
     constexpr int NW = kMergeNT / 64;
-    __shared__ int list[kMergeRound];
-    __shared__ float part[NW][EPC][64];
+    __shared__ float part[NW][CPL][EPC][64];
     const int s = blockIdx.y, b = blockIdx.z;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nchunk = d_bytes >> 4;
-    const int c = blockIdx.x * 64 + lane;
-    const char *col = vis + (size_t)b * Nv * d_bytes + (size_t)min(c, nchunk - 1) * 16;
+    const char *vb = vis + (size_t)b * Nv * d_bytes;
+    int cc[CPL];
+#pragma unroll
+    for (int t = 0; t < CPL; ++t) cc[t] = blockIdx.x * 64 * CPL + t * 64 + lane;
     const int total = mcount[(size_t)b * N1 + s];
-    const int32_t *src = mlist + (size_t)b * ngroups * Nv + mstart[(size_t)b * N1 + s];
+    const int32_t *lst = mlist + (size_t)b * ngroups * Nv + mstart[(size_t)b * N1 + s];
 
-    float acc[EPC];
+    float acc[CPL][EPC];
 #pragma unroll
-    for (int e = 0; e < EPC; ++e) acc[e] = 0.f;
-    for (int r0 = 0; r0 < total; r0 += kMergeRound) {
-        const int cnt = min(kMergeRound, total - r0);
-        for (int m = tid; m < cnt; m += kMergeNT) list[m] = src[r0 + m];
-        __syncthreads();
-        for (int m0 = wave; m0 < cnt; m0 += NW * kMergeU) {
-            uint4 v[kMergeU];
+    for (int t = 0; t < CPL; ++t)
 #pragma unroll
-            for (int u = 0; u < kMergeU; ++u)
-                v[u] = ld16(col + (size_t)list[min(m0 + u * NW, cnt - 1)] * d_bytes);
+        for (int e = 0; e < EPC; ++e) acc[t][e] = 0.f;
+    for (int m0 = wave; m0 < total; m0 += NW * kMergeU) {
+        uint4 v[kMergeU][CPL];
 #pragma unroll
-            for (int u = 0; u < kMergeU; ++u) {
-                if (m0 + u * NW >= cnt) break;
-                add16<DT>(acc, v[u]);
-            }
+        for (int u = 0; u < kMergeU; ++u) {
+            const char *row = vb + (size_t)lst[min(m0 + u * NW, total - 1)] * d_bytes;
+#pragma unroll
+            for (int t = 0; t < CPL; ++t) v[u][t] = ld16(row + (size_t)min(cc[t], nchunk - 1) * 16);
         }
-        __syncthreads();  // the list is rewritten by the next round
+#pragma unroll
+        for (int u = 0; u < kMergeU; ++u) {
+            if (m0 + u * NW >= total) break;
+#pragma unroll
+            for (int t = 0; t < CPL; ++t) add16<DT>(acc[t], v[u][t]);
+        }
     }
-    merge_finish<DT, NW>(acc, part, wave, lane, c, nchunk, total,
-                         merged + ((size_t)b * N1 + s) * d_bytes);
+    char *out = merged + ((size_t)b * N1 + s) * d_bytes;
+    if (wave > 0) {
+#pragma unroll
+        for (int t = 0; t < CPL; ++t)
+#pragma unroll
+            for (int e = 0; e < EPC; ++e) part[wave][t][e][lane] = acc[t][e];
+    }
+    __syncthreads();
+    if (wave == 0) {
+        const float cntf = (float)total;
+#pragma unroll
+        for (int t = 0; t < CPL; ++t) {
+#pragma unroll
+            for (int w2 = 1; w2 < NW; ++w2)
+#pragma unroll
+                for (int e = 0; e < EPC; ++e) acc[t][e] += part[w2][t][e][lane];
+            if (cc[t] >= nchunk) continue;
+            uint32_t w4[4];
+            if (DT == kBF16) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    w4[q] = f32_to_bf16_rne(acc[t][2 * q] / cntf) |
+                            (f32_to_bf16_rne(acc[t][2 * q + 1] / cntf) << 16);
+            } else {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) w4[q] = __float_as_uint(acc[t][q] / cntf);
+            }
+            st16(out + (size_t)cc[t] * 16, uint4{w4[0], w4[1], w4[2], w4[3]});
+        }
+    }
 }
 
 // ----------------------------------------------------------------------------
@@ -993,18 +1026,22 @@ hipError_t launch_bucket(const int32_t *assign, int B, int Nv, int N1, int32_t *
     return hipGetLastError();
 }
 
+constexpr int kMergeCPL = 2;  // chunks per lane of merge_csr
+
 hipError_t launch_merge_csr(int dt, const void *vis, int B, int Nv, int d, int N1,
                             const int32_t *mcount, const int32_t *mstart, const int32_t *mlist,
                             void *merged, hipStream_t st) {
     const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
     const int ngroups = (N1 + kBucketSlots - 1) / kBucketSlots;
-    const dim3 grid((d_bytes / 16 + 63) / 64, N1, B);
+    const dim3 grid((d_bytes / 16 + 64 * kMergeCPL - 1) / (64 * kMergeCPL), N1, B);
     if (dt == kBF16)
-        hipLaunchKernelGGL(merge_csr_kernel<kBF16>, grid, dim3(kMergeNT), 0, st, (const char *)vis,
-                           Nv, d_bytes, mcount, mstart, mlist, N1, ngroups, (char *)merged);
+        hipLaunchKernelGGL((merge_csr_kernel<kBF16, kMergeCPL>), grid, dim3(kMergeNT), 0, st,
+                           (const char *)vis, Nv, d_bytes, mcount, mstart, mlist, N1, ngroups,
+                           (char *)merged);
     else
-        hipLaunchKernelGGL(merge_csr_kernel<kF32>, grid, dim3(kMergeNT), 0, st, (const char *)vis,
-                           Nv, d_bytes, mcount, mstart, mlist, N1, ngroups, (char *)merged);
+        hipLaunchKernelGGL((merge_csr_kernel<kF32, kMergeCPL>), grid, dim3(kMergeNT), 0, st,
+                           (const char *)vis, Nv, d_bytes, mcount, mstart, mlist, N1, ngroups,
+                           (char *)merged);
     return hipGetLastError();
 }
 

@@ -56,10 +56,12 @@ hipError_t launch_bucket(const int32_t *assign, int B, int Nv, int N1, int32_t *
 hipError_t launch_merge_csr(int dt, const void *vis, int B, int Nv, int d, int N1,
                             const int32_t *mcount, const int32_t *mstart, const int32_t *mlist,
                             void *merged, hipStream_t st);
-// Whether the merge reads member lists built by the bucket kernel (large
-// inputs) instead of scanning the assignment in every workgroup.
-inline bool merge_uses_lists(int N1, int d_bytes) {
-    return (long long)((d_bytes / 16 + 63) / 64) * N1 * 4 > d_bytes;
+// Whether the merge reads member lists built by the bucket kernel instead of
+// scanning the assignment in every workgroup: for batches (one extra launch
+// is then cheap next to the work), and whenever the scans would read more
+// than the rows they add.
+inline bool merge_uses_lists(int B, int N1, int d_bytes) {
+    return B > 1 || (long long)((d_bytes / 16 + 63) / 64) * N1 * 4 > d_bytes;
 }
 hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
                         const int32_t *assign, void *merged, hipStream_t st);
