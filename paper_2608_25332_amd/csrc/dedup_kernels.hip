@@ -109,8 +109,14 @@ __global__ __launch_bounds__(256) void cos_partial_kernel(
 // order, forms cos = dot / (|a| |v|) (0 for a zero vector), writes
 // M[b][Nt][Nv], the row sums of M over this workgroup's 64 tokens
 // rowsum[b][Nv/64][Nt] and (first row group) the inverse token norms.
-constexpr int kRedTok = 64, kRedRows = 4, kRedU = 16;
+constexpr int kRedTok = 64, kRedRows = 4;
 
+// Slice loads in flight per block of a reduction: the smallest of 1, 2, 4, 8,
+// 16 that covers KS (a block of clamped loads past KS would only repeat the
+// last slice).
+inline int reduce_unroll(int KS) { return KS <= 1 ? 1 : KS <= 2 ? 2 : KS <= 4 ? 4 : KS <= 8 ? 8 : 16; }
+
+template <int kRedU>
 __global__ __launch_bounds__(256) void cos_reduce_kernel(
     const float *__restrict__ part, const float *__restrict__ ssv, const float *__restrict__ ssa,
     int B, int Nv, int Nt, int KS, float *__restrict__ M, float *__restrict__ rowsum,
@@ -412,8 +418,7 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(
 // gram_reduce: grid (ceil(Mp / 2), B), 128 threads, one wave per pruned row.
 // Adds the k slices in slice order, forms the cosine to every kept token and
 // writes the slot of the best one (higher cosine, then lower slot).
-constexpr int kGramU = 16;
-
+template <int kGramU>
 __global__ __launch_bounds__(128) void gram_reduce_kernel(
     const float *__restrict__ part, int B, int Mp, int N1, int Nv, int KS,
     const float *__restrict__ invn, const int32_t *__restrict__ pruned,
@@ -908,8 +913,19 @@ hipError_t launch_cos_partial(int dt, const void *vis, const void *anchors, int 
 hipError_t launch_cos_reduce(const float *part, const float *ssv, const float *ssa, int B, int Nv,
                              int Nt, int KS, float *M, float *rowsum, float *invn, hipStream_t st) {
     dim3 grid((Nv + kRedTok - 1) / kRedTok, (Nt + kRedRows - 1) / kRedRows, B);
-    hipLaunchKernelGGL(cos_reduce_kernel, grid, dim3(256), 0, st, part, ssv, ssa, B, Nv, Nt, KS, M,
-                       rowsum, invn);
+#define PV_RED_CASE(u)                                                                             \
+    case u:                                                                                        \
+        hipLaunchKernelGGL(cos_reduce_kernel<u>, grid, dim3(256), 0, st, part, ssv, ssa, B, Nv, Nt, \
+                           KS, M, rowsum, invn);                                                   \
+        break;
+    switch (reduce_unroll(KS)) {
+        PV_RED_CASE(1)
+        PV_RED_CASE(2)
+        PV_RED_CASE(4)
+        PV_RED_CASE(8)
+        PV_RED_CASE(16)
+    }
+#undef PV_RED_CASE
     return hipGetLastError();
 }
 
@@ -996,8 +1012,19 @@ hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, 
                               const float *invn, const int32_t *pruned, const int32_t *kept,
                               int32_t *assign, hipStream_t st) {
     dim3 grid((Mp + 1) / 2, B);
-    hipLaunchKernelGGL(gram_reduce_kernel, grid, dim3(128), 0, st, part, B, Mp, N1, Nv, KS, invn,
-                       pruned, kept, assign);
+#define PV_RED_CASE(u)                                                                             \
+    case u:                                                                                        \
+        hipLaunchKernelGGL(gram_reduce_kernel<u>, grid, dim3(128), 0, st, part, B, Mp, N1, Nv, KS, \
+                           invn, pruned, kept, assign);                                            \
+        break;
+    switch (reduce_unroll(KS)) {
+        PV_RED_CASE(1)
+        PV_RED_CASE(2)
+        PV_RED_CASE(4)
+        PV_RED_CASE(8)
+        PV_RED_CASE(16)
+    }
+#undef PV_RED_CASE
     return hipGetLastError();
 }
 
