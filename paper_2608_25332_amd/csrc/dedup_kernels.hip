@@ -207,8 +207,7 @@ __global__ __launch_bounds__(64 * NW) void cos_full_kernel(
         char *dst = ring[wave][i % kFNS];
 #pragma unroll
         for (int q = 0; q < IPW; ++q)
-            __builtin_amdgcn_global_load_lds(src[q] + (size_t)i * 128, (lds_void_t *)(dst + q * 1024),
-                                             16, 0, 0);
+            lds_dma16(src[q] + (size_t)i * 128, dst + q * 1024);
     };
 #pragma unroll
     for (int pp = 0; pp < kFNS - 1; ++pp)

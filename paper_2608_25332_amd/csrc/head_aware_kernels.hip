@@ -6,9 +6,9 @@
 // sums along a column (over the text rows), so there is no single-pass form:
 // a row's normaliser is only known once the whole row is seen.
 //
-// score_partial (grid: 16-row blocks x selected heads x B) keeps the 16 query
-// rows of its block in registers as MFMA fragments and streams the head's
-// keys from HBM/L2 through LDS, 64 keys per chunk.  When the chunks number at
+// score_partial (grid: 16-row blocks x selected heads x B, XCD ordered) keeps
+// the 16 query rows of its block in registers as MFMA fragments and streams
+// the head's keys from HBM/L2 straight into LDS, 64 keys per chunk.  When the chunks number at
 // most MAXC the logits stay in registers between the row statistics and the
 // column sums (one pass over K); otherwise the keys are streamed again in a
 // second pass.  Only the selected heads are ever read and the attention map
@@ -16,6 +16,7 @@
 // row-block) column sums in a fixed order and runs the top-N_2.
 #include "pv_launch.h"
 #include "pv_device.h"
+#include "pv_tile_lds.h"
 
 #include <math.h>
 
@@ -30,32 +31,37 @@ __device__ __forceinline__ void lse_merge(float &m, float &l, float m2, float l2
     m = mn;
 }
 
-// Key rows are staged through LDS 64 at a time (one 16-key block per wave)
-// with row-major 16-byte loads: 4*NKS consecutive lanes read one key row, the
-// access pattern that moves the most bytes per clock into a CU.  The MFMA
-// fragments are then read from LDS.
-constexpr int kScoreCK = 64;  // keys per staged chunk
+// Key rows are streamed through an LDS ring 64 at a time with direct-to-LDS
+// loads (one CU sustains several times the bytes register loads reach), the
+// next chunks in flight while the current one is multiplied; each wave takes
+// one 16-key block of the chunk.  The row blocks of one head are adjacent in
+// the XCD-ordered grid, so they share the head's K in one L2.
+constexpr int kScoreCK = 64;     // keys per staged chunk
+constexpr int kScoreFlush = 8;   // chunks of column sums held in registers
+constexpr int kScoreLdsCap = 160 * 1024;
 
 template <int NKS>
 struct ScoreStage {
-    static constexpr int RB = 64 * NKS;     // bytes of one key row
-    static constexpr int STRIDE = RB + 16;  // LDS bytes per staged row (16-byte pad)
-    static constexpr int PPR = RB / 16;     // 16-byte pieces per row
-    static constexpr int PPT = kScoreCK * PPR / kScoreNT;  // pieces per thread per chunk
-    static constexpr int LDS = kScoreCK * STRIDE;
-    static_assert(kScoreCK * PPR % kScoreNT == 0, "chunk must fill the loaders evenly");
+    static constexpr int RB = 64 * NKS;                 // bytes of one key row
+    static constexpr int PPR = RB / 16;                 // 16-byte pieces per row
+    static constexpr int SWZ = (NKS % 2 == 0) ? 7 : 3;  // piece swizzle within a row
+    static constexpr int STAGE = kScoreCK * RB;         // bytes of one chunk
+    static constexpr int IPW = STAGE / 1024 / 4;        // loads per wave per chunk
+    static constexpr int NS = NKS <= 8 ? 3 : 2;         // ring stages
+    static_assert(STAGE % 4096 == 0, "chunk must split evenly over the waves");
 };
 
 template <int DT, int NKS, int MAXC>
 __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads, int H, int Nt, int N,
-    int n_heads, float scale_log2e, float *__restrict__ partial) {
+    int n_heads, float scale_log2e, float *__restrict__ partial, int cols_in_lds) {
     using S = ScoreStage<NKS>;
-    __shared__ __attribute__((aligned(16))) char kst[S::LDS];
+    __shared__ __attribute__((aligned(16))) char ring[S::NS][S::STAGE];
     __shared__ float sm_m[4][16], sm_l[4][16];
     __shared__ float row_m[16], row_il[16];
-    const int rb = blockIdx.x, hi = blockIdx.y, b = blockIdx.z;
-    const int nrb = gridDim.x;
+    const int nrb = (Nt + 15) / 16;
+    const int L = xcd_tile(blockIdx.x, gridDim.x);
+    const int rb = L % nrb, hi = (L / nrb) % n_heads, b = L / (nrb * n_heads);
     const int tid = threadIdx.x, lane = tid & 63;
     // uniform wave index: the block guards around the MFMAs become scalar
     // branches (an MFMA does not honour the execution mask)
@@ -63,48 +69,63 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     const int h = heads.h[b * n_heads + hi];
     const char *qb = q + ((size_t)b * H + h) * Nt * S::RB;
     const char *kb = k + ((size_t)b * H + h) * N * S::RB;
-    const int koff = (lane >> 4) * 16;
 
-    uint4 qf[NKS];
-    {
-        const char *qr = qb + (size_t)min(rb * 16 + (lane & 15), Nt - 1) * S::RB + koff;
-#pragma unroll
-        for (int s = 0; s < NKS; ++s) qf[s] = ld16(qr + s * 64);
-    }
     const int nch = (N + kScoreCK - 1) / kScoreCK;
+    uint4 qf[NKS];  // the 16 query rows as MFMA fragments (loaded below)
 
-    int srow[S::PPT], scol[S::PPT];
+    // this lane's source key row and piece for each of its loads of a chunk
+    int srow[S::IPW], sbyte[S::IPW];
 #pragma unroll
-    for (int p = 0; p < S::PPT; ++p) {
-        const int qq = tid + kScoreNT * p;
-        srow[p] = qq / S::PPR;
-        scol[p] = (qq % S::PPR) * 16;
+    for (int t = 0; t < S::IPW; ++t) {
+        const int pos = (wave * S::IPW + t) * 64 + lane;
+        const int r = pos / S::PPR, slot = pos % S::PPR;
+        srow[t] = r;
+        sbyte[t] = (slot ^ (r & S::SWZ)) << 4;
     }
-    // one pass over the keys: stage chunk ch (the next one is in flight while
-    // this one is multiplied) and hand this wave's 16x16 logit block to body
-    auto sweep = [&](auto body) {
-        uint4 buf[S::PPT];
-        auto fetch = [&](int ch) {
+    auto issue = [&](int ch) {
+        char *dst = ring[ch % S::NS] + wave * S::IPW * 1024;
 #pragma unroll
-            for (int p = 0; p < S::PPT; ++p) {
-                const int row = min(ch * kScoreCK + srow[p], N - 1);  // past the end: last key
-                buf[p] = ld16(kb + (size_t)row * S::RB + scol[p]);
-            }
-        };
-        fetch(0);
-        for (int ch = 0; ch < nch; ++ch) {
-            __syncthreads();  // the previous chunk's fragment reads are done
-#pragma unroll
-            for (int p = 0; p < S::PPT; ++p) st16(kst + srow[p] * S::STRIDE + scol[p], buf[p]);
-            __syncthreads();
-            if (ch + 1 < nch) fetch(ch + 1);
-            const char *fr = kst + (wave * 16 + (lane & 15)) * S::STRIDE + koff;
-            f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int s = 0; s < NKS; ++s) acc = mma16<DT>(qf[s], ld16(fr + s * 64), acc);
-            body(ch, acc);
+        for (int t = 0; t < S::IPW; ++t) {
+            const int row = min(ch * kScoreCK + srow[t], N - 1);  // past the end: last key
+            lds_dma16(kb + (size_t)row * S::RB + sbyte[t], dst + t * 1024);
         }
     };
+    // A pass over the keys: start() issues the first chunks; chunk(ch) waits
+    // for chunk ch, keeps the next ones in flight and returns this wave's
+    // 16 x 16 logit block (query rows x keys wave*16 .. wave*16+15 of the
+    // chunk); finish() lets the ring be refilled by a later pass.
+    auto start = [&]() {
+#pragma unroll
+        for (int pp = 0; pp < S::NS - 1; ++pp)
+            if (pp < nch) issue(pp);
+    };
+    // The vector-memory counter orders the direct-to-LDS loads among
+    // themselves only: while other loads or stores are in flight (the query
+    // fragments, the column sums) a partial wait could pass before a chunk
+    // has landed.  chunk(ch, true) waits for everything instead.
+    auto chunk = [&](int ch, bool drain) -> f32x4_t {
+        if (!drain && ch + S::NS - 1 <= nch) wait_vmcnt<S::IPW * (S::NS - 2)>();
+        else wait_vmcnt<0>();
+        bare_barrier();  // chunk ch is in LDS; chunk ch - 1 has been read
+        if (ch + S::NS - 1 < nch) issue(ch + S::NS - 1);
+        const char *sp = ring[ch % S::NS];
+        const int r = wave * 16 + (lane & 15);
+        uint4 kf[NKS];
+#pragma unroll
+        for (int s = 0; s < NKS; ++s) {
+            const int piece = s * 4 + (lane >> 4);
+            kf[s] = lds_read16(sp + r * S::RB + ((piece ^ (r & S::SWZ)) << 4));
+        }
+        lds_wait();
+        f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int s = 0; s < NKS; ++s) {
+            lds_after_wait(kf[s]);
+            acc = mma16<DT>(qf[s], kf[s], acc);
+        }
+        return acc;
+    };
+    auto finish = [&]() { bare_barrier(); };
 
     // pass 1: running (max, sum of exp) of the logits, per lane and row; with
     // MAXC > 0 the logit blocks also stay in registers for pass 2
@@ -114,17 +135,34 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         m[i] = -INFINITY;
         l[i] = 0.f;
     }
-    f32x4_t keep[MAXC > 0 ? MAXC : 1];
-    sweep([&](int ch, const f32x4_t &acc) {
-        if (MAXC > 0) {
-#pragma unroll
-            for (int c = 0; c < (MAXC > 0 ? MAXC : 1); ++c) keep[c] = (c == ch) ? acc : keep[c];
-        }
+    auto stats = [&](const f32x4_t &acc, int ch) {
         if (ch * kScoreCK + wave * 16 + (lane & 15) < N) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) lse_merge(m[i], l[i], acc[i] * scale_log2e, 1.f);
         }
-    });
+    };
+    f32x4_t keep[MAXC > 0 ? MAXC : 1];
+    start();
+    // the query rows' fragments load while the first key chunks stream in
+    {
+        const char *qr = qb + (size_t)min(rb * 16 + (lane & 15), Nt - 1) * S::RB + (lane >> 4) * 16;
+#pragma unroll
+        for (int s = 0; s < NKS; ++s) qf[s] = ld16(qr + s * 64);
+    }
+    if constexpr (MAXC > 0) {
+        // unrolled with constant indices (nch is uniform): each block stays
+        // in its own registers
+#pragma unroll
+        for (int ch = 0; ch < MAXC; ++ch) {
+            if (ch < nch) {
+                keep[ch] = chunk(ch, ch == 0);
+                stats(keep[ch], ch);
+            }
+        }
+    } else {
+        for (int ch = 0; ch < nch; ++ch) stats(chunk(ch, ch == 0), ch);
+    }
+    finish();
     // combine the 16 lanes that hold the same rows, then the 4 waves
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) {
@@ -173,9 +211,44 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         for (int c = 0; c < (MAXC > 0 ? MAXC : 1); ++c)
             if (c < nch) emit(keep[c], c * kScoreCK + wave * 16 + (lane & 15));
     } else {
-        sweep([&](int ch, const f32x4_t &acc) {
-            emit(acc, ch * kScoreCK + wave * 16 + (lane & 15));
-        });
+        // Stores must not be in flight at a partial wait (see chunk()): the
+        // column sums go to LDS while the keys stream and to memory after
+        // the pass, or, where N of them do not fit beside the ring, are held
+        // in registers kScoreFlush chunks at a time and stored, the next
+        // chunk then waiting for everything.
+        extern __shared__ float colsum[];  // [N] when cols_in_lds
+        float pend[kScoreFlush];
+#pragma unroll
+        for (int u = 0; u < kScoreFlush; ++u) pend[u] = 0.f;
+        start();
+        for (int ch = 0; ch < nch; ++ch) {
+            const bool after_flush = !cols_in_lds && ch > 0 && ch % kScoreFlush == 0;
+            const f32x4_t acc = chunk(ch, ch == 0 || after_flush);
+            float cs = 0.f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) cs += exp2f(acc[i] * scale_log2e - rm[i]) * ril[i];
+            cs += __shfl_xor(cs, 16, 64);
+            cs += __shfl_xor(cs, 32, 64);
+            const int col = ch * kScoreCK + wave * 16 + (lane & 15);
+            if (cols_in_lds) {
+                if (lane < 16 && col < N) colsum[col] = cs;
+            } else {
+                const int u0 = ch % kScoreFlush;
+#pragma unroll
+                for (int u = 0; u < kScoreFlush; ++u) pend[u] = (u == u0) ? cs : pend[u];
+                if (u0 == kScoreFlush - 1 || ch == nch - 1) {
+                    const int c0 = ch - u0;
+#pragma unroll
+                    for (int u = 0; u < kScoreFlush; ++u) {
+                        const int cu = (c0 + u) * kScoreCK + wave * 16 + (lane & 15);
+                        if (u <= u0 && lane < 16 && cu < N) out[cu] = pend[u];
+                    }
+                }
+            }
+        }
+        finish();
+        if (cols_in_lds)
+            for (int c = tid; c < N; c += kScoreNT) out[c] = colsum[c];
     }
 }
 
@@ -220,10 +293,16 @@ template <int DT, int NKS, int MAXC>
 static hipError_t score_go(const void *q, const void *k, const HeadArgs &heads, int B, int H,
                            int Nt, int N, int n_heads, float scale_log2e, float *partial,
                            hipStream_t st) {
-    dim3 grid((Nt + 15) / 16, n_heads, B);
-    hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC>), grid, dim3(kScoreNT), 0, st,
-                       (const char *)q, (const char *)k, heads, H, Nt, N, n_heads, scale_log2e,
-                       partial);
+    using S = ScoreStage<NKS>;
+    dim3 grid(((Nt + 15) / 16) * n_heads * B);
+    // two-pass form: the N column sums in dynamic LDS when they fit beside
+    // the ring and the row statistics (at most 64 KiB of it)
+    const size_t cols = (size_t)N * sizeof(float);
+    const bool in_lds = MAXC == 0 && cols <= 65536 &&
+                        (size_t)S::NS * S::STAGE + 1024 + cols <= (size_t)kScoreLdsCap;
+    hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC>), grid, dim3(kScoreNT),
+                       in_lds ? cols : 0, st, (const char *)q, (const char *)k, heads, H, Nt, N,
+                       n_heads, scale_log2e, partial, in_lds ? 1 : 0);
     return hipGetLastError();
 }
 

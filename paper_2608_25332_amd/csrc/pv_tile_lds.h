@@ -47,6 +47,14 @@ __device__ __forceinline__ void bare_barrier() {
 }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
+
+// One direct-to-LDS load: 16 bytes from g per lane into LDS at
+// lds + 16 * lane.  A __device__ function: target builtins written inside a
+// lambda of a kernel template keep the host compile from emitting the
+// kernel's launch stub.
+__device__ __forceinline__ void lds_dma16(const void *g, char *lds) {
+    __builtin_amdgcn_global_load_lds(g, (lds_void_t *)lds, 16, 0, 0);
+}
 typedef unsigned lds_u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint4 lds_read16(const char *p) {
@@ -118,8 +126,7 @@ struct TileGemmLds {
             char *dst = ring[i % NSTAGE] + wave * IPW * 1024;
 #pragma unroll
             for (int q = 0; q < IPW; ++q)
-                __builtin_amdgcn_global_load_lds(src[q] + (size_t)i * CHUNK,
-                                                 (lds_void_t *)(dst + q * 1024), 16, 0, 0);
+                lds_dma16(src[q] + (size_t)i * CHUNK, dst + q * 1024);
         };
 #pragma unroll
         for (int p = 0; p < NSTAGE - 1; ++p)

@@ -196,3 +196,18 @@ def test_dedup_split_validation(lib):
     bad = list(args)
     bad[7] = 0  # budget
     assert s(*bad, FAKE, FAKE, FAKE) == -3
+
+
+def test_every_kernel_launch_stub_is_defined():
+    """A kernel whose host-side launch stub is missing leaves an undefined
+    __device_stub__ symbol in the library; loading it would then fail on the
+    GPU machine."""
+    import shutil
+    import subprocess
+    from paper_2608_25332_amd import provip
+    if shutil.which("nm") is None:
+        pytest.skip("nm not available")
+    out = subprocess.run(["nm", "-D", "--undefined-only", provip.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    missing = [l.split()[-1] for l in out.splitlines() if "__device_stub__" in l]
+    assert not missing, missing[:5]
