@@ -60,6 +60,12 @@ def parse():
     ap.add_argument("--calib-mib", type=int, default=256)
     ap.add_argument("--split", action="store_true",
                     help="time the step with the merge branch on a second stream")
+    ap.add_argument("--cold-mib", type=int, default=640,
+                    help="input copies rotated through for the cold-cache timing (0 disables it)")
+    ap.add_argument("--score-sweep", action="store_true",
+                    help="instead of the step: the head-aware call at the LLaVA-1.5-7B shape over "
+                         "a batch sweep, with the selected heads and with all heads; prints its "
+                         "own JSON line")
     return ap.parse_args()
 
 
@@ -384,23 +390,168 @@ def stage_breakdown(torch, step):
     return {k: graph_time_us(torch, f) for k, f in cuts.items()}
 
 
+def replay_percentiles(torch, fn_replay, reps=400):
+    """p10 / p50 / p90 (us) of single replays, each between its own pair of
+    HIP events (consecutive replays, so each still follows the previous one
+    as in the timed loop)."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, z in ev:
+        a.record()
+        fn_replay()
+        z.record()
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(z) * 1000.0 for a, z in ev])
+    return {"p10": float(np.percentile(t, 10)), "p50": float(np.percentile(t, 50)),
+            "p90": float(np.percentile(t, 90))}
+
+
+def cold_times(torch, step, dev, budget_mib, rounds=6):
+    """Step and dedup-call time with cold caches: enough copies of the step's
+    inputs (visual tokens, anchors, Q, K and V of all tokens) that one
+    rotation through them moves more than budget_mib, which is above the
+    256 MB MALL and the L2s, so every replay finds its inputs in HBM only.
+    One graph per copy; the replays go round robin."""
+    names = ("vis", "anc", "q", "kf", "vf")
+    orig = {n: getattr(step, n) for n in names}
+    per_copy = sum(t.numel() * t.element_size() for t in orig.values())
+    ncopy = max(2, -(-(budget_mib << 20) // per_copy))
+    copies = [{n: t.clone() for n, t in orig.items()} for _ in range(ncopy)]
+    stream = torch.cuda.current_stream(dev)
+    pv, w = step.pv, step.w
+
+    def capture(fn):
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            fn()
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        return g
+
+    g_step, g_dedup = [], []
+    try:
+        for c in copies:
+            for n in names:
+                setattr(step, n, c[n])
+            g_step.append(capture(step.run))
+            g_dedup.append(capture(lambda: pv.pv_prune_dedup(step.vis, step.anc, w.N1, out=step.o1,
+                                                             workspace=step.ws1)))
+    finally:
+        for n in names:
+            setattr(step, n, orig[n])
+    torch.cuda.synchronize()
+    out = {"input_copies": ncopy, "rotation_mib": round(ncopy * per_copy / 2**20, 1)}
+    for key, gs in (("step", g_step), ("dedup_full", g_dedup)):
+        for g in gs:
+            g.replay()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        z = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(rounds):
+            for g in gs:
+                g.replay()
+        z.record()
+        torch.cuda.synchronize()
+        out[key] = a.elapsed_time(z) * 1000.0 / (rounds * len(gs))
+    del g_step, g_dedup, copies
+    torch.cuda.synchronize()
+    return out
+
+
+def score_sweep(torch, dev):
+    """Head-aware call at the LLaVA-1.5-7B shape (32 heads x 128, 64 text
+    rows, 192 kept keys, keep 64) over B = 1 .. 256, with 4 selected heads
+    per sample and with all 32 heads.  Per point: the call's time from graph
+    replays, the score kernel's average duration from back-to-back launches
+    between HIP events, and the kernel's algorithmic HBM bytes (Q and K of
+    the heads read) over that duration."""
+    from paper_2608_25332_amd import provip as pv
+
+    H, Nt, N, hd, N2 = 32, 64, 192, 128, 64
+    Bmax = 256
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(2)
+    q_all = torch.randn((Bmax, H, Nt, hd), generator=gen, device=dev).to(torch.bfloat16)
+    k_all = torch.randn((Bmax, H, N, hd), generator=gen, device=dev).to(torch.bfloat16)
+    rng = np.random.default_rng(2)
+    rows = []
+    for nh in (4, H):
+        for B in (1, 4, 16, 64, 256):
+            q, k = q_all[:B], k_all[:B]
+            heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+            out = {"kept": torch.empty((B, N2), dtype=torch.int32, device=dev),
+                   "score": torch.empty((B, N), dtype=torch.float32, device=dev)}
+            ws = torch.empty(pv.pv_head_aware_workspace_bytes(B, H, Nt, N, hd, nh, N2, 1),
+                             dtype=torch.uint8, device=dev)
+            call = lambda: pv.pv_prune_head_aware(q, k, heads, N2, out=out, workspace=ws)
+            call_us = graph_time_us(torch, call, reps=200)
+            reps = 20
+            samples = []
+            for _ in range(5):
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(Step.HEAD_EVENTS)]
+                for e in ev:
+                    e.record()
+                r = pv.pv_prune_head_aware(q, k, heads, N2, out=out, workspace=ws, events=ev,
+                                           reps=reps)
+                torch.cuda.synchronize()
+                i = r["kernel_names"].index("score_partial")
+                samples.append(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / reps)
+            kus = float(np.median(samples))
+            nbytes = B * nh * (Nt + N) * hd * 2
+            gbs = nbytes / (kus * 1e-6) / 1e9
+            rows.append({"B": B, "heads_per_sample": nh, "call_us": call_us,
+                         "score_kernel_us": kus, "algorithmic_bytes": nbytes,
+                         "achieved_GBs": gbs, "frac_hbm": gbs / HBM_PEAK_GBS})
+            print(f"[score-sweep] B={B} heads={nh} call {call_us:.2f} us, kernel {kus:.2f} us, "
+                  f"{gbs:.0f} GB/s", file=sys.stderr, flush=True)
+            del out, ws
+    return {"score_sweep": rows, "shape": {"H": H, "Nt": Nt, "N": N, "hd": hd, "N2": N2,
+                                           "dtype": "bf16"},
+            "note": "warm caches; at B=256 with all heads the call reads 537 MB"}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, seconds):
     """The CPU oracle, as it stands, over repeats of the same batch until the
-    time budget is used (at least one full step)."""
+    time budget is used (at least one full step); seconds per stage too."""
     import oracle
 
     s = w.spec
     reps = 0
+    st = {"dedup": 0.0, "head_aware": 0.0, "gather": 0.0}
     t0 = time.perf_counter()
     while True:
+        a = time.perf_counter()
         ref = oracle.dedup(w.anchors, w.vis, w.N1)
         kept1 = ref["kept"]
-        k1 = np.stack([w.k_full[b][:, kept1[b]] for b in range(s.B)])
-        v1 = np.stack([w.v_full[b][:, kept1[b]] for b in range(s.B)])
+        b = time.perf_counter()
+        k1 = np.stack([w.k_full[i][:, kept1[i]] for i in range(s.B)])
+        v1 = np.stack([w.v_full[i][:, kept1[i]] for i in range(s.B)])
+        c = time.perf_counter()
         kept2, _ = oracle.head_aware(w.q, k1, w.heads, w.N2)
+        d = time.perf_counter()
         oracle.gather(ref["merged"], kept2)
         oracle.gather(k1, kept2)
         oracle.gather(v1, kept2)
+        e = time.perf_counter()
+        st["dedup"] += b - a
+        st["head_aware"] += d - c
+        st["gather"] += (c - b) + (e - d)
         reps += 1
         el = time.perf_counter() - t0
         if el >= seconds:
@@ -409,7 +560,9 @@ def cpu_baseline(w, seconds):
     return {"value": toks / el, "unit": "visual tokens/s", "cores": 1, "kind": "oracle",
             "sample": f"{reps} full steps (dedup+merge, head-aware, gathers) of the {s.name} batch "
                       f"(B={s.B}, Nv={s.Nv}) in {el:.2f} s, single-threaded fp64 C oracle",
-            "seconds": round(el, 3)}
+            "seconds": round(el, 3),
+            "seconds_per_step_by_stage": {k: round(v / reps, 4) for k, v in st.items()},
+            "cpu_model": cpu_model(), "host_cpus": os.cpu_count()}
 
 
 def main():
@@ -427,6 +580,9 @@ def main():
         sys.exit(1)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.score_sweep:
+        print(json.dumps(score_sweep(torch, dev)), flush=True)
+        return
     w = W.make_workload(args.workload)
     s = w.spec
     step = Step(w, dev, split=args.split)
@@ -492,6 +648,8 @@ def main():
     torch.cuda.synchronize()
     ms_total = t_start.elapsed_time(t_end)
     ms_per_step = ms_total / args.steps
+    pct = replay_percentiles(torch, run_once)
+    cold = cold_times(torch, step, dev, args.cold_mib) if args.cold_mib > 0 else None
 
     # ---- per-kernel durations (each kernel launched back to back between events)
     kern_us = kernel_times(torch, step, args.kernel_reps, args.kernel_iters)
@@ -554,7 +712,8 @@ def main():
                    "timing": ("hip-graph replay of the full step" +
                               (", merge branch on a second stream" if args.split else "")
                               if graph is not None else "eager")},
-        "latency_us": {"pipeline": ms_per_step * 1000.0, "kernels": kern_us,
+        "latency_us": {"pipeline": ms_per_step * 1000.0, "pipeline_single_replays": pct,
+                       "pipeline_cold": cold, "kernels": kern_us,
                        "stages": stage_us, "calls_graph_replay": breakdown},
         "roofline": rf,
         "roofline_kernels": kernels,

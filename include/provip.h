@@ -63,7 +63,7 @@ typedef enum { PV_F32 = 0, PV_BF16 = 1 } pv_dtype;
 #define PV_MAX_TEXT 1024      /* text rows per sample (Nt)                   */
 #define PV_MAX_DIM 16384      /* embedding width d                           */
 #define PV_MAX_HEAD_DIM 256   /* head width hd                               */
-#define PV_MAX_HEAD_LIST 512  /* B * n_heads entries of one head-aware call   */
+#define PV_MAX_HEADS 512      /* n_heads of one head-aware call              */
 
 /* Static string for a pv_status value (never NULL). */
 const char *pv_status_string(int status);
@@ -145,8 +145,8 @@ int pv_prune_dedup_split(const void *vis, const void *anchors, int B, int Nv, in
  * kept       [B][budget]     int32 out  required
  * score      [B][N]          float32 out  v, may be NULL
  * Sizes: 1 <= N <= PV_MAX_TOKENS, 1 <= Nt <= PV_MAX_TEXT, hd % 32 == 0,
- *        32 <= hd <= PV_MAX_HEAD_DIM, 1 <= n_heads <= H,
- *        B * n_heads <= PV_MAX_HEAD_LIST, 1 <= budget <= N.
+ *        32 <= hd <= PV_MAX_HEAD_DIM, 1 <= n_heads <= min(H, PV_MAX_HEADS),
+ *        1 <= budget <= N.
  * ---------------------------------------------------------------------- */
 size_t pv_head_aware_workspace_bytes(int B, int H, int Nt, int N, int hd, int n_heads,
                                      int budget, int dtype);

@@ -299,8 +299,8 @@ int check_head(const void *q, const void *k, const int32_t *heads, int n_heads, 
     if (B < 1 || B > 65535 || H < 1 || Nt < 1 || Nt > PV_MAX_TEXT || N < 1 || N > PV_MAX_TOKENS ||
         hd < 32 || hd > PV_MAX_HEAD_DIM || hd % 32 != 0)
         return PV_ERR_SHAPE;
-    if (n_heads < 1 || n_heads > H || n_heads > pv::kMaxHeadArgs) return PV_ERR_HEADS;
-    if ((long long)B * n_heads > PV_MAX_HEAD_LIST) return PV_ERR_SHAPE;
+    static_assert(PV_MAX_HEADS == pv::kMaxHeadArgs, "one sample's head list fits one launch");
+    if (n_heads < 1 || n_heads > H || n_heads > PV_MAX_HEADS) return PV_ERR_HEADS;
     for (int b = 0; b < B; ++b) {
         const int32_t *hb = heads + (size_t)b * n_heads;
         for (int i = 0; i < n_heads; ++i) {
@@ -332,12 +332,8 @@ int head_impl(const void *q, const void *k, const int32_t *heads, int n_heads, i
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
 
-    pv::HeadArgs ha;
-    memset(&ha, 0, sizeof(ha));
-    memcpy(ha.h, heads, sizeof(int32_t) * (size_t)B * n_heads);
-
     if (!tr.launch("score_partial", [&] {
-            return pv::launch_score_partial(dt, q, k, ha, B, H, Nt, N, hd, n_heads, P.partial, st);
+            return pv::launch_score_partial(dt, q, k, heads, B, H, Nt, N, hd, n_heads, P.partial, st);
         }))
         return PV_ERR_HIP;
     const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));

@@ -19,6 +19,7 @@
 #include "pv_tile_lds.h"
 
 #include <math.h>
+#include <string.h>
 
 namespace pv {
 
@@ -53,25 +54,27 @@ struct ScoreStage {
 
 template <int DT, int NKS, int MAXC>
 __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
-    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads, int H, int Nt, int N,
-    int n_heads, float scale_log2e, float *__restrict__ partial, int cols_in_lds) {
+    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads, int b0, int H, int Nt,
+    int N, int n_heads, float scale_log2e, float *__restrict__ partial, int cols_in_lds) {
     using S = ScoreStage<NKS>;
     __shared__ __attribute__((aligned(16))) char ring[S::NS][S::STAGE];
+    __shared__ __attribute__((aligned(16))) char qrows[16 * S::RB];
     __shared__ float sm_m[4][16], sm_l[4][16];
     __shared__ float row_m[16], row_il[16];
     const int nrb = (Nt + 15) / 16;
     const int L = xcd_tile(blockIdx.x, gridDim.x);
-    const int rb = L % nrb, hi = (L / nrb) % n_heads, b = L / (nrb * n_heads);
+    // heads.h lists the heads of samples b0, b0 + 1, ... of this launch
+    const int rb = L % nrb, hi = (L / nrb) % n_heads, bl = L / (nrb * n_heads), b = b0 + bl;
     const int tid = threadIdx.x, lane = tid & 63;
     // uniform wave index: the block guards around the MFMAs become scalar
     // branches (an MFMA does not honour the execution mask)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int h = heads.h[b * n_heads + hi];
+    const int h = heads.h[bl * n_heads + hi];
     const char *qb = q + ((size_t)b * H + h) * Nt * S::RB;
     const char *kb = k + ((size_t)b * H + h) * N * S::RB;
 
     const int nch = (N + kScoreCK - 1) / kScoreCK;
-    uint4 qf[NKS];  // the 16 query rows as MFMA fragments (loaded below)
+    uint4 qf[NKS];  // the 16 query rows as MFMA fragments
 
     // this lane's source key row and piece for each of its loads of a chunk
     int srow[S::IPW], sbyte[S::IPW];
@@ -90,24 +93,52 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
             lds_dma16(kb + (size_t)row * S::RB + sbyte[t], dst + t * 1024);
         }
     };
-    // A pass over the keys: start() issues the first chunks; chunk(ch) waits
-    // for chunk ch, keeps the next ones in flight and returns this wave's
-    // 16 x 16 logit block (query rows x keys wave*16 .. wave*16+15 of the
-    // chunk); finish() lets the ring be refilled by a later pass.
+    // Every global load of the kernel is a direct-to-LDS load, and those
+    // retire in the order they were issued, so a partial wait on the load
+    // counter names exactly the chunks still in flight.  (With ordinary
+    // loads or stores outstanding as well no such guarantee holds: the query
+    // rows go through LDS for that reason, and stores wait for a full drain.)
+    //
+    // The query block (16 rows, NKS KiB) is loaded once, 1 KiB per load,
+    // spread over the waves; it is issued before the first key chunk, so
+    // waiting for chunk 0 waits for it too.
+    auto issue_q = [&]() {
+        for (int p = wave; p < NKS; p += 4) {
+            const int off = p * 1024 + lane * 16;
+            const int r = off / S::RB;
+            lds_dma16(qb + (size_t)min(rb * 16 + r, Nt - 1) * S::RB + off % S::RB, qrows + p * 1024);
+        }
+    };
+    // A pass over the keys: start() fills the whole ring (no buffer is reused
+    // before chunk NS); chunk(ch) waits for chunk ch, refills the buffer freed
+    // by chunk ch - 1 and returns this wave's 16 x 16 logit block (query rows
+    // x keys wave*16 .. wave*16+15 of the chunk); finish() lets the ring be
+    // refilled by a later pass.
     auto start = [&]() {
 #pragma unroll
-        for (int pp = 0; pp < S::NS - 1; ++pp)
+        for (int pp = 0; pp < S::NS; ++pp)
             if (pp < nch) issue(pp);
     };
-    // The vector-memory counter orders the direct-to-LDS loads among
-    // themselves only: while other loads or stores are in flight (the query
-    // fragments, the column sums) a partial wait could pass before a chunk
-    // has landed.  chunk(ch, true) waits for everything instead.
+    // the query fragments, once the first wait has covered their loads
+    auto read_q = [&]() {
+#pragma unroll
+        for (int s = 0; s < NKS; ++s)
+            qf[s] = lds_read16(qrows + (lane & 15) * S::RB + (s * 4 + (lane >> 4)) * 16);
+        lds_wait();
+#pragma unroll
+        for (int s = 0; s < NKS; ++s) lds_after_wait(qf[s]);
+    };
     auto chunk = [&](int ch, bool drain) -> f32x4_t {
-        if (!drain && ch + S::NS - 1 <= nch) wait_vmcnt<S::IPW * (S::NS - 2)>();
+        // chunks issued so far, and how many of them are younger than ch
+        const int issued = ch == 0 ? min(S::NS, nch) : min(ch + S::NS - 1, nch);
+        const int younger = drain ? 0 : issued - 1 - ch;
+        static_assert(S::NS <= 3, "at most two chunks younger than the one waited for");
+        if (younger >= 2) wait_vmcnt<S::IPW * 2>();
+        else if (younger == 1) wait_vmcnt<S::IPW>();
         else wait_vmcnt<0>();
         bare_barrier();  // chunk ch is in LDS; chunk ch - 1 has been read
-        if (ch + S::NS - 1 < nch) issue(ch + S::NS - 1);
+        if (ch >= 1 && ch + S::NS - 1 < nch) issue(ch + S::NS - 1);
+        if (ch == 0) read_q();
         const char *sp = ring[ch % S::NS];
         const int r = wave * 16 + (lane & 15);
         uint4 kf[NKS];
@@ -142,25 +173,20 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         }
     };
     f32x4_t keep[MAXC > 0 ? MAXC : 1];
+    issue_q();
     start();
-    // the query rows' fragments load while the first key chunks stream in
-    {
-        const char *qr = qb + (size_t)min(rb * 16 + (lane & 15), Nt - 1) * S::RB + (lane >> 4) * 16;
-#pragma unroll
-        for (int s = 0; s < NKS; ++s) qf[s] = ld16(qr + s * 64);
-    }
     if constexpr (MAXC > 0) {
         // unrolled with constant indices (nch is uniform): each block stays
         // in its own registers
 #pragma unroll
         for (int ch = 0; ch < MAXC; ++ch) {
             if (ch < nch) {
-                keep[ch] = chunk(ch, ch == 0);
+                keep[ch] = chunk(ch, false);
                 stats(keep[ch], ch);
             }
         }
     } else {
-        for (int ch = 0; ch < nch; ++ch) stats(chunk(ch, ch == 0), ch);
+        for (int ch = 0; ch < nch; ++ch) stats(chunk(ch, false), ch);
     }
     finish();
     // combine the 16 lanes that hold the same rows, then the 4 waves
@@ -223,7 +249,7 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         start();
         for (int ch = 0; ch < nch; ++ch) {
             const bool after_flush = !cols_in_lds && ch > 0 && ch % kScoreFlush == 0;
-            const f32x4_t acc = chunk(ch, ch == 0 || after_flush);
+            const f32x4_t acc = chunk(ch, after_flush);
             float cs = 0.f;
 #pragma unroll
             for (int i = 0; i < 4; ++i) cs += exp2f(acc[i] * scale_log2e - rm[i]) * ril[i];
@@ -289,21 +315,32 @@ __global__ __launch_bounds__(NT) void score_select_kernel(const float *__restric
     block_topk<NT, EMAX>(key, N, budget, kept + (size_t)b * budget, nullptr, nullptr, sm);
 }
 
+// The head lists travel as a kernel argument of bounded size: a launch covers
+// as many samples as fit, and larger batches take several launches.
 template <int DT, int NKS, int MAXC>
-static hipError_t score_go(const void *q, const void *k, const HeadArgs &heads, int B, int H,
+static hipError_t score_go(const void *q, const void *k, const int32_t *heads, int B, int H,
                            int Nt, int N, int n_heads, float scale_log2e, float *partial,
                            hipStream_t st) {
     using S = ScoreStage<NKS>;
-    dim3 grid(((Nt + 15) / 16) * n_heads * B);
     // two-pass form: the N column sums in dynamic LDS when they fit beside
     // the ring and the row statistics (at most 64 KiB of it)
     const size_t cols = (size_t)N * sizeof(float);
     const bool in_lds = MAXC == 0 && cols <= 65536 &&
-                        (size_t)S::NS * S::STAGE + 1024 + cols <= (size_t)kScoreLdsCap;
-    hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC>), grid, dim3(kScoreNT),
-                       in_lds ? cols : 0, st, (const char *)q, (const char *)k, heads, H, Nt, N,
-                       n_heads, scale_log2e, partial, in_lds ? 1 : 0);
-    return hipGetLastError();
+                        (size_t)S::NS * S::STAGE + 16 * S::RB + 1024 + cols <= (size_t)kScoreLdsCap;
+    const int per_launch = kMaxHeadArgs / n_heads;
+    HeadArgs ha;
+    for (int b0 = 0; b0 < B; b0 += per_launch) {
+        const int nb = B - b0 < per_launch ? B - b0 : per_launch;
+        for (int i = 0; i < kMaxHeadArgs; ++i)
+            ha.h[i] = i < nb * n_heads ? heads[(size_t)b0 * n_heads + i] : 0;
+        dim3 grid(((Nt + 15) / 16) * n_heads * nb);
+        hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC>), grid, dim3(kScoreNT),
+                           in_lds ? cols : 0, st, (const char *)q, (const char *)k, ha, b0, H, Nt,
+                           N, n_heads, scale_log2e, partial, in_lds ? 1 : 0);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 // Logit blocks held in registers between the two passes: the smallest of 1,
@@ -314,7 +351,7 @@ template <int NKS>
 constexpr int score_maxc_cap() { return NKS <= 4 ? 16 : (NKS <= 8 ? 8 : 4); }
 
 template <int DT, int NKS>
-static hipError_t score_nks(const void *q, const void *k, const HeadArgs &heads, int B, int H,
+static hipError_t score_nks(const void *q, const void *k, const int32_t *heads, int B, int H,
                             int Nt, int N, int n_heads, float sl2e, float *partial,
                             hipStream_t st) {
     const int nch = (N + kScoreCK - 1) / kScoreCK;
@@ -333,7 +370,7 @@ static hipError_t score_nks(const void *q, const void *k, const HeadArgs &heads,
 }
 
 template <int DT>
-static hipError_t score_dt(int nks, const void *q, const void *k, const HeadArgs &heads, int B,
+static hipError_t score_dt(int nks, const void *q, const void *k, const int32_t *heads, int B,
                            int H, int Nt, int N, int n_heads, float sl2e,
                            float *partial, hipStream_t st) {
 #define PV_NKS_CASE(n) \
@@ -357,7 +394,7 @@ static hipError_t score_dt(int nks, const void *q, const void *k, const HeadArgs
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_score_partial(int dt, const void *q, const void *k, const HeadArgs &heads,
+hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads,
                                 int B, int H, int Nt, int N, int hd, int n_heads, float *partial,
                                 hipStream_t st) {
     const int esz = (dt == kBF16) ? 2 : 4;
@@ -370,17 +407,24 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const Head
 
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,
                                float *v, int budget, int32_t *kept, hipStream_t st) {
-    if (N <= 256 * 4)
-        hipLaunchKernelGGL((score_select_kernel<256, 4>), dim3(B), dim3(256), 0, st, partial,
-                           nparts, N, inv_norm, v, budget, kept);
-    else if (N <= 512 * 8)
-        hipLaunchKernelGGL((score_select_kernel<512, 8>), dim3(B), dim3(512), 0, st, partial,
-                           nparts, N, inv_norm, v, budget, kept);
+    // as many threads as keys where possible: each thread's partial sums are
+    // then all in flight at once
+#define PV_SEL_CASE(nt, e)                                                                         \
+    hipLaunchKernelGGL((score_select_kernel<nt, e>), dim3(B), dim3(nt), 0, st, partial, nparts, N, \
+                       inv_norm, v, budget, kept)
+    if (N <= 256)
+        PV_SEL_CASE(256, 1);
+    else if (N <= 1024)
+        PV_SEL_CASE(1024, 1);
+    else if (N <= 1024 * 2)
+        PV_SEL_CASE(1024, 2);
+    else if (N <= 1024 * 4)
+        PV_SEL_CASE(1024, 4);
     else if (N <= 1024 * 16)
-        hipLaunchKernelGGL((score_select_kernel<1024, 16>), dim3(B), dim3(1024), 0, st, partial,
-                           nparts, N, inv_norm, v, budget, kept);
+        PV_SEL_CASE(1024, 16);
     else
         return hipErrorInvalidValue;
+#undef PV_SEL_CASE
     return hipGetLastError();
 }
 

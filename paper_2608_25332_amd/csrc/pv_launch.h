@@ -67,7 +67,7 @@ hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
                         const int32_t *assign, void *merged, hipStream_t st);
 
 // ---- head-aware pruning (Sec. 4.4)
-hipError_t launch_score_partial(int dt, const void *q, const void *k, const HeadArgs &heads,
+hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 int B, int H, int Nt, int N, int hd, int n_heads, float *partial,
                                 hipStream_t st);
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,

@@ -311,6 +311,7 @@ HEAD_EDGE = [
     (1, 2, 16, 300, 256, 1, 30, "f32"),       # widest head, streamed twice
     (2, 3, 40, 70, 160, 2, 9, "bf16"),
     (1, 2, 33, 257, 224, 2, 64, "f32"),
+    (40, 16, 16, 64, 64, 16, 20, "bf16"),     # 640 head-list entries: two launches
     (1, 2, 16, 9000, 256, 1, 500, "f32"),     # column sums flushed from registers
     (1, 1, 9, 12100, 224, 1, 900, "f32"),     # the same, 14 pieces per key row
 ]
