@@ -184,9 +184,13 @@ DEDUP_EDGE = [
     (1, 40, 4, 192, 1, "bf16"),
     (1, 40, 4, 256, 3, "bf16"),
     (2, 40, 4, 320, 7, "f32"),
-    # split-k cosine (batches too large for the full-k small-input pass)
+    # split-k cosine (batches too large for the full-k small-input pass),
+    # ragged tiles in both directions
     (64, 200, 33, 1024, 70, "bf16"),
     (48, 150, 5, 2048, 40, "f32"),
+    (8, 1000, 130, 256, 300, "bf16"),
+    (2, 1500, 100, 2048, 400, "bf16"),
+    (1, 1200, 70, 2048, 300, "f32"),
     # full-k Gram tiles: one kept tile (slot written directly), and two kept
     # tiles in fp32 (per-tile candidates merged by gram_finish)
     (128, 300, 4, 64, 100, "bf16"),
@@ -239,17 +243,27 @@ def test_dedup_one_slot_takes_almost_everything():
     check_merged(g["merged"][0], vis[0], g["kept"][0], g["assign"][0], np.arange(40), "bf16")
 
 
-def test_dedup_zero_vectors():
-    """A zero visual token or anchor has cosine 0 to everything."""
+@pytest.mark.parametrize("B,Nv,Nt,d,dt", [
+    (1, 40, 4, 64, "f32"),         # one full-k pass over 16 x 16 tiles
+    (130, 70, 100, 128, "bf16"),   # split-k products, many samples
+    (1, 1500, 100, 2048, "bf16"),  # split-k products, long rows
+])
+def test_dedup_zero_vectors(B, Nv, Nt, d, dt):
+    """A zero visual token or anchor has cosine 0 to everything (each way
+    the cosines are formed)."""
+    _say(f"[dedup-zero] B={B} Nv={Nv} Nt={Nt} d={d} {dt}")
     rng = np.random.default_rng(5)
-    vis = rng.standard_normal((1, 40, 64)).astype(np.float32)
-    anc = rng.standard_normal((1, 4, 64)).astype(np.float32)
-    vis[0, 7] = 0.0
-    anc[0, 2] = 0.0
-    g = run_dedup(vis, anc, "f32", 10)
-    p = oracle.maxpool(oracle.center(oracle.cosine(anc[0], vis[0])))
-    assert rel_err(g["score"][0], p) <= 1e-5
-    check_kept(g["kept"][0], p, 10, "f32")
+    vis = rng.standard_normal((B, Nv, d)).astype(np.float32)
+    anc = rng.standard_normal((B, Nt, d)).astype(np.float32)
+    if dt == "bf16":
+        vis, anc = W.bf16_round(vis), W.bf16_round(anc)
+    vis[:, 7] = 0.0
+    anc[:, 2] = 0.0
+    g = run_dedup(vis, anc, dt, 10)
+    for b in range(min(B, 3)):
+        p = oracle.maxpool(oracle.center(oracle.cosine(anc[b], vis[b])))
+        assert rel_err(g["score"][b], p) <= TOL[dt]
+        check_kept(g["kept"][b], p, 10, dt)
 
 
 # ----------------------------------------------------------- head-aware -----
