@@ -12,6 +12,8 @@ Function map (paper passages are cited at each C function):
   topk                       -- retention of the N_1 / N_2 highest scores
   assign / merge             -- Sec. 4.3, nearest-centroid aggregation
   attention / head_aware     -- Sec. 4.4, equations for S^vis and v
+  head_confidence /
+  visual_heads               -- Sec. 4.4, equations for C^h and V_l
   gather                     -- compaction of kept rows (Sec. 4.1)
   dedup                      -- Sec. 4.3 end to end
 
@@ -85,6 +87,10 @@ def _declare(lib):
     lib.orc_head_aware_score.restype = _int
     lib.orc_head_aware.argtypes = [_D, _D, _int, _int, _int, _int, _I, _int, _int, _I, _D]
     lib.orc_head_aware.restype = _int
+    lib.orc_head_confidence.argtypes = [_D, _D, _int, _int, _int, _int, _D]
+    lib.orc_head_confidence.restype = _int
+    lib.orc_visual_heads.argtypes = [_D, _D, _int, _int, _int, _int, _int, _I, _D]
+    lib.orc_visual_heads.restype = _int
     lib.orc_gather.argtypes = [_U8, _U8, _I, _int, _int, _int, _int, _i64,
                                _i64, _i64, _i64, _i64, _i64, _i64]
     lib.orc_gather.restype = _int
@@ -246,6 +252,37 @@ def head_aware(q, k, heads, n2: int, *, lib=None):
         if rc != 0:
             raise OracleError(f"orc_head_aware rc={rc}")
     return kept, v
+
+
+def head_confidence(q, k, *, lib=None) -> np.ndarray:
+    """One sample: q [H, nt, hd], k [H, n, hd] -> C [H] (Sec. 4.4, equation
+    for C^h)."""
+    lib = lib or load()
+    q, k = _f64(q), _f64(k)
+    H, nt, hd = q.shape
+    n = k.shape[1]
+    c = np.empty(H, np.float64)
+    rc = lib.orc_head_confidence(_pd(q), _pd(k), H, nt, n, hd, _pd(c))
+    if rc != 0:
+        raise OracleError(f"orc_head_confidence rc={rc}")
+    return c
+
+
+def visual_heads(q, k, n_vis: int, *, lib=None):
+    """Sec. 4.4 over a batch: q [B,H,nt,hd], k [B,H,n,hd] -> (heads [B,n_vis]
+    ascending, C [B,H])."""
+    lib = lib or load()
+    Q, K = _f64(q), _f64(k)
+    B, H, nt, hd = Q.shape
+    n = K.shape[2]
+    heads = np.empty((B, n_vis), np.int32)
+    conf = np.empty((B, H), np.float64)
+    for b in range(B):
+        rc = lib.orc_visual_heads(_pd(Q[b]), _pd(K[b]), H, nt, n, hd, int(n_vis), _pi(heads[b]),
+                                  _pd(conf[b]))
+        if rc != 0:
+            raise OracleError(f"orc_visual_heads rc={rc}")
+    return heads, conf
 
 
 # ---------------------------------------------------------------- gather --

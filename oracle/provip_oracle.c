@@ -305,6 +305,56 @@ int orc_head_aware(const double *q, const double *k, int H, int nt, int n, int h
 }
 
 /* --------------------------------------------------------------------------
+ * Sec. 4.4, equation for C^h: the confidence of head h is the variance of
+ * its cross-modal attention scores over the visual keys, taken for each
+ * critical text row and summed over those rows,
+ *     C[h] = sum_i Var_j(A_h[i][j]).
+ * Reading: the population variance (divide by n), written as the mean of
+ * the squared deviations from the row mean; the rows passed in are the
+ * critical text rows.
+ * q: [H][nt][hd], k: [H][n][hd], conf: [H].  Returns 0, or -3 on no memory.
+ * ------------------------------------------------------------------------ */
+int orc_head_confidence(const double *q, const double *k, int H, int nt, int n, int hd,
+                        double *conf)
+{
+    double *A = (double *)malloc(sizeof(double) * (size_t)nt * n);
+    if (!A) return -3;
+    for (int h = 0; h < H; ++h) {
+        orc_attention(q + (size_t)h * nt * hd, k + (size_t)h * n * hd, nt, n, hd, A);
+        double c = 0.0;
+        for (int i = 0; i < nt; ++i) {
+            const double *row = A + (size_t)i * n;
+            double mean = 0.0;
+            for (int j = 0; j < n; ++j) mean += row[j];
+            mean /= (double)n;
+            double var = 0.0;
+            for (int j = 0; j < n; ++j) var += (row[j] - mean) * (row[j] - mean);
+            c += var / (double)n;
+        }
+        conf[h] = c;
+    }
+    free(A);
+    return 0;
+}
+
+/* --------------------------------------------------------------------------
+ * Sec. 4.4, equation for V_l: the visual heads are the N_vis heads of
+ * highest confidence (same order rule as orc_topk: a tie goes to the lower
+ * head id), listed in ascending order.  conf_out may be NULL.
+ * ------------------------------------------------------------------------ */
+int orc_visual_heads(const double *q, const double *k, int H, int nt, int n, int hd,
+                     int n_vis, int32_t *heads, double *conf_out)
+{
+    double *c = (double *)malloc(sizeof(double) * (size_t)H);
+    if (!c) return -3;
+    int rc = orc_head_confidence(q, k, H, nt, n, hd, c);
+    if (rc == 0) rc = orc_topk(c, H, n_vis, heads);
+    if (rc == 0 && conf_out) memcpy(conf_out, c, sizeof(double) * (size_t)H);
+    free(c);
+    return rc;
+}
+
+/* --------------------------------------------------------------------------
  * Sec. 4.1: pruned tokens are excluded from all later computation, so the
  * rows of the kept tokens are compacted, in token order.  Byte copy:
  *     dst[b][g][r] = src[b][g][idx[b][r]]   (rows of row_bytes bytes).

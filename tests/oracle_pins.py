@@ -334,6 +334,96 @@ def pin_head_aware_topk(lib):
         assert np.array_equal(kept[b], np.sort(np.argsort(-v[b], kind="stable")[:5]))
 
 
+# ------------------------------------------------------- Eq. C^h, V_l ------
+
+def pin_confidence_closed_forms(lib):
+    """Sec. 4.4, equation for C^h, on rows whose variance is known exactly:
+    Q = 0 gives uniform rows (variance 0); two keys with logits 0 and t give
+    the row (1 - s, s) with s the logistic of t, whose population variance
+    is (s - 1/2)^2; a dominant key (one-hot row) gives (n - 1) / n^2."""
+    hd = 4
+    # head 0: Q = 0 over 7 keys; head 1: two keys, logit difference per row
+    q = np.zeros((2, 3, hd))
+    k = np.zeros((2, 7, hd))
+    k[0] = np.random.default_rng(31).standard_normal((7, hd))
+    ts = np.array([0.5, -1.25, 2.0])
+    q[1, :, 0] = ts * math.sqrt(hd)   # logit of key 1 minus key 0 = t
+    k[1, 1, 0] = 1.0
+    c2 = O.head_confidence(q, k[:, :7], lib=lib)
+    assert abs(c2[0]) < 1e-30
+    # head 1 has only two meaningful keys: redo with n = 2
+    q2 = q[1:2]
+    k2 = k[1:2, :2]
+    c = O.head_confidence(q2, k2, lib=lib)
+    want = sum((1.0 / (1.0 + math.exp(-t)) - 0.5) ** 2 for t in ts)
+    assert abs(c[0] - want) < 1e-15
+    # one dominant key per row: logits differ by 800 -> exactly one-hot in fp64
+    n = 9
+    q3 = np.zeros((1, 4, hd))
+    k3 = np.zeros((1, n, hd))
+    q3[0, :, 0] = 800.0 * math.sqrt(hd)
+    k3[0, 5, 0] = 1.0
+    c3 = O.head_confidence(q3, k3, lib=lib)
+    assert abs(c3[0] - 4 * (n - 1) / n ** 2) < 1e-15
+
+
+def pin_confidence_library(lib):
+    """Special case reducing to library routines: numpy's population
+    variance (np.var) of torch.softmax rows in float64, summed per head."""
+    import torch
+    rng = np.random.default_rng(32)
+    H, nt, n, hd = 5, 6, 21, 16
+    q = rng.standard_normal((H, nt, hd)) * 2
+    k = rng.standard_normal((H, n, hd)) * 2
+    A = torch.softmax(torch.from_numpy(q) @ torch.from_numpy(k).transpose(1, 2).contiguous()
+                      / math.sqrt(hd), dim=-1).numpy()
+    want = np.var(A, axis=2).sum(axis=1)
+    c = O.head_confidence(q, k, lib=lib)
+    assert np.max(np.abs(c - want)) < 1e-15 * max(1.0, want.max())
+
+
+def pin_confidence_invariants(lib):
+    """The confidence does not depend on the order of the keys or of the
+    text rows; heads are independent (permuting heads permutes C); adding
+    one vector to every key of a head leaves its C unchanged."""
+    rng = np.random.default_rng(33)
+    H, nt, n, hd = 4, 5, 13, 8
+    q = rng.standard_normal((H, nt, hd)) * 2
+    k = rng.standard_normal((H, n, hd)) * 2
+    c = O.head_confidence(q, k, lib=lib)
+    assert np.all(c > 0)
+    ck = O.head_confidence(q, k[:, rng.permutation(n)], lib=lib)
+    cq = O.head_confidence(q[:, rng.permutation(nt)], k, lib=lib)
+    perm = rng.permutation(H)
+    ch = O.head_confidence(q[perm], k[perm], lib=lib)
+    w = rng.standard_normal(hd) * 3
+    cs = O.head_confidence(q, k + w[None, None, :], lib=lib)
+    assert np.max(np.abs(ck - c)) < 1e-15 and np.max(np.abs(cq - c)) < 1e-15
+    assert np.array_equal(ch, c[perm])
+    assert np.max(np.abs(cs - c)) < 1e-13
+
+
+def pin_visual_heads_topk(lib):
+    """Sec. 4.4, equation for V_l: the N_vis heads of largest C, ascending;
+    the same total order as the token top-k (numpy stable argsort); N_vis = H
+    keeps every head.  A head whose queries are zero (uniform attention,
+    C = 0) is never chosen while another head has C > 0."""
+    rng = np.random.default_rng(34)
+    B, H, nt, n, hd = 3, 8, 5, 11, 8
+    q = rng.standard_normal((B, H, nt, hd)) * 2
+    k = rng.standard_normal((B, H, n, hd)) * 2
+    q[:, 6] = 0.0
+    for nv in (1, 3, H - 1, H):
+        heads, conf = O.visual_heads(q, k, nv, lib=lib)
+        for b in range(B):
+            assert np.array_equal(heads[b], np.sort(np.argsort(-conf[b], kind="stable")[:nv]))
+            assert abs(conf[b, 6]) < 1e-30
+            if nv < H:
+                assert 6 not in heads[b]
+        if nv == H:
+            assert np.array_equal(heads, np.tile(np.arange(H), (B, 1)))
+
+
 # ---------------------------------------------------------------- gather ---
 
 def pin_gather_bytes(lib):

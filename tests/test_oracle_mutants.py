@@ -45,6 +45,15 @@ MUTANTS = [
     ("headaware-row-sum-not-col", "for (int i = 0; i < nt; ++i) s += S[(size_t)i * n + j];",
      "for (int i = 0; i < nt; ++i) s += S[(size_t)(j % nt) * n + (i % n)];"),
     ("gather-src-stride", "src + b * sb + g * sg + j * sr", "src + b * sb + j * sr"),
+    ("confidence-no-mean-subtraction", "var += (row[j] - mean) * (row[j] - mean);",
+     "var += row[j] * row[j];"),
+    ("confidence-sample-variance", "c += var / (double)n;", "c += var / (double)(n - 1);"),
+    ("confidence-row-mean-not-sum", "conf[h] = c;", "conf[h] = c / (double)nt;"),
+    ("confidence-std-not-var", "c += var / (double)n;", "c += sqrt(var / (double)n);"),
+    ("confidence-first-row-only", "for (int i = 0; i < nt; ++i) {\n            const double *row = A + (size_t)i * n;",
+     "for (int i = 0; i < 1; ++i) {\n            const double *row = A + (size_t)i * n;"),
+    ("visual-heads-lowest", "if (rc == 0) rc = orc_topk(c, H, n_vis, heads);",
+     "for (int h = 0; h < H; ++h) c[h] = -c[h];\n    if (rc == 0) rc = orc_topk(c, H, n_vis, heads);"),
 ]
 
 
