@@ -515,6 +515,39 @@ def score_sweep(torch, dev):
             "note": "warm caches; at B=256 with all heads the call reads 537 MB"}
 
 
+def visual_heads_timing(torch, step, n_vis=6):
+    """Visual-head identification (all H heads of the N1 kept keys, the
+    paper's N_vis = 6) at the step's shape: the call from graph replays and
+    the confidence kernel's average duration between HIP events, with its
+    roofline position (all heads of Q and K are read once)."""
+    pv, w = step.pv, step.w
+    s = w.spec
+    B, H, Nt, N1, hd = s.B, s.H, s.Nt, w.N1, s.hd
+    n_vis = min(n_vis, H)
+    dev = step.q.device
+    out = {"heads": torch.empty((B, n_vis), dtype=torch.int32, device=dev),
+           "conf": torch.empty((B, H), dtype=torch.float32, device=dev)}
+    ws = torch.empty(pv.pv_visual_heads_workspace_bytes(B, H, Nt), dtype=torch.uint8, device=dev)
+    call = lambda: pv.pv_visual_heads(step.q, step.k1, n_vis, out=out, workspace=ws)
+    call_us = graph_time_us(torch, call)
+    reps, samples = 20, []
+    for _ in range(5):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        for e in ev:
+            e.record()
+        r = pv.pv_visual_heads(step.q, step.k1, n_vis, out=out, workspace=ws, events=ev, reps=reps)
+        torch.cuda.synchronize()
+        i = r["kernel_names"].index("head_conf")
+        samples.append(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / reps)
+    kus = float(np.median(samples))
+    e = 2 if w.dtype == "bf16" else 4
+    a = {"bytes": B * H * (Nt + N1) * hd * e, "flops": 2.0 * B * H * Nt * N1 * hd}
+    rf = roof(a, kus * 1e-6)
+    return {"n_vis": n_vis, "call_us": call_us, "head_conf_us": kus,
+            "roofline": {"bound": rf["bound"], "achieved": rf["achieved"], "unit": rf["unit"],
+                         "frac": rf["frac"], "algorithmic_bytes": a["bytes"]}}
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -663,6 +696,7 @@ def main():
             step.split = args.split
     breakdown["step_two_streams" if not args.split else "step_single_stream"] = graph_time_us(
         torch, other)
+    vis_heads = visual_heads_timing(torch, step)
     step.run()
     torch.cuda.synchronize()
     # the outputs after all of the above still match the first eager step
@@ -718,6 +752,8 @@ def main():
         "roofline": rf,
         "roofline_kernels": kernels,
         "roofline_stages": stages,
+        # outside the step: visual-head identification at the same layer
+        "visual_heads": vis_heads,
         "csrc_digest": csrc_digest(),
     }
     if args.cpu_seconds > 0:

@@ -157,6 +157,49 @@ int pv_prune_head_aware(const void *q, const void *k, const int32_t *heads_host,
                         void *stream);
 
 /* -------------------------------------------------------------------------
+ * The same with the head lists in DEVICE memory, for lists that a kernel
+ * produced (pv_visual_heads) and that the caller does not read back.
+ *
+ * heads_dev  [B][n_heads]    int32      DEVICE memory, 4-byte aligned.  The
+ *            library cannot check it before the kernels run: entries outside
+ *            [0, H) are clamped into range and a repeated entry is counted as
+ *            often as it appears (memory-safe; v is then the mean over the
+ *            list as given).  Lists from pv_visual_heads are always valid.
+ * Everything else, the workspace and the errors are those of
+ * pv_prune_head_aware; results for a valid list are bit-identical to it.
+ * ---------------------------------------------------------------------- */
+int pv_prune_head_aware_dev(const void *q, const void *k, const int32_t *heads_dev, int n_heads,
+                            int B, int H, int Nt, int N, int hd, int dtype, int budget,
+                            int32_t *kept, float *score, void *workspace, size_t workspace_bytes,
+                            void *stream);
+
+/* -------------------------------------------------------------------------
+ * Visual-head identification at a shallow pruning layer (Sec. 4.4,
+ * equations for C^h and V_l).
+ *
+ * Per sample b and head h (every head 0..H-1):
+ *   A_h[i][j] = softmax_j( q[b][h][i] . k[b][h][j] / sqrt(hd) )  as above
+ *   C[b][h]   = sum_i Var_j(A_h[i][j])     population variance over the N
+ *               keys, summed over the Nt rows passed in (the critical text
+ *               rows)
+ *   heads_out = the n_vis heads with the highest C (ties: lower head id),
+ *               ascending: the list pv_prune_head_aware_dev takes.
+ * One pass over the keys; the attention map is never written out.
+ *
+ * q          [B][H][Nt][hd]  dtype      text-query rows
+ * k          [B][H][N][hd]   dtype      keys of the N visual tokens
+ * heads_out  [B][n_vis]      int32 out  required
+ * conf       [B][H]          float32 out  C, may be NULL
+ * Sizes as pv_prune_head_aware, plus H <= PV_MAX_HEADS, 1 <= n_vis <= H
+ * (else PV_ERR_HEADS).  workspace: pv_visual_heads_workspace_bytes(B, H, Nt).
+ * ---------------------------------------------------------------------- */
+size_t pv_visual_heads_workspace_bytes(int B, int H, int Nt);
+
+int pv_visual_heads(const void *q, const void *k, int B, int H, int Nt, int N, int hd, int dtype,
+                    int n_vis, int32_t *heads_out, float *conf, void *workspace,
+                    size_t workspace_bytes, void *stream);
+
+/* -------------------------------------------------------------------------
  * The retention rule of both stages on its own (Sec. 4.3: keep the N_1
  * tokens with the highest p; Sec. 4.4: keep the N_2 tokens with the highest
  * v), for callers that compute their own scores.  Per sample b: the k
@@ -236,6 +279,17 @@ int pv_prune_head_aware_timed(const void *q, const void *k, const int32_t *heads
                               int budget, int32_t *kept, float *score, void *workspace,
                               size_t workspace_bytes, void *stream, void *const *events,
                               int n_events, int reps, int *n_kernels, const char **names);
+
+int pv_prune_head_aware_dev_timed(const void *q, const void *k, const int32_t *heads_dev,
+                                  int n_heads, int B, int H, int Nt, int N, int hd, int dtype,
+                                  int budget, int32_t *kept, float *score, void *workspace,
+                                  size_t workspace_bytes, void *stream, void *const *events,
+                                  int n_events, int reps, int *n_kernels, const char **names);
+
+int pv_visual_heads_timed(const void *q, const void *k, int B, int H, int Nt, int N, int hd,
+                          int dtype, int n_vis, int32_t *heads_out, float *conf, void *workspace,
+                          size_t workspace_bytes, void *stream, void *const *events, int n_events,
+                          int reps, int *n_kernels, const char **names);
 
 #ifdef __cplusplus
 }

@@ -292,15 +292,30 @@ HeadPlan plan_head(void *ws, int B, int Nt, int N, int n_heads, bool want_v) {
     return P;
 }
 
-int check_head(const void *q, const void *k, const int32_t *heads, int n_heads, int B, int H,
-               int Nt, int N, int hd, int dtype, int budget, const int32_t *kept) {
-    if (!q || !k || !heads || !kept) return PV_ERR_NULL;
+int check_qk(const void *q, const void *k, int B, int H, int Nt, int N, int hd, int dtype) {
+    if (!q || !k) return PV_ERR_NULL;
     if (dtype != PV_F32 && dtype != PV_BF16) return PV_ERR_DTYPE;
     if (B < 1 || B > 65535 || H < 1 || Nt < 1 || Nt > PV_MAX_TEXT || N < 1 || N > PV_MAX_TOKENS ||
         hd < 32 || hd > PV_MAX_HEAD_DIM || hd % 32 != 0)
         return PV_ERR_SHAPE;
+    if (!aligned16(q) || !aligned16(k)) return PV_ERR_ALIGN;
+    return PV_OK;
+}
+
+// heads: the host list (checked here), or NULL when the list is on the device
+// (heads_dev, which cannot be checked before the kernels read it).
+int check_head(const void *q, const void *k, const int32_t *heads, const int32_t *heads_dev,
+               int n_heads, int B, int H, int Nt, int N, int hd, int dtype, int budget,
+               const int32_t *kept) {
+    if (!kept || (!heads && !heads_dev)) return PV_ERR_NULL;
+    int rc = check_qk(q, k, B, H, Nt, N, hd, dtype);
+    if (rc != PV_OK) return rc;
     static_assert(PV_MAX_HEADS == pv::kMaxHeadArgs, "one sample's head list fits one launch");
     if (n_heads < 1 || n_heads > H || n_heads > PV_MAX_HEADS) return PV_ERR_HEADS;
+    if (!heads) {
+        if ((uintptr_t)heads_dev % 4) return PV_ERR_ALIGN;
+        return (budget < 1 || budget > N) ? PV_ERR_BUDGET : PV_OK;
+    }
     for (int b = 0; b < B; ++b) {
         const int32_t *hb = heads + (size_t)b * n_heads;
         for (int i = 0; i < n_heads; ++i) {
@@ -313,12 +328,12 @@ int check_head(const void *q, const void *k, const int32_t *heads, int n_heads, 
     return PV_OK;
 }
 
-int head_impl(const void *q, const void *k, const int32_t *heads, int n_heads, int B, int H, int Nt,
-              int N, int hd, int dtype, int budget, int32_t *kept, float *score, void *workspace,
-              size_t ws_bytes, void *stream, void *const *events, int n_events, int reps,
-              int *n_kernels, const char **names) {
+int head_impl(const void *q, const void *k, const int32_t *heads, const int32_t *heads_dev,
+              int n_heads, int B, int H, int Nt, int N, int hd, int dtype, int budget,
+              int32_t *kept, float *score, void *workspace, size_t ws_bytes, void *stream,
+              void *const *events, int n_events, int reps, int *n_kernels, const char **names) {
     if (reps < 1) return PV_ERR_SHAPE;
-    int rc = check_head(q, k, heads, n_heads, B, H, Nt, N, hd, dtype, budget, kept);
+    int rc = check_head(q, k, heads, heads_dev, n_heads, B, H, Nt, N, hd, dtype, budget, kept);
     if (rc != PV_OK) return rc;
     HeadPlan P0 = plan_head(nullptr, B, Nt, N, n_heads, score == nullptr);
     if (!workspace || ws_bytes < P0.bytes) return PV_ERR_WORKSPACE;
@@ -333,13 +348,50 @@ int head_impl(const void *q, const void *k, const int32_t *heads, int n_heads, i
     if (!tr.handles_ok()) return PV_ERR_NULL;
 
     if (!tr.launch("score_partial", [&] {
-            return pv::launch_score_partial(dt, q, k, heads, B, H, Nt, N, hd, n_heads, P.partial, st);
+            return pv::launch_score_partial(dt, q, k, heads, heads_dev, B, H, Nt, N, hd, n_heads,
+                                            P.partial, st);
         }))
         return PV_ERR_HIP;
     const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
     if (!tr.launch("score_select", [&] {
             return pv::launch_score_select(P.partial, B, n_heads * P.nrb, N, inv_norm, v, budget,
                                            kept, st);
+        }))
+        return PV_ERR_HIP;
+    if (!tr.after_all()) return PV_ERR_HIP;
+    if (n_kernels) *n_kernels = tr.launched;
+    return PV_OK;
+}
+
+size_t vis_heads_bytes(int B, int H, int Nt) {
+    Carve c(nullptr);
+    c.take<float>((size_t)B * H * ((Nt + 15) / 16));
+    return c.off + kAlign;
+}
+
+int vis_heads_impl(const void *q, const void *k, int B, int H, int Nt, int N, int hd, int dtype,
+                   int n_vis, int32_t *heads_out, float *conf, void *workspace, size_t ws_bytes,
+                   void *stream, void *const *events, int n_events, int reps, int *n_kernels,
+                   const char **names) {
+    if (reps < 1) return PV_ERR_SHAPE;
+    if (!heads_out) return PV_ERR_NULL;
+    int rc = check_qk(q, k, B, H, Nt, N, hd, dtype);
+    if (rc != PV_OK) return rc;
+    if (H > PV_MAX_HEADS || n_vis < 1 || n_vis > H) return PV_ERR_HEADS;
+    if (!workspace || ws_bytes < vis_heads_bytes(B, H, Nt)) return PV_ERR_WORKSPACE;
+    for (const void *p : {(const void *)heads_out, (const void *)conf, (const void *)workspace})
+        if (p && !aligned16(p)) return PV_ERR_ALIGN;
+    float *part = (float *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
+    const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
+    hipStream_t st = (hipStream_t)stream;
+    Trace tr{events, n_events, names, reps, st};
+    if (!tr.handles_ok()) return PV_ERR_NULL;
+    if (!tr.launch("head_conf", [&] {
+            return pv::launch_head_conf(dt, q, k, B, H, Nt, N, hd, part, st);
+        }))
+        return PV_ERR_HIP;
+    if (!tr.launch("conf_select", [&] {
+            return pv::launch_conf_select(part, B, H, Nt, conf, n_vis, heads_out, st);
         }))
         return PV_ERR_HIP;
     if (!tr.after_all()) return PV_ERR_HIP;
@@ -414,8 +466,9 @@ PV_API int pv_prune_head_aware(const void *q, const void *k, const int32_t *head
                                int B, int H, int Nt, int N, int hd, int dtype, int budget,
                                int32_t *kept, float *score, void *workspace, size_t workspace_bytes,
                                void *stream) {
-    return head_impl(q, k, heads_host, n_heads, B, H, Nt, N, hd, dtype, budget, kept, score,
-                     workspace, workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr);
+    if (!heads_host) return PV_ERR_NULL;
+    return head_impl(q, k, heads_host, nullptr, n_heads, B, H, Nt, N, hd, dtype, budget, kept,
+                     score, workspace, workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr);
 }
 
 PV_API int pv_prune_head_aware_timed(const void *q, const void *k, const int32_t *heads_host,
@@ -423,8 +476,52 @@ PV_API int pv_prune_head_aware_timed(const void *q, const void *k, const int32_t
                                      int budget, int32_t *kept, float *score, void *workspace,
                                      size_t workspace_bytes, void *stream, void *const *events,
                                      int n_events, int reps, int *n_kernels, const char **names) {
-    return head_impl(q, k, heads_host, n_heads, B, H, Nt, N, hd, dtype, budget, kept, score,
-                     workspace, workspace_bytes, stream, events, n_events, reps, n_kernels, names);
+    if (!heads_host) return PV_ERR_NULL;
+    return head_impl(q, k, heads_host, nullptr, n_heads, B, H, Nt, N, hd, dtype, budget, kept,
+                     score, workspace, workspace_bytes, stream, events, n_events, reps, n_kernels,
+                     names);
+}
+
+PV_API int pv_prune_head_aware_dev(const void *q, const void *k, const int32_t *heads_dev,
+                                   int n_heads, int B, int H, int Nt, int N, int hd, int dtype,
+                                   int budget, int32_t *kept, float *score, void *workspace,
+                                   size_t workspace_bytes, void *stream) {
+    if (!heads_dev) return PV_ERR_NULL;
+    return head_impl(q, k, nullptr, heads_dev, n_heads, B, H, Nt, N, hd, dtype, budget, kept,
+                     score, workspace, workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr);
+}
+
+PV_API int pv_prune_head_aware_dev_timed(const void *q, const void *k, const int32_t *heads_dev,
+                                         int n_heads, int B, int H, int Nt, int N, int hd,
+                                         int dtype, int budget, int32_t *kept, float *score,
+                                         void *workspace, size_t workspace_bytes, void *stream,
+                                         void *const *events, int n_events, int reps,
+                                         int *n_kernels, const char **names) {
+    if (!heads_dev) return PV_ERR_NULL;
+    return head_impl(q, k, nullptr, heads_dev, n_heads, B, H, Nt, N, hd, dtype, budget, kept,
+                     score, workspace, workspace_bytes, stream, events, n_events, reps, n_kernels,
+                     names);
+}
+
+PV_API size_t pv_visual_heads_workspace_bytes(int B, int H, int Nt) {
+    if (B < 1 || H < 1 || Nt < 1) return 0;
+    return vis_heads_bytes(B, H, Nt);
+}
+
+PV_API int pv_visual_heads(const void *q, const void *k, int B, int H, int Nt, int N, int hd,
+                           int dtype, int n_vis, int32_t *heads_out, float *conf, void *workspace,
+                           size_t workspace_bytes, void *stream) {
+    return vis_heads_impl(q, k, B, H, Nt, N, hd, dtype, n_vis, heads_out, conf, workspace,
+                          workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr);
+}
+
+PV_API int pv_visual_heads_timed(const void *q, const void *k, int B, int H, int Nt, int N, int hd,
+                                 int dtype, int n_vis, int32_t *heads_out, float *conf,
+                                 void *workspace, size_t workspace_bytes, void *stream,
+                                 void *const *events, int n_events, int reps, int *n_kernels,
+                                 const char **names) {
+    return vis_heads_impl(q, k, B, H, Nt, N, hd, dtype, n_vis, heads_out, conf, workspace,
+                          workspace_bytes, stream, events, n_events, reps, n_kernels, names);
 }
 
 namespace {

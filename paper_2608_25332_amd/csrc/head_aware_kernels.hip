@@ -32,6 +32,18 @@ __device__ __forceinline__ void lse_merge(float &m, float &l, float m2, float l2
     m = mn;
 }
 
+// The same merge carrying the sum of squared exponentials, s = sum 2^(2(x - m)),
+// which rescales by the square of the factor that rescales l.
+__device__ __forceinline__ void lse_merge2(float &m, float &l, float &s, float m2, float l2,
+                                           float s2) {
+    const float mn = fmaxf(m, m2);
+    if (mn == -INFINITY) return;
+    const float a = exp2f(m - mn), c = exp2f(m2 - mn);
+    l = l * a + l2 * c;
+    s = s * (a * a) + s2 * (c * c);
+    m = mn;
+}
+
 // Key rows are streamed through an LDS ring 64 at a time with direct-to-LDS
 // loads (one CU sustains several times the bytes register loads reach), the
 // next chunks in flight while the current one is multiplied; each wave takes
@@ -52,14 +64,23 @@ struct ScoreStage {
     static_assert(STAGE % 4096 == 0, "chunk must split evenly over the waves");
 };
 
-template <int DT, int NKS, int MAXC>
+// Where the head of list entry hi of sample b comes from.
+enum HeadSource { kHeadsArg = 0, kHeadsDevice = 1, kHeadsAll = 2 };
+
+// CONF = false: column sums of the normalised rows (the score).  CONF = true:
+// one pass only, also carrying the sum of squared probabilities of each row,
+// and one number per workgroup: the sum over its rows of the row variance
+// (the head confidence of this row block).
+template <int DT, int NKS, int MAXC, bool CONF>
 __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
-    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads, int b0, int H, int Nt,
-    int N, int n_heads, float scale_log2e, float *__restrict__ partial, int cols_in_lds) {
+    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
+    const int32_t *__restrict__ heads_dev, int head_src, int b0, int H, int Nt, int N,
+    int n_heads, float scale_log2e, float *__restrict__ partial, int cols_in_lds) {
+    static_assert(!CONF || MAXC == 0, "the confidence needs no second pass");
     using S = ScoreStage<NKS>;
     __shared__ __attribute__((aligned(16))) char ring[S::NS][S::STAGE];
     __shared__ __attribute__((aligned(16))) char qrows[16 * S::RB];
-    __shared__ float sm_m[4][16], sm_l[4][16];
+    __shared__ float sm_m[4][16], sm_l[4][16], sm_s[CONF ? 4 : 1][16];
     __shared__ float row_m[16], row_il[16];
     const int nrb = (Nt + 15) / 16;
     const int L = xcd_tile(blockIdx.x, gridDim.x);
@@ -69,7 +90,10 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     // uniform wave index: the block guards around the MFMAs become scalar
     // branches (an MFMA does not honour the execution mask)
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int h = heads.h[bl * n_heads + hi];
+    int h;
+    if (head_src == kHeadsAll) h = hi;
+    else if (head_src == kHeadsDevice) h = min(max(heads_dev[(size_t)b * n_heads + hi], 0), H - 1);
+    else h = heads.h[bl * n_heads + hi];
     const char *qb = q + ((size_t)b * H + h) * Nt * S::RB;
     const char *kb = k + ((size_t)b * H + h) * N * S::RB;
 
@@ -160,16 +184,20 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
 
     // pass 1: running (max, sum of exp) of the logits, per lane and row; with
     // MAXC > 0 the logit blocks also stay in registers for pass 2
-    float m[4], l[4];
+    float m[4], l[4], sq[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         m[i] = -INFINITY;
         l[i] = 0.f;
+        sq[i] = 0.f;
     }
     auto stats = [&](const f32x4_t &acc, int ch) {
         if (ch * kScoreCK + wave * 16 + (lane & 15) < N) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) lse_merge(m[i], l[i], acc[i] * scale_log2e, 1.f);
+            for (int i = 0; i < 4; ++i) {
+                if (CONF) lse_merge2(m[i], l[i], sq[i], acc[i] * scale_log2e, 1.f, 1.f);
+                else lse_merge(m[i], l[i], acc[i] * scale_log2e, 1.f);
+            }
         }
     };
     f32x4_t keep[MAXC > 0 ? MAXC : 1];
@@ -196,7 +224,12 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         for (int i = 0; i < 4; ++i) {
             const float m2 = __shfl_xor(m[i], off, 64);
             const float l2 = __shfl_xor(l[i], off, 64);
-            lse_merge(m[i], l[i], m2, l2);
+            if (CONF) {
+                const float s2 = __shfl_xor(sq[i], off, 64);
+                lse_merge2(m[i], l[i], sq[i], m2, l2, s2);
+            } else {
+                lse_merge(m[i], l[i], m2, l2);
+            }
         }
     }
     if ((lane & 15) == 0) {
@@ -204,9 +237,28 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         for (int i = 0; i < 4; ++i) {
             sm_m[wave][(lane >> 4) * 4 + i] = m[i];
             sm_l[wave][(lane >> 4) * 4 + i] = l[i];
+            if (CONF) sm_s[CONF ? wave : 0][(lane >> 4) * 4 + i] = sq[i];
         }
     }
     __syncthreads();
+    if constexpr (CONF) {
+        // Var_j(A[i][j]) = (sum_j A^2 - 1/N) / N with sum_j A^2 = s / l^2;
+        // the 16 rows added in order (rows past Nt add nothing)
+        if (tid < 16) {
+            float mm = sm_m[0][tid], ll = sm_l[0][tid], ss = sm_s[0][tid];
+#pragma unroll
+            for (int w = 1; w < 4; ++w) lse_merge2(mm, ll, ss, sm_m[w][tid], sm_l[w][tid], sm_s[w][tid]);
+            const float inv_n = 1.0f / (float)N;
+            row_m[tid] = (rb * 16 + tid < Nt) ? (ss / (ll * ll) - inv_n) * inv_n : 0.f;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            float c = 0.f;
+            for (int r = 0; r < 16; ++r) c += row_m[r];
+            partial[((size_t)b * H + h) * nrb + rb] = c;
+        }
+        return;
+    }
     if (tid < 16) {
         float mm = sm_m[0][tid], ll = sm_l[0][tid];
 #pragma unroll
@@ -317,26 +369,41 @@ __global__ __launch_bounds__(NT) void score_select_kernel(const float *__restric
 
 // The head lists travel as a kernel argument of bounded size: a launch covers
 // as many samples as fit, and larger batches take several launches.
-template <int DT, int NKS, int MAXC>
-static hipError_t score_go(const void *q, const void *k, const int32_t *heads, int B, int H,
-                           int Nt, int N, int n_heads, float scale_log2e, float *partial,
-                           hipStream_t st) {
+struct ScoreLaunch {
+    const void *q, *k;
+    const int32_t *heads_host;  // kHeadsArg: host list [B][n_heads]
+    const int32_t *heads_dev;   // kHeadsDevice: device list [B][n_heads]
+    int src;
+    int B, H, Nt, N, n_heads;
+    float sl2e;
+    float *partial;
+    hipStream_t st;
+};
+
+// A host head list travels as a kernel argument of bounded size: a launch
+// covers as many samples as fit, and larger batches take several launches.
+// Device lists and the all-heads form need one launch.
+template <int DT, int NKS, int MAXC, bool CONF>
+static hipError_t score_go(const ScoreLaunch &a) {
     using S = ScoreStage<NKS>;
     // two-pass form: the N column sums in dynamic LDS when they fit beside
     // the ring and the row statistics (at most 64 KiB of it)
-    const size_t cols = (size_t)N * sizeof(float);
-    const bool in_lds = MAXC == 0 && cols <= 65536 &&
+    const size_t cols = (size_t)a.N * sizeof(float);
+    const bool in_lds = !CONF && MAXC == 0 && cols <= 65536 &&
                         (size_t)S::NS * S::STAGE + 16 * S::RB + 1024 + cols <= (size_t)kScoreLdsCap;
-    const int per_launch = kMaxHeadArgs / n_heads;
+    const int nrb = (a.Nt + 15) / 16;
+    const int per_launch = a.src == kHeadsArg ? kMaxHeadArgs / a.n_heads : a.B;
     HeadArgs ha;
-    for (int b0 = 0; b0 < B; b0 += per_launch) {
-        const int nb = B - b0 < per_launch ? B - b0 : per_launch;
+    for (int b0 = 0; b0 < a.B; b0 += per_launch) {
+        const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
         for (int i = 0; i < kMaxHeadArgs; ++i)
-            ha.h[i] = i < nb * n_heads ? heads[(size_t)b0 * n_heads + i] : 0;
-        dim3 grid(((Nt + 15) / 16) * n_heads * nb);
-        hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC>), grid, dim3(kScoreNT),
-                           in_lds ? cols : 0, st, (const char *)q, (const char *)k, ha, b0, H, Nt,
-                           N, n_heads, scale_log2e, partial, in_lds ? 1 : 0);
+            ha.h[i] = (a.src == kHeadsArg && i < nb * a.n_heads)
+                          ? a.heads_host[(size_t)b0 * a.n_heads + i] : 0;
+        dim3 grid(nrb * a.n_heads * nb);
+        hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC, CONF>), grid, dim3(kScoreNT),
+                           in_lds ? cols : 0, a.st, (const char *)a.q, (const char *)a.k, ha,
+                           a.heads_dev, a.src, b0, a.H, a.Nt, a.N, a.n_heads, a.sl2e, a.partial,
+                           in_lds ? 1 : 0);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -350,32 +417,30 @@ static hipError_t score_go(const void *q, const void *k, const int32_t *heads, i
 template <int NKS>
 constexpr int score_maxc_cap() { return NKS <= 4 ? 16 : (NKS <= 8 ? 8 : 4); }
 
-template <int DT, int NKS>
-static hipError_t score_nks(const void *q, const void *k, const int32_t *heads, int B, int H,
-                            int Nt, int N, int n_heads, float sl2e, float *partial,
-                            hipStream_t st) {
-    const int nch = (N + kScoreCK - 1) / kScoreCK;
-    constexpr int cap = score_maxc_cap<NKS>();
-#define PV_MAXC_CASE(mc)                                                                           \
-    if (nch <= mc && mc <= cap)                                                                    \
-        return score_go<DT, NKS, (mc <= cap ? mc : 0)>(q, k, heads, B, H, Nt, N, n_heads, sl2e,   \
-                                                       partial, st);
-    PV_MAXC_CASE(1)
-    PV_MAXC_CASE(2)
-    PV_MAXC_CASE(4)
-    PV_MAXC_CASE(8)
-    PV_MAXC_CASE(16)
+template <int DT, int NKS, bool CONF>
+static hipError_t score_nks(const ScoreLaunch &a) {
+    if constexpr (CONF) {
+        return score_go<DT, NKS, 0, true>(a);
+    } else {
+        const int nch = (a.N + kScoreCK - 1) / kScoreCK;
+        constexpr int cap = score_maxc_cap<NKS>();
+#define PV_MAXC_CASE(mc) \
+    if (nch <= mc && mc <= cap) return score_go<DT, NKS, (mc <= cap ? mc : 0), false>(a);
+        PV_MAXC_CASE(1)
+        PV_MAXC_CASE(2)
+        PV_MAXC_CASE(4)
+        PV_MAXC_CASE(8)
+        PV_MAXC_CASE(16)
 #undef PV_MAXC_CASE
-    return score_go<DT, NKS, 0>(q, k, heads, B, H, Nt, N, n_heads, sl2e, partial, st);
+        return score_go<DT, NKS, 0, false>(a);
+    }
 }
 
-template <int DT>
-static hipError_t score_dt(int nks, const void *q, const void *k, const int32_t *heads, int B,
-                           int H, int Nt, int N, int n_heads, float sl2e,
-                           float *partial, hipStream_t st) {
+template <int DT, bool CONF>
+static hipError_t score_dt(int nks, const ScoreLaunch &a) {
 #define PV_NKS_CASE(n) \
     case n:            \
-        return score_nks<DT, n>(q, k, heads, B, H, Nt, N, n_heads, sl2e, partial, st);
+        return score_nks<DT, n, CONF>(a);
     switch (nks) {
         PV_NKS_CASE(1)
         PV_NKS_CASE(2)
@@ -394,15 +459,62 @@ static hipError_t score_dt(int nks, const void *q, const void *k, const int32_t 
     return hipErrorInvalidValue;
 }
 
-hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads,
-                                int B, int H, int Nt, int N, int hd, int n_heads, float *partial,
-                                hipStream_t st) {
+template <bool CONF>
+static hipError_t score_any(int dt, int hd, ScoreLaunch a) {
     const int esz = (dt == kBF16) ? 2 : 4;
-    const int hd_bytes = hd * esz;
-    const int nks = hd_bytes / 64;
-    const float sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
-    if (dt == kBF16) return score_dt<kBF16>(nks, q, k, heads, B, H, Nt, N, n_heads, sl2e, partial, st);
-    return score_dt<kF32>(nks, q, k, heads, B, H, Nt, N, n_heads, sl2e, partial, st);
+    const int nks = hd * esz / 64;
+    a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
+    if (dt == kBF16) return score_dt<kBF16, CONF>(nks, a);
+    return score_dt<kF32, CONF>(nks, a);
+}
+
+hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
+                                const int32_t *heads_dev, int B, int H, int Nt, int N, int hd,
+                                int n_heads, float *partial, hipStream_t st) {
+    ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg,
+                  B, H, Nt, N, n_heads, 0.f, partial, st};
+    return score_any<false>(dt, hd, a);
+}
+
+hipError_t launch_head_conf(int dt, const void *q, const void *k, int B, int H, int Nt, int N,
+                            int hd, float *partial, hipStream_t st) {
+    ScoreLaunch a{q, k, nullptr, nullptr, kHeadsAll, B, H, Nt, N, H, 0.f, partial, st};
+    return score_any<true>(dt, hd, a);
+}
+
+// ----------------------------------------------------------------------------
+// conf_select: one workgroup per sample.  C[h] = the row-block partials of
+// head h added in order; the n_vis heads of largest C (ties to the lower
+// head id) are written in ascending order.
+// ----------------------------------------------------------------------------
+__global__ __launch_bounds__(256) void conf_select_kernel(const float *__restrict__ part, int H,
+                                                          int nrb, float *__restrict__ conf,
+                                                          int n_vis, int32_t *__restrict__ heads) {
+    __shared__ TopkSmem sm;
+    const int b = blockIdx.x;
+    const int E = topk_per_thread(H, 256), h0 = threadIdx.x * E;
+    uint32_t key[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const int h = h0 + e;
+        key[e] = 0u;
+        if (e < E && h < H) {
+            const float *ph = part + ((size_t)b * H + h) * nrb;
+            float c = 0.f;
+            for (int r = 0; r < nrb; ++r) c += ph[r];
+            if (conf) conf[(size_t)b * H + h] = c;
+            key[e] = order_key(c);
+        }
+    }
+    block_topk<256, 2>(key, H, n_vis, heads + (size_t)b * n_vis, nullptr, nullptr, sm);
+}
+
+hipError_t launch_conf_select(const float *partial, int B, int H, int Nt, float *conf, int n_vis,
+                              int32_t *heads, hipStream_t st) {
+    if (H > 512) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(conf_select_kernel, dim3(B), dim3(256), 0, st, partial, H, (Nt + 15) / 16,
+                       conf, n_vis, heads);
+    return hipGetLastError();
 }
 
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,

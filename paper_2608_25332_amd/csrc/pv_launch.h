@@ -67,9 +67,16 @@ hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
                         const int32_t *assign, void *merged, hipStream_t st);
 
 // ---- head-aware pruning (Sec. 4.4)
+// heads_dev == nullptr: the head list is heads_host (host memory); else the
+// device list heads_dev (entries clamped into [0, H)).
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
-                                int B, int H, int Nt, int N, int hd, int n_heads, float *partial,
-                                hipStream_t st);
+                                const int32_t *heads_dev, int B, int H, int Nt, int N, int hd,
+                                int n_heads, float *partial, hipStream_t st);
+// Head confidence of every head, per 16-row block: partial[b][h][rb].
+hipError_t launch_head_conf(int dt, const void *q, const void *k, int B, int H, int Nt, int N,
+                            int hd, float *partial, hipStream_t st);
+hipError_t launch_conf_select(const float *partial, int B, int H, int Nt, float *conf, int n_vis,
+                              int32_t *heads, hipStream_t st);
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,
                                float *v, int budget, int32_t *kept, hipStream_t st);
 

@@ -83,6 +83,20 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_head_aware_timed.argtypes = ha + [ctypes.POINTER(_vp), _i, _i,
                                                    ctypes.POINTER(_i), names_t]
     lib.pv_prune_head_aware_timed.restype = _i
+    had = [_vp, _vp, _vp] + ha[3:]
+    lib.pv_prune_head_aware_dev.argtypes = had
+    lib.pv_prune_head_aware_dev.restype = _i
+    lib.pv_prune_head_aware_dev_timed.argtypes = had + [ctypes.POINTER(_vp), _i, _i,
+                                                        ctypes.POINTER(_i), names_t]
+    lib.pv_prune_head_aware_dev_timed.restype = _i
+    lib.pv_visual_heads_workspace_bytes.argtypes = [_i, _i, _i]
+    lib.pv_visual_heads_workspace_bytes.restype = _sz
+    vh = [_vp, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _sz, _vp]
+    lib.pv_visual_heads.argtypes = vh
+    lib.pv_visual_heads.restype = _i
+    lib.pv_visual_heads_timed.argtypes = vh + [ctypes.POINTER(_vp), _i, _i, ctypes.POINTER(_i),
+                                               names_t]
+    lib.pv_visual_heads_timed.restype = _i
     lib.pv_prune_gather.argtypes = [_vp, _vp, _vp, _i, _i, _i, _i, _i64, _i64, _i64, _i64, _i64,
                                     _i64, _i64, _vp]
     lib.pv_prune_gather.restype = _i
@@ -211,10 +225,11 @@ def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
                         want_score: bool = True, out: Optional[dict] = None,
                         workspace: Optional[torch.Tensor] = None,
                         events: Optional[Sequence] = None, reps: int = 1):
-    """Head-aware pruning.  q [B,H,Nt,hd], k [B,H,N,hd] (same dtype), heads: host
-    int sequence [B, n_heads].  Returns dict(kept [B,budget] int32,
-    score [B,N] f32 | None, n_kernels).  events / reps: see
-    pv_prune_head_aware_timed (profiling only)."""
+    """Head-aware pruning.  q [B,H,Nt,hd], k [B,H,N,hd] (same dtype), heads:
+    host int sequence [B, n_heads], or an int32 tensor [B, n_heads] on q's
+    device (pv_prune_head_aware_dev: e.g. the list pv_visual_heads wrote).
+    Returns dict(kept [B,budget] int32, score [B,N] f32 | None, n_kernels).
+    events / reps: see pv_prune_head_aware_timed (profiling only)."""
     import numpy as np
 
     lib = load()
@@ -224,7 +239,14 @@ def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
     Bk, Hk, N, hdk = k.shape
     if (Bk, Hk, hdk) != (B, H, hd) or k.dtype != q.dtype:
         raise ValueError("k must be [B, H, N, hd] with the dtype of q")
-    hs = np.ascontiguousarray(np.asarray(heads, dtype=np.int32).reshape(B, -1))
+    on_dev = isinstance(heads, torch.Tensor) and heads.device.type != "cpu"
+    if on_dev:
+        if heads.dtype != torch.int32 or heads.dim() != 2 or heads.shape[0] != B:
+            raise ValueError("a device head list must be int32 [B, n_heads]")
+        _contig(heads, "heads")
+        hs = heads
+    else:
+        hs = np.ascontiguousarray(np.asarray(heads, dtype=np.int32).reshape(B, -1))
     n_heads = hs.shape[1]
     code = _dtype_code(q)
     dev = q.device
@@ -240,13 +262,56 @@ def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     ev, nev, nm = _events_array(events)
     nk = _i(0)
-    rc = lib.pv_prune_head_aware_timed(q.data_ptr(), k.data_ptr(),
-                                       hs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n_heads,
-                                       B, H, Nt, N, hd, code, int(budget), kept.data_ptr(),
-                                       _ptr(score), workspace.data_ptr(), workspace.numel(),
-                                       _stream(dev), ev, nev, int(reps), ctypes.byref(nk), nm)
+    if on_dev:
+        rc = lib.pv_prune_head_aware_dev_timed(q.data_ptr(), k.data_ptr(), hs.data_ptr(), n_heads,
+                                               B, H, Nt, N, hd, code, int(budget), kept.data_ptr(),
+                                               _ptr(score), workspace.data_ptr(), workspace.numel(),
+                                               _stream(dev), ev, nev, int(reps), ctypes.byref(nk),
+                                               nm)
+    else:
+        rc = lib.pv_prune_head_aware_timed(q.data_ptr(), k.data_ptr(),
+                                           hs.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)),
+                                           n_heads, B, H, Nt, N, hd, code, int(budget),
+                                           kept.data_ptr(), _ptr(score), workspace.data_ptr(),
+                                           workspace.numel(), _stream(dev), ev, nev, int(reps),
+                                           ctypes.byref(nk), nm)
     _check("pv_prune_head_aware", rc, lib)
     return {"kept": kept, "score": score, "n_kernels": nk.value,
+            "kernel_names": _names(nm, min(nk.value, max(nev - 1, 0))), "workspace": workspace}
+
+
+def pv_visual_heads(q: torch.Tensor, k: torch.Tensor, n_vis: int, *, want_conf: bool = True,
+                    out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None,
+                    events: Optional[Sequence] = None, reps: int = 1):
+    """Visual-head identification.  q [B,H,Nt,hd], k [B,H,N,hd].  Returns
+    dict(heads [B,n_vis] int32 on the device, ascending; conf [B,H] f32 |
+    None, n_kernels).  The head list can go straight to pv_prune_head_aware."""
+    lib = load()
+    _contig(q, "q")
+    _contig(k, "k")
+    B, H, Nt, hd = q.shape
+    Bk, Hk, N, hdk = k.shape
+    if (Bk, Hk, hdk) != (B, H, hd) or k.dtype != q.dtype:
+        raise ValueError("k must be [B, H, N, hd] with the dtype of q")
+    dev = q.device
+    o = out if out is not None else {}
+    heads = o.get("heads")
+    if heads is None:
+        heads = torch.empty((B, n_vis), dtype=torch.int32, device=dev)
+    conf = o.get("conf") if want_conf else None
+    if want_conf and conf is None:
+        conf = torch.empty((B, H), dtype=torch.float32, device=dev)
+    nbytes = lib.pv_visual_heads_workspace_bytes(B, H, Nt)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    ev, nev, nm = _events_array(events)
+    nk = _i(0)
+    rc = lib.pv_visual_heads_timed(q.data_ptr(), k.data_ptr(), B, H, Nt, N, hd, _dtype_code(q),
+                                   int(n_vis), heads.data_ptr(), _ptr(conf), workspace.data_ptr(),
+                                   workspace.numel(), _stream(dev), ev, nev, int(reps),
+                                   ctypes.byref(nk), nm)
+    _check("pv_visual_heads", rc, lib)
+    return {"heads": heads, "conf": conf, "n_kernels": nk.value,
             "kernel_names": _names(nm, min(nk.value, max(nev - 1, 0))), "workspace": workspace}
 
 

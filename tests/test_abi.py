@@ -116,6 +116,41 @@ def test_head_aware_validation(lib):
     assert _heads(lib, [[0], [1], [4]], B=3) == -4   # a later sample is checked too
 
 
+def test_head_aware_dev_validation(lib):
+    f = lib.pv_prune_head_aware_dev
+
+    def call(hd_ptr=FAKE, n_heads=2, H=4, hd=64, budget=8, q=FAKE, ws=FAKE, wsb=1 << 40):
+        return f(q, FAKE, hd_ptr, n_heads, 1, H, 16, 32, hd, 1, budget, FAKE, None, ws, wsb, None)
+    assert call(hd_ptr=None) == -1
+    assert call(q=None) == -1
+    assert call(n_heads=0) == -4
+    assert call(n_heads=5) == -4           # more than H
+    assert call(hd_ptr=FAKE + 2) == -8     # int32 list must be 4-byte aligned
+    assert call(hd=40) == -2
+    assert call(budget=33) == -3
+    assert call(ws=None) == -6
+
+
+def test_visual_heads_validation(lib):
+    f = lib.pv_visual_heads
+    assert lib.pv_visual_heads_workspace_bytes(1, 32, 64) > 0
+    assert lib.pv_visual_heads_workspace_bytes(0, 32, 64) == 0
+
+    def call(H=32, n_vis=6, Nt=64, N=192, hd=128, dt=1, out=FAKE, q=FAKE, ws=FAKE, wsb=1 << 40):
+        return f(q, FAKE, 1, H, Nt, N, hd, dt, n_vis, out, None, ws, wsb, None)
+    assert call(out=None) == -1
+    assert call(q=None) == -1
+    assert call(n_vis=0) == -4
+    assert call(n_vis=33) == -4
+    assert call(H=600, n_vis=6) == -4      # beyond PV_MAX_HEADS
+    assert call(hd=48) == -2
+    assert call(N=0) == -2
+    assert call(dt=7) == -5
+    assert call(ws=None) == -6
+    assert call(wsb=4) == -6
+    assert call(out=FAKE + 4) == -8
+
+
 def test_gather_validation(lib):
     g = lib.pv_prune_gather
     args = dict(src=FAKE, dst=FAKE, idx=FAKE, B=1, n=8, k=4, G=1, rb=256)

@@ -1,0 +1,158 @@
+"""Visual-head identification (Sec. 4.4, equations for C^h and V_l) on the
+GPU against the CPU oracle, and head-aware pruning with head lists that stay
+in device memory.  All calls go through the C ABI."""
+
+from __future__ import annotations
+
+import functools
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_25332_amd import workloads as W
+from parity_util import TOL, check_kept, rel_err, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+N_VIS = 6  # visual heads per pruning layer in the paper's experiments
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_25332_amd import provip
+    provip.load()
+
+
+@functools.lru_cache(maxsize=None)
+def workload(wid: int):
+    return W.make_workload(wid)
+
+
+def _subset_keys(w, n, seed):
+    rng = np.random.default_rng(seed)
+    idx = np.stack([np.sort(rng.choice(w.spec.Nv, n, replace=False)) for _ in range(w.spec.B)])
+    return np.ascontiguousarray(np.stack([w.k_full[b][:, idx[b]] for b in range(w.spec.B)]))
+
+
+def run_vis(q_np, k_np, dtype, n_vis):
+    from paper_2608_25332_amd import provip
+    r = provip.pv_visual_heads(to_dev(q_np, dtype), to_dev(k_np, dtype), n_vis)
+    torch.cuda.synchronize()
+    return to_host(r["heads"]), to_host(r["conf"])
+
+
+def check_heads(heads, conf_ref, n_vis, dtype):
+    for b in range(conf_ref.shape[0]):
+        check_kept(heads[b], conf_ref[b], n_vis, dtype)
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_visual_heads_parity(wid):
+    w = workload(wid)
+    dt = w.dtype
+    n_vis = min(N_VIS, w.spec.H - 1)
+    _say(f"[visual-heads] workload {wid} n_vis={n_vis}")
+    k1 = _subset_keys(w, w.N1, 500 + wid)
+    heads, conf = run_vis(w.q, k1, dt, n_vis)
+    ref_heads, ref_conf = oracle.visual_heads(w.q, k1, n_vis)
+    assert rel_err(conf, ref_conf) <= TOL[dt], rel_err(conf, ref_conf)
+    check_heads(heads, ref_conf, n_vis, dt)
+
+
+VIS_EDGE = [
+    # (B, H, Nt, N, hd, n_vis, dtype)
+    (1, 1, 1, 1, 32, 1, "f32"),         # one key: every row is (1), variance 0
+    (1, 3, 1, 15, 64, 3, "bf16"),       # every head chosen
+    (2, 8, 17, 70, 64, 1, "bf16"),      # ragged rows and keys
+    (3, 16, 33, 200, 128, 5, "bf16"),
+    (1, 4, 16, 300, 256, 2, "f32"),     # widest head
+    (2, 5, 40, 1500, 96, 2, "f32"),     # many chunks of keys
+    (1, 40, 128, 1152, 128, 6, "bf16"),
+]
+
+
+@pytest.mark.parametrize("B,H,Nt,N,hd,n_vis,dt", VIS_EDGE)
+def test_visual_heads_edges(B, H, Nt, N, hd, n_vis, dt):
+    _say(f"[visual-heads-edge] B={B} H={H} Nt={Nt} N={N} hd={hd} n_vis={n_vis} {dt}")
+    rng = np.random.default_rng(B * 100 + N)
+    q = (rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32)
+    k = (rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32)
+    if dt == "bf16":
+        q, k = W.bf16_round(q), W.bf16_round(k)
+    heads, conf = run_vis(q, k, dt, n_vis)
+    ref_heads, ref_conf = oracle.visual_heads(q, k, n_vis)
+    if np.max(np.abs(ref_conf)) == 0.0:
+        assert np.max(np.abs(conf)) < 1e-7
+    else:
+        assert rel_err(conf, ref_conf) <= TOL[dt], rel_err(conf, ref_conf)
+    check_heads(heads, ref_conf, n_vis, dt)
+    if n_vis == H:
+        assert np.array_equal(heads, np.tile(np.arange(H), (B, 1)))
+
+
+def test_visual_heads_uniform_head_is_never_chosen():
+    """A head whose queries are zero attends uniformly (C = 0): it is never
+    among the visual heads while other heads have C > 0."""
+    rng = np.random.default_rng(7)
+    B, H, Nt, N, hd = 2, 8, 20, 100, 64
+    q = rng.standard_normal((B, H, Nt, hd)).astype(np.float32) * 2
+    k = rng.standard_normal((B, H, N, hd)).astype(np.float32) * 2
+    q[:, 3] = 0.0
+    heads, conf = run_vis(q, k, "f32", H - 1)
+    assert np.all(np.abs(conf[:, 3]) < 1e-9)
+    assert not np.any(heads == 3)
+
+
+def test_head_aware_device_list_matches_host_list():
+    """The device-list entry point gives bit-identical results to the host
+    list (same kernels), over a batch that needs two launches for the host
+    list (640 list entries)."""
+    from paper_2608_25332_amd import provip
+    rng = np.random.default_rng(8)
+    B, H, Nt, N, hd, nh = 40, 16, 16, 96, 64, 16
+    q = W.bf16_round(rng.standard_normal((B, H, Nt, hd)).astype(np.float32))
+    k = W.bf16_round(rng.standard_normal((B, H, N, hd)).astype(np.float32))
+    hs = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+    qd, kd = to_dev(q, "bf16"), to_dev(k, "bf16")
+    a = provip.pv_prune_head_aware(qd, kd, hs, 20)
+    b = provip.pv_prune_head_aware(qd, kd, torch.from_numpy(hs).to("cuda:0"), 20)
+    torch.cuda.synchronize()
+    assert torch.equal(a["kept"], b["kept"])
+    assert torch.equal(a["score"], b["score"])
+
+
+@pytest.mark.parametrize("wid", [2, 4])
+def test_visual_heads_then_head_aware(wid):
+    """The shallow-layer chain of Sec. 4.4: identify the visual heads, then
+    aggregate over them, with the list never leaving the GPU; compared with
+    the oracle run on the oracle's own visual heads (where the two head sets
+    agree)."""
+    from paper_2608_25332_amd import provip
+    w = workload(wid)
+    dt = w.dtype
+    k1 = _subset_keys(w, w.N1, 600 + wid)
+    qd, kd = to_dev(w.q, dt), to_dev(k1, dt)
+    vh = provip.pv_visual_heads(qd, kd, N_VIS)
+    r = provip.pv_prune_head_aware(qd, kd, vh["heads"], w.N2)
+    torch.cuda.synchronize()
+    ref_heads, ref_conf = oracle.visual_heads(w.q, k1, N_VIS)
+    gh = to_host(vh["heads"])
+    same = [b for b in range(w.spec.B) if np.array_equal(gh[b], ref_heads[b])]
+    assert same, "no sample where the head sets agree"
+    ref_kept, ref_v = oracle.head_aware(w.q[same], k1[same], ref_heads[same], w.N2)
+    v = to_host(r["score"])[same]
+    kept = to_host(r["kept"])[same]
+    assert rel_err(v, ref_v) <= TOL[dt]
+    for i in range(len(same)):
+        check_kept(kept[i], ref_v[i], w.N2, dt)
