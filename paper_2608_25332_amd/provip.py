@@ -221,6 +221,10 @@ def pv_head_aware_workspace_bytes(B: int, H: int, Nt: int, N: int, hd: int, n_he
     return int(load().pv_head_aware_workspace_bytes(B, H, Nt, N, hd, n_heads, budget, dtype))
 
 
+def pv_visual_heads_workspace_bytes(B: int, H: int, Nt: int) -> int:
+    return int(load().pv_visual_heads_workspace_bytes(B, H, Nt))
+
+
 def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
                         want_score: bool = True, out: Optional[dict] = None,
                         workspace: Optional[torch.Tensor] = None,
