@@ -8,6 +8,7 @@ code with the HIP library: the arithmetic lives in ``provip_oracle.c``
 ctypes, one sample at a time.
 
 Function map (paper passages are cited at each C function):
+  critical_text              -- Sec. 4.2, equations for r and T
   cosine / center / maxpool  -- Sec. 4.3, equations for M, M-hat and p
   topk                       -- retention of the N_1 / N_2 highest scores
   assign / merge             -- Sec. 4.3, nearest-centroid aggregation
@@ -87,6 +88,8 @@ def _declare(lib):
     lib.orc_head_aware_score.restype = _int
     lib.orc_head_aware.argtypes = [_D, _D, _int, _int, _int, _int, _I, _int, _int, _I, _D]
     lib.orc_head_aware.restype = _int
+    lib.orc_critical_text.argtypes = [_D, _int, _int, _D, _I]
+    lib.orc_critical_text.restype = _int
     lib.orc_head_confidence.argtypes = [_D, _D, _int, _int, _int, _int, _D]
     lib.orc_head_confidence.restype = _int
     lib.orc_visual_heads.argtypes = [_D, _D, _int, _int, _int, _int, _int, _I, _D]
@@ -114,6 +117,25 @@ def _pi(a: np.ndarray):
 
 class OracleError(RuntimeError):
     pass
+
+
+# ------------------------------------------------------- critical text --
+
+def critical_text(text, *, lib=None):
+    """Sec. 4.2 over a batch: text [B, nt, d] -> (r [B, nt], mask [B, nt]
+    int32 with 1 for the critical tokens, count [B])."""
+    lib = lib or load()
+    E = _f64(text)
+    B, nt, d = E.shape
+    r = np.empty((B, nt), np.float64)
+    mask = np.empty((B, nt), np.int32)
+    count = np.empty(B, np.int32)
+    for b in range(B):
+        c = lib.orc_critical_text(_pd(E[b]), nt, d, _pd(r[b]), _pi(mask[b]))
+        if c < 0:
+            raise OracleError(f"orc_critical_text rc={c}")
+        count[b] = c
+    return r, mask, count
 
 
 # ---------------------------------------------------------------- stage A --

@@ -21,6 +21,59 @@
 #include <string.h>
 
 /* --------------------------------------------------------------------------
+ * Sec. 4.2, equations for r and T: critical text tokens from the text's own
+ * similarity, decoupled from the image.  With E the text embeddings [nt][d],
+ *     r[j] = (1/nt) sum_i softmax_j(e_i . e_j)     (no scaling of E E^T),
+ *     T    = { j : r[j] > mean(r) }.
+ * Reading: when no r[j] lies strictly above the mean (all equal; N(0,1)
+ * rows of width >= 256 give that, every softmax row being one-hot on its
+ * own token), T is every token.
+ * E: [nt][d]; r: [nt] out; mask: [nt] out, 1 for j in T.  Returns |T|, or
+ * -3 on no memory.
+ * ------------------------------------------------------------------------ */
+int orc_critical_text(const double *E, int nt, int d, double *r, int32_t *mask)
+{
+    double *S = (double *)malloc(sizeof(double) * (size_t)nt * nt);
+    if (!S) return -3;
+    for (int i = 0; i < nt; ++i) {
+        double *row = S + (size_t)i * nt;
+        for (int j = 0; j < nt; ++j) {
+            double s = 0.0;
+            for (int c = 0; c < d; ++c) s += E[(size_t)i * d + c] * E[(size_t)j * d + c];
+            row[j] = s;
+        }
+        double m = row[0];
+        for (int j = 1; j < nt; ++j)
+            if (row[j] > m) m = row[j];
+        double z = 0.0;
+        for (int j = 0; j < nt; ++j) {
+            row[j] = exp(row[j] - m);
+            z += row[j];
+        }
+        for (int j = 0; j < nt; ++j) row[j] /= z;
+    }
+    for (int j = 0; j < nt; ++j) {
+        double s = 0.0;
+        for (int i = 0; i < nt; ++i) s += S[(size_t)i * nt + j];
+        r[j] = s / (double)nt;
+    }
+    double mean = 0.0;
+    for (int j = 0; j < nt; ++j) mean += r[j];
+    mean /= (double)nt;
+    int count = 0;
+    for (int j = 0; j < nt; ++j) {
+        mask[j] = r[j] > mean ? 1 : 0;
+        count += mask[j];
+    }
+    if (count == 0) {
+        for (int j = 0; j < nt; ++j) mask[j] = 1;
+        count = nt;
+    }
+    free(S);
+    return count;
+}
+
+/* --------------------------------------------------------------------------
  * Sec. 4.3, equation for M: cosine similarity between the i-th critical text
  * token and the j-th visual token,
  *     M[i][j] = (t_i . v_j) / (|t_i| |v_j|).

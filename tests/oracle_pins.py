@@ -33,6 +33,61 @@ def _rot(d, rng):
     return q
 
 
+# ----------------------------------------------------------- Eq. r, T -----
+
+def pin_critical_text_two_tokens(lib):
+    """Sec. 4.2 on two orthogonal text tokens of squared norms a and b: the
+    logits are [[a, 0], [0, b]], so with s(x) the logistic function
+    r = ((s(a) + 1 - s(b)) / 2, (1 - s(a) + s(b)) / 2), and T holds the token
+    of larger norm alone (r[0] > 1/2 exactly when a > b)."""
+    for a, b in ((1.5, 0.25), (0.2, 2.0), (3.0, 2.9)):
+        E = np.zeros((1, 2, 3))
+        E[0, 0, 0] = math.sqrt(a)
+        E[0, 1, 2] = math.sqrt(b)
+        r, mask, count = O.critical_text(E, lib=lib)
+        sg = lambda x: 1.0 / (1.0 + math.exp(-x))
+        want = np.array([(sg(a) + 1 - sg(b)) / 2, (1 - sg(a) + sg(b)) / 2])
+        assert np.max(np.abs(r[0] - want)) < 1e-15
+        assert mask[0].tolist() == ([1, 0] if a > b else [0, 1]) and count[0] == 1
+
+
+def pin_critical_text_strictly_above_mean(lib):
+    """Sec. 4.2, equation for T keeps tokens strictly above the mean.  Four
+    integer vectors whose logit gaps (>= 2048) make every softmax row exact
+    in float64: rows (1,0,0,0), (1/2,1/2,0,0), (1/2,0,1/2,0), (0,1/2,1/2,0),
+    so r = (1/2, 1/4, 1/4, 0) and the mean is 1/4: T = {0} only."""
+    E = np.array([[[256.0, 0, 0], [128, 128, 0], [128, 0, 128], [0, 32, 32]]])
+    r, mask, count = O.critical_text(E, lib=lib)
+    assert r[0].tolist() == [0.5, 0.25, 0.25, 0.0]
+    assert mask[0].tolist() == [1, 0, 0, 0] and count[0] == 1
+
+
+def pin_critical_text_library_and_fallback(lib):
+    """r is the column mean of torch.softmax(E E^T) in float64 (no scale),
+    sums to 1, and permuting the tokens permutes r and T; when every r is
+    equal (orthogonal rows of equal norm: each row's softmax is the same up
+    to a shift and one-hot in float64) no token is above the mean and T is
+    every token."""
+    import torch
+    rng = np.random.default_rng(35)
+    E = rng.standard_normal((3, 9, 12)) * 0.4
+    r, mask, count = O.critical_text(E, lib=lib)
+    for b in range(3):
+        t = torch.from_numpy(E[b])
+        want = torch.softmax(t @ t.T, dim=-1).mean(dim=0).numpy()
+        assert np.max(np.abs(r[b] - want)) < 1e-15
+        assert abs(r[b].sum() - 1.0) < 1e-14
+        assert np.array_equal(mask[b], (want > want.mean()).astype(np.int32))
+        assert count[b] == mask[b].sum() and 0 < count[b] < 9
+    perm = rng.permutation(9)
+    rp, mp, _ = O.critical_text(E[:, perm], lib=lib)
+    assert np.max(np.abs(rp - r[:, perm])) < 1e-15 and np.array_equal(mp, mask[:, perm])
+    Q = _rot(8, rng) * 100.0            # 8 orthogonal rows, squared norm 1e4
+    r2, m2, c2 = O.critical_text(Q[None], lib=lib)
+    assert np.all(r2 == 0.125)
+    assert c2[0] == 8 and np.all(m2 == 1)
+
+
 # ------------------------------------------------------------------ Eq. M --
 
 def pin_cosine_known_angles(lib):

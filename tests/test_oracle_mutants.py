@@ -45,6 +45,13 @@ MUTANTS = [
     ("headaware-row-sum-not-col", "for (int i = 0; i < nt; ++i) s += S[(size_t)i * n + j];",
      "for (int i = 0; i < nt; ++i) s += S[(size_t)(j % nt) * n + (i % n)];"),
     ("gather-src-stride", "src + b * sb + g * sg + j * sr", "src + b * sb + j * sr"),
+    ("text-scaled-logits", "row[j] = s;\n        }\n        double m = row[0];\n        for (int j = 1; j < nt; ++j)",
+     "row[j] = s / sqrt((double)d);\n        }\n        double m = row[0];\n        for (int j = 1; j < nt; ++j)"),
+    ("text-row-mean-not-column", "for (int i = 0; i < nt; ++i) s += S[(size_t)i * nt + j];",
+     "for (int i = 0; i < nt; ++i) s += S[(size_t)j * nt + i];"),
+    ("text-at-or-above-mean", "mask[j] = r[j] > mean ? 1 : 0;", "mask[j] = r[j] >= mean ? 1 : 0;"),
+    ("text-below-mean", "mask[j] = r[j] > mean ? 1 : 0;", "mask[j] = r[j] < mean ? 1 : 0;"),
+    ("text-no-fallback", "if (count == 0) {", "if (count < 0) {"),
     ("confidence-no-mean-subtraction", "var += (row[j] - mean) * (row[j] - mean);",
      "var += row[j] * row[j];"),
     ("confidence-sample-variance", "c += var / (double)n;", "c += var / (double)(n - 1);"),
