@@ -548,6 +548,32 @@ def visual_heads_timing(torch, step, n_vis=6):
                          "frac": rf["frac"], "algorithmic_bytes": a["bytes"]}}
 
 
+def critical_text_timing(torch, step):
+    """Critical text selection over the step's text rows (the anchors): the
+    call from graph replays and the kernels' average durations."""
+    pv, w = step.pv, step.w
+    s = w.spec
+    dev = step.anc.device
+    out = {"mask": torch.empty((s.B, s.Nt), dtype=torch.int32, device=dev),
+           "count": torch.empty((s.B,), dtype=torch.int32, device=dev),
+           "r": torch.empty((s.B, s.Nt), dtype=torch.float32, device=dev)}
+    code = 1 if w.dtype == "bf16" else 0
+    ws = torch.empty(pv.pv_critical_text_workspace_bytes(s.B, s.Nt, s.d, code), dtype=torch.uint8,
+                     device=dev)
+    call = lambda: pv.pv_critical_text(step.anc, out=out, workspace=ws)
+    call_us = graph_time_us(torch, call)
+    reps, per = 20, {}
+    for _ in range(5):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        for e in ev:
+            e.record()
+        r = pv.pv_critical_text(step.anc, out=out, workspace=ws, events=ev, reps=reps)
+        torch.cuda.synchronize()
+        for i, nm in enumerate(r["kernel_names"]):
+            per.setdefault(nm, []).append(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / reps)
+    return {"call_us": call_us, "kernels_us": {k: float(np.median(v)) for k, v in per.items()}}
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -697,6 +723,7 @@ def main():
     breakdown["step_two_streams" if not args.split else "step_single_stream"] = graph_time_us(
         torch, other)
     vis_heads = visual_heads_timing(torch, step)
+    crit_text = critical_text_timing(torch, step)
     step.run()
     torch.cuda.synchronize()
     # the outputs after all of the above still match the first eager step
@@ -752,8 +779,10 @@ def main():
         "roofline": rf,
         "roofline_kernels": kernels,
         "roofline_stages": stages,
-        # outside the step: visual-head identification at the same layer
+        # outside the step: visual-head identification at the same layer and
+        # critical text selection over the same text rows
         "visual_heads": vis_heads,
+        "critical_text": crit_text,
         "csrc_digest": csrc_digest(),
     }
     if args.cpu_seconds > 0:

@@ -72,6 +72,29 @@ const char *pv_status_string(int status);
 int pv_version(void);
 
 /* -------------------------------------------------------------------------
+ * Critical text tokens (Sec. 4.2, equations for r and T).
+ *
+ * Per sample b, with e_i the text embeddings text[b][i]:
+ *   r[j]  = (1/Nt) sum_i softmax_j( e_i . e_j )   (the unscaled self-similarity)
+ *   T     = { j : r[j] > mean(r) }; when no token lies strictly above the
+ *           mean (all r equal), T is every token
+ *   mask[b][j] = 1 for j in T, else 0;  count[b] = |T|
+ * The mask goes to pv_prune_dedup_masked (anchors) and
+ * pv_visual_heads_masked (rows of the confidence).
+ *
+ * text   [B][Nt][d]  dtype        text embeddings
+ * mask   [B][Nt]     int32 out    required
+ * count  [B]         int32 out    required
+ * r      [B][Nt]     float32 out  may be NULL
+ * Sizes: 1 <= Nt <= PV_MAX_TEXT, 64 <= d <= PV_MAX_DIM with d % 64 == 0.
+ * ---------------------------------------------------------------------- */
+size_t pv_critical_text_workspace_bytes(int B, int Nt, int d, int dtype);
+
+int pv_critical_text(const void *text, int B, int Nt, int d, int dtype, int32_t *mask,
+                     int32_t *count, float *r, void *workspace, size_t workspace_bytes,
+                     void *stream);
+
+/* -------------------------------------------------------------------------
  * Pruning before the LLM (Sec. 4.3).
  *
  * Per sample b (all B samples independent):
@@ -126,6 +149,22 @@ int pv_prune_dedup_split(const void *vis, const void *anchors, int B, int Nv, in
                          int dtype, int budget, int32_t *kept, float *score, int32_t *assign,
                          void *merged, void *workspace, size_t workspace_bytes, void *stream,
                          void *merge_stream, void *selected, void *merged_done);
+
+/* -------------------------------------------------------------------------
+ * pv_prune_dedup with the anchors restricted to the critical text rows: M
+ * has one row per anchor i with anchor_mask[b][i] != 0 (Sec. 4.3 builds M
+ * over the critical text tokens only), so the row means and the max-pool
+ * run over those rows.  A sample whose mask has no row set uses every row.
+ *
+ * anchor_mask [B][Nt]  int32  DEVICE memory, 4-byte aligned (e.g. the mask
+ *                             of pv_critical_text for the same rows)
+ * Everything else, the workspace and the errors are those of pv_prune_dedup
+ * (PV_ERR_NULL if anchor_mask is NULL).
+ * ---------------------------------------------------------------------- */
+int pv_prune_dedup_masked(const void *vis, const void *anchors, const int32_t *anchor_mask,
+                          int B, int Nv, int Nt, int d, int dtype, int budget, int32_t *kept,
+                          float *score, int32_t *assign, void *merged, void *workspace,
+                          size_t workspace_bytes, void *stream);
 
 /* -------------------------------------------------------------------------
  * Head-aware pruning at a pruning layer (Sec. 4.4, equations for S^vis and v).
@@ -194,6 +233,14 @@ int pv_prune_head_aware_dev(const void *q, const void *k, const int32_t *heads_d
  * (else PV_ERR_HEADS).  workspace: pv_visual_heads_workspace_bytes(B, H, Nt).
  * ---------------------------------------------------------------------- */
 size_t pv_visual_heads_workspace_bytes(int B, int H, int Nt);
+
+/* The same with the confidence summed over the rows i with
+ * row_mask[b][i] != 0 only (the critical text rows of Sec. 4.4; a sample
+ * whose mask has no row set uses every row).  row_mask: [B][Nt] int32 in
+ * DEVICE memory, 4-byte aligned; PV_ERR_NULL if NULL. */
+int pv_visual_heads_masked(const void *q, const void *k, const int32_t *row_mask, int B, int H,
+                           int Nt, int N, int hd, int dtype, int n_vis, int32_t *heads_out,
+                           float *conf, void *workspace, size_t workspace_bytes, void *stream);
 
 int pv_visual_heads(const void *q, const void *k, int B, int H, int Nt, int N, int hd, int dtype,
                     int n_vis, int32_t *heads_out, float *conf, void *workspace,
@@ -290,6 +337,24 @@ int pv_visual_heads_timed(const void *q, const void *k, int B, int H, int Nt, in
                           int dtype, int n_vis, int32_t *heads_out, float *conf, void *workspace,
                           size_t workspace_bytes, void *stream, void *const *events, int n_events,
                           int reps, int *n_kernels, const char **names);
+
+int pv_critical_text_timed(const void *text, int B, int Nt, int d, int dtype, int32_t *mask,
+                           int32_t *count, float *r, void *workspace, size_t workspace_bytes,
+                           void *stream, void *const *events, int n_events, int reps,
+                           int *n_kernels, const char **names);
+
+int pv_prune_dedup_masked_timed(const void *vis, const void *anchors, const int32_t *anchor_mask,
+                                int B, int Nv, int Nt, int d, int dtype, int budget,
+                                int32_t *kept, float *score, int32_t *assign, void *merged,
+                                void *workspace, size_t workspace_bytes, void *stream,
+                                void *const *events, int n_events, int reps, int *n_kernels,
+                                const char **names);
+
+int pv_visual_heads_masked_timed(const void *q, const void *k, const int32_t *row_mask, int B,
+                                 int H, int Nt, int N, int hd, int dtype, int n_vis,
+                                 int32_t *heads_out, float *conf, void *workspace,
+                                 size_t workspace_bytes, void *stream, void *const *events,
+                                 int n_events, int reps, int *n_kernels, const char **names);
 
 #ifdef __cplusplus
 }

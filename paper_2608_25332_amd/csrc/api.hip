@@ -169,10 +169,12 @@ struct Fork {
 int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int d, int dtype,
                int budget, int32_t *kept, float *score, int32_t *assign, void *merged,
                void *workspace, size_t ws_bytes, void *stream, void *const *events, int n_events,
-               int reps, int *n_kernels, const char **names, const Fork *fork = nullptr) {
+               int reps, int *n_kernels, const char **names, const Fork *fork = nullptr,
+               const int32_t *anchor_mask = nullptr) {
     if (reps < 1) return PV_ERR_SHAPE;
     int rc = check_dedup(vis, anchors, B, Nv, Nt, d, dtype, budget, kept);
     if (rc != PV_OK) return rc;
+    if (anchor_mask && (uintptr_t)anchor_mask % 4) return PV_ERR_ALIGN;
     const bool need_assign = assign != nullptr || merged != nullptr;
     const int esz = (dtype == PV_BF16) ? 2 : 4;
     DedupPlan P0 = plan_dedup(nullptr, B, Nv, Nt, d, esz, budget, score == nullptr,
@@ -211,7 +213,7 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
             return PV_ERR_HIP;
     }
     if (!tr.launch("center", [&] {
-            return pv::launch_center(P.M, P.rowsum, P.njt, B, Nt, Nv, p, st);
+            return pv::launch_center(P.M, P.rowsum, anchor_mask, P.njt, B, Nt, Nv, p, st);
         }))
         return PV_ERR_HIP;
     if (!tr.launch("select", [&] {
@@ -372,9 +374,10 @@ size_t vis_heads_bytes(int B, int H, int Nt) {
 int vis_heads_impl(const void *q, const void *k, int B, int H, int Nt, int N, int hd, int dtype,
                    int n_vis, int32_t *heads_out, float *conf, void *workspace, size_t ws_bytes,
                    void *stream, void *const *events, int n_events, int reps, int *n_kernels,
-                   const char **names) {
+                   const char **names, const int32_t *row_mask = nullptr) {
     if (reps < 1) return PV_ERR_SHAPE;
     if (!heads_out) return PV_ERR_NULL;
+    if (row_mask && (uintptr_t)row_mask % 4) return PV_ERR_ALIGN;
     int rc = check_qk(q, k, B, H, Nt, N, hd, dtype);
     if (rc != PV_OK) return rc;
     if (H > PV_MAX_HEADS || n_vis < 1 || n_vis > H) return PV_ERR_HEADS;
@@ -387,11 +390,68 @@ int vis_heads_impl(const void *q, const void *k, int B, int H, int Nt, int N, in
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
     if (!tr.launch("head_conf", [&] {
-            return pv::launch_head_conf(dt, q, k, B, H, Nt, N, hd, part, st);
+            return pv::launch_head_conf(dt, q, k, row_mask, B, H, Nt, N, hd, part, st);
         }))
         return PV_ERR_HIP;
     if (!tr.launch("conf_select", [&] {
             return pv::launch_conf_select(part, B, H, Nt, conf, n_vis, heads_out, st);
+        }))
+        return PV_ERR_HIP;
+    if (!tr.after_all()) return PV_ERR_HIP;
+    if (n_kernels) *n_kernels = tr.launched;
+    return PV_OK;
+}
+
+struct TextPlan {
+    int ks;
+    float *part, *ssv, *ssa, *G;
+    size_t bytes;
+};
+
+TextPlan plan_text(void *ws, int B, int Nt, int d, int esz) {
+    TextPlan P;
+    const int nch = d * esz / 128;
+    P.ks = pick_slices(n_tiles(Nt, Nt, B, pv::kSplitTile), nch);
+    Carve c(ws);
+    P.part = c.take<float>((size_t)P.ks * B * Nt * Nt);
+    P.ssv = c.take<float>((size_t)P.ks * B * Nt);
+    P.ssa = c.take<float>((size_t)P.ks * B * Nt);
+    P.G = c.take<float>((size_t)B * Nt * Nt);
+    P.bytes = c.off + kAlign;
+    return P;
+}
+
+int text_impl(const void *text, int B, int Nt, int d, int dtype, int32_t *mask, int32_t *count,
+              float *r, void *workspace, size_t ws_bytes, void *stream, void *const *events,
+              int n_events, int reps, int *n_kernels, const char **names) {
+    if (reps < 1) return PV_ERR_SHAPE;
+    if (!text || !mask || !count) return PV_ERR_NULL;
+    if (dtype != PV_F32 && dtype != PV_BF16) return PV_ERR_DTYPE;
+    if (B < 1 || B > 65535 || Nt < 1 || Nt > PV_MAX_TEXT || d < 64 || d > PV_MAX_DIM || d % 64)
+        return PV_ERR_SHAPE;
+    const int esz = dtype == PV_BF16 ? 2 : 4;
+    if (!workspace || ws_bytes < plan_text(nullptr, B, Nt, d, esz).bytes) return PV_ERR_WORKSPACE;
+    for (const void *p : {text, (const void *)mask, (const void *)count, (const void *)r,
+                          (const void *)workspace})
+        if (p && !aligned16(p)) return PV_ERR_ALIGN;
+    char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
+    TextPlan P = plan_text(wsa, B, Nt, d, esz);
+    const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
+    hipStream_t st = (hipStream_t)stream;
+    Trace tr{events, n_events, names, reps, st};
+    if (!tr.handles_ok()) return PV_ERR_NULL;
+    // E E^T: the text rows are both operands of the split-k product
+    if (!tr.launch("text_gram", [&] {
+            return pv::launch_cos_partial(dt, text, text, B, Nt, Nt, d, P.ks, P.part, P.ssv, P.ssa,
+                                          st);
+        }))
+        return PV_ERR_HIP;
+    if (!tr.launch("text_gram_sum", [&] {
+            return pv::launch_text_gram_sum(P.part, B, Nt, P.ks, P.G, st);
+        }))
+        return PV_ERR_HIP;
+    if (!tr.launch("text_rank", [&] {
+            return pv::launch_text_rank(P.G, B, Nt, r, mask, count, st);
         }))
         return PV_ERR_HIP;
     if (!tr.after_all()) return PV_ERR_HIP;
@@ -450,6 +510,48 @@ PV_API int pv_prune_dedup_split(const void *vis, const void *anchors, int B, int
     const Fork f{(hipStream_t)merge_stream, (hipEvent_t)selected, (hipEvent_t)merged_done};
     return dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, budget, kept, score, assign, merged,
                       workspace, workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr, &f);
+}
+
+PV_API int pv_prune_dedup_masked(const void *vis, const void *anchors, const int32_t *anchor_mask,
+                                 int B, int Nv, int Nt, int d, int dtype, int budget,
+                                 int32_t *kept, float *score, int32_t *assign, void *merged,
+                                 void *workspace, size_t workspace_bytes, void *stream) {
+    if (!anchor_mask) return PV_ERR_NULL;
+    return dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, budget, kept, score, assign, merged,
+                      workspace, workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr, nullptr,
+                      anchor_mask);
+}
+
+PV_API int pv_prune_dedup_masked_timed(const void *vis, const void *anchors,
+                                       const int32_t *anchor_mask, int B, int Nv, int Nt, int d,
+                                       int dtype, int budget, int32_t *kept, float *score,
+                                       int32_t *assign, void *merged, void *workspace,
+                                       size_t workspace_bytes, void *stream, void *const *events,
+                                       int n_events, int reps, int *n_kernels, const char **names) {
+    if (!anchor_mask) return PV_ERR_NULL;
+    return dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, budget, kept, score, assign, merged,
+                      workspace, workspace_bytes, stream, events, n_events, reps, n_kernels, names,
+                      nullptr, anchor_mask);
+}
+
+PV_API size_t pv_critical_text_workspace_bytes(int B, int Nt, int d, int dtype) {
+    if (B < 1 || Nt < 1 || d < 64 || (dtype != PV_F32 && dtype != PV_BF16)) return 0;
+    return plan_text(nullptr, B, Nt, d, dtype == PV_BF16 ? 2 : 4).bytes;
+}
+
+PV_API int pv_critical_text(const void *text, int B, int Nt, int d, int dtype, int32_t *mask,
+                            int32_t *count, float *r, void *workspace, size_t workspace_bytes,
+                            void *stream) {
+    return text_impl(text, B, Nt, d, dtype, mask, count, r, workspace, workspace_bytes, stream,
+                     nullptr, 0, 1, nullptr, nullptr);
+}
+
+PV_API int pv_critical_text_timed(const void *text, int B, int Nt, int d, int dtype, int32_t *mask,
+                                  int32_t *count, float *r, void *workspace,
+                                  size_t workspace_bytes, void *stream, void *const *events,
+                                  int n_events, int reps, int *n_kernels, const char **names) {
+    return text_impl(text, B, Nt, d, dtype, mask, count, r, workspace, workspace_bytes, stream,
+                     events, n_events, reps, n_kernels, names);
 }
 
 PV_API size_t pv_head_aware_workspace_bytes(int B, int H, int Nt, int N, int hd, int n_heads,
@@ -513,6 +615,27 @@ PV_API int pv_visual_heads(const void *q, const void *k, int B, int H, int Nt, i
                            size_t workspace_bytes, void *stream) {
     return vis_heads_impl(q, k, B, H, Nt, N, hd, dtype, n_vis, heads_out, conf, workspace,
                           workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr);
+}
+
+PV_API int pv_visual_heads_masked(const void *q, const void *k, const int32_t *row_mask, int B,
+                                  int H, int Nt, int N, int hd, int dtype, int n_vis,
+                                  int32_t *heads_out, float *conf, void *workspace,
+                                  size_t workspace_bytes, void *stream) {
+    if (!row_mask) return PV_ERR_NULL;
+    return vis_heads_impl(q, k, B, H, Nt, N, hd, dtype, n_vis, heads_out, conf, workspace,
+                          workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr, row_mask);
+}
+
+PV_API int pv_visual_heads_masked_timed(const void *q, const void *k, const int32_t *row_mask,
+                                        int B, int H, int Nt, int N, int hd, int dtype, int n_vis,
+                                        int32_t *heads_out, float *conf, void *workspace,
+                                        size_t workspace_bytes, void *stream, void *const *events,
+                                        int n_events, int reps, int *n_kernels,
+                                        const char **names) {
+    if (!row_mask) return PV_ERR_NULL;
+    return vis_heads_impl(q, k, B, H, Nt, N, hd, dtype, n_vis, heads_out, conf, workspace,
+                          workspace_bytes, stream, events, n_events, reps, n_kernels, names,
+                          row_mask);
 }
 
 PV_API int pv_visual_heads_timed(const void *q, const void *k, int B, int H, int Nt, int N, int hd,

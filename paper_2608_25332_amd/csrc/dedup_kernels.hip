@@ -278,11 +278,17 @@ constexpr int kCenNT = 256;
 constexpr int kCenTok = 64;
 
 __global__ __launch_bounds__(kCenNT) void center_kernel(const float *__restrict__ M,
-                                                        const float *__restrict__ rowsum, int njt,
-                                                        int Nt, int Nv, float *__restrict__ p) {
-    extern __shared__ float mu[];  // [Nt]
+                                                        const float *__restrict__ rowsum,
+                                                        const int32_t *__restrict__ row_mask,
+                                                        int njt, int Nt, int Nv,
+                                                        float *__restrict__ p) {
+    extern __shared__ float mu[];  // [Nt]: row mean, or +inf for a row that is not an anchor
     __shared__ float part[4][kCenTok];
+    __shared__ int any_row;
     const int b = blockIdx.y, tid = threadIdx.x;
+    if (tid == 0) any_row = 0;
+    __syncthreads();
+    bool masked = false;  // whether this thread set any row to +inf
     // Row means of M over all Nv tokens, from the per-tile partial sums
     // (added in tile order).
     for (int i = tid; i < Nt; i += kCenNT) {
@@ -296,7 +302,27 @@ __global__ __launch_bounds__(kCenNT) void center_kernel(const float *__restrict_
             for (int u = 0; u < 16; ++u)
                 if (t0 + u < njt) s += v[u];
         }
-        mu[i] = s / (float)Nv;
+        const bool use = !row_mask || row_mask[(size_t)b * Nt + i] != 0;
+        mu[i] = use ? s / (float)Nv : INFINITY;
+        masked |= !use;
+        if (use) any_row = 1;
+    }
+    __syncthreads();
+    // an empty mask means every row
+    if (!any_row && masked) {
+        for (int i = tid; i < Nt; i += kCenNT) {
+            const float *rs = rowsum + (size_t)b * njt * Nt + i;
+            float s = 0.f;
+            for (int t0 = 0; t0 < njt; t0 += 16) {
+                float v[16];
+#pragma unroll
+                for (int u = 0; u < 16; ++u) v[u] = rs[(size_t)min(t0 + u, njt - 1) * Nt];
+#pragma unroll
+                for (int u = 0; u < 16; ++u)
+                    if (t0 + u < njt) s += v[u];
+            }
+            mu[i] = s / (float)Nv;
+        }
     }
     __syncthreads();
     const int jl = tid & (kCenTok - 1), g = tid / kCenTok;
@@ -948,11 +974,11 @@ hipError_t launch_cos_full(int dt, const void *vis, const void *anchors, int B, 
     return hipGetLastError();
 }
 
-hipError_t launch_center(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
-                         float *p, hipStream_t st) {
+hipError_t launch_center(const float *M, const float *rowsum, const int32_t *row_mask, int njt,
+                         int B, int Nt, int Nv, float *p, hipStream_t st) {
     dim3 grid((Nv + kCenTok - 1) / kCenTok, B);
     hipLaunchKernelGGL(center_kernel, grid, dim3(kCenNT), (size_t)Nt * sizeof(float), st, M, rowsum,
-                       njt, Nt, Nv, p);
+                       row_mask, njt, Nt, Nv, p);
     return hipGetLastError();
 }
 

@@ -74,8 +74,9 @@ enum HeadSource { kHeadsArg = 0, kHeadsDevice = 1, kHeadsAll = 2 };
 template <int DT, int NKS, int MAXC, bool CONF>
 __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
-    const int32_t *__restrict__ heads_dev, int head_src, int b0, int H, int Nt, int N,
-    int n_heads, float scale_log2e, float *__restrict__ partial, int cols_in_lds) {
+    const int32_t *__restrict__ heads_dev, int head_src, const int32_t *__restrict__ row_mask,
+    int b0, int H, int Nt, int N, int n_heads, float scale_log2e, float *__restrict__ partial,
+    int cols_in_lds) {
     static_assert(!CONF || MAXC == 0, "the confidence needs no second pass");
     using S = ScoreStage<NKS>;
     __shared__ __attribute__((aligned(16))) char ring[S::NS][S::STAGE];
@@ -242,6 +243,15 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     }
     __syncthreads();
     if constexpr (CONF) {
+        // rows outside row_mask add nothing (an empty mask means every row)
+        __shared__ int any_row;
+        if (row_mask) {
+            if (tid == 0) any_row = 0;
+            __syncthreads();
+            for (int i = tid; i < Nt; i += kScoreNT)
+                if (row_mask[(size_t)b * Nt + i] != 0) any_row = 1;
+            __syncthreads();
+        }
         // Var_j(A[i][j]) = (sum_j A^2 - 1/N) / N with sum_j A^2 = s / l^2;
         // the 16 rows added in order (rows past Nt add nothing)
         if (tid < 16) {
@@ -249,7 +259,9 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
 #pragma unroll
             for (int w = 1; w < 4; ++w) lse_merge2(mm, ll, ss, sm_m[w][tid], sm_l[w][tid], sm_s[w][tid]);
             const float inv_n = 1.0f / (float)N;
-            row_m[tid] = (rb * 16 + tid < Nt) ? (ss / (ll * ll) - inv_n) * inv_n : 0.f;
+            const int i = rb * 16 + tid;
+            const bool use = i < Nt && (!row_mask || !any_row || row_mask[(size_t)b * Nt + i] != 0);
+            row_m[tid] = use ? (ss / (ll * ll) - inv_n) * inv_n : 0.f;
         }
         __syncthreads();
         if (tid == 0) {
@@ -374,6 +386,7 @@ struct ScoreLaunch {
     const int32_t *heads_host;  // kHeadsArg: host list [B][n_heads]
     const int32_t *heads_dev;   // kHeadsDevice: device list [B][n_heads]
     int src;
+    const int32_t *row_mask;    // confidence only: rows summed (may be NULL)
     int B, H, Nt, N, n_heads;
     float sl2e;
     float *partial;
@@ -402,8 +415,8 @@ static hipError_t score_go(const ScoreLaunch &a) {
         dim3 grid(nrb * a.n_heads * nb);
         hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC, CONF>), grid, dim3(kScoreNT),
                            in_lds ? cols : 0, a.st, (const char *)a.q, (const char *)a.k, ha,
-                           a.heads_dev, a.src, b0, a.H, a.Nt, a.N, a.n_heads, a.sl2e, a.partial,
-                           in_lds ? 1 : 0);
+                           a.heads_dev, a.src, a.row_mask, b0, a.H, a.Nt, a.N, a.n_heads, a.sl2e,
+                           a.partial, in_lds ? 1 : 0);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -471,14 +484,14 @@ static hipError_t score_any(int dt, int hd, ScoreLaunch a) {
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, int B, int H, int Nt, int N, int hd,
                                 int n_heads, float *partial, hipStream_t st) {
-    ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg,
+    ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg, nullptr,
                   B, H, Nt, N, n_heads, 0.f, partial, st};
     return score_any<false>(dt, hd, a);
 }
 
-hipError_t launch_head_conf(int dt, const void *q, const void *k, int B, int H, int Nt, int N,
-                            int hd, float *partial, hipStream_t st) {
-    ScoreLaunch a{q, k, nullptr, nullptr, kHeadsAll, B, H, Nt, N, H, 0.f, partial, st};
+hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask, int B,
+                            int H, int Nt, int N, int hd, float *partial, hipStream_t st) {
+    ScoreLaunch a{q, k, nullptr, nullptr, kHeadsAll, row_mask, B, H, Nt, N, H, 0.f, partial, st};
     return score_any<true>(dt, hd, a);
 }
 

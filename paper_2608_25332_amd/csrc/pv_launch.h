@@ -32,8 +32,10 @@ hipError_t launch_cos_partial(int dt, const void *vis, const void *anchors, int 
                               int d, int KS, float *part, float *ssv, float *ssa, hipStream_t st);
 hipError_t launch_cos_reduce(const float *part, const float *ssv, const float *ssa, int B, int Nv,
                              int Nt, int KS, float *M, float *rowsum, float *invn, hipStream_t st);
-hipError_t launch_center(const float *M, const float *rowsum, int njt, int B, int Nt, int Nv,
-                         float *p, hipStream_t st);
+// row_mask [B][Nt] (device, may be NULL): rows with 0 are not anchors; a
+// sample whose mask has no row set uses every row.
+hipError_t launch_center(const float *M, const float *rowsum, const int32_t *row_mask, int njt,
+                         int B, int Nt, int Nv, float *p, hipStream_t st);
 hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kept, int32_t *pruned,
                          int32_t *slot_of, hipStream_t st);
 hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
@@ -66,6 +68,12 @@ inline bool merge_uses_lists(int B, int N1, int d_bytes) {
 hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
                         const int32_t *assign, void *merged, hipStream_t st);
 
+// ---- critical text tokens (Sec. 4.2)
+hipError_t launch_text_gram_sum(const float *part, int B, int Nt, int KS, float *G,
+                                hipStream_t st);
+hipError_t launch_text_rank(const float *G, int B, int Nt, float *r, int32_t *mask, int32_t *count,
+                            hipStream_t st);
+
 // ---- head-aware pruning (Sec. 4.4)
 // heads_dev == nullptr: the head list is heads_host (host memory); else the
 // device list heads_dev (entries clamped into [0, H)).
@@ -73,8 +81,9 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const int3
                                 const int32_t *heads_dev, int B, int H, int Nt, int N, int hd,
                                 int n_heads, float *partial, hipStream_t st);
 // Head confidence of every head, per 16-row block: partial[b][h][rb].
-hipError_t launch_head_conf(int dt, const void *q, const void *k, int B, int H, int Nt, int N,
-                            int hd, float *partial, hipStream_t st);
+// row_mask as for launch_center: the rows summed into the confidence.
+hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask, int B,
+                            int H, int Nt, int N, int hd, float *partial, hipStream_t st);
 hipError_t launch_conf_select(const float *partial, int B, int H, int Nt, float *conf, int n_vis,
                               int32_t *heads, hipStream_t st);
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,

@@ -83,6 +83,19 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_head_aware_timed.argtypes = ha + [ctypes.POINTER(_vp), _i, _i,
                                                    ctypes.POINTER(_i), names_t]
     lib.pv_prune_head_aware_timed.restype = _i
+    timed_tail = [ctypes.POINTER(_vp), _i, _i, ctypes.POINTER(_i), names_t]
+    dm = [_vp, _vp, _vp] + ded[2:]
+    lib.pv_prune_dedup_masked.argtypes = dm
+    lib.pv_prune_dedup_masked.restype = _i
+    lib.pv_prune_dedup_masked_timed.argtypes = dm + timed_tail
+    lib.pv_prune_dedup_masked_timed.restype = _i
+    lib.pv_critical_text_workspace_bytes.argtypes = [_i, _i, _i, _i]
+    lib.pv_critical_text_workspace_bytes.restype = _sz
+    ct = [_vp, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.pv_critical_text.argtypes = ct
+    lib.pv_critical_text.restype = _i
+    lib.pv_critical_text_timed.argtypes = ct + timed_tail
+    lib.pv_critical_text_timed.restype = _i
     had = [_vp, _vp, _vp] + ha[3:]
     lib.pv_prune_head_aware_dev.argtypes = had
     lib.pv_prune_head_aware_dev.restype = _i
@@ -97,6 +110,11 @@ def load(path: str = LIB_PATH):
     lib.pv_visual_heads_timed.argtypes = vh + [ctypes.POINTER(_vp), _i, _i, ctypes.POINTER(_i),
                                                names_t]
     lib.pv_visual_heads_timed.restype = _i
+    vhm = [_vp, _vp, _vp] + vh[2:]
+    lib.pv_visual_heads_masked.argtypes = vhm
+    lib.pv_visual_heads_masked.restype = _i
+    lib.pv_visual_heads_masked_timed.argtypes = vhm + timed_tail
+    lib.pv_visual_heads_masked_timed.restype = _i
     lib.pv_prune_gather.argtypes = [_vp, _vp, _vp, _i, _i, _i, _i, _i64, _i64, _i64, _i64, _i64,
                                     _i64, _i64, _vp]
     lib.pv_prune_gather.restype = _i
@@ -159,11 +177,14 @@ def pv_dedup_workspace_bytes(B: int, Nv: int, Nt: int, d: int, budget: int, dtyp
 def pv_prune_dedup(vis: torch.Tensor, anchors: torch.Tensor, budget: int, *,
                    want_score: bool = True, want_assign: bool = True, want_merged: bool = True,
                    out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None,
-                   events: Optional[Sequence] = None, reps: int = 1, split=None):
+                   events: Optional[Sequence] = None, reps: int = 1, split=None,
+                   anchor_mask: Optional[torch.Tensor] = None):
     """Pruning before the LLM.  vis [B, Nv, d], anchors [B, Nt, d] (same dtype).
     Returns dict(kept [B,budget] int32, score [B,Nv] f32 | None,
     assign [B,Nv] int32 | None, merged [B,budget,d] | None, n_kernels).
     events / reps: see pv_prune_dedup_timed (profiling only).
+    anchor_mask: int32 [B, Nt] on the device (e.g. pv_critical_text's mask):
+    only the rows set are anchors (pv_prune_dedup_masked).
     split = (merge_stream, selected, merged_done) (a torch stream and two torch
     events, already recorded once so that their HIP events exist): runs
     pv_prune_dedup_split; assign and merged are ready after merged_done."""
@@ -195,6 +216,8 @@ def pv_prune_dedup(vis: torch.Tensor, anchors: torch.Tensor, budget: int, *,
     if split is not None:
         if events:
             raise ValueError("events and split cannot be combined")
+        if anchor_mask is not None:
+            raise ValueError("anchor_mask and split cannot be combined")
         merge_stream, selected, merged_done = split
         rc = lib.pv_prune_dedup_split(vis.data_ptr(), anchors.data_ptr(), B, Nv, Nt, d, code,
                                       int(budget), kept.data_ptr(), _ptr(score), _ptr(assign),
@@ -206,10 +229,21 @@ def pv_prune_dedup(vis: torch.Tensor, anchors: torch.Tensor, budget: int, *,
                 "n_kernels": None, "kernel_names": [], "workspace": workspace}
     ev, nev, nm = _events_array(events)
     nk = _i(0)
-    rc = lib.pv_prune_dedup_timed(vis.data_ptr(), anchors.data_ptr(), B, Nv, Nt, d, code,
-                                  int(budget), kept.data_ptr(), _ptr(score), _ptr(assign),
-                                  _ptr(merged), workspace.data_ptr(), workspace.numel(),
-                                  _stream(dev), ev, nev, int(reps), ctypes.byref(nk), nm)
+    if anchor_mask is not None:
+        if split is not None:
+            raise ValueError("anchor_mask and split cannot be combined")
+        _check_mask(anchor_mask, B, Nt, dev, "anchor_mask")
+        rc = lib.pv_prune_dedup_masked_timed(vis.data_ptr(), anchors.data_ptr(),
+                                             anchor_mask.data_ptr(), B, Nv, Nt, d, code,
+                                             int(budget), kept.data_ptr(), _ptr(score),
+                                             _ptr(assign), _ptr(merged), workspace.data_ptr(),
+                                             workspace.numel(), _stream(dev), ev, nev, int(reps),
+                                             ctypes.byref(nk), nm)
+    else:
+        rc = lib.pv_prune_dedup_timed(vis.data_ptr(), anchors.data_ptr(), B, Nv, Nt, d, code,
+                                      int(budget), kept.data_ptr(), _ptr(score), _ptr(assign),
+                                      _ptr(merged), workspace.data_ptr(), workspace.numel(),
+                                      _stream(dev), ev, nev, int(reps), ctypes.byref(nk), nm)
     _check("pv_prune_dedup", rc, lib)
     return {"kept": kept, "score": score, "assign": assign, "merged": merged,
             "n_kernels": nk.value, "kernel_names": _names(nm, min(nk.value, max(nev - 1, 0))),
@@ -219,6 +253,50 @@ def pv_prune_dedup(vis: torch.Tensor, anchors: torch.Tensor, budget: int, *,
 def pv_head_aware_workspace_bytes(B: int, H: int, Nt: int, N: int, hd: int, n_heads: int,
                                   budget: int, dtype: int) -> int:
     return int(load().pv_head_aware_workspace_bytes(B, H, Nt, N, hd, n_heads, budget, dtype))
+
+
+def _check_mask(m: torch.Tensor, B: int, Nt: int, dev, name: str):
+    if (m.dtype != torch.int32 or tuple(m.shape) != (B, Nt) or m.device != dev
+            or not m.is_contiguous()):
+        raise ValueError(f"{name} must be a contiguous int32 [B, Nt] tensor on {dev}")
+
+
+def pv_critical_text_workspace_bytes(B: int, Nt: int, d: int, dtype: int) -> int:
+    return int(load().pv_critical_text_workspace_bytes(B, Nt, d, dtype))
+
+
+def pv_critical_text(text: torch.Tensor, *, want_r: bool = True, out: Optional[dict] = None,
+                     workspace: Optional[torch.Tensor] = None,
+                     events: Optional[Sequence] = None, reps: int = 1):
+    """Critical text tokens.  text [B, Nt, d].  Returns dict(mask [B,Nt]
+    int32 (1 = critical), count [B] int32, r [B,Nt] f32 | None)."""
+    lib = load()
+    _contig(text, "text")
+    B, Nt, d = text.shape
+    code = _dtype_code(text)
+    dev = text.device
+    o = out if out is not None else {}
+    mask = o.get("mask")
+    if mask is None:
+        mask = torch.empty((B, Nt), dtype=torch.int32, device=dev)
+    count = o.get("count")
+    if count is None:
+        count = torch.empty((B,), dtype=torch.int32, device=dev)
+    r = o.get("r") if want_r else None
+    if want_r and r is None:
+        r = torch.empty((B, Nt), dtype=torch.float32, device=dev)
+    nbytes = lib.pv_critical_text_workspace_bytes(B, Nt, d, code)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    ev, nev, nm = _events_array(events)
+    nk = _i(0)
+    rc = lib.pv_critical_text_timed(text.data_ptr(), B, Nt, d, code, mask.data_ptr(),
+                                    count.data_ptr(), _ptr(r), workspace.data_ptr(),
+                                    workspace.numel(), _stream(dev), ev, nev, int(reps),
+                                    ctypes.byref(nk), nm)
+    _check("pv_critical_text", rc, lib)
+    return {"mask": mask, "count": count, "r": r, "n_kernels": nk.value,
+            "kernel_names": _names(nm, min(nk.value, max(nev - 1, 0))), "workspace": workspace}
 
 
 def pv_visual_heads_workspace_bytes(B: int, H: int, Nt: int) -> int:
@@ -286,10 +364,13 @@ def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
 
 def pv_visual_heads(q: torch.Tensor, k: torch.Tensor, n_vis: int, *, want_conf: bool = True,
                     out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None,
-                    events: Optional[Sequence] = None, reps: int = 1):
+                    events: Optional[Sequence] = None, reps: int = 1,
+                    row_mask: Optional[torch.Tensor] = None):
     """Visual-head identification.  q [B,H,Nt,hd], k [B,H,N,hd].  Returns
     dict(heads [B,n_vis] int32 on the device, ascending; conf [B,H] f32 |
-    None, n_kernels).  The head list can go straight to pv_prune_head_aware."""
+    None, n_kernels).  The head list can go straight to pv_prune_head_aware.
+    row_mask: int32 [B, Nt] on the device: the confidence sums over the rows
+    set only (pv_visual_heads_masked)."""
     lib = load()
     _contig(q, "q")
     _contig(k, "k")
@@ -310,10 +391,18 @@ def pv_visual_heads(q: torch.Tensor, k: torch.Tensor, n_vis: int, *, want_conf: 
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     ev, nev, nm = _events_array(events)
     nk = _i(0)
-    rc = lib.pv_visual_heads_timed(q.data_ptr(), k.data_ptr(), B, H, Nt, N, hd, _dtype_code(q),
-                                   int(n_vis), heads.data_ptr(), _ptr(conf), workspace.data_ptr(),
-                                   workspace.numel(), _stream(dev), ev, nev, int(reps),
-                                   ctypes.byref(nk), nm)
+    if row_mask is not None:
+        _check_mask(row_mask, B, Nt, dev, "row_mask")
+        rc = lib.pv_visual_heads_masked_timed(q.data_ptr(), k.data_ptr(), row_mask.data_ptr(), B,
+                                              H, Nt, N, hd, _dtype_code(q), int(n_vis),
+                                              heads.data_ptr(), _ptr(conf), workspace.data_ptr(),
+                                              workspace.numel(), _stream(dev), ev, nev, int(reps),
+                                              ctypes.byref(nk), nm)
+    else:
+        rc = lib.pv_visual_heads_timed(q.data_ptr(), k.data_ptr(), B, H, Nt, N, hd,
+                                       _dtype_code(q), int(n_vis), heads.data_ptr(), _ptr(conf),
+                                       workspace.data_ptr(), workspace.numel(), _stream(dev), ev,
+                                       nev, int(reps), ctypes.byref(nk), nm)
     _check("pv_visual_heads", rc, lib)
     return {"heads": heads, "conf": conf, "n_kernels": nk.value,
             "kernel_names": _names(nm, min(nk.value, max(nev - 1, 0))), "workspace": workspace}

@@ -151,6 +151,43 @@ def test_visual_heads_validation(lib):
     assert call(out=FAKE + 4) == -8
 
 
+def test_critical_text_validation(lib):
+    f = lib.pv_critical_text
+    assert lib.pv_critical_text_workspace_bytes(1, 64, 4096, 1) > 0
+    assert lib.pv_critical_text_workspace_bytes(1, 64, 4096, 9) == 0
+
+    def call(text=FAKE, Nt=64, d=4096, dt=1, mask=FAKE, count=FAKE, ws=FAKE, wsb=1 << 40):
+        return f(text, 1, Nt, d, dt, mask, count, None, ws, wsb, None)
+    assert call(text=None) == -1
+    assert call(mask=None) == -1
+    assert call(count=None) == -1
+    assert call(Nt=0) == -2
+    assert call(Nt=1025) == -2
+    assert call(d=100) == -2
+    assert call(dt=2) == -5
+    assert call(ws=None) == -6
+    assert call(wsb=16) == -6
+    assert call(mask=FAKE + 4) == -8
+
+
+def test_masked_variants_validation(lib):
+    d = lib.pv_prune_dedup_masked(FAKE, FAKE, None, 1, 576, 64, 4096, 1, 192, FAKE, None, None,
+                                  None, FAKE, 1 << 40, None)
+    assert d == -1
+    d = lib.pv_prune_dedup_masked(FAKE, FAKE, FAKE + 2, 1, 576, 64, 4096, 1, 192, FAKE, None,
+                                  None, None, FAKE, 1 << 40, None)
+    assert d == -8
+    d = lib.pv_prune_dedup_masked(FAKE, FAKE, FAKE, 1, 576, 64, 4096, 1, 577, FAKE, None, None,
+                                  None, FAKE, 1 << 40, None)
+    assert d == -3
+    v = lib.pv_visual_heads_masked(FAKE, FAKE, None, 1, 32, 64, 192, 128, 1, 6, FAKE, None, FAKE,
+                                   1 << 40, None)
+    assert v == -1
+    v = lib.pv_visual_heads_masked(FAKE, FAKE, FAKE + 1, 1, 32, 64, 192, 128, 1, 6, FAKE, None,
+                                   FAKE, 1 << 40, None)
+    assert v == -8
+
+
 def test_gather_validation(lib):
     g = lib.pv_prune_gather
     args = dict(src=FAKE, dst=FAKE, idx=FAKE, B=1, n=8, k=4, G=1, rb=256)
