@@ -1,13 +1,13 @@
 // "Row x row" tile product on the matrix cores with operands streamed straight
 // into LDS (gfx950 global_load_lds_dwordx4).
 //
-// Same contract as TileGemm: C[m][n] = dot(A_row(m), B_row(n)) over a range
-// of 128-byte k chunks, rows addressed through a per-row pointer.  The
-// difference is the load path.  A direct-to-LDS load writes the 16 bytes of
-// lane i to LDS byte 16 * i of the instruction's 1 KB block without passing
-// through registers; on this chip one CU then sustains several times the
-// bytes per second that register loads reach, and the loads of the next
-// NSTAGE - 1 chunks stay in flight while the current one is multiplied.
+// C[m][n] = dot(A_row(m), B_row(n)) over a range of 128-byte k chunks, rows
+// addressed through a per-row pointer (gathered row lists cost nothing
+// extra).  A direct-to-LDS load writes the 16 bytes of lane i to LDS byte
+// 16 * i of the instruction's 1 KB block without passing through registers;
+// on this chip one CU then sustains several times the bytes per second that
+// register loads reach, and the loads of the next NSTAGE - 1 chunks stay in
+// flight while the current one is multiplied.
 //
 // LDS layout of one stage: row r's 128-byte chunk occupies bytes
 // [128 r, 128 r + 128), its eight 16-byte pieces stored at slot
