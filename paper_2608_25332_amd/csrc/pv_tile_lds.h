@@ -64,6 +64,13 @@ __device__ __forceinline__ uint4 lds_read16(const char *p) {
     return uint4{r.x, r.y, r.z, r.w};
 }
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+// Wait until at most N LDS reads of this wave are outstanding (they complete
+// in issue order; N <= 15).
+template <int N>
+__device__ __forceinline__ void lds_wait_n() {
+    static_assert(N >= 0 && N <= 15, "lgkmcnt is a 4-bit count");
+    asm volatile("s_waitcnt lgkmcnt(%0)" ::"n"(N) : "memory");
+}
 // Ties a fragment to the preceding lds_wait(): volatile asm statements keep
 // their order, so no use of the value can be scheduled before the wait.
 __device__ __forceinline__ void lds_after_wait(uint4 &v) {
@@ -143,39 +150,47 @@ struct TileGemmLds {
             bare_barrier();  // all of chunk i is in LDS; chunk i - 1 has been read
             if (i + NSTAGE - 1 < nc) issue(i + NSTAGE - 1);
             const char *sp = ring[i % NSTAGE];
+            // both 64-byte windows of the chunk are read up front: the
+            // second window's reads are in flight while the first window's
+            // MFMAs run
+            uint4 af[2][FM], bfr[2][FN];
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
                 const int piece = s * 4 + kq;
-                uint4 af[FM], bfr[FN];
 #pragma unroll
                 for (int f = 0; f < FM; ++f) {
                     const int r = a_row + f * 16;
-                    af[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
+                    af[s][f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
                 }
 #pragma unroll
                 for (int f = 0; f < FN; ++f) {
                     const int r = b_row + f * 16;
-                    bfr[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
+                    bfr[s][f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
                 }
-                lds_wait();
+            }
 #pragma unroll
-                for (int f = 0; f < FM; ++f) lds_after_wait(af[f]);
+            for (int s = 0; s < 2; ++s) {
+                if (s == 0) lds_wait_n<(FM + FN <= 15 ? FM + FN : 0)>();
+                else lds_wait();
 #pragma unroll
-                for (int f = 0; f < FN; ++f) lds_after_wait(bfr[f]);
+                for (int f = 0; f < FM; ++f) lds_after_wait(af[s][f]);
+#pragma unroll
+                for (int f = 0; f < FN; ++f) lds_after_wait(bfr[s][f]);
                 if (WANT_SS) {
                     if (wn == 0) {
 #pragma unroll
-                        for (int f = 0; f < FM; ++f) ssa[f] += sumsq16<DT>(af[f]);
+                        for (int f = 0; f < FM; ++f) ssa[f] += sumsq16<DT>(af[s][f]);
                     }
                     if (wm == 0) {
 #pragma unroll
-                        for (int f = 0; f < FN; ++f) ssb[f] += sumsq16<DT>(bfr[f]);
+                        for (int f = 0; f < FN; ++f) ssb[f] += sumsq16<DT>(bfr[s][f]);
                     }
                 }
 #pragma unroll
                 for (int f = 0; f < FM; ++f)
 #pragma unroll
-                    for (int g = 0; g < FN; ++g) acc[f][g] = mma16<DT>(af[f], bfr[g], acc[f][g]);
+                    for (int g = 0; g < FN; ++g)
+                        acc[f][g] = mma16<DT>(af[s][f], bfr[s][g], acc[f][g]);
             }
         }
         bare_barrier();  // the stages may be reused by a later call
