@@ -13,6 +13,8 @@ Function map (paper passages are cited at each C function):
   topk                       -- retention of the N_1 / N_2 highest scores
   assign / merge             -- Sec. 4.3, nearest-centroid aggregation
   attention / head_aware     -- Sec. 4.4, equations for S^vis and v
+  attention_in_model /
+  head_aware_in_model        -- Sec. 4.4 on the visual slice of the model's softmax
   head_confidence /
   visual_heads               -- Sec. 4.4, equations for C^h and V_l
   gather                     -- compaction of kept rows (Sec. 4.1)
@@ -90,6 +92,10 @@ def _declare(lib):
     lib.orc_head_aware.restype = _int
     lib.orc_critical_text.argtypes = [_D, _int, _int, _D, _I]
     lib.orc_critical_text.restype = _int
+    lib.orc_attention_in_model.argtypes = [_D, _D, _D, _int, _int, _int, _D]
+    lib.orc_attention_in_model.restype = None
+    lib.orc_head_aware_score_in_model.argtypes = [_D, _D, _D, _int, _int, _int, _int, _I, _int, _D]
+    lib.orc_head_aware_score_in_model.restype = _int
     lib.orc_head_confidence.argtypes = [_D, _D, _int, _int, _int, _int, _D]
     lib.orc_head_confidence.restype = _int
     lib.orc_visual_heads.argtypes = [_D, _D, _int, _int, _int, _int, _int, _I, _D]
@@ -273,6 +279,39 @@ def head_aware(q, k, heads, n2: int, *, lib=None):
                                 int(n2), _pi(kept[b]), _pd(v[b]))
         if rc != 0:
             raise OracleError(f"orc_head_aware rc={rc}")
+    return kept, v
+
+
+def attention_in_model(q, k, lse, *, lib=None) -> np.ndarray:
+    """One head, the visual slice of the model's softmax: q [nt, hd], k [n,
+    hd], lse [nt] (log-sum-exp of the other keys' scaled logits) -> [nt, n]."""
+    lib = lib or load()
+    q, k, lse = _f64(q), _f64(k), _f64(lse)
+    nt, hd = q.shape
+    n = k.shape[0]
+    A = np.empty((nt, n), np.float64)
+    lib.orc_attention_in_model(_pd(q), _pd(k), _pd(lse), nt, n, hd, _pd(A))
+    return A
+
+
+def head_aware_in_model(q, k, heads, lse, n2: int, *, lib=None):
+    """Sec. 4.4 on the in-model map over a batch: q [B,H,nt,hd], k
+    [B,H,n,hd], heads [B,nh], lse [B,H,nt] -> (kept [B,n2], v [B,n])."""
+    lib = lib or load()
+    Q, K, L = _f64(q), _f64(k), _f64(lse)
+    hs = _i32(heads)
+    B, H, nt, hd = Q.shape
+    n = K.shape[2]
+    v = np.empty((B, n), np.float64)
+    kept = np.empty((B, n2), np.int32)
+    for b in range(B):
+        rc = lib.orc_head_aware_score_in_model(_pd(Q[b]), _pd(K[b]), _pd(L[b]), H, nt, n, hd,
+                                               _pi(hs[b]), hs.shape[1], _pd(v[b]))
+        if rc != 0:
+            raise OracleError(f"orc_head_aware_score_in_model rc={rc}")
+        rc = lib.orc_topk(_pd(v[b]), n, int(n2), _pi(kept[b]))
+        if rc != 0:
+            raise OracleError(f"orc_topk rc={rc}")
     return kept, v
 
 

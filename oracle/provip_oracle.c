@@ -358,6 +358,77 @@ int orc_head_aware(const double *q, const double *k, int H, int nt, int n, int h
 }
 
 /* --------------------------------------------------------------------------
+ * Sec. 4.4 with the cross-modal map taken as the model has it: in the
+ * backbone, a text row's softmax runs over every key before it (system,
+ * visual and earlier text tokens), so A^cross is the visual slice of that
+ * row and does not sum to 1.  The non-visual keys enter only through the
+ * log-sum-exp of their scaled logits, one number per row:
+ *     A[i][j] = exp(s_ij) / (sum_j' exp(s_ij') + exp(lse[i])),
+ * with s_ij = q_i . k_j / sqrt(hd).  lse[i] = -inf (no other keys) gives
+ * orc_attention.  The largest of the row's logits and lse[i] is
+ * subtracted before exponentiation (exact in real arithmetic).
+ * q: [nt][hd], k: [n][hd], lse: [nt], A: [nt][n].
+ * ------------------------------------------------------------------------ */
+void orc_attention_in_model(const double *q, const double *k, const double *lse, int nt, int n,
+                            int hd, double *A)
+{
+    double scale = 1.0 / sqrt((double)hd);
+    for (int i = 0; i < nt; ++i) {
+        double *row = A + (size_t)i * n;
+        for (int j = 0; j < n; ++j) {
+            double s = 0.0;
+            for (int c = 0; c < hd; ++c) s += q[(size_t)i * hd + c] * k[(size_t)j * hd + c];
+            row[j] = s * scale;
+        }
+        double m = lse[i];
+        for (int j = 0; j < n; ++j)
+            if (row[j] > m) m = row[j];
+        double z = exp(lse[i] - m);
+        for (int j = 0; j < n; ++j) {
+            row[j] = exp(row[j] - m);
+            z += row[j];
+        }
+        for (int j = 0; j < n; ++j) row[j] /= z;
+    }
+}
+
+/* --------------------------------------------------------------------------
+ * Sec. 4.4, equations for S^vis and v on the in-model map above, for one
+ * sample.  lse: [H][nt].  Returns 0, or -1 on a bad head id.
+ * ------------------------------------------------------------------------ */
+int orc_head_aware_score_in_model(const double *q, const double *k, const double *lse, int H,
+                                  int nt, int n, int hd, const int32_t *heads, int nh, double *v)
+{
+    double *A = (double *)malloc(sizeof(double) * (size_t)nt * n);
+    double *S = (double *)calloc((size_t)nt * n, sizeof(double));
+    int rc = 0;
+    if (!A || !S) {
+        rc = -3;
+        goto done;
+    }
+    for (int t = 0; t < nh; ++t) {
+        int h = heads[t];
+        if (h < 0 || h >= H) {
+            rc = -1;
+            goto done;
+        }
+        orc_attention_in_model(q + (size_t)h * nt * hd, k + (size_t)h * n * hd,
+                               lse + (size_t)h * nt, nt, n, hd, A);
+        for (size_t e = 0; e < (size_t)nt * n; ++e) S[e] += A[e];
+    }
+    for (size_t e = 0; e < (size_t)nt * n; ++e) S[e] /= (double)nh;
+    for (int j = 0; j < n; ++j) {
+        double s = 0.0;
+        for (int i = 0; i < nt; ++i) s += S[(size_t)i * n + j];
+        v[j] = s / (double)nt;
+    }
+done:
+    free(A);
+    free(S);
+    return rc;
+}
+
+/* --------------------------------------------------------------------------
  * Sec. 4.4, equation for C^h: the confidence of head h is the variance of
  * its cross-modal attention scores over the visual keys, taken for each
  * critical text row and summed over those rows,

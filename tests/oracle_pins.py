@@ -389,6 +389,82 @@ def pin_head_aware_topk(lib):
         assert np.array_equal(kept[b], np.sort(np.argsort(-v[b], kind="stable")[:5]))
 
 
+# ----------------------------------------- in-model softmax domain --------
+
+def pin_in_model_is_the_visual_slice(lib):
+    """The in-model map is the visual slice of one softmax over explicit
+    non-visual keys and the visual keys (torch, float64): the non-visual keys
+    enter only through the log-sum-exp of their scaled logits."""
+    import torch
+    rng = np.random.default_rng(36)
+    nt, n, n_other, hd = 6, 11, 7, 16
+    q = rng.standard_normal((nt, hd)) * 2
+    k = rng.standard_normal((n, hd)) * 2
+    k_other = rng.standard_normal((n_other, hd)) * 2
+    Q, K, Ko = (torch.from_numpy(x) for x in (q, k, k_other))
+    full = torch.softmax(torch.cat([Q @ Ko.T, Q @ K.T], dim=1) / math.sqrt(hd), dim=-1)
+    want = full[:, n_other:].numpy()
+    lse = torch.logsumexp(Q @ Ko.T / math.sqrt(hd), dim=1).numpy()
+    A = O.attention_in_model(q, k, lse, lib=lib)
+    assert np.max(np.abs(A - want)) < 1e-15
+    # every row's visual mass is below 1 by the other keys' share
+    assert np.all(A.sum(1) < 1.0)
+    assert np.max(np.abs(A.sum(1) - want.sum(1))) < 1e-15
+
+
+def pin_in_model_closed_forms(lib):
+    """lse = -inf is the plain map; one visual key with scaled logit s and
+    lse = t gives the logistic s(s - t); adding c to every logit and to lse
+    leaves A unchanged."""
+    rng = np.random.default_rng(37)
+    q = rng.standard_normal((4, 8)) * 2
+    k = rng.standard_normal((9, 8)) * 2
+    A0 = O.attention_in_model(q, k, np.full(4, -np.inf), lib=lib)
+    assert np.array_equal(A0, O.attention(q, k, lib=lib))
+    hd = 4
+    ts = np.array([-1.5, 0.0, 2.25])
+    qq = np.zeros((3, hd))
+    qq[:, 0] = math.sqrt(hd)            # scaled logit of the key = 0.7
+    kk = np.zeros((1, hd))
+    kk[0, 0] = 0.7
+    A1 = O.attention_in_model(qq, kk, ts, lib=lib)
+    want = 1.0 / (1.0 + np.exp(-(0.7 - ts)))
+    assert np.max(np.abs(A1[:, 0] - want)) < 1e-15
+    lse = rng.standard_normal(4)
+    w = rng.standard_normal(8)
+    A2 = O.attention_in_model(q, k, lse, lib=lib)
+    # a key shift by w adds q.w / sqrt(hd) to every visual logit of a row
+    shift = q @ w / math.sqrt(8)
+    A3 = O.attention_in_model(q, k + w[None, :], lse + shift, lib=lib)
+    assert np.max(np.abs(A3 - A2)) < 1e-13
+
+
+def pin_head_aware_in_model(lib):
+    """v on the in-model map: heads outside the list are never read, and the
+    plain head-aware score is the case lse = -inf."""
+    rng = np.random.default_rng(38)
+    B, H, nt, n, hd = 2, 4, 5, 12, 8
+    q = rng.standard_normal((B, H, nt, hd))
+    k = rng.standard_normal((B, H, n, hd))
+    heads = np.array([[0, 2], [3, 1]], np.int32)
+    lse = rng.standard_normal((B, H, nt)) + 1.0
+    kept, v = O.head_aware_in_model(q, k, heads, lse, 4, lib=lib)
+    k2 = k.copy()
+    k2[0, 1] = 0.0
+    k2[1, 0] = 5.0
+    lse2 = lse.copy()
+    lse2[0, 3] = 9.0
+    kept2, v2 = O.head_aware_in_model(q, k2, heads, lse2, 4, lib=lib)
+    assert np.array_equal(v, v2) and np.array_equal(kept, kept2)
+    for b in range(B):
+        A = [O.attention_in_model(q[b, h], k[b, h], lse[b, h], lib=lib) for h in heads[b]]
+        want = np.mean([a.mean(0) for a in A], axis=0)
+        assert np.max(np.abs(v[b] - want)) < 1e-15
+    _, vp = O.head_aware_in_model(q, k, heads, np.full((B, H, nt), -np.inf), 4, lib=lib)
+    _, vplain = O.head_aware(q, k, heads, 4, lib=lib)
+    assert np.array_equal(vp, vplain)
+
+
 # ------------------------------------------------------- Eq. C^h, V_l ------
 
 def pin_confidence_closed_forms(lib):

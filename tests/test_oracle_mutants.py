@@ -45,6 +45,9 @@ MUTANTS = [
     ("headaware-row-sum-not-col", "for (int i = 0; i < nt; ++i) s += S[(size_t)i * n + j];",
      "for (int i = 0; i < nt; ++i) s += S[(size_t)(j % nt) * n + (i % n)];"),
     ("gather-src-stride", "src + b * sb + g * sg + j * sr", "src + b * sb + j * sr"),
+    ("in-model-lse-dropped", "double z = exp(lse[i] - m);", "double z = 0.0;"),
+    ("in-model-lse-unshifted", "double z = exp(lse[i] - m);", "double z = exp(lse[i]);"),
+    ("in-model-lse-scaled-again", "double z = exp(lse[i] - m);", "double z = exp(lse[i] * scale - m);"),
     ("text-scaled-logits", "row[j] = s;\n        }\n        double m = row[0];\n        for (int j = 1; j < nt; ++j)",
      "row[j] = s / sqrt((double)d);\n        }\n        double m = row[0];\n        for (int j = 1; j < nt; ++j)"),
     ("text-row-mean-not-column", "for (int i = 0; i < nt; ++i) s += S[(size_t)i * nt + j];",
