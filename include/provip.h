@@ -213,6 +213,28 @@ int pv_prune_head_aware_dev(const void *q, const void *k, const int32_t *heads_d
                             void *stream);
 
 /* -------------------------------------------------------------------------
+ * Head-aware pruning on the cross-modal map as the model has it (Sec. 4.4:
+ * A^cross is the visual slice of the backbone's attention, whose softmax also
+ * runs over the system and text keys before each text row).  The other keys
+ * enter through one number per row:
+ *   row_lse[b][h][i] = log sum_{other keys j} exp( q . k_j / sqrt(hd) )
+ *   A_h[i][j]        = exp(s_ij) / ( sum_{visual j'} exp(s_ij') + exp(row_lse) )
+ * so a row's visual mass is below 1; v, the selection and everything else
+ * are those of pv_prune_head_aware.  row_lse = NULL, or -INFINITY entries,
+ * give the plain call's results.
+ *
+ * heads_host / heads_dev  exactly one non-NULL: the host list of
+ *            pv_prune_head_aware or the device list of
+ *            pv_prune_head_aware_dev (PV_ERR_HEADS if both are given)
+ * row_lse    [B][H][Nt]  float32  DEVICE memory, 4-byte aligned, finite or
+ *            -INFINITY, natural-log units; may be NULL
+ * ---------------------------------------------------------------------- */
+int pv_prune_head_aware_ex(const void *q, const void *k, const int32_t *heads_host,
+                           const int32_t *heads_dev, int n_heads, int B, int H, int Nt, int N,
+                           int hd, int dtype, int budget, const float *row_lse, int32_t *kept,
+                           float *score, void *workspace, size_t workspace_bytes, void *stream);
+
+/* -------------------------------------------------------------------------
  * Visual-head identification at a shallow pruning layer (Sec. 4.4,
  * equations for C^h and V_l).
  *
@@ -337,6 +359,13 @@ int pv_visual_heads_timed(const void *q, const void *k, int B, int H, int Nt, in
                           int dtype, int n_vis, int32_t *heads_out, float *conf, void *workspace,
                           size_t workspace_bytes, void *stream, void *const *events, int n_events,
                           int reps, int *n_kernels, const char **names);
+
+int pv_prune_head_aware_ex_timed(const void *q, const void *k, const int32_t *heads_host,
+                                 const int32_t *heads_dev, int n_heads, int B, int H, int Nt,
+                                 int N, int hd, int dtype, int budget, const float *row_lse,
+                                 int32_t *kept, float *score, void *workspace,
+                                 size_t workspace_bytes, void *stream, void *const *events,
+                                 int n_events, int reps, int *n_kernels, const char **names);
 
 int pv_critical_text_timed(const void *text, int B, int Nt, int d, int dtype, int32_t *mask,
                            int32_t *count, float *r, void *workspace, size_t workspace_bytes,

@@ -333,8 +333,11 @@ int check_head(const void *q, const void *k, const int32_t *heads, const int32_t
 int head_impl(const void *q, const void *k, const int32_t *heads, const int32_t *heads_dev,
               int n_heads, int B, int H, int Nt, int N, int hd, int dtype, int budget,
               int32_t *kept, float *score, void *workspace, size_t ws_bytes, void *stream,
-              void *const *events, int n_events, int reps, int *n_kernels, const char **names) {
+              void *const *events, int n_events, int reps, int *n_kernels, const char **names,
+              const float *row_lse = nullptr) {
     if (reps < 1) return PV_ERR_SHAPE;
+    if (heads && heads_dev) return PV_ERR_HEADS;  // one list, on one side
+    if (row_lse && (uintptr_t)row_lse % 4) return PV_ERR_ALIGN;
     int rc = check_head(q, k, heads, heads_dev, n_heads, B, H, Nt, N, hd, dtype, budget, kept);
     if (rc != PV_OK) return rc;
     HeadPlan P0 = plan_head(nullptr, B, Nt, N, n_heads, score == nullptr);
@@ -350,8 +353,8 @@ int head_impl(const void *q, const void *k, const int32_t *heads, const int32_t 
     if (!tr.handles_ok()) return PV_ERR_NULL;
 
     if (!tr.launch("score_partial", [&] {
-            return pv::launch_score_partial(dt, q, k, heads, heads_dev, B, H, Nt, N, hd, n_heads,
-                                            P.partial, st);
+            return pv::launch_score_partial(dt, q, k, heads, heads_dev, row_lse, B, H, Nt, N, hd,
+                                            n_heads, P.partial, st);
         }))
         return PV_ERR_HIP;
     const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
@@ -603,6 +606,28 @@ PV_API int pv_prune_head_aware_dev_timed(const void *q, const void *k, const int
     return head_impl(q, k, nullptr, heads_dev, n_heads, B, H, Nt, N, hd, dtype, budget, kept,
                      score, workspace, workspace_bytes, stream, events, n_events, reps, n_kernels,
                      names);
+}
+
+PV_API int pv_prune_head_aware_ex(const void *q, const void *k, const int32_t *heads_host,
+                                  const int32_t *heads_dev, int n_heads, int B, int H, int Nt,
+                                  int N, int hd, int dtype, int budget, const float *row_lse,
+                                  int32_t *kept, float *score, void *workspace,
+                                  size_t workspace_bytes, void *stream) {
+    return head_impl(q, k, heads_host, heads_dev, n_heads, B, H, Nt, N, hd, dtype, budget, kept,
+                     score, workspace, workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr,
+                     row_lse);
+}
+
+PV_API int pv_prune_head_aware_ex_timed(const void *q, const void *k, const int32_t *heads_host,
+                                        const int32_t *heads_dev, int n_heads, int B, int H,
+                                        int Nt, int N, int hd, int dtype, int budget,
+                                        const float *row_lse, int32_t *kept, float *score,
+                                        void *workspace, size_t workspace_bytes, void *stream,
+                                        void *const *events, int n_events, int reps,
+                                        int *n_kernels, const char **names) {
+    return head_impl(q, k, heads_host, heads_dev, n_heads, B, H, Nt, N, hd, dtype, budget, kept,
+                     score, workspace, workspace_bytes, stream, events, n_events, reps, n_kernels,
+                     names, row_lse);
 }
 
 PV_API size_t pv_visual_heads_workspace_bytes(int B, int H, int Nt) {

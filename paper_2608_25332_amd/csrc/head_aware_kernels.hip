@@ -75,8 +75,8 @@ template <int DT, int NKS, int MAXC, bool CONF>
 __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
     const int32_t *__restrict__ heads_dev, int head_src, const int32_t *__restrict__ row_mask,
-    int b0, int H, int Nt, int N, int n_heads, float scale_log2e, float *__restrict__ partial,
-    int cols_in_lds) {
+    const float *__restrict__ row_lse, int b0, int H, int Nt, int N, int n_heads,
+    float scale_log2e, float *__restrict__ partial, int cols_in_lds) {
     static_assert(!CONF || MAXC == 0, "the confidence needs no second pass");
     using S = ScoreStage<NKS>;
     __shared__ __attribute__((aligned(16))) char ring[S::NS][S::STAGE];
@@ -275,6 +275,12 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         float mm = sm_m[0][tid], ll = sm_l[0][tid];
 #pragma unroll
         for (int w = 1; w < 4; ++w) lse_merge(mm, ll, sm_m[w][tid], sm_l[w][tid]);
+        // the model's row also runs over the non-visual keys: their
+        // log-sum-exp (natural log, scaled logits) joins the normaliser
+        if (row_lse) {
+            const float t = row_lse[((size_t)b * H + h) * Nt + min(rb * 16 + tid, Nt - 1)];
+            lse_merge(mm, ll, t * 1.4426950408889634f, 1.f);
+        }
         row_m[tid] = mm;
         row_il[tid] = (rb * 16 + tid < Nt) ? 1.0f / ll : 0.f;  // masked rows add nothing
     }
@@ -387,6 +393,7 @@ struct ScoreLaunch {
     const int32_t *heads_dev;   // kHeadsDevice: device list [B][n_heads]
     int src;
     const int32_t *row_mask;    // confidence only: rows summed (may be NULL)
+    const float *row_lse;       // score only: [B][H][Nt] non-visual log-sum-exp (may be NULL)
     int B, H, Nt, N, n_heads;
     float sl2e;
     float *partial;
@@ -415,8 +422,8 @@ static hipError_t score_go(const ScoreLaunch &a) {
         dim3 grid(nrb * a.n_heads * nb);
         hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC, CONF>), grid, dim3(kScoreNT),
                            in_lds ? cols : 0, a.st, (const char *)a.q, (const char *)a.k, ha,
-                           a.heads_dev, a.src, a.row_mask, b0, a.H, a.Nt, a.N, a.n_heads, a.sl2e,
-                           a.partial, in_lds ? 1 : 0);
+                           a.heads_dev, a.src, a.row_mask, a.row_lse, b0, a.H, a.Nt, a.N,
+                           a.n_heads, a.sl2e, a.partial, in_lds ? 1 : 0);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -482,16 +489,18 @@ static hipError_t score_any(int dt, int hd, ScoreLaunch a) {
 }
 
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
-                                const int32_t *heads_dev, int B, int H, int Nt, int N, int hd,
-                                int n_heads, float *partial, hipStream_t st) {
+                                const int32_t *heads_dev, const float *row_lse, int B, int H,
+                                int Nt, int N, int hd, int n_heads, float *partial,
+                                hipStream_t st) {
     ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg, nullptr,
-                  B, H, Nt, N, n_heads, 0.f, partial, st};
+                  row_lse, B, H, Nt, N, n_heads, 0.f, partial, st};
     return score_any<false>(dt, hd, a);
 }
 
 hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask, int B,
                             int H, int Nt, int N, int hd, float *partial, hipStream_t st) {
-    ScoreLaunch a{q, k, nullptr, nullptr, kHeadsAll, row_mask, B, H, Nt, N, H, 0.f, partial, st};
+    ScoreLaunch a{q, k, nullptr, nullptr, kHeadsAll, row_mask, nullptr, B, H, Nt, N, H, 0.f,
+                  partial, st};
     return score_any<true>(dt, hd, a);
 }
 

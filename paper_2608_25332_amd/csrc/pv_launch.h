@@ -77,9 +77,12 @@ hipError_t launch_text_rank(const float *G, int B, int Nt, float *r, int32_t *ma
 // ---- head-aware pruning (Sec. 4.4)
 // heads_dev == nullptr: the head list is heads_host (host memory); else the
 // device list heads_dev (entries clamped into [0, H)).
+// row_lse [B][H][Nt] (may be NULL): log-sum-exp of each row's scaled logits
+// over the non-visual keys, which join the softmax normaliser.
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
-                                const int32_t *heads_dev, int B, int H, int Nt, int N, int hd,
-                                int n_heads, float *partial, hipStream_t st);
+                                const int32_t *heads_dev, const float *row_lse, int B, int H,
+                                int Nt, int N, int hd, int n_heads, float *partial,
+                                hipStream_t st);
 // Head confidence of every head, per 16-row block: partial[b][h][rb].
 // row_mask as for launch_center: the rows summed into the confidence.
 hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask, int B,

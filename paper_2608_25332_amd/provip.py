@@ -102,6 +102,11 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_head_aware_dev_timed.argtypes = had + [ctypes.POINTER(_vp), _i, _i,
                                                         ctypes.POINTER(_i), names_t]
     lib.pv_prune_head_aware_dev_timed.restype = _i
+    hax = [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _vp, _sz, _vp]
+    lib.pv_prune_head_aware_ex.argtypes = hax
+    lib.pv_prune_head_aware_ex.restype = _i
+    lib.pv_prune_head_aware_ex_timed.argtypes = hax + timed_tail
+    lib.pv_prune_head_aware_ex_timed.restype = _i
     lib.pv_visual_heads_workspace_bytes.argtypes = [_i, _i, _i]
     lib.pv_visual_heads_workspace_bytes.restype = _sz
     vh = [_vp, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _sz, _vp]
@@ -306,10 +311,13 @@ def pv_visual_heads_workspace_bytes(B: int, H: int, Nt: int) -> int:
 def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
                         want_score: bool = True, out: Optional[dict] = None,
                         workspace: Optional[torch.Tensor] = None,
-                        events: Optional[Sequence] = None, reps: int = 1):
+                        events: Optional[Sequence] = None, reps: int = 1,
+                        row_lse: Optional[torch.Tensor] = None):
     """Head-aware pruning.  q [B,H,Nt,hd], k [B,H,N,hd] (same dtype), heads:
     host int sequence [B, n_heads], or an int32 tensor [B, n_heads] on q's
     device (pv_prune_head_aware_dev: e.g. the list pv_visual_heads wrote).
+    row_lse: float32 [B,H,Nt] on the device, the log-sum-exp of each row's
+    scaled logits over the non-visual keys (pv_prune_head_aware_ex).
     Returns dict(kept [B,budget] int32, score [B,N] f32 | None, n_kernels).
     events / reps: see pv_prune_head_aware_timed (profiling only)."""
     import numpy as np
@@ -344,7 +352,18 @@ def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     ev, nev, nm = _events_array(events)
     nk = _i(0)
-    if on_dev:
+    if row_lse is not None:
+        if (row_lse.dtype != torch.float32 or tuple(row_lse.shape) != (B, H, Nt)
+                or row_lse.device != dev or not row_lse.is_contiguous()):
+            raise ValueError(f"row_lse must be a contiguous float32 [B, H, Nt] tensor on {dev}")
+        hh = None if on_dev else hs.ctypes.data_as(ctypes.c_void_p)
+        hd_ptr = hs.data_ptr() if on_dev else None
+        rc = lib.pv_prune_head_aware_ex_timed(q.data_ptr(), k.data_ptr(), hh, hd_ptr, n_heads, B,
+                                              H, Nt, N, hd, code, int(budget), row_lse.data_ptr(),
+                                              kept.data_ptr(), _ptr(score), workspace.data_ptr(),
+                                              workspace.numel(), _stream(dev), ev, nev, int(reps),
+                                              ctypes.byref(nk), nm)
+    elif on_dev:
         rc = lib.pv_prune_head_aware_dev_timed(q.data_ptr(), k.data_ptr(), hs.data_ptr(), n_heads,
                                                B, H, Nt, N, hd, code, int(budget), kept.data_ptr(),
                                                _ptr(score), workspace.data_ptr(), workspace.numel(),

@@ -131,6 +131,21 @@ def test_head_aware_dev_validation(lib):
     assert call(ws=None) == -6
 
 
+def test_head_aware_ex_validation(lib):
+    f = lib.pv_prune_head_aware_ex
+    hs = np.zeros(2, np.int32)
+    hp = hs.ctypes.data_as(ctypes.c_void_p)
+
+    def call(hh=hp, hdev=None, lse=None, n_heads=2):
+        return f(FAKE, FAKE, hh, hdev, n_heads, 1, 4, 16, 32, 64, 1, 8, lse, FAKE, None, FAKE,
+                 1 << 40, None)
+    assert call(hh=None) == -1            # no list at all
+    assert call(hdev=FAKE) == -4          # two lists
+    assert call(lse=FAKE + 2) == -8       # row_lse not 4-byte aligned
+    hs[:] = [0, 0]
+    assert call() == -4                   # the host list is still checked
+
+
 def test_visual_heads_validation(lib):
     f = lib.pv_visual_heads
     assert lib.pv_visual_heads_workspace_bytes(1, 32, 64) > 0

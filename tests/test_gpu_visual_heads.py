@@ -1,6 +1,8 @@
 """Visual-head identification (Sec. 4.4, equations for C^h and V_l) on the
-GPU against the CPU oracle, and head-aware pruning with head lists that stay
-in device memory.  All calls go through the C ABI."""
+GPU against the CPU oracle, head-aware pruning with head lists that stay in
+device memory, and head-aware pruning on the model's softmax domain (the
+non-visual keys through one log-sum-exp per row).  All calls go through the
+C ABI."""
 
 from __future__ import annotations
 
@@ -156,3 +158,51 @@ def test_visual_heads_then_head_aware(wid):
     assert rel_err(v, ref_v) <= TOL[dt]
     for i in range(len(same)):
         check_kept(kept[i], ref_v[i], w.N2, dt)
+
+
+def _lse_of_other_keys(q, n_other, seed, scale=1.5):
+    """Inputs for the in-model domain: synthetic non-visual keys per head and
+    the log-sum-exp of each text row's scaled logits over them (float64)."""
+    rng = np.random.default_rng(seed)
+    B, H, Nt, hd = q.shape
+    ko = rng.standard_normal((B, H, n_other, hd)) * scale
+    lg = np.einsum("bhid,bhjd->bhij", q.astype(np.float64), ko) / np.sqrt(hd)
+    m = lg.max(-1, keepdims=True)
+    return (m[..., 0] + np.log(np.exp(lg - m).sum(-1))).astype(np.float32)
+
+
+@pytest.mark.parametrize("wid,n_other", [(2, 40), (4, 600), (1, 3)])
+def test_head_aware_in_model_parity(wid, n_other):
+    from paper_2608_25332_amd import provip
+    w = workload(wid)
+    dt = w.dtype
+    _say(f"[head-aware-in-model] workload {wid} other keys {n_other}")
+    k1 = _subset_keys(w, w.N1, 700 + wid)
+    lse = _lse_of_other_keys(w.q, n_other, 800 + wid)
+    r = provip.pv_prune_head_aware(to_dev(w.q, dt), to_dev(k1, dt), w.heads, w.N2,
+                                   row_lse=torch.from_numpy(lse).to("cuda:0"))
+    torch.cuda.synchronize()
+    v, kept = to_host(r["score"]), to_host(r["kept"])
+    ref_kept, ref_v = oracle.head_aware_in_model(w.q, k1, w.heads, lse.astype(np.float64), w.N2)
+    assert rel_err(v, ref_v) <= TOL[dt], rel_err(v, ref_v)
+    for b in range(w.spec.B):
+        check_kept(kept[b], ref_v[b], w.N2, dt)
+        assert float(np.sum(v[b], dtype=np.float64)) < 1.0
+
+
+def test_head_aware_in_model_minus_inf_is_plain():
+    """row_lse = -inf everywhere gives the plain call's bits, with host and
+    device head lists."""
+    from paper_2608_25332_amd import provip
+    w = workload(2)
+    k1 = _subset_keys(w, w.N1, 900)
+    qd, kd = to_dev(w.q, "bf16"), to_dev(k1, "bf16")
+    B, H, Nt = w.q.shape[:3]
+    lse = torch.full((B, H, Nt), float("-inf"), dtype=torch.float32, device="cuda:0")
+    plain = provip.pv_prune_head_aware(qd, kd, w.heads, w.N2)
+    a = provip.pv_prune_head_aware(qd, kd, w.heads, w.N2, row_lse=lse)
+    b = provip.pv_prune_head_aware(qd, kd, torch.from_numpy(np.ascontiguousarray(w.heads, np.int32))
+                                   .to("cuda:0"), w.N2, row_lse=lse)
+    torch.cuda.synchronize()
+    for r in (a, b):
+        assert torch.equal(r["score"], plain["score"]) and torch.equal(r["kept"], plain["kept"])
