@@ -348,6 +348,188 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     }
 }
 
+// ----------------------------------------------------------------------------
+// score_head: one workgroup per (selected head, sample), for up to 64 text
+// rows and 256 keys (the shapes of the paper's layers).  Wave w owns text
+// rows 16 w .. 16 w + 15 for every key, so its row statistics need no
+// exchange with the other waves, and the head's keys are read into LDS once
+// for all rows (score_partial reads them once per 16-row block).  The query
+// block and the (at most four) key chunks are all issued at the start; the
+// logits stay in registers; the four waves' column sums meet in LDS and are
+// added in wave order.  Writes one row of column sums per (sample, head).
+// ----------------------------------------------------------------------------
+constexpr int kHeadMaxRows = 64;
+constexpr int kHeadMaxChunks = 4;
+
+template <int DT, int NKS>
+__global__ __launch_bounds__(kScoreNT) void score_head_kernel(
+    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
+    const int32_t *__restrict__ heads_dev, int head_src, const float *__restrict__ row_lse, int b0,
+    int H, int Nt, int N, int n_heads, float scale_log2e, float *__restrict__ partial) {
+    using S = ScoreStage<NKS>;
+    constexpr int MAXC = kHeadMaxChunks;
+    // the key chunks in dynamic LDS, nch of them (so that two workgroups fit
+    // on a CU for 192 keys)
+    extern __shared__ __attribute__((aligned(16))) char kdyn[];
+    auto kbuf = [&](int ch) { return kdyn + ch * S::STAGE; };
+    __shared__ __attribute__((aligned(16))) char qrows[kHeadMaxRows * S::RB];
+    __shared__ float colpart[4][MAXC * kScoreCK];
+    const int L = blockIdx.x;
+    const int hi = L % n_heads, bl = L / n_heads, b = b0 + bl;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int h;
+    if (head_src == kHeadsDevice) h = min(max(heads_dev[(size_t)b * n_heads + hi], 0), H - 1);
+    else h = heads.h[bl * n_heads + hi];
+    const char *qb = q + ((size_t)b * H + h) * Nt * S::RB;
+    const char *kb = k + ((size_t)b * H + h) * N * S::RB;
+    const int nch = (N + kScoreCK - 1) / kScoreCK;  // <= MAXC (host-checked)
+
+    // every load of the kernel is a direct-to-LDS load, issued up front:
+    // the query rows (rows past Nt repeat the last one), then each chunk
+    const int nq = ((Nt + 15) / 16) * 16 * S::RB / 1024;  // 1 KiB pieces of the query block
+    for (int pce = wave; pce < nq; pce += 4) {
+        const int off = pce * 1024 + lane * 16;
+        lds_dma16(qb + (size_t)min(off / S::RB, Nt - 1) * S::RB + off % S::RB, qrows + pce * 1024);
+    }
+#pragma unroll
+    for (int ch = 0; ch < MAXC; ++ch) {
+        if (ch < nch) {
+#pragma unroll
+            for (int t = 0; t < S::IPW; ++t) {
+                const int pos = (wave * S::IPW + t) * 64 + lane;
+                const int r = pos / S::PPR, slot = pos % S::PPR;
+                const int row = min(ch * kScoreCK + r, N - 1);  // past the end: last key
+                lds_dma16(kb + (size_t)row * S::RB + ((slot ^ (r & S::SWZ)) << 4),
+                          kbuf(ch) + (wave * S::IPW + t) * 1024);
+            }
+        }
+    }
+    wait_vmcnt<0>();
+    bare_barrier();
+
+    const bool rows_live = wave * 16 < Nt;  // uniform: this wave has rows to score
+    // logits of this wave's 16 rows x every key: lane holds rows
+    // 4 (lane / 16) + i of column (lane % 16) of each 16-key block
+    f32x4_t keep[MAXC][4];
+    if (rows_live) {
+        uint4 qf[NKS];
+        const int qr = wave * 16 + (lane & 15);
+#pragma unroll
+        for (int s = 0; s < NKS; ++s) qf[s] = lds_read16(qrows + qr * S::RB + (s * 4 + (lane >> 4)) * 16);
+        lds_wait();
+#pragma unroll
+        for (int s = 0; s < NKS; ++s) lds_after_wait(qf[s]);
+#pragma unroll
+        for (int ch = 0; ch < MAXC; ++ch) {
+            if (ch < nch) {
+#pragma unroll
+                for (int kq = 0; kq < 4; ++kq) {
+                    const int r = kq * 16 + (lane & 15);
+                    uint4 kf[NKS];
+#pragma unroll
+                    for (int s = 0; s < NKS; ++s) {
+                        const int piece = s * 4 + (lane >> 4);
+                        kf[s] = lds_read16(kbuf(ch) + r * S::RB + ((piece ^ (r & S::SWZ)) << 4));
+                    }
+                    lds_wait();
+                    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int s = 0; s < NKS; ++s) {
+                        lds_after_wait(kf[s]);
+                        acc = mma16<DT>(qf[s], kf[s], acc);
+                    }
+                    keep[ch][kq] = acc;
+                }
+            }
+        }
+    }
+    // Row statistics with every logit at hand: the row maximum first, then
+    // one exponential per logit (kept in place of it) and their sum.  Keys
+    // past N are left out of both.
+    float m[4], il[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) m[i] = -INFINITY;
+    if (rows_live) {
+#pragma unroll
+        for (int ch = 0; ch < MAXC; ++ch) {
+            if (ch < nch) {
+#pragma unroll
+                for (int kq = 0; kq < 4; ++kq) {
+                    const bool col_ok = ch * kScoreCK + kq * 16 + (lane & 15) < N;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float x = col_ok ? keep[ch][kq][i] * scale_log2e : -INFINITY;
+                        keep[ch][kq][i] = x;
+                        m[i] = fmaxf(m[i], x);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) m[i] = fmaxf(m[i], __shfl_xor(m[i], off, 64));
+        }
+    }
+    float l[4] = {0.f, 0.f, 0.f, 0.f};
+    if (rows_live) {
+#pragma unroll
+        for (int ch = 0; ch < MAXC; ++ch) {
+            if (ch < nch) {
+#pragma unroll
+                for (int kq = 0; kq < 4; ++kq) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float e = exp2f(keep[ch][kq][i] - m[i]);  // 0 for keys past N
+                        keep[ch][kq][i] = e;
+                        l[i] += e;
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) l[i] += __shfl_xor(l[i], off, 64);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = wave * 16 + (lane >> 4) * 4 + i;
+        float mm = m[i], ll = l[i];
+        if (rows_live && row_lse) {
+            // the non-visual keys join the normaliser on the scale of the
+            // kept exponentials (relative to m; an overflow only means the
+            // row's visual mass is 0 in fp32)
+            const float t = row_lse[((size_t)b * H + h) * Nt + min(row, Nt - 1)] * 1.4426950408889634f;
+            ll += exp2f(t - mm);
+        }
+        il[i] = (rows_live && row < Nt) ? 1.0f / ll : 0.f;  // masked rows add nothing
+    }
+    // this wave's column sums over its 16 rows, chunk by chunk
+#pragma unroll
+    for (int ch = 0; ch < MAXC; ++ch) {
+        if (ch < nch) {
+#pragma unroll
+            for (int kq = 0; kq < 4; ++kq) {
+                float cs = 0.f;
+                if (rows_live) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) cs += keep[ch][kq][i] * il[i];
+                }
+                cs += __shfl_xor(cs, 16, 64);
+                cs += __shfl_xor(cs, 32, 64);
+                if (lane < 16) colpart[wave][ch * kScoreCK + kq * 16 + lane] = cs;
+            }
+        }
+    }
+    __syncthreads();
+    float *out = partial + ((size_t)b * n_heads + hi) * N;
+    for (int j = tid; j < N; j += kScoreNT)
+        out[j] = ((colpart[0][j] + colpart[1][j]) + colpart[2][j]) + colpart[3][j];
+}
+
 constexpr int kSelU = 16;
 
 template <int NT, int EMAX>
@@ -479,6 +661,25 @@ static hipError_t score_dt(int nks, const ScoreLaunch &a) {
     return hipErrorInvalidValue;
 }
 
+template <int DT, int NKS>
+static hipError_t score_head_go(const ScoreLaunch &a) {
+    const int per_launch = a.src == kHeadsArg ? kMaxHeadArgs / a.n_heads : a.B;
+    HeadArgs ha;
+    for (int b0 = 0; b0 < a.B; b0 += per_launch) {
+        const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
+        for (int i = 0; i < kMaxHeadArgs; ++i)
+            ha.h[i] = (a.src == kHeadsArg && i < nb * a.n_heads)
+                          ? a.heads_host[(size_t)b0 * a.n_heads + i] : 0;
+        const size_t kbytes = (size_t)((a.N + kScoreCK - 1) / kScoreCK) * ScoreStage<NKS>::STAGE;
+        hipLaunchKernelGGL((score_head_kernel<DT, NKS>), dim3(a.n_heads * nb), dim3(kScoreNT),
+                           kbytes, a.st, (const char *)a.q, (const char *)a.k, ha, a.heads_dev, a.src,
+                           a.row_lse, b0, a.H, a.Nt, a.N, a.n_heads, a.sl2e, a.partial);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 template <bool CONF>
 static hipError_t score_any(int dt, int hd, ScoreLaunch a) {
     const int esz = (dt == kBF16) ? 2 : 4;
@@ -488,12 +689,27 @@ static hipError_t score_any(int dt, int hd, ScoreLaunch a) {
     return score_dt<kF32, CONF>(nks, a);
 }
 
+// The whole-head form pays once there are enough (head, sample) pairs to
+// fill the chip (measured: from 128 pairs it is faster, below it the
+// 16-row blocks spread over more CUs and win by ~0.5 us).
+bool score_uses_head_form(int dt, int B, int n_heads, int Nt, int N, int hd) {
+    const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
+    return (nks == 2 || nks == 4) && Nt <= kHeadMaxRows && N <= kHeadMaxChunks * kScoreCK &&
+           (long long)B * n_heads >= 128;
+}
+
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, const float *row_lse, int B, int H,
                                 int Nt, int N, int hd, int n_heads, float *partial,
                                 hipStream_t st) {
     ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg, nullptr,
                   row_lse, B, H, Nt, N, n_heads, 0.f, partial, st};
+    if (score_uses_head_form(dt, B, n_heads, Nt, N, hd)) {
+        a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
+        const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
+        if (dt == kBF16) return nks == 2 ? score_head_go<kBF16, 2>(a) : score_head_go<kBF16, 4>(a);
+        return nks == 2 ? score_head_go<kF32, 2>(a) : score_head_go<kF32, 4>(a);
+    }
     return score_any<false>(dt, hd, a);
 }
 

@@ -77,6 +77,10 @@ hipError_t launch_text_rank(const float *G, int B, int Nt, float *r, int32_t *ma
 // ---- head-aware pruning (Sec. 4.4)
 // heads_dev == nullptr: the head list is heads_host (host memory); else the
 // device list heads_dev (entries clamped into [0, H)).
+// Whether the score runs one workgroup per (head, sample) (score_head) and
+// writes one row of column sums per (sample, head) instead of one per
+// 16-row block.
+bool score_uses_head_form(int dt, int B, int n_heads, int Nt, int N, int hd);
 // row_lse [B][H][Nt] (may be NULL): log-sum-exp of each row's scaled logits
 // over the non-visual keys, which join the softmax normaliser.
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,

@@ -328,6 +328,12 @@ HEAD_EDGE = [
     (40, 16, 16, 64, 64, 16, 20, "bf16"),     # 640 head-list entries: two launches
     (1, 2, 16, 9000, 256, 1, 500, "f32"),     # column sums flushed from registers
     (1, 1, 9, 12100, 224, 1, 900, "f32"),     # the same, 14 pieces per key row
+    # one workgroup per (head, sample) once there are >= 128 of them
+    (32, 8, 64, 256, 128, 4, 60, "bf16"),     # four full key chunks
+    (64, 4, 33, 70, 64, 2, 10, "f32"),        # ragged rows (an idle wave) and keys
+    (128, 2, 1, 1, 32, 1, 1, "f32"),          # one row, one key
+    (130, 3, 50, 200, 64, 1, 20, "bf16"),
+    (16, 32, 64, 192, 128, 32, 64, "bf16"),   # every head of the LLaVA-1.5 layer
 ]
 
 

@@ -206,3 +206,23 @@ def test_head_aware_in_model_minus_inf_is_plain():
     torch.cuda.synchronize()
     for r in (a, b):
         assert torch.equal(r["score"], plain["score"]) and torch.equal(r["kept"], plain["kept"])
+
+
+def test_head_aware_in_model_whole_head_form():
+    """The in-model domain on the one-workgroup-per-(head, sample) form
+    (128 pairs)."""
+    from paper_2608_25332_amd import provip
+    rng = np.random.default_rng(12)
+    B, H, Nt, N, hd, nh = 32, 8, 64, 192, 128, 4
+    q = W.bf16_round((rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32))
+    k = W.bf16_round((rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32))
+    heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+    lse = _lse_of_other_keys(q, 50, 13)
+    r = provip.pv_prune_head_aware(to_dev(q, "bf16"), to_dev(k, "bf16"), heads, 30,
+                                   row_lse=torch.from_numpy(lse).to("cuda:0"))
+    torch.cuda.synchronize()
+    v, kept = to_host(r["score"]), to_host(r["kept"])
+    ref_kept, ref_v = oracle.head_aware_in_model(q, k, heads, lse.astype(np.float64), 30)
+    assert rel_err(v, ref_v) <= TOL["bf16"], rel_err(v, ref_v)
+    for b in range(B):
+        check_kept(kept[b], ref_v[b], 30, "bf16")
