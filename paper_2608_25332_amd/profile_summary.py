@@ -6,6 +6,8 @@ with the sources.
   python -m paper_2608_25332_amd.profile_summary pmc <fetch counter_collection.csv> \\
       <write counter_collection.csv> --workload NAME --calib-bytes N \\
       --digest D --command "CMD" --command2 "CMD2"        > summary.md
+  python -m paper_2608_25332_amd.profile_summary counters <counter_collection.csv>... \\
+      --workload NAME --command "CMD" [--command "CMD2"] --note TEXT > summary.md
 
 pmc: FETCH_SIZE and WRITE_SIZE (KiB per dispatch, summed over the L2
 channels) of every library kernel, averaged over its dispatches and scaled
@@ -153,6 +155,38 @@ def pmc(args) -> str:
     return "\n".join(out) + "\n"
 
 
+def counters(args) -> str:
+    """Per library kernel, the mean per dispatch of every counter in the given
+    counter_collection.csv files (one rocprofv3 --pmc run each)."""
+    vals = defaultdict(lambda: defaultdict(list))
+    for path in args.csv:
+        rows = list(csv.DictReader(open(path)))
+        per = defaultdict(float)
+        names = {}
+        for r in rows:
+            key = (r["Dispatch_Id"], r["Counter_Name"])
+            per[key] += float(r["Counter_Value"])
+            names[r["Dispatch_Id"]] = r["Kernel_Name"]
+        for (disp, cname), v in per.items():
+            n = names[disp]
+            if n.startswith(("pv::", "void pv::")):
+                vals[kernel_key(n)][cname].append(v)
+    cnames = sorted({c for d in vals.values() for c in d})
+    out = [f"# Hardware counters per dispatch: {args.workload}", "",
+           "Commands (repository root on one MI355X, one run per line):", "", "```"]
+    out += list(args.command) + ["```", "", args.note, "",
+                                 "| kernel | dispatches | " + " | ".join(cnames) + " |",
+                                 "|---|---|" + "---|" * len(cnames)]
+    for k, d in sorted(vals.items()):
+        n = max(len(v) for v in d.values())
+        cells = []
+        for c in cnames:
+            v = d.get(c)
+            cells.append("" if not v else f"{sum(v) / len(v):.1f}")
+        out.append(f"| {k} | {n} | " + " | ".join(cells) + " |")
+    return "\n".join(out) + "\n"
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -170,8 +204,13 @@ def main(argv=None):
     p.add_argument("--digest", required=True)
     p.add_argument("--command", required=True)
     p.add_argument("--command2", required=True)
+    c = sub.add_parser("counters")
+    c.add_argument("csv", nargs="+")
+    c.add_argument("--workload", required=True)
+    c.add_argument("--command", action="append", required=True)
+    c.add_argument("--note", default="")
     a = ap.parse_args(argv)
-    sys.stdout.write(trace(a) if a.cmd == "trace" else pmc(a))
+    sys.stdout.write({"trace": trace, "pmc": pmc, "counters": counters}[a.cmd](a))
 
 
 if __name__ == "__main__":
