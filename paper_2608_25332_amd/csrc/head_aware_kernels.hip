@@ -206,18 +206,92 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     start();
     if constexpr (MAXC > 0) {
         // unrolled with constant indices (nch is uniform): each block stays
-        // in its own registers
+        // in its own registers; the statistics come after the last chunk
 #pragma unroll
-        for (int ch = 0; ch < MAXC; ++ch) {
-            if (ch < nch) {
-                keep[ch] = chunk(ch, false);
-                stats(keep[ch], ch);
-            }
-        }
+        for (int ch = 0; ch < MAXC; ++ch)
+            if (ch < nch) keep[ch] = chunk(ch, false);
     } else {
         for (int ch = 0; ch < nch; ++ch) stats(chunk(ch, false), ch);
     }
     finish();
+    if constexpr (MAXC > 0 && !CONF) {
+        // Every logit at hand: the row maximum first (lanes, then waves),
+        // then one exponential per logit, kept in place, and the row sums.
+        // Keys past N are left out of both.
+#pragma unroll
+        for (int ch = 0; ch < MAXC; ++ch) {
+            if (ch < nch) {
+                const bool col_ok = ch * kScoreCK + wave * 16 + (lane & 15) < N;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float x = col_ok ? keep[ch][i] * scale_log2e : -INFINITY;
+                    keep[ch][i] = x;
+                    m[i] = fmaxf(m[i], x);
+                }
+            }
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) m[i] = fmaxf(m[i], __shfl_xor(m[i], off, 64));
+        if ((lane & 15) == 0)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) sm_m[wave][(lane >> 4) * 4 + i] = m[i];
+        __syncthreads();
+        if (tid < 16)
+            row_m[tid] = fmaxf(fmaxf(sm_m[0][tid], sm_m[1][tid]), fmaxf(sm_m[2][tid], sm_m[3][tid]));
+        __syncthreads();
+        float rmx[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rmx[i] = row_m[(lane >> 4) * 4 + i];
+#pragma unroll
+        for (int ch = 0; ch < MAXC; ++ch) {
+            if (ch < nch) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float e = exp2f(keep[ch][i] - rmx[i]);  // 0 for keys past N
+                    keep[ch][i] = e;
+                    l[i] += e;
+                }
+            }
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) l[i] += __shfl_xor(l[i], off, 64);
+        if ((lane & 15) == 0)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) sm_l[wave][(lane >> 4) * 4 + i] = l[i];
+        __syncthreads();
+        if (tid < 16) {
+            float ll = ((sm_l[0][tid] + sm_l[1][tid]) + sm_l[2][tid]) + sm_l[3][tid];
+            // the non-visual keys join the normaliser on the scale of the
+            // kept exponentials (relative to the row maximum)
+            if (row_lse) {
+                const float t = row_lse[((size_t)b * H + h) * Nt + min(rb * 16 + tid, Nt - 1)];
+                ll += exp2f(t * 1.4426950408889634f - row_m[tid]);
+            }
+            row_il[tid] = (rb * 16 + tid < Nt) ? 1.0f / ll : 0.f;  // masked rows add nothing
+        }
+        __syncthreads();
+        float rl[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rl[i] = row_il[(lane >> 4) * 4 + i];
+        float *outp = partial + (((size_t)b * n_heads + hi) * nrb + rb) * N;
+#pragma unroll
+        for (int ch = 0; ch < MAXC; ++ch) {
+            if (ch < nch) {
+                float cs = 0.f;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) cs += keep[ch][i] * rl[i];
+                cs += __shfl_xor(cs, 16, 64);
+                cs += __shfl_xor(cs, 32, 64);
+                const int col = ch * kScoreCK + wave * 16 + (lane & 15);
+                if (lane < 16 && col < N) outp[col] = cs;
+            }
+        }
+        return;
+    }
     // combine the 16 lanes that hold the same rows, then the 4 waves
 #pragma unroll
     for (int off = 1; off < 16; off <<= 1) {
@@ -293,20 +367,9 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         ril[i] = row_il[(lane >> 4) * 4 + i];
     }
     float *out = partial + (((size_t)b * n_heads + hi) * nrb + rb) * N;
-    // pass 2: normalised probabilities, summed over the 16 rows of each column
-    auto emit = [&](const f32x4_t &acc, int col) {
-        float cs = 0.f;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) cs += exp2f(acc[i] * scale_log2e - rm[i]) * ril[i];
-        cs += __shfl_xor(cs, 16, 64);
-        cs += __shfl_xor(cs, 32, 64);
-        if (lane < 16 && col < N) out[col] = cs;
-    };
-    if (MAXC > 0) {
-#pragma unroll
-        for (int c = 0; c < (MAXC > 0 ? MAXC : 1); ++c)
-            if (c < nch) emit(keep[c], c * kScoreCK + wave * 16 + (lane & 15));
-    } else {
+    // pass 2 (keys streamed again): normalised probabilities, summed over the
+    // 16 rows of each column
+    if constexpr (MAXC == 0) {
         // Stores must not be in flight at a partial wait (see chunk()): the
         // column sums go to LDS while the keys stream and to memory after
         // the pass, or, where N of them do not fit beside the ring, are held
