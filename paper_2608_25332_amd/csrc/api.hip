@@ -87,7 +87,7 @@ struct DedupPlan {
     bool cos_full;                 // cosine in one full-k pass (small inputs)
     int ks_cos, njt;               // cosine: k slices, token tiles of the row sums
     int Mp;
-    bool gram_big;                 // full-k 256x128 tiles (operands streamed into LDS)
+    bool gram_big;                 // full-k 128x128 tiles (operands streamed into LDS)
     int ks_gram, ntn;              // split-k slices (small) / column tiles (big)
     // workspace
     bool lists;                    // merge reads bucketed member lists
@@ -106,7 +106,7 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
     P.njt = P.cos_full ? pv::cos_full_row_tiles(Nv) : pv::cos_row_tiles(Nv);
     P.Mp = Nv - budget;
     const int Mp1 = P.Mp > 0 ? P.Mp : 1;
-    P.gram_big = (long long)((Mp1 + pv::kGramTileM - 1) / pv::kGramTileM) *
+    P.gram_big = (long long)((Mp1 + pv::kGramBigM - 1) / pv::kGramBigM) *
                      ((budget + pv::kGramTileN - 1) / pv::kGramTileN) * B >= 128;
     P.ks_gram = P.gram_big ? 1 : pick_slices(n_tiles(Mp1, budget, B, T), P.nch);
     P.ntn = P.gram_big ? (budget + pv::kGramTileN - 1) / pv::kGramTileN : 1;

@@ -508,8 +508,12 @@ __global__ __launch_bounds__(128) void gram_reduce_kernel(
 
 // gram_tile: the large, MFMA-bound Grams.  1-D grid over (sample, pruned
 // tile, kept tile) in XCD order (the kept tiles of one pruned tile are
-// adjacent, so they share its rows in one L2); 256 x 128 tiles with the
-// operands streamed straight into LDS (TileGemmLds), eight waves of 64 x 64.
+// adjacent, so they share its rows in one L2); 128 x 128 tiles with the
+// operands streamed straight into LDS (TileGemmLds), four waves of 64 x 64.
+// The ring is two stages of 32 KB, so two workgroups share a CU: with one
+// chunk in flight per workgroup, the chunk latency of one is covered by the
+// MFMAs of the other (measured: 20% faster than one 256 x 128 workgroup of
+// eight waves per CU, whose waves all meet at every chunk's barrier).
 // Writes the best (cosine, slot) of every pruned row within this kept tile,
 // or the slot itself when there is only one kept tile.
 template <int DT, int BM, int BN, int WM, int WN, int NS>
@@ -1004,8 +1008,8 @@ static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int3
                                int32_t *best_slot, int32_t *assign, hipStream_t st) {
     const int esz = (DT == kBF16) ? 2 : 4;
     const int ntm = (Mp + kGramTileM - 1) / kGramTileM, ntn = (N1 + kGramTileN - 1) / kGramTileN;
-    hipLaunchKernelGGL((gram_tile_kernel<DT, kGramTileM, kGramTileN, 4, 2, 2>),
-                       dim3(B * ntm * ntn), dim3(512), 0, st, (const char *)vis, Nv, d * esz, kept,
+    hipLaunchKernelGGL((gram_tile_kernel<DT, kGramTileM, kGramTileN, 2, 2, 2>),
+                       dim3(B * ntm * ntn), dim3(256), 0, st, (const char *)vis, Nv, d * esz, kept,
                        N1, pruned, Mp, invn, ntm, ntn, best_val, best_slot, assign);
     return hipGetLastError();
 }

@@ -45,7 +45,9 @@ hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, 
                               const float *invn, const int32_t *pruned, const int32_t *kept,
                               int32_t *assign, hipStream_t st);
 // Tile of the full-k Gram (pruned rows x kept rows) used for large inputs.
-constexpr int kGramTileM = 256, kGramTileN = 128;
+// The full-k form is chosen when the product holds at least 128 blocks of
+// kGramBigM x kGramTileN (enough work to keep every CU busy without split-k).
+constexpr int kGramTileM = 128, kGramTileN = 128, kGramBigM = 256;
 hipError_t launch_gram_tile(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                             int N1, const int32_t *pruned, int Mp, const float *invn,
                             float *best_val, int32_t *best_slot, int32_t *assign, hipStream_t st);
