@@ -272,71 +272,80 @@ __global__ __launch_bounds__(64 * NW) void cos_full_kernel(
 }
 
 // ----------------------------------------------------------------------------
-// center: grid (ceil(Nv / 64), B), 256 threads; 4 threads per token.
+// center: grid (ceil(Nv / 64), B), 256 threads.  Two phases, each with all of
+// its loads in flight before the first is used, so that a phase costs one
+// memory latency: the row means from the per-tile partial sums (4 threads per
+// row, each adding every fourth tile in tile order, the four partials then
+// added in order), and the max over the rows (4 threads per token).
 // ----------------------------------------------------------------------------
 constexpr int kCenNT = 256;
 constexpr int kCenTok = 64;
+constexpr int kCenU = 16;  // loads in flight per thread
+
+// base[t * stride] added over t = t0, t0 + step, ... < n, in that order
+// (n >= 1; the addresses of a block are clamped, so every load is valid).
+__device__ __forceinline__ float strided_sum(const float *__restrict__ base, size_t stride, int t0,
+                                             int step, int n) {
+    float s = 0.f;
+    for (int c = t0; c < n; c += step * kCenU) {
+        float v[kCenU];
+#pragma unroll
+        for (int u = 0; u < kCenU; ++u) v[u] = base[(size_t)min(c + u * step, n - 1) * stride];
+#pragma unroll
+        for (int u = 0; u < kCenU; ++u)
+            if (c + u * step < n) s += v[u];
+    }
+    return s;
+}
 
 __global__ __launch_bounds__(kCenNT) void center_kernel(const float *__restrict__ M,
                                                         const float *__restrict__ rowsum,
                                                         const int32_t *__restrict__ row_mask,
                                                         int njt, int Nt, int Nv,
                                                         float *__restrict__ p) {
-    extern __shared__ float mu[];  // [Nt]: row mean, or +inf for a row that is not an anchor
-    __shared__ float part[4][kCenTok];
+    // [0, Nt): row means; [Nt, 2 Nt): the same with +inf for rows that are
+    // not anchors (a row at +inf never wins the max)
+    extern __shared__ float mu[];
+    __shared__ float rpart[4][kCenTok];
     __shared__ int any_row;
     const int b = blockIdx.y, tid = threadIdx.x;
-    if (tid == 0) any_row = 0;
-    __syncthreads();
-    bool masked = false;  // whether this thread set any row to +inf
-    // Row means of M over all Nv tokens, from the per-tile partial sums
-    // (added in tile order).
-    for (int i = tid; i < Nt; i += kCenNT) {
-        const float *rs = rowsum + (size_t)b * njt * Nt + i;
+    if (tid == 0) any_row = row_mask ? 0 : 1;
+    for (int r0 = 0; r0 < Nt; r0 += kCenTok) {
+        const int i = r0 + (tid >> 2), q = tid & 3;
         float s = 0.f;
-        for (int t0 = 0; t0 < njt; t0 += 16) {
-            float v[16];
-#pragma unroll
-            for (int u = 0; u < 16; ++u) v[u] = rs[(size_t)min(t0 + u, njt - 1) * Nt];
-#pragma unroll
-            for (int u = 0; u < 16; ++u)
-                if (t0 + u < njt) s += v[u];
+        if (i < Nt) s = strided_sum(rowsum + (size_t)b * njt * Nt + i, Nt, q, 4, njt);
+        rpart[q][tid >> 2] = s;
+        __syncthreads();
+        if (tid < kCenTok && r0 + tid < Nt) {
+            const int ii = r0 + tid;
+            const float m = (((rpart[0][tid] + rpart[1][tid]) + rpart[2][tid]) + rpart[3][tid]) / (float)Nv;
+            const bool use = !row_mask || row_mask[(size_t)b * Nt + ii] != 0;
+            mu[ii] = m;
+            mu[Nt + ii] = use ? m : INFINITY;
+            if (use && row_mask) any_row = 1;
         }
-        const bool use = !row_mask || row_mask[(size_t)b * Nt + i] != 0;
-        mu[i] = use ? s / (float)Nv : INFINITY;
-        masked |= !use;
-        if (use) any_row = 1;
+        __syncthreads();
     }
-    __syncthreads();
     // an empty mask means every row
-    if (!any_row && masked) {
-        for (int i = tid; i < Nt; i += kCenNT) {
-            const float *rs = rowsum + (size_t)b * njt * Nt + i;
-            float s = 0.f;
-            for (int t0 = 0; t0 < njt; t0 += 16) {
-                float v[16];
-#pragma unroll
-                for (int u = 0; u < 16; ++u) v[u] = rs[(size_t)min(t0 + u, njt - 1) * Nt];
-#pragma unroll
-                for (int u = 0; u < 16; ++u)
-                    if (t0 + u < njt) s += v[u];
-            }
-            mu[i] = s / (float)Nv;
-        }
-    }
-    __syncthreads();
+    const float *mrow = (row_mask && any_row) ? mu + Nt : mu;
     const int jl = tid & (kCenTok - 1), g = tid / kCenTok;
     const int j = blockIdx.x * kCenTok + jl;
     float m = -INFINITY;
     if (j < Nv) {
         const float *col = M + (size_t)b * Nt * Nv + j;
-#pragma unroll 4
-        for (int i = g; i < Nt; i += 4) m = fmaxf(m, col[(size_t)i * Nv] - mu[i]);
+        for (int i0 = g; i0 < Nt; i0 += 4 * kCenU) {
+            float v[kCenU];
+#pragma unroll
+            for (int u = 0; u < kCenU; ++u) v[u] = col[(size_t)min(i0 + 4 * u, Nt - 1) * Nv];
+#pragma unroll
+            for (int u = 0; u < kCenU; ++u)
+                if (i0 + 4 * u < Nt) m = fmaxf(m, v[u] - mrow[i0 + 4 * u]);
+        }
     }
-    part[g][jl] = m;
+    rpart[g][jl] = m;
     __syncthreads();
     if (g == 0 && j < Nv)
-        p[(size_t)b * Nv + j] = fmaxf(fmaxf(part[0][jl], part[1][jl]), fmaxf(part[2][jl], part[3][jl]));
+        p[(size_t)b * Nv + j] = fmaxf(fmaxf(rpart[0][jl], rpart[1][jl]), fmaxf(rpart[2][jl], rpart[3][jl]));
 }
 
 // ----------------------------------------------------------------------------
@@ -981,7 +990,7 @@ hipError_t launch_cos_full(int dt, const void *vis, const void *anchors, int B, 
 hipError_t launch_center(const float *M, const float *rowsum, const int32_t *row_mask, int njt,
                          int B, int Nt, int Nv, float *p, hipStream_t st) {
     dim3 grid((Nv + kCenTok - 1) / kCenTok, B);
-    hipLaunchKernelGGL(center_kernel, grid, dim3(kCenNT), (size_t)Nt * sizeof(float), st, M, rowsum,
+    hipLaunchKernelGGL(center_kernel, grid, dim3(kCenNT), 2 * (size_t)Nt * sizeof(float), st, M, rowsum,
                        row_mask, njt, Nt, Nv, p);
     return hipGetLastError();
 }
