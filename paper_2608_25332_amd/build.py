@@ -23,6 +23,10 @@ HIP_FLAGS = [
     "-fvisibility=hidden",
     # keep the compiler from forming packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA results in ordinary VGPRs: the score kernels read every logit
+    # with vector instructions, which would otherwise copy each one out of
+    # the accumulation registers first
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     "-Wall",
     "-Wno-unused-result",
 ]

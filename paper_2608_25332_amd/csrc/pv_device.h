@@ -75,6 +75,36 @@ __device__ __forceinline__ f32x4_t mma16<kF32>(uint4 a, uint4 b, f32x4_t acc) {
 __device__ __forceinline__ uint4 ld16(const void *p) { return *reinterpret_cast<const uint4 *>(p); }
 __device__ __forceinline__ void st16(void *p, uint4 v) { *reinterpret_cast<uint4 *>(p) = v; }
 
+// 2^x on the transcendental unit, without the library's range reduction for
+// results below the smallest normal float (they flush to 0, which no softmax
+// sum here can notice next to its maximum term, 1).
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// Lane exchange within a row of 16 lanes through DPP (no LDS round trip).
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+// Maximum and sum over the 16 lanes of a row (lanes 16 r .. 16 r + 15), left
+// in every lane of the row.  Partners: lane ^ 1 and lane ^ 2 (quad
+// permutations), then the mirror within 8 and within 16 lanes, which after
+// the first steps hold the same values as lane ^ 4 and lane ^ 8: the sums
+// pair up as an xor butterfly over 1, 2, 4, 8 does, and give its bits.
+__device__ __forceinline__ float row16_max(float x) {
+    x = fmaxf(x, dpp_f32<0xB1>(x));   // quad_perm [1, 0, 3, 2]
+    x = fmaxf(x, dpp_f32<0x4E>(x));   // quad_perm [2, 3, 0, 1]
+    x = fmaxf(x, dpp_f32<0x141>(x));  // row_half_mirror
+    x = fmaxf(x, dpp_f32<0x140>(x));  // row_mirror
+    return x;
+}
+__device__ __forceinline__ float row16_sum(float x) {
+    x += dpp_f32<0xB1>(x);
+    x += dpp_f32<0x4E>(x);
+    x += dpp_f32<0x141>(x);
+    x += dpp_f32<0x140>(x);
+    return x;
+}
+
 // Order-preserving 32-bit key of a float: larger float <=> larger key.
 // -0 is mapped to the key of +0 so that the two tie.
 __device__ __forceinline__ uint32_t order_key(float f) {

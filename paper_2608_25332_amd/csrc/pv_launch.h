@@ -14,6 +14,12 @@ constexpr int kMaxHeadArgs = 512;
 struct HeadArgs {
     int32_t h[kMaxHeadArgs];
 };
+// The same list one byte per entry (heads < 256), for launches over many
+// (head, sample) pairs: entry i is byte i % 4 of word i / 4.
+constexpr int kMaxHeadArgs8 = 2048;
+struct HeadArgs8 {
+    uint32_t w[kMaxHeadArgs8 / 4];
+};
 
 // ---- pruning before the LLM (Sec. 4.3)
 constexpr int kSplitTile = 64;  // tile edge of the split-k products

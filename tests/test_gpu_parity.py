@@ -353,6 +353,67 @@ def test_head_aware_edges(B, H, Nt, N, hd, nh, budget, dt):
         check_kept(kept[b], ref_v[b], budget, dt)
 
 
+STREAM_CASES = [
+    # (B, H, Nt, N, hd, heads per sample, budget, dtype): at least 512
+    # (head, sample) pairs, so the host-list call runs the persistent form
+    (160, 8, 64, 192, 128, 4, 64, "bf16"),
+    (300, 4, 40, 130, 64, 2, 20, "bf16"),    # ragged rows and keys, 2 workgroups per CU
+    (130, 8, 20, 100, 64, 4, 30, "f32"),
+    (600, 4, 64, 192, 128, 4, 64, "bf16"),   # 2400 pairs: two launches
+    (512, 2, 1, 1, 128, 1, 1, "bf16"),       # one row, one key
+]
+
+
+@pytest.mark.parametrize("B,H,Nt,N,hd,nh,budget,dt", STREAM_CASES)
+def test_head_aware_stream_form(B, H, Nt, N, hd, nh, budget, dt):
+    """The persistent form (host head lists, many pairs) gives the bits of
+    the one-workgroup-per-pair form (device head lists) and matches the
+    oracle."""
+    from paper_2608_25332_amd import provip
+    _say(f"[head-stream] B={B} H={H} Nt={Nt} N={N} hd={hd} nh={nh} budget={budget} {dt}")
+    rng = np.random.default_rng(B * 31 + N)
+    q = (rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32)
+    k = (rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32)
+    if dt == "bf16":
+        q, k = W.bf16_round(q), W.bf16_round(k)
+    heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+    qd, kd = to_dev(q, dt), to_dev(k, dt)
+    a = provip.pv_prune_head_aware(qd, kd, heads, budget)
+    b = provip.pv_prune_head_aware(qd, kd, torch.from_numpy(heads).to("cuda:0"), budget)
+    torch.cuda.synchronize()
+    assert torch.equal(a["score"], b["score"]) and torch.equal(a["kept"], b["kept"])
+    sel = np.arange(0, B, max(1, B // 40))  # the oracle on a spread of samples
+    _, ref_v = oracle.head_aware(q[sel], k[sel], heads[sel], budget)
+    v, kept = to_host(a["score"])[sel], to_host(a["kept"])[sel]
+    assert rel_err(v, ref_v) <= TOL[dt], rel_err(v, ref_v)
+    for i in range(len(sel)):
+        check_kept(kept[i], ref_v[i], budget, dt)
+
+
+def test_head_aware_stream_form_in_model():
+    """The in-model domain (row log-sum-exps through LDS) on the persistent
+    form, against the oracle."""
+    from paper_2608_25332_amd import provip
+    rng = np.random.default_rng(21)
+    B, H, Nt, N, hd, nh = 136, 8, 64, 192, 128, 4
+    q = W.bf16_round((rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32))
+    k = W.bf16_round((rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32))
+    heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+    # log-sum-exp of each row's scaled logits over 50 synthetic non-visual keys
+    ko = rng.standard_normal((B, H, 50, hd)) * 1.5
+    lg = np.einsum("bhid,bhjd->bhij", q.astype(np.float64), ko) / np.sqrt(hd)
+    mx = lg.max(-1, keepdims=True)
+    lse = (mx[..., 0] + np.log(np.exp(lg - mx).sum(-1))).astype(np.float32)
+    r = provip.pv_prune_head_aware(to_dev(q, "bf16"), to_dev(k, "bf16"), heads, 30,
+                                   row_lse=torch.from_numpy(lse).to("cuda:0"))
+    torch.cuda.synchronize()
+    v, kept = to_host(r["score"]), to_host(r["kept"])
+    ref_kept, ref_v = oracle.head_aware_in_model(q, k, heads, lse.astype(np.float64), 30)
+    assert rel_err(v, ref_v) <= TOL["bf16"], rel_err(v, ref_v)
+    for b in range(B):
+        check_kept(kept[b], ref_v[b], 30, "bf16")
+
+
 def test_head_aware_duplicate_keys_tie():
     """Exact duplicate keys get bit-identical v, and the lower index wins."""
     rng = np.random.default_rng(9)
