@@ -359,7 +359,7 @@ int head_impl(const void *q, const void *k, const int32_t *heads, const int32_t 
         return PV_ERR_HIP;
     const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
     if (!tr.launch("score_select", [&] {
-            const int parts = pv::score_uses_head_form(dt, B, n_heads, Nt, N, hd) ? 1 : P.nrb;
+            const int parts = pv::score_uses_head_form(dt, B, H, n_heads, Nt, N, hd) ? 1 : P.nrb;
             return pv::launch_score_select(P.partial, B, n_heads * parts, N, inv_norm, v, budget,
                                            kept, st);
         }))

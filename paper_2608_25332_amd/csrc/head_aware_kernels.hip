@@ -510,7 +510,7 @@ __device__ __forceinline__ void head_chunk_logits(const char *kb, const uint4 (&
 
 template <int DT, int NKS>
 __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
-    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
+    const char *__restrict__ q, const char *__restrict__ k, HeadArgs8 heads,
     const int32_t *__restrict__ heads_dev, int head_src, const float *__restrict__ row_lse, int b0,
     int H, int Nt, int N, int n_heads, float scale_log2e, float *__restrict__ partial) {
     using S = ScoreStage<NKS>;
@@ -527,7 +527,10 @@ __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     int h;
     if (head_src == kHeadsDevice) h = min(max(heads_dev[(size_t)b * n_heads + hi], 0), H - 1);
-    else h = heads.h[bl * n_heads + hi];
+    else {
+        const int e = bl * n_heads + hi;
+        h = (int)((heads.w[e >> 2] >> ((e & 3) * 8)) & 0xFFu);
+    }
     const char *qb = q + ((size_t)b * H + h) * Nt * S::RB;
     const char *kb = k + ((size_t)b * H + h) * N * S::RB;
     const int nch = (N + kScoreCK - 1) / kScoreCK;  // <= MAXC (host-checked)
@@ -616,198 +619,6 @@ __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
     float *out = partial + ((size_t)b * n_heads + hi) * N;
     for (int j = tid; j < N; j += kScoreNT)
         out[j] = ((colpart[0][j] + colpart[1][j]) + colpart[2][j]) + colpart[3][j];
-}
-
-// ----------------------------------------------------------------------------
-// score_stream: the whole-head form as a persistent kernel, for batches with
-// many (head, sample) pairs.  One workgroup per CU takes the pairs
-// blockIdx.x, blockIdx.x + gridDim.x, ... and keeps the next pair's query
-// block and keys in flight (two LDS buffers) while it scores the current one,
-// so that the loads of a CU never stop; a workgroup that loads, scores and
-// exits leaves its CU's memory pipe idle for the scoring and the next
-// dispatch.  The per-pair arithmetic is score_head's, in the same order, so
-// the two forms give identical bits.
-// ----------------------------------------------------------------------------
-constexpr int kStreamMaxChunks = 3;  // keys <= 192
-
-// Largest buffer of score_stream: 64 query rows (whole 4 KiB groups of
-// pieces), three key chunks and four copies of 64 row log-sum-exps.
-template <int NKS>
-struct StreamBuf {
-    static constexpr int QB = ((kHeadMaxRows * ScoreStage<NKS>::RB + 4095) / 4096) * 4096;
-    static constexpr int BYTES = QB + kStreamMaxChunks * ScoreStage<NKS>::STAGE + 4 * 256;
-};
-
-template <int DT, int NKS>
-__global__ __launch_bounds__(kScoreNT) void score_stream_kernel(
-    const char *__restrict__ q, const char *__restrict__ k, HeadArgs8 heads,
-    const float *__restrict__ row_lse, int b0, int n_items, int H, int Nt, int N, int n_heads,
-    float scale_log2e, float *__restrict__ partial) {
-    using S = ScoreStage<NKS>;
-    constexpr int MAXC = kStreamMaxChunks;
-    // buffer u of the two: the query rows (nq 1 KiB pieces, rows past Nt
-    // repeat the last one), then nch key chunks (static: at most 130 KiB)
-    __shared__ __attribute__((aligned(16))) char sbuf[2 * StreamBuf<NKS>::BYTES];
-    __shared__ float colpart[4][MAXC * kScoreCK];
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int nch = (N + kScoreCK - 1) / kScoreCK;  // <= MAXC (host-checked)
-    // the head of pair it, read from the list's 32-bit words (a scalar load:
-    // a byte load would be a vector load, and waiting for it would also wait
-    // for the loads in flight)
-    auto head_at = [&](int it) -> int {
-        const uint32_t w = heads.w[it >> 2];
-        return (int)((w >> ((it & 3) * 8)) & 0xFFu);
-    };
-    const int nq = ((Nt + 15) / 16) * 16 * S::RB / 1024;
-    const int qpw = (nq + 3) / 4;  // query pieces per wave (the last repeated to even out)
-    // per buffer: query pieces, key chunks, then (with row_lse) one copy of
-    // the pair's 64 row log-sum-exps per wave
-    const int ubytes = qpw * 4 * 1024 + nch * S::STAGE + (row_lse ? 4 * 256 : 0);
-    auto qbuf = [&](int u) { return sbuf + u * ubytes; };
-    auto kbuf = [&](int u, int ch) { return sbuf + u * ubytes + qpw * 4 * 1024 + ch * S::STAGE; };
-    auto lbuf = [&](int u) { return sbuf + u * ubytes + qpw * 4 * 1024 + nch * S::STAGE + wave * 256; };
-    // Every wave issues the same number of direct-to-LDS loads per pair
-    // (qpw + nch * IPW, plus one with row_lse), so one wait count names "all
-    // but the next pair".
-    auto issue = [&](int it, int u) {
-        const int b = b0 + it / n_heads, h = head_at(it);
-        if (row_lse)
-            lds_dma4(row_lse + ((size_t)b * H + h) * Nt + min(lane, Nt - 1), lbuf(u));
-        const char *qb = q + ((size_t)b * H + h) * Nt * S::RB;
-        const char *kb = k + ((size_t)b * H + h) * N * S::RB;
-        for (int t = 0; t < qpw; ++t) {
-            const int pce = min(wave + 4 * t, nq - 1);
-            const int off = pce * 1024 + lane * 16;
-            lds_dma16(qb + (size_t)min(off / S::RB, Nt - 1) * S::RB + off % S::RB,
-                      qbuf(u) + pce * 1024);
-        }
-#pragma unroll
-        for (int ch = 0; ch < MAXC; ++ch) {
-            if (ch < nch) {
-#pragma unroll
-                for (int t = 0; t < S::IPW; ++t) {
-                    const int pos = (wave * S::IPW + t) * 64 + lane;
-                    const int r = pos / S::PPR, slot = pos % S::PPR;
-                    const int row = min(ch * kScoreCK + r, N - 1);  // past the end: last key
-                    lds_dma16(kb + (size_t)row * S::RB + ((slot ^ (r & S::SWZ)) << 4),
-                              kbuf(u, ch) + (wave * S::IPW + t) * 1024);
-                }
-            }
-        }
-    };
-    const int per_pair = qpw + nch * S::IPW + (row_lse ? 1 : 0);  // loads per wave per pair (<= 17)
-    int it = blockIdx.x;
-    if (it < n_items) issue(it, 0);
-    if (it + (int)gridDim.x < n_items) issue(it + gridDim.x, 1);
-    const bool rows_live = wave * 16 < Nt;  // uniform: this wave has rows to score
-    for (int u = 0; it < n_items; it += gridDim.x, u ^= 1) {
-        const bool more = it + (int)gridDim.x < n_items;
-        // this pair's loads are done once at most the next pair's are in
-        // flight (loads retire in order; the stores of the previous pair, if
-        // still in flight, only make the wait stricter)
-        if (more) {
-            switch (per_pair) {
-#define PV_WAIT_CASE(n) \
-    case n:             \
-        wait_vmcnt<n>(); \
-        break;
-                PV_WAIT_CASE(1) PV_WAIT_CASE(2) PV_WAIT_CASE(3) PV_WAIT_CASE(4) PV_WAIT_CASE(5)
-                PV_WAIT_CASE(6) PV_WAIT_CASE(7) PV_WAIT_CASE(8) PV_WAIT_CASE(9) PV_WAIT_CASE(10)
-                PV_WAIT_CASE(11) PV_WAIT_CASE(12) PV_WAIT_CASE(13) PV_WAIT_CASE(14)
-                PV_WAIT_CASE(15) PV_WAIT_CASE(16) PV_WAIT_CASE(17)
-#undef PV_WAIT_CASE
-                default: wait_vmcnt<0>();
-            }
-        } else {
-            wait_vmcnt<0>();
-        }
-        bare_barrier();  // the pair is in LDS for every wave
-
-        f32x4_t keep[MAXC][4];
-        if (rows_live) {
-            uint4 qf[NKS];
-            const int qr = wave * 16 + (lane & 15);
-#pragma unroll
-            for (int s = 0; s < NKS; ++s)
-                qf[s] = lds_read16(qbuf(u) + qr * S::RB + (s * 4 + (lane >> 4)) * 16);
-            lds_wait();
-#pragma unroll
-            for (int s = 0; s < NKS; ++s) lds_after_wait(qf[s]);
-#pragma unroll
-            for (int ch = 0; ch < MAXC; ++ch)
-                if (ch < nch) head_chunk_logits<DT, NKS>(kbuf(u, ch), qf, lane, keep[ch]);
-        }
-        // Row statistics (registers and lane exchanges only), finished
-        // before the next loads are issued: a load of row_lse after them
-        // would make the compiler wait for those too.
-        const int b = b0 + it / n_heads, hi = it % n_heads;
-        float m[4], il[4];
-        if (rows_live) head_row_max<MAXC>(keep, nch, N, lane, scale_log2e, m);
-        float l[4] = {0.f, 0.f, 0.f, 0.f};
-        if (rows_live) {
-            head_row_exp<MAXC>(keep, nch, scale_log2e, m, l);
-#pragma unroll
-            for (int i = 0; i < 4; ++i) l[i] = row16_sum(l[i]);
-        }
-        float lse[4] = {0.f, 0.f, 0.f, 0.f};
-        if (rows_live && row_lse) {
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                lse[i] = lds_read4(reinterpret_cast<const float *>(lbuf(u)) + wave * 16 + (lane >> 4) * 4 + i);
-            lds_wait();
-#pragma unroll
-            for (int i = 0; i < 4; ++i) lse[i] = lds_after_wait4(lse[i]);
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int row = wave * 16 + (lane >> 4) * 4 + i;
-            float ll = l[i];
-            if (rows_live && row_lse) ll += exp2_hw(lse[i] * 1.4426950408889634f - m[i]);
-            il[i] = (rows_live && row < Nt) ? 1.0f / ll : 0.f;  // masked rows add nothing
-        }
-        bare_barrier();  // buffer u has been read by every wave
-        if (it + 2 * (int)gridDim.x < n_items) issue(it + 2 * gridDim.x, u);
-
-        // Column sums of this wave's rows, exchanged through LDS with inline
-        // reads and writes: the compiler would otherwise wait for the loads
-        // just issued before touching LDS.
-        // (all sums first, then the writes: each inline write orders the
-        // exchanges around it)
-        float csum[MAXC][4];
-#pragma unroll
-        for (int ch = 0; ch < MAXC; ++ch) {
-#pragma unroll
-            for (int kq = 0; kq < 4; ++kq) {
-                float cs = 0.f;
-                if (rows_live) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) cs += keep[ch][kq][i] * il[i];
-                }
-                cs += __shfl_xor(cs, 16, 64);
-                cs += __shfl_xor(cs, 32, 64);
-                csum[ch][kq] = cs;
-            }
-        }
-#pragma unroll
-        for (int ch = 0; ch < MAXC; ++ch)
-            if (ch < nch && lane < 16)
-#pragma unroll
-                for (int kq = 0; kq < 4; ++kq)
-                    lds_write4(&colpart[wave][ch * kScoreCK + kq * 16 + lane], csum[ch][kq]);
-        lds_wait();
-        bare_barrier();  // every wave's column sums are in LDS
-        float *out = partial + ((size_t)b * n_heads + hi) * N;
-        for (int j = tid; j < N; j += kScoreNT) {
-            const float c0 = lds_read4(&colpart[0][j]), c1 = lds_read4(&colpart[1][j]);
-            const float c2 = lds_read4(&colpart[2][j]), c3 = lds_read4(&colpart[3][j]);
-            lds_wait();
-            out[j] = ((lds_after_wait4(c0) + lds_after_wait4(c1)) + lds_after_wait4(c2)) +
-                     lds_after_wait4(c3);
-        }
-        // colpart is rewritten only after the next pair's first barrier,
-        // which every wave reaches with its reads above complete
-    }
 }
 
 constexpr int kSelU = 16;
@@ -943,49 +754,19 @@ static hipError_t score_dt(int nks, const ScoreLaunch &a) {
 
 template <int DT, int NKS>
 static hipError_t score_head_go(const ScoreLaunch &a) {
-    const int per_launch = a.src == kHeadsArg ? kMaxHeadArgs / a.n_heads : a.B;
-    HeadArgs ha;
+    const int per_launch = a.src == kHeadsArg ? kMaxHeadArgs8 / a.n_heads : a.B;
+    HeadArgs8 ha;
     for (int b0 = 0; b0 < a.B; b0 += per_launch) {
         const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
-        for (int i = 0; i < kMaxHeadArgs; ++i)
-            ha.h[i] = (a.src == kHeadsArg && i < nb * a.n_heads)
-                          ? a.heads_host[(size_t)b0 * a.n_heads + i] : 0;
+        for (int i = 0; i < kMaxHeadArgs8 / 4; ++i) ha.w[i] = 0u;
+        if (a.src == kHeadsArg)
+            for (int i = 0; i < nb * a.n_heads; ++i)
+                ha.w[i >> 2] |= (uint32_t)(a.heads_host[(size_t)b0 * a.n_heads + i] & 0xFF)
+                                << ((i & 3) * 8);
         const size_t kbytes = (size_t)((a.N + kScoreCK - 1) / kScoreCK) * ScoreStage<NKS>::STAGE;
         hipLaunchKernelGGL((score_head_kernel<DT, NKS>), dim3(a.n_heads * nb), dim3(kScoreNT),
                            kbytes, a.st, (const char *)a.q, (const char *)a.k, ha, a.heads_dev, a.src,
                            a.row_lse, b0, a.H, a.Nt, a.N, a.n_heads, a.sl2e, a.partial);
-        const hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-    }
-    return hipSuccess;
-}
-
-template <int DT, int NKS>
-static hipError_t score_stream_go(const ScoreLaunch &a) {
-    using S = ScoreStage<NKS>;
-    const int nch = (a.N + kScoreCK - 1) / kScoreCK;
-    const int nq = ((a.Nt + 15) / 16) * 16 * S::RB / 1024;
-    const size_t ubytes = (size_t)((nq + 3) / 4) * 4 * 1024 + (size_t)nch * S::STAGE +
-                          (a.row_lse ? 4 * 256 : 0);
-    if (ubytes > (size_t)StreamBuf<NKS>::BYTES) return hipErrorInvalidValue;
-    const size_t lds = 2 * (size_t)StreamBuf<NKS>::BYTES + sizeof(float) * 4 * kStreamMaxChunks * kScoreCK;
-    int dev = 0, ncu = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        ncu < 1)
-        ncu = 256;
-    const int per_cu = (int)((size_t)kScoreLdsCap / lds) > 0 ? (int)((size_t)kScoreLdsCap / lds) : 1;
-    const int per_launch = kMaxHeadArgs8 / a.n_heads;  // samples per launch
-    HeadArgs8 ha;
-    for (int b0 = 0; b0 < a.B; b0 += per_launch) {
-        const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
-        const int items = nb * a.n_heads;
-        for (int i = 0; i < kMaxHeadArgs8 / 4; ++i) ha.w[i] = 0u;
-        for (int i = 0; i < items; ++i)
-            ha.w[i >> 2] |= (uint32_t)(a.heads_host[(size_t)b0 * a.n_heads + i] & 0xFF) << ((i & 3) * 8);
-        const int grid = items < ncu * per_cu ? items : ncu * per_cu;
-        hipLaunchKernelGGL((score_stream_kernel<DT, NKS>), dim3(grid), dim3(kScoreNT), 0, a.st, (const char *)a.q, (const char *)a.k, ha, a.row_lse,
-                           b0, items, a.H, a.Nt, a.N, a.n_heads, a.sl2e, a.partial);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -1004,18 +785,10 @@ static hipError_t score_any(int dt, int hd, ScoreLaunch a) {
 // The whole-head form pays once there are enough (head, sample) pairs to
 // fill the chip (measured: from 128 pairs it is faster, below it the
 // 16-row blocks spread over more CUs and win by ~0.5 us).
-bool score_uses_head_form(int dt, int B, int n_heads, int Nt, int N, int hd) {
+bool score_uses_head_form(int dt, int B, int H, int n_heads, int Nt, int N, int hd) {
     const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
-    return (nks == 2 || nks == 4) && Nt <= kHeadMaxRows && N <= kHeadMaxChunks * kScoreCK &&
-           (long long)B * n_heads >= 128;
-}
-
-// The persistent form of it: host head lists of heads < 256, at most 192
-// keys, and at least two (head, sample) pairs per CU of the chip.
-static bool score_uses_stream_form(int dt, int B, int H, int n_heads, int Nt, int N, int hd,
-                                   bool host_list) {
-    return host_list && H <= 256 && N <= kStreamMaxChunks * kScoreCK &&
-           score_uses_head_form(dt, B, n_heads, Nt, N, hd) && (long long)B * n_heads >= 512;
+    return (nks == 2 || nks == 4) && H <= 256 && Nt <= kHeadMaxRows &&
+           N <= kHeadMaxChunks * kScoreCK && (long long)B * n_heads >= 128;
 }
 
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
@@ -1024,13 +797,7 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const int3
                                 hipStream_t st) {
     ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg, nullptr,
                   row_lse, B, H, Nt, N, n_heads, 0.f, partial, st};
-    if (score_uses_stream_form(dt, B, H, n_heads, Nt, N, hd, heads_dev == nullptr)) {
-        a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
-        const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
-        if (dt == kBF16) return nks == 2 ? score_stream_go<kBF16, 2>(a) : score_stream_go<kBF16, 4>(a);
-        return nks == 2 ? score_stream_go<kF32, 2>(a) : score_stream_go<kF32, 4>(a);
-    }
-    if (score_uses_head_form(dt, B, n_heads, Nt, N, hd)) {
+    if (score_uses_head_form(dt, B, H, n_heads, Nt, N, hd)) {
         a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
         const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
         if (dt == kBF16) return nks == 2 ? score_head_go<kBF16, 2>(a) : score_head_go<kBF16, 4>(a);

@@ -14,12 +14,14 @@ constexpr int kMaxHeadArgs = 512;
 struct HeadArgs {
     int32_t h[kMaxHeadArgs];
 };
-// The same list one byte per entry (heads < 256), for launches over many
-// (head, sample) pairs: entry i is byte i % 4 of word i / 4.
+// The same list one byte per entry (heads < 256): entry i is byte i % 4 of
+// word i / 4.  Four times the entries in the same argument bytes, so a
+// large batch of (head, sample) pairs takes few launches.
 constexpr int kMaxHeadArgs8 = 2048;
 struct HeadArgs8 {
     uint32_t w[kMaxHeadArgs8 / 4];
 };
+
 
 // ---- pruning before the LLM (Sec. 4.3)
 constexpr int kSplitTile = 64;  // tile edge of the split-k products
@@ -88,7 +90,7 @@ hipError_t launch_text_rank(const float *G, int B, int Nt, float *r, int32_t *ma
 // Whether the score runs one workgroup per (head, sample) (score_head) and
 // writes one row of column sums per (sample, head) instead of one per
 // 16-row block.
-bool score_uses_head_form(int dt, int B, int n_heads, int Nt, int N, int hd);
+bool score_uses_head_form(int dt, int B, int H, int n_heads, int Nt, int N, int hd);
 // row_lse [B][H][Nt] (may be NULL): log-sum-exp of each row's scaled logits
 // over the non-visual keys, which join the softmax normaliser.
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,

@@ -55,10 +55,6 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 __device__ __forceinline__ void lds_dma16(const void *g, char *lds) {
     __builtin_amdgcn_global_load_lds(g, (lds_void_t *)lds, 16, 0, 0);
 }
-// The same with 4 bytes per lane (to lds + 4 * lane).
-__device__ __forceinline__ void lds_dma4(const void *g, char *lds) {
-    __builtin_amdgcn_global_load_lds(g, (lds_void_t *)lds, 4, 0, 0);
-}
 typedef unsigned lds_u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ uint4 lds_read16(const char *p) {
@@ -81,25 +77,6 @@ __device__ __forceinline__ void lds_after_wait(uint4 &v) {
     lds_u32x4_t r = {v.x, v.y, v.z, v.w};
     asm volatile("" : "+v"(r));
     v = uint4{r.x, r.y, r.z, r.w};
-}
-
-// 4-byte LDS read and write as inline assembly, for LDS traffic issued while
-// direct-to-LDS loads are in flight (the compiler would drain those loads
-// before an ordinary LDS access).  A read's value is used only after
-// lds_wait(), through lds_after_wait4.
-__device__ __forceinline__ float lds_read4(const float *p) {
-    float r;
-    const unsigned addr = (unsigned)(uintptr_t)p;
-    asm volatile("ds_read_b32 %0, %1" : "=v"(r) : "v"(addr) : "memory");
-    return r;
-}
-__device__ __forceinline__ void lds_write4(float *p, float v) {
-    const unsigned addr = (unsigned)(uintptr_t)p;
-    asm volatile("ds_write_b32 %0, %1" ::"v"(addr), "v"(v) : "memory");
-}
-__device__ __forceinline__ float lds_after_wait4(float v) {
-    asm volatile("" : "+v"(v));
-    return v;
 }
 
 template <int DT, int BM, int BN, int WM, int WN, int NSTAGE>

@@ -325,7 +325,7 @@ HEAD_EDGE = [
     (1, 2, 16, 300, 256, 1, 30, "f32"),       # widest head, streamed twice
     (2, 3, 40, 70, 160, 2, 9, "bf16"),
     (1, 2, 33, 257, 224, 2, 64, "f32"),
-    (40, 16, 16, 64, 64, 16, 20, "bf16"),     # 640 head-list entries: two launches
+    (40, 16, 80, 64, 64, 16, 20, "bf16"),     # 640 head-list entries of 16-row blocks: two launches
     (1, 2, 16, 9000, 256, 1, 500, "f32"),     # column sums flushed from registers
     (1, 1, 9, 12100, 224, 1, 900, "f32"),     # the same, 14 pieces per key row
     # one workgroup per (head, sample) once there are >= 128 of them
@@ -353,24 +353,24 @@ def test_head_aware_edges(B, H, Nt, N, hd, nh, budget, dt):
         check_kept(kept[b], ref_v[b], budget, dt)
 
 
-STREAM_CASES = [
-    # (B, H, Nt, N, hd, heads per sample, budget, dtype): at least 512
-    # (head, sample) pairs, so the host-list call runs the persistent form
+LARGE_BATCH_CASES = [
+    # (B, H, Nt, N, hd, heads per sample, budget, dtype): batches of 520 to
+    # 2400 (head, sample) pairs
     (160, 8, 64, 192, 128, 4, 64, "bf16"),
     (300, 4, 40, 130, 64, 2, 20, "bf16"),    # ragged rows and keys, 2 workgroups per CU
     (130, 8, 20, 100, 64, 4, 30, "f32"),
-    (600, 4, 64, 192, 128, 4, 64, "bf16"),   # 2400 pairs: two launches
+    (600, 4, 64, 192, 128, 4, 64, "bf16"),   # 2400 pairs: two launches of host lists
     (512, 2, 1, 1, 128, 1, 1, "bf16"),       # one row, one key
 ]
 
 
-@pytest.mark.parametrize("B,H,Nt,N,hd,nh,budget,dt", STREAM_CASES)
-def test_head_aware_stream_form(B, H, Nt, N, hd, nh, budget, dt):
-    """The persistent form (host head lists, many pairs) gives the bits of
-    the one-workgroup-per-pair form (device head lists) and matches the
+@pytest.mark.parametrize("B,H,Nt,N,hd,nh,budget,dt", LARGE_BATCH_CASES)
+def test_head_aware_large_batches(B, H, Nt, N, hd, nh, budget, dt):
+    """Large batches: host head lists (several launches of bounded lists)
+    give the bits of device head lists (one launch), and both match the
     oracle."""
     from paper_2608_25332_amd import provip
-    _say(f"[head-stream] B={B} H={H} Nt={Nt} N={N} hd={hd} nh={nh} budget={budget} {dt}")
+    _say(f"[head-large] B={B} H={H} Nt={Nt} N={N} hd={hd} nh={nh} budget={budget} {dt}")
     rng = np.random.default_rng(B * 31 + N)
     q = (rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32)
     k = (rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32)
@@ -390,9 +390,9 @@ def test_head_aware_stream_form(B, H, Nt, N, hd, nh, budget, dt):
         check_kept(kept[i], ref_v[i], budget, dt)
 
 
-def test_head_aware_stream_form_in_model():
-    """The in-model domain (row log-sum-exps through LDS) on the persistent
-    form, against the oracle."""
+def test_head_aware_large_batch_in_model():
+    """The in-model domain on a batch of 544 (head, sample) pairs, against the
+    oracle."""
     from paper_2608_25332_amd import provip
     rng = np.random.default_rng(21)
     B, H, Nt, N, hd, nh = 136, 8, 64, 192, 128, 4
