@@ -704,11 +704,11 @@ static hipError_t score_go(const ScoreLaunch &a) {
 }
 
 // Logit blocks held in registers between the two passes: the smallest of 1,
-// 2, 4, 8, 16 chunks that covers the keys, within a register budget that
+// 2, 4, 8, 16, 32 chunks that covers the keys, within a register budget that
 // shrinks as the head width grows; otherwise the keys are streamed twice
 // (MAXC = 0).
 template <int NKS>
-constexpr int score_maxc_cap() { return NKS <= 4 ? 16 : (NKS <= 8 ? 8 : 4); }
+constexpr int score_maxc_cap() { return NKS <= 4 ? 32 : (NKS <= 8 ? 8 : 4); }
 
 template <int DT, int NKS, bool CONF>
 static hipError_t score_nks(const ScoreLaunch &a) {
@@ -724,6 +724,7 @@ static hipError_t score_nks(const ScoreLaunch &a) {
         PV_MAXC_CASE(4)
         PV_MAXC_CASE(8)
         PV_MAXC_CASE(16)
+        PV_MAXC_CASE(32)
 #undef PV_MAXC_CASE
         return score_go<DT, NKS, 0, false>(a);
     }
