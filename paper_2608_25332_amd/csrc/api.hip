@@ -72,10 +72,13 @@ long long n_tiles(int rows_m, int rows_n, int B, int t) {
     return (long long)((rows_m + t - 1) / t) * ((rows_n + t - 1) / t) * B;
 }
 
-// k slices of a split-k product: about three workgroups per CU (256 CUs; three
-// 48 KB LDS rings fit one CU), at least four 128-byte chunks in every slice.
-int pick_slices(long long tiles, int nchunks) {
-    long long ks = (768 + tiles / 2) / tiles;
+// k slices of a split-k product: about `target` workgroups (768: three per CU
+// of 256, as three 48 KB LDS rings fit one CU; 512 for the 64 KB rings of the
+// wide cosine tiles), at least four 128-byte chunks in every slice.
+int pick_slices(long long tiles, int nchunks, int target = 768, bool whole_round = false) {
+    // whole_round: no more workgroups than target (a second partial round of
+    // workgroups would cost a whole extra round of the ring)
+    long long ks = whole_round ? target / tiles : (target + tiles / 2) / tiles;
     const long long max_ks = nchunks / 4 > 1 ? nchunks / 4 : 1;
     if (ks > max_ks) ks = max_ks;
     if (ks < 1) ks = 1;
@@ -101,7 +104,10 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
     DedupPlan P;
     P.nch = d * esz / 128;
     const int T = pv::kSplitTile;
-    P.ks_cos = pick_slices(n_tiles(Nv, Nt, B, T), P.nch);
+    // wide cosine tiles: two workgroups per CU (512 for the chip)
+    P.ks_cos = pv::cos_uses_wide_tiles(Nt, Nv)
+                   ? pick_slices(n_tiles(Nv, Nt, B, pv::kWideTile), P.nch, 512, true)
+                   : pick_slices(n_tiles(Nv, Nt, B, T), P.nch);
     P.cos_full = pv::cos_use_full(B, Nv, Nt, d * esz);
     P.njt = P.cos_full ? pv::cos_full_row_tiles(Nv) : pv::cos_row_tiles(Nv);
     P.Mp = Nv - budget;
@@ -415,7 +421,8 @@ struct TextPlan {
 TextPlan plan_text(void *ws, int B, int Nt, int d, int esz) {
     TextPlan P;
     const int nch = d * esz / 128;
-    P.ks = pick_slices(n_tiles(Nt, Nt, B, pv::kSplitTile), nch);
+    P.ks = pv::cos_uses_wide_tiles(Nt, Nt) ? pick_slices(n_tiles(Nt, Nt, B, pv::kWideTile), nch, 512, true)
+                                            : pick_slices(n_tiles(Nt, Nt, B, pv::kSplitTile), nch);
     Carve c(ws);
     P.part = c.take<float>((size_t)P.ks * B * Nt * Nt);
     P.ssv = c.take<float>((size_t)P.ks * B * Nt);

@@ -44,12 +44,17 @@ using PTile = TileGemmLds<DT, kPT, kPT, 2, 2, NS>;
 // anchor rows).  Writes partial dot products part[ks][b][Nt][Nv] and partial
 // sums of squares of the token rows ssv[ks][b][Nv] and anchor rows
 // ssa[ks][b][Nt].
-template <int DT, int NS>
+//
+// Tiles of BT x BT (four waves of BT/2 x BT/2): 64 with a three-stage ring
+// (three workgroups per CU), or 128 with two stages (two per CU) when there
+// are more than 64 anchors, which then halves the rows each CU loads per
+// output.
+template <int DT, int NS, int BT>
 __global__ __launch_bounds__(256) void cos_partial_kernel(
     const char *__restrict__ vis, const char *__restrict__ anchors, int B, int Nv, int Nt,
     int d_bytes, int njt, int nit, int KS, float *__restrict__ part, float *__restrict__ ssv,
     float *__restrict__ ssa) {
-    using G = PTile<DT, NS>;
+    using G = TileGemmLds<DT, BT, BT, 2, 2, NS>;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / 2, wn = wave % 2;
@@ -59,12 +64,12 @@ __global__ __launch_bounds__(256) void cos_partial_kernel(
     const int it = (tile / njt) % nit;
     const int ks = (tile / (njt * nit)) % KS;
     const int b = tile / (njt * nit * KS);
-    const int i0 = it * kPT, j0 = jt * kPT;
+    const int i0 = it * BT, j0 = jt * BT;
     const char *abase = anchors + (size_t)b * Nt * d_bytes;
     const char *vbase = vis + (size_t)b * Nv * d_bytes;
     auto row_ptr = [&](int r) -> const char * {
-        if (r < kPT) return abase + (size_t)min(i0 + r, Nt - 1) * d_bytes;
-        return vbase + (size_t)min(j0 + r - kPT, Nv - 1) * d_bytes;
+        if (r < BT) return abase + (size_t)min(i0 + r, Nt - 1) * d_bytes;
+        return vbase + (size_t)min(j0 + r - BT, Nv - 1) * d_bytes;
     };
     const int nch = d_bytes / G::CHUNK;
     const int c0 = (int)(((long long)nch * ks) / KS), c1 = (int)(((long long)nch * (ks + 1)) / KS);
@@ -918,6 +923,59 @@ __global__ __launch_bounds__(kMergeNT) void merge_csr_kernel(
     }
 }
 
+// cos_reduce4: the same for Nv % 4 == 0, four tokens per thread (16-byte
+// loads of the slices, a wave covers 256 tokens of one anchor row): grid
+// (ceil(Nv / 256), ceil(Nt / 4), B).  The row sums of M over each 64-token
+// tile are the thread's four cosines added in order, then the 16 lanes of the
+// tile (a DPP row reduction); the layout of rowsum is cos_reduce's.
+constexpr int kRed4Tok = 256;
+
+template <int kRedU>
+__global__ __launch_bounds__(256) void cos_reduce4_kernel(
+    const float *__restrict__ part, const float *__restrict__ ssv, const float *__restrict__ ssa,
+    int B, int Nv, int Nt, int KS, float *__restrict__ M, float *__restrict__ rowsum,
+    float *__restrict__ invn_vis) {
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int b = blockIdx.z;
+    const int njt = (Nv + kRedTok - 1) / kRedTok;  // 64-token tiles of rowsum
+    const int i = blockIdx.y * kRedRows + wave;
+    const int j = blockIdx.x * kRed4Tok + lane * 4;
+    const int jc = min(j, Nv - 4), ic = min(i, Nt - 1);
+    float4 sv = {0.f, 0.f, 0.f, 0.f}, dot = {0.f, 0.f, 0.f, 0.f};
+    float sa = 0.f;
+    for (int ks0 = 0; ks0 < KS; ks0 += kRedU) {
+        float4 v[kRedU], p[kRedU];
+        float a[kRedU];
+#pragma unroll
+        for (int u = 0; u < kRedU; ++u) {
+            const size_t kb = (size_t)min(ks0 + u, KS - 1) * B + b;
+            v[u] = *reinterpret_cast<const float4 *>(ssv + kb * Nv + jc);
+            a[u] = ssa[kb * Nt + ic];
+            p[u] = *reinterpret_cast<const float4 *>(part + (kb * Nt + ic) * Nv + jc);
+        }
+#pragma unroll
+        for (int u = 0; u < kRedU; ++u) {
+            if (ks0 + u < KS) {
+                sv.x += v[u].x; sv.y += v[u].y; sv.z += v[u].z; sv.w += v[u].w;
+                sa += a[u];
+                dot.x += p[u].x; dot.y += p[u].y; dot.z += p[u].z; dot.w += p[u].w;
+            }
+        }
+    }
+    auto inv = [](float q) { return (q > 0.f) ? 1.0f / sqrtf(q) : 0.f; };
+    const float4 iv = {inv(sv.x), inv(sv.y), inv(sv.z), inv(sv.w)};
+    const float ia = inv(sa);
+    const bool live = j < Nv;  // Nv % 4 == 0: all four tokens or none
+    if (blockIdx.y == 0 && wave == 0 && live) *reinterpret_cast<float4 *>(invn_vis + (size_t)b * Nv + j) = iv;
+    const float4 cs = {dot.x * ia * iv.x, dot.y * ia * iv.y, dot.z * ia * iv.z, dot.w * ia * iv.w};
+    if (i < Nt && live) *reinterpret_cast<float4 *>(M + ((size_t)b * Nt + i) * Nv + j) = cs;
+    float rs = live ? ((cs.x + cs.y) + cs.z) + cs.w : 0.f;
+    rs = row16_sum(rs);
+    const int jt = blockIdx.x * (kRed4Tok / kRedTok) + (lane >> 4);
+    if ((lane & 15) == 0 && i < Nt && jt < njt) rowsum[((size_t)b * njt + jt) * Nt + i] = rs;
+}
+
 // ----------------------------------------------------------------------------
 // launchers
 // ----------------------------------------------------------------------------
@@ -926,30 +984,49 @@ __global__ __launch_bounds__(kMergeNT) void merge_csr_kernel(
 // gain.
 constexpr int kSplitNS = 3;
 
-template <int DT, int NS>
-static void cos_partial_go(dim3 grid, const void *vis, const void *anchors, int B, int Nv, int Nt,
-                           int d_bytes, int njt, int nit, int KS, float *part, float *ssv,
-                           float *ssa, hipStream_t st) {
-    hipLaunchKernelGGL((cos_partial_kernel<DT, NS>), grid, dim3(256), 0, st, (const char *)vis,
+template <int DT, int NS, int BT>
+static void cos_partial_go(const void *vis, const void *anchors, int B, int Nv, int Nt,
+                           int d_bytes, int KS, float *part, float *ssv, float *ssa,
+                           hipStream_t st) {
+    const int njt = (Nv + BT - 1) / BT, nit = (Nt + BT - 1) / BT;
+    const dim3 grid(B * KS * nit * njt);
+    hipLaunchKernelGGL((cos_partial_kernel<DT, NS, BT>), grid, dim3(256), 0, st, (const char *)vis,
                        (const char *)anchors, B, Nv, Nt, d_bytes, njt, nit, KS, part, ssv, ssa);
 }
 
 hipError_t launch_cos_partial(int dt, const void *vis, const void *anchors, int B, int Nv, int Nt,
                               int d, int KS, float *part, float *ssv, float *ssa, hipStream_t st) {
     const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
-    const int njt = (Nv + kPT - 1) / kPT, nit = (Nt + kPT - 1) / kPT;
-    const dim3 grid(B * KS * nit * njt);
-    if (dt == kBF16)
-        cos_partial_go<kBF16, kSplitNS>(grid, vis, anchors, B, Nv, Nt, d_bytes, njt, nit, KS, part,
-                                        ssv, ssa, st);
-    else
-        cos_partial_go<kF32, kSplitNS>(grid, vis, anchors, B, Nv, Nt, d_bytes, njt, nit, KS, part,
-                                       ssv, ssa, st);
+    const bool wide = cos_uses_wide_tiles(Nt, Nv);
+    if (dt == kBF16) {
+        if (wide) cos_partial_go<kBF16, 2, kWideTile>(vis, anchors, B, Nv, Nt, d_bytes, KS, part, ssv, ssa, st);
+        else cos_partial_go<kBF16, kSplitNS, kPT>(vis, anchors, B, Nv, Nt, d_bytes, KS, part, ssv, ssa, st);
+    } else {
+        if (wide) cos_partial_go<kF32, 2, kWideTile>(vis, anchors, B, Nv, Nt, d_bytes, KS, part, ssv, ssa, st);
+        else cos_partial_go<kF32, kSplitNS, kPT>(vis, anchors, B, Nv, Nt, d_bytes, KS, part, ssv, ssa, st);
+    }
     return hipGetLastError();
 }
 
 hipError_t launch_cos_reduce(const float *part, const float *ssv, const float *ssa, int B, int Nv,
                              int Nt, int KS, float *M, float *rowsum, float *invn, hipStream_t st) {
+    if (Nv % 4 == 0) {
+        dim3 grid4((Nv + kRed4Tok - 1) / kRed4Tok, (Nt + kRedRows - 1) / kRedRows, B);
+#define PV_RED4_CASE(u)                                                                             \
+    case u:                                                                                         \
+        hipLaunchKernelGGL(cos_reduce4_kernel<u>, grid4, dim3(256), 0, st, part, ssv, ssa, B, Nv,   \
+                           Nt, KS, M, rowsum, invn);                                                \
+        break;
+        switch (reduce_unroll(KS)) {
+            PV_RED4_CASE(1)
+            PV_RED4_CASE(2)
+            PV_RED4_CASE(4)
+            PV_RED4_CASE(8)
+            PV_RED4_CASE(16)
+        }
+#undef PV_RED4_CASE
+        return hipGetLastError();
+    }
     dim3 grid((Nv + kRedTok - 1) / kRedTok, (Nt + kRedRows - 1) / kRedRows, B);
 #define PV_RED_CASE(u)                                                                             \
     case u:                                                                                        \

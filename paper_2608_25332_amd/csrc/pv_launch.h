@@ -25,6 +25,10 @@ struct HeadArgs8 {
 
 // ---- pruning before the LLM (Sec. 4.3)
 constexpr int kSplitTile = 64;  // tile edge of the split-k products
+constexpr int kWideTile = 128;  // the cosine's tile edge with more than 64 anchors
+// Whether the split-k cosine runs on kWideTile tiles (two workgroups per CU)
+// instead of kSplitTile tiles (three per CU).
+inline bool cos_uses_wide_tiles(int Nt, int Nv) { return Nt > 64 && Nv >= 512; }
 int cos_row_tiles(int Nv);      // token tiles of the row sums written by cos_reduce
 int cos_full_row_tiles(int Nv); // token tiles of the row sums written by cos_full
 // Whether the cosine runs as one full-k pass over 16 x 16 tiles (small inputs:
