@@ -168,7 +168,7 @@ __global__ __launch_bounds__(256) void cos_reduce_kernel(
 // ----------------------------------------------------------------------------
 // cos_full: the cosine for small inputs (one sample of LLaVA-1.5 size), where
 // a split-k pass plus its reduction costs two launches for a few MB.  1-D grid
-// over (sample, anchor tile, token tile) of 16 x 16 tiles in XCD order, 512
+// over (sample, token tile, anchor tile) of 16 x 16 tiles in XCD order, 512
 // threads.  Each workgroup computes its tile of M over the whole k range: the
 // eight waves take an eighth of k each and stream their part of the 32 rows
 // straight into their own LDS ring, so the k loop needs no barrier.  The wave
@@ -189,8 +189,12 @@ __global__ __launch_bounds__(64 * NW) void cos_full_kernel(
     __shared__ float ssab[NW][kFT], ssvb[NW][kFT];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // anchor tiles fastest: the run of tiles an XCD receives covers every
+    // anchor tile of a few token tiles, so its L2 holds all the anchor rows
+    // and few token rows (token tiles fastest would give it one anchor tile
+    // and many token tiles, and every XCD would fetch the token rows again)
     const int L = xcd_tile(blockIdx.x, gridDim.x);
-    const int jt = L % njt, it = (L / njt) % nit, b = L / (njt * nit);
+    const int it = L % nit, jt = (L / nit) % njt, b = L / (njt * nit);
     const int i0 = it * kFT, j0 = jt * kFT;
     const char *abase = anchors + (size_t)b * Nt * d_bytes;
     const char *vbase = vis + (size_t)b * Nv * d_bytes;
