@@ -321,6 +321,8 @@ HEAD_EDGE = [
     (2, 4, 5, 50, 96, 1, 7, "f32"),
     (1, 2, 200, 2100, 128, 2, 600, "bf16"),   # keys streamed twice
     (2, 3, 40, 1500, 128, 2, 200, "bf16"),    # 24 chunks of logits held in registers
+    (1, 4, 50, 900, 64, 2, 100, "bf16"),      # 15 chunks, ragged, logits held
+    (2, 2, 20, 700, 32, 1, 50, "f32"),        # 11 chunks, fp32, logits held
     (1, 2, 20, 600, 256, 1, 100, "bf16"),     # wide head, streamed twice
     (1, 2, 16, 130, 256, 2, 30, "f32"),       # widest head, logits kept
     (1, 2, 16, 300, 256, 1, 30, "f32"),       # widest head, streamed twice
