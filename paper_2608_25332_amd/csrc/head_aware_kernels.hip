@@ -130,8 +130,10 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     auto issue_q = [&]() {
         for (int p = wave; p < NKS; p += 4) {
             const int off = p * 1024 + lane * 16;
-            const int r = off / S::RB;
-            lds_dma16(qb + (size_t)min(rb * 16 + r, Nt - 1) * S::RB + off % S::RB, qrows + p * 1024);
+            const int r = off / S::RB, slot = (off % S::RB) >> 4;
+            // the keys' piece swizzle, so the fragment reads spread over the banks
+            lds_dma16(qb + (size_t)min(rb * 16 + r, Nt - 1) * S::RB + ((slot ^ (r & S::SWZ)) << 4),
+                      qrows + p * 1024);
         }
     };
     // A pass over the keys: start() fills the whole ring (no buffer is reused
@@ -148,7 +150,8 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     auto read_q = [&]() {
 #pragma unroll
         for (int s = 0; s < NKS; ++s)
-            qf[s] = lds_read16(qrows + (lane & 15) * S::RB + (s * 4 + (lane >> 4)) * 16);
+            qf[s] = lds_read16(qrows + (lane & 15) * S::RB +
+                               (((s * 4 + (lane >> 4)) ^ ((lane & 15) & S::SWZ)) << 4));
         lds_wait();
 #pragma unroll
         for (int s = 0; s < NKS; ++s) lds_after_wait(qf[s]);
@@ -540,7 +543,9 @@ __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
     const int nq = ((Nt + 15) / 16) * 16 * S::RB / 1024;  // 1 KiB pieces of the query block
     for (int pce = wave; pce < nq; pce += 4) {
         const int off = pce * 1024 + lane * 16;
-        lds_dma16(qb + (size_t)min(off / S::RB, Nt - 1) * S::RB + off % S::RB, qrows + pce * 1024);
+        const int r = off / S::RB, slot = (off % S::RB) >> 4;
+        lds_dma16(qb + (size_t)min(r, Nt - 1) * S::RB + ((slot ^ (r & S::SWZ)) << 4),
+                  qrows + pce * 1024);
     }
 #pragma unroll
     for (int ch = 0; ch < MAXC; ++ch) {
@@ -566,7 +571,8 @@ __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
         uint4 qf[NKS];
         const int qr = wave * 16 + (lane & 15);
 #pragma unroll
-        for (int s = 0; s < NKS; ++s) qf[s] = lds_read16(qrows + qr * S::RB + (s * 4 + (lane >> 4)) * 16);
+        for (int s = 0; s < NKS; ++s)
+            qf[s] = lds_read16(qrows + qr * S::RB + (((s * 4 + (lane >> 4)) ^ (qr & S::SWZ)) << 4));
         lds_wait();
 #pragma unroll
         for (int s = 0; s < NKS; ++s) lds_after_wait(qf[s]);
