@@ -115,6 +115,14 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
     P.gram_big = (long long)((Mp1 + pv::kGramBigM - 1) / pv::kGramBigM) *
                      ((budget + pv::kGramTileN - 1) / pv::kGramTileN) * B >= 128;
     P.ks_gram = P.gram_big ? 1 : pick_slices(n_tiles(Mp1, budget, B, T), P.nch);
+    {
+        // a single round of at most one workgroup per CU when the slice cap
+        // leaves between one and two workgroups per CU: the CUs that would
+        // hold two set the kernel's time
+        const long long t = n_tiles(Mp1, budget, B, T);
+        if (t * P.ks_gram > 256 && t * P.ks_gram < 512 && 256 / t >= 1) P.ks_gram = (int)(256 / t);
+        else if (t * P.ks_gram > 768 && t * P.ks_gram < 1536 && 768 / t >= 1) P.ks_gram = (int)(768 / t);
+    }
     P.ntn = P.gram_big ? (budget + pv::kGramTileN - 1) / pv::kGramTileN : 1;
     Carve c(ws);
     if (P.cos_full) {
