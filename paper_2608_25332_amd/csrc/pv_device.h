@@ -113,15 +113,48 @@ __device__ __forceinline__ uint32_t order_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// Inclusive prefix sum across the 64 lanes of a wave.
+// Lane exchange within a row of 16 lanes through DPP; a lane whose source
+// falls outside the row reads 0.
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int x) {
+    return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
+}
+
+// Inclusive prefix sum across the 64 lanes of a wave (every lane active):
+// within each row of 16 by DPP row shifts of 1, 2, 4, 8, then the totals of
+// the rows below from lanes 15, 31, 47.  Integer sums, so the order of the
+// additions does not matter.
 __device__ __forceinline__ int wave_incl_scan(int x) {
-    const int lane = threadIdx.x & 63;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        int y = __shfl_up(x, off, 64);
-        if (lane >= off) x += y;
-    }
-    return x;
+    const int row = (threadIdx.x & 63) >> 4;
+    x += dpp_i32<0x111>(x);  // row_shr:1
+    x += dpp_i32<0x112>(x);  // row_shr:2
+    x += dpp_i32<0x114>(x);  // row_shr:4
+    x += dpp_i32<0x118>(x);  // row_shr:8
+    const int t0 = __builtin_amdgcn_readlane(x, 15);
+    const int t1 = __builtin_amdgcn_readlane(x, 31);
+    const int t2 = __builtin_amdgcn_readlane(x, 47);
+    return x + (row >= 1 ? t0 : 0) + (row >= 2 ? t1 : 0) + (row >= 3 ? t2 : 0);
+}
+
+// Minimum and maximum over the 64 lanes of a wave, returned to every lane:
+// row reductions by DPP (as row16_max), then lanes 0, 16, 32, 48.
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
+    x = min(x, (uint32_t)dpp_i32<0xB1>((int)x));
+    x = min(x, (uint32_t)dpp_i32<0x4E>((int)x));
+    x = min(x, (uint32_t)dpp_i32<0x141>((int)x));
+    x = min(x, (uint32_t)dpp_i32<0x140>((int)x));
+    const uint32_t a = __builtin_amdgcn_readlane(x, 0), b = __builtin_amdgcn_readlane(x, 16);
+    const uint32_t c = __builtin_amdgcn_readlane(x, 32), d = __builtin_amdgcn_readlane(x, 48);
+    return min(min(a, b), min(c, d));
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
+    x = max(x, (uint32_t)dpp_i32<0xB1>((int)x));
+    x = max(x, (uint32_t)dpp_i32<0x4E>((int)x));
+    x = max(x, (uint32_t)dpp_i32<0x141>((int)x));
+    x = max(x, (uint32_t)dpp_i32<0x140>((int)x));
+    const uint32_t a = __builtin_amdgcn_readlane(x, 0), b = __builtin_amdgcn_readlane(x, 16);
+    const uint32_t c = __builtin_amdgcn_readlane(x, 32), d = __builtin_amdgcn_readlane(x, 48);
+    return max(max(a, b), max(c, d));
 }
 
 // Exclusive prefix sum over a block of NT threads; *total gets the block sum.
@@ -203,11 +236,8 @@ __device__ __forceinline__ void block_topk(const uint32_t (&key)[EMAX], int n, i
             hi = max(hi, key[e]);
         }
     }
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        lo = min(lo, (uint32_t)__shfl_xor((int)lo, off, 64));
-        hi = max(hi, (uint32_t)__shfl_xor((int)hi, off, 64));
-    }
+    lo = wave_min_u32(lo);
+    hi = wave_max_u32(hi);
     if (lane == 0) {
         sm.wlo[wave] = lo;
         sm.whi[wave] = hi;
@@ -247,9 +277,8 @@ __device__ __forceinline__ void block_topk(const uint32_t (&key)[EMAX], int n, i
                 const int h0 = sm.hist[cur][4 * lane], h1 = sm.hist[cur][4 * lane + 1];
                 const int h2 = sm.hist[cur][4 * lane + 2], h3 = sm.hist[cur][4 * lane + 3];
                 const int mine = h0 + h1 + h2 + h3;
-                const int rev = __shfl(mine, 63 - lane, 64);
-                const int inc = wave_incl_scan(rev);
-                const int suffix_incl = __shfl(inc, 63 - lane, 64);  // lanes >= this one
+                const int inc = wave_incl_scan(mine);
+                const int suffix_incl = __builtin_amdgcn_readlane(inc, 63) - inc + mine;  // lanes >= this one
                 const int above = suffix_incl - mine;                 // bins > 4*lane+3
                 const int ge3 = above + h3, ge2 = ge3 + h2, ge1 = ge2 + h1, ge0 = ge1 + h0;
                 int dsel = -1, gt = 0, cnt = 0;
