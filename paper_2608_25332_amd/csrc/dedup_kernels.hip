@@ -160,8 +160,7 @@ __global__ __launch_bounds__(256) void cos_reduce_kernel(
     const float cs = dot * inv_a * inv_v;
     if (i < Nt && j < Nv) M[((size_t)b * Nt + i) * Nv + j] = cs;
     float rs = (j < Nv) ? cs : 0.f;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) rs += __shfl_xor(rs, off, 64);
+    rs = wave_sum64(rs);
     if (lane == 0 && i < Nt) rowsum[((size_t)b * njt + jt) * Nt + i] = rs;
 }
 
@@ -275,8 +274,7 @@ __global__ __launch_bounds__(64 * NW) void cos_full_kernel(
     if (i < Nt && j < Nv) M[((size_t)b * Nt + i) * Nv + j] = cs;
     if (it == 0 && ii == 0 && j < Nv) invn_vis[(size_t)b * Nv + j] = inv_v;
     float rs = (j < Nv) ? cs : 0.f;
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) rs += __shfl_xor(rs, off, 64);
+    rs = row16_sum(rs);
     if (jj == 0 && i < Nt) rowsum[((size_t)b * njt + jt) * Nt + i] = rs;
 }
 
@@ -385,6 +383,41 @@ __global__ __launch_bounds__(NT) void select_kernel(const float *__restrict__ p,
 // ----------------------------------------------------------------------------
 __device__ __forceinline__ bool better(float v, int s, float bv, int bs) {
     return v > bv || (v == bv && s < bs);
+}
+
+// The best (value, slot) of the 16 lanes of each row, left in every lane of
+// the row: DPP exchanges pairing lanes as an xor butterfly over 1, 2, 4, 8
+// does (the order is total, so any pairing gives the same best).
+__device__ __forceinline__ void row16_best(float &bv, int &bs) {
+    auto step = [&](float ov, int os) {
+        if (better(ov, os, bv, bs)) {
+            bv = ov;
+            bs = os;
+        }
+    };
+    step(dpp_f32<0xB1>(bv), dpp_i32<0xB1>(bs));
+    step(dpp_f32<0x4E>(bv), dpp_i32<0x4E>(bs));
+    step(dpp_f32<0x141>(bv), dpp_i32<0x141>(bs));
+    step(dpp_f32<0x140>(bv), dpp_i32<0x140>(bs));
+}
+
+// The same over the 64 lanes of a wave (every lane active), returned to
+// every lane: the rows, then their bests read from lanes 0, 16, 32, 48.
+__device__ __forceinline__ void wave_best(float &bv, int &bs) {
+    row16_best(bv, bs);
+    float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bv), 0));
+    int sl = __builtin_amdgcn_readlane(bs, 0);
+#pragma unroll
+    for (int r = 1; r < 4; ++r) {
+        const float rv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bv), 16 * r));
+        const int rs = __builtin_amdgcn_readlane(bs, 16 * r);
+        if (better(rv, rs, v, sl)) {
+            v = rv;
+            sl = rs;
+        }
+    }
+    bv = v;
+    bs = sl;
 }
 
 // gram_finish: grid (ceil(Mp / 256), B).  Best column tile of every pruned
@@ -512,15 +545,7 @@ __global__ __launch_bounds__(128) void gram_reduce_kernel(
             }
         }
     }
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const float ov = __shfl_xor(bv, off, 64);
-        const int os = __shfl_xor(bs, off, 64);
-        if (better(ov, os, bv, bs)) {
-            bv = ov;
-            bs = os;
-        }
-    }
+    wave_best(bv, bs);
     if (lane == 0) assign[(size_t)b * Nv + tok] = bs;
 }
 
@@ -584,15 +609,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
                     bs = slot;
                 }
             }
-#pragma unroll
-            for (int off = 1; off < 16; off <<= 1) {
-                const float ov = __shfl_xor(bv, off, 64);
-                const int os = __shfl_xor(bs, off, 64);
-                if (better(ov, os, bv, bs)) {
-                    bv = ov;
-                    bs = os;
-                }
-            }
+            row16_best(bv, bs);
             if ((lane & 15) == 0) {
                 red_v[wn][r] = bv;
                 red_s[wn][r] = bs;

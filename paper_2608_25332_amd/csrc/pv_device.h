@@ -113,6 +113,18 @@ __device__ __forceinline__ uint32_t order_key(float f) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
+// Sum over the 64 lanes of a wave (every lane active), in every lane: the
+// rows by row16_sum, then (row 0 + row 1) + (row 2 + row 3), the order of an
+// xor butterfly over 16 and 32, so the bits are that butterfly's.
+__device__ __forceinline__ float wave_sum64(float x) {
+    x = row16_sum(x);
+    const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+    const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+    const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+    const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+    return (a + b) + (c + d);
+}
+
 // Lane exchange within a row of 16 lanes through DPP; a lane whose source
 // falls outside the row reads 0.
 template <int CTRL>
