@@ -294,21 +294,25 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
         }
         return;
     }
-    // combine the 16 lanes that hold the same rows, then the 4 waves
-#pragma unroll
-    for (int off = 1; off < 16; off <<= 1) {
+    // combine the 16 lanes that hold the same rows (DPP partners of an xor
+    // butterfly over 1, 2, 4, 8; both lanes of a pair compute the same merge,
+    // so the pairing gives the butterfly's bits), then the 4 waves
+    auto merge_step = [&](auto xch) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const float m2 = __shfl_xor(m[i], off, 64);
-            const float l2 = __shfl_xor(l[i], off, 64);
+            const float m2 = xch(m[i]), l2 = xch(l[i]);
             if (CONF) {
-                const float s2 = __shfl_xor(sq[i], off, 64);
+                const float s2 = xch(sq[i]);
                 lse_merge2(m[i], l[i], sq[i], m2, l2, s2);
             } else {
                 lse_merge(m[i], l[i], m2, l2);
             }
         }
-    }
+    };
+    merge_step([](float x) { return dpp_f32<0xB1>(x); });
+    merge_step([](float x) { return dpp_f32<0x4E>(x); });
+    merge_step([](float x) { return dpp_f32<0x141>(x); });
+    merge_step([](float x) { return dpp_f32<0x140>(x); });
     if ((lane & 15) == 0) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {

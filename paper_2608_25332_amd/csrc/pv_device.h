@@ -125,6 +125,16 @@ __device__ __forceinline__ float wave_sum64(float x) {
     return (a + b) + (c + d);
 }
 
+// Maximum over the 64 lanes of a wave (every lane active), in every lane.
+__device__ __forceinline__ float wave_max_f32(float x) {
+    x = row16_max(x);
+    const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+    const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+    const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+    const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+    return fmaxf(fmaxf(a, b), fmaxf(c, d));
+}
+
 // Lane exchange within a row of 16 lanes through DPP; a lane whose source
 // falls outside the row reads 0.
 template <int CTRL>

@@ -33,10 +33,9 @@ __global__ __launch_bounds__(256) void text_gram_sum_kernel(const float *__restr
 }
 
 // Sum of one value per thread over the workgroup, in a fixed order: the
-// wave's lanes by a butterfly, then the waves in index order.
+// wave's lanes in the order of a butterfly, then the waves in index order.
 __device__ __forceinline__ float block_sum_fixed(float v, float *wsum) {
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) v += __shfl_xor(v, off, 64);
+    v = wave_sum64(v);
     const int wave = threadIdx.x >> 6;
     __syncthreads();
     if ((threadIdx.x & 63) == 0) wsum[wave] = v;
@@ -71,16 +70,14 @@ __global__ __launch_bounds__(kRankNT) void text_rank_kernel(const float *__restr
             g[t] = j < Nt ? row[j] : -INFINITY;
             m = fmaxf(m, g[t]);
         }
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) m = fmaxf(m, __shfl_xor(m, off, 64));
+        m = wave_max_f32(m);
         float l = 0.f;
 #pragma unroll
         for (int t = 0; t < kRankPer; ++t) {
             g[t] = expf(g[t] - m);  // 0 past the end
             l += g[t];
         }
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) l += __shfl_xor(l, off, 64);
+        l = wave_sum64(l);
         const float il = 1.0f / l;
 #pragma unroll
         for (int t = 0; t < kRankPer; ++t) {
