@@ -18,7 +18,7 @@ namespace pv {
 
 constexpr int kRankNT = 1024;
 constexpr int kRankW = kRankNT / 64;           // waves
-constexpr int kRankPer = PV_MAX_TEXT / 64;     // row elements per lane
+constexpr int kRankRows = 4;                   // rows a wave loads at once
 
 // G[b][i][j] = sum over k slices of part[ks][b][i][j], slices in order.
 __global__ __launch_bounds__(256) void text_gram_sum_kernel(const float *__restrict__ part, int B,
@@ -46,10 +46,12 @@ __device__ __forceinline__ float block_sum_fixed(float v, float *wsum) {
 }
 
 // One workgroup per sample.  Each wave takes rows w, w + kRankW, ...: a
-// row's values stay in registers (kRankPer per lane) for its maximum, its
-// sum of exponentials and its normalised probabilities, which the wave adds
-// into its own column sums in LDS; the waves' column sums are then added in
-// wave order.
+// row's values stay in registers (PER per lane, PER * 64 >= Nt) for its
+// maximum, its sum of exponentials and its normalised probabilities, which
+// the wave adds into its own column sums in LDS, row after row; the waves'
+// column sums are then added in wave order.  The loads of kRankRows rows are
+// issued together.
+template <int PER>
 __global__ __launch_bounds__(kRankNT) void text_rank_kernel(const float *__restrict__ G, int Nt,
                                                             float *__restrict__ r_out,
                                                             int32_t *__restrict__ mask,
@@ -60,29 +62,37 @@ __global__ __launch_bounds__(kRankNT) void text_rank_kernel(const float *__restr
     const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const float *Gb = G + (size_t)b * Nt * Nt;
     for (int j = lane; j < Nt; j += 64) csum[wave][j] = 0.f;
-    for (int i = wave; i < Nt; i += kRankW) {
-        const float *row = Gb + (size_t)i * Nt;
-        float g[kRankPer];
-        float m = -INFINITY;
+    for (int i0 = wave; i0 < Nt; i0 += kRankRows * kRankW) {
+        float g[kRankRows][PER];
 #pragma unroll
-        for (int t = 0; t < kRankPer; ++t) {
-            const int j = lane + 64 * t;
-            g[t] = j < Nt ? row[j] : -INFINITY;
-            m = fmaxf(m, g[t]);
+        for (int q = 0; q < kRankRows; ++q) {
+            const int i = i0 + q * kRankW;
+#pragma unroll
+            for (int t = 0; t < PER; ++t) {
+                const int j = lane + 64 * t;
+                g[q][t] = (i < Nt && j < Nt) ? Gb[(size_t)i * Nt + j] : -INFINITY;
+            }
         }
-        m = wave_max_f32(m);
-        float l = 0.f;
 #pragma unroll
-        for (int t = 0; t < kRankPer; ++t) {
-            g[t] = expf(g[t] - m);  // 0 past the end
-            l += g[t];
-        }
-        l = wave_sum64(l);
-        const float il = 1.0f / l;
+        for (int q = 0; q < kRankRows; ++q) {
+            if (i0 + q * kRankW >= Nt) break;  // uniform over the wave
+            float m = -INFINITY;
 #pragma unroll
-        for (int t = 0; t < kRankPer; ++t) {
-            const int j = lane + 64 * t;
-            if (j < Nt) csum[wave][j] += g[t] * il;
+            for (int t = 0; t < PER; ++t) m = fmaxf(m, g[q][t]);
+            m = wave_max_f32(m);
+            float l = 0.f;
+#pragma unroll
+            for (int t = 0; t < PER; ++t) {
+                g[q][t] = expf(g[q][t] - m);  // 0 past the end
+                l += g[q][t];
+            }
+            l = wave_sum64(l);
+            const float il = 1.0f / l;
+#pragma unroll
+            for (int t = 0; t < PER; ++t) {
+                const int j = lane + 64 * t;
+                if (j < Nt) csum[wave][j] += g[q][t] * il;
+            }
         }
     }
     __syncthreads();
@@ -116,7 +126,15 @@ hipError_t launch_text_gram_sum(const float *part, int B, int Nt, int KS, float 
 hipError_t launch_text_rank(const float *G, int B, int Nt, float *r, int32_t *mask, int32_t *count,
                             hipStream_t st) {
     if (Nt > PV_MAX_TEXT) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(text_rank_kernel, dim3(B), dim3(kRankNT), 0, st, G, Nt, r, mask, count);
+#define PV_RANK_CASE(per)                                                                     \
+    hipLaunchKernelGGL(text_rank_kernel<per>, dim3(B), dim3(kRankNT), 0, st, G, Nt, r, mask, \
+                       count)
+    if (Nt <= 64) PV_RANK_CASE(1);
+    else if (Nt <= 128) PV_RANK_CASE(2);
+    else if (Nt <= 256) PV_RANK_CASE(4);
+    else if (Nt <= 512) PV_RANK_CASE(8);
+    else PV_RANK_CASE(PV_MAX_TEXT / 64);
+#undef PV_RANK_CASE
     return hipGetLastError();
 }
 
