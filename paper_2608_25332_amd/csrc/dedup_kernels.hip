@@ -316,6 +316,14 @@ __global__ __launch_bounds__(kCenNT) void center_kernel(const float *__restrict_
     __shared__ float rpart[4][kCenTok];
     __shared__ int any_row;
     const int b = blockIdx.y, tid = threadIdx.x;
+    const int jl = tid & (kCenTok - 1), g = tid / kCenTok;
+    const int j = blockIdx.x * kCenTok + jl;
+    // the first block of this thread's column of M does not depend on the
+    // row means: its loads are in flight during the first phase
+    const float *col = M + (size_t)b * Nt * Nv + min(j, Nv - 1);
+    float v0[kCenU];
+#pragma unroll
+    for (int u = 0; u < kCenU; ++u) v0[u] = col[(size_t)min(g + 4 * u, Nt - 1) * Nv];
     if (tid == 0) any_row = row_mask ? 0 : 1;
     for (int r0 = 0; r0 < Nt; r0 += kCenTok) {
         const int i = r0 + (tid >> 2), q = tid & 3;
@@ -335,12 +343,12 @@ __global__ __launch_bounds__(kCenNT) void center_kernel(const float *__restrict_
     }
     // an empty mask means every row
     const float *mrow = (row_mask && any_row) ? mu + Nt : mu;
-    const int jl = tid & (kCenTok - 1), g = tid / kCenTok;
-    const int j = blockIdx.x * kCenTok + jl;
     float m = -INFINITY;
     if (j < Nv) {
-        const float *col = M + (size_t)b * Nt * Nv + j;
-        for (int i0 = g; i0 < Nt; i0 += 4 * kCenU) {
+#pragma unroll
+        for (int u = 0; u < kCenU; ++u)
+            if (g + 4 * u < Nt) m = fmaxf(m, v0[u] - mrow[g + 4 * u]);
+        for (int i0 = g + 4 * kCenU; i0 < Nt; i0 += 4 * kCenU) {
             float v[kCenU];
 #pragma unroll
             for (int u = 0; u < kCenU; ++u) v[u] = col[(size_t)min(i0 + 4 * u, Nt - 1) * Nv];
