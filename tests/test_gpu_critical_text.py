@@ -59,6 +59,8 @@ TEXT_CASES = [
     (2, 128, 4096, 0.027, "bf16"),
     (4, 37, 1024, 0.054, "bf16"),
     (1, 300, 512, 0.077, "f32"),
+    (1, 700, 256, 0.1, "f32"),       # 11 row elements per lane; wide self-similarity tiles
+    (2, 1024, 128, 0.15, "bf16"),    # the most text rows
     (1, 1, 64, 1.0, "f32"),          # one token: r = 1, every token kept
 ]
 
