@@ -59,7 +59,11 @@ def parse():
                          "known size (--calib-mib) to scale the counters; no timing")
     ap.add_argument("--calib-mib", type=int, default=256)
     ap.add_argument("--split", action="store_true",
-                    help="time the step with the merge branch on a second stream")
+                    help="time the step with the merge branch on a second stream "
+                         "(the same as --streams 2)")
+    ap.add_argument("--streams", choices=["1", "2", "auto"], default="auto",
+                    help="the step on one stream, with the merge branch on a second stream, or "
+                         "whichever of the two replays faster (measured before the timed steps)")
     ap.add_argument("--cold-mib", type=int, default=640,
                     help="input copies rotated through for the cold-cache timing (0 disables it)")
     ap.add_argument("--score-sweep", action="store_true",
@@ -644,13 +648,26 @@ def main():
         return
     w = W.make_workload(args.workload)
     s = w.spec
-    step = Step(w, dev, split=args.split)
+    step = Step(w, dev, split=args.split or args.streams == "2")
     stream = torch.cuda.current_stream(dev)
 
     # eager reference outputs
     step.run()
     torch.cuda.synchronize()
     ref = step.snapshot()
+
+    # one stream or two: the merge branch on a second stream overlaps the
+    # K/V gather and the head-aware score, which pays once those take longer
+    # than the cross-stream dependencies cost (the large workloads); picked
+    # from graph replays of both forms before any timed step
+    mode_us = {}
+    if args.streams == "auto" and not args.split and not args.pmc_pass and not args.no_graph:
+        for sp in (False, True):
+            step.split = sp
+            mode_us["two_streams" if sp else "one_stream"] = graph_time_us(torch, step.run, reps=300)
+        step.split = mode_us["two_streams"] < mode_us["one_stream"]
+        torch.cuda.synchronize()
+    split = step.split
 
     if args.pmc_pass:
         # every dispatch of a library kernel here runs in the step's own
@@ -715,12 +732,12 @@ def main():
     breakdown = stage_breakdown(torch, step)
 
     def other():
-        step.split = not args.split
+        step.split = not split
         try:
             step.run()
         finally:
-            step.split = args.split
-    breakdown["step_two_streams" if not args.split else "step_single_stream"] = graph_time_us(
+            step.split = split
+    breakdown["step_two_streams" if not split else "step_single_stream"] = graph_time_us(
         torch, other)
     vis_heads = visual_heads_timing(torch, step)
     crit_text = critical_text_timing(torch, step)
@@ -770,12 +787,14 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "B": s.B, "Nv": s.Nv, "d": s.d, "H": s.H, "hd": s.hd,
                    "Nt": s.Nt, "heads_per_sample": int(w.heads.shape[1]), "N1": w.N1, "N2": w.N2,
+                   "streams": 2 if split else 1,
                    "timing": ("hip-graph replay of the full step" +
-                              (", merge branch on a second stream" if args.split else "")
+                              (", merge branch on a second stream" if split else "")
                               if graph is not None else "eager")},
         "latency_us": {"pipeline": ms_per_step * 1000.0, "pipeline_single_replays": pct,
                        "pipeline_cold": cold, "kernels": kern_us,
-                       "stages": stage_us, "calls_graph_replay": breakdown},
+                       "stages": stage_us, "calls_graph_replay": breakdown,
+                       "stream_choice_us": mode_us or None},
         "roofline": rf,
         "roofline_kernels": kernels,
         "roofline_stages": stages,
