@@ -195,6 +195,10 @@ DEDUP_EDGE = [
     # tiles in fp32 (per-tile candidates merged by gram_finish)
     (128, 300, 4, 64, 100, "bf16"),
     (64, 600, 4, 128, 200, "f32"),
+    # split-k cosine on 128 x 128 tiles at the boundary (65 anchors, 512 tokens)
+    (16, 512, 65, 2048, 100, "bf16"),
+    # four-token slice reduction at its smallest (8 tokens, many anchors)
+    (64, 8, 130, 4096, 3, "f32"),
     # merge through bucketed member lists (narrow rows, many slots)
     (1, 1000, 8, 64, 70, "bf16"),
     (2, 700, 5, 128, 200, "f32"),
