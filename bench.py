@@ -61,9 +61,11 @@ def parse():
     ap.add_argument("--split", action="store_true",
                     help="time the step with the merge branch on a second stream "
                          "(the same as --streams 2)")
-    ap.add_argument("--streams", choices=["1", "2", "auto"], default="auto",
-                    help="the step on one stream, with the merge branch on a second stream, or "
-                         "whichever of the two replays faster (measured before the timed steps)")
+    ap.add_argument("--streams", choices=["1", "2", "shared", "auto"], default="auto",
+                    help="the step as four calls on one stream, with the merge branch on a "
+                         "second stream, as one pv_prune_pipeline call (the two chains after "
+                         "the top-N1 share launches), or whichever of the three replays fastest "
+                         "(measured before the timed steps)")
     ap.add_argument("--cold-mib", type=int, default=640,
                     help="input copies rotated through for the cold-cache timing (0 disables it)")
     ap.add_argument("--score-sweep", action="store_true",
@@ -76,7 +78,9 @@ def parse():
 class Step:
     """Buffers and the kernel sequence of one step (all preallocated)."""
 
-    def __init__(self, w, dev, split=False):
+    FORMS = ("one_stream", "two_streams", "shared_launches")
+
+    def __init__(self, w, dev, form="one_stream"):
         import torch
 
         from paper_2608_25332_amd import provip
@@ -115,9 +119,17 @@ class Step:
         self.ws2 = torch.empty(provip.pv_head_aware_workspace_bytes(B, H, s.Nt, N1, hd,
                                                                     self.heads.shape[1], N2, code),
                                dtype=torch.uint8, device=dev)
+        self.wsp = torch.empty(provip.pv_pipeline_workspace_bytes(
+            B, Nv, s.Nt, d, H, hd, self.heads.shape[1], N1, N2, code), dtype=torch.uint8,
+            device=dev)
+        self.pipe_out = {"kept1": self.o1["kept"], "score1": self.o1["score"],
+                         "assign": self.o1["assign"], "merged": self.o1["merged"], "k1": self.k1,
+                         "v1": self.v1, "kept2": self.o2["kept"], "score2": self.o2["score"],
+                         "hidden2": self.hid2, "k2": self.k2, "v2": self.v2}
         # second stream (default priority) and the fork/join events of the
         # two-stream step; torch creates a HIP event on its first record
-        self.split = split
+        assert form in self.FORMS
+        self.form = form
         self.side = torch.cuda.Stream(dev)
         self.ev_sel = torch.cuda.Event()
         self.ev_done = torch.cuda.Event()
@@ -133,12 +145,17 @@ class Step:
                                       outs=[self.hid2, self.k2, self.v2])
 
     def run(self):
-        """Enqueue one step on the current stream.  With self.split the
+        """Enqueue one step on the current stream.  In the two-stream form the
         nearest-centroid and merge kernels run on a second stream, overlapped
         with the K/V gather and the head-aware score (they meet again before
-        the final gather, which needs the merged rows)."""
+        the final gather, which needs the merged rows).  In the shared-launch
+        form the step is one pv_prune_pipeline call, whose two chains after
+        the top-N1 share launches where the shapes allow it."""
         pv, w = self.pv, self.w
-        if self.split:
+        if self.form == "shared_launches":
+            pv.pv_prune_pipeline(self.vis, self.anc, self.q, self.kf, self.vf, self.heads, w.N1,
+                                 w.N2, out=self.pipe_out, workspace=self.wsp)
+        elif self.form == "two_streams":
             cur = self.torch.cuda.current_stream()
             pv.pv_prune_dedup(self.vis, self.anc, w.N1, out=self.o1, workspace=self.ws1,
                               split=(self.side, self.ev_sel, self.ev_done))
@@ -648,7 +665,9 @@ def main():
         return
     w = W.make_workload(args.workload)
     s = w.spec
-    step = Step(w, dev, split=args.split or args.streams == "2")
+    first = {"1": "one_stream", "2": "two_streams", "shared": "shared_launches",
+             "auto": "one_stream"}[args.streams]
+    step = Step(w, dev, form="two_streams" if args.split else first)
     stream = torch.cuda.current_stream(dev)
 
     # eager reference outputs
@@ -656,18 +675,21 @@ def main():
     torch.cuda.synchronize()
     ref = step.snapshot()
 
-    # one stream or two: the merge branch on a second stream overlaps the
+    # the form of the step: the merge branch on a second stream overlaps the
     # K/V gather and the head-aware score, which pays once those take longer
-    # than the cross-stream dependencies cost (the large workloads); picked
-    # from graph replays of both forms before any timed step
+    # than the cross-stream dependencies cost (the large workloads); shared
+    # launches take three kernel boundaries off the chain where the shapes
+    # allow them (the small batches).  Picked from graph replays of every
+    # form before any timed step.
     mode_us = {}
     if args.streams == "auto" and not args.split and not args.pmc_pass and not args.no_graph:
-        for sp in (False, True):
-            step.split = sp
-            mode_us["two_streams" if sp else "one_stream"] = graph_time_us(torch, step.run, reps=300)
-        step.split = mode_us["two_streams"] < mode_us["one_stream"]
+        for f in Step.FORMS:
+            step.form = f
+            mode_us[f] = graph_time_us(torch, step.run, reps=300)
+        step.form = min(mode_us, key=lambda f: mode_us[f])
         torch.cuda.synchronize()
-    split = step.split
+    form = step.form
+    split = form == "two_streams"
 
     if args.pmc_pass:
         # every dispatch of a library kernel here runs in the step's own
@@ -731,14 +753,17 @@ def main():
     kern_us = kernel_times(torch, step, args.kernel_reps, args.kernel_iters)
     breakdown = stage_breakdown(torch, step)
 
-    def other():
-        step.split = not split
-        try:
-            step.run()
-        finally:
-            step.split = split
-    breakdown["step_two_streams" if not split else "step_single_stream"] = graph_time_us(
-        torch, other)
+    for f in Step.FORMS:
+        if f == form:
+            continue
+
+        def other(f=f):
+            step.form = f
+            try:
+                step.run()
+            finally:
+                step.form = form
+        breakdown["step_" + f] = graph_time_us(torch, other)
     vis_heads = visual_heads_timing(torch, step)
     crit_text = critical_text_timing(torch, step)
     step.run()
@@ -787,10 +812,11 @@ def main():
         "data": "synthetic",
         "config": {"workload": s.name, "B": s.B, "Nv": s.Nv, "d": s.d, "H": s.H, "hd": s.hd,
                    "Nt": s.Nt, "heads_per_sample": int(w.heads.shape[1]), "N1": w.N1, "N2": w.N2,
-                   "streams": 2 if split else 1,
+                   "streams": 2 if split else 1, "step_form": form,
                    "timing": ("hip-graph replay of the full step" +
-                              (", merge branch on a second stream" if split else "")
-                              if graph is not None else "eager")},
+                              {"one_stream": "", "two_streams": ", merge branch on a second stream",
+                               "shared_launches": ", one pv_prune_pipeline call (shared launches)"}
+                              [form] if graph is not None else "eager")},
         "latency_us": {"pipeline": ms_per_step * 1000.0, "pipeline_single_replays": pct,
                        "pipeline_cold": cold, "kernels": kern_us,
                        "stages": stage_us, "calls_graph_replay": breakdown,

@@ -385,6 +385,50 @@ int pv_visual_heads_masked_timed(const void *q, const void *k, const int32_t *ro
                                  size_t workspace_bytes, void *stream, void *const *events,
                                  int n_events, int reps, int *n_kernels, const char **names);
 
+/* -------------------------------------------------------------------------
+ * The whole pruning step in one call (Sec. 4.1, 4.3 and 4.4 in sequence):
+ *   1. pv_prune_dedup of vis against the text anchors, with the merge
+ *      -> kept1 [B][budget1], score1 [B][Nv], assign [B][Nv],
+ *         merged [B][budget1][d];
+ *   2. the K and V rows of the budget1 kept tokens, compacted as
+ *      pv_prune_gather does: k_full, v_full [B][H][Nv][hd] -> k1, v1
+ *      [B][H][budget1][hd] (these stand for the keys and values that the
+ *      layers up to the pruning layer produce for the retained tokens);
+ *   3. pv_prune_head_aware of q [B][H][Nt][hd] over k1 with the host head
+ *      list heads_host [B][n_heads] -> kept2 [B][budget2] (indices into the
+ *      budget1 retained tokens), score2 [B][budget1];
+ *   4. the compaction of merged, k1 and v1 to the budget2 kept tokens
+ *      -> hidden2 [B][budget2][d], k2, v2 [B][H][budget2][hd].
+ * Every output is the bit-for-bit result of the four calls made one after
+ * another.  Where the shapes allow it (the split-k Gram and the plain merge
+ * of the dedup, the 16-row score blocks, 256-byte head rows, budget1 <= 256),
+ * the two independent chains that follow the top-budget1 selection share
+ * launches: the K/V compaction rides in the Gram's launch, the Gram's argmax
+ * in the score's, and the score's top-budget2 in the merge's, which takes
+ * three kernel boundaries off the step.  All pointers are DEVICE memory,
+ * contiguous, 16-byte aligned and required (none may be NULL); heads_host is
+ * HOST memory.  Errors as for the calls it combines.
+ * ---------------------------------------------------------------------- */
+size_t pv_pipeline_workspace_bytes(int B, int Nv, int Nt, int d, int H, int hd, int n_heads,
+                                   int budget1, int budget2, int dtype);
+
+int pv_prune_pipeline(const void *vis, const void *anchors, const void *q, const void *k_full,
+                      const void *v_full, const int32_t *heads_host, int n_heads, int B, int Nv,
+                      int Nt, int d, int H, int hd, int dtype, int budget1, int budget2,
+                      int32_t *kept1, float *score1, int32_t *assign, void *merged, void *k1,
+                      void *v1, int32_t *kept2, float *score2, void *hidden2, void *k2, void *v2,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+/* The same step with every kernel in its own launch (the reference against
+ * which the shared launches are checked; same arguments and results). */
+int pv_prune_pipeline_separate(const void *vis, const void *anchors, const void *q,
+                               const void *k_full, const void *v_full, const int32_t *heads_host,
+                               int n_heads, int B, int Nv, int Nt, int d, int H, int hd, int dtype,
+                               int budget1, int budget2, int32_t *kept1, float *score1,
+                               int32_t *assign, void *merged, void *k1, void *v1, int32_t *kept2,
+                               float *score2, void *hidden2, void *k2, void *v2, void *workspace,
+                               size_t workspace_bytes, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

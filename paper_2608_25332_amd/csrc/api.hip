@@ -6,6 +6,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include "pv_jobs.h"
 #include "pv_launch.h"
 
 #define PV_API extern "C" __attribute__((visibility("default")))
@@ -733,12 +734,13 @@ PV_API int pv_select_topk(const float *scores, int B, int n, int k, int32_t *kep
     return PV_OK;
 }
 
-PV_API int pv_prune_gather_batch(const pv_gather_desc *descs, int n_desc, const int32_t *idx, int B,
-                                 int k, void *stream) {
+namespace {
+
+int make_gather(const pv_gather_desc *descs, int n_desc, const int32_t *idx, int B, int k,
+                pv::GatherArgs &ga) {
     if (!descs || !idx) return PV_ERR_NULL;
     if (n_desc < 1 || n_desc > PV_MAX_GATHER || B < 1 || k < 1) return PV_ERR_SHAPE;
     if (!aligned16(idx)) return PV_ERR_ALIGN;
-    pv::GatherArgs ga;
     memset(&ga, 0, sizeof(ga));
     ga.n = n_desc;
     int64_t run = 0;
@@ -751,6 +753,16 @@ PV_API int pv_prune_gather_batch(const pv_gather_desc *descs, int n_desc, const 
         if (run > 0x7FFFFFFF) return PV_ERR_SHAPE;
     }
     ga.bstart[n_desc] = (int)run;
+    return PV_OK;
+}
+
+}  // namespace
+
+PV_API int pv_prune_gather_batch(const pv_gather_desc *descs, int n_desc, const int32_t *idx, int B,
+                                 int k, void *stream) {
+    pv::GatherArgs ga;
+    const int rc = make_gather(descs, n_desc, idx, B, k, ga);
+    if (rc != PV_OK) return rc;
     if (pv::launch_gather(ga, idx, B, k, (hipStream_t)stream) != hipSuccess) return PV_ERR_HIP;
     return PV_OK;
 }
@@ -774,4 +786,167 @@ PV_API int pv_prune_gather(const void *src, void *dst, const int32_t *idx, int B
     d.dst_group_stride = dst_group_stride;
     d.dst_row_stride = dst_row_stride;
     return pv_prune_gather_batch(&d, 1, idx, B, k, stream);
+}
+
+// ---------------------------------------------------------------------------
+// The whole pruning step in one call: dedup (with the merge), the K/V rows of
+// the N_1 kept tokens, the head-aware score and top-N_2, and the compaction of
+// the merged hidden rows, K and V to the N_2 kept tokens.
+// ---------------------------------------------------------------------------
+namespace {
+
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct PipeSizes {
+    size_t dedup, head, total;
+};
+
+PipeSizes pipe_sizes(int B, int Nv, int Nt, int d, int esz, int N1, int n_heads) {
+    const DedupPlan D = plan_dedup(nullptr, B, Nv, Nt, d, esz, N1, false, false, true);
+    const HeadPlan Hh = plan_head(nullptr, B, Nt, N1, n_heads, false);
+    return PipeSizes{round_up(D.bytes), Hh.bytes, round_up(D.bytes) + Hh.bytes};
+}
+
+pv_gather_desc kv_desc(const void *src, void *dst, int H, int n_src, int k, int64_t row) {
+    pv_gather_desc g;
+    g.src = src;
+    g.dst = dst;
+    g.n_src = n_src;
+    g.groups = H;
+    g.row_bytes = row;
+    g.src_batch_stride = (int64_t)H * n_src * row;
+    g.src_group_stride = (int64_t)n_src * row;
+    g.src_row_stride = row;
+    g.dst_batch_stride = (int64_t)H * k * row;
+    g.dst_group_stride = (int64_t)k * row;
+    g.dst_row_stride = row;
+    return g;
+}
+
+int pipeline_impl(const void *vis, const void *anchors, const void *q, const void *k_full,
+                  const void *v_full, const int32_t *heads, int n_heads, int B, int Nv, int Nt,
+                  int d, int H, int hd, int dtype, int N1, int N2, int32_t *kept1, float *score1,
+                  int32_t *assign, void *merged, void *k1, void *v1, int32_t *kept2, float *score2,
+                  void *hidden2, void *k2, void *v2, void *workspace, size_t ws_bytes, void *stream,
+                  int force_separate) {
+    int rc = check_dedup(vis, anchors, B, Nv, Nt, d, dtype, N1, kept1);
+    if (rc != PV_OK) return rc;
+    if (!q || !k_full || !v_full || !heads || !score1 || !assign || !merged || !k1 || !v1 ||
+        !kept2 || !score2 || !hidden2 || !k2 || !v2)
+        return PV_ERR_NULL;
+    rc = check_head(q, k1, heads, nullptr, n_heads, B, H, Nt, N1, hd, dtype, N2, kept2);
+    if (rc != PV_OK) return rc;
+    const int esz = (dtype == PV_BF16) ? 2 : 4;
+    const PipeSizes sz = pipe_sizes(B, Nv, Nt, d, esz, N1, n_heads);
+    if (!workspace || ws_bytes < sz.total) return PV_ERR_WORKSPACE;
+    const void *const ptrs[] = {vis,    anchors, q,      k_full, v_full, kept1,   score1, assign, merged,
+                                k1,     v1,      kept2,  score2, hidden2, k2,     v2,     workspace};
+    for (const void *p : ptrs)
+        if (!aligned16(p)) return PV_ERR_ALIGN;
+    const int64_t row_kv = (int64_t)hd * esz, row_h = (int64_t)d * esz;
+    const pv_gather_desc g1[2] = {kv_desc(k_full, k1, H, Nv, N1, row_kv),
+                                  kv_desc(v_full, v1, H, Nv, N1, row_kv)};
+    pv_gather_desc g2[3] = {kv_desc(merged, hidden2, 1, N1, N2, row_h),
+                            kv_desc(k1, k2, H, N1, N2, row_kv), kv_desc(v1, v2, H, N1, N2, row_kv)};
+    pv::GatherArgs ga1, ga2;
+    if ((rc = make_gather(g1, 2, kept1, B, N1, ga1)) != PV_OK) return rc;
+    if ((rc = make_gather(g2, 3, kept2, B, N2, ga2)) != PV_OK) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
+    char *ws_head = wsa + sz.dedup;
+
+    const DedupPlan P = plan_dedup(wsa, B, Nv, Nt, d, esz, N1, false, false, true);
+    const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
+    // the two chains after the top-N_1 share launches when the dedup takes
+    // the split-k Gram and the plain merge, and the score its 16-row blocks
+    const bool carry = !force_separate && P.Mp > 0 && !P.gram_big && !P.lists && N1 <= 256 &&
+                       pv::score_can_carry_reduce(dt, hd) &&
+                       !pv::score_uses_head_form(dt, B, H, n_heads, Nt, N1, hd);
+    if (!carry) {
+        rc = dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, N1, kept1, score1, assign, merged, wsa,
+                        sz.dedup, stream, nullptr, 0, 1, nullptr, nullptr);
+        if (rc != PV_OK) return rc;
+        if (pv::launch_gather(ga1, kept1, B, N1, st) != hipSuccess) return PV_ERR_HIP;
+        rc = head_impl(q, k1, heads, nullptr, n_heads, B, H, Nt, N1, hd, dtype, N2, kept2, score2,
+                       ws_head, sz.head, stream, nullptr, 0, 1, nullptr, nullptr);
+        if (rc != PV_OK) return rc;
+        if (pv::launch_gather(ga2, kept2, B, N2, st) != hipSuccess) return PV_ERR_HIP;
+        return PV_OK;
+    }
+    const HeadPlan Hh = plan_head(ws_head, B, Nt, N1, n_heads, false);
+    // cosine, centring, top-N_1
+    if (P.cos_full) {
+        if (pv::launch_cos_full(dt, vis, anchors, B, Nv, Nt, d, P.M, P.rowsum, P.invn, st) !=
+            hipSuccess)
+            return PV_ERR_HIP;
+    } else {
+        if (pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart, P.ssv, P.ssa,
+                                   st) != hipSuccess ||
+            pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M, P.rowsum,
+                                  P.invn, st) != hipSuccess)
+            return PV_ERR_HIP;
+    }
+    if (pv::launch_center(P.M, P.rowsum, nullptr, P.njt, B, Nt, Nv, score1, st) != hipSuccess ||
+        pv::launch_select(score1, B, Nv, N1, kept1, P.pruned, assign, st) != hipSuccess)
+        return PV_ERR_HIP;
+    // Gram partials + the K/V rows of the kept tokens
+    pv::GatherJob gj;
+    gj.ga = ga1;
+    gj.idx = kept1;
+    gj.k = N1;
+    gj.nblocks = ga1.bstart[ga1.n];
+    if (pv::launch_gram_partial(dt, vis, B, Nv, d, kept1, N1, P.pruned, P.Mp, P.ks_gram, P.gpart,
+                                st, &gj) != hipSuccess)
+        return PV_ERR_HIP;
+    // score blocks + the Gram's argmax
+    const pv::ReduceJob rj{P.gpart, B, P.Mp, N1, Nv, P.ks_gram, P.invn, P.pruned, kept1, assign,
+                           B * ((P.Mp + pv::kReduceRowsPerBlock - 1) / pv::kReduceRowsPerBlock)};
+    if (pv::launch_score_partial(dt, q, k1, heads, nullptr, nullptr, B, H, Nt, N1, hd, n_heads,
+                                 Hh.partial, st, &rj) != hipSuccess)
+        return PV_ERR_HIP;
+    // merge + the score's top-N_2
+    const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
+    const pv::SelectJob sj{Hh.partial, n_heads * Hh.nrb, N1, inv_norm, score2, N2, kept2, B};
+    if (pv::launch_merge(dt, vis, B, Nv, d, N1, assign, merged, st, &sj) != hipSuccess)
+        return PV_ERR_HIP;
+    // merged hidden rows, K and V of the N_2 kept tokens
+    if (pv::launch_gather(ga2, kept2, B, N2, st) != hipSuccess) return PV_ERR_HIP;
+    return PV_OK;
+}
+
+}  // namespace
+
+PV_API size_t pv_pipeline_workspace_bytes(int B, int Nv, int Nt, int d, int H, int hd,
+                                          int n_heads, int budget1, int budget2, int dtype) {
+    (void)H;
+    (void)hd;
+    (void)budget2;
+    if (B < 1 || Nv < 1 || Nt < 1 || d < 1 || n_heads < 1 || budget1 < 1 || budget1 > Nv)
+        return 0;
+    return pipe_sizes(B, Nv, Nt, d, (dtype == PV_BF16) ? 2 : 4, budget1, n_heads).total;
+}
+
+PV_API int pv_prune_pipeline(const void *vis, const void *anchors, const void *q,
+                             const void *k_full, const void *v_full, const int32_t *heads_host,
+                             int n_heads, int B, int Nv, int Nt, int d, int H, int hd, int dtype,
+                             int budget1, int budget2, int32_t *kept1, float *score1,
+                             int32_t *assign, void *merged, void *k1, void *v1, int32_t *kept2,
+                             float *score2, void *hidden2, void *k2, void *v2, void *workspace,
+                             size_t workspace_bytes, void *stream) {
+    return pipeline_impl(vis, anchors, q, k_full, v_full, heads_host, n_heads, B, Nv, Nt, d, H, hd,
+                         dtype, budget1, budget2, kept1, score1, assign, merged, k1, v1, kept2,
+                         score2, hidden2, k2, v2, workspace, workspace_bytes, stream, 0);
+}
+
+PV_API int pv_prune_pipeline_separate(const void *vis, const void *anchors, const void *q,
+                                      const void *k_full, const void *v_full,
+                                      const int32_t *heads_host, int n_heads, int B, int Nv,
+                                      int Nt, int d, int H, int hd, int dtype, int budget1,
+                                      int budget2, int32_t *kept1, float *score1, int32_t *assign,
+                                      void *merged, void *k1, void *v1, int32_t *kept2,
+                                      float *score2, void *hidden2, void *k2, void *v2,
+                                      void *workspace, size_t workspace_bytes, void *stream) {
+    return pipeline_impl(vis, anchors, q, k_full, v_full, heads_host, n_heads, B, Nv, Nt, d, H, hd,
+                         dtype, budget1, budget2, kept1, score1, assign, merged, k1, v1, kept2,
+                         score2, hidden2, k2, v2, workspace, workspace_bytes, stream, 1);
 }

@@ -18,10 +18,12 @@
 // Workgroups never wait on or signal each other: every cross-workgroup
 // dependency is a kernel boundary, so no kernel needs a device-wide fence
 // (on this chip a device-scope fence writes back and invalidates the L2).
+#include "pv_jobs.h"
 #include "pv_launch.h"
 #include "pv_tile_lds.h"
 
 #include <math.h>
+#include <string.h>
 
 namespace pv {
 
@@ -385,49 +387,9 @@ __global__ __launch_bounds__(NT) void select_kernel(const float *__restrict__ p,
 }
 
 // ----------------------------------------------------------------------------
-// Nearest centroid: best (cosine, slot) of every pruned row.  Ordering by
-// higher cosine, then lower slot, is a total order, so the maximum does not
-// depend on the order in which candidates are combined.
+// Nearest centroid: best (cosine, slot) of every pruned row, with the total
+// order of `better` (higher cosine, then lower slot).
 // ----------------------------------------------------------------------------
-__device__ __forceinline__ bool better(float v, int s, float bv, int bs) {
-    return v > bv || (v == bv && s < bs);
-}
-
-// The best (value, slot) of the 16 lanes of each row, left in every lane of
-// the row: DPP exchanges pairing lanes as an xor butterfly over 1, 2, 4, 8
-// does (the order is total, so any pairing gives the same best).
-__device__ __forceinline__ void row16_best(float &bv, int &bs) {
-    auto step = [&](float ov, int os) {
-        if (better(ov, os, bv, bs)) {
-            bv = ov;
-            bs = os;
-        }
-    };
-    step(dpp_f32<0xB1>(bv), dpp_i32<0xB1>(bs));
-    step(dpp_f32<0x4E>(bv), dpp_i32<0x4E>(bs));
-    step(dpp_f32<0x141>(bv), dpp_i32<0x141>(bs));
-    step(dpp_f32<0x140>(bv), dpp_i32<0x140>(bs));
-}
-
-// The same over the 64 lanes of a wave (every lane active), returned to
-// every lane: the rows, then their bests read from lanes 0, 16, 32, 48.
-__device__ __forceinline__ void wave_best(float &bv, int &bs) {
-    row16_best(bv, bs);
-    float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bv), 0));
-    int sl = __builtin_amdgcn_readlane(bs, 0);
-#pragma unroll
-    for (int r = 1; r < 4; ++r) {
-        const float rv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bv), 16 * r));
-        const int rs = __builtin_amdgcn_readlane(bs, 16 * r);
-        if (better(rv, rs, v, sl)) {
-            v = rv;
-            sl = rs;
-        }
-    }
-    bv = v;
-    bs = sl;
-}
-
 // gram_finish: grid (ceil(Mp / 256), B).  Best column tile of every pruned
 // row, combined in tile order with the total order above.
 constexpr int kFinNT = 256;
@@ -455,18 +417,23 @@ __global__ __launch_bounds__(kFinNT) void gram_finish_kernel(const float *__rest
 
 // gram_partial: 1-D grid over (sample, k slice, kept tile, pruned tile) in
 // XCD order (pruned tiles of one kept tile and slice are adjacent: they share
-// the kept rows).  Writes partial dot products part[ks][b][Mp][N1].
+// the kept rows).  Writes partial dot products part[ks][b][Mp][N1].  The
+// workgroups past the tiles, if any, run the gather job gj.
 template <int DT, int NS>
 __global__ __launch_bounds__(256) void gram_partial_kernel(
     const char *__restrict__ vis, int B, int Nv, int d_bytes, const int32_t *__restrict__ kept,
     int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn, int KS,
-    float *__restrict__ part) {
+    float *__restrict__ part, GatherJob gj) {
     using G = PTile<DT, NS>;
     __shared__ int32_t rowtok[G::ROWS];
+    const int total = B * KS * ntn * ntm;
+    if ((int)blockIdx.x >= total) {
+        gather_block(gj.ga, gj.idx, gj.k, blockIdx.x - total);
+        return;
+    }
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / 2, wn = wave % 2;
-    const int total = B * KS * ntn * ntm;
     const int tile = xcd_tile(blockIdx.x, total);
     const int mt = tile % ntm;
     const int nt = (tile / ntm) % ntn;
@@ -499,62 +466,13 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(
         }
 }
 
-// gram_reduce: grid (ceil(Mp / 2), B), 128 threads, one wave per pruned row.
-// Adds the k slices in slice order, forms the cosine to every kept token and
-// writes the slot of the best one (higher cosine, then lower slot).
+// gram_reduce: grid (ceil(Mp / 2), B), 128 threads, one wave per pruned row
+// (gram_reduce_row).
 template <int kGramU>
-__global__ __launch_bounds__(128) void gram_reduce_kernel(
-    const float *__restrict__ part, int B, int Mp, int N1, int Nv, int KS,
-    const float *__restrict__ invn, const int32_t *__restrict__ pruned,
-    const int32_t *__restrict__ kept, int32_t *__restrict__ assign) {
-    constexpr int CPL = 4;  // columns per lane per pass
-    const int lane = threadIdx.x & 63;
+__global__ __launch_bounds__(128) void gram_reduce_kernel(ReduceJob j) {
     const int m = blockIdx.x * 2 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int b = blockIdx.y;
-    if (m >= Mp) return;
-    const int tok = pruned[(size_t)b * Mp + m];
-    const float ia = invn[(size_t)b * Nv + tok];
-    const size_t kstride = (size_t)B * Mp * N1;
-    const float *prow = part + ((size_t)b * Mp + m) * N1;
-    float bv = -INFINITY;
-    int bs = 0x7FFFFFFF;
-    for (int n0 = 0; n0 < N1; n0 += 64 * CPL) {
-        int nc[CPL];
-        float kin[CPL], dot[CPL];
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            nc[c] = min(n0 + c * 64 + lane, N1 - 1);
-            kin[c] = invn[(size_t)b * Nv + kept[(size_t)b * N1 + nc[c]]];
-            dot[c] = 0.f;
-        }
-        // slices in blocks of kGramU with clamped addresses: every load of a
-        // block is in flight at once; added in slice order
-        for (int ks0 = 0; ks0 < KS; ks0 += kGramU) {
-            float v[kGramU][CPL];
-#pragma unroll
-            for (int u = 0; u < kGramU; ++u)
-#pragma unroll
-                for (int c = 0; c < CPL; ++c)
-                    v[u][c] = prow[(size_t)min(ks0 + u, KS - 1) * kstride + nc[c]];
-#pragma unroll
-            for (int u = 0; u < kGramU; ++u)
-                if (ks0 + u < KS) {
-#pragma unroll
-                    for (int c = 0; c < CPL; ++c) dot[c] += v[u][c];
-                }
-        }
-#pragma unroll
-        for (int c = 0; c < CPL; ++c) {
-            const int n = n0 + c * 64 + lane;
-            const float cs = dot[c] * ia * kin[c];
-            if (n < N1 && better(cs, n, bv, bs)) {
-                bv = cs;
-                bs = n;
-            }
-        }
-    }
-    wave_best(bv, bs);
-    if (lane == 0) assign[(size_t)b * Nv + tok] = bs;
+    if (m >= j.Mp) return;
+    gram_reduce_row<kGramU>(j, m, blockIdx.y, threadIdx.x & 63);
 }
 
 // gram_tile: the large, MFMA-bound Grams.  1-D grid over (sample, pruned
@@ -647,7 +565,8 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
 }
 
 // ----------------------------------------------------------------------------
-// merge: grid (ceil(d_bytes / 1024), N1, B), 256 threads.  A workgroup owns
+// merge: ceil(d_bytes / 1024) x N1 x B workgroups of 256 threads (1-D grid,
+// column block fastest, then slot, then sample).  A workgroup owns
 // one slot s and one 1 KB column block (16 bytes per lane).  The members of s
 // (the tokens whose assignment is s, the kept token itself included) are
 // listed in ascending token order with one block scan per round of 4096
@@ -713,17 +632,26 @@ template <int DT>
 __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict__ vis, int Nv,
                                                          int d_bytes,
                                                          const int32_t *__restrict__ assign,
-                                                         int N1, char *__restrict__ merged) {
+                                                         int N1, int B, char *__restrict__ merged,
+                                                         SelectJob sj) {
     constexpr int EPC = (DT == kBF16) ? 8 : 4;  // elements per 16-byte chunk
     constexpr int NW = kMergeNT / 64;
     __shared__ int list[kMergeRound];
     __shared__ int wsum[NW];
     __shared__ float part[NW][EPC][64];
-    const int s = blockIdx.y, b = blockIdx.z;
+    // 1-D grid: column block fastest, then slot, then sample; the workgroups
+    // past them, if any, run the score selection job sj (one per sample)
+    const int gx = (d_bytes / 16 + 63) / 64;
+    const int L = blockIdx.x, main_blocks = gx * N1 * B;
+    if (L >= main_blocks) {
+        score_select_block<kMergeNT, 1>(sj, L - main_blocks);
+        return;
+    }
+    const int bx = L % gx, s = (L / gx) % N1, b = L / (gx * N1);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nchunk = d_bytes >> 4;
-    const int c = blockIdx.x * 64 + lane;
+    const int c = bx * 64 + lane;
     const char *col = vis + (size_t)b * Nv * d_bytes + (size_t)min(c, nchunk - 1) * 16;
     const int32_t *as = assign + (size_t)b * Nv;
 
@@ -1132,23 +1060,29 @@ static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int3
 template <int DT, int NS>
 static void gram_partial_go(dim3 grid, const void *vis, int B, int Nv, int d_bytes,
                             const int32_t *kept, int N1, const int32_t *pruned, int Mp, int ntm,
-                            int ntn, int KS, float *part, hipStream_t st) {
+                            int ntn, int KS, float *part, const GatherJob &gj, hipStream_t st) {
     hipLaunchKernelGGL((gram_partial_kernel<DT, NS>), grid, dim3(256), 0, st, (const char *)vis, B,
-                       Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS, part);
+                       Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS, part, gj);
 }
 
 hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                                int N1, const int32_t *pruned, int Mp, int KS, float *part,
-                               hipStream_t st) {
+                               hipStream_t st, const GatherJob *with) {
     const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
     const int ntm = (Mp + kPT - 1) / kPT, ntn = (N1 + kPT - 1) / kPT;
-    const dim3 grid(B * KS * ntm * ntn);
+    GatherJob gj;
+    if (with) {
+        gj = *with;
+    } else {
+        memset(&gj, 0, sizeof(gj));
+    }
+    const dim3 grid(B * KS * ntm * ntn + gj.nblocks);
     if (dt == kBF16)
         gram_partial_go<kBF16, kSplitNS>(grid, vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn,
-                                         KS, part, st);
+                                         KS, part, gj, st);
     else
         gram_partial_go<kF32, kSplitNS>(grid, vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn,
-                                        KS, part, st);
+                                        KS, part, gj, st);
     return hipGetLastError();
 }
 
@@ -1156,10 +1090,10 @@ hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, 
                               const float *invn, const int32_t *pruned, const int32_t *kept,
                               int32_t *assign, hipStream_t st) {
     dim3 grid((Mp + 1) / 2, B);
-#define PV_RED_CASE(u)                                                                             \
-    case u:                                                                                        \
-        hipLaunchKernelGGL(gram_reduce_kernel<u>, grid, dim3(128), 0, st, part, B, Mp, N1, Nv, KS, \
-                           invn, pruned, kept, assign);                                            \
+    const ReduceJob j{part, B, Mp, N1, Nv, KS, invn, pruned, kept, assign, 0};
+#define PV_RED_CASE(u)                                                      \
+    case u:                                                                 \
+        hipLaunchKernelGGL(gram_reduce_kernel<u>, grid, dim3(128), 0, st, j); \
         break;
     switch (reduce_unroll(KS)) {
         PV_RED_CASE(1)
@@ -1217,15 +1151,25 @@ hipError_t launch_merge_csr(int dt, const void *vis, int B, int Nv, int d, int N
 }
 
 hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
-                        const int32_t *assign, void *merged, hipStream_t st) {
+                        const int32_t *assign, void *merged, hipStream_t st, const SelectJob *with) {
     const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
-    const dim3 grid((d_bytes / 16 + 63) / 64, N1, B);
+    SelectJob sj;
+    if (with) {
+        // the carried selection runs on the merge's 256 threads, one key each
+        if (with->N > kMergeNT) return hipErrorInvalidValue;
+        sj = *with;
+    } else {
+        memset(&sj, 0, sizeof(sj));
+    }
+    const long long blocks = (long long)((d_bytes / 16 + 63) / 64) * N1 * B + sj.nblocks;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const dim3 grid((unsigned)blocks);
     if (dt == kBF16)
         hipLaunchKernelGGL(merge_kernel<kBF16>, grid, dim3(kMergeNT), 0, st, (const char *)vis, Nv,
-                           d * 2, assign, N1, (char *)merged);
+                           d * 2, assign, N1, B, (char *)merged, sj);
     else
         hipLaunchKernelGGL(merge_kernel<kF32>, grid, dim3(kMergeNT), 0, st, (const char *)vis, Nv,
-                           d * 4, assign, N1, (char *)merged);
+                           d * 4, assign, N1, B, (char *)merged, sj);
     return hipGetLastError();
 }
 

@@ -14,8 +14,8 @@
 // second pass.  Only the selected heads are ever read and the attention map
 // is never written out.  score_select (one workgroup per sample) adds the per-(head,
 // row-block) column sums in a fixed order and runs the top-N_2.
+#include "pv_jobs.h"
 #include "pv_launch.h"
-#include "pv_device.h"
 #include "pv_tile_lds.h"
 
 #include <math.h>
@@ -71,20 +71,39 @@ enum HeadSource { kHeadsArg = 0, kHeadsDevice = 1, kHeadsAll = 2 };
 // one pass only, also carrying the sum of squared probabilities of each row,
 // and one number per workgroup: the sum over its rows of the row variance
 // (the head confidence of this row block).
+// Score kernels that can carry the split-k Gram's argmax (ReduceJob).
+constexpr bool score_carries_reduce(int nks, bool conf) { return nks == 4 && !conf; }
+
 template <int DT, int NKS, int MAXC, bool CONF>
 __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
     const int32_t *__restrict__ heads_dev, int head_src, const int32_t *__restrict__ row_mask,
     const float *__restrict__ row_lse, int b0, int H, int Nt, int N, int n_heads,
-    float scale_log2e, float *__restrict__ partial, int cols_in_lds) {
+    float scale_log2e, float *__restrict__ partial, int cols_in_lds, ReduceJob rj) {
     static_assert(!CONF || MAXC == 0, "the confidence needs no second pass");
+    static_assert(kScoreNT / 64 == kReduceRowsPerBlock, "one carried Gram row per wave");
     using S = ScoreStage<NKS>;
     __shared__ __attribute__((aligned(16))) char ring[S::NS][S::STAGE];
     __shared__ __attribute__((aligned(16))) char qrows[16 * S::RB];
     __shared__ float sm_m[4][16], sm_l[4][16], sm_s[CONF ? 4 : 1][16];
     __shared__ float row_m[16], row_il[16];
+    // the workgroups past the score blocks, if any, run the carried Gram
+    // argmax, one pruned row per wave.  Only the 256-byte head rows carry it:
+    // their occupancy is set by LDS, so the argmax's registers cost nothing
+    // there (launch_score_partial refuses a job for other widths).
+    const int n_score = (int)gridDim.x - rj.nblocks;
+    if constexpr (score_carries_reduce(NKS, CONF)) {
+        if ((int)blockIdx.x >= n_score) {
+            const int v = blockIdx.x - n_score;
+            const int per = (rj.Mp + kReduceRowsPerBlock - 1) / kReduceRowsPerBlock;
+            const int m = (v % per) * kReduceRowsPerBlock +
+                          __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+            if (m < rj.Mp) gram_reduce_row<16>(rj, m, v / per, threadIdx.x & 63);
+            return;
+        }
+    }
     const int nrb = (Nt + 15) / 16;
-    const int L = xcd_tile(blockIdx.x, gridDim.x);
+    const int L = xcd_tile(blockIdx.x, n_score);
     // heads.h lists the heads of samples b0, b0 + 1, ... of this launch
     const int rb = L % nrb, hi = (L / nrb) % n_heads, bl = L / (nrb * n_heads), b = b0 + bl;
     const int tid = threadIdx.x, lane = tid & 63;
@@ -631,41 +650,9 @@ __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
         out[j] = ((colpart[0][j] + colpart[1][j]) + colpart[2][j]) + colpart[3][j];
 }
 
-constexpr int kSelU = 16;
-
 template <int NT, int EMAX>
-__global__ __launch_bounds__(NT) void score_select_kernel(const float *__restrict__ partial,
-                                                          int nparts, int N, float inv_norm,
-                                                          float *__restrict__ v, int budget,
-                                                          int32_t *__restrict__ kept) {
-    __shared__ TopkSmem sm;
-    const int b = blockIdx.x;
-    const float *pb = partial + (size_t)b * nparts * N;
-    float *vb = v + (size_t)b * N;
-    const int E = topk_per_thread(N, NT), j0 = threadIdx.x * E;
-    uint32_t key[EMAX];
-#pragma unroll
-    for (int e = 0; e < EMAX; ++e) {
-        const int j = j0 + e;
-        key[e] = 0u;
-        if (e < E && j < N) {
-            // partials in blocks of kSelU with clamped addresses (all loads of a
-            // block in flight), added in part order
-            float s = 0.f;
-            for (int t0 = 0; t0 < nparts; t0 += kSelU) {
-                float v[kSelU];
-#pragma unroll
-                for (int u = 0; u < kSelU; ++u) v[u] = pb[(size_t)min(t0 + u, nparts - 1) * N + j];
-#pragma unroll
-                for (int u = 0; u < kSelU; ++u)
-                    if (t0 + u < nparts) s += v[u];
-            }
-            s *= inv_norm;
-            vb[j] = s;
-            key[e] = order_key(s);
-        }
-    }
-    block_topk<NT, EMAX>(key, N, budget, kept + (size_t)b * budget, nullptr, nullptr, sm);
+__global__ __launch_bounds__(NT) void score_select_kernel(SelectJob sj) {
+    score_select_block<NT, EMAX>(sj, blockIdx.x);
 }
 
 // The head lists travel as a kernel argument of bounded size: a launch covers
@@ -681,6 +668,7 @@ struct ScoreLaunch {
     float sl2e;
     float *partial;
     hipStream_t st;
+    const ReduceJob *rj = nullptr;  // carried by the first launch (score only)
 };
 
 // A host head list travels as a kernel argument of bounded size: a launch
@@ -702,11 +690,17 @@ static hipError_t score_go(const ScoreLaunch &a) {
         for (int i = 0; i < kMaxHeadArgs; ++i)
             ha.h[i] = (a.src == kHeadsArg && i < nb * a.n_heads)
                           ? a.heads_host[(size_t)b0 * a.n_heads + i] : 0;
-        dim3 grid(nrb * a.n_heads * nb);
+        ReduceJob rj;
+        if (a.rj && b0 == 0) {
+            rj = *a.rj;
+        } else {
+            memset(&rj, 0, sizeof(rj));
+        }
+        dim3 grid(nrb * a.n_heads * nb + rj.nblocks);
         hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC, CONF>), grid, dim3(kScoreNT),
                            in_lds ? cols : 0, a.st, (const char *)a.q, (const char *)a.k, ha,
                            a.heads_dev, a.src, a.row_mask, a.row_lse, b0, a.H, a.Nt, a.N,
-                           a.n_heads, a.sl2e, a.partial, in_lds ? 1 : 0);
+                           a.n_heads, a.sl2e, a.partial, in_lds ? 1 : 0, rj);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -802,15 +796,22 @@ bool score_uses_head_form(int dt, int B, int H, int n_heads, int Nt, int N, int 
            N <= kHeadMaxChunks * kScoreCK && (long long)B * n_heads >= 128;
 }
 
+bool score_can_carry_reduce(int dt, int hd) {
+    return score_carries_reduce(hd * ((dt == kBF16) ? 2 : 4) / 64, false);
+}
+
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, const float *row_lse, int B, int H,
                                 int Nt, int N, int hd, int n_heads, float *partial,
-                                hipStream_t st) {
+                                hipStream_t st, const ReduceJob *with) {
     ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg, nullptr,
                   row_lse, B, H, Nt, N, n_heads, 0.f, partial, st};
+    a.rj = with;
+    const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
+    if (with && !score_carries_reduce(nks, false)) return hipErrorInvalidValue;
     if (score_uses_head_form(dt, B, H, n_heads, Nt, N, hd)) {
+        if (with) return hipErrorInvalidValue;  // the whole-head form carries nothing
         a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
-        const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
         if (dt == kBF16) return nks == 2 ? score_head_go<kBF16, 2>(a) : score_head_go<kBF16, 4>(a);
         return nks == 2 ? score_head_go<kF32, 2>(a) : score_head_go<kF32, 4>(a);
     }
@@ -863,9 +864,9 @@ hipError_t launch_score_select(const float *partial, int B, int nparts, int N, f
                                float *v, int budget, int32_t *kept, hipStream_t st) {
     // as many threads as keys where possible: each thread's partial sums are
     // then all in flight at once
-#define PV_SEL_CASE(nt, e)                                                                         \
-    hipLaunchKernelGGL((score_select_kernel<nt, e>), dim3(B), dim3(nt), 0, st, partial, nparts, N, \
-                       inv_norm, v, budget, kept)
+    const SelectJob sj{partial, nparts, N, inv_norm, v, budget, kept, 0};
+#define PV_SEL_CASE(nt, e) \
+    hipLaunchKernelGGL((score_select_kernel<nt, e>), dim3(B), dim3(nt), 0, st, sj)
     if (N <= 256)
         PV_SEL_CASE(256, 1);
     else if (N <= 1024)

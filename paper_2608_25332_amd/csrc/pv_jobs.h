@@ -1,0 +1,219 @@
+// Steps of the pipeline that can ride along in another stage's launch.
+//
+// At small batches every kernel of the pipeline is a few microseconds, most
+// of it the launch itself, and the two chains that follow the top-N_1
+// selection (nearest kept token -> merge, and K/V of the kept tokens ->
+// head-aware score -> top-N_2) do not depend on each other.  A launch can
+// then carry the next step of the other chain as extra workgroups appended
+// after its own: the gather of the kept rows with the Gram, the Gram's
+// argmax with the score, the score's top-N_2 with the merge.  The bodies
+// below are those steps' workgroup bodies, shared by their own kernels and
+// by the kernels that carry them; a job with nblocks == 0 adds nothing.
+#pragma once
+
+#include "pv_device.h"
+#include "pv_launch.h"
+
+namespace pv {
+
+// ---- order-preserving row compaction (Sec. 4.1) ---------------------------
+constexpr int kGatherNT = 256;
+
+struct GatherJob {
+    GatherArgs ga;
+    const int32_t *idx;  // [B][k] kept indices
+    int k;
+    int nblocks;  // workgroups of the gather (ga.bstart[ga.n]); 0: none
+};
+
+// Workgroup blk of the gather: a contiguous span of 16-byte pieces of one
+// plane (sample x head group) of one tensor; rows whose index is out of
+// range are written as zeros.
+__device__ __forceinline__ void gather_block(const GatherArgs &ga, const int32_t *__restrict__ idx,
+                                             int k, int blk) {
+    int t = 0;
+#pragma unroll
+    for (int u = 1; u < kMaxGather; ++u)
+        if (u < ga.n && blk >= ga.bstart[u]) t = u;
+    const GatherDesc &g = ga.d[t];
+    const int local = blk - ga.bstart[t];
+    const int plane = local / g.bpp, sub = local - plane * g.bpp;
+    const int b = plane / g.groups, gr = plane - b * g.groups;
+    const int ppp = k * g.cpr;  // pieces in this plane
+    const char *s0 = g.src + b * g.sb + gr * g.sg;
+    char *d0 = g.dst + b * g.db + gr * g.dg;
+    const int32_t *ib = idx + (size_t)b * k;
+    uint4 v[kGatherIT];
+    int rr[kGatherIT], cc[kGatherIT];
+#pragma unroll
+    for (int it = 0; it < kGatherIT; ++it) {
+        const int e = (sub * kGatherIT + it) * kGatherNT + threadIdx.x;
+        const int ec = e < ppp ? e : ppp - 1;
+        const int r = ec / g.cpr, c = ec - r * g.cpr;
+        rr[it] = e < ppp ? r : -1;
+        cc[it] = c;
+        const int j = ib[r];
+        v[it] = uint4{0u, 0u, 0u, 0u};
+        if (j >= 0 && j < g.n_src) v[it] = ld16(s0 + (int64_t)j * g.sr + (int64_t)c * 16);
+    }
+#pragma unroll
+    for (int it = 0; it < kGatherIT; ++it)
+        if (rr[it] >= 0) st16(d0 + (int64_t)rr[it] * g.dr + (int64_t)cc[it] * 16, v[it]);
+}
+
+// ---- nearest kept token (Sec. 4.3, assignment of the pruned tokens) -------
+// Ordering by higher cosine, then lower slot, is a total order, so the
+// maximum does not depend on the order in which candidates are combined.
+__device__ __forceinline__ bool better(float v, int s, float bv, int bs) {
+    return v > bv || (v == bv && s < bs);
+}
+
+// The best (value, slot) of the 16 lanes of each row, left in every lane of
+// the row: DPP exchanges pairing lanes as an xor butterfly over 1, 2, 4, 8
+// does (the order is total, so any pairing gives the same best).
+__device__ __forceinline__ void row16_best(float &bv, int &bs) {
+    auto step = [&](float ov, int os) {
+        if (better(ov, os, bv, bs)) {
+            bv = ov;
+            bs = os;
+        }
+    };
+    step(dpp_f32<0xB1>(bv), dpp_i32<0xB1>(bs));
+    step(dpp_f32<0x4E>(bv), dpp_i32<0x4E>(bs));
+    step(dpp_f32<0x141>(bv), dpp_i32<0x141>(bs));
+    step(dpp_f32<0x140>(bv), dpp_i32<0x140>(bs));
+}
+
+// The same over the 64 lanes of a wave (every lane active), returned to
+// every lane: the rows, then their bests read from lanes 0, 16, 32, 48.
+__device__ __forceinline__ void wave_best(float &bv, int &bs) {
+    row16_best(bv, bs);
+    float v = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bv), 0));
+    int sl = __builtin_amdgcn_readlane(bs, 0);
+#pragma unroll
+    for (int r = 1; r < 4; ++r) {
+        const float rv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(bv), 16 * r));
+        const int rs = __builtin_amdgcn_readlane(bs, 16 * r);
+        if (better(rv, rs, v, sl)) {
+            v = rv;
+            sl = rs;
+        }
+    }
+    bv = v;
+    bs = sl;
+}
+
+// The split-k Gram's partial dot products part[KS][B][Mp][N1] -> the slot of
+// the nearest kept token of every pruned row.
+struct ReduceJob {
+    const float *part;
+    int B, Mp, N1, Nv, KS;
+    const float *invn;      // [B][Nv] inverse token norms
+    const int32_t *pruned;  // [B][Mp]
+    const int32_t *kept;    // [B][N1]
+    int32_t *assign;        // [B][Nv]
+    int nblocks;            // workgroups of four rows carried by another launch; 0: none
+};
+
+// One wave, pruned row m of sample b: adds the k slices in slice order,
+// forms the cosine to every kept token and writes the slot of the best one
+// (higher cosine, then lower slot).  Slices are loaded in blocks of U with
+// clamped addresses, so every load of a block is in flight at once.
+template <int U>
+__device__ __forceinline__ void gram_reduce_row(const ReduceJob &j, int m, int b, int lane) {
+    constexpr int CPL = 4;  // columns per lane per pass
+    const int tok = j.pruned[(size_t)b * j.Mp + m];
+    const float ia = j.invn[(size_t)b * j.Nv + tok];
+    const size_t kstride = (size_t)j.B * j.Mp * j.N1;
+    const float *prow = j.part + ((size_t)b * j.Mp + m) * j.N1;
+    float bv = -INFINITY;
+    int bs = 0x7FFFFFFF;
+    for (int n0 = 0; n0 < j.N1; n0 += 64 * CPL) {
+        int nc[CPL];
+        float kin[CPL], dot[CPL];
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            nc[c] = min(n0 + c * 64 + lane, j.N1 - 1);
+            kin[c] = j.invn[(size_t)b * j.Nv + j.kept[(size_t)b * j.N1 + nc[c]]];
+            dot[c] = 0.f;
+        }
+        for (int ks0 = 0; ks0 < j.KS; ks0 += U) {
+            float v[U][CPL];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int c = 0; c < CPL; ++c)
+                    v[u][c] = prow[(size_t)min(ks0 + u, j.KS - 1) * kstride + nc[c]];
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (ks0 + u < j.KS) {
+#pragma unroll
+                    for (int c = 0; c < CPL; ++c) dot[c] += v[u][c];
+                }
+        }
+#pragma unroll
+        for (int c = 0; c < CPL; ++c) {
+            const int n = n0 + c * 64 + lane;
+            const float cs = dot[c] * ia * kin[c];
+            if (n < j.N1 && better(cs, n, bv, bs)) {
+                bv = cs;
+                bs = n;
+            }
+        }
+    }
+    wave_best(bv, bs);
+    if (lane == 0) j.assign[(size_t)b * j.Nv + tok] = bs;
+}
+
+// Rows of gram_reduce_row per carried workgroup (one per wave of 256).
+constexpr int kReduceRowsPerBlock = 4;
+
+// ---- head-aware score: v and the top-N_2 (Eq. v, Sec. 4.2) ---------------
+constexpr int kSelU = 16;
+
+struct SelectJob {
+    const float *partial;  // [B][nparts][N] column sums of the score blocks
+    int nparts, N;
+    float inv_norm;        // 1 / (rows x heads)
+    float *v;              // [B][N]
+    int budget;
+    int32_t *kept;         // [B][budget]
+    int nblocks;           // samples carried by another launch; 0: none
+};
+
+// Workgroup of NT threads, sample b: v[j] = inv_norm x the partials of column
+// j added in part order, then the top-budget of v (lower index first among
+// equal scores), ascending.
+template <int NT, int EMAX>
+__device__ __forceinline__ void score_select_block(const SelectJob &sj, int b) {
+    __shared__ TopkSmem sm;
+    const int N = sj.N, nparts = sj.nparts;
+    const float *pb = sj.partial + (size_t)b * nparts * N;
+    float *vb = sj.v + (size_t)b * N;
+    const int E = topk_per_thread(N, NT), j0 = threadIdx.x * E;
+    uint32_t key[EMAX];
+#pragma unroll
+    for (int e = 0; e < EMAX; ++e) {
+        const int j = j0 + e;
+        key[e] = 0u;
+        if (e < E && j < N) {
+            // partials in blocks of kSelU with clamped addresses (all loads of a
+            // block in flight), added in part order
+            float s = 0.f;
+            for (int t0 = 0; t0 < nparts; t0 += kSelU) {
+                float v[kSelU];
+#pragma unroll
+                for (int u = 0; u < kSelU; ++u) v[u] = pb[(size_t)min(t0 + u, nparts - 1) * N + j];
+#pragma unroll
+                for (int u = 0; u < kSelU; ++u)
+                    if (t0 + u < nparts) s += v[u];
+            }
+            s *= sj.inv_norm;
+            vb[j] = s;
+            key[e] = order_key(s);
+        }
+    }
+    block_topk<NT, EMAX>(key, N, sj.budget, sj.kept + (size_t)b * sj.budget, nullptr, nullptr, sm);
+}
+
+}  // namespace pv

@@ -6,6 +6,11 @@
 
 namespace pv {
 
+// Work another launch can carry (pv_jobs.h).
+struct GatherJob;
+struct ReduceJob;
+struct SelectJob;
+
 // Element types of the inputs (values of pv_dtype).
 constexpr int kF32 = 0;
 constexpr int kBF16 = 1;
@@ -50,9 +55,10 @@ hipError_t launch_center(const float *M, const float *rowsum, const int32_t *row
                          int B, int Nt, int Nv, float *p, hipStream_t st);
 hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kept, int32_t *pruned,
                          int32_t *slot_of, hipStream_t st);
+// with: a gather carried as extra workgroups of the same launch (or NULL).
 hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                                int N1, const int32_t *pruned, int Mp, int KS, float *part,
-                               hipStream_t st);
+                               hipStream_t st, const GatherJob *with = nullptr);
 hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, int KS,
                               const float *invn, const int32_t *pruned, const int32_t *kept,
                               int32_t *assign, hipStream_t st);
@@ -79,8 +85,10 @@ hipError_t launch_merge_csr(int dt, const void *vis, int B, int Nv, int d, int N
 inline bool merge_uses_lists(int B, int N1, int d_bytes) {
     return B > 1 || (long long)((d_bytes / 16 + 63) / 64) * N1 * 4 > d_bytes;
 }
+// with: the score's top-N_2 carried as extra workgroups (N <= 256), or NULL.
 hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
-                        const int32_t *assign, void *merged, hipStream_t st);
+                        const int32_t *assign, void *merged, hipStream_t st,
+                        const SelectJob *with = nullptr);
 
 // ---- critical text tokens (Sec. 4.2)
 hipError_t launch_text_gram_sum(const float *part, int B, int Nt, int KS, float *G,
@@ -95,12 +103,16 @@ hipError_t launch_text_rank(const float *G, int B, int Nt, float *r, int32_t *ma
 // writes one row of column sums per (sample, head) instead of one per
 // 16-row block.
 bool score_uses_head_form(int dt, int B, int H, int n_heads, int Nt, int N, int hd);
+// Whether the score launch can carry the split-k Gram's argmax (ReduceJob).
+bool score_can_carry_reduce(int dt, int hd);
 // row_lse [B][H][Nt] (may be NULL): log-sum-exp of each row's scaled logits
 // over the non-visual keys, which join the softmax normaliser.
+// with: the split-k Gram's argmax carried as extra workgroups of the first
+// launch (or NULL); not with the whole-head form.
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, const float *row_lse, int B, int H,
                                 int Nt, int N, int hd, int n_heads, float *partial,
-                                hipStream_t st);
+                                hipStream_t st, const ReduceJob *with = nullptr);
 // Head confidence of every head, per 16-row block: partial[b][h][rb].
 // row_mask as for launch_center: the rows summed into the confidence.
 hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask, int B,

@@ -127,6 +127,13 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_gather_batch.restype = _i
     lib.pv_select_topk.argtypes = [_vp, _i, _i, _i, _vp, _vp, _vp, _vp]
     lib.pv_select_topk.restype = _i
+    lib.pv_pipeline_workspace_bytes.argtypes = [_i] * 10
+    lib.pv_pipeline_workspace_bytes.restype = _sz
+    pipe = [_vp] * 6 + [_i] * 10 + [_vp] * 12 + [_sz, _vp]
+    lib.pv_prune_pipeline.argtypes = pipe
+    lib.pv_prune_pipeline.restype = _i
+    lib.pv_prune_pipeline_separate.argtypes = pipe
+    lib.pv_prune_pipeline_separate.restype = _i
     _lib = lib
     return lib
 
@@ -518,3 +525,68 @@ def pv_prune_gather_batch(srcs: Sequence[torch.Tensor], idx: torch.Tensor, *,
     rc = lib.pv_prune_gather_batch(descs, len(srcs), idx.data_ptr(), B, k, _stream(idx.device))
     _check("pv_prune_gather_batch", rc, lib)
     return res
+
+
+# ----------------------------------------------------------------------------
+PIPELINE_OUTPUTS = ("kept1", "score1", "assign", "merged", "k1", "v1", "kept2", "score2",
+                    "hidden2", "k2", "v2")
+
+
+def pv_pipeline_workspace_bytes(B: int, Nv: int, Nt: int, d: int, H: int, hd: int, n_heads: int,
+                                budget1: int, budget2: int, dtype: int) -> int:
+    return int(load().pv_pipeline_workspace_bytes(B, Nv, Nt, d, H, hd, n_heads, budget1, budget2,
+                                                  dtype))
+
+
+def pv_prune_pipeline(vis: torch.Tensor, anchors: torch.Tensor, q: torch.Tensor,
+                      k_full: torch.Tensor, v_full: torch.Tensor, heads, budget1: int,
+                      budget2: int, *, out: Optional[dict] = None,
+                      workspace: Optional[torch.Tensor] = None, separate: bool = False):
+    """The whole pruning step (pv_prune_pipeline): dedup with the merge, the
+    K/V rows of the budget1 kept tokens, head-aware score and top-budget2,
+    and the compaction of the merged hidden rows, K and V.
+    vis [B,Nv,d], anchors [B,Nt,d], q [B,H,Nt,hd], k_full / v_full
+    [B,H,Nv,hd] (one dtype), heads: host ints [B, n_heads].  Returns a dict
+    with PIPELINE_OUTPUTS (see include/provip.h for their shapes).
+    separate=True runs every kernel in its own launch
+    (pv_prune_pipeline_separate)."""
+    import numpy as np
+
+    lib = load()
+    for t, n in ((vis, "vis"), (anchors, "anchors"), (q, "q"), (k_full, "k_full"),
+                 (v_full, "v_full")):
+        _contig(t, n)
+    B, Nv, d = vis.shape
+    _, H, Nt, hd = q.shape
+    if (tuple(anchors.shape) != (B, Nt, d) or tuple(k_full.shape) != (B, H, Nv, hd)
+            or tuple(v_full.shape) != (B, H, Nv, hd)
+            or len({t.dtype for t in (vis, anchors, q, k_full, v_full)}) != 1):
+        raise ValueError("anchors [B,Nt,d], q [B,H,Nt,hd], k_full/v_full [B,H,Nv,hd], one dtype")
+    hs = np.ascontiguousarray(np.asarray(heads, dtype=np.int32).reshape(B, -1))
+    n_heads = hs.shape[1]
+    code = _dtype_code(vis)
+    dev, dt = vis.device, vis.dtype
+    i32, f32 = torch.int32, torch.float32
+    shapes = {"kept1": ((B, budget1), i32), "score1": ((B, Nv), f32), "assign": ((B, Nv), i32),
+              "merged": ((B, budget1, d), dt), "k1": ((B, H, budget1, hd), dt),
+              "v1": ((B, H, budget1, hd), dt), "kept2": ((B, budget2), i32),
+              "score2": ((B, budget1), f32), "hidden2": ((B, budget2, d), dt),
+              "k2": ((B, H, budget2, hd), dt), "v2": ((B, H, budget2, hd), dt)}
+    o = dict(out) if out is not None else {}
+    for name in PIPELINE_OUTPUTS:
+        if o.get(name) is None:
+            shp, ty = shapes[name]
+            o[name] = torch.empty(shp, dtype=ty, device=dev)
+        else:
+            _contig(o[name], name)
+    nbytes = lib.pv_pipeline_workspace_bytes(B, Nv, Nt, d, H, hd, n_heads, budget1, budget2, code)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    fn = lib.pv_prune_pipeline_separate if separate else lib.pv_prune_pipeline
+    rc = fn(vis.data_ptr(), anchors.data_ptr(), q.data_ptr(), k_full.data_ptr(),
+            v_full.data_ptr(), hs.ctypes.data_as(ctypes.c_void_p), n_heads, B, Nv,
+            Nt, d, H, hd, code, budget1, budget2, *[o[n].data_ptr() for n in PIPELINE_OUTPUTS],
+            workspace.data_ptr(), workspace.numel(), _stream(dev))
+    _check("pv_prune_pipeline_separate" if separate else "pv_prune_pipeline", rc, lib)
+    o["workspace"] = workspace
+    return o

@@ -298,3 +298,46 @@ def test_every_kernel_launch_stub_is_defined():
                          text=True, check=True).stdout
     missing = [l.split()[-1] for l in out.splitlines() if "__device_stub__" in l]
     assert not missing, missing[:5]
+
+
+def _pipe(lib, heads=(1,), B=1, Nv=64, Nt=16, d=256, H=4, hd=64, dt=1, b1=32, b2=16, ws=FAKE,
+          wsb=1 << 40, null_at=None, misalign_at=None):
+    hs = np.ascontiguousarray(np.asarray(heads, dtype=np.int32).reshape(B, -1))
+    ptrs = [FAKE] * 16  # vis anchors q k_full v_full, then the 11 outputs
+    if null_at is not None:
+        ptrs[null_at] = None
+    if misalign_at is not None:
+        ptrs[misalign_at] = FAKE + 8
+    return lib.pv_prune_pipeline(*ptrs[:5], hs.ctypes.data_as(ctypes.c_void_p), hs.shape[1], B,
+                                 Nv, Nt, d, H, hd, dt, b1, b2, *ptrs[5:], ws, wsb, None)
+
+
+def test_pipeline_validation(lib):
+    for i in range(16):
+        assert _pipe(lib, null_at=i) == -1, i   # every pointer is required
+    assert _pipe(lib, ws=None) == -6
+    assert _pipe(lib, wsb=8) == -6
+    assert _pipe(lib, b1=0) == -3
+    assert _pipe(lib, b1=65) == -3
+    assert _pipe(lib, b2=33) == -3              # budget2 counts the budget1 kept tokens
+    assert _pipe(lib, heads=(4,)) == -4
+    assert _pipe(lib, heads=(1, 1)) == -4
+    assert _pipe(lib, d=100) == -2
+    assert _pipe(lib, hd=48) == -2
+    assert _pipe(lib, dt=3) == -5
+    assert _pipe(lib, misalign_at=3) == -8
+    assert _pipe(lib, misalign_at=12) == -8
+    for f in (lib.pv_prune_pipeline, lib.pv_prune_pipeline_separate):
+        hs = np.zeros((1, 1), np.int32)
+        assert f(None, *[FAKE] * 4, hs.ctypes.data_as(ctypes.c_void_p), 1, 1, 64, 16, 256, 4, 64,
+                 1, 32, 16, *[FAKE] * 11, FAKE, 1 << 40, None) == -1
+
+
+def test_pipeline_workspace_query(lib):
+    f = lib.pv_pipeline_workspace_bytes
+    small = f(1, 576, 64, 4096, 32, 128, 4, 192, 64, 1)
+    dedup = lib.pv_dedup_workspace_bytes(1, 576, 64, 4096, 192, 1)
+    head = lib.pv_head_aware_workspace_bytes(1, 32, 64, 192, 128, 4, 64, 1)
+    assert small >= dedup and small >= head
+    assert f(16, 576, 64, 4096, 32, 128, 4, 192, 64, 1) > small
+    assert f(1, 576, 64, 4096, 32, 128, 4, 0, 64, 1) == 0

@@ -8,8 +8,8 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 
-@pytest.mark.parametrize("split", [True, False])
-def test_graph_replays_match_eager(split):
+@pytest.mark.parametrize("form", ["one_stream", "two_streams", "shared_launches"])
+def test_graph_replays_match_eager(form):
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     import bench
@@ -17,7 +17,7 @@ def test_graph_replays_match_eager(split):
 
     dev = torch.device("cuda:0")
     w = W.make_workload(2)
-    step = bench.Step(w, dev, split=split)
+    step = bench.Step(w, dev, form=form)
     step.run()
     torch.cuda.synchronize()
     ref = step.snapshot()
@@ -33,7 +33,7 @@ def test_graph_replays_match_eager(split):
     torch.cuda.synchronize()
     for i in range(5):
         # scribble over the outputs eagerly, then replay
-        for t in (step.o1["kept"], step.o1["assign"], step.o2["kept"], step.hid2):
+        for t in (step.o1["kept"], step.o1["assign"], step.o2["kept"], step.hid2, step.k2):
             t.zero_()
         torch.cuda.synchronize()
         g.replay()

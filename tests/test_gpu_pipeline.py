@@ -1,0 +1,154 @@
+"""The whole pruning step in one call (pv_prune_pipeline).
+
+Where the shapes allow it, the two chains that follow the top-N_1 selection
+share launches (the K/V compaction rides in the Gram's launch, the Gram's
+argmax in the score's, the score's top-N_2 in the merge's).  Every output
+must equal, bit for bit, the same step with every kernel in its own launch
+(pv_prune_pipeline_separate, which is the four calls made one after another),
+and the step must match the oracle as the separate calls do.
+"""
+
+from __future__ import annotations
+
+import functools
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_25332_amd import workloads as W
+from parity_util import check_kept, to_dev, to_host
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2608_25332_amd import provip
+    provip.load()
+
+
+@functools.lru_cache(maxsize=None)
+def workload(wid: int):
+    return W.make_workload(wid)
+
+
+def _inputs(w):
+    dt = w.dtype
+    return (to_dev(w.vis, dt), to_dev(w.anchors, dt), to_dev(w.q, dt), to_dev(w.k_full, dt),
+            to_dev(w.v_full, dt))
+
+
+def _both(ins, heads, N1, N2):
+    """Outputs of the shared-launch step and of the separate step, each into
+    buffers filled with a different pattern first (so that nothing left in
+    place by one passes for the other's result)."""
+    from paper_2608_25332_amd import provip
+    res = []
+    for sep, fill in ((False, 0x5A), (True, 0x3C)):
+        o = provip.pv_prune_pipeline(*ins, heads, N1, N2, separate=sep)
+        for n in provip.PIPELINE_OUTPUTS:
+            o[n].view(torch.uint8).fill_(fill)
+        o = provip.pv_prune_pipeline(*ins, heads, N1, N2, out=o, workspace=o["workspace"],
+                                     separate=sep)
+        torch.cuda.synchronize()
+        res.append(o)
+    return res
+
+
+def _assert_same(a, b):
+    from paper_2608_25332_amd import provip
+    for n in provip.PIPELINE_OUTPUTS:
+        x = a[n].view(torch.uint8) if a[n].dtype == torch.bfloat16 else a[n]
+        y = b[n].view(torch.uint8) if b[n].dtype == torch.bfloat16 else b[n]
+        assert torch.equal(x, y), f"{n} differs between the shared and the separate launches"
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_pipeline_shared_launches_equal_separate(wid):
+    w = workload(wid)
+    _say(f"[pipeline] workload {wid} ({w.spec.name})")
+    fused, sep = _both(_inputs(w), w.heads, w.N1, w.N2)
+    _assert_same(fused, sep)
+
+
+@pytest.mark.parametrize("wid", [1, 2])
+def test_pipeline_against_oracle(wid):
+    """The step bench.py times, in one call, against the oracle."""
+    from paper_2608_25332_amd import provip
+    w = workload(wid)
+    dt = w.dtype
+    _say(f"[pipeline-oracle] workload {wid}")
+    o = provip.pv_prune_pipeline(*_inputs(w), w.heads, w.N1, w.N2)
+    torch.cuda.synchronize()
+    ref = oracle.dedup(w.anchors, w.vis, w.N1)
+    kept1 = to_host(o["kept1"])
+    for b in range(w.spec.B):
+        check_kept(kept1[b], ref["p"][b], w.N1, dt)
+    k1_ref = np.stack([w.k_full[b][:, kept1[b]] for b in range(w.spec.B)])
+    v1_ref = np.stack([w.v_full[b][:, kept1[b]] for b in range(w.spec.B)])
+    assert np.array_equal(to_host(o["k1"]), k1_ref)
+    assert np.array_equal(to_host(o["v1"]), v1_ref)
+    _, v_ref = oracle.head_aware(w.q, k1_ref, w.heads, w.N2)
+    kept2 = to_host(o["kept2"])
+    for b in range(w.spec.B):
+        check_kept(kept2[b], v_ref[b], w.N2, dt)
+    assert np.array_equal(to_host(o["hidden2"]), oracle.gather(to_host(o["merged"]), kept2))
+    assert np.array_equal(to_host(o["k2"]), oracle.gather(k1_ref, kept2))
+    assert np.array_equal(to_host(o["v2"]), oracle.gather(v1_ref, kept2))
+    if wid == 1:
+        # the tiny fp32 workload is checked in full: assignment and merge too
+        assert np.array_equal(to_host(o["kept1"]), ref["kept"])
+        assert np.array_equal(to_host(o["assign"]), ref["assign"])
+        m = to_host(o["merged"])
+        assert np.max(np.abs(m - ref["merged"])) <= 1e-5 * np.max(np.abs(ref["merged"]))
+
+
+# (B, Nv, Nt, d, H, hd, n_heads, N1, N2, dtype): shapes on both sides of
+# every condition for the shared launches
+EDGE = [
+    (1, 100, 5, 64, 2, 128, 1, 37, 5, "bf16"),      # ragged tiles, one head
+    (3, 300, 20, 256, 8, 128, 3, 256, 100, "bf16"),  # N1 = 256: the widest carried top-k
+    (2, 300, 20, 256, 8, 128, 3, 257, 100, "bf16"),  # N1 = 257: separate launches
+    (2, 64, 16, 256, 4, 64, 2, 64, 10, "bf16"),      # N1 = Nv: nothing pruned, no Gram
+    (2, 90, 16, 128, 4, 64, 2, 40, 7, "bf16"),       # 128-byte head rows: separate launches
+    (2, 90, 16, 128, 4, 64, 2, 40, 7, "f32"),        # 256-byte fp32 head rows: shared
+    (65, 100, 80, 64, 8, 128, 8, 40, 10, "bf16"),    # 520 head pairs: two score launches
+    (1, 40, 3, 64, 1, 128, 1, 1, 1, "bf16"),         # budgets of one
+    (8, 576, 64, 512, 8, 128, 4, 192, 64, "bf16"),   # LLaVA-like token counts, narrow rows
+]
+
+
+@pytest.mark.parametrize("B,Nv,Nt,d,H,hd,nh,N1,N2,dt", EDGE)
+def test_pipeline_edges(B, Nv, Nt, d, H, hd, nh, N1, N2, dt):
+    _say(f"[pipeline-edge] B={B} Nv={Nv} Nt={Nt} d={d} H={H} hd={hd} heads={nh} "
+         f"N1={N1} N2={N2} {dt}")
+    rng = np.random.default_rng(B * 1000 + Nv + N1)
+    f = (lambda a: W.bf16_round(a)) if dt == "bf16" else (lambda a: a)
+    vis = f(rng.standard_normal((B, Nv, d)).astype(np.float32))
+    anc = f(rng.standard_normal((B, Nt, d)).astype(np.float32))
+    q = f(rng.standard_normal((B, H, Nt, hd)).astype(np.float32))
+    kf = f(rng.standard_normal((B, H, Nv, hd)).astype(np.float32))
+    vf = f(rng.standard_normal((B, H, Nv, hd)).astype(np.float32))
+    heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+    ins = tuple(to_dev(a, dt) for a in (vis, anc, q, kf, vf))
+    fused, sep = _both(ins, heads, N1, N2)
+    _assert_same(fused, sep)
+    # the separate step is the four calls: check its selections against the
+    # oracle on the first and last sample
+    for b in sorted({0, B - 1}):
+        ref = oracle.dedup(anc[b:b + 1], vis[b:b + 1], N1)
+        check_kept(to_host(sep["kept1"])[b], ref["p"][0], N1, dt)
+        kept1 = to_host(sep["kept1"])[b]
+        _, v_ref = oracle.head_aware(q[b:b + 1], kf[b:b + 1][:, :, kept1], heads[b:b + 1], N2)
+        check_kept(to_host(sep["kept2"])[b], v_ref[0], N2, dt)
