@@ -7,14 +7,17 @@
 //                 and partial sums of squares
 //   cos_reduce    adds the k slices: cosines M, per-tile row sums, inverse
 //                 norms of the visual tokens
-//   center        p[j] = max_i (M[i][j] - mean_i)  (folded into select when
-//                 one sample's M is small)
+//   center        p[j] = max_i (M[i][j] - mean_i)
 //   select        top-N_1 radix select, one workgroup per sample
 //   gram_partial  pruned x kept Gram on MFMA, split over k
 //   gram_reduce   adds the k slices, cosine, row argmax -> assignment
 //     (large Grams instead: gram_tile, LDS-staged 128x128 full-k tiles with a
 //      fused argmax per column tile, then gram_finish across column tiles)
 //   merge         centroid <- mean of itself and its members
+// In the whole-step call (pv_prune_pipeline) gram_partial also carries the
+// K/V compaction of the kept tokens and merge the head-aware top-N_2, as
+// extra workgroups (pv_jobs.h); gram_reduce's rows then ride in the score's
+// launch.
 // Workgroups never wait on or signal each other: every cross-workgroup
 // dependency is a kernel boundary, so no kernel needs a device-wide fence
 // (on this chip a device-scope fence writes back and invalidates the L2).
@@ -417,20 +420,15 @@ __global__ __launch_bounds__(kFinNT) void gram_finish_kernel(const float *__rest
 
 // gram_partial: 1-D grid over (sample, k slice, kept tile, pruned tile) in
 // XCD order (pruned tiles of one kept tile and slice are adjacent: they share
-// the kept rows).  Writes partial dot products part[ks][b][Mp][N1].  The
-// workgroups past the tiles, if any, run the gather job gj.
+// the kept rows).  Writes partial dot products part[ks][b][Mp][N1].
 template <int DT, int NS>
-__global__ __launch_bounds__(256) void gram_partial_kernel(
-    const char *__restrict__ vis, int B, int Nv, int d_bytes, const int32_t *__restrict__ kept,
-    int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn, int KS,
-    float *__restrict__ part, GatherJob gj) {
+__device__ __forceinline__ void gram_partial_tile(const char *__restrict__ vis, int B, int Nv,
+                                                  int d_bytes, const int32_t *__restrict__ kept,
+                                                  int N1, const int32_t *__restrict__ pruned,
+                                                  int Mp, int ntm, int ntn, int KS,
+                                                  float *__restrict__ part, int total) {
     using G = PTile<DT, NS>;
     __shared__ int32_t rowtok[G::ROWS];
-    const int total = B * KS * ntn * ntm;
-    if ((int)blockIdx.x >= total) {
-        gather_block(gj.ga, gj.idx, gj.k, blockIdx.x - total);
-        return;
-    }
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave / 2, wn = wave % 2;
@@ -464,6 +462,31 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(
                 if (m < Mp && n < N1) pb[(size_t)m * N1 + n] = acc[fm][fn][e];
             }
         }
+}
+
+template <int DT, int NS>
+__global__ __launch_bounds__(256) void gram_partial_kernel(
+    const char *__restrict__ vis, int B, int Nv, int d_bytes, const int32_t *__restrict__ kept,
+    int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn, int KS,
+    float *__restrict__ part) {
+    gram_partial_tile<DT, NS>(vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS, part,
+                              B * KS * ntn * ntm);
+}
+
+// The same with a gather carried by the workgroups past the tiles (a kernel
+// of its own: the job's arguments would slow the plain form down).
+template <int DT, int NS>
+__global__ __launch_bounds__(256) void gram_partial_gather_kernel(
+    const char *__restrict__ vis, int B, int Nv, int d_bytes, const int32_t *__restrict__ kept,
+    int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn, int KS,
+    float *__restrict__ part, GatherJob gj) {
+    const int total = B * KS * ntn * ntm;
+    if ((int)blockIdx.x >= total) {
+        gather_block(gj.ga, gj.idx, gj.k, blockIdx.x - total);
+        return;
+    }
+    gram_partial_tile<DT, NS>(vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS, part,
+                              total);
 }
 
 // gram_reduce: grid (ceil(Mp / 2), B), 128 threads, one wave per pruned row
@@ -565,8 +588,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
 }
 
 // ----------------------------------------------------------------------------
-// merge: ceil(d_bytes / 1024) x N1 x B workgroups of 256 threads (1-D grid,
-// column block fastest, then slot, then sample).  A workgroup owns
+// merge: grid (ceil(d_bytes / 1024), N1, B), 256 threads.  A workgroup owns
 // one slot s and one 1 KB column block (16 bytes per lane).  The members of s
 // (the tokens whose assignment is s, the kept token itself included) are
 // listed in ascending token order with one block scan per round of 4096
@@ -632,22 +654,20 @@ template <int DT>
 __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict__ vis, int Nv,
                                                          int d_bytes,
                                                          const int32_t *__restrict__ assign,
-                                                         int N1, int B, char *__restrict__ merged,
+                                                         int N1, char *__restrict__ merged,
                                                          SelectJob sj) {
     constexpr int EPC = (DT == kBF16) ? 8 : 4;  // elements per 16-byte chunk
     constexpr int NW = kMergeNT / 64;
     __shared__ int list[kMergeRound];
     __shared__ int wsum[NW];
     __shared__ float part[NW][EPC][64];
-    // 1-D grid: column block fastest, then slot, then sample; the workgroups
-    // past them, if any, run the score selection job sj (one per sample)
-    const int gx = (d_bytes / 16 + 63) / 64;
-    const int L = blockIdx.x, main_blocks = gx * N1 * B;
-    if (L >= main_blocks) {
-        score_select_block<kMergeNT, 1>(sj, L - main_blocks);
+    const int bx = blockIdx.x, s = blockIdx.y, b = blockIdx.z;
+    // a carried score selection takes one more row of slots: workgroup
+    // (0, N1, b) runs sample b's, the rest of that row has nothing to do
+    if (s >= N1) {
+        if (bx == 0 && b < sj.nblocks) score_select_block<kMergeNT, 1>(sj, b);
         return;
     }
-    const int bx = L % gx, s = (L / gx) % N1, b = L / (gx * N1);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nchunk = d_bytes >> 4;
@@ -1060,9 +1080,15 @@ static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int3
 template <int DT, int NS>
 static void gram_partial_go(dim3 grid, const void *vis, int B, int Nv, int d_bytes,
                             const int32_t *kept, int N1, const int32_t *pruned, int Mp, int ntm,
-                            int ntn, int KS, float *part, const GatherJob &gj, hipStream_t st) {
-    hipLaunchKernelGGL((gram_partial_kernel<DT, NS>), grid, dim3(256), 0, st, (const char *)vis, B,
-                       Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS, part, gj);
+                            int ntn, int KS, float *part, const GatherJob *gj, hipStream_t st) {
+    if (gj)
+        hipLaunchKernelGGL((gram_partial_gather_kernel<DT, NS>), grid, dim3(256), 0, st,
+                           (const char *)vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS,
+                           part, *gj);
+    else
+        hipLaunchKernelGGL((gram_partial_kernel<DT, NS>), grid, dim3(256), 0, st,
+                           (const char *)vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS,
+                           part);
 }
 
 hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
@@ -1070,19 +1096,13 @@ hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, co
                                hipStream_t st, const GatherJob *with) {
     const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
     const int ntm = (Mp + kPT - 1) / kPT, ntn = (N1 + kPT - 1) / kPT;
-    GatherJob gj;
-    if (with) {
-        gj = *with;
-    } else {
-        memset(&gj, 0, sizeof(gj));
-    }
-    const dim3 grid(B * KS * ntm * ntn + gj.nblocks);
+    const dim3 grid(B * KS * ntm * ntn + (with ? with->nblocks : 0));
     if (dt == kBF16)
         gram_partial_go<kBF16, kSplitNS>(grid, vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn,
-                                         KS, part, gj, st);
+                                         KS, part, with, st);
     else
         gram_partial_go<kF32, kSplitNS>(grid, vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn,
-                                        KS, part, gj, st);
+                                        KS, part, with, st);
     return hipGetLastError();
 }
 
@@ -1161,15 +1181,16 @@ hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
     } else {
         memset(&sj, 0, sizeof(sj));
     }
-    const long long blocks = (long long)((d_bytes / 16 + 63) / 64) * N1 * B + sj.nblocks;
-    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-    const dim3 grid((unsigned)blocks);
+    // (measured: the same work on a 1-D grid with the coordinates decoded in
+    // the kernel is 15% slower at B = 1)
+    if (sj.nblocks != 0 && sj.nblocks != B) return hipErrorInvalidValue;
+    const dim3 grid((d_bytes / 16 + 63) / 64, N1 + (sj.nblocks ? 1 : 0), B);
     if (dt == kBF16)
         hipLaunchKernelGGL(merge_kernel<kBF16>, grid, dim3(kMergeNT), 0, st, (const char *)vis, Nv,
-                           d * 2, assign, N1, B, (char *)merged, sj);
+                           d * 2, assign, N1, (char *)merged, sj);
     else
         hipLaunchKernelGGL(merge_kernel<kF32>, grid, dim3(kMergeNT), 0, st, (const char *)vis, Nv,
-                           d * 4, assign, N1, B, (char *)merged, sj);
+                           d * 4, assign, N1, (char *)merged, sj);
     return hipGetLastError();
 }
 

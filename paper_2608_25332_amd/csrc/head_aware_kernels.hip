@@ -71,37 +71,24 @@ enum HeadSource { kHeadsArg = 0, kHeadsDevice = 1, kHeadsAll = 2 };
 // one pass only, also carrying the sum of squared probabilities of each row,
 // and one number per workgroup: the sum over its rows of the row variance
 // (the head confidence of this row block).
-// Score kernels that can carry the split-k Gram's argmax (ReduceJob).
+// Score kernels that can carry the split-k Gram's argmax (ReduceJob): the
+// 256-byte head rows, whose occupancy is set by LDS, so the argmax's
+// registers cost nothing there.
 constexpr bool score_carries_reduce(int nks, bool conf) { return nks == 4 && !conf; }
 
+// One score workgroup; n_score: workgroups of the launch that score.
 template <int DT, int NKS, int MAXC, bool CONF>
-__global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
-    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
+__device__ __forceinline__ void score_partial_block(
+    const char *__restrict__ q, const char *__restrict__ k, const HeadArgs &heads,
     const int32_t *__restrict__ heads_dev, int head_src, const int32_t *__restrict__ row_mask,
     const float *__restrict__ row_lse, int b0, int H, int Nt, int N, int n_heads,
-    float scale_log2e, float *__restrict__ partial, int cols_in_lds, ReduceJob rj) {
+    float scale_log2e, float *__restrict__ partial, int cols_in_lds, int n_score) {
     static_assert(!CONF || MAXC == 0, "the confidence needs no second pass");
-    static_assert(kScoreNT / 64 == kReduceRowsPerBlock, "one carried Gram row per wave");
     using S = ScoreStage<NKS>;
     __shared__ __attribute__((aligned(16))) char ring[S::NS][S::STAGE];
     __shared__ __attribute__((aligned(16))) char qrows[16 * S::RB];
     __shared__ float sm_m[4][16], sm_l[4][16], sm_s[CONF ? 4 : 1][16];
     __shared__ float row_m[16], row_il[16];
-    // the workgroups past the score blocks, if any, run the carried Gram
-    // argmax, one pruned row per wave.  Only the 256-byte head rows carry it:
-    // their occupancy is set by LDS, so the argmax's registers cost nothing
-    // there (launch_score_partial refuses a job for other widths).
-    const int n_score = (int)gridDim.x - rj.nblocks;
-    if constexpr (score_carries_reduce(NKS, CONF)) {
-        if ((int)blockIdx.x >= n_score) {
-            const int v = blockIdx.x - n_score;
-            const int per = (rj.Mp + kReduceRowsPerBlock - 1) / kReduceRowsPerBlock;
-            const int m = (v % per) * kReduceRowsPerBlock +
-                          __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-            if (m < rj.Mp) gram_reduce_row<16>(rj, m, v / per, threadIdx.x & 63);
-            return;
-        }
-    }
     const int nrb = (Nt + 15) / 16;
     const int L = xcd_tile(blockIdx.x, n_score);
     // heads.h lists the heads of samples b0, b0 + 1, ... of this launch
@@ -436,6 +423,40 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     }
 }
 
+template <int DT, int NKS, int MAXC, bool CONF>
+__global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
+    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
+    const int32_t *__restrict__ heads_dev, int head_src, const int32_t *__restrict__ row_mask,
+    const float *__restrict__ row_lse, int b0, int H, int Nt, int N, int n_heads,
+    float scale_log2e, float *__restrict__ partial, int cols_in_lds) {
+    score_partial_block<DT, NKS, MAXC, CONF>(q, k, heads, heads_dev, head_src, row_mask, row_lse,
+                                             b0, H, Nt, N, n_heads, scale_log2e, partial,
+                                             cols_in_lds, gridDim.x);
+}
+
+// The same with the split-k Gram's argmax carried by the workgroups past the
+// score blocks, one pruned row per wave (a kernel of its own: the job slows
+// the plain form down).
+template <int DT, int NKS, int MAXC>
+__global__ __launch_bounds__(kScoreNT) void score_partial_reduce_kernel(
+    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
+    const int32_t *__restrict__ heads_dev, int head_src, const float *__restrict__ row_lse,
+    int b0, int H, int Nt, int N, int n_heads, float scale_log2e, float *__restrict__ partial,
+    int cols_in_lds, ReduceJob rj) {
+    static_assert(kScoreNT / 64 == kReduceRowsPerBlock, "one carried Gram row per wave");
+    const int n_score = (int)gridDim.x - rj.nblocks;
+    if ((int)blockIdx.x >= n_score) {
+        const int v = blockIdx.x - n_score;
+        const int per = (rj.Mp + kReduceRowsPerBlock - 1) / kReduceRowsPerBlock;
+        const int m = (v % per) * kReduceRowsPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        if (m < rj.Mp) gram_reduce_row<16>(rj, m, v / per, threadIdx.x & 63);
+        return;
+    }
+    score_partial_block<DT, NKS, MAXC, false>(q, k, heads, heads_dev, head_src, nullptr, row_lse,
+                                              b0, H, Nt, N, n_heads, scale_log2e, partial,
+                                              cols_in_lds, n_score);
+}
+
 // ----------------------------------------------------------------------------
 // score_head: one workgroup per (selected head, sample), for up to 64 text
 // rows and 256 keys (the shapes of the paper's layers).  Wave w owns text
@@ -697,10 +718,21 @@ static hipError_t score_go(const ScoreLaunch &a) {
             memset(&rj, 0, sizeof(rj));
         }
         dim3 grid(nrb * a.n_heads * nb + rj.nblocks);
-        hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC, CONF>), grid, dim3(kScoreNT),
-                           in_lds ? cols : 0, a.st, (const char *)a.q, (const char *)a.k, ha,
-                           a.heads_dev, a.src, a.row_mask, a.row_lse, b0, a.H, a.Nt, a.N,
-                           a.n_heads, a.sl2e, a.partial, in_lds ? 1 : 0, rj);
+        bool carried = false;
+        if constexpr (score_carries_reduce(NKS, CONF)) {
+            if (rj.nblocks > 0) {
+                hipLaunchKernelGGL((score_partial_reduce_kernel<DT, NKS, MAXC>), grid,
+                                   dim3(kScoreNT), in_lds ? cols : 0, a.st, (const char *)a.q,
+                                   (const char *)a.k, ha, a.heads_dev, a.src, a.row_lse, b0, a.H,
+                                   a.Nt, a.N, a.n_heads, a.sl2e, a.partial, in_lds ? 1 : 0, rj);
+                carried = true;
+            }
+        }
+        if (!carried)
+            hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC, CONF>), grid, dim3(kScoreNT),
+                               in_lds ? cols : 0, a.st, (const char *)a.q, (const char *)a.k, ha,
+                               a.heads_dev, a.src, a.row_mask, a.row_lse, b0, a.H, a.Nt, a.N,
+                               a.n_heads, a.sl2e, a.partial, in_lds ? 1 : 0);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
