@@ -17,8 +17,12 @@ events (the step is launch-bound at this size).  Then every kernel of the
 step is launched back to back between two HIP events on the library's
 stream (the *_timed entry points with reps > 1) for its average duration,
 which gives the per-kernel and per-stage roofline positions and the
-roofline of the dominant kernel.  The CPU oracle is timed on a bounded
-sample of the same workload on the host.
+roofline of the dominant kernel.  The step takes whichever of three forms
+replays fastest: the four calls on one stream, the merge branch on a
+second stream, or one pv_prune_pipeline call whose two chains after the
+top-N1 share launches; the roofline line is taken over the kernels of the
+form that is timed (pv_prune_pipeline_timed for the shared launches).  The
+CPU oracle is timed on a bounded sample of the same workload on the host.
 
 Prints one JSON line.
 """
@@ -190,6 +194,18 @@ STAGE_OF = {
 }
 
 
+# kernel of the shared-launch step (pv_prune_pipeline_timed's name) -> the
+# two kernels of the separate step whose work it does
+SHARED_PARTS = {"gram_partial+gather_kv1": ("gram_partial", "gather_kv1"),
+                "score_partial+gram_reduce": ("score_partial", "gram_reduce"),
+                "merge+score_select": ("merge", "score_select")}
+# kernel name in bench.py -> the name rocprofv3 reports (without "_kernel" and
+# template arguments), which keys the committed counter summaries
+PROFILED_NAME = {"gram_partial+gather_kv1": "gram_partial_gather",
+                 "score_partial+gram_reduce": "score_partial_reduce",
+                 "merge+score_select": "merge", "gather_kv1": "gather", "gather_hkv2": "gather"}
+
+
 def algorithmic(w):
     """Algorithmic HBM bytes and flops per launch (one batch), per kernel and
     per stage: the bytes a step must move at least (its inputs read once,
@@ -232,6 +248,10 @@ def algorithmic(w):
         # read + write the hidden, K and V rows of the N2 kept tokens
         "gather_hkv2": dict(bytes=2 * B * N2 * (d + 2 * H * hd) * e, flops=0.0),
     }
+    # kernels of the shared-launch step: each carries the work of two
+    for a, b in SHARED_PARTS.values():
+        kern[a + "+" + b] = dict(bytes=kern[a]["bytes"] + kern[b]["bytes"],
+                                 flops=kern[a]["flops"] + kern[b]["flops"])
     stage = {
         "cosine": dict(bytes=B * (Nv + Nt) * d * e + B * Nv * 4, flops=2.0 * B * Nt * Nv * d),
         "select": kern["select"],
@@ -325,6 +345,40 @@ def kernel_times(torch, step, reps, iters):
     return {k: float(np.median(v)) for k, v in per.items()}
 
 
+def shared_kernel_times(torch, step, reps, iters):
+    """kernel_times for the shared-launch step (pv_prune_pipeline_timed):
+    every launch of the one call repeated reps times back to back between
+    two HIP events.  Empty when the shapes give no shared launches."""
+    pv, w = step.pv, step.w
+    per = {}
+    hold_ms = 4.0
+    done = 0
+    while done < iters:
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(10)]
+        spun = torch.cuda.Event()
+        for e in ev + [spun]:
+            e.record()
+        torch.cuda.synchronize()
+        torch.cuda._sleep(sleep_cycles_for(torch, hold_ms))
+        spun.record()
+        r = pv.pv_prune_pipeline(step.vis, step.anc, step.q, step.kf, step.vf, step.heads, w.N1,
+                                 w.N2, out=step.pipe_out, workspace=step.wsp, events=ev,
+                                 reps=reps)
+        starved = spun.query()
+        torch.cuda.synchronize()
+        if r["n_kernels"] == 0:
+            return {}
+        if starved:
+            hold_ms *= 2
+            if hold_ms > 1000:
+                raise RuntimeError("host cannot keep ahead of the GPU for the kernel timing")
+            continue
+        done += 1
+        for i, nm in enumerate(r["kernel_names"]):
+            per.setdefault(nm, []).append(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / reps)
+    return {k: float(np.median(v)) for k, v in per.items()}
+
+
 def csrc_digest():
     """Digest of the library sources: counter figures taken from a build with
     another digest no longer describe the kernels."""
@@ -357,7 +411,7 @@ def load_traffic(workload, kernel):
         return None
     if rec.get("csrc_digest") != csrc_digest():
         return None
-    k = rec.get("kernels", {}).get(kernel)
+    k = rec.get("kernels", {}).get(PROFILED_NAME.get(kernel, kernel))
     if not k:
         return None
     return float(k["fetch_bytes"]) + float(k["write_bytes"])
@@ -704,7 +758,8 @@ def main():
         for _ in range(3):
             dst.copy_(src)
         torch.cuda.synchronize()
-        print(json.dumps({"pmc_pass": s.name, "steps": args.steps, "calib_bytes": n,
+        print(json.dumps({"pmc_pass": s.name, "step_form": form, "steps": args.steps,
+                          "calib_bytes": n,
                           "csrc_digest": csrc_digest()}), flush=True)
         return
 
@@ -751,6 +806,7 @@ def main():
 
     # ---- per-kernel durations (each kernel launched back to back between events)
     kern_us = kernel_times(torch, step, args.kernel_reps, args.kernel_iters)
+    shared_us = shared_kernel_times(torch, step, args.kernel_reps, args.kernel_iters)
     breakdown = stage_breakdown(torch, step)
 
     for f in Step.FORMS:
@@ -788,11 +844,18 @@ def main():
         r = roof(alg_s[st_name], us * 1e-6)
         stages[st_name] = {"us": us, "bound": r["bound"], "achieved": r["achieved"],
                            "unit": r["unit"], "frac": r["frac"]}
-    dom = max(kern_us, key=lambda k: kern_us[k])
+    shared = {}
+    for k, us in shared_us.items():
+        r = roof(alg_k[k], us * 1e-6)
+        shared[k] = {"us": us, "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"],
+                     "frac": r["frac"]}
+    # the dominant kernel of the form the timed step runs
+    step_us = shared_us if form == "shared_launches" and shared_us else kern_us
+    dom = max(step_us, key=lambda k: step_us[k])
     a = alg_k[dom]
-    rf = roof(a, kern_us[dom] * 1e-6)
+    rf = roof(a, step_us[dom] * 1e-6)
     traffic = load_traffic(s.name, dom)
-    rf.update({"traffic": traffic, "kernel": dom, "kernel_us": kern_us[dom],
+    rf.update({"traffic": traffic, "kernel": dom, "kernel_us": step_us[dom],
                "algorithmic_bytes": a["bytes"], "algorithmic_flops": a["flops"]})
 
     toks = s.B * s.Nv
@@ -819,10 +882,12 @@ def main():
                               [form] if graph is not None else "eager")},
         "latency_us": {"pipeline": ms_per_step * 1000.0, "pipeline_single_replays": pct,
                        "pipeline_cold": cold, "kernels": kern_us,
+                       "kernels_shared_launches": shared_us or None,
                        "stages": stage_us, "calls_graph_replay": breakdown,
                        "stream_choice_us": mode_us or None},
         "roofline": rf,
         "roofline_kernels": kernels,
+        "roofline_kernels_shared_launches": shared or None,
         "roofline_stages": stages,
         # outside the step: visual-head identification at the same layer and
         # critical text selection over the same text rows

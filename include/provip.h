@@ -419,6 +419,21 @@ int pv_prune_pipeline(const void *vis, const void *anchors, const void *q, const
                       void *v1, int32_t *kept2, float *score2, void *hidden2, void *k2, void *v2,
                       void *workspace, size_t workspace_bytes, void *stream);
 
+/* The step with an event recorded around each of its launches, as the other
+ * *_timed calls do (profiling only).  Where the launches are shared, the
+ * kernel names are "cos_full" (or "cos_partial", "cos_reduce"), "center",
+ * "select", "gram_partial+gather_kv1", "score_partial+gram_reduce",
+ * "merge+score_select" and "gather_hkv2"; where they are not, the step runs
+ * once without events and *n_kernels is 0. */
+int pv_prune_pipeline_timed(const void *vis, const void *anchors, const void *q,
+                            const void *k_full, const void *v_full, const int32_t *heads_host,
+                            int n_heads, int B, int Nv, int Nt, int d, int H, int hd, int dtype,
+                            int budget1, int budget2, int32_t *kept1, float *score1,
+                            int32_t *assign, void *merged, void *k1, void *v1, int32_t *kept2,
+                            float *score2, void *hidden2, void *k2, void *v2, void *workspace,
+                            size_t workspace_bytes, void *stream, void *const *events,
+                            int n_events, int reps, int *n_kernels, const char **names);
+
 /* The same step with every kernel in its own launch (the reference against
  * which the shared launches are checked; same arguments and results). */
 int pv_prune_pipeline_separate(const void *vis, const void *anchors, const void *q,

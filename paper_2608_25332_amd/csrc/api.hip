@@ -828,7 +828,10 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
                   int d, int H, int hd, int dtype, int N1, int N2, int32_t *kept1, float *score1,
                   int32_t *assign, void *merged, void *k1, void *v1, int32_t *kept2, float *score2,
                   void *hidden2, void *k2, void *v2, void *workspace, size_t ws_bytes, void *stream,
-                  int force_separate) {
+                  int force_separate, void *const *events = nullptr, int n_events = 0,
+                  int reps = 1, int *n_kernels = nullptr, const char **names = nullptr) {
+    if (reps < 1) return PV_ERR_SHAPE;
+    if (n_kernels) *n_kernels = 0;
     int rc = check_dedup(vis, anchors, B, Nv, Nt, d, dtype, N1, kept1);
     if (rc != PV_OK) return rc;
     if (!q || !k_full || !v_full || !heads || !score1 || !assign || !merged || !k1 || !v1 ||
@@ -852,6 +855,8 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
     if ((rc = make_gather(g1, 2, kept1, B, N1, ga1)) != PV_OK) return rc;
     if ((rc = make_gather(g2, 3, kept2, B, N2, ga2)) != PV_OK) return rc;
     hipStream_t st = (hipStream_t)stream;
+    Trace tr{events, n_events, names, reps, st};
+    if (!tr.handles_ok()) return PV_ERR_NULL;
     char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
     char *ws_head = wsa + sz.dedup;
 
@@ -876,18 +881,30 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
     const HeadPlan Hh = plan_head(ws_head, B, Nt, N1, n_heads, false);
     // cosine, centring, top-N_1
     if (P.cos_full) {
-        if (pv::launch_cos_full(dt, vis, anchors, B, Nv, Nt, d, P.M, P.rowsum, P.invn, st) !=
-            hipSuccess)
+        if (!tr.launch("cos_full", [&] {
+                return pv::launch_cos_full(dt, vis, anchors, B, Nv, Nt, d, P.M, P.rowsum, P.invn,
+                                           st);
+            }))
             return PV_ERR_HIP;
     } else {
-        if (pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart, P.ssv, P.ssa,
-                                   st) != hipSuccess ||
-            pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M, P.rowsum,
-                                  P.invn, st) != hipSuccess)
+        if (!tr.launch("cos_partial", [&] {
+                return pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart,
+                                              P.ssv, P.ssa, st);
+            }))
+            return PV_ERR_HIP;
+        if (!tr.launch("cos_reduce", [&] {
+                return pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M,
+                                             P.rowsum, P.invn, st);
+            }))
             return PV_ERR_HIP;
     }
-    if (pv::launch_center(P.M, P.rowsum, nullptr, P.njt, B, Nt, Nv, score1, st) != hipSuccess ||
-        pv::launch_select(score1, B, Nv, N1, kept1, P.pruned, assign, st) != hipSuccess)
+    if (!tr.launch("center", [&] {
+            return pv::launch_center(P.M, P.rowsum, nullptr, P.njt, B, Nt, Nv, score1, st);
+        }))
+        return PV_ERR_HIP;
+    if (!tr.launch("select", [&] {
+            return pv::launch_select(score1, B, Nv, N1, kept1, P.pruned, assign, st);
+        }))
         return PV_ERR_HIP;
     // Gram partials + the K/V rows of the kept tokens
     pv::GatherJob gj;
@@ -895,22 +912,31 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
     gj.idx = kept1;
     gj.k = N1;
     gj.nblocks = ga1.bstart[ga1.n];
-    if (pv::launch_gram_partial(dt, vis, B, Nv, d, kept1, N1, P.pruned, P.Mp, P.ks_gram, P.gpart,
-                                st, &gj) != hipSuccess)
+    if (!tr.launch("gram_partial+gather_kv1", [&] {
+            return pv::launch_gram_partial(dt, vis, B, Nv, d, kept1, N1, P.pruned, P.Mp,
+                                           P.ks_gram, P.gpart, st, &gj);
+        }))
         return PV_ERR_HIP;
     // score blocks + the Gram's argmax
     const pv::ReduceJob rj{P.gpart, B, P.Mp, N1, Nv, P.ks_gram, P.invn, P.pruned, kept1, assign,
                            B * ((P.Mp + pv::kReduceRowsPerBlock - 1) / pv::kReduceRowsPerBlock)};
-    if (pv::launch_score_partial(dt, q, k1, heads, nullptr, nullptr, B, H, Nt, N1, hd, n_heads,
-                                 Hh.partial, st, &rj) != hipSuccess)
+    if (!tr.launch("score_partial+gram_reduce", [&] {
+            return pv::launch_score_partial(dt, q, k1, heads, nullptr, nullptr, B, H, Nt, N1, hd,
+                                            n_heads, Hh.partial, st, &rj);
+        }))
         return PV_ERR_HIP;
     // merge + the score's top-N_2
     const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
     const pv::SelectJob sj{Hh.partial, n_heads * Hh.nrb, N1, inv_norm, score2, N2, kept2, B};
-    if (pv::launch_merge(dt, vis, B, Nv, d, N1, assign, merged, st, &sj) != hipSuccess)
+    if (!tr.launch("merge+score_select", [&] {
+            return pv::launch_merge(dt, vis, B, Nv, d, N1, assign, merged, st, &sj);
+        }))
         return PV_ERR_HIP;
     // merged hidden rows, K and V of the N_2 kept tokens
-    if (pv::launch_gather(ga2, kept2, B, N2, st) != hipSuccess) return PV_ERR_HIP;
+    if (!tr.launch("gather_hkv2", [&] { return pv::launch_gather(ga2, kept2, B, N2, st); }))
+        return PV_ERR_HIP;
+    if (!tr.after_all()) return PV_ERR_HIP;
+    if (n_kernels) *n_kernels = tr.launched;
     return PV_OK;
 }
 
@@ -949,4 +975,19 @@ PV_API int pv_prune_pipeline_separate(const void *vis, const void *anchors, cons
     return pipeline_impl(vis, anchors, q, k_full, v_full, heads_host, n_heads, B, Nv, Nt, d, H, hd,
                          dtype, budget1, budget2, kept1, score1, assign, merged, k1, v1, kept2,
                          score2, hidden2, k2, v2, workspace, workspace_bytes, stream, 1);
+}
+
+PV_API int pv_prune_pipeline_timed(const void *vis, const void *anchors, const void *q,
+                                   const void *k_full, const void *v_full,
+                                   const int32_t *heads_host, int n_heads, int B, int Nv, int Nt,
+                                   int d, int H, int hd, int dtype, int budget1, int budget2,
+                                   int32_t *kept1, float *score1, int32_t *assign, void *merged,
+                                   void *k1, void *v1, int32_t *kept2, float *score2,
+                                   void *hidden2, void *k2, void *v2, void *workspace,
+                                   size_t workspace_bytes, void *stream, void *const *events,
+                                   int n_events, int reps, int *n_kernels, const char **names) {
+    return pipeline_impl(vis, anchors, q, k_full, v_full, heads_host, n_heads, B, Nv, Nt, d, H, hd,
+                         dtype, budget1, budget2, kept1, score1, assign, merged, k1, v1, kept2,
+                         score2, hidden2, k2, v2, workspace, workspace_bytes, stream, 0, events,
+                         n_events, reps, n_kernels, names);
 }

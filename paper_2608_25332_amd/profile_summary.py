@@ -46,7 +46,7 @@ def split_trace(path: str):
     rows = list(csv.DictReader(open(path)))
     rows.sort(key=lambda r: int(r["Start_Timestamp"]))
     names = [short(r["Kernel_Name"]) for r in rows]
-    grid = [r["Grid_Size_X"] for r in rows]
+    grid = [(r["Grid_Size_X"], r.get("Grid_Size_Y", "1"), r.get("Grid_Size_Z", "1")) for r in rows]
     dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
     b2b, seq = defaultdict(list), defaultdict(list)
     i = 0
@@ -58,6 +58,26 @@ def split_trace(path: str):
         i = j + 1
     mean = lambda v: sum(v) / len(v) if v else float("nan")
     return {n: (mean(b2b[n]), mean(seq[n])) for n in set(b2b) | set(seq)}
+
+
+def b2b_by_shape(path: str):
+    """Mean duration (us) and count of the back-to-back dispatches (runs of at
+    least 10 identical launches) per (kernel, grid size in work-items)."""
+    rows = list(csv.DictReader(open(path)))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    key = [(short(r["Kernel_Name"]), "x".join(r.get(f"Grid_Size_{a}", "1") for a in "XYZ"))
+           for r in rows]
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
+    out = defaultdict(list)
+    i = 0
+    while i < len(rows):
+        j = i
+        while j + 1 < len(rows) and key[j + 1] == key[i]:
+            j += 1
+        if j - i + 1 >= 10:
+            out[key[i]].extend(dur[i:j + 1])
+        i = j + 1
+    return {k: (sum(v) / len(v), len(v)) for k, v in out.items()}
 
 
 def trace(args) -> str:
@@ -80,12 +100,25 @@ def trace(args) -> str:
         b, q = split.get(n, (float("nan"), float("nan")))
         out.append(f"| `{n}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | {b:.2f} | "
                    f"{q:.2f} | {float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} |")
+    if args.trace_csv:
+        shapes = b2b_by_shape(args.trace_csv)
+        out += ["", "Back-to-back dispatches by launch shape (grid in work-items; the kernels "
+                "that carry another step's workgroups run at their own shapes):", "",
+                "| kernel | grid | dispatches | avg us |", "|---|---|---|---|"]
+        for (n, g), (us, cnt) in sorted(shapes.items()):
+            if n.startswith("pv::") or "_kernel" in n:
+                out.append(f"| `{n}` | {g} | {cnt} | {us:.2f} |")
     if bench:
         ks = bench["latency_us"]["kernels"]
         rf = bench["roofline"]
-        out += ["", "The same run's bench.py line, HIP-event average per launch (us):", "",
-                "| kernel | us |", "|---|---|"]
+        out += ["", "The same run's bench.py line, HIP-event average per launch (us), the four "
+                "calls made separately:", "", "| kernel | us |", "|---|---|"]
         out += [f"| {k} | {v:.2f} |" for k, v in ks.items()]
+        sh = bench["latency_us"].get("kernels_shared_launches")
+        if sh:
+            out += ["", "and the launches of the one-call step (pv_prune_pipeline_timed):", "",
+                    "| kernel | us |", "|---|---|"]
+            out += [f"| {k} | {v:.2f} |" for k, v in sh.items()]
         out += ["", f"Step (HIP-graph replay): {bench['latency_us']['pipeline']:.2f} us, "
                 f"{bench['value'] / 1e6:.2f} M visual tokens/s.  Dominant kernel "
                 f"`{rf['kernel']}`: {rf['kernel_us']:.2f} us by HIP events."]

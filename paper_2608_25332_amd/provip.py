@@ -134,6 +134,8 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_pipeline.restype = _i
     lib.pv_prune_pipeline_separate.argtypes = pipe
     lib.pv_prune_pipeline_separate.restype = _i
+    lib.pv_prune_pipeline_timed.argtypes = pipe + timed_tail
+    lib.pv_prune_pipeline_timed.restype = _i
     _lib = lib
     return lib
 
@@ -541,7 +543,8 @@ def pv_pipeline_workspace_bytes(B: int, Nv: int, Nt: int, d: int, H: int, hd: in
 def pv_prune_pipeline(vis: torch.Tensor, anchors: torch.Tensor, q: torch.Tensor,
                       k_full: torch.Tensor, v_full: torch.Tensor, heads, budget1: int,
                       budget2: int, *, out: Optional[dict] = None,
-                      workspace: Optional[torch.Tensor] = None, separate: bool = False):
+                      workspace: Optional[torch.Tensor] = None, separate: bool = False,
+                      events: Optional[Sequence] = None, reps: int = 1):
     """The whole pruning step (pv_prune_pipeline): dedup with the merge, the
     K/V rows of the budget1 kept tokens, head-aware score and top-budget2,
     and the compaction of the merged hidden rows, K and V.
@@ -549,7 +552,9 @@ def pv_prune_pipeline(vis: torch.Tensor, anchors: torch.Tensor, q: torch.Tensor,
     [B,H,Nv,hd] (one dtype), heads: host ints [B, n_heads].  Returns a dict
     with PIPELINE_OUTPUTS (see include/provip.h for their shapes).
     separate=True runs every kernel in its own launch
-    (pv_prune_pipeline_separate)."""
+    (pv_prune_pipeline_separate).  events / reps: see pv_prune_pipeline_timed
+    (profiling only); the result then also holds n_kernels and
+    kernel_names."""
     import numpy as np
 
     lib = load()
@@ -582,11 +587,22 @@ def pv_prune_pipeline(vis: torch.Tensor, anchors: torch.Tensor, q: torch.Tensor,
     nbytes = lib.pv_pipeline_workspace_bytes(B, Nv, Nt, d, H, hd, n_heads, budget1, budget2, code)
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
-    fn = lib.pv_prune_pipeline_separate if separate else lib.pv_prune_pipeline
-    rc = fn(vis.data_ptr(), anchors.data_ptr(), q.data_ptr(), k_full.data_ptr(),
-            v_full.data_ptr(), hs.ctypes.data_as(ctypes.c_void_p), n_heads, B, Nv,
-            Nt, d, H, hd, code, budget1, budget2, *[o[n].data_ptr() for n in PIPELINE_OUTPUTS],
-            workspace.data_ptr(), workspace.numel(), _stream(dev))
-    _check("pv_prune_pipeline_separate" if separate else "pv_prune_pipeline", rc, lib)
+    args = [vis.data_ptr(), anchors.data_ptr(), q.data_ptr(), k_full.data_ptr(),
+            v_full.data_ptr(), hs.ctypes.data_as(ctypes.c_void_p), n_heads, B, Nv, Nt, d, H, hd,
+            code, budget1, budget2, *[o[n].data_ptr() for n in PIPELINE_OUTPUTS],
+            workspace.data_ptr(), workspace.numel(), _stream(dev)]
+    if events is not None:
+        if separate:
+            raise ValueError("events are for the shared-launch step")
+        ev, nev, nm = _events_array(events)
+        nk = _i(0)
+        rc = lib.pv_prune_pipeline_timed(*args, ev, nev, reps, ctypes.byref(nk), nm)
+        _check("pv_prune_pipeline_timed", rc, lib)
+        o["n_kernels"] = nk.value
+        o["kernel_names"] = _names(nm, nk.value)
+    else:
+        fn = lib.pv_prune_pipeline_separate if separate else lib.pv_prune_pipeline
+        rc = fn(*args)
+        _check("pv_prune_pipeline_separate" if separate else "pv_prune_pipeline", rc, lib)
     o["workspace"] = workspace
     return o

@@ -114,23 +114,31 @@ def test_pipeline_against_oracle(wid):
         assert np.max(np.abs(m - ref["merged"])) <= 1e-5 * np.max(np.abs(ref["merged"]))
 
 
-# (B, Nv, Nt, d, H, hd, n_heads, N1, N2, dtype): shapes on both sides of
-# every condition for the shared launches
+# (B, Nv, Nt, d, H, hd, n_heads, N1, N2, dtype, shared): shapes on both sides
+# of every condition for the shared launches (split-k Gram, plain merge -
+# one sample with N1 x ceil(row bytes / 1 KiB) x 4 <= row bytes -, 16-row
+# score blocks over 256-byte head rows, N1 <= 256); `shared` says whether
+# the step must take them
 EDGE = [
-    (1, 100, 5, 64, 2, 128, 1, 37, 5, "bf16"),      # ragged tiles, one head
-    (3, 300, 20, 256, 8, 128, 3, 256, 100, "bf16"),  # N1 = 256: the widest carried top-k
-    (2, 300, 20, 256, 8, 128, 3, 257, 100, "bf16"),  # N1 = 257: separate launches
-    (2, 64, 16, 256, 4, 64, 2, 64, 10, "bf16"),      # N1 = Nv: nothing pruned, no Gram
-    (2, 90, 16, 128, 4, 64, 2, 40, 7, "bf16"),       # 128-byte head rows: separate launches
-    (2, 90, 16, 128, 4, 64, 2, 40, 7, "f32"),        # 256-byte fp32 head rows: shared
-    (65, 100, 80, 64, 8, 128, 8, 40, 10, "bf16"),    # 520 head pairs: two score launches
-    (1, 40, 3, 64, 1, 128, 1, 1, 1, "bf16"),         # budgets of one
-    (8, 576, 64, 512, 8, 128, 4, 192, 64, "bf16"),   # LLaVA-like token counts, narrow rows
+    (1, 100, 5, 512, 2, 128, 1, 37, 5, "bf16", True),       # ragged tiles, one head
+    (1, 300, 20, 512, 8, 128, 3, 256, 100, "bf16", True),   # N1 = 256: the widest carried top-k
+    (1, 300, 20, 512, 8, 128, 3, 257, 100, "bf16", False),  # N1 = 257
+    (1, 64, 16, 512, 4, 64, 2, 64, 10, "bf16", False),      # N1 = Nv: nothing pruned, no Gram
+    (1, 90, 16, 512, 4, 64, 2, 40, 7, "bf16", False),       # 128-byte head rows
+    (1, 90, 16, 256, 4, 64, 2, 40, 7, "f32", True),         # 256-byte fp32 head rows
+    (1, 500, 130, 512, 8, 128, 4, 200, 50, "bf16", True),   # nine 16-row score blocks
+    (1, 1500, 100, 512, 8, 128, 4, 250, 60, "bf16", True),  # many pruned rows
+    (1, 40, 3, 64, 1, 128, 1, 1, 1, "bf16", True),          # budgets of one
+    (1, 200, 8, 64, 2, 128, 2, 100, 9, "bf16", False),      # member-list merge (narrow rows)
+    (2, 90, 16, 256, 4, 64, 2, 40, 7, "f32", False),        # two samples: member-list merge
+    (65, 100, 80, 64, 8, 128, 8, 40, 10, "bf16", False),    # 520 head pairs: two score launches
+    (8, 576, 64, 512, 8, 128, 4, 192, 64, "bf16", False),   # LLaVA-like token counts, batch
 ]
 
 
-@pytest.mark.parametrize("B,Nv,Nt,d,H,hd,nh,N1,N2,dt", EDGE)
-def test_pipeline_edges(B, Nv, Nt, d, H, hd, nh, N1, N2, dt):
+@pytest.mark.parametrize("B,Nv,Nt,d,H,hd,nh,N1,N2,dt,shared", EDGE)
+def test_pipeline_edges(B, Nv, Nt, d, H, hd, nh, N1, N2, dt, shared):
+    from paper_2608_25332_amd import provip
     _say(f"[pipeline-edge] B={B} Nv={Nv} Nt={Nt} d={d} H={H} hd={hd} heads={nh} "
          f"N1={N1} N2={N2} {dt}")
     rng = np.random.default_rng(B * 1000 + Nv + N1)
@@ -144,6 +152,13 @@ def test_pipeline_edges(B, Nv, Nt, d, H, hd, nh, N1, N2, dt):
     ins = tuple(to_dev(a, dt) for a in (vis, anc, q, kf, vf))
     fused, sep = _both(ins, heads, N1, N2)
     _assert_same(fused, sep)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(10)]
+    for e in ev:
+        e.record()
+    timed = provip.pv_prune_pipeline(*ins, heads, N1, N2, events=ev)
+    torch.cuda.synchronize()
+    assert (timed["n_kernels"] > 0) == shared, timed.get("kernel_names")
+    _assert_same(timed, sep)
     # the separate step is the four calls: check its selections against the
     # oracle on the first and last sample
     for b in sorted({0, B - 1}):
@@ -152,3 +167,28 @@ def test_pipeline_edges(B, Nv, Nt, d, H, hd, nh, N1, N2, dt):
         kept1 = to_host(sep["kept1"])[b]
         _, v_ref = oracle.head_aware(q[b:b + 1], kf[b:b + 1][:, :, kept1], heads[b:b + 1], N2)
         check_kept(to_host(sep["kept2"])[b], v_ref[0], N2, dt)
+
+
+@pytest.mark.parametrize("wid", [2, 3])
+def test_pipeline_timed_reps_leave_results_unchanged(wid):
+    """The timed call (events around each launch, every launch repeated)
+    gives the untimed call's outputs; at the LLaVA-1.5 shape it reports the
+    seven shared launches, at B = 16 (member-list merge) none."""
+    from paper_2608_25332_amd import provip
+    w = workload(wid)
+    _say(f"[pipeline-timed] workload {wid}")
+    ins = _inputs(w)
+    ref = provip.pv_prune_pipeline(*ins, w.heads, w.N1, w.N2)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(10)]
+    for e in ev:
+        e.record()
+    got = provip.pv_prune_pipeline(*ins, w.heads, w.N1, w.N2, events=ev, reps=3)
+    torch.cuda.synchronize()
+    _assert_same(got, ref)
+    if wid == 2:
+        assert got["kernel_names"] == ["cos_full", "center", "select", "gram_partial+gather_kv1",
+                                       "score_partial+gram_reduce", "merge+score_select",
+                                       "gather_hkv2"]
+    else:
+        assert got["n_kernels"] == 0
