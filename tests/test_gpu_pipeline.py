@@ -115,14 +115,14 @@ def test_pipeline_against_oracle(wid):
 
 
 # (B, Nv, Nt, d, H, hd, n_heads, N1, N2, dtype, shared): shapes on both sides
-# of every condition for the shared launches (split-k Gram, plain merge -
-# one sample with N1 x ceil(row bytes / 1 KiB) x 4 <= row bytes -, 16-row
-# score blocks over 256-byte head rows, N1 <= 256); `shared` says whether
-# the step must take them
+# of every condition for the shared launches (split-k Gram; 16-row score
+# blocks over 256-byte head rows; the plain merge - one sample with
+# N1 x ceil(row bytes / 1 KiB) x 4 <= row bytes -; N1 <= 256); `shared` says
+# whether the step must take them
 EDGE = [
     (1, 100, 5, 512, 2, 128, 1, 37, 5, "bf16", True),       # ragged tiles, one head
-    (1, 300, 20, 512, 8, 128, 3, 256, 100, "bf16", True),   # N1 = 256: the widest carried top-k
-    (1, 300, 20, 512, 8, 128, 3, 257, 100, "bf16", False),  # N1 = 257
+    (1, 300, 20, 512, 8, 128, 3, 256, 100, "bf16", True),   # N1 = 256: the widest merge-carried top-k
+    (1, 300, 20, 512, 8, 128, 3, 257, 100, "bf16", False),  # N1 = 257: member-list merge
     (1, 64, 16, 512, 4, 64, 2, 64, 10, "bf16", False),      # N1 = Nv: nothing pruned, no Gram
     (1, 90, 16, 512, 4, 64, 2, 40, 7, "bf16", False),       # 128-byte head rows
     (1, 90, 16, 256, 4, 64, 2, 40, 7, "f32", True),         # 256-byte fp32 head rows
@@ -130,9 +130,12 @@ EDGE = [
     (1, 1500, 100, 512, 8, 128, 4, 250, 60, "bf16", True),  # many pruned rows
     (1, 40, 3, 64, 1, 128, 1, 1, 1, "bf16", True),          # budgets of one
     (1, 200, 8, 64, 2, 128, 2, 100, 9, "bf16", False),      # member-list merge (narrow rows)
+    (1, 1300, 16, 64, 2, 128, 1, 1024, 50, "bf16", False),  # N1 = 1024
     (2, 90, 16, 256, 4, 64, 2, 40, 7, "f32", False),        # two samples: member-list merge
     (65, 100, 80, 64, 8, 128, 8, 40, 10, "bf16", False),    # 520 head pairs: two score launches
     (8, 576, 64, 512, 8, 128, 4, 192, 64, "bf16", False),   # LLaVA-like token counts, batch
+    (8, 2000, 16, 64, 2, 128, 1, 600, 50, "bf16", False),   # full-k Gram tiles
+    (32, 100, 16, 64, 8, 128, 4, 50, 10, "bf16", False),    # whole-head score form
 ]
 
 
@@ -172,8 +175,7 @@ def test_pipeline_edges(B, Nv, Nt, d, H, hd, nh, N1, N2, dt, shared):
 @pytest.mark.parametrize("wid", [2, 3])
 def test_pipeline_timed_reps_leave_results_unchanged(wid):
     """The timed call (events around each launch, every launch repeated)
-    gives the untimed call's outputs; at the LLaVA-1.5 shape it reports the
-    seven shared launches, at B = 16 (member-list merge) none."""
+    gives the untimed call's outputs and names the shared launches."""
     from paper_2608_25332_amd import provip
     w = workload(wid)
     _say(f"[pipeline-timed] workload {wid}")
@@ -190,5 +192,5 @@ def test_pipeline_timed_reps_leave_results_unchanged(wid):
         assert got["kernel_names"] == ["cos_full", "center", "select", "gram_partial+gather_kv1",
                                        "score_partial+gram_reduce", "merge+score_select",
                                        "gather_hkv2"]
-    else:
+    else:  # B = 16: member-list merge, separate launches
         assert got["n_kernels"] == 0
