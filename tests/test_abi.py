@@ -341,3 +341,15 @@ def test_pipeline_workspace_query(lib):
     assert small >= dedup and small >= head
     assert f(16, 576, 64, 4096, 32, 128, 4, 192, 64, 1) > small
     assert f(1, 576, 64, 4096, 32, 128, 4, 0, 64, 1) == 0
+
+
+def test_pipeline_timed_validation(lib):
+    hs = np.ones((1, 1), np.int32)
+    args = [FAKE] * 5 + [hs.ctypes.data_as(ctypes.c_void_p), 1, 1, 64, 16, 256, 4, 64, 1, 32, 16]
+    args += [FAKE] * 11 + [FAKE, 1 << 40, None]
+    evs = (ctypes.c_void_p * 3)(FAKE, None, FAKE)
+    assert lib.pv_prune_pipeline_timed(*args, evs, 3, 0, None, None) == -2   # reps < 1
+    assert lib.pv_prune_pipeline_timed(*args, evs, 3, 1, None, None) == -1   # a NULL event
+    bad = list(args)
+    bad[0] = None
+    assert lib.pv_prune_pipeline_timed(*bad, None, 0, 1, None, None) == -1
