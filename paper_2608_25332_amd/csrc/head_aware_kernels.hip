@@ -562,11 +562,10 @@ __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
     int H, int Nt, int N, int n_heads, float scale_log2e, float *__restrict__ partial) {
     using S = ScoreStage<NKS>;
     constexpr int MAXC = kHeadMaxChunks;
-    // the key chunks in dynamic LDS, nch of them (so that two workgroups fit
-    // on a CU for 192 keys)
+    // the key chunks in dynamic LDS, nch of them (so that three workgroups
+    // fit on a CU for 192 keys)
     extern __shared__ __attribute__((aligned(16))) char kdyn[];
     auto kbuf = [&](int ch) { return kdyn + ch * S::STAGE; };
-    __shared__ __attribute__((aligned(16))) char qrows[kHeadMaxRows * S::RB];
     __shared__ float colpart[4][MAXC * kScoreCK];
     const int L = blockIdx.x;
     const int hi = L % n_heads, bl = L / n_heads, b = b0 + bl;
@@ -582,14 +581,17 @@ __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
     const char *kb = k + ((size_t)b * H + h) * N * S::RB;
     const int nch = (N + kScoreCK - 1) / kScoreCK;  // <= MAXC (host-checked)
 
-    // every load of the kernel is a direct-to-LDS load, issued up front:
-    // the query rows (rows past Nt repeat the last one), then each chunk
-    const int nq = ((Nt + 15) / 16) * 16 * S::RB / 1024;  // 1 KiB pieces of the query block
-    for (int pce = wave; pce < nq; pce += 4) {
-        const int off = pce * 1024 + lane * 16;
-        const int r = off / S::RB, slot = (off % S::RB) >> 4;
-        lds_dma16(qb + (size_t)min(r, Nt - 1) * S::RB + ((slot ^ (r & S::SWZ)) << 4),
-                  qrows + pce * 1024);
+    // every load of the kernel is issued up front: this wave's query rows
+    // straight into MFMA fragments (rows past Nt repeat the last one; the
+    // wave's 16 rows are one contiguous block), then each key chunk
+    // direct-to-LDS.  Keeping the query rows out of LDS is what lets a third
+    // workgroup onto a CU.
+    const bool rows_live = wave * 16 < Nt;  // uniform: this wave has rows to score
+    uint4 qf[NKS];
+    if (rows_live) {
+        const char *qrow = qb + (size_t)min(wave * 16 + (lane & 15), Nt - 1) * S::RB;
+#pragma unroll
+        for (int s = 0; s < NKS; ++s) qf[s] = ld16(qrow + ((s * 4 + (lane >> 4)) << 4));
     }
 #pragma unroll
     for (int ch = 0; ch < MAXC; ++ch) {
@@ -607,19 +609,10 @@ __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
     wait_vmcnt<0>();
     bare_barrier();
 
-    const bool rows_live = wave * 16 < Nt;  // uniform: this wave has rows to score
     // logits of this wave's 16 rows x every key: lane holds rows
     // 4 (lane / 16) + i of column (lane % 16) of each 16-key block
     f32x4_t keep[MAXC][4];
     if (rows_live) {
-        uint4 qf[NKS];
-        const int qr = wave * 16 + (lane & 15);
-#pragma unroll
-        for (int s = 0; s < NKS; ++s)
-            qf[s] = lds_read16(qrows + qr * S::RB + (((s * 4 + (lane >> 4)) ^ (qr & S::SWZ)) << 4));
-        lds_wait();
-#pragma unroll
-        for (int s = 0; s < NKS; ++s) lds_after_wait(qf[s]);
 #pragma unroll
         for (int ch = 0; ch < MAXC; ++ch)
             if (ch < nch) head_chunk_logits<DT, NKS>(kbuf(ch), qf, lane, keep[ch]);
