@@ -541,7 +541,8 @@ def cold_times(torch, step, dev, budget_mib, rounds=6):
 def score_sweep(torch, dev):
     """Head-aware call at the LLaVA-1.5-7B shape (32 heads x 128, 64 text
     rows, 192 kept keys, keep 64) over B = 1 .. 256, with 4 selected heads
-    per sample and with all 32 heads.  Per point: the call's time from graph
+    per sample and with all 32 heads (host head lists), and with all heads
+    from a device list at B = 64 .. 256.  Per point: the call's time from graph
     replays, the score kernel's average duration from back-to-back launches
     between HIP events, and the kernel's algorithmic HBM bytes (Q and K of
     the heads read) over that duration."""
@@ -555,36 +556,42 @@ def score_sweep(torch, dev):
     k_all = torch.randn((Bmax, H, N, hd), generator=gen, device=dev).to(torch.bfloat16)
     rng = np.random.default_rng(2)
     rows = []
-    for nh in (4, H):
-        for B in (1, 4, 16, 64, 256):
-            q, k = q_all[:B], k_all[:B]
-            heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
-            out = {"kept": torch.empty((B, N2), dtype=torch.int32, device=dev),
-                   "score": torch.empty((B, N), dtype=torch.float32, device=dev)}
-            ws = torch.empty(pv.pv_head_aware_workspace_bytes(B, H, Nt, N, hd, nh, N2, 1),
-                             dtype=torch.uint8, device=dev)
-            call = lambda: pv.pv_prune_head_aware(q, k, heads, N2, out=out, workspace=ws)
-            call_us = graph_time_us(torch, call, reps=200)
-            reps = 20
-            samples = []
-            for _ in range(5):
-                ev = [torch.cuda.Event(enable_timing=True) for _ in range(Step.HEAD_EVENTS)]
-                for e in ev:
-                    e.record()
-                r = pv.pv_prune_head_aware(q, k, heads, N2, out=out, workspace=ws, events=ev,
-                                           reps=reps)
-                torch.cuda.synchronize()
-                i = r["kernel_names"].index("score_partial")
-                samples.append(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / reps)
-            kus = float(np.median(samples))
-            nbytes = B * nh * (Nt + N) * hd * 2
-            gbs = nbytes / (kus * 1e-6) / 1e9
-            rows.append({"B": B, "heads_per_sample": nh, "call_us": call_us,
-                         "score_kernel_us": kus, "algorithmic_bytes": nbytes,
-                         "achieved_GBs": gbs, "frac_hbm": gbs / HBM_PEAK_GBS})
-            print(f"[score-sweep] B={B} heads={nh} call {call_us:.2f} us, kernel {kus:.2f} us, "
-                  f"{gbs:.0f} GB/s", file=sys.stderr, flush=True)
-            del out, ws
+    # host head lists at every point; device lists (one launch whatever the
+    # batch) where a host list would take several launches or nearly so
+    points = [(nh, B, False) for nh in (4, H) for B in (1, 4, 16, 64, 256)]
+    points += [(H, B, True) for B in (64, 128, 256)]
+    for nh, B, on_dev in points:
+        q, k = q_all[:B], k_all[:B]
+        heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+        if on_dev:
+            heads = torch.from_numpy(heads).to(dev)
+        out = {"kept": torch.empty((B, N2), dtype=torch.int32, device=dev),
+               "score": torch.empty((B, N), dtype=torch.float32, device=dev)}
+        ws = torch.empty(pv.pv_head_aware_workspace_bytes(B, H, Nt, N, hd, nh, N2, 1),
+                         dtype=torch.uint8, device=dev)
+        call = lambda: pv.pv_prune_head_aware(q, k, heads, N2, out=out, workspace=ws)
+        call_us = graph_time_us(torch, call, reps=200)
+        reps = 20
+        samples = []
+        for _ in range(5):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(Step.HEAD_EVENTS)]
+            for e in ev:
+                e.record()
+            r = pv.pv_prune_head_aware(q, k, heads, N2, out=out, workspace=ws, events=ev,
+                                       reps=reps)
+            torch.cuda.synchronize()
+            i = r["kernel_names"].index("score_partial")
+            samples.append(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / reps)
+        kus = float(np.median(samples))
+        nbytes = B * nh * (Nt + N) * hd * 2
+        gbs = nbytes / (kus * 1e-6) / 1e9
+        rows.append({"B": B, "heads_per_sample": nh, "heads_on_device": on_dev,
+                     "call_us": call_us, "score_kernel_us": kus, "algorithmic_bytes": nbytes,
+                     "achieved_GBs": gbs, "frac_hbm": gbs / HBM_PEAK_GBS})
+        print(f"[score-sweep] B={B} heads={nh}{' (device list)' if on_dev else ''} "
+              f"call {call_us:.2f} us, kernel {kus:.2f} us, {gbs:.0f} GB/s", file=sys.stderr,
+              flush=True)
+        del out, ws
     return {"score_sweep": rows, "shape": {"H": H, "Nt": Nt, "N": N, "hd": hd, "N2": N2,
                                            "dtype": "bf16"},
             "note": "warm caches; at B=256 with all heads the call reads 537 MB"}
