@@ -181,6 +181,38 @@ struct Fork {
     hipEvent_t merged_done;
 };
 
+// The kernels of the dedup up to the top-N_1: the cosine to the anchors,
+// centring and max-pool into p, and the selection (kept, the pruned list
+// and, with slot_of, each kept token's own slot).
+bool launch_front(Trace &tr, const DedupPlan &P, int dt, const void *vis, const void *anchors,
+                  const int32_t *anchor_mask, int B, int Nv, int Nt, int d, int budget, float *p,
+                  int32_t *kept, int32_t *slot_of, hipStream_t st) {
+    if (P.cos_full) {
+        if (!tr.launch("cos_full", [&] {
+                return pv::launch_cos_full(dt, vis, anchors, B, Nv, Nt, d, P.M, P.rowsum, P.invn,
+                                           st);
+            }))
+            return false;
+    } else {
+        if (!tr.launch("cos_partial", [&] {
+                return pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart,
+                                              P.ssv, P.ssa, st);
+            }))
+            return false;
+        if (!tr.launch("cos_reduce", [&] {
+                return pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M,
+                                             P.rowsum, P.invn, st);
+            }))
+            return false;
+    }
+    return tr.launch("center", [&] {
+               return pv::launch_center(P.M, P.rowsum, anchor_mask, P.njt, B, Nt, Nv, p, st);
+           }) &&
+           tr.launch("select", [&] {
+               return pv::launch_select(p, B, Nv, budget, kept, P.pruned, slot_of, st);
+           });
+}
+
 int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int d, int dtype,
                int budget, int32_t *kept, float *score, int32_t *assign, void *merged,
                void *workspace, size_t ws_bytes, void *stream, void *const *events, int n_events,
@@ -209,32 +241,8 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     hipStream_t st = (hipStream_t)stream;
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
-    if (P.cos_full) {
-        if (!tr.launch("cos_full", [&] {
-                return pv::launch_cos_full(dt, vis, anchors, B, Nv, Nt, d, P.M, P.rowsum, P.invn,
-                                           st);
-            }))
-            return PV_ERR_HIP;
-    } else {
-        if (!tr.launch("cos_partial", [&] {
-                return pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart,
-                                              P.ssv, P.ssa, st);
-            }))
-            return PV_ERR_HIP;
-        if (!tr.launch("cos_reduce", [&] {
-                return pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M,
-                                             P.rowsum, P.invn, st);
-            }))
-            return PV_ERR_HIP;
-    }
-    if (!tr.launch("center", [&] {
-            return pv::launch_center(P.M, P.rowsum, anchor_mask, P.njt, B, Nt, Nv, p, st);
-        }))
-        return PV_ERR_HIP;
-    if (!tr.launch("select", [&] {
-            return pv::launch_select(p, B, Nv, budget, kept, P.pruned, need_assign ? asg : nullptr,
-                                     st);
-        }))
+    if (!launch_front(tr, P, dt, vis, anchors, anchor_mask, B, Nv, Nt, d, budget, p, kept,
+                      need_assign ? asg : nullptr, st))
         return PV_ERR_HIP;
     hipStream_t sm = st;  // stream of the assignment and merge kernels
     if (fork) {
@@ -880,31 +888,8 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
     }
     const HeadPlan Hh = plan_head(ws_head, B, Nt, N1, n_heads, false);
     // cosine, centring, top-N_1
-    if (P.cos_full) {
-        if (!tr.launch("cos_full", [&] {
-                return pv::launch_cos_full(dt, vis, anchors, B, Nv, Nt, d, P.M, P.rowsum, P.invn,
-                                           st);
-            }))
-            return PV_ERR_HIP;
-    } else {
-        if (!tr.launch("cos_partial", [&] {
-                return pv::launch_cos_partial(dt, vis, anchors, B, Nv, Nt, d, P.ks_cos, P.cpart,
-                                              P.ssv, P.ssa, st);
-            }))
-            return PV_ERR_HIP;
-        if (!tr.launch("cos_reduce", [&] {
-                return pv::launch_cos_reduce(P.cpart, P.ssv, P.ssa, B, Nv, Nt, P.ks_cos, P.M,
-                                             P.rowsum, P.invn, st);
-            }))
-            return PV_ERR_HIP;
-    }
-    if (!tr.launch("center", [&] {
-            return pv::launch_center(P.M, P.rowsum, nullptr, P.njt, B, Nt, Nv, score1, st);
-        }))
-        return PV_ERR_HIP;
-    if (!tr.launch("select", [&] {
-            return pv::launch_select(score1, B, Nv, N1, kept1, P.pruned, assign, st);
-        }))
+    if (!launch_front(tr, P, dt, vis, anchors, nullptr, B, Nv, Nt, d, N1, score1, kept1, assign,
+                      st))
         return PV_ERR_HIP;
     // Gram partials + the K/V rows of the kept tokens
     pv::GatherJob gj;
