@@ -52,8 +52,10 @@ typedef enum {
     PV_ERR_DTYPE = -5,     /* dtype is not PV_F32 or PV_BF16                   */
     PV_ERR_WORKSPACE = -6, /* workspace NULL or smaller than the query         */
     PV_ERR_HIP = -7,       /* a kernel launch failed                            */
-    PV_ERR_ALIGN = -8      /* a pointer, row size or stride is not 16-byte
+    PV_ERR_ALIGN = -8,     /* a pointer, row size or stride is not 16-byte
                               aligned                                          */
+    PV_ERR_SCRATCH = -9    /* pv_prune_pipeline_noalloc: the problem needs
+                              more than PV_STATIC_SCRATCH_BYTES of scratch     */
 } pv_status;
 
 typedef enum { PV_F32 = 0, PV_BF16 = 1 } pv_dtype;
@@ -443,6 +445,36 @@ int pv_prune_pipeline_separate(const void *vis, const void *anchors, const void 
                                int32_t *assign, void *merged, void *k1, void *v1, int32_t *kept2,
                                float *score2, void *hidden2, void *k2, void *v2, void *workspace,
                                size_t workspace_bytes, void *stream);
+
+/* -------------------------------------------------------------------------
+ * pv_prune_pipeline without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops
+ * and harnesses that forbid hipMalloc.  Same arguments (minus workspace and
+ * workspace_bytes), same kernels and bit-identical results.
+ *
+ * The scratch is a static device array inside the library, one copy per
+ * GPU, of PV_STATIC_SCRATCH_BYTES; each GPU holds it from the library's
+ * first call there until the process ends.  The call allocates nothing: no
+ * hipMalloc, hipFree or allocating library routine.  The first call on a GPU
+ * looks up that GPU's copy (make the stream's device current, as for every
+ * call).  Every call on one GPU uses the same array and leaves its contents
+ * behind; nothing in it needs to start at any value.  Two calls that overlap
+ * in time on one GPU (two streams, two host threads) race on the array:
+ * order them on one stream or with events.
+ *
+ * Errors: those of pv_prune_pipeline, plus PV_ERR_SCRATCH (nothing is
+ * enqueued) when pv_pipeline_workspace_bytes() of the same sizes exceeds
+ * PV_STATIC_SCRATCH_BYTES, and PV_ERR_HIP if the array's device address
+ * cannot be found.
+ * ---------------------------------------------------------------------- */
+#define PV_STATIC_SCRATCH_BYTES (64u << 20)
+
+int pv_prune_pipeline_noalloc(const void *vis, const void *anchors, const void *q,
+                              const void *k_full, const void *v_full, const int32_t *heads_host,
+                              int n_heads, int B, int Nv, int Nt, int d, int H, int hd, int dtype,
+                              int budget1, int budget2, int32_t *kept1, float *score1,
+                              int32_t *assign, void *merged, void *k1, void *v1, int32_t *kept2,
+                              float *score2, void *hidden2, void *k2, void *v2, void *stream);
 
 #ifdef __cplusplus
 }

@@ -6,6 +6,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "pv_jobs.h"
 #include "pv_launch.h"
 
@@ -500,6 +502,8 @@ PV_API const char *pv_status_string(int status) {
         case PV_ERR_WORKSPACE: return "workspace missing or smaller than the query";
         case PV_ERR_HIP: return "kernel launch failed";
         case PV_ERR_ALIGN: return "pointer, row size or stride not 16-byte aligned";
+        case PV_ERR_SCRATCH:
+            return "the problem needs more scratch than the library's static buffer holds";
     }
     return "unknown status";
 }
@@ -975,4 +979,67 @@ PV_API int pv_prune_pipeline_timed(const void *vis, const void *anchors, const v
                          dtype, budget1, budget2, kept1, score1, assign, merged, k1, v1, kept2,
                          score2, hidden2, k2, v2, workspace, workspace_bytes, stream, 0, events,
                          n_events, reps, n_kernels, names);
+}
+
+// ---------------------------------------------------------------------------
+// The step without a workspace argument, for callers that cannot allocate.
+//
+// The scratch lives in this file-scope array: one copy per GPU, allocated
+// when the library's code object is loaded on that GPU and held until the
+// process ends.  Host code never uses the array's name as an address (on the
+// host it is only a stand-in for the device symbol): the device address of
+// each GPU's copy is looked up once, with that GPU current, and kept.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) unsigned char scratch[PV_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch[kMaxDevices];
+
+// Device address of the current GPU's copy of `scratch` (PV_ERR_HIP if the
+// lookup fails or the device id is out of range).
+int scratch_of_current_device(void **out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return PV_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return PV_ERR_HIP;
+        g_scratch[dev] = p;
+    }
+    *out = g_scratch[dev];
+    return PV_OK;
+}
+
+}  // namespace
+
+PV_API int pv_prune_pipeline_noalloc(const void *vis, const void *anchors, const void *q,
+                                     const void *k_full, const void *v_full,
+                                     const int32_t *heads_host, int n_heads, int B, int Nv,
+                                     int Nt, int d, int H, int hd, int dtype, int budget1,
+                                     int budget2, int32_t *kept1, float *score1, int32_t *assign,
+                                     void *merged, void *k1, void *v1, int32_t *kept2,
+                                     float *score2, void *hidden2, void *k2, void *v2,
+                                     void *stream) {
+    // the checks that need no device first, so that a rejected call touches
+    // no GPU state
+    int rc = check_dedup(vis, anchors, B, Nv, Nt, d, dtype, budget1, kept1);
+    if (rc != PV_OK) return rc;
+    if (!heads_host) return PV_ERR_NULL;
+    rc = check_head(q, k_full, heads_host, nullptr, n_heads, B, H, Nt, budget1, hd, dtype,
+                    budget2, kept2);
+    if (rc != PV_OK) return rc;
+    const int esz = (dtype == PV_BF16) ? 2 : 4;
+    // the step carves its workspace from a 256-byte boundary, which the
+    // array's start already is
+    if (pipe_sizes(B, Nv, Nt, d, esz, budget1, n_heads).total > (size_t)PV_STATIC_SCRATCH_BYTES)
+        return PV_ERR_SCRATCH;
+    void *ws = nullptr;
+    if ((rc = scratch_of_current_device(&ws)) != PV_OK) return rc;
+    return pipeline_impl(vis, anchors, q, k_full, v_full, heads_host, n_heads, B, Nv, Nt, d, H,
+                         hd, dtype, budget1, budget2, kept1, score1, assign, merged, k1, v1,
+                         kept2, score2, hidden2, k2, v2, ws, (size_t)PV_STATIC_SCRATCH_BYTES,
+                         stream, 0);
 }

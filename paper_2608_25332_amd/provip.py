@@ -24,7 +24,11 @@ PV_BF16 = 1
 STATUS = {
     0: "PV_OK", -1: "PV_ERR_NULL", -2: "PV_ERR_SHAPE", -3: "PV_ERR_BUDGET", -4: "PV_ERR_HEADS",
     -5: "PV_ERR_DTYPE", -6: "PV_ERR_WORKSPACE", -7: "PV_ERR_HIP", -8: "PV_ERR_ALIGN",
+    -9: "PV_ERR_SCRATCH",
 }
+
+# size of the library's static scratch array (pv_prune_pipeline_noalloc)
+PV_STATIC_SCRATCH_BYTES = 64 << 20
 
 _lib = None
 
@@ -136,6 +140,8 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_pipeline_separate.restype = _i
     lib.pv_prune_pipeline_timed.argtypes = pipe + timed_tail
     lib.pv_prune_pipeline_timed.restype = _i
+    lib.pv_prune_pipeline_noalloc.argtypes = [_vp] * 6 + [_i] * 10 + [_vp] * 11 + [_vp]
+    lib.pv_prune_pipeline_noalloc.restype = _i
     _lib = lib
     return lib
 
@@ -606,3 +612,33 @@ def pv_prune_pipeline(vis: torch.Tensor, anchors: torch.Tensor, q: torch.Tensor,
         _check("pv_prune_pipeline_separate" if separate else "pv_prune_pipeline", rc, lib)
     o["workspace"] = workspace
     return o
+
+
+def pv_prune_pipeline_noalloc(vis: torch.Tensor, anchors: torch.Tensor, q: torch.Tensor,
+                              k_full: torch.Tensor, v_full: torch.Tensor, heads, budget1: int,
+                              budget2: int, *, out: dict):
+    """The whole step with the library's static scratch instead of a
+    workspace (pv_prune_pipeline_noalloc): nothing is allocated on the
+    device, so every output must be passed in `out` (PIPELINE_OUTPUTS, the
+    shapes of pv_prune_pipeline's).  Calls that overlap in time on one GPU
+    race on the scratch."""
+    import numpy as np
+
+    lib = load()
+    for t, n in ((vis, "vis"), (anchors, "anchors"), (q, "q"), (k_full, "k_full"),
+                 (v_full, "v_full")):
+        _contig(t, n)
+    B, Nv, d = vis.shape
+    _, H, Nt, hd = q.shape
+    hs = np.ascontiguousarray(np.asarray(heads, dtype=np.int32).reshape(B, -1))
+    missing = [n for n in PIPELINE_OUTPUTS if out.get(n) is None]
+    if missing:
+        raise ValueError(f"pv_prune_pipeline_noalloc allocates nothing: pass {missing} in out")
+    for n in PIPELINE_OUTPUTS:
+        _contig(out[n], n)
+    rc = lib.pv_prune_pipeline_noalloc(
+        vis.data_ptr(), anchors.data_ptr(), q.data_ptr(), k_full.data_ptr(), v_full.data_ptr(),
+        hs.ctypes.data_as(ctypes.c_void_p), hs.shape[1], B, Nv, Nt, d, H, hd, _dtype_code(vis),
+        budget1, budget2, *[out[n].data_ptr() for n in PIPELINE_OUTPUTS], _stream(vis.device))
+    _check("pv_prune_pipeline_noalloc", rc, lib)
+    return out

@@ -51,7 +51,7 @@ def test_exported_c_symbols_are_declared():
 
 
 def test_status_strings(lib):
-    for s in range(-8, 1):
+    for s in range(-9, 1):
         assert len(lib.pv_status_string(s)) > 0
     assert lib.pv_status_string(-99) == b"unknown status"
     assert lib.pv_version() >> 16 == 1
@@ -353,3 +353,34 @@ def test_pipeline_timed_validation(lib):
     bad = list(args)
     bad[0] = None
     assert lib.pv_prune_pipeline_timed(*bad, None, 0, 1, None, None) == -1
+
+
+def _noalloc(lib, heads=(1,), B=1, Nv=64, Nt=16, d=256, H=4, hd=64, dt=1, b1=32, b2=16,
+             null_at=None):
+    hs = np.ascontiguousarray(np.asarray(heads, dtype=np.int32).reshape(B, -1))
+    ptrs = [FAKE] * 16
+    if null_at is not None:
+        ptrs[null_at] = None
+    return lib.pv_prune_pipeline_noalloc(*ptrs[:5], hs.ctypes.data_as(ctypes.c_void_p),
+                                         hs.shape[1], B, Nv, Nt, d, H, hd, dt, b1, b2, *ptrs[5:],
+                                         None)
+
+
+def test_pipeline_noalloc_rejects_on_the_host(lib):
+    """The step on the static scratch: bad arguments and problems larger than
+    the scratch are rejected before any device call (these return without a
+    GPU)."""
+    from paper_2608_25332_amd import provip
+    assert _noalloc(lib, null_at=0) == -1
+    assert _noalloc(lib, heads=(4,)) == -4
+    assert _noalloc(lib, b1=65) == -3
+    assert _noalloc(lib, d=100) == -2
+    # the 13B 8-frame step fits; 16 samples of it do not
+    big = dict(heads=[list(range(5))] * 16, B=16, Nv=4608, Nt=128, d=5120, H=40, hd=128,
+               b1=1152, b2=512)
+    assert lib.pv_pipeline_workspace_bytes(16, 4608, 128, 5120, 40, 128, 5, 1152, 512, 1) > \
+        provip.PV_STATIC_SCRATCH_BYTES
+    assert _noalloc(lib, **big) == -9
+    assert lib.pv_pipeline_workspace_bytes(2, 4608, 128, 5120, 40, 128, 5, 1152, 512, 1) <= \
+        provip.PV_STATIC_SCRATCH_BYTES
+    assert b"scratch" in lib.pv_status_string(-9)
