@@ -72,6 +72,9 @@ def parse():
                          "(measured before the timed steps)")
     ap.add_argument("--cold-mib", type=int, default=640,
                     help="input copies rotated through for the cold-cache timing (0 disables it)")
+    ap.add_argument("--per-config", default="3,4,5",
+                    help="workload ids measured after the headline for the per_config block "
+                         "(empty: none)")
     ap.add_argument("--score-sweep", action="store_true",
                     help="instead of the step: the head-aware call at the LLaVA-1.5-7B shape over "
                          "a batch sweep, with the selected heads and with all heads; prints its "
@@ -667,43 +670,260 @@ def cpu_model():
     return "unknown"
 
 
-def cpu_baseline(w, seconds):
-    """The CPU oracle, as it stands, over repeats of the same batch until the
-    time budget is used (at least one full step); seconds per stage too."""
+def _oracle_step(w, b0: int, b1: int):
+    """One full step of the oracle over samples [b0, b1) of the batch: dedup
+    with the merge, the K/V rows of the kept tokens, head-aware, gathers.
+    Returns the seconds of (dedup, head_aware, gather)."""
     import oracle
 
     s = w.spec
+    a = time.perf_counter()
+    ref = oracle.dedup(w.anchors[b0:b1], w.vis[b0:b1], w.N1)
+    kept1 = ref["kept"]
+    b = time.perf_counter()
+    k1 = np.stack([w.k_full[b0 + i][:, kept1[i]] for i in range(b1 - b0)])
+    v1 = np.stack([w.v_full[b0 + i][:, kept1[i]] for i in range(b1 - b0)])
+    c = time.perf_counter()
+    kept2, _ = oracle.head_aware(w.q[b0:b1], k1, w.heads[b0:b1], w.N2)
+    d = time.perf_counter()
+    oracle.gather(ref["merged"], kept2)
+    oracle.gather(k1, kept2)
+    oracle.gather(v1, kept2)
+    e = time.perf_counter()
+    del s
+    return (b - a, d - c, (c - b) + (e - d))
+
+
+def cpu_baseline(w, seconds):
+    """The CPU oracle, as it stands, over repeats of the same batch until the
+    time budget is used (at least one full step): first on one thread, then
+    with every host CPU (up to 16) running whole steps at once.  The figure
+    reported is the all-cores one; the one-thread figure and the seconds per
+    stage are kept beside it."""
+    from oracle.parallel import workers
+
+    s = w.spec
     reps = 0
-    st = {"dedup": 0.0, "head_aware": 0.0, "gather": 0.0}
+    st = [0.0, 0.0, 0.0]
     t0 = time.perf_counter()
     while True:
-        a = time.perf_counter()
-        ref = oracle.dedup(w.anchors, w.vis, w.N1)
-        kept1 = ref["kept"]
-        b = time.perf_counter()
-        k1 = np.stack([w.k_full[i][:, kept1[i]] for i in range(s.B)])
-        v1 = np.stack([w.v_full[i][:, kept1[i]] for i in range(s.B)])
-        c = time.perf_counter()
-        kept2, _ = oracle.head_aware(w.q, k1, w.heads, w.N2)
-        d = time.perf_counter()
-        oracle.gather(ref["merged"], kept2)
-        oracle.gather(k1, kept2)
-        oracle.gather(v1, kept2)
-        e = time.perf_counter()
-        st["dedup"] += b - a
-        st["head_aware"] += d - c
-        st["gather"] += (c - b) + (e - d)
+        for i, x in enumerate(_oracle_step(w, 0, s.B)):
+            st[i] += x
         reps += 1
         el = time.perf_counter() - t0
-        if el >= seconds:
+        if el >= seconds / 2:
             break
-    toks = reps * s.B * s.Nv
-    return {"value": toks / el, "unit": "visual tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{reps} full steps (dedup+merge, head-aware, gathers) of the {s.name} batch "
-                      f"(B={s.B}, Nv={s.Nv}) in {el:.2f} s, single-threaded fp64 C oracle",
-            "seconds": round(el, 3),
-            "seconds_per_step_by_stage": {k: round(v / reps, 4) for k, v in st.items()},
+    single = reps * s.B * s.Nv / el
+    # all cores: every thread runs whole steps of the batch (ctypes releases
+    # the GIL inside the oracle's C functions)
+    import threading
+
+    n = workers()
+    done = [0] * n
+    deadline = time.perf_counter() + seconds / 2
+
+    def worker(i):
+        while True:
+            _oracle_step(w, 0, s.B)
+            done[i] += 1
+            if time.perf_counter() >= deadline:
+                return
+
+    t1 = time.perf_counter()
+    th = [threading.Thread(target=worker, args=(i,)) for i in range(n)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    el_all = time.perf_counter() - t1
+    steps_all = sum(done)
+    value = steps_all * s.B * s.Nv / el_all
+    return {"value": value, "unit": "visual tokens/s", "cores": n, "kind": "oracle",
+            "sample": f"{steps_all} full steps (dedup+merge, head-aware, gathers) of the {s.name} "
+                      f"batch (B={s.B}, Nv={s.Nv}) in {el_all:.2f} s, {n} threads each running "
+                      f"whole steps of the fp64 C oracle",
+            "seconds": round(el_all, 3),
+            "single_thread": {"value": single, "cores": 1, "steps": reps,
+                              "seconds": round(el, 3),
+                              "seconds_per_step_by_stage": {
+                                  k: round(v / reps, 4)
+                                  for k, v in zip(("dedup", "head_aware", "gather"), st)}},
             "cpu_model": cpu_model(), "host_cpus": os.cpu_count()}
+
+
+def cpu_baseline_one_sample(w):
+    """A bounded sample of a large workload: sample 0 of the batch, one full
+    step of the oracle with the row ranges of its two big products (the
+    cosine to the anchors, the nearest kept token of every row) spread over
+    every host CPU (up to 16).  Visual tokens/s = Nv over its seconds."""
+    import oracle
+    from oracle.parallel import oracle_assign, oracle_p, workers
+
+    s = w.spec
+    t0 = time.perf_counter()
+    p = oracle_p(w.anchors[:1], w.vis[:1])[0]
+    kept1 = oracle.topk(p, w.N1)
+    asg, _, _ = oracle_assign(w.vis[0], kept1, np.arange(s.Nv, dtype=np.int32))
+    merged = oracle.merge(w.vis[0], kept1, asg)
+    k1 = w.k_full[0][:, kept1][None]
+    v1 = w.v_full[0][:, kept1][None]
+    kept2, _ = oracle.head_aware(w.q[:1], k1, w.heads[:1], w.N2)
+    oracle.gather(merged[None], kept2)
+    oracle.gather(k1, kept2)
+    oracle.gather(v1, kept2)
+    el = time.perf_counter() - t0
+    return {"value": s.Nv / el, "unit": "visual tokens/s", "cores": workers(), "kind": "oracle",
+            "sample": f"sample 0 of the {s.name} batch (Nv={s.Nv}), one full step in {el:.2f} s, "
+                      f"row ranges of the cosine and nearest-centroid products over "
+                      f"{workers()} threads",
+            "seconds": round(el, 3)}
+
+
+def prepare(w, dev, args):
+    """A Step in the form that replays fastest (unless one is forced)."""
+    import torch
+
+    first = {"1": "one_stream", "2": "two_streams", "shared": "shared_launches",
+             "auto": "one_stream"}[args.streams]
+    step = Step(w, dev, form="two_streams" if args.split else first)
+    step.run()
+    torch.cuda.synchronize()
+    ref = step.snapshot()
+    mode_us = {}
+    if args.streams == "auto" and not args.split and not args.pmc_pass and not args.no_graph:
+        for f in Step.FORMS:
+            step.form = f
+            mode_us[f] = graph_time_us(torch, step.run, reps=300)
+        step.form = min(mode_us, key=lambda f: mode_us[f])
+        torch.cuda.synchronize()
+    return step, ref, mode_us
+
+
+def capture_step(torch, step, dev, ref):
+    """The step captured as one HIP graph; every replay must reproduce the
+    eager result."""
+    stream = torch.cuda.current_stream(dev)
+    side = torch.cuda.Stream(dev)
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        for _ in range(3):
+            step.run()
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step.run()
+    torch.cuda.synchronize()
+    for _ in range(3):
+        graph.replay()
+        torch.cuda.synchronize()
+        snap = step.snapshot()
+        for k in ref:
+            if not torch.equal(ref[k], snap[k]):
+                raise RuntimeError(f"graph replay differs from eager in {k}")
+        step.run()
+        torch.cuda.synchronize()
+    return graph
+
+
+def timed_steps(torch, run_once, steps, warmup):
+    for _ in range(warmup):
+        run_once()
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record()
+    for _ in range(steps):
+        run_once()
+    t_end.record()
+    torch.cuda.synchronize()
+    return t_start.elapsed_time(t_end) / steps
+
+
+def rooflines(w, form, kern_us, shared_us):
+    """Roofline of every kernel and stage, and of the dominant kernel of the
+    form that is timed (with its HBM traffic from the committed counter
+    summary when that matches the sources)."""
+    alg_k, alg_s = algorithmic(w)
+    kernels = {}
+    for k, us in kern_us.items():
+        r = roof(alg_k[k], us * 1e-6)
+        kernels[k] = {"us": us, "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"],
+                      "frac": r["frac"]}
+        if alg_k[k]["flops"] > 0 and k.startswith("gram"):
+            # the Gram against the matrix cores whatever its bound
+            kernels[k]["frac_of_bf16_mfma_peak"] = alg_k[k]["flops"] / (us * 1e-6) / 1e12 / \
+                BF16_PEAK_TFLOPS
+    stage_us = {}
+    for k, us in kern_us.items():
+        stage_us[STAGE_OF[k]] = stage_us.get(STAGE_OF[k], 0.0) + us
+    stages = {}
+    for st_name, us in stage_us.items():
+        r = roof(alg_s[st_name], us * 1e-6)
+        stages[st_name] = {"us": us, "bound": r["bound"], "achieved": r["achieved"],
+                           "unit": r["unit"], "frac": r["frac"]}
+    shared = {}
+    for k, us in shared_us.items():
+        r = roof(alg_k[k], us * 1e-6)
+        shared[k] = {"us": us, "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"],
+                     "frac": r["frac"]}
+    step_us = shared_us if form == "shared_launches" and shared_us else kern_us
+    dom = max(step_us, key=lambda k: step_us[k])
+    a = alg_k[dom]
+    rf = roof(a, step_us[dom] * 1e-6)
+    rf.update({"traffic": load_traffic(w.spec.name, dom), "kernel": dom,
+               "kernel_us": step_us[dom], "algorithmic_bytes": a["bytes"],
+               "algorithmic_flops": a["flops"]})
+    return rf, kernels, stages, shared, stage_us
+
+
+def config_of(w, form, split, graph):
+    s = w.spec
+    return {"workload": s.name, "B": s.B, "Nv": s.Nv, "d": s.d, "H": s.H, "hd": s.hd,
+            "Nt": s.Nt, "heads_per_sample": int(w.heads.shape[1]), "N1": w.N1, "N2": w.N2,
+            "streams": 2 if split else 1, "step_form": form,
+            "timing": ("hip-graph replay of the full step" +
+                       {"one_stream": "", "two_streams": ", merge branch on a second stream",
+                        "shared_launches": ", one pv_prune_pipeline call (shared launches)"}[form]
+                       if graph is not None else "eager")}
+
+
+def measure_other(torch, wid, dev, args):
+    """One of the larger workloads, for the per_config block: the step's
+    graph-replay time in its fastest form, every kernel's duration and
+    roofline, the per-stage roofline and a bounded CPU-oracle sample."""
+    from paper_2608_25332_amd import workloads as W
+
+    t0 = time.perf_counter()
+    w = W.make_workload(wid)
+    step, ref, mode_us = prepare(w, dev, args)
+    graph = capture_step(torch, step, dev, ref)
+    steps = max(20, min(args.steps, int(2e5 / max(min(mode_us.values()) if mode_us else 200, 1))))
+    ms = timed_steps(torch, graph.replay, steps, max(5, args.warmup // 10))
+    kern_us = kernel_times(torch, step, args.kernel_reps, max(3, args.kernel_iters // 2))
+    shared_us = shared_kernel_times(torch, step, args.kernel_reps, max(3, args.kernel_iters // 2))
+    step.run()
+    torch.cuda.synchronize()
+    snap = step.snapshot()
+    for k in ref:
+        if not torch.equal(ref[k], snap[k]):
+            raise RuntimeError(f"benchmark output drifted in {k} ({w.spec.name})")
+    rf, kernels, stages, shared, stage_us = rooflines(w, step.form, kern_us, shared_us)
+    out = {"config": config_of(w, step.form, step.form == "two_streams", graph),
+           "steps": steps, "ms_per_step": ms, "value": w.spec.B * w.spec.Nv / (ms * 1e-3),
+           "unit": "visual tokens/s", "stream_choice_us": mode_us or None,
+           "latency_us": {"kernels": kern_us, "kernels_shared_launches": shared_us or None,
+                          "stages": stage_us},
+           "roofline": rf, "roofline_kernels": kernels, "roofline_stages": stages,
+           "roofline_kernels_shared_launches": shared or None, "csrc_digest": csrc_digest()}
+    del graph, step
+    torch.cuda.synchronize()
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline_one_sample(w)
+    out["wall_s"] = round(time.perf_counter() - t0, 1)
+    print(f"[bench] {w.spec.name}: {ms * 1000:.1f} us/step ({out['config']['step_form']}), "
+          f"{out['wall_s']} s", file=sys.stderr, flush=True)
+    return out
 
 
 def main():
@@ -726,29 +946,7 @@ def main():
         return
     w = W.make_workload(args.workload)
     s = w.spec
-    first = {"1": "one_stream", "2": "two_streams", "shared": "shared_launches",
-             "auto": "one_stream"}[args.streams]
-    step = Step(w, dev, form="two_streams" if args.split else first)
-    stream = torch.cuda.current_stream(dev)
-
-    # eager reference outputs
-    step.run()
-    torch.cuda.synchronize()
-    ref = step.snapshot()
-
-    # the form of the step: the merge branch on a second stream overlaps the
-    # K/V gather and the head-aware score, which pays once those take longer
-    # than the cross-stream dependencies cost (the large workloads); shared
-    # launches take three kernel boundaries off the chain where the shapes
-    # allow them (the small batches).  Picked from graph replays of every
-    # form before any timed step.
-    mode_us = {}
-    if args.streams == "auto" and not args.split and not args.pmc_pass and not args.no_graph:
-        for f in Step.FORMS:
-            step.form = f
-            mode_us[f] = graph_time_us(torch, step.run, reps=300)
-        step.form = min(mode_us, key=lambda f: mode_us[f])
-        torch.cuda.synchronize()
+    step, ref, mode_us = prepare(w, dev, args)
     form = step.form
     split = form == "two_streams"
 
@@ -771,43 +969,9 @@ def main():
         return
 
     # ---- headline: graph replay
-    use_graph = not args.no_graph
-    graph = None
-    if use_graph:
-        side = torch.cuda.Stream(dev)
-        side.wait_stream(stream)
-        with torch.cuda.stream(side):
-            for _ in range(3):
-                step.run()
-        stream.wait_stream(side)
-        torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            step.run()
-        torch.cuda.synchronize()
-        # every replay must reproduce the eager result
-        for _ in range(3):
-            graph.replay()
-            torch.cuda.synchronize()
-            snap = step.snapshot()
-            for k in ref:
-                if not torch.equal(ref[k], snap[k]):
-                    raise RuntimeError(f"graph replay differs from eager in {k}")
-            step.run()
-            torch.cuda.synchronize()
+    graph = None if args.no_graph else capture_step(torch, step, dev, ref)
     run_once = graph.replay if graph is not None else step.run
-    for _ in range(args.warmup):
-        run_once()
-    torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record()
-    for _ in range(args.steps):
-        run_once()
-    t_end.record()
-    torch.cuda.synchronize()
-    ms_total = t_start.elapsed_time(t_end)
-    ms_per_step = ms_total / args.steps
+    ms_per_step = timed_steps(torch, run_once, args.steps, args.warmup)
     pct = replay_percentiles(torch, run_once)
     cold = cold_times(torch, step, dev, args.cold_mib) if args.cold_mib > 0 else None
 
@@ -836,34 +1000,9 @@ def main():
     for k in ref:
         if not torch.equal(ref[k], snap[k]):
             raise RuntimeError(f"benchmark output drifted in {k}")
-
-    alg_k, alg_s = algorithmic(w)
-    kernels = {}
-    for k, us in kern_us.items():
-        r = roof(alg_k[k], us * 1e-6)
-        kernels[k] = {"us": us, "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"],
-                      "frac": r["frac"]}
-    stage_us = {}
-    for k, us in kern_us.items():
-        stage_us[STAGE_OF[k]] = stage_us.get(STAGE_OF[k], 0.0) + us
-    stages = {}
-    for st_name, us in stage_us.items():
-        r = roof(alg_s[st_name], us * 1e-6)
-        stages[st_name] = {"us": us, "bound": r["bound"], "achieved": r["achieved"],
-                           "unit": r["unit"], "frac": r["frac"]}
-    shared = {}
-    for k, us in shared_us.items():
-        r = roof(alg_k[k], us * 1e-6)
-        shared[k] = {"us": us, "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"],
-                     "frac": r["frac"]}
-    # the dominant kernel of the form the timed step runs
-    step_us = shared_us if form == "shared_launches" and shared_us else kern_us
-    dom = max(step_us, key=lambda k: step_us[k])
-    a = alg_k[dom]
-    rf = roof(a, step_us[dom] * 1e-6)
-    traffic = load_traffic(s.name, dom)
-    rf.update({"traffic": traffic, "kernel": dom, "kernel_us": step_us[dom],
-               "algorithmic_bytes": a["bytes"], "algorithmic_flops": a["flops"]})
+    rf, kernels, stages, shared, stage_us = rooflines(w, form, kern_us, shared_us)
+    del graph, step
+    torch.cuda.synchronize()
 
     toks = s.B * s.Nv
     value = toks / (ms_per_step * 1e-3)
@@ -880,13 +1019,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if w.dtype == "bf16" else "f32",
         "data": "synthetic",
-        "config": {"workload": s.name, "B": s.B, "Nv": s.Nv, "d": s.d, "H": s.H, "hd": s.hd,
-                   "Nt": s.Nt, "heads_per_sample": int(w.heads.shape[1]), "N1": w.N1, "N2": w.N2,
-                   "streams": 2 if split else 1, "step_form": form,
-                   "timing": ("hip-graph replay of the full step" +
-                              {"one_stream": "", "two_streams": ", merge branch on a second stream",
-                               "shared_launches": ", one pv_prune_pipeline call (shared launches)"}
-                              [form] if graph is not None else "eager")},
+        "config": config_of(w, form, split, run_once if not args.no_graph else None),
         "latency_us": {"pipeline": ms_per_step * 1000.0, "pipeline_single_replays": pct,
                        "pipeline_cold": cold, "kernels": kern_us,
                        "kernels_shared_launches": shared_us or None,
@@ -904,6 +1037,16 @@ def main():
     }
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    # the larger workloads: the same step and roofline figures, not the headline
+    others = [int(x) for x in args.per_config.split(",") if x.strip()] if args.per_config else []
+    per = {}
+    for wid in others:
+        if wid == args.workload:
+            continue
+        m = measure_other(torch, wid, dev, args)
+        per[m["config"]["workload"]] = m
+    if per:
+        line["per_config"] = per
     print(json.dumps(line), flush=True)
 
 

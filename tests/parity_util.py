@@ -90,3 +90,45 @@ def check_merged(gpu_merged: np.ndarray, vis: np.ndarray, kept, assign, slots, d
         assert np.all(np.abs(g - r) <= ulp * 1.0001), float(np.max(np.abs(g - r) / ulp))
     else:
         assert rel_err(g, ref) <= TOL["f32"]
+
+
+from oracle.parallel import oracle_assign, oracle_p, workers  # noqa: E402,F401
+
+
+def check_assign_all(gpu_assign: np.ndarray, vis_b: np.ndarray, kept: np.ndarray, dtype: str):
+    """check_assign_rows over every pruned row of one sample, with the oracle
+    run in parallel.  Returns #exempt rows."""
+    pruned = np.setdiff1d(np.arange(vis_b.shape[0]), kept).astype(np.int32)
+    if len(pruned) == 0:
+        return 0
+    a, b1, b2 = oracle_assign(vis_b, kept, pruned)
+    g = np.asarray(gpu_assign)[pruned]
+    close = (b1 - b2) < TAU_ASSIGN[dtype]
+    bad = (g != a) & ~close
+    assert not bad.any(), (f"assign differs at rows {pruned[bad][:8]}: gpu {g[bad][:8]} "
+                           f"oracle {a[bad][:8]}")
+    return int(close.sum())
+
+
+def check_dedup_sample(g: dict, b: int, vis_b: np.ndarray, p_ref: np.ndarray, n1: int,
+                       dtype: str):
+    """One sample of pv_prune_dedup's outputs (keys kept/score/assign/merged,
+    host arrays) against the oracle: p, the kept set, the nearest kept token
+    of every pruned row and every merged slot.  Returns (#near-tie tokens,
+    #near-tie rows)."""
+    assert rel_err(g["score"][b], p_ref) <= TOL[dtype], rel_err(g["score"][b], p_ref)
+    kept = np.asarray(g["kept"][b])
+    ex_k = check_kept(kept, p_ref, n1, dtype)
+    ex_a = check_assign_all(g["assign"][b], vis_b, kept, dtype)
+    check_merged(g["merged"][b], vis_b, kept, g["assign"][b], np.arange(n1), dtype)
+    return ex_k, ex_a
+
+
+_P_CACHE: dict = {}
+
+
+def oracle_p_workload(wid: int, anchors: np.ndarray, vis: np.ndarray) -> np.ndarray:
+    """oracle_p of a seeded workload, computed once per process."""
+    if wid not in _P_CACHE:
+        _P_CACHE[wid] = oracle_p(anchors, vis)
+    return _P_CACHE[wid]

@@ -1,10 +1,10 @@
 """HIP path vs the CPU oracle, element by element, on the seeded workloads.
 
-All calls go through the C ABI (ctypes binding).  Tiny and LLaVA-1.5 sizes
-are checked in full; at the larger sizes the oracle is run on whole samples
-for the scores and selections and on sampled rows / slots for the
-nearest-centroid assignment and the merge (each decision is computed by the
-oracle one by one, with the GPU's own kept list and assignment as input).
+All calls go through the C ABI (ctypes binding).  Every workload is checked
+in full: p and the kept set of every sample, the nearest kept token of every
+pruned row (the oracle given the GPU's kept list) and every merged slot (the
+oracle given the GPU's assignment).  At the large workloads the oracle runs
+over row ranges in parallel threads (the same arithmetic as one call).
 """
 
 from __future__ import annotations
@@ -17,8 +17,8 @@ import pytest
 
 import oracle
 from paper_2608_25332_amd import workloads as W
-from parity_util import (TOL, check_assign_rows, check_kept, check_merged, rel_err, to_dev,
-                         to_host)
+from parity_util import (TOL, check_assign_rows, check_dedup_sample, check_kept, check_merged,
+                         oracle_p_workload, rel_err, to_dev, to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -54,37 +54,27 @@ def run_dedup(vis_np, anc_np, dtype, budget):
 
 # --------------------------------------------------------------- dedup ------
 
-FULL_SAMPLES = {1: None, 2: None, 3: [0, 7, 15], 4: [0, 3], 5: [0, 1]}
-
-
 @pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
 def test_dedup_parity(wid):
     w = workload(wid, with_kv=False)
     dt = w.dtype
     _say(f"[dedup] workload {wid} {w.spec.name} B={w.spec.B} Nv={w.spec.Nv} d={w.spec.d}")
     g = run_dedup(w.vis, w.anchors, dt, w.N1)
-    B, Nv = w.spec.B, w.spec.Nv
-    samples = FULL_SAMPLES[wid] or list(range(B))
-    rng = np.random.default_rng(100 + wid)
-    exempt = 0
+    B = w.spec.B
     for b in range(B):
         kept = g["kept"][b]
         assert np.all(np.diff(kept) > 0) and kept.shape == (w.N1,)
         # kept tokens are their own centroids; every token has a valid slot
         assert np.array_equal(g["assign"][b][kept], np.arange(w.N1))
         assert g["assign"][b].min() >= 0 and g["assign"][b].max() < w.N1
-    for b in samples:
-        M = oracle.cosine(w.anchors[b], w.vis[b])
-        p = oracle.maxpool(oracle.center(M))
-        assert rel_err(g["score"][b], p) <= TOL[dt], rel_err(g["score"][b], p)
-        exempt += check_kept(g["kept"][b], p, w.N1, dt)
-        kept = g["kept"][b]
-        pruned = np.setdiff1d(np.arange(Nv), kept)
-        rows = pruned if Nv <= 576 else np.sort(rng.choice(pruned, 48, replace=False))
-        check_assign_rows(g["assign"][b], w.vis[b], kept, rows, dt)
-        slots = np.arange(w.N1) if Nv <= 576 else np.sort(rng.choice(w.N1, 16, replace=False))
-        check_merged(g["merged"][b], w.vis[b], kept, g["assign"][b], slots, dt)
-    _say(f"[dedup] workload {wid}: ok, {exempt} near-tie tokens exempt")
+    p_ref = oracle_p_workload(wid, w.anchors, w.vis)
+    ex_k = ex_a = 0
+    for b in range(B):
+        k, a = check_dedup_sample(g, b, w.vis[b], p_ref[b], w.N1, dt)
+        ex_k += k
+        ex_a += a
+    _say(f"[dedup] workload {wid}: ok on all {B} samples, every pruned row and slot; "
+         f"{ex_k} near-tie tokens, {ex_a} near-tie rows exempt")
 
 
 def test_dedup_tiny_exact_against_full_oracle():
@@ -483,13 +473,15 @@ def test_gather_out_of_range_rows_are_zero():
 
 # ------------------------------------------------------------- pipeline -----
 
-@pytest.mark.parametrize("wid", [1, 2])
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
 def test_pipeline_against_oracle(wid):
-    """The step bench.py times: dedup -> K/V of the kept tokens -> head-aware
-    -> compaction of hidden (merged), K and V."""
+    """The step bench.py times, as separate calls: dedup -> K/V of the kept
+    tokens -> head-aware -> compaction of hidden (merged), K and V; every
+    sample, pruned row and slot against the oracle."""
     from paper_2608_25332_amd import provip
     w = workload(wid)
     dt = w.dtype
+    _say(f"[pipeline-calls] workload {wid}")
     vis, anc = to_dev(w.vis, dt), to_dev(w.anchors, dt)
     q, kf, vf = to_dev(w.q, dt), to_dev(w.k_full, dt), to_dev(w.v_full, dt)
     r = provip.pv_prune_dedup(vis, anc, w.N1)
@@ -497,17 +489,19 @@ def test_pipeline_against_oracle(wid):
     h = provip.pv_prune_head_aware(q, k1, w.heads, w.N2)
     hid2, k2, v2 = provip.pv_prune_gather_batch([r["merged"], k1, v1], h["kept"])
     torch.cuda.synchronize()
-    ref = oracle.dedup(w.anchors, w.vis, w.N1)
-    kept1 = to_host(r["kept"])
+    g = {k: to_host(r[k]) for k in ("kept", "score", "assign", "merged")}
+    p_ref = oracle_p_workload(wid, w.anchors, w.vis)
     for b in range(w.spec.B):
-        check_kept(kept1[b], ref["p"][b], w.N1, dt)
+        check_dedup_sample(g, b, w.vis[b], p_ref[b], w.N1, dt)
+    kept1 = g["kept"]
     k1_ref = np.stack([w.k_full[b][:, kept1[b]] for b in range(w.spec.B)])
     assert np.array_equal(to_host(k1), k1_ref)
     _, v_ref = oracle.head_aware(w.q, k1_ref, w.heads, w.N2)
     kept2 = to_host(h["kept"])
+    assert rel_err(to_host(h["score"]), v_ref) <= TOL[dt]
     for b in range(w.spec.B):
         check_kept(kept2[b], v_ref[b], w.N2, dt)
-    assert np.array_equal(to_host(hid2), oracle.gather(to_host(r["merged"]), kept2))
+    assert np.array_equal(to_host(hid2), oracle.gather(g["merged"], kept2))
     assert np.array_equal(to_host(k2), oracle.gather(k1_ref, kept2))
     v1_ref = np.stack([w.v_full[b][:, kept1[b]] for b in range(w.spec.B)])
     assert np.array_equal(to_host(v2), oracle.gather(v1_ref, kept2))

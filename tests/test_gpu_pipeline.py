@@ -18,7 +18,8 @@ import pytest
 
 import oracle
 from paper_2608_25332_amd import workloads as W
-from parity_util import check_kept, to_dev, to_host
+from parity_util import (TOL, check_dedup_sample, check_kept, oracle_p_workload, rel_err, to_dev,
+                         to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -82,36 +83,42 @@ def test_pipeline_shared_launches_equal_separate(wid):
     _assert_same(fused, sep)
 
 
-@pytest.mark.parametrize("wid", [1, 2])
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
 def test_pipeline_against_oracle(wid):
-    """The step bench.py times, in one call, against the oracle."""
+    """The step bench.py times, in one call, against the oracle: every
+    sample's p and kept set, the nearest kept token of every pruned row,
+    every merged slot, the head-aware score and selection, and the
+    compacted tensors byte for byte."""
     from paper_2608_25332_amd import provip
     w = workload(wid)
     dt = w.dtype
     _say(f"[pipeline-oracle] workload {wid}")
     o = provip.pv_prune_pipeline(*_inputs(w), w.heads, w.N1, w.N2)
     torch.cuda.synchronize()
-    ref = oracle.dedup(w.anchors, w.vis, w.N1)
-    kept1 = to_host(o["kept1"])
+    g = {"kept": to_host(o["kept1"]), "score": to_host(o["score1"]),
+         "assign": to_host(o["assign"]), "merged": to_host(o["merged"])}
+    p_ref = oracle_p_workload(wid, w.anchors, w.vis)
     for b in range(w.spec.B):
-        check_kept(kept1[b], ref["p"][b], w.N1, dt)
+        check_dedup_sample(g, b, w.vis[b], p_ref[b], w.N1, dt)
+    kept1 = g["kept"]
     k1_ref = np.stack([w.k_full[b][:, kept1[b]] for b in range(w.spec.B)])
     v1_ref = np.stack([w.v_full[b][:, kept1[b]] for b in range(w.spec.B)])
     assert np.array_equal(to_host(o["k1"]), k1_ref)
     assert np.array_equal(to_host(o["v1"]), v1_ref)
     _, v_ref = oracle.head_aware(w.q, k1_ref, w.heads, w.N2)
+    assert rel_err(to_host(o["score2"]), v_ref) <= TOL[dt]
     kept2 = to_host(o["kept2"])
     for b in range(w.spec.B):
         check_kept(kept2[b], v_ref[b], w.N2, dt)
-    assert np.array_equal(to_host(o["hidden2"]), oracle.gather(to_host(o["merged"]), kept2))
+    assert np.array_equal(to_host(o["hidden2"]), oracle.gather(g["merged"], kept2))
     assert np.array_equal(to_host(o["k2"]), oracle.gather(k1_ref, kept2))
     assert np.array_equal(to_host(o["v2"]), oracle.gather(v1_ref, kept2))
     if wid == 1:
-        # the tiny fp32 workload is checked in full: assignment and merge too
-        assert np.array_equal(to_host(o["kept1"]), ref["kept"])
-        assert np.array_equal(to_host(o["assign"]), ref["assign"])
-        m = to_host(o["merged"])
-        assert np.max(np.abs(m - ref["merged"])) <= 1e-5 * np.max(np.abs(ref["merged"]))
+        # the tiny fp32 workload has no near ties: the whole step is exact
+        ref = oracle.dedup(w.anchors, w.vis, w.N1)
+        assert np.array_equal(g["kept"], ref["kept"])
+        assert np.array_equal(g["assign"], ref["assign"])
+        assert np.max(np.abs(g["merged"] - ref["merged"])) <= 1e-5 * np.max(np.abs(ref["merged"]))
 
 
 # (B, Nv, Nt, d, H, hd, n_heads, N1, N2, dtype, shared): shapes on both sides
@@ -162,13 +169,17 @@ def test_pipeline_edges(B, Nv, Nt, d, H, hd, nh, N1, N2, dt, shared):
     torch.cuda.synchronize()
     assert (timed["n_kernels"] > 0) == shared, timed.get("kernel_names")
     _assert_same(timed, sep)
-    # the separate step is the four calls: check its selections against the
-    # oracle on the first and last sample
-    for b in sorted({0, B - 1}):
-        ref = oracle.dedup(anc[b:b + 1], vis[b:b + 1], N1)
-        check_kept(to_host(sep["kept1"])[b], ref["p"][0], N1, dt)
-        kept1 = to_host(sep["kept1"])[b]
+    # the separate step is the four calls: every sample against the oracle
+    # (p, kept set, the nearest kept token of every pruned row, every merged
+    # slot, the head-aware score and selection)
+    sh = {"kept": to_host(sep["kept1"]), "score": to_host(sep["score1"]),
+          "assign": to_host(sep["assign"]), "merged": to_host(sep["merged"])}
+    for b in range(B):
+        ref = oracle.dedup(anc[b:b + 1], vis[b:b + 1], N1, want_assign=False)
+        check_dedup_sample(sh, b, vis[b], ref["p"][0], N1, dt)
+        kept1 = sh["kept"][b]
         _, v_ref = oracle.head_aware(q[b:b + 1], kf[b:b + 1][:, :, kept1], heads[b:b + 1], N2)
+        assert rel_err(to_host(sep["score2"])[b], v_ref[0]) <= TOL[dt]
         check_kept(to_host(sep["kept2"])[b], v_ref[0], N2, dt)
 
 
