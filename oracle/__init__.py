@@ -17,6 +17,8 @@ Function map (paper passages are cited at each C function):
   head_aware_in_model        -- Sec. 4.4 on the visual slice of the model's softmax
   head_confidence /
   visual_heads               -- Sec. 4.4, equations for C^h and V_l
+  head_confidence_in_model /
+  visual_heads_in_model      -- the same on the visual slice of the model's softmax
   gather                     -- compaction of kept rows (Sec. 4.1)
   dedup                      -- Sec. 4.3 end to end
 
@@ -100,6 +102,10 @@ def _declare(lib):
     lib.orc_head_confidence.restype = _int
     lib.orc_visual_heads.argtypes = [_D, _D, _int, _int, _int, _int, _int, _I, _D]
     lib.orc_visual_heads.restype = _int
+    lib.orc_head_confidence_in_model.argtypes = [_D, _D, _D, _int, _int, _int, _int, _D]
+    lib.orc_head_confidence_in_model.restype = _int
+    lib.orc_visual_heads_in_model.argtypes = [_D, _D, _D, _int, _int, _int, _int, _int, _I, _D]
+    lib.orc_visual_heads_in_model.restype = _int
     lib.orc_gather.argtypes = [_U8, _U8, _I, _int, _int, _int, _int, _i64,
                                _i64, _i64, _i64, _i64, _i64, _i64]
     lib.orc_gather.restype = _int
@@ -343,6 +349,38 @@ def visual_heads(q, k, n_vis: int, *, lib=None):
                                   _pd(conf[b]))
         if rc != 0:
             raise OracleError(f"orc_visual_heads rc={rc}")
+    return heads, conf
+
+
+def head_confidence_in_model(q, k, lse, *, lib=None) -> np.ndarray:
+    """One sample on the model's softmax domain: q [H, nt, hd], k [H, n, hd],
+    lse [H, nt] (log-sum-exp of each row's scaled logits over the
+    non-visual keys) -> C [H]."""
+    lib = lib or load()
+    q, k, lse = _f64(q), _f64(k), _f64(lse)
+    H, nt, hd = q.shape
+    n = k.shape[1]
+    c = np.empty(H, np.float64)
+    rc = lib.orc_head_confidence_in_model(_pd(q), _pd(k), _pd(lse), H, nt, n, hd, _pd(c))
+    if rc != 0:
+        raise OracleError(f"orc_head_confidence_in_model rc={rc}")
+    return c
+
+
+def visual_heads_in_model(q, k, lse, n_vis: int, *, lib=None):
+    """Sec. 4.4 on the model's softmax domain over a batch: q [B,H,nt,hd],
+    k [B,H,n,hd], lse [B,H,nt] -> (heads [B,n_vis] ascending, C [B,H])."""
+    lib = lib or load()
+    Q, K, L = _f64(q), _f64(k), _f64(lse)
+    B, H, nt, hd = Q.shape
+    n = K.shape[2]
+    heads = np.empty((B, n_vis), np.int32)
+    conf = np.empty((B, H), np.float64)
+    for b in range(B):
+        rc = lib.orc_visual_heads_in_model(_pd(Q[b]), _pd(K[b]), _pd(L[b]), H, nt, n, hd,
+                                           int(n_vis), _pi(heads[b]), _pd(conf[b]))
+        if rc != 0:
+            raise OracleError(f"orc_visual_heads_in_model rc={rc}")
     return heads, conf
 
 

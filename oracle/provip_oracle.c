@@ -479,6 +479,61 @@ int orc_visual_heads(const double *q, const double *k, int H, int nt, int n, int
 }
 
 /* --------------------------------------------------------------------------
+ * Sec. 4.4, equation for C^h, with A^cross taken as the model has it: the
+ * visual slice of each text row's softmax over every key before it (the map
+ * of orc_attention_in_model, whose non-visual keys enter through one
+ * log-sum-exp per row).  The slice of a row sums to less than 1; its
+ * variance is the population variance of its n entries about their own
+ * mean, and C[h] sums it over the rows passed in.  lse = -inf everywhere
+ * gives orc_head_confidence.
+ * q: [H][nt][hd], k: [H][n][hd], lse: [H][nt], conf: [H].
+ * Returns 0, or -3 on no memory.
+ * ------------------------------------------------------------------------ */
+int orc_head_confidence_in_model(const double *q, const double *k, const double *lse, int H,
+                                 int nt, int n, int hd, double *conf)
+{
+    double *slice_map = (double *)malloc(sizeof(double) * (size_t)nt * n);
+    if (!slice_map) return -3;
+    for (int h = 0; h < H; ++h) {
+        orc_attention_in_model(q + (size_t)h * nt * hd, k + (size_t)h * n * hd,
+                               lse + (size_t)h * nt, nt, n, hd, slice_map);
+        double total = 0.0;
+        for (int i = 0; i < nt; ++i) {
+            const double *slice = slice_map + (size_t)i * n;
+            double avg = 0.0;
+            for (int j = 0; j < n; ++j) avg += slice[j];
+            avg /= (double)n;
+            double sq_dev = 0.0;
+            for (int j = 0; j < n; ++j) {
+                double dev = slice[j] - avg;
+                sq_dev += dev * dev;
+            }
+            total += sq_dev / (double)n;
+        }
+        conf[h] = total;
+    }
+    free(slice_map);
+    return 0;
+}
+
+/* --------------------------------------------------------------------------
+ * Sec. 4.4, equation for V_l on the confidence above: the N_vis heads of
+ * highest C (orc_topk's order rule), ascending.  conf_out may be NULL.
+ * ------------------------------------------------------------------------ */
+int orc_visual_heads_in_model(const double *q, const double *k, const double *lse, int H,
+                              int nt, int n, int hd, int n_vis, int32_t *heads,
+                              double *conf_out)
+{
+    double *cm = (double *)malloc(sizeof(double) * (size_t)H);
+    if (!cm) return -3;
+    int rc = orc_head_confidence_in_model(q, k, lse, H, nt, n, hd, cm);
+    if (rc == 0) rc = orc_topk(cm, H, n_vis, heads);
+    if (rc == 0 && conf_out) memcpy(conf_out, cm, sizeof(double) * (size_t)H);
+    free(cm);
+    return rc;
+}
+
+/* --------------------------------------------------------------------------
  * Sec. 4.1: pruned tokens are excluded from all later computation, so the
  * rows of the kept tokens are compacted, in token order.  Byte copy:
  *     dst[b][g][r] = src[b][g][idx[b][r]]   (rows of row_bytes bytes).

@@ -555,6 +555,85 @@ def pin_visual_heads_topk(lib):
             assert np.array_equal(heads, np.tile(np.arange(H), (B, 1)))
 
 
+# ------------------------------- Eq. C^h on the model's softmax domain -----
+
+def _slice_logits(q, k, ko, hd):
+    import torch
+    Q, K, Ko = (torch.from_numpy(x) for x in (q, k, ko))
+    lo = torch.matmul(Q, Ko.transpose(-1, -2).contiguous()) / math.sqrt(hd)
+    lv = torch.matmul(Q, K.transpose(-1, -2).contiguous()) / math.sqrt(hd)
+    return lo, lv
+
+
+def pin_confidence_in_model_visual_slice(lib):
+    """Sec. 4.4, equation for C^h on A^cross as the model has it: numpy's
+    population variance (np.var) of the visual slice of one torch softmax
+    (float64) over explicit non-visual keys and the visual keys, summed over
+    the rows.  The other keys enter only through their log-sum-exp, and
+    their share of each row changes C."""
+    import torch
+    rng = np.random.default_rng(41)
+    H, nt, n, n_other, hd = 4, 6, 13, 9, 16
+    q = rng.standard_normal((H, nt, hd)) * 2
+    k = rng.standard_normal((H, n, hd)) * 2
+    ko = rng.standard_normal((H, n_other, hd)) * 2
+    lo, lv = _slice_logits(q, k, ko, hd)
+    full = torch.softmax(torch.cat([lo, lv], dim=-1), dim=-1).numpy()
+    want = np.var(full[..., n_other:], axis=2).sum(axis=1)
+    lse = torch.logsumexp(lo, dim=-1).numpy()
+    c = O.head_confidence_in_model(q, k, lse, lib=lib)
+    assert np.max(np.abs(c - want)) < 1e-15 * max(1.0, want.max())
+    c_plain = O.head_confidence(q, k, lib=lib)
+    assert np.max(np.abs(c - c_plain)) > 1e-3 * c_plain.max()
+
+
+def pin_confidence_in_model_closed_forms(lib):
+    """lse = -inf everywhere is the plain confidence, bit for bit; two
+    visual keys with scaled logits 0 and b and lse = t give the slice
+    (1, e^b) / (1 + e^b + e^t), whose population variance is
+    ((A_1 - A_2) / 2)^2; permuting the visual keys leaves C unchanged."""
+    rng = np.random.default_rng(42)
+    H, nt, n, hd = 3, 5, 11, 8
+    q = rng.standard_normal((H, nt, hd)) * 2
+    k = rng.standard_normal((H, n, hd)) * 2
+    c0 = O.head_confidence_in_model(q, k, np.full((H, nt), -np.inf), lib=lib)
+    assert np.array_equal(c0, O.head_confidence(q, k, lib=lib))
+    lse = rng.standard_normal((H, nt))
+    c1 = O.head_confidence_in_model(q, k, lse, lib=lib)
+    cp = O.head_confidence_in_model(q, k[:, rng.permutation(n)], lse, lib=lib)
+    assert np.max(np.abs(cp - c1)) < 1e-15
+    hd2 = 4
+    bs = np.array([0.5, -1.0, 2.0, 0.0])
+    ts = np.array([1.0, -0.5, 3.0, -2.0])
+    q2 = np.zeros((1, 4, hd2))
+    q2[0, :, 0] = bs * math.sqrt(hd2)   # key 1's scaled logit is b; key 0's is 0
+    k2 = np.zeros((1, 2, hd2))
+    k2[0, 1, 0] = 1.0
+    c2 = O.head_confidence_in_model(q2, k2, ts[None], lib=lib)
+    den = 1.0 + np.exp(bs) + np.exp(ts)
+    want = np.sum(((1.0 - np.exp(bs)) / den / 2.0) ** 2)
+    assert abs(c2[0] - want) < 1e-16
+
+
+def pin_visual_heads_in_model_topk(lib):
+    """Sec. 4.4, equation for V_l on the in-model confidence: the N_vis heads
+    of largest C (numpy stable argsort order), ascending; with lse = -inf the
+    plain visual heads."""
+    rng = np.random.default_rng(43)
+    B, H, nt, n, hd = 2, 7, 4, 9, 8
+    q = rng.standard_normal((B, H, nt, hd)) * 2
+    k = rng.standard_normal((B, H, n, hd)) * 2
+    lse = rng.standard_normal((B, H, nt)) + 1.5
+    for nv in (1, 3, H):
+        heads, conf = O.visual_heads_in_model(q, k, lse, nv, lib=lib)
+        for b in range(B):
+            assert np.array_equal(heads[b], np.sort(np.argsort(-conf[b], kind="stable")[:nv]))
+            assert np.array_equal(conf[b], O.head_confidence_in_model(q[b], k[b], lse[b], lib=lib))
+    hp, cp = O.visual_heads_in_model(q, k, np.full((B, H, nt), -np.inf), 3, lib=lib)
+    hv, cv = O.visual_heads(q, k, 3, lib=lib)
+    assert np.array_equal(hp, hv) and np.array_equal(cp, cv)
+
+
 # ---------------------------------------------------------------- gather ---
 
 def pin_gather_bytes(lib):

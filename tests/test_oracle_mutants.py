@@ -64,6 +64,18 @@ MUTANTS = [
      "for (int i = 0; i < 1; ++i) {\n            const double *row = A + (size_t)i * n;"),
     ("visual-heads-lowest", "if (rc == 0) rc = orc_topk(c, H, n_vis, heads);",
      "for (int h = 0; h < H; ++h) c[h] = -c[h];\n    if (rc == 0) rc = orc_topk(c, H, n_vis, heads);"),
+    ("confidence-in-model-visual-only",
+     "orc_attention_in_model(q + (size_t)h * nt * hd, k + (size_t)h * n * hd,\n                               lse + (size_t)h * nt, nt, n, hd, slice_map);",
+     "orc_attention(q + (size_t)h * nt * hd, k + (size_t)h * n * hd, nt, n, hd, slice_map);"),
+    ("confidence-in-model-lse-of-head-0", "lse + (size_t)h * nt, nt, n, hd, slice_map);",
+     "lse, nt, n, hd, slice_map);"),
+    ("confidence-in-model-mean-assumes-unit-mass", "avg /= (double)n;", "avg = 1.0 / (double)n;"),
+    ("confidence-in-model-sample-variance", "total += sq_dev / (double)n;",
+     "total += sq_dev / (double)(n - 1);"),
+    ("confidence-in-model-first-row-only", "const double *slice = slice_map + (size_t)i * n;",
+     "const double *slice = slice_map;"),
+    ("visual-heads-in-model-lowest", "if (rc == 0) rc = orc_topk(cm, H, n_vis, heads);",
+     "for (int h = 0; h < H; ++h) cm[h] = -cm[h];\n    if (rc == 0) rc = orc_topk(cm, H, n_vis, heads);"),
 ]
 
 
