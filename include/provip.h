@@ -270,6 +270,25 @@ int pv_visual_heads(const void *q, const void *k, int B, int H, int Nt, int N, i
                     int n_vis, int32_t *heads_out, float *conf, void *workspace,
                     size_t workspace_bytes, void *stream);
 
+/* Visual heads on the cross-modal map as the model has it (Sec. 4.4: the
+ * confidence is taken on A^cross, the visual slice of the backbone's
+ * attention, whose softmax also runs over the system and text keys before
+ * each text row).  With row_lse as in pv_prune_head_aware_ex,
+ *   A_h[i][j] = exp(s_ij) / ( sum_{visual j'} exp(s_ij') + exp(row_lse[b][h][i]) )
+ *   C[b][h]   = sum_i Var_j(A_h[i][j])    population variance of the row's
+ *               visual slice (which sums to less than 1) over the N keys.
+ * row_mask  [B][Nt] int32  DEVICE, may be NULL: the rows summed, as in
+ *           pv_visual_heads_masked (NULL: every row)
+ * row_lse   [B][H][Nt] float32 DEVICE, 4-byte aligned, finite or -INFINITY
+ *           (natural-log units), may be NULL: NULL or -INFINITY entries give
+ *           pv_visual_heads(_masked)'s results bit for bit.
+ * Everything else, the workspace and the errors are those of
+ * pv_visual_heads. */
+int pv_visual_heads_ex(const void *q, const void *k, const int32_t *row_mask,
+                       const float *row_lse, int B, int H, int Nt, int N, int hd, int dtype,
+                       int n_vis, int32_t *heads_out, float *conf, void *workspace,
+                       size_t workspace_bytes, void *stream);
+
 /* -------------------------------------------------------------------------
  * The retention rule of both stages on its own (Sec. 4.3: keep the N_1
  * tokens with the highest p; Sec. 4.4: keep the N_2 tokens with the highest
@@ -380,6 +399,13 @@ int pv_prune_dedup_masked_timed(const void *vis, const void *anchors, const int3
                                 void *workspace, size_t workspace_bytes, void *stream,
                                 void *const *events, int n_events, int reps, int *n_kernels,
                                 const char **names);
+
+int pv_visual_heads_ex_timed(const void *q, const void *k, const int32_t *row_mask,
+                             const float *row_lse, int B, int H, int Nt, int N, int hd,
+                             int dtype, int n_vis, int32_t *heads_out, float *conf,
+                             void *workspace, size_t workspace_bytes, void *stream,
+                             void *const *events, int n_events, int reps, int *n_kernels,
+                             const char **names);
 
 int pv_visual_heads_masked_timed(const void *q, const void *k, const int32_t *row_mask, int B,
                                  int H, int Nt, int N, int hd, int dtype, int n_vis,

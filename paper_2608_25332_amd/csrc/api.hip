@@ -403,10 +403,12 @@ size_t vis_heads_bytes(int B, int H, int Nt) {
 int vis_heads_impl(const void *q, const void *k, int B, int H, int Nt, int N, int hd, int dtype,
                    int n_vis, int32_t *heads_out, float *conf, void *workspace, size_t ws_bytes,
                    void *stream, void *const *events, int n_events, int reps, int *n_kernels,
-                   const char **names, const int32_t *row_mask = nullptr) {
+                   const char **names, const int32_t *row_mask = nullptr,
+                   const float *row_lse = nullptr) {
     if (reps < 1) return PV_ERR_SHAPE;
     if (!heads_out) return PV_ERR_NULL;
     if (row_mask && (uintptr_t)row_mask % 4) return PV_ERR_ALIGN;
+    if (row_lse && (uintptr_t)row_lse % 4) return PV_ERR_ALIGN;
     int rc = check_qk(q, k, B, H, Nt, N, hd, dtype);
     if (rc != PV_OK) return rc;
     if (H > PV_MAX_HEADS || n_vis < 1 || n_vis > H) return PV_ERR_HEADS;
@@ -419,7 +421,7 @@ int vis_heads_impl(const void *q, const void *k, int B, int H, int Nt, int N, in
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
     if (!tr.launch("head_conf", [&] {
-            return pv::launch_head_conf(dt, q, k, row_mask, B, H, Nt, N, hd, part, st);
+            return pv::launch_head_conf(dt, q, k, row_mask, row_lse, B, H, Nt, N, hd, part, st);
         }))
         return PV_ERR_HIP;
     if (!tr.launch("conf_select", [&] {
@@ -690,6 +692,26 @@ PV_API int pv_visual_heads_masked_timed(const void *q, const void *k, const int3
     return vis_heads_impl(q, k, B, H, Nt, N, hd, dtype, n_vis, heads_out, conf, workspace,
                           workspace_bytes, stream, events, n_events, reps, n_kernels, names,
                           row_mask);
+}
+
+PV_API int pv_visual_heads_ex(const void *q, const void *k, const int32_t *row_mask,
+                              const float *row_lse, int B, int H, int Nt, int N, int hd, int dtype,
+                              int n_vis, int32_t *heads_out, float *conf, void *workspace,
+                              size_t workspace_bytes, void *stream) {
+    return vis_heads_impl(q, k, B, H, Nt, N, hd, dtype, n_vis, heads_out, conf, workspace,
+                          workspace_bytes, stream, nullptr, 0, 1, nullptr, nullptr, row_mask,
+                          row_lse);
+}
+
+PV_API int pv_visual_heads_ex_timed(const void *q, const void *k, const int32_t *row_mask,
+                                    const float *row_lse, int B, int H, int Nt, int N, int hd,
+                                    int dtype, int n_vis, int32_t *heads_out, float *conf,
+                                    void *workspace, size_t workspace_bytes, void *stream,
+                                    void *const *events, int n_events, int reps, int *n_kernels,
+                                    const char **names) {
+    return vis_heads_impl(q, k, B, H, Nt, N, hd, dtype, n_vis, heads_out, conf, workspace,
+                          workspace_bytes, stream, events, n_events, reps, n_kernels, names,
+                          row_mask, row_lse);
 }
 
 PV_API int pv_visual_heads_timed(const void *q, const void *k, int B, int H, int Nt, int N, int hd,

@@ -338,8 +338,13 @@ __device__ __forceinline__ void score_partial_block(
                 if (row_mask[(size_t)b * Nt + i] != 0) any_row = 1;
             __syncthreads();
         }
-        // Var_j(A[i][j]) = (sum_j A^2 - 1/N) / N with sum_j A^2 = s / l^2;
-        // the 16 rows added in order (rows past Nt add nothing)
+        // Var_j(A[i][j]) = (sum_j A^2 - S^2 / N) / N over the N visual keys,
+        // with D the row's normaliser, S = l / D its visual mass and
+        // sum_j A^2 = s / D^2.  Over the visual keys alone D = l and S = 1;
+        // on the model's domain the other keys join D through their
+        // log-sum-exp (row_lse, natural log of the scaled logits), on the
+        // scale of the kept exponentials (relative to the row maximum).  The
+        // 16 rows are added in order (rows past Nt add nothing).
         if (tid < 16) {
             float mm = sm_m[0][tid], ll = sm_l[0][tid], ss = sm_s[0][tid];
 #pragma unroll
@@ -347,7 +352,13 @@ __device__ __forceinline__ void score_partial_block(
             const float inv_n = 1.0f / (float)N;
             const int i = rb * 16 + tid;
             const bool use = i < Nt && (!row_mask || !any_row || row_mask[(size_t)b * Nt + i] != 0);
-            row_m[tid] = use ? (ss / (ll * ll) - inv_n) * inv_n : 0.f;
+            float den = ll;
+            if (row_lse) {
+                const float t = row_lse[((size_t)b * H + h) * Nt + min(i, Nt - 1)] * 1.4426950408889634f;
+                den = ll + exp2_hw(t - mm);  // an overflow means the visual mass is 0 in fp32
+            }
+            const float mass = ll / den;
+            row_m[tid] = use ? (ss / (den * den) - mass * mass * inv_n) * inv_n : 0.f;
         }
         __syncthreads();
         if (tid == 0) {
@@ -677,7 +688,7 @@ struct ScoreLaunch {
     const int32_t *heads_dev;   // kHeadsDevice: device list [B][n_heads]
     int src;
     const int32_t *row_mask;    // confidence only: rows summed (may be NULL)
-    const float *row_lse;       // score only: [B][H][Nt] non-visual log-sum-exp (may be NULL)
+    const float *row_lse;       // [B][H][Nt] non-visual log-sum-exp (may be NULL)
     int B, H, Nt, N, n_heads;
     float sl2e;
     float *partial;
@@ -843,9 +854,10 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const int3
     return score_any<false>(dt, hd, a);
 }
 
-hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask, int B,
-                            int H, int Nt, int N, int hd, float *partial, hipStream_t st) {
-    ScoreLaunch a{q, k, nullptr, nullptr, kHeadsAll, row_mask, nullptr, B, H, Nt, N, H, 0.f,
+hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask,
+                            const float *row_lse, int B, int H, int Nt, int N, int hd,
+                            float *partial, hipStream_t st) {
+    ScoreLaunch a{q, k, nullptr, nullptr, kHeadsAll, row_mask, row_lse, B, H, Nt, N, H, 0.f,
                   partial, st};
     return score_any<true>(dt, hd, a);
 }

@@ -115,8 +115,11 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const int3
                                 hipStream_t st, const ReduceJob *with = nullptr);
 // Head confidence of every head, per 16-row block: partial[b][h][rb].
 // row_mask as for launch_center: the rows summed into the confidence.
-hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask, int B,
-                            int H, int Nt, int N, int hd, float *partial, hipStream_t st);
+// row_lse as for launch_score_partial (may be NULL): the variance is then
+// taken over the visual slice of the model's softmax.
+hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask,
+                            const float *row_lse, int B, int H, int Nt, int N, int hd,
+                            float *partial, hipStream_t st);
 hipError_t launch_conf_select(const float *partial, int B, int H, int Nt, float *conf, int n_vis,
                               int32_t *heads, hipStream_t st);
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,

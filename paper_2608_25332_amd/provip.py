@@ -124,6 +124,11 @@ def load(path: str = LIB_PATH):
     lib.pv_visual_heads_masked.restype = _i
     lib.pv_visual_heads_masked_timed.argtypes = vhm + timed_tail
     lib.pv_visual_heads_masked_timed.restype = _i
+    vhx = [_vp, _vp, _vp, _vp] + vh[2:]
+    lib.pv_visual_heads_ex.argtypes = vhx
+    lib.pv_visual_heads_ex.restype = _i
+    lib.pv_visual_heads_ex_timed.argtypes = vhx + timed_tail
+    lib.pv_visual_heads_ex_timed.restype = _i
     lib.pv_prune_gather.argtypes = [_vp, _vp, _vp, _i, _i, _i, _i, _i64, _i64, _i64, _i64, _i64,
                                     _i64, _i64, _vp]
     lib.pv_prune_gather.restype = _i
@@ -399,12 +404,16 @@ def pv_prune_head_aware(q: torch.Tensor, k: torch.Tensor, heads, budget: int, *,
 def pv_visual_heads(q: torch.Tensor, k: torch.Tensor, n_vis: int, *, want_conf: bool = True,
                     out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None,
                     events: Optional[Sequence] = None, reps: int = 1,
-                    row_mask: Optional[torch.Tensor] = None):
+                    row_mask: Optional[torch.Tensor] = None,
+                    row_lse: Optional[torch.Tensor] = None):
     """Visual-head identification.  q [B,H,Nt,hd], k [B,H,N,hd].  Returns
     dict(heads [B,n_vis] int32 on the device, ascending; conf [B,H] f32 |
     None, n_kernels).  The head list can go straight to pv_prune_head_aware.
     row_mask: int32 [B, Nt] on the device: the confidence sums over the rows
-    set only (pv_visual_heads_masked)."""
+    set only (pv_visual_heads_masked).  row_lse: float32 [B, H, Nt] on the
+    device: the log-sum-exp of each row's scaled logits over the non-visual
+    keys, so that the variance is taken on the model's softmax domain
+    (pv_visual_heads_ex)."""
     lib = load()
     _contig(q, "q")
     _contig(k, "k")
@@ -425,7 +434,18 @@ def pv_visual_heads(q: torch.Tensor, k: torch.Tensor, n_vis: int, *, want_conf: 
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     ev, nev, nm = _events_array(events)
     nk = _i(0)
-    if row_mask is not None:
+    if row_lse is not None:
+        if row_mask is not None:
+            _check_mask(row_mask, B, Nt, dev, "row_mask")
+        if (tuple(row_lse.shape) != (B, H, Nt) or row_lse.dtype != torch.float32
+                or row_lse.device != dev or not row_lse.is_contiguous()):
+            raise ValueError("row_lse must be a contiguous float32 [B, H, Nt] device tensor")
+        rc = lib.pv_visual_heads_ex_timed(q.data_ptr(), k.data_ptr(), _ptr(row_mask),
+                                          row_lse.data_ptr(), B, H, Nt, N, hd, _dtype_code(q),
+                                          int(n_vis), heads.data_ptr(), _ptr(conf),
+                                          workspace.data_ptr(), workspace.numel(), _stream(dev),
+                                          ev, nev, int(reps), ctypes.byref(nk), nm)
+    elif row_mask is not None:
         _check_mask(row_mask, B, Nt, dev, "row_mask")
         rc = lib.pv_visual_heads_masked_timed(q.data_ptr(), k.data_ptr(), row_mask.data_ptr(), B,
                                               H, Nt, N, hd, _dtype_code(q), int(n_vis),

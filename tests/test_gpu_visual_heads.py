@@ -226,3 +226,113 @@ def test_head_aware_in_model_whole_head_form():
     assert rel_err(v, ref_v) <= TOL["bf16"], rel_err(v, ref_v)
     for b in range(B):
         check_kept(kept[b], ref_v[b], 30, "bf16")
+
+
+# ------------------------------- visual heads on the model's softmax domain --
+
+def _lse_of_other_keys(q, n_other, seed, scale=1.5):
+    """log-sum-exp (float32) of each row's scaled logits over n_other
+    synthetic non-visual keys (system + preceding text)."""
+    rng = np.random.default_rng(seed)
+    B, H, Nt, hd = q.shape
+    ko = rng.standard_normal((B, H, n_other, hd)) * scale
+    lg = np.matmul(q.astype(np.float64), np.swapaxes(ko, -1, -2)) / np.sqrt(hd)
+    mx = lg.max(-1, keepdims=True)
+    return (mx[..., 0] + np.log(np.exp(lg - mx).sum(-1))).astype(np.float32)
+
+
+def run_vis_ex(q_np, k_np, lse_np, dtype, n_vis, mask_np=None):
+    from paper_2608_25332_amd import provip
+    lse = torch.from_numpy(np.ascontiguousarray(lse_np, np.float32)).to("cuda:0")
+    mask = None if mask_np is None else torch.from_numpy(np.ascontiguousarray(mask_np, np.int32)).to("cuda:0")
+    r = provip.pv_visual_heads(to_dev(q_np, dtype), to_dev(k_np, dtype), n_vis, row_lse=lse,
+                               row_mask=mask)
+    torch.cuda.synchronize()
+    return to_host(r["heads"]), to_host(r["conf"])
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 4, 5])
+def test_visual_heads_in_model_parity(wid):
+    """C^h on the visual slice of the model's softmax, against the oracle:
+    the non-visual keys (35 synthetic system/text keys per row) enter through
+    one log-sum-exp per row."""
+    w = workload(wid)
+    dt = w.dtype
+    n_vis = min(N_VIS, w.spec.H - 1)
+    _say(f"[visual-heads-in-model] workload {wid} n_vis={n_vis}")
+    k1 = _subset_keys(w, w.N1, 700 + wid)
+    lse = _lse_of_other_keys(w.q, 35, 800 + wid, scale=0.05 if wid > 1 else 1.5)
+    heads, conf = run_vis_ex(w.q, k1, lse, dt, n_vis)
+    ref_heads, ref_conf = oracle.visual_heads_in_model(w.q, k1, lse.astype(np.float64), n_vis)
+    assert rel_err(conf, ref_conf) <= TOL[dt], rel_err(conf, ref_conf)
+    check_heads(heads, ref_conf, n_vis, dt)
+
+
+VIS_EX_EDGE = [
+    # (B, H, Nt, N, hd, n_vis, dtype, lse offset): offset shifts every lse
+    (1, 1, 1, 1, 32, 1, "f32", 0.0),
+    (2, 8, 17, 70, 64, 3, "bf16", 0.0),      # ragged rows and keys
+    (3, 16, 33, 200, 128, 5, "bf16", 2.0),   # the other keys hold most of each row
+    (1, 4, 16, 300, 256, 2, "f32", -3.0),    # widest head, small non-visual share
+    (2, 5, 40, 1500, 96, 2, "f32", 0.0),     # many chunks of keys
+    (1, 6, 20, 100, 64, 2, "f32", 200.0),    # visual mass ~ e^-200: underflows to 0
+]
+
+
+@pytest.mark.parametrize("B,H,Nt,N,hd,n_vis,dt,off", VIS_EX_EDGE)
+def test_visual_heads_in_model_edges(B, H, Nt, N, hd, n_vis, dt, off):
+    _say(f"[visual-heads-in-model-edge] B={B} H={H} Nt={Nt} N={N} hd={hd} n_vis={n_vis} {dt} {off}")
+    rng = np.random.default_rng(B * 300 + N)
+    q = (rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32)
+    k = (rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32)
+    if dt == "bf16":
+        q, k = W.bf16_round(q), W.bf16_round(k)
+    lse = _lse_of_other_keys(q, 20, B * 7 + N) + np.float32(off)
+    heads, conf = run_vis_ex(q, k, lse, dt, n_vis)
+    ref_heads, ref_conf = oracle.visual_heads_in_model(q, k, lse.astype(np.float64), n_vis)
+    if off >= 100.0:
+        # every visual slice is below the smallest float: C is 0 on the GPU
+        assert np.max(np.abs(conf)) == 0.0 and np.max(np.abs(ref_conf)) < 1e-80
+        return
+    assert rel_err(conf, ref_conf) <= TOL[dt], rel_err(conf, ref_conf)
+    check_heads(heads, ref_conf, n_vis, dt)
+
+
+def test_visual_heads_in_model_plain_cases():
+    """row_lse of -inf everywhere gives the plain call's bits; a head that
+    is peaked on its visual keys but gives them almost none of its row's
+    mass drops out of the visual heads on the model's domain."""
+    rng = np.random.default_rng(17)
+    B, H, Nt, N, hd = 2, 8, 24, 150, 64
+    q = W.bf16_round((rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32))
+    k = W.bf16_round((rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32))
+    h_plain, c_plain = run_vis(q, k, "bf16", 3)
+    h_inf, c_inf = run_vis_ex(q, k, np.full((B, H, Nt), -np.inf, np.float32), "bf16", 3)
+    assert np.array_equal(h_plain, h_inf) and np.array_equal(c_plain, c_inf)
+    # the top head of sample 0 loses its rows to the other keys (mass ~ e^-12)
+    top = int(np.argmax(c_plain[0]))
+    lse = _lse_of_other_keys(q, 10, 5)
+    lse[0, top] += 12.0
+    h_m, c_m = run_vis_ex(q, k, lse, "bf16", 3)
+    ref_h, ref_c = oracle.visual_heads_in_model(q, k, lse.astype(np.float64), 3)
+    assert rel_err(c_m, ref_c) <= TOL["bf16"]
+    check_heads(h_m, ref_c, 3, "bf16")
+    assert top not in h_m[0].tolist()
+
+
+def test_visual_heads_in_model_masked():
+    """row_mask and row_lse together: the oracle run on the masked rows only."""
+    rng = np.random.default_rng(19)
+    B, H, Nt, N, hd = 3, 8, 40, 120, 128
+    q = W.bf16_round((rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32))
+    k = W.bf16_round((rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32))
+    lse = _lse_of_other_keys(q, 15, 6)
+    mask = (rng.random((B, Nt)) < 0.4).astype(np.int32)
+    mask[2] = 0  # an empty mask means every row
+    heads, conf = run_vis_ex(q, k, lse, "bf16", 4, mask_np=mask)
+    for b in range(B):
+        rows = np.nonzero(mask[b])[0] if mask[b].any() else np.arange(Nt)
+        rh, rc = oracle.visual_heads_in_model(q[b:b + 1][:, :, rows], k[b:b + 1],
+                                              lse[b:b + 1][:, :, rows].astype(np.float64), 4)
+        assert rel_err(conf[b:b + 1], rc) <= TOL["bf16"]
+        check_heads(heads[b:b + 1], rc, 4, "bf16")
