@@ -659,6 +659,37 @@ def critical_text_timing(torch, step):
     return {"call_us": call_us, "kernels_us": {k: float(np.median(v)) for k, v in per.items()}}
 
 
+def progressive_timing(torch, w, dev):
+    """The progressive schedule (pv_prune_progressive: critical text ->
+    pruning before the LLM on the critical rows -> visual heads and
+    head-aware pruning at the shallow layer -> all-head pruning at the middle
+    layer) at the workload's shape, with a second seeded projection standing
+    in for the middle layer: the call from graph replays, and visual tokens
+    per second over it."""
+    from paper_2608_25332_amd import provip as pv
+    from paper_2608_25332_amd import workloads as W
+
+    q_m, k_m = W.make_middle_layer(w)
+    N1, n_vis, N2, N3 = W.progressive_budgets(w.spec)
+
+    def dev_t(a):
+        if w.dtype == "bf16":
+            return torch.from_numpy(W.bf16_bits(a).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+    ins = [dev_t(a) for a in (w.anchors, w.vis, w.q, w.k_full, q_m, k_m)]
+    o = pv.pv_prune_progressive(*ins, N1, n_vis, N2, N3)
+    ws = o.pop("workspace")
+    call = lambda: pv.pv_prune_progressive(*ins, N1, n_vis, N2, N3, out=o, workspace=ws)
+    us = graph_time_us(torch, call, reps=300)
+    s = w.spec
+    return {"call_us": us, "value": s.B * s.Nv / (us * 1e-6), "unit": "visual tokens/s",
+            "budgets": {"N1": N1, "n_vis": n_vis, "N2": N2, "N3": N3},
+            "note": "critical text, masked dedup with merge, visual heads + head-aware at a "
+                    "shallow layer, all-head pruning at a middle layer (synthetic per-layer "
+                    "Q/K), compactions between; one HIP graph"}
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -909,13 +940,15 @@ def measure_other(torch, wid, dev, args):
         if not torch.equal(ref[k], snap[k]):
             raise RuntimeError(f"benchmark output drifted in {k} ({w.spec.name})")
     rf, kernels, stages, shared, stage_us = rooflines(w, step.form, kern_us, shared_us)
+    prog = progressive_timing(torch, w, dev)
     out = {"config": config_of(w, step.form, step.form == "two_streams", graph),
            "steps": steps, "ms_per_step": ms, "value": w.spec.B * w.spec.Nv / (ms * 1e-3),
            "unit": "visual tokens/s", "stream_choice_us": mode_us or None,
            "latency_us": {"kernels": kern_us, "kernels_shared_launches": shared_us or None,
                           "stages": stage_us},
            "roofline": rf, "roofline_kernels": kernels, "roofline_stages": stages,
-           "roofline_kernels_shared_launches": shared or None, "csrc_digest": csrc_digest()}
+           "roofline_kernels_shared_launches": shared or None, "progressive": prog,
+           "csrc_digest": csrc_digest()}
     del graph, step
     torch.cuda.synchronize()
     if args.cpu_seconds > 0:
@@ -993,6 +1026,7 @@ def main():
         breakdown["step_" + f] = graph_time_us(torch, other)
     vis_heads = visual_heads_timing(torch, step)
     crit_text = critical_text_timing(torch, step)
+    prog = progressive_timing(torch, w, dev)
     step.run()
     torch.cuda.synchronize()
     # the outputs after all of the above still match the first eager step
@@ -1033,6 +1067,8 @@ def main():
         # critical text selection over the same text rows
         "visual_heads": vis_heads,
         "critical_text": crit_text,
+        # the method's whole progressive schedule in one call
+        "progressive": prog,
         "csrc_digest": csrc_digest(),
     }
     if args.cpu_seconds > 0:

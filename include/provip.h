@@ -473,6 +473,50 @@ int pv_prune_pipeline_separate(const void *vis, const void *anchors, const void 
                                size_t workspace_bytes, void *stream);
 
 /* -------------------------------------------------------------------------
+ * The progressive schedule of the method in one call (Sec. 4 Overview and
+ * Sec. 4.2-4.4): the sequential stages, each the library's call for it, so
+ * every output is the bit-for-bit result of those calls made in turn.
+ *   1. critical text tokens of `text` (pv_critical_text) -> text_mask;
+ *   2. pruning before the LLM on the critical rows (pv_prune_dedup_masked
+ *      with the merge) -> kept1 [B][budget1], assign [B][Nv],
+ *      merged [B][budget1][d];
+ *   3. shallow pruning layer: the keys of the budget1 retained tokens are
+ *      gathered from k_s_all; visual heads over the critical rows
+ *      (pv_visual_heads_masked, n_vis of them) -> vis_heads [B][n_vis],
+ *      conf [B][H]; head-aware pruning on those heads over every text row
+ *      (pv_prune_head_aware_dev) -> score2 [B][budget1]; the budget2
+ *      survivors' token indices -> kept2 [B][budget2] and their merged rows
+ *      -> hidden2 [B][budget2][d];
+ *   4. middle pruning layer: the keys of the budget2 survivors are gathered
+ *      from k_m_all; head-aware pruning over every head (the all-head
+ *      aggregation, no head identification) -> score3 [B][budget2]; the
+ *      budget3 survivors' token indices -> kept3 [B][budget3] and rows
+ *      -> hidden3 [B][budget3][d].
+ * text    [B][Nt][d]      dtype  text embeddings (critical-text selection and
+ *                                the anchors of stage 2)
+ * vis     [B][Nv][d]      dtype  visual embeddings
+ * q_s     [B][H][Nt][hd]  dtype  text-query rows at the shallow layer
+ * k_s_all [B][H][Nv][hd]  dtype  shallow-layer keys of every visual token
+ * q_m, k_m_all            the same at the middle layer
+ * kept1, kept2, kept3     original token indices, ascending
+ * conf, score2, score3 may be NULL; every other pointer is required.  All
+ * pointers are DEVICE memory, contiguous and 16-byte aligned.
+ * Sizes: those of the calls above; 1 <= n_vis <= H,
+ * 1 <= budget3 <= budget2 <= budget1 <= Nv (else PV_ERR_HEADS /
+ * PV_ERR_BUDGET).  workspace: pv_progressive_workspace_bytes.
+ * ---------------------------------------------------------------------- */
+size_t pv_progressive_workspace_bytes(int B, int Nv, int Nt, int d, int H, int hd, int budget1,
+                                      int n_vis, int budget2, int budget3, int dtype);
+
+int pv_prune_progressive(const void *text, const void *vis, const void *q_s, const void *k_s_all,
+                         const void *q_m, const void *k_m_all, int B, int Nv, int Nt, int d,
+                         int H, int hd, int dtype, int budget1, int n_vis, int budget2,
+                         int budget3, int32_t *text_mask, int32_t *kept1, int32_t *assign,
+                         void *merged, int32_t *vis_heads, float *conf, int32_t *kept2,
+                         float *score2, void *hidden2, int32_t *kept3, float *score3,
+                         void *hidden3, void *workspace, size_t workspace_bytes, void *stream);
+
+/* -------------------------------------------------------------------------
  * pv_prune_pipeline without a workspace argument, for callers that cannot
  * allocate device memory: code under HIP graph capture, tight serving loops
  * and harnesses that forbid hipMalloc.  Same arguments (minus workspace and

@@ -7,6 +7,7 @@
 #include <string.h>
 
 #include <mutex>
+#include <vector>
 
 #include "pv_jobs.h"
 #include "pv_launch.h"
@@ -1001,6 +1002,158 @@ PV_API int pv_prune_pipeline_timed(const void *vis, const void *anchors, const v
                          dtype, budget1, budget2, kept1, score1, assign, merged, k1, v1, kept2,
                          score2, hidden2, k2, v2, workspace, workspace_bytes, stream, 0, events,
                          n_events, reps, n_kernels, names);
+}
+
+// ---------------------------------------------------------------------------
+// The progressive schedule in one call: critical text, pruning before the
+// LLM on the critical rows, visual heads and head-aware pruning at a shallow
+// layer, all-head pruning at a middle layer, with the compactions between.
+// Every stage is the library's own call for that stage, so every output is
+// the bit-for-bit result of those calls made in turn.
+// ---------------------------------------------------------------------------
+namespace {
+
+struct ProgPlan {
+    size_t text, dedup, vh, head_b, head_c;
+    int32_t *count, *k2loc, *k3loc;
+    char *ks, *km;
+    char *ws_text, *ws_dedup, *ws_vh, *ws_head_b, *ws_head_c;
+    size_t bytes;
+};
+
+ProgPlan plan_prog(void *ws, int B, int Nv, int Nt, int d, int H, int hd, int esz, int N1,
+                   int n_vis, int N2, int N3, bool want_s2, bool want_s3) {
+    ProgPlan P;
+    P.text = plan_text(nullptr, B, Nt, d, esz).bytes;
+    P.dedup = plan_dedup(nullptr, B, Nv, Nt, d, esz, N1, true, false, true).bytes;
+    P.vh = vis_heads_bytes(B, H, Nt);
+    P.head_b = plan_head(nullptr, B, Nt, N1, n_vis, !want_s2).bytes;
+    P.head_c = plan_head(nullptr, B, Nt, N2, H, !want_s3).bytes;
+    Carve c(ws);
+    P.ws_text = c.take<char>(P.text);
+    P.ws_dedup = c.take<char>(P.dedup);
+    P.ws_vh = c.take<char>(P.vh);
+    P.ws_head_b = c.take<char>(P.head_b);
+    P.ws_head_c = c.take<char>(P.head_c);
+    P.count = c.take<int32_t>((size_t)B);
+    P.k2loc = c.take<int32_t>((size_t)B * N2);
+    P.k3loc = c.take<int32_t>((size_t)B * N3);
+    P.ks = c.take<char>((size_t)B * H * N1 * hd * esz);
+    P.km = c.take<char>((size_t)B * H * N2 * hd * esz);
+    P.bytes = c.off + kAlign;
+    return P;
+}
+
+int progressive_impl(const void *text, const void *vis, const void *q_s, const void *k_s_all,
+                     const void *q_m, const void *k_m_all, int B, int Nv, int Nt, int d, int H,
+                     int hd, int dtype, int N1, int n_vis, int N2, int N3, int32_t *text_mask,
+                     int32_t *kept1, int32_t *assign, void *merged, int32_t *vis_heads,
+                     float *conf, int32_t *kept2, float *score2, void *hidden2, int32_t *kept3,
+                     float *score3, void *hidden3, void *workspace, size_t ws_bytes,
+                     void *stream) {
+    int rc = check_dedup(vis, text, B, Nv, Nt, d, dtype, N1, kept1);
+    if (rc != PV_OK) return rc;
+    if ((rc = check_qk(q_s, k_s_all, B, H, Nt, Nv, hd, dtype)) != PV_OK) return rc;
+    if ((rc = check_qk(q_m, k_m_all, B, H, Nt, Nv, hd, dtype)) != PV_OK) return rc;
+    if (!text_mask || !assign || !merged || !vis_heads || !kept2 || !hidden2 || !kept3 ||
+        !hidden3)
+        return PV_ERR_NULL;
+    if (H > PV_MAX_HEADS || n_vis < 1 || n_vis > H) return PV_ERR_HEADS;
+    if (N2 < 1 || N2 > N1 || N3 < 1 || N3 > N2) return PV_ERR_BUDGET;
+    const void *const ptrs[] = {text_mask, kept1, assign, merged, vis_heads, conf, kept2,
+                                score2, hidden2, kept3, score3, hidden3, workspace};
+    for (const void *p : ptrs)
+        if (p && !aligned16(p)) return PV_ERR_ALIGN;
+    const int esz = (dtype == PV_BF16) ? 2 : 4;
+    if (!workspace ||
+        ws_bytes < plan_prog(nullptr, B, Nv, Nt, d, H, hd, esz, N1, n_vis, N2, N3, score2 != nullptr,
+                             score3 != nullptr).bytes)
+        return PV_ERR_WORKSPACE;
+    char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
+    const ProgPlan P = plan_prog(wsa, B, Nv, Nt, d, H, hd, esz, N1, n_vis, N2, N3,
+                                 score2 != nullptr, score3 != nullptr);
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t row_kv = (int64_t)hd * esz, row_h = (int64_t)d * esz;
+    // critical text tokens (Sec. 4.2)
+    rc = text_impl(text, B, Nt, d, dtype, text_mask, P.count, nullptr, P.ws_text, P.text, stream,
+                   nullptr, 0, 1, nullptr, nullptr);
+    if (rc != PV_OK) return rc;
+    // pruning before the LLM on the critical rows (Sec. 4.3), with the merge
+    rc = dedup_impl(vis, text, B, Nv, Nt, d, dtype, N1, kept1, nullptr, assign, merged,
+                    P.ws_dedup, P.dedup, stream, nullptr, 0, 1, nullptr, nullptr, nullptr,
+                    text_mask);
+    if (rc != PV_OK) return rc;
+    // the shallow layer's keys of the N1 retained tokens
+    pv::GatherArgs ga;
+    {
+        const pv_gather_desc g = kv_desc(k_s_all, P.ks, H, Nv, N1, row_kv);
+        if ((rc = make_gather(&g, 1, kept1, B, N1, ga)) != PV_OK) return rc;
+        if (pv::launch_gather(ga, kept1, B, N1, st) != hipSuccess) return PV_ERR_HIP;
+    }
+    // visual heads over the critical rows, then head-aware pruning on them
+    // (Sec. 4.4, equations for C^h, V_l, S^vis and v)
+    rc = vis_heads_impl(q_s, P.ks, B, H, Nt, N1, hd, dtype, n_vis, vis_heads, conf, P.ws_vh,
+                        P.vh, stream, nullptr, 0, 1, nullptr, nullptr, text_mask);
+    if (rc != PV_OK) return rc;
+    rc = head_impl(q_s, P.ks, nullptr, vis_heads, n_vis, B, H, Nt, N1, hd, dtype, N2, P.k2loc,
+                   score2, P.ws_head_b, P.head_b, stream, nullptr, 0, 1, nullptr, nullptr);
+    if (rc != PV_OK) return rc;
+    // survivors of the shallow layer: token indices, merged rows, and the
+    // middle layer's keys of those tokens
+    if (pv::launch_compose_index(kept1, P.k2loc, B, N1, N2, kept2, st) != hipSuccess)
+        return PV_ERR_HIP;
+    {
+        const pv_gather_desc g = kv_desc(merged, hidden2, 1, N1, N2, row_h);
+        if ((rc = make_gather(&g, 1, P.k2loc, B, N2, ga)) != PV_OK) return rc;
+        if (pv::launch_gather(ga, P.k2loc, B, N2, st) != hipSuccess) return PV_ERR_HIP;
+        const pv_gather_desc gk = kv_desc(k_m_all, P.km, H, Nv, N2, row_kv);
+        if ((rc = make_gather(&gk, 1, kept2, B, N2, ga)) != PV_OK) return rc;
+        if (pv::launch_gather(ga, kept2, B, N2, st) != hipSuccess) return PV_ERR_HIP;
+    }
+    // the middle layer: every head (the all-head aggregation, no head
+    // identification)
+    std::vector<int32_t> all((size_t)B * H);
+    for (int b = 0; b < B; ++b)
+        for (int h = 0; h < H; ++h) all[(size_t)b * H + h] = h;
+    rc = head_impl(q_m, P.km, all.data(), nullptr, H, B, H, Nt, N2, hd, dtype, N3, P.k3loc,
+                   score3, P.ws_head_c, P.head_c, stream, nullptr, 0, 1, nullptr, nullptr);
+    if (rc != PV_OK) return rc;
+    if (pv::launch_compose_index(kept2, P.k3loc, B, N2, N3, kept3, st) != hipSuccess)
+        return PV_ERR_HIP;
+    {
+        const pv_gather_desc g = kv_desc(hidden2, hidden3, 1, N2, N3, row_h);
+        if ((rc = make_gather(&g, 1, P.k3loc, B, N3, ga)) != PV_OK) return rc;
+        if (pv::launch_gather(ga, P.k3loc, B, N3, st) != hipSuccess) return PV_ERR_HIP;
+    }
+    return PV_OK;
+}
+
+}  // namespace
+
+PV_API size_t pv_progressive_workspace_bytes(int B, int Nv, int Nt, int d, int H, int hd,
+                                             int budget1, int n_vis, int budget2, int budget3,
+                                             int dtype) {
+    if (B < 1 || Nv < 1 || Nt < 1 || d < 1 || H < 1 || hd < 1 || budget1 < 1 || budget1 > Nv ||
+        n_vis < 1 || n_vis > H || budget2 < 1 || budget2 > budget1 || budget3 < 1 ||
+        budget3 > budget2 || (dtype != PV_F32 && dtype != PV_BF16))
+        return 0;
+    return plan_prog(nullptr, B, Nv, Nt, d, H, hd, dtype == PV_BF16 ? 2 : 4, budget1, n_vis,
+                     budget2, budget3, false, false)
+        .bytes;
+}
+
+PV_API int pv_prune_progressive(const void *text, const void *vis, const void *q_s,
+                                const void *k_s_all, const void *q_m, const void *k_m_all, int B,
+                                int Nv, int Nt, int d, int H, int hd, int dtype, int budget1,
+                                int n_vis, int budget2, int budget3, int32_t *text_mask,
+                                int32_t *kept1, int32_t *assign, void *merged,
+                                int32_t *vis_heads, float *conf, int32_t *kept2, float *score2,
+                                void *hidden2, int32_t *kept3, float *score3, void *hidden3,
+                                void *workspace, size_t workspace_bytes, void *stream) {
+    return progressive_impl(text, vis, q_s, k_s_all, q_m, k_m_all, B, Nv, Nt, d, H, hd, dtype,
+                            budget1, n_vis, budget2, budget3, text_mask, kept1, assign, merged,
+                            vis_heads, conf, kept2, score2, hidden2, kept3, score3, hidden3,
+                            workspace, workspace_bytes, stream);
 }
 
 // ---------------------------------------------------------------------------

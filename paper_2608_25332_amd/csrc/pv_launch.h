@@ -141,5 +141,8 @@ struct GatherArgs {
     int n;
 };
 hipError_t launch_gather(const GatherArgs &ga, const int32_t *idx, int B, int k, hipStream_t st);
+// out[b][r] = base[b][idx[b][r]] (b < B, r < k; idx clamped into [0, n_base)).
+hipError_t launch_compose_index(const int32_t *base, const int32_t *idx, int B, int n_base, int k,
+                                int32_t *out, hipStream_t st);
 
 }  // namespace pv

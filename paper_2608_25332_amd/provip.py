@@ -145,6 +145,10 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_pipeline_separate.restype = _i
     lib.pv_prune_pipeline_timed.argtypes = pipe + timed_tail
     lib.pv_prune_pipeline_timed.restype = _i
+    lib.pv_progressive_workspace_bytes.argtypes = [_i] * 11
+    lib.pv_progressive_workspace_bytes.restype = _sz
+    lib.pv_prune_progressive.argtypes = [_vp] * 6 + [_i] * 11 + [_vp] * 12 + [_vp, _sz, _vp]
+    lib.pv_prune_progressive.restype = _i
     lib.pv_prune_pipeline_noalloc.argtypes = [_vp] * 6 + [_i] * 10 + [_vp] * 11 + [_vp]
     lib.pv_prune_pipeline_noalloc.restype = _i
     _lib = lib
@@ -662,3 +666,57 @@ def pv_prune_pipeline_noalloc(vis: torch.Tensor, anchors: torch.Tensor, q: torch
         budget1, budget2, *[out[n].data_ptr() for n in PIPELINE_OUTPUTS], _stream(vis.device))
     _check("pv_prune_pipeline_noalloc", rc, lib)
     return out
+
+
+PROGRESSIVE_OUTPUTS = ("text_mask", "kept1", "assign", "merged", "vis_heads", "conf", "kept2",
+                       "score2", "hidden2", "kept3", "score3", "hidden3")
+
+
+def pv_prune_progressive(text: torch.Tensor, vis: torch.Tensor, q_s: torch.Tensor,
+                         k_s_all: torch.Tensor, q_m: torch.Tensor, k_m_all: torch.Tensor,
+                         budget1: int, n_vis: int, budget2: int, budget3: int, *,
+                         out: Optional[dict] = None, workspace: Optional[torch.Tensor] = None):
+    """The progressive schedule in one call (pv_prune_progressive): critical
+    text, pruning before the LLM on the critical rows, visual heads and
+    head-aware pruning at the shallow layer (q_s, k_s_all), all-head pruning
+    at the middle layer (q_m, k_m_all).  text [B,Nt,d], vis [B,Nv,d], q_*
+    [B,H,Nt,hd], k_*_all [B,H,Nv,hd] (one dtype).  Returns a dict with
+    PROGRESSIVE_OUTPUTS (shapes in include/provip.h)."""
+    lib = load()
+    for t, n in ((text, "text"), (vis, "vis"), (q_s, "q_s"), (k_s_all, "k_s_all"), (q_m, "q_m"),
+                 (k_m_all, "k_m_all")):
+        _contig(t, n)
+    B, Nv, d = vis.shape
+    _, H, Nt, hd = q_s.shape
+    if (tuple(text.shape) != (B, Nt, d) or tuple(k_s_all.shape) != (B, H, Nv, hd)
+            or tuple(q_m.shape) != (B, H, Nt, hd) or tuple(k_m_all.shape) != (B, H, Nv, hd)
+            or len({t.dtype for t in (text, vis, q_s, k_s_all, q_m, k_m_all)}) != 1):
+        raise ValueError("text [B,Nt,d], q_* [B,H,Nt,hd], k_*_all [B,H,Nv,hd], one dtype")
+    code = _dtype_code(vis)
+    dev, dt = vis.device, vis.dtype
+    i32, f32 = torch.int32, torch.float32
+    shapes = {"text_mask": ((B, Nt), i32), "kept1": ((B, budget1), i32),
+              "assign": ((B, Nv), i32), "merged": ((B, budget1, d), dt),
+              "vis_heads": ((B, n_vis), i32), "conf": ((B, H), f32),
+              "kept2": ((B, budget2), i32), "score2": ((B, budget1), f32),
+              "hidden2": ((B, budget2, d), dt), "kept3": ((B, budget3), i32),
+              "score3": ((B, budget2), f32), "hidden3": ((B, budget3, d), dt)}
+    o = dict(out) if out is not None else {}
+    for name in PROGRESSIVE_OUTPUTS:
+        if o.get(name) is None:
+            shp, ty = shapes[name]
+            o[name] = torch.empty(shp, dtype=ty, device=dev)
+        else:
+            _contig(o[name], name)
+    nbytes = lib.pv_progressive_workspace_bytes(B, Nv, Nt, d, H, hd, budget1, n_vis, budget2,
+                                                budget3, code)
+    if workspace is None or workspace.numel() < nbytes:
+        workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+    rc = lib.pv_prune_progressive(
+        text.data_ptr(), vis.data_ptr(), q_s.data_ptr(), k_s_all.data_ptr(), q_m.data_ptr(),
+        k_m_all.data_ptr(), B, Nv, Nt, d, H, hd, code, budget1, n_vis, budget2, budget3,
+        *[o[n].data_ptr() for n in PROGRESSIVE_OUTPUTS], workspace.data_ptr(),
+        workspace.numel(), _stream(dev))
+    _check("pv_prune_progressive", rc, lib)
+    o["workspace"] = workspace
+    return o

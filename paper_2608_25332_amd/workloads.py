@@ -297,3 +297,33 @@ def make_workload(wid: int, seed: Optional[int] = None, *, B: Optional[int] = No
     heads = heads.astype(np.int32)
     return Workload(spec, vis, anchors, q, k_full, v_full, heads, spec.N1, spec.N2, spec.dtype,
                     dup_pairs=dup_pairs, followers=followers)
+
+
+def make_middle_layer(w: Workload, seed: Optional[int] = None):
+    """Text-query rows and keys of every visual token at a second, deeper
+    pruning layer, for the progressive schedule: the first layer's recipe
+    with projections of their own (seeded by `seed`, default 1000 + the
+    workload number).  Returns (q_m [B,H,Nt,hd], k_m_all [B,H,Nv,hd]) in the
+    workload's storage values (bf16 values widened to float32, or float32)."""
+    s = w.spec
+    seed = 1000 + s.wid if seed is None else int(seed)
+    rng_q, rng_k = _rng_streams(seed, 2)
+    Bn, Nv, d, H, hd, Nt = s.B, s.Nv, s.d, s.H, s.hd, s.Nt
+    if w.dtype == "f32":
+        q = rng_q.standard_normal((Bn, H, Nt, hd)).astype(np.float32)
+        k = rng_k.standard_normal((Bn, H, Nv, hd)).astype(np.float32)
+        return q, k
+    scale = np.float32(1.0 / math.sqrt(d))
+    wq = rng_q.standard_normal((d, H * hd), dtype=np.float32) * scale
+    q = bf16_round(np.stack([_project_heads(w.anchors[b], wq, H, hd) for b in range(Bn)], 0))
+    del wq
+    wk = rng_k.standard_normal((d, H * hd), dtype=np.float32) * scale
+    k = bf16_round(np.stack([_project_heads(w.vis[b], wk, H, hd) for b in range(Bn)], 0))
+    return q, k
+
+
+def progressive_budgets(spec: Spec):
+    """Budgets of the progressive schedule for a workload: N1 and N2 of the
+    workload, N3 = N2 / 2 at the middle layer, and N_vis = 6 visual heads
+    (the paper's setting; half the heads where there are fewer than 12)."""
+    return spec.N1, min(6, spec.H // 2), spec.N2, max(1, spec.N2 // 2)

@@ -384,3 +384,31 @@ def test_pipeline_noalloc_rejects_on_the_host(lib):
     assert lib.pv_pipeline_workspace_bytes(2, 4608, 128, 5120, 40, 128, 5, 1152, 512, 1) <= \
         provip.PV_STATIC_SCRATCH_BYTES
     assert b"scratch" in lib.pv_status_string(-9)
+
+
+def _prog(lib, B=1, Nv=64, Nt=16, d=256, H=4, hd=64, dt=1, b1=32, nv=2, b2=16, b3=8, null_at=None,
+          ws=FAKE, wsb=1 << 40):
+    ptrs = [FAKE] * 18  # six inputs, then the twelve outputs
+    if null_at is not None:
+        ptrs[null_at] = None
+    return lib.pv_prune_progressive(*ptrs[:6], B, Nv, Nt, d, H, hd, dt, b1, nv, b2, b3,
+                                    *ptrs[6:], ws, wsb, None)
+
+
+def test_progressive_validation(lib):
+    """The progressive schedule's host checks (nothing is enqueued)."""
+    assert _prog(lib, null_at=0) == -1          # text
+    assert _prog(lib, null_at=6) == -1          # text_mask
+    assert _prog(lib, null_at=17) == -1         # hidden3
+    assert _prog(lib, b1=65) == -3
+    assert _prog(lib, b2=33) == -3              # budget2 > budget1
+    assert _prog(lib, b3=17) == -3              # budget3 > budget2
+    assert _prog(lib, b3=0) == -3
+    assert _prog(lib, nv=5) == -4               # more visual heads than heads
+    assert _prog(lib, nv=0) == -4
+    assert _prog(lib, hd=48) == -2
+    assert _prog(lib, ws=None) == -6
+    assert _prog(lib, wsb=64) == -6
+    f = lib.pv_progressive_workspace_bytes
+    assert f(1, 576, 64, 4096, 32, 128, 192, 6, 64, 32, 1) > 0
+    assert f(1, 576, 64, 4096, 32, 128, 192, 6, 64, 65, 1) == 0
