@@ -306,6 +306,7 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
 struct HeadPlan {
     int nrb;
     float *partial;
+    float *stats;  // row statistics of the split score form
     float *v;
     size_t bytes;
 };
@@ -315,6 +316,7 @@ HeadPlan plan_head(void *ws, int B, int Nt, int N, int n_heads, bool want_v) {
     P.nrb = (Nt + 15) / 16;
     Carve c(ws);
     P.partial = c.take<float>((size_t)B * n_heads * P.nrb * N);
+    P.stats = c.take<float>(pv::score_split_stats_bytes(B, n_heads, Nt, N) / sizeof(float));
     P.v = want_v ? c.take<float>((size_t)B * N) : nullptr;
     P.bytes = c.off + kAlign;
     return P;
@@ -380,12 +382,12 @@ int head_impl(const void *q, const void *k, const int32_t *heads, const int32_t 
 
     if (!tr.launch("score_partial", [&] {
             return pv::launch_score_partial(dt, q, k, heads, heads_dev, row_lse, B, H, Nt, N, hd,
-                                            n_heads, P.partial, st);
+                                            n_heads, P.partial, P.stats, st);
         }))
         return PV_ERR_HIP;
     const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
     if (!tr.launch("score_select", [&] {
-            const int parts = pv::score_uses_head_form(dt, B, H, n_heads, Nt, N, hd) ? 1 : P.nrb;
+            const int parts = pv::score_parts(dt, B, H, n_heads, Nt, N, hd);
             return pv::launch_score_select(P.partial, B, n_heads * parts, N, inv_norm, v, budget,
                                            kept, st);
         }))
@@ -901,7 +903,8 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
     // the split-k Gram and the plain merge, and the score its 16-row blocks
     const bool carry = !force_separate && P.Mp > 0 && !P.gram_big && !P.lists && N1 <= 256 &&
                        pv::score_can_carry_reduce(dt, hd) &&
-                       !pv::score_uses_head_form(dt, B, H, n_heads, Nt, N1, hd);
+                       !pv::score_uses_head_form(dt, B, H, n_heads, Nt, N1, hd) &&
+                       !pv::score_uses_split_form(dt, B, H, n_heads, Nt, N1, hd);
     if (!carry) {
         rc = dedup_impl(vis, anchors, B, Nv, Nt, d, dtype, N1, kept1, score1, assign, merged, wsa,
                         sz.dedup, stream, nullptr, 0, 1, nullptr, nullptr);
@@ -934,7 +937,7 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
                            B * ((P.Mp + pv::kReduceRowsPerBlock - 1) / pv::kReduceRowsPerBlock)};
     if (!tr.launch("score_partial+gram_reduce", [&] {
             return pv::launch_score_partial(dt, q, k1, heads, nullptr, nullptr, B, H, Nt, N1, hd,
-                                            n_heads, Hh.partial, st, &rj);
+                                            n_heads, Hh.partial, Hh.stats, st, &rj);
         }))
         return PV_ERR_HIP;
     // merge + the score's top-N_2

@@ -675,6 +675,190 @@ __global__ __launch_bounds__(kScoreNT) void score_head_kernel(
         out[j] = ((colpart[0][j] + colpart[1][j]) + colpart[2][j]) + colpart[3][j];
 }
 
+// ----------------------------------------------------------------------------
+// score_split: long key lists on few (head, sample) pairs (the hi-res and 13B
+// shapes), where one workgroup per 16-row block would re-read each head's
+// keys once per block and leave most CUs idle.  A workgroup owns one
+// (64-key chunk, selected head, sample) and every text row, in XCD order so
+// that the chunks of one head share its query rows in one L2.
+//   score_split_stats: each row's maximum and sum of exponentials over the
+//       chunk's keys -> stats[b][hi][chunk][row] (max in scaled log2 units,
+//       sum relative to it);
+//   score_split_cols: every row's statistics merged over the chunks in chunk
+//       order (with the non-visual keys' log-sum-exp on the model's domain),
+//       the chunk's logits formed again, and the normalised probabilities
+//       summed over the rows -> partial[b][hi][key], the layout of the
+//       whole-head form.
+// Each pass reads the keys once; the attention map is never written.  The
+// chunk's keys go to LDS once; each wave takes 16 rows of a 64-row block at
+// a time, its query fragments loaded straight into registers.
+// ----------------------------------------------------------------------------
+constexpr int kSplitRowsPerPass = 64;  // rows of one pass of the four waves
+
+// The (chunk, head, sample) of this workgroup and the head it reads.
+struct SplitCoord {
+    int s, hi, b, h;
+};
+
+__device__ __forceinline__ SplitCoord split_coord(const HeadArgs &heads,
+                                                  const int32_t *__restrict__ heads_dev,
+                                                  int head_src, int b0, int H, int nsplit,
+                                                  int n_heads) {
+    SplitCoord c;
+    const int L = xcd_tile(blockIdx.x, gridDim.x);
+    c.s = L % nsplit;
+    c.hi = (L / nsplit) % n_heads;
+    const int bl = L / (nsplit * n_heads);
+    c.b = b0 + bl;
+    if (head_src == kHeadsDevice) c.h = min(max(heads_dev[(size_t)c.b * n_heads + c.hi], 0), H - 1);
+    else c.h = heads.h[bl * n_heads + c.hi];
+    return c;
+}
+
+// The chunk's (at most 64) keys into LDS (rows past N repeat the last key).
+template <int NKS>
+__device__ __forceinline__ void split_load_keys(const char *kb, int key0, int N, char *kbuf,
+                                                int wave, int lane) {
+    using S = ScoreStage<NKS>;
+#pragma unroll
+    for (int t = 0; t < S::IPW; ++t) {
+        const int pos = (wave * S::IPW + t) * 64 + lane;
+        const int r = pos / S::PPR, slot = pos % S::PPR;
+        const int row = min(key0 + r, N - 1);
+        lds_dma16(kb + (size_t)row * S::RB + ((slot ^ (r & S::SWZ)) << 4),
+                  kbuf + (wave * S::IPW + t) * 1024);
+    }
+    wait_vmcnt<0>();
+    bare_barrier();
+}
+
+// Logits of this wave's 16 rows starting at r0 against the chunk:
+// keep[0][kq] = rows 4 (lane / 16) + i x keys 16 kq + lane % 16.
+template <int DT, int NKS>
+__device__ __forceinline__ void split_logits(const char *qb, int r0, int Nt, const char *kbuf,
+                                             int lane, f32x4_t (&keep)[1][4]) {
+    using S = ScoreStage<NKS>;
+    uint4 qf[NKS];
+    const char *qrow = qb + (size_t)min(r0 + (lane & 15), Nt - 1) * S::RB;
+#pragma unroll
+    for (int s = 0; s < NKS; ++s) qf[s] = ld16(qrow + ((s * 4 + (lane >> 4)) << 4));
+    head_chunk_logits<DT, NKS>(kbuf, qf, lane, keep[0]);
+}
+
+template <int DT, int NKS>
+__global__ __launch_bounds__(kScoreNT) void score_split_stats_kernel(
+    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
+    const int32_t *__restrict__ heads_dev, int head_src, int b0, int H, int Nt, int N,
+    int n_heads, int nsplit, float scale_log2e, float2 *__restrict__ stats) {
+    using S = ScoreStage<NKS>;
+    __shared__ __attribute__((aligned(16))) char kbuf[S::STAGE];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const SplitCoord c = split_coord(heads, heads_dev, head_src, b0, H, nsplit, n_heads);
+    const char *qb = q + ((size_t)c.b * H + c.h) * Nt * S::RB;
+    const char *kb = k + ((size_t)c.b * H + c.h) * N * S::RB;
+    const int key0 = c.s * kScoreCK;
+    split_load_keys<NKS>(kb, key0, N, kbuf, wave, lane);
+    float2 *out = stats + (((size_t)c.b * n_heads + c.hi) * nsplit + c.s) * Nt;
+    for (int r0 = wave * 16; r0 < Nt; r0 += kSplitRowsPerPass) {  // uniform per wave
+        f32x4_t keep[1][4];
+        split_logits<DT, NKS>(qb, r0, Nt, kbuf, lane, keep);
+        float m[4], l[4] = {0.f, 0.f, 0.f, 0.f};
+        head_row_max<1>(keep, 1, N - key0, lane, scale_log2e, m);  // keys past N left out
+        head_row_exp<1>(keep, 1, scale_log2e, m, l);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) l[i] = row16_sum(l[i]);
+        if ((lane & 15) == 0) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int row = r0 + (lane >> 4) * 4 + i;
+                if (row < Nt) out[row] = make_float2(m[i], l[i]);
+            }
+        }
+    }
+}
+
+constexpr int kSplitStatU = 8;  // chunk statistics in flight per row
+
+template <int DT, int NKS>
+__global__ __launch_bounds__(kScoreNT) void score_split_cols_kernel(
+    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
+    const int32_t *__restrict__ heads_dev, int head_src, const float *__restrict__ row_lse,
+    int b0, int H, int Nt, int N, int n_heads, int nsplit, float scale_log2e,
+    const float2 *__restrict__ stats, float *__restrict__ partial) {
+    using S = ScoreStage<NKS>;
+    __shared__ __attribute__((aligned(16))) char kbuf[S::STAGE];
+    __shared__ float colpart[4][kScoreCK];
+    extern __shared__ float2 rowstat[];  // [Nt]: (row maximum, 1 / normaliser)
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const SplitCoord c = split_coord(heads, heads_dev, head_src, b0, H, nsplit, n_heads);
+    const char *qb = q + ((size_t)c.b * H + c.h) * Nt * S::RB;
+    const char *kb = k + ((size_t)c.b * H + c.h) * N * S::RB;
+    const int key0 = c.s * kScoreCK;
+    // the keys' loads first; the rows' statistics are merged while they fly
+    {
+#pragma unroll
+        for (int t = 0; t < S::IPW; ++t) {
+            const int pos = (wave * S::IPW + t) * 64 + lane;
+            const int r = pos / S::PPR, slot = pos % S::PPR;
+            const int row = min(key0 + r, N - 1);
+            lds_dma16(kb + (size_t)row * S::RB + ((slot ^ (r & S::SWZ)) << 4),
+                      kbuf + (wave * S::IPW + t) * 1024);
+        }
+    }
+    // every row's statistics over all chunks, merged in chunk order
+    const float2 *st = stats + ((size_t)c.b * n_heads + c.hi) * nsplit * Nt;
+    for (int row = tid; row < Nt; row += kScoreNT) {
+        float mm = -INFINITY, ll = 0.f;
+        for (int s0 = 0; s0 < nsplit; s0 += kSplitStatU) {
+            float2 v[kSplitStatU];
+#pragma unroll
+            for (int u = 0; u < kSplitStatU; ++u)
+                v[u] = st[(size_t)min(s0 + u, nsplit - 1) * Nt + row];
+#pragma unroll
+            for (int u = 0; u < kSplitStatU; ++u)
+                if (s0 + u < nsplit) lse_merge(mm, ll, v[u].x, v[u].y);
+        }
+        // the model's row also runs over the non-visual keys: their
+        // log-sum-exp (natural log, scaled logits) joins the normaliser
+        if (row_lse) lse_merge(mm, ll, row_lse[((size_t)c.b * H + c.h) * Nt + row] * 1.4426950408889634f, 1.f);
+        rowstat[row] = make_float2(mm, 1.0f / ll);
+    }
+    wait_vmcnt<0>();
+    __syncthreads();  // the keys and every row's statistics are in LDS
+    float cs[4] = {0.f, 0.f, 0.f, 0.f};
+    const int nkeys = N - key0;
+    for (int r0 = wave * 16; r0 < Nt; r0 += kSplitRowsPerPass) {  // uniform per wave
+        f32x4_t keep[1][4];
+        split_logits<DT, NKS>(qb, r0, Nt, kbuf, lane, keep);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = r0 + (lane >> 4) * 4 + i;
+            const float2 rs = rowstat[min(row, Nt - 1)];
+            const float il = row < Nt ? rs.y : 0.f;  // rows past Nt add nothing
+#pragma unroll
+            for (int kq = 0; kq < 4; ++kq) {
+                const bool col_ok = kq * 16 + (lane & 15) < nkeys;
+                const float e = exp2_hw(fmaf(keep[0][kq][i], scale_log2e, -rs.x));
+                cs[kq] += col_ok ? e * il : 0.f;
+            }
+        }
+    }
+    // this wave's column sums over its rows, then the four waves in order
+#pragma unroll
+    for (int kq = 0; kq < 4; ++kq) {
+        float v = cs[kq];
+        v += __shfl_xor(v, 16, 64);
+        v += __shfl_xor(v, 32, 64);
+        if (lane < 16) colpart[wave][kq * 16 + lane] = v;
+    }
+    __syncthreads();
+    if (tid < kScoreCK && tid < nkeys)
+        partial[((size_t)c.b * n_heads + c.hi) * N + key0 + tid] =
+            ((colpart[0][tid] + colpart[1][tid]) + colpart[2][tid]) + colpart[3][tid];
+}
+
 template <int NT, int EMAX>
 __global__ __launch_bounds__(NT) void score_select_kernel(SelectJob sj) {
     score_select_block<NT, EMAX>(sj, blockIdx.x);
@@ -814,6 +998,34 @@ static hipError_t score_head_go(const ScoreLaunch &a) {
     return hipSuccess;
 }
 
+// The split form: two launches per bounded head list, statistics then
+// column sums.
+template <int DT, int NKS>
+static hipError_t score_split_go(const ScoreLaunch &a, float2 *stats) {
+    const int nsplit = (a.N + kScoreCK - 1) / kScoreCK;
+    const int per_launch = a.src == kHeadsArg ? kMaxHeadArgs / a.n_heads : a.B;
+    HeadArgs ha;
+    for (int b0 = 0; b0 < a.B; b0 += per_launch) {
+        const int nb = a.B - b0 < per_launch ? a.B - b0 : per_launch;
+        for (int i = 0; i < kMaxHeadArgs; ++i)
+            ha.h[i] = (a.src == kHeadsArg && i < nb * a.n_heads)
+                          ? a.heads_host[(size_t)b0 * a.n_heads + i] : 0;
+        const dim3 grid(nsplit * a.n_heads * nb);
+        hipLaunchKernelGGL((score_split_stats_kernel<DT, NKS>), grid, dim3(kScoreNT), 0, a.st,
+                           (const char *)a.q, (const char *)a.k, ha, a.heads_dev, a.src, b0, a.H,
+                           a.Nt, a.N, a.n_heads, nsplit, a.sl2e, stats);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL((score_split_cols_kernel<DT, NKS>), grid, dim3(kScoreNT),
+                           (size_t)a.Nt * sizeof(float2), a.st, (const char *)a.q,
+                           (const char *)a.k, ha, a.heads_dev, a.src, a.row_lse, b0, a.H, a.Nt,
+                           a.N, a.n_heads, nsplit, a.sl2e, stats, a.partial);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 template <bool CONF>
 static hipError_t score_any(int dt, int hd, ScoreLaunch a) {
     const int esz = (dt == kBF16) ? 2 : 4;
@@ -832,6 +1044,22 @@ bool score_uses_head_form(int dt, int B, int H, int n_heads, int Nt, int N, int 
            N <= kHeadMaxChunks * kScoreCK && (long long)B * n_heads >= 128;
 }
 
+// The split form pays for long key lists when the 16-row blocks would not
+// give every CU a workgroup (one per 16 rows, selected head and sample).
+bool score_uses_split_form(int dt, int B, int H, int n_heads, int Nt, int N, int hd) {
+    const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
+    if (score_uses_head_form(dt, B, H, n_heads, Nt, N, hd)) return false;
+    return (nks == 2 || nks == 4) && N > 4 * kScoreCK &&
+           (long long)((Nt + 15) / 16) * n_heads * B < 256;
+}
+
+int score_parts(int dt, int B, int H, int n_heads, int Nt, int N, int hd) {
+    if (score_uses_head_form(dt, B, H, n_heads, Nt, N, hd) ||
+        score_uses_split_form(dt, B, H, n_heads, Nt, N, hd))
+        return 1;
+    return (Nt + 15) / 16;
+}
+
 bool score_can_carry_reduce(int dt, int hd) {
     return score_carries_reduce(hd * ((dt == kBF16) ? 2 : 4) / 64, false);
 }
@@ -839,12 +1067,20 @@ bool score_can_carry_reduce(int dt, int hd) {
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, const float *row_lse, int B, int H,
                                 int Nt, int N, int hd, int n_heads, float *partial,
-                                hipStream_t st, const ReduceJob *with) {
+                                float *split_stats, hipStream_t st, const ReduceJob *with) {
     ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg, nullptr,
                   row_lse, B, H, Nt, N, n_heads, 0.f, partial, st};
     a.rj = with;
     const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
     if (with && !score_carries_reduce(nks, false)) return hipErrorInvalidValue;
+    if (score_uses_split_form(dt, B, H, n_heads, Nt, N, hd)) {
+        if (with || !split_stats) return hipErrorInvalidValue;  // the split form carries nothing
+        a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
+        float2 *stats = reinterpret_cast<float2 *>(split_stats);
+        if (dt == kBF16)
+            return nks == 2 ? score_split_go<kBF16, 2>(a, stats) : score_split_go<kBF16, 4>(a, stats);
+        return nks == 2 ? score_split_go<kF32, 2>(a, stats) : score_split_go<kF32, 4>(a, stats);
+    }
     if (score_uses_head_form(dt, B, H, n_heads, Nt, N, hd)) {
         if (with) return hipErrorInvalidValue;  // the whole-head form carries nothing
         a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));

@@ -103,16 +103,30 @@ hipError_t launch_text_rank(const float *G, int B, int Nt, float *r, int32_t *ma
 // writes one row of column sums per (sample, head) instead of one per
 // 16-row block.
 bool score_uses_head_form(int dt, int B, int H, int n_heads, int Nt, int N, int hd);
+// Whether the score runs split over 64-key chunks of every head (two
+// launches: row statistics, then column sums; one row of column sums per
+// (sample, head)).
+bool score_uses_split_form(int dt, int B, int H, int n_heads, int Nt, int N, int hd);
+// Rows of column sums the score writes per (sample, selected head): 1 for the
+// whole-head and split forms, one per 16-row block otherwise.
+int score_parts(int dt, int B, int H, int n_heads, int Nt, int N, int hd);
+// Bytes of the split form's row statistics (float2 per row, chunk, head and
+// sample).
+inline size_t score_split_stats_bytes(int B, int n_heads, int Nt, int N) {
+    return (size_t)B * n_heads * ((N + 63) / 64) * Nt * 8;
+}
 // Whether the score launch can carry the split-k Gram's argmax (ReduceJob).
 bool score_can_carry_reduce(int dt, int hd);
 // row_lse [B][H][Nt] (may be NULL): log-sum-exp of each row's scaled logits
 // over the non-visual keys, which join the softmax normaliser.
 // with: the split-k Gram's argmax carried as extra workgroups of the first
 // launch (or NULL); not with the whole-head form.
+// split_stats: workspace of score_split_stats_bytes (used by the split form).
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, const float *row_lse, int B, int H,
                                 int Nt, int N, int hd, int n_heads, float *partial,
-                                hipStream_t st, const ReduceJob *with = nullptr);
+                                float *split_stats, hipStream_t st,
+                                const ReduceJob *with = nullptr);
 // Head confidence of every head, per 16-row block: partial[b][h][rb].
 // row_mask as for launch_center: the rows summed into the confidence.
 // row_lse as for launch_score_partial (may be NULL): the variance is then

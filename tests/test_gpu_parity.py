@@ -331,12 +331,33 @@ HEAD_EDGE = [
     (128, 2, 1, 1, 32, 1, 1, "f32"),          # one row, one key
     (130, 3, 50, 200, 64, 1, 20, "bf16"),
     (16, 32, 64, 192, 128, 32, 64, "bf16"),   # every head of the LLaVA-1.5 layer
+    # split over 64-key chunks (long key lists on few head-sample pairs)
+    (1, 4, 128, 960, 128, 4, 320, "bf16"),    # one hi-res sample
+    (2, 5, 128, 1152, 128, 5, 512, "bf16"),   # the 13B batch
+    (3, 4, 17, 300, 64, 2, 50, "f32"),        # last chunk of 44 keys, 256-byte fp32 rows
+    (1, 3, 1, 257, 64, 1, 10, "bf16"),        # one row; last chunk of one key
+    (2, 8, 200, 700, 128, 3, 99, "bf16"),     # four passes of 64 rows, ragged
+    # the 16-row blocks at long key lists (enough blocks to fill the chip)
+    (16, 4, 64, 1500, 128, 4, 200, "bf16"),   # 24 chunks of logits held in registers
+    (10, 2, 200, 2100, 128, 2, 600, "bf16"),  # keys streamed twice
 ]
+
+
+def score_form(B, H, Nt, N, hd, nh, dt):
+    """The score form the library picks (its rule, restated for the test
+    log): whole-head, split over key chunks, or 16-row blocks."""
+    nks = hd * (2 if dt == "bf16" else 4) // 64
+    if nks in (2, 4) and H <= 256 and Nt <= 64 and N <= 256 and B * nh >= 128:
+        return "whole-head"
+    if nks in (2, 4) and N > 256 and ((Nt + 15) // 16) * nh * B < 256:
+        return "split"
+    return "row-blocks"
 
 
 @pytest.mark.parametrize("B,H,Nt,N,hd,nh,budget,dt", HEAD_EDGE)
 def test_head_aware_edges(B, H, Nt, N, hd, nh, budget, dt):
-    _say(f"[head-edge] B={B} H={H} Nt={Nt} N={N} hd={hd} nh={nh} budget={budget} {dt}")
+    _say(f"[head-edge] B={B} H={H} Nt={Nt} N={N} hd={hd} nh={nh} budget={budget} {dt} "
+         f"({score_form(B, H, Nt, N, hd, nh, dt)})")
     rng = np.random.default_rng(B * 1000 + N)
     q = (rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32)
     k = (rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32)
@@ -517,3 +538,32 @@ def test_abi_errors_on_gpu():
     with pytest.raises(provip.ProvipError) as e:
         provip.pv_prune_head_aware(q, q, [[1, 1]], 4)
     assert e.value.status == -4
+
+
+
+@pytest.mark.parametrize("B,H,Nt,N,hd,nh", [(1, 4, 128, 960, 128, 4), (2, 6, 70, 1100, 64, 3)])
+def test_head_aware_split_form_in_model(B, H, Nt, N, hd, nh):
+    """The split score form on the model's softmax domain (row_lse merged
+    after the chunks' statistics) and with a device head list, against the
+    oracle."""
+    from paper_2608_25332_amd import provip
+    assert score_form(B, H, Nt, N, hd, nh, "bf16") == "split"
+    rng = np.random.default_rng(B * 13 + N)
+    q = W.bf16_round((rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32))
+    k = W.bf16_round((rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32))
+    heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+    ko = rng.standard_normal((B, H, 40, hd)) * 1.5
+    lg = np.matmul(q.astype(np.float64), np.swapaxes(ko, -1, -2)) / np.sqrt(hd)
+    mx = lg.max(-1, keepdims=True)
+    lse = (mx[..., 0] + np.log(np.exp(lg - mx).sum(-1))).astype(np.float32)
+    qd, kd = to_dev(q, "bf16"), to_dev(k, "bf16")
+    r = provip.pv_prune_head_aware(qd, kd, heads, 100, row_lse=torch.from_numpy(lse).to("cuda:0"))
+    r2 = provip.pv_prune_head_aware(qd, kd, torch.from_numpy(heads).to("cuda:0"), 100,
+                                    row_lse=torch.from_numpy(lse).to("cuda:0"))
+    torch.cuda.synchronize()
+    assert torch.equal(r["score"], r2["score"]) and torch.equal(r["kept"], r2["kept"])
+    v, kept = to_host(r["score"]), to_host(r["kept"])
+    _, ref_v = oracle.head_aware_in_model(q, k, heads, lse.astype(np.float64), 100)
+    assert rel_err(v, ref_v) <= TOL["bf16"], rel_err(v, ref_v)
+    for b in range(B):
+        check_kept(kept[b], ref_v[b], 100, "bf16")
