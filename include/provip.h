@@ -31,6 +31,12 @@
  *     equal.  Inputs must be finite (NaN/Inf give unspecified selections).
  *   - Results are deterministic: two calls on the same inputs return the same
  *     bits (no floating-point atomics; every reduction has a fixed order).
+ *   - Widths: an embedding width d or head width hd may be any multiple of 8
+ *     in range.  The matrix-core kernels stream 128-byte chunks of embedding
+ *     rows and a multiple of 32 elements of head rows; a call whose rows
+ *     have another width first copies them, zero-padded, into its workspace
+ *     (zeros change no dot product and no norm; the attention scale keeps
+ *     the true hd).  The workspace queries include those copies.
  */
 #ifndef PROVIP_H
 #define PROVIP_H
@@ -88,7 +94,7 @@ int pv_version(void);
  * mask   [B][Nt]     int32 out    required
  * count  [B]         int32 out    required
  * r      [B][Nt]     float32 out  may be NULL
- * Sizes: 1 <= Nt <= PV_MAX_TEXT, 64 <= d <= PV_MAX_DIM with d % 64 == 0.
+ * Sizes: 1 <= Nt <= PV_MAX_TEXT, 8 <= d <= PV_MAX_DIM with d % 8 == 0.
  * ---------------------------------------------------------------------- */
 size_t pv_critical_text_workspace_bytes(int B, int Nt, int d, int dtype);
 
@@ -119,7 +125,7 @@ int pv_critical_text(const void *text, int B, int Nt, int d, int dtype, int32_t 
  * assign   [B][Nv]         int32 out    may be NULL
  * merged   [B][budget][d]  dtype out    may be NULL (then no merge is run)
  * Sizes: 1 <= Nv <= PV_MAX_TOKENS, 1 <= Nt <= PV_MAX_TEXT,
- *        64 <= d <= PV_MAX_DIM with d % 64 == 0, 1 <= budget <= Nv.
+ *        8 <= d <= PV_MAX_DIM with d % 8 == 0, 1 <= budget <= Nv.
  * ---------------------------------------------------------------------- */
 size_t pv_dedup_workspace_bytes(int B, int Nv, int Nt, int d, int budget, int dtype);
 
@@ -185,8 +191,8 @@ int pv_prune_dedup_masked(const void *vis, const void *anchors, const int32_t *a
  * heads_host [B][n_heads]    int32      HOST memory; distinct ids in [0, H)
  * kept       [B][budget]     int32 out  required
  * score      [B][N]          float32 out  v, may be NULL
- * Sizes: 1 <= N <= PV_MAX_TOKENS, 1 <= Nt <= PV_MAX_TEXT, hd % 32 == 0,
- *        32 <= hd <= PV_MAX_HEAD_DIM, 1 <= n_heads <= min(H, PV_MAX_HEADS),
+ * Sizes: 1 <= N <= PV_MAX_TOKENS, 1 <= Nt <= PV_MAX_TEXT, hd % 8 == 0,
+ *        8 <= hd <= PV_MAX_HEAD_DIM, 1 <= n_heads <= min(H, PV_MAX_HEADS),
  *        1 <= budget <= N.
  * ---------------------------------------------------------------------- */
 size_t pv_head_aware_workspace_bytes(int B, int H, int Nt, int N, int hd, int n_heads,
@@ -254,9 +260,12 @@ int pv_prune_head_aware_ex(const void *q, const void *k, const int32_t *heads_ho
  * heads_out  [B][n_vis]      int32 out  required
  * conf       [B][H]          float32 out  C, may be NULL
  * Sizes as pv_prune_head_aware, plus H <= PV_MAX_HEADS, 1 <= n_vis <= H
- * (else PV_ERR_HEADS).  workspace: pv_visual_heads_workspace_bytes(B, H, Nt).
+ * (else PV_ERR_HEADS).  workspace: pv_visual_heads_workspace_bytes_hd(B, H,
+ * Nt, N, hd, dtype); pv_visual_heads_workspace_bytes(B, H, Nt) gives the
+ * same for hd % 32 == 0.
  * ---------------------------------------------------------------------- */
 size_t pv_visual_heads_workspace_bytes(int B, int H, int Nt);
+size_t pv_visual_heads_workspace_bytes_hd(int B, int H, int Nt, int N, int hd, int dtype);
 
 /* The same with the confidence summed over the rows i with
  * row_mask[b][i] != 0 only (the critical text rows of Sec. 4.4; a sample

@@ -35,6 +35,16 @@ struct Carve {
 
 bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
 
+size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Widths the matrix-core kernels stream: embedding rows in 128-byte k chunks,
+// head rows in 64-byte windows with a whole number of 128-byte chunks for
+// fp32 (a multiple of 32 elements either way).  A row of another width (any
+// multiple of 8 elements) is copied into a zero-padded row of the next such
+// width first; zeros change no dot product and no norm.
+int padded_d(int d, int esz) { return (d * esz + 127) / 128 * 128 / esz; }
+int padded_hd(int hd) { return (hd + 31) / 32 * 32; }
+
 // Launches the kernels of one call.  With events, events[i] is recorded
 // before kernel i and events[n] after the last one; with reps > 1 every
 // kernel is launched reps times back to back between its two events (the
@@ -164,12 +174,23 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
     return P;
 }
 
+// Workspace of a dedup call: its plan at the streamed width, plus the padded
+// copies of the visual tokens and the anchors when d is not that width.
+size_t dedup_total_bytes(int B, int Nv, int Nt, int d, int esz, int budget, bool want_p,
+                         bool want_assign, bool want_merged) {
+    const int dp = padded_d(d, esz);
+    size_t b = round_up(plan_dedup(nullptr, B, Nv, Nt, dp, esz, budget, want_p, want_assign,
+                                   want_merged).bytes);
+    if (dp != d) b += round_up((size_t)B * Nv * dp * esz) + round_up((size_t)B * Nt * dp * esz);
+    return b + kAlign;
+}
+
 int check_dedup(const void *vis, const void *anchors, int B, int Nv, int Nt, int d, int dtype,
                 int budget, const int32_t *kept) {
     if (!vis || !anchors || !kept) return PV_ERR_NULL;
     if (dtype != PV_F32 && dtype != PV_BF16) return PV_ERR_DTYPE;
     if (B < 1 || B > 65535 || Nv < 1 || Nv > PV_MAX_TOKENS || Nt < 1 || Nt > PV_MAX_TEXT ||
-        d < 64 || d > PV_MAX_DIM || d % 64 != 0)
+        d < 8 || d > PV_MAX_DIM || d % 8 != 0)
         return PV_ERR_SHAPE;
     if (budget < 1 || budget > Nv) return PV_ERR_BUDGET;
     return PV_OK;
@@ -227,16 +248,17 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     if (anchor_mask && (uintptr_t)anchor_mask % 4) return PV_ERR_ALIGN;
     const bool need_assign = assign != nullptr || merged != nullptr;
     const int esz = (dtype == PV_BF16) ? 2 : 4;
-    DedupPlan P0 = plan_dedup(nullptr, B, Nv, Nt, d, esz, budget, score == nullptr,
-                              need_assign && !assign, merged != nullptr);
+    const int dp = padded_d(d, esz);  // the width the products stream
     if (!workspace) return PV_ERR_WORKSPACE;
-    if (ws_bytes < P0.bytes) return PV_ERR_WORKSPACE;
+    if (ws_bytes < dedup_total_bytes(B, Nv, Nt, d, esz, budget, score == nullptr,
+                                     need_assign && !assign, merged != nullptr))
+        return PV_ERR_WORKSPACE;
     for (const void *p : {vis, anchors, (const void *)kept, (const void *)score,
                           (const void *)assign, (const void *)merged, (const void *)workspace})
         if (p && !aligned16(p)) return PV_ERR_ALIGN;
     // carve from a 256-aligned start
     char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
-    DedupPlan P = plan_dedup(wsa, B, Nv, Nt, d, esz, budget, score == nullptr,
+    DedupPlan P = plan_dedup(wsa, B, Nv, Nt, dp, esz, budget, score == nullptr,
                              need_assign && !assign, merged != nullptr);
     float *p = score ? score : P.p;
     int32_t *asg = assign ? assign : P.assign;
@@ -244,7 +266,22 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     hipStream_t st = (hipStream_t)stream;
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
-    if (!launch_front(tr, P, dt, vis, anchors, anchor_mask, B, Nv, Nt, d, budget, p, kept,
+    // the rows the products read: the inputs, or their zero-padded copies
+    const void *vis_k = vis, *anc_k = anchors;
+    if (dp != d) {
+        char *vp = wsa + round_up(P.bytes);
+        char *ap = vp + round_up((size_t)B * Nv * dp * esz);
+        if (!tr.launch("pad", [&] {
+                return pv::launch_pad_rows(vis, vp, (long long)B * Nv, d * esz, dp * esz, st);
+            }) ||
+            !tr.launch("pad", [&] {
+                return pv::launch_pad_rows(anchors, ap, (long long)B * Nt, d * esz, dp * esz, st);
+            }))
+            return PV_ERR_HIP;
+        vis_k = vp;
+        anc_k = ap;
+    }
+    if (!launch_front(tr, P, dt, vis_k, anc_k, anchor_mask, B, Nv, Nt, dp, budget, p, kept,
                       need_assign ? asg : nullptr, st))
         return PV_ERR_HIP;
     hipStream_t sm = st;  // stream of the assignment and merge kernels
@@ -257,7 +294,7 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     if (need_assign && P.Mp > 0) {
         if (P.gram_big) {
             if (!tr.launch("gram_tile", [&] {
-                    return pv::launch_gram_tile(dt, vis, B, Nv, d, kept, budget, P.pruned, P.Mp,
+                    return pv::launch_gram_tile(dt, vis_k, B, Nv, dp, kept, budget, P.pruned, P.Mp,
                                                 P.invn, P.best_val, P.best_slot, asg, sm);
                 }))
                 return PV_ERR_HIP;
@@ -270,8 +307,8 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
             }
         } else {
             if (!tr.launch("gram_partial", [&] {
-                    return pv::launch_gram_partial(dt, vis, B, Nv, d, kept, budget, P.pruned, P.Mp,
-                                                   P.ks_gram, P.gpart, sm);
+                    return pv::launch_gram_partial(dt, vis_k, B, Nv, dp, kept, budget, P.pruned,
+                                                   P.Mp, P.ks_gram, P.gpart, sm);
                 }))
                 return PV_ERR_HIP;
             if (!tr.launch("gram_reduce", [&] {
@@ -322,11 +359,20 @@ HeadPlan plan_head(void *ws, int B, int Nt, int N, int n_heads, bool want_v) {
     return P;
 }
 
+// Workspace of a head-aware call: its plan, plus zero-padded copies of Q and
+// K when hd is not a streamed width.
+size_t head_total_bytes(int B, int H, int Nt, int N, int hd, int esz, int n_heads, bool want_v) {
+    size_t b = round_up(plan_head(nullptr, B, Nt, N, n_heads, want_v).bytes);
+    const int hp = padded_hd(hd);
+    if (hp != hd) b += round_up((size_t)B * H * Nt * hp * esz) + round_up((size_t)B * H * N * hp * esz);
+    return b + kAlign;
+}
+
 int check_qk(const void *q, const void *k, int B, int H, int Nt, int N, int hd, int dtype) {
     if (!q || !k) return PV_ERR_NULL;
     if (dtype != PV_F32 && dtype != PV_BF16) return PV_ERR_DTYPE;
     if (B < 1 || B > 65535 || H < 1 || Nt < 1 || Nt > PV_MAX_TEXT || N < 1 || N > PV_MAX_TOKENS ||
-        hd < 32 || hd > PV_MAX_HEAD_DIM || hd % 32 != 0)
+        hd < 8 || hd > PV_MAX_HEAD_DIM || hd % 8 != 0)
         return PV_ERR_SHAPE;
     if (!aligned16(q) || !aligned16(k)) return PV_ERR_ALIGN;
     return PV_OK;
@@ -368,8 +414,9 @@ int head_impl(const void *q, const void *k, const int32_t *heads, const int32_t 
     if (row_lse && (uintptr_t)row_lse % 4) return PV_ERR_ALIGN;
     int rc = check_head(q, k, heads, heads_dev, n_heads, B, H, Nt, N, hd, dtype, budget, kept);
     if (rc != PV_OK) return rc;
-    HeadPlan P0 = plan_head(nullptr, B, Nt, N, n_heads, score == nullptr);
-    if (!workspace || ws_bytes < P0.bytes) return PV_ERR_WORKSPACE;
+    const int esz = (dtype == PV_BF16) ? 2 : 4;
+    if (!workspace || ws_bytes < head_total_bytes(B, H, Nt, N, hd, esz, n_heads, score == nullptr))
+        return PV_ERR_WORKSPACE;
     for (const void *p : {q, k, (const void *)kept, (const void *)score, (const void *)workspace})
         if (p && !aligned16(p)) return PV_ERR_ALIGN;
     char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
@@ -379,15 +426,31 @@ int head_impl(const void *q, const void *k, const int32_t *heads, const int32_t 
     hipStream_t st = (hipStream_t)stream;
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
+    // the rows the products read: the inputs, or their zero-padded copies
+    const int hp = padded_hd(hd);
+    const void *q_k = q, *k_k = k;
+    if (hp != hd) {
+        char *qp = wsa + round_up(P.bytes);
+        char *kp = qp + round_up((size_t)B * H * Nt * hp * esz);
+        if (!tr.launch("pad", [&] {
+                return pv::launch_pad_rows(q, qp, (long long)B * H * Nt, hd * esz, hp * esz, st);
+            }) ||
+            !tr.launch("pad", [&] {
+                return pv::launch_pad_rows(k, kp, (long long)B * H * N, hd * esz, hp * esz, st);
+            }))
+            return PV_ERR_HIP;
+        q_k = qp;
+        k_k = kp;
+    }
 
     if (!tr.launch("score_partial", [&] {
-            return pv::launch_score_partial(dt, q, k, heads, heads_dev, row_lse, B, H, Nt, N, hd,
-                                            n_heads, P.partial, P.stats, st);
+            return pv::launch_score_partial(dt, q_k, k_k, heads, heads_dev, row_lse, B, H, Nt, N,
+                                            hp, hd, n_heads, P.partial, P.stats, st);
         }))
         return PV_ERR_HIP;
     const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
     if (!tr.launch("score_select", [&] {
-            const int parts = pv::score_parts(dt, B, H, n_heads, Nt, N, hd);
+            const int parts = pv::score_parts(dt, B, H, n_heads, Nt, N, hp);
             return pv::launch_score_select(P.partial, B, n_heads * parts, N, inv_norm, v, budget,
                                            kept, st);
         }))
@@ -403,6 +466,14 @@ size_t vis_heads_bytes(int B, int H, int Nt) {
     return c.off + kAlign;
 }
 
+// The same plus zero-padded copies of Q and K when hd is not a streamed width.
+size_t vis_heads_total_bytes(int B, int H, int Nt, int N, int hd, int esz) {
+    size_t b = round_up(vis_heads_bytes(B, H, Nt));
+    const int hp = padded_hd(hd);
+    if (hp != hd) b += round_up((size_t)B * H * Nt * hp * esz) + round_up((size_t)B * H * N * hp * esz);
+    return b + kAlign;
+}
+
 int vis_heads_impl(const void *q, const void *k, int B, int H, int Nt, int N, int hd, int dtype,
                    int n_vis, int32_t *heads_out, float *conf, void *workspace, size_t ws_bytes,
                    void *stream, void *const *events, int n_events, int reps, int *n_kernels,
@@ -415,16 +486,36 @@ int vis_heads_impl(const void *q, const void *k, int B, int H, int Nt, int N, in
     int rc = check_qk(q, k, B, H, Nt, N, hd, dtype);
     if (rc != PV_OK) return rc;
     if (H > PV_MAX_HEADS || n_vis < 1 || n_vis > H) return PV_ERR_HEADS;
-    if (!workspace || ws_bytes < vis_heads_bytes(B, H, Nt)) return PV_ERR_WORKSPACE;
+    const int esz = (dtype == PV_BF16) ? 2 : 4;
+    if (!workspace || ws_bytes < vis_heads_total_bytes(B, H, Nt, N, hd, esz))
+        return PV_ERR_WORKSPACE;
     for (const void *p : {(const void *)heads_out, (const void *)conf, (const void *)workspace})
         if (p && !aligned16(p)) return PV_ERR_ALIGN;
-    float *part = (float *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
+    char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
+    float *part = (float *)wsa;
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
     hipStream_t st = (hipStream_t)stream;
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
+    // the rows the products read: the inputs, or their zero-padded copies
+    const int hp = padded_hd(hd);
+    const void *q_k = q, *k_k = k;
+    if (hp != hd) {
+        char *qp = wsa + round_up(vis_heads_bytes(B, H, Nt));
+        char *kp = qp + round_up((size_t)B * H * Nt * hp * esz);
+        if (!tr.launch("pad", [&] {
+                return pv::launch_pad_rows(q, qp, (long long)B * H * Nt, hd * esz, hp * esz, st);
+            }) ||
+            !tr.launch("pad", [&] {
+                return pv::launch_pad_rows(k, kp, (long long)B * H * N, hd * esz, hp * esz, st);
+            }))
+            return PV_ERR_HIP;
+        q_k = qp;
+        k_k = kp;
+    }
     if (!tr.launch("head_conf", [&] {
-            return pv::launch_head_conf(dt, q, k, row_mask, row_lse, B, H, Nt, N, hd, part, st);
+            return pv::launch_head_conf(dt, q_k, k_k, row_mask, row_lse, B, H, Nt, N, hp, hd, part,
+                                        st);
         }))
         return PV_ERR_HIP;
     if (!tr.launch("conf_select", [&] {
@@ -441,6 +532,17 @@ struct TextPlan {
     float *part, *ssv, *ssa, *G;
     size_t bytes;
 };
+
+TextPlan plan_text(void *ws, int B, int Nt, int d, int esz);
+
+// Workspace of the critical-text call, with a zero-padded copy of the text
+// rows when d is not a streamed width.
+size_t text_total_bytes(int B, int Nt, int d, int esz) {
+    const int dp = padded_d(d, esz);
+    size_t b = round_up(plan_text(nullptr, B, Nt, dp, esz).bytes);
+    if (dp != d) b += round_up((size_t)B * Nt * dp * esz);
+    return b + kAlign;
+}
 
 TextPlan plan_text(void *ws, int B, int Nt, int d, int esz) {
     TextPlan P;
@@ -462,23 +564,33 @@ int text_impl(const void *text, int B, int Nt, int d, int dtype, int32_t *mask, 
     if (reps < 1) return PV_ERR_SHAPE;
     if (!text || !mask || !count) return PV_ERR_NULL;
     if (dtype != PV_F32 && dtype != PV_BF16) return PV_ERR_DTYPE;
-    if (B < 1 || B > 65535 || Nt < 1 || Nt > PV_MAX_TEXT || d < 64 || d > PV_MAX_DIM || d % 64)
+    if (B < 1 || B > 65535 || Nt < 1 || Nt > PV_MAX_TEXT || d < 8 || d > PV_MAX_DIM || d % 8)
         return PV_ERR_SHAPE;
     const int esz = dtype == PV_BF16 ? 2 : 4;
-    if (!workspace || ws_bytes < plan_text(nullptr, B, Nt, d, esz).bytes) return PV_ERR_WORKSPACE;
+    if (!workspace || ws_bytes < text_total_bytes(B, Nt, d, esz)) return PV_ERR_WORKSPACE;
     for (const void *p : {text, (const void *)mask, (const void *)count, (const void *)r,
                           (const void *)workspace})
         if (p && !aligned16(p)) return PV_ERR_ALIGN;
     char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
-    TextPlan P = plan_text(wsa, B, Nt, d, esz);
+    const int dp = padded_d(d, esz);  // the width the product streams
+    TextPlan P = plan_text(wsa, B, Nt, dp, esz);
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
     hipStream_t st = (hipStream_t)stream;
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
+    const void *text_k = text;
+    if (dp != d) {
+        char *tp = wsa + round_up(P.bytes);
+        if (!tr.launch("pad", [&] {
+                return pv::launch_pad_rows(text, tp, (long long)B * Nt, d * esz, dp * esz, st);
+            }))
+            return PV_ERR_HIP;
+        text_k = tp;
+    }
     // E E^T: the text rows are both operands of the split-k product
     if (!tr.launch("text_gram", [&] {
-            return pv::launch_cos_partial(dt, text, text, B, Nt, Nt, d, P.ks, P.part, P.ssv, P.ssa,
-                                          st);
+            return pv::launch_cos_partial(dt, text_k, text_k, B, Nt, Nt, dp, P.ks, P.part, P.ssv,
+                                          P.ssa, st);
         }))
         return PV_ERR_HIP;
     if (!tr.launch("text_gram_sum", [&] {
@@ -516,10 +628,10 @@ PV_API const char *pv_status_string(int status) {
 PV_API int pv_version(void) { return (1 << 16) | 0; }
 
 PV_API size_t pv_dedup_workspace_bytes(int B, int Nv, int Nt, int d, int budget, int dtype) {
-    if (B < 1 || Nv < 1 || Nt < 1 || d < 64 || budget < 1 || budget > Nv) return 0;
+    if (B < 1 || Nv < 1 || Nt < 1 || d < 8 || budget < 1 || budget > Nv) return 0;
     if (dtype != PV_F32 && dtype != PV_BF16) return 0;
     // sized for the case that needs the most: no score or assign output
-    return plan_dedup(nullptr, B, Nv, Nt, d, dtype == PV_BF16 ? 2 : 4, budget, true, true, true).bytes;
+    return dedup_total_bytes(B, Nv, Nt, d, dtype == PV_BF16 ? 2 : 4, budget, true, true, true);
 }
 
 PV_API int pv_prune_dedup(const void *vis, const void *anchors, int B, int Nv, int Nt, int d,
@@ -572,8 +684,8 @@ PV_API int pv_prune_dedup_masked_timed(const void *vis, const void *anchors,
 }
 
 PV_API size_t pv_critical_text_workspace_bytes(int B, int Nt, int d, int dtype) {
-    if (B < 1 || Nt < 1 || d < 64 || (dtype != PV_F32 && dtype != PV_BF16)) return 0;
-    return plan_text(nullptr, B, Nt, d, dtype == PV_BF16 ? 2 : 4).bytes;
+    if (B < 1 || Nt < 1 || d < 8 || (dtype != PV_F32 && dtype != PV_BF16)) return 0;
+    return text_total_bytes(B, Nt, d, dtype == PV_BF16 ? 2 : 4);
 }
 
 PV_API int pv_critical_text(const void *text, int B, int Nt, int d, int dtype, int32_t *mask,
@@ -593,12 +705,10 @@ PV_API int pv_critical_text_timed(const void *text, int B, int Nt, int d, int dt
 
 PV_API size_t pv_head_aware_workspace_bytes(int B, int H, int Nt, int N, int hd, int n_heads,
                                             int budget, int dtype) {
-    (void)H;
-    (void)hd;
     (void)budget;
-    (void)dtype;
-    if (B < 1 || Nt < 1 || N < 1 || n_heads < 1) return 0;
-    return plan_head(nullptr, B, Nt, N, n_heads, true).bytes;
+    if (B < 1 || H < 1 || Nt < 1 || N < 1 || hd < 1 || n_heads < 1) return 0;
+    if (dtype != PV_F32 && dtype != PV_BF16) return 0;
+    return head_total_bytes(B, H, Nt, N, hd, dtype == PV_BF16 ? 2 : 4, n_heads, true);
 }
 
 PV_API int pv_prune_head_aware(const void *q, const void *k, const int32_t *heads_host, int n_heads,
@@ -667,6 +777,12 @@ PV_API int pv_prune_head_aware_ex_timed(const void *q, const void *k, const int3
 PV_API size_t pv_visual_heads_workspace_bytes(int B, int H, int Nt) {
     if (B < 1 || H < 1 || Nt < 1) return 0;
     return vis_heads_bytes(B, H, Nt);
+}
+
+PV_API size_t pv_visual_heads_workspace_bytes_hd(int B, int H, int Nt, int N, int hd, int dtype) {
+    if (B < 1 || H < 1 || Nt < 1 || N < 1 || hd < 1) return 0;
+    if (dtype != PV_F32 && dtype != PV_BF16) return 0;
+    return vis_heads_total_bytes(B, H, Nt, N, hd, dtype == PV_BF16 ? 2 : 4);
 }
 
 PV_API int pv_visual_heads(const void *q, const void *k, int B, int H, int Nt, int N, int hd,
@@ -832,16 +948,14 @@ PV_API int pv_prune_gather(const void *src, void *dst, const int32_t *idx, int B
 // ---------------------------------------------------------------------------
 namespace {
 
-size_t round_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
-
 struct PipeSizes {
     size_t dedup, head, total;
 };
 
-PipeSizes pipe_sizes(int B, int Nv, int Nt, int d, int esz, int N1, int n_heads) {
-    const DedupPlan D = plan_dedup(nullptr, B, Nv, Nt, d, esz, N1, false, false, true);
-    const HeadPlan Hh = plan_head(nullptr, B, Nt, N1, n_heads, false);
-    return PipeSizes{round_up(D.bytes), Hh.bytes, round_up(D.bytes) + Hh.bytes};
+PipeSizes pipe_sizes(int B, int Nv, int Nt, int d, int H, int hd, int esz, int N1, int n_heads) {
+    const size_t D = round_up(dedup_total_bytes(B, Nv, Nt, d, esz, N1, false, false, true));
+    const size_t Hh = head_total_bytes(B, H, Nt, N1, hd, esz, n_heads, false);
+    return PipeSizes{D, Hh, D + Hh};
 }
 
 pv_gather_desc kv_desc(const void *src, void *dst, int H, int n_src, int k, int64_t row) {
@@ -877,7 +991,7 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
     rc = check_head(q, k1, heads, nullptr, n_heads, B, H, Nt, N1, hd, dtype, N2, kept2);
     if (rc != PV_OK) return rc;
     const int esz = (dtype == PV_BF16) ? 2 : 4;
-    const PipeSizes sz = pipe_sizes(B, Nv, Nt, d, esz, N1, n_heads);
+    const PipeSizes sz = pipe_sizes(B, Nv, Nt, d, H, hd, esz, N1, n_heads);
     if (!workspace || ws_bytes < sz.total) return PV_ERR_WORKSPACE;
     const void *const ptrs[] = {vis,    anchors, q,      k_full, v_full, kept1,   score1, assign, merged,
                                 k1,     v1,      kept2,  score2, hidden2, k2,     v2,     workspace};
@@ -901,7 +1015,8 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
     // the two chains after the top-N_1 share launches when the dedup takes
     // the split-k Gram and the plain merge, and the score its 16-row blocks
-    const bool carry = !force_separate && P.Mp > 0 && !P.gram_big && !P.lists && N1 <= 256 &&
+    const bool carry = !force_separate && padded_d(d, esz) == d && padded_hd(hd) == hd &&
+                       P.Mp > 0 && !P.gram_big && !P.lists && N1 <= 256 &&
                        pv::score_can_carry_reduce(dt, hd) &&
                        !pv::score_uses_head_form(dt, B, H, n_heads, Nt, N1, hd) &&
                        !pv::score_uses_split_form(dt, B, H, n_heads, Nt, N1, hd);
@@ -937,7 +1052,7 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
                            B * ((P.Mp + pv::kReduceRowsPerBlock - 1) / pv::kReduceRowsPerBlock)};
     if (!tr.launch("score_partial+gram_reduce", [&] {
             return pv::launch_score_partial(dt, q, k1, heads, nullptr, nullptr, B, H, Nt, N1, hd,
-                                            n_heads, Hh.partial, Hh.stats, st, &rj);
+                                            hd, n_heads, Hh.partial, Hh.stats, st, &rj);
         }))
         return PV_ERR_HIP;
     // merge + the score's top-N_2
@@ -964,7 +1079,8 @@ PV_API size_t pv_pipeline_workspace_bytes(int B, int Nv, int Nt, int d, int H, i
     (void)budget2;
     if (B < 1 || Nv < 1 || Nt < 1 || d < 1 || n_heads < 1 || budget1 < 1 || budget1 > Nv)
         return 0;
-    return pipe_sizes(B, Nv, Nt, d, (dtype == PV_BF16) ? 2 : 4, budget1, n_heads).total;
+    if (H < 1 || hd < 1) return 0;
+    return pipe_sizes(B, Nv, Nt, d, H, hd, (dtype == PV_BF16) ? 2 : 4, budget1, n_heads).total;
 }
 
 PV_API int pv_prune_pipeline(const void *vis, const void *anchors, const void *q,
@@ -1027,11 +1143,11 @@ struct ProgPlan {
 ProgPlan plan_prog(void *ws, int B, int Nv, int Nt, int d, int H, int hd, int esz, int N1,
                    int n_vis, int N2, int N3, bool want_s2, bool want_s3) {
     ProgPlan P;
-    P.text = plan_text(nullptr, B, Nt, d, esz).bytes;
-    P.dedup = plan_dedup(nullptr, B, Nv, Nt, d, esz, N1, true, false, true).bytes;
-    P.vh = vis_heads_bytes(B, H, Nt);
-    P.head_b = plan_head(nullptr, B, Nt, N1, n_vis, !want_s2).bytes;
-    P.head_c = plan_head(nullptr, B, Nt, N2, H, !want_s3).bytes;
+    P.text = text_total_bytes(B, Nt, d, esz);
+    P.dedup = dedup_total_bytes(B, Nv, Nt, d, esz, N1, true, false, true);
+    P.vh = vis_heads_total_bytes(B, H, Nt, N1, hd, esz);
+    P.head_b = head_total_bytes(B, H, Nt, N1, hd, esz, n_vis, !want_s2);
+    P.head_c = head_total_bytes(B, H, Nt, N2, hd, esz, H, !want_s3);
     Carve c(ws);
     P.ws_text = c.take<char>(P.text);
     P.ws_dedup = c.take<char>(P.dedup);
@@ -1212,7 +1328,7 @@ PV_API int pv_prune_pipeline_noalloc(const void *vis, const void *anchors, const
     const int esz = (dtype == PV_BF16) ? 2 : 4;
     // the step carves its workspace from a 256-byte boundary, which the
     // array's start already is
-    if (pipe_sizes(B, Nv, Nt, d, esz, budget1, n_heads).total > (size_t)PV_STATIC_SCRATCH_BYTES)
+    if (pipe_sizes(B, Nv, Nt, d, H, hd, esz, budget1, n_heads).total > (size_t)PV_STATIC_SCRATCH_BYTES)
         return PV_ERR_SCRATCH;
     void *ws = nullptr;
     if ((rc = scratch_of_current_device(&ws)) != PV_OK) return rc;

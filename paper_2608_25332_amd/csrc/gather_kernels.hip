@@ -44,4 +44,34 @@ hipError_t launch_compose_index(const int32_t *base, const int32_t *idx, int B, 
     return hipGetLastError();
 }
 
+// Rows of a width the matrix-core kernels do not stream (their k chunks are
+// 128 bytes of an embedding row and 64 or 128 bytes of a head row) copied
+// into rows of the next such width, the tail filled with zeros: a zero
+// element changes no dot product and no norm.  dst row r = src row r
+// (in_bytes) followed by zeros up to out_bytes; both multiples of 16.
+__global__ __launch_bounds__(256) void pad_rows_kernel(const char *__restrict__ src,
+                                                       char *__restrict__ dst, long long n_rows,
+                                                       int in_pieces, int out_pieces) {
+    const long long total = n_rows * out_pieces;
+    for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < total;
+         i += (long long)gridDim.x * 256) {
+        const long long r = i / out_pieces;
+        const int p = (int)(i - r * out_pieces);
+        uint4 v = {0u, 0u, 0u, 0u};
+        if (p < in_pieces) v = ld16(src + (r * in_pieces + p) * 16);
+        st16(dst + i * 16, v);
+    }
+}
+
+hipError_t launch_pad_rows(const void *src, void *dst, long long n_rows, int in_bytes,
+                           int out_bytes, hipStream_t st) {
+    const long long total = n_rows * (out_bytes / 16);
+    long long blocks = (total + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL(pad_rows_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+                       (const char *)src, (char *)dst, n_rows, in_bytes / 16, out_bytes / 16);
+    return hipGetLastError();
+}
+
 }  // namespace pv

@@ -877,6 +877,7 @@ struct ScoreLaunch {
     float sl2e;
     float *partial;
     hipStream_t st;
+    int hd_scale = 0;  // head width of the attention scale (0: the row width)
     const ReduceJob *rj = nullptr;  // carried by the first launch (score only)
 };
 
@@ -1026,11 +1027,16 @@ static hipError_t score_split_go(const ScoreLaunch &a, float2 *stats) {
     return hipSuccess;
 }
 
+// log2(e) / sqrt(head width): the attention scale in base-2 units.
+static float scale_log2e_of(const ScoreLaunch &a, int hd) {
+    return (float)(1.4426950408889634 / sqrt((double)(a.hd_scale > 0 ? a.hd_scale : hd)));
+}
+
 template <bool CONF>
 static hipError_t score_any(int dt, int hd, ScoreLaunch a) {
     const int esz = (dt == kBF16) ? 2 : 4;
     const int nks = hd * esz / 64;
-    a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
+    a.sl2e = scale_log2e_of(a, hd);
     if (dt == kBF16) return score_dt<kBF16, CONF>(nks, a);
     return score_dt<kF32, CONF>(nks, a);
 }
@@ -1066,16 +1072,17 @@ bool score_can_carry_reduce(int dt, int hd) {
 
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, const float *row_lse, int B, int H,
-                                int Nt, int N, int hd, int n_heads, float *partial,
+                                int Nt, int N, int hd, int hd_scale, int n_heads, float *partial,
                                 float *split_stats, hipStream_t st, const ReduceJob *with) {
     ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg, nullptr,
                   row_lse, B, H, Nt, N, n_heads, 0.f, partial, st};
     a.rj = with;
+    a.hd_scale = hd_scale;
     const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
     if (with && !score_carries_reduce(nks, false)) return hipErrorInvalidValue;
     if (score_uses_split_form(dt, B, H, n_heads, Nt, N, hd)) {
         if (with || !split_stats) return hipErrorInvalidValue;  // the split form carries nothing
-        a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
+        a.sl2e = scale_log2e_of(a, hd);
         float2 *stats = reinterpret_cast<float2 *>(split_stats);
         if (dt == kBF16)
             return nks == 2 ? score_split_go<kBF16, 2>(a, stats) : score_split_go<kBF16, 4>(a, stats);
@@ -1083,7 +1090,7 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const int3
     }
     if (score_uses_head_form(dt, B, H, n_heads, Nt, N, hd)) {
         if (with) return hipErrorInvalidValue;  // the whole-head form carries nothing
-        a.sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
+        a.sl2e = scale_log2e_of(a, hd);
         if (dt == kBF16) return nks == 2 ? score_head_go<kBF16, 2>(a) : score_head_go<kBF16, 4>(a);
         return nks == 2 ? score_head_go<kF32, 2>(a) : score_head_go<kF32, 4>(a);
     }
@@ -1092,9 +1099,10 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const int3
 
 hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask,
                             const float *row_lse, int B, int H, int Nt, int N, int hd,
-                            float *partial, hipStream_t st) {
+                            int hd_scale, float *partial, hipStream_t st) {
     ScoreLaunch a{q, k, nullptr, nullptr, kHeadsAll, row_mask, row_lse, B, H, Nt, N, H, 0.f,
                   partial, st};
+    a.hd_scale = hd_scale;
     return score_any<true>(dt, hd, a);
 }
 

@@ -122,9 +122,12 @@ bool score_can_carry_reduce(int dt, int hd);
 // with: the split-k Gram's argmax carried as extra workgroups of the first
 // launch (or NULL); not with the whole-head form.
 // split_stats: workspace of score_split_stats_bytes (used by the split form).
+// hd: the width of the q and k rows (a multiple of 32); hd_scale: the head
+// width of the attention scale 1 / sqrt(hd_scale) (the rows may be padded
+// with zeros past it).
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, const float *row_lse, int B, int H,
-                                int Nt, int N, int hd, int n_heads, float *partial,
+                                int Nt, int N, int hd, int hd_scale, int n_heads, float *partial,
                                 float *split_stats, hipStream_t st,
                                 const ReduceJob *with = nullptr);
 // Head confidence of every head, per 16-row block: partial[b][h][rb].
@@ -133,7 +136,7 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const int3
 // taken over the visual slice of the model's softmax.
 hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t *row_mask,
                             const float *row_lse, int B, int H, int Nt, int N, int hd,
-                            float *partial, hipStream_t st);
+                            int hd_scale, float *partial, hipStream_t st);
 hipError_t launch_conf_select(const float *partial, int B, int H, int Nt, float *conf, int n_vis,
                               int32_t *heads, hipStream_t st);
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,
@@ -155,6 +158,9 @@ struct GatherArgs {
     int n;
 };
 hipError_t launch_gather(const GatherArgs &ga, const int32_t *idx, int B, int k, hipStream_t st);
+// dst row r = src row r (in_bytes) then zeros up to out_bytes (multiples of 16).
+hipError_t launch_pad_rows(const void *src, void *dst, long long n_rows, int in_bytes,
+                           int out_bytes, hipStream_t st);
 // out[b][r] = base[b][idx[b][r]] (b < B, r < k; idx clamped into [0, n_base)).
 hipError_t launch_compose_index(const int32_t *base, const int32_t *idx, int B, int n_base, int k,
                                 int32_t *out, hipStream_t st);

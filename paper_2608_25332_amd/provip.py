@@ -112,6 +112,8 @@ def load(path: str = LIB_PATH):
     lib.pv_prune_head_aware_ex_timed.argtypes = hax + timed_tail
     lib.pv_prune_head_aware_ex_timed.restype = _i
     lib.pv_visual_heads_workspace_bytes.argtypes = [_i, _i, _i]
+    lib.pv_visual_heads_workspace_bytes_hd.argtypes = [_i] * 6
+    lib.pv_visual_heads_workspace_bytes_hd.restype = _sz
     lib.pv_visual_heads_workspace_bytes.restype = _sz
     vh = [_vp, _vp, _i, _i, _i, _i, _i, _i, _i, _vp, _vp, _vp, _sz, _vp]
     lib.pv_visual_heads.argtypes = vh
@@ -433,7 +435,7 @@ def pv_visual_heads(q: torch.Tensor, k: torch.Tensor, n_vis: int, *, want_conf: 
     conf = o.get("conf") if want_conf else None
     if want_conf and conf is None:
         conf = torch.empty((B, H), dtype=torch.float32, device=dev)
-    nbytes = lib.pv_visual_heads_workspace_bytes(B, H, Nt)
+    nbytes = lib.pv_visual_heads_workspace_bytes_hd(B, H, Nt, N, hd, _dtype_code(q))
     if workspace is None or workspace.numel() < nbytes:
         workspace = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
     ev, nev, nm = _events_array(events)

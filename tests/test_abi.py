@@ -72,7 +72,8 @@ def test_dedup_validation(lib):
     assert _dedup(lib, dt=7) == -5
     assert _dedup(lib, Nv=0) == -2
     assert _dedup(lib, d=100) == -2
-    assert _dedup(lib, d=32) == -2
+    assert _dedup(lib, d=36) == -2
+    assert _dedup(lib, d=4) == -2
     assert _dedup(lib, Nt=0) == -2
     assert _dedup(lib, Nv=20000) == -2
     assert _dedup(lib, budget=0) == -3
@@ -104,7 +105,8 @@ def test_head_aware_validation(lib):
     assert _heads(lib, [-1]) == -4
     assert _heads(lib, [1, 1]) == -4       # repeated
     assert _heads(lib, [0, 1, 2, 3, 0]) == -4  # more heads than H
-    assert _heads(lib, [1], hd=48) == -2
+    assert _heads(lib, [1], hd=44) == -2
+    assert _heads(lib, [1], hd=4) == -2
     assert _heads(lib, [1], hd=512) == -2
     assert _heads(lib, [1], N=0) == -2
     assert _heads(lib, [1], budget=0) == -3
@@ -126,7 +128,7 @@ def test_head_aware_dev_validation(lib):
     assert call(n_heads=0) == -4
     assert call(n_heads=5) == -4           # more than H
     assert call(hd_ptr=FAKE + 2) == -8     # int32 list must be 4-byte aligned
-    assert call(hd=40) == -2
+    assert call(hd=44) == -2
     assert call(budget=33) == -3
     assert call(ws=None) == -6
 
@@ -158,7 +160,7 @@ def test_visual_heads_validation(lib):
     assert call(n_vis=0) == -4
     assert call(n_vis=33) == -4
     assert call(H=600, n_vis=6) == -4      # beyond PV_MAX_HEADS
-    assert call(hd=48) == -2
+    assert call(hd=44) == -2
     assert call(N=0) == -2
     assert call(dt=7) == -5
     assert call(ws=None) == -6
@@ -323,7 +325,7 @@ def test_pipeline_validation(lib):
     assert _pipe(lib, heads=(4,)) == -4
     assert _pipe(lib, heads=(1, 1)) == -4
     assert _pipe(lib, d=100) == -2
-    assert _pipe(lib, hd=48) == -2
+    assert _pipe(lib, hd=44) == -2
     assert _pipe(lib, dt=3) == -5
     assert _pipe(lib, misalign_at=3) == -8
     assert _pipe(lib, misalign_at=12) == -8
@@ -406,9 +408,29 @@ def test_progressive_validation(lib):
     assert _prog(lib, b3=0) == -3
     assert _prog(lib, nv=5) == -4               # more visual heads than heads
     assert _prog(lib, nv=0) == -4
-    assert _prog(lib, hd=48) == -2
+    assert _prog(lib, hd=44) == -2
     assert _prog(lib, ws=None) == -6
     assert _prog(lib, wsb=64) == -6
     f = lib.pv_progressive_workspace_bytes
     assert f(1, 576, 64, 4096, 32, 128, 192, 6, 64, 32, 1) > 0
     assert f(1, 576, 64, 4096, 32, 128, 192, 6, 64, 65, 1) == 0
+
+
+def test_ragged_widths_grow_the_workspace(lib):
+    """Widths that are multiples of 8 but not of the streamed chunk (d = 4104,
+    hd = 72 / 80 / 112) are accepted; their workspaces hold the zero-padded
+    copies of the rows."""
+    a = lib.pv_dedup_workspace_bytes(2, 576, 64, 4096, 192, 1)
+    b = lib.pv_dedup_workspace_bytes(2, 576, 64, 4104, 192, 1)
+    assert b >= a + 2 * (576 + 64) * 4160 * 2
+    for hd in (72, 80, 112):
+        w0 = lib.pv_head_aware_workspace_bytes(2, 8, 64, 300, 128, 4, 50, 1)
+        w1 = lib.pv_head_aware_workspace_bytes(2, 8, 64, 300, hd, 4, 50, 1)
+        assert w1 > 2 * 8 * (64 + 300) * ((hd + 31) // 32 * 32) * 2
+        assert w0 < w1
+        v1 = lib.pv_visual_heads_workspace_bytes_hd(2, 8, 64, 300, hd, 1)
+        assert v1 > lib.pv_visual_heads_workspace_bytes(2, 8, 64)
+    assert lib.pv_visual_heads_workspace_bytes_hd(2, 8, 64, 300, 128, 1) >= \
+        lib.pv_visual_heads_workspace_bytes(2, 8, 64)
+    assert lib.pv_critical_text_workspace_bytes(1, 64, 4104, 1) > \
+        lib.pv_critical_text_workspace_bytes(1, 64, 4096, 1)

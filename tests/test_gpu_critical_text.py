@@ -62,6 +62,8 @@ TEXT_CASES = [
     (1, 700, 256, 0.1, "f32"),       # 11 row elements per lane; wide self-similarity tiles
     (2, 1024, 128, 0.15, "bf16"),    # the most text rows
     (1, 1, 64, 1.0, "f32"),          # one token: r = 1, every token kept
+    (2, 64, 4104, 0.027, "bf16"),    # a width that is not a multiple of 64 (zero-padded rows)
+    (1, 30, 40, 0.3, "f32"),
 ]
 
 

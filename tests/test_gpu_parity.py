@@ -192,6 +192,14 @@ DEDUP_EDGE = [
     # merge through bucketed member lists (narrow rows, many slots)
     (1, 1000, 8, 64, 70, "bf16"),
     (2, 700, 5, 128, 200, "f32"),
+    # widths that are multiples of 8 but not of the streamed chunk: the rows
+    # are copied zero-padded into the workspace first
+    (2, 300, 20, 4104, 100, "bf16"),
+    (1, 200, 9, 4104, 50, "f32"),
+    (1, 50, 3, 8, 10, "f32"),
+    (3, 90, 12, 72, 30, "bf16"),
+    (16, 200, 64, 520, 64, "bf16"),       # split-k cosine on padded rows
+    (64, 600, 4, 1000, 200, "bf16"),      # full-k Gram tiles on padded rows
 ]
 
 
@@ -340,6 +348,14 @@ HEAD_EDGE = [
     # the 16-row blocks at long key lists (enough blocks to fill the chip)
     (16, 4, 64, 1500, 128, 4, 200, "bf16"),   # 24 chunks of logits held in registers
     (10, 2, 200, 2100, 128, 2, 600, "bf16"),  # keys streamed twice
+    # head widths that are multiples of 8 but not of 32 (zero-padded copies;
+    # the scale stays 1 / sqrt(hd))
+    (2, 4, 17, 100, 72, 2, 30, "bf16"),
+    (1, 3, 20, 300, 80, 2, 50, "f32"),
+    (2, 8, 64, 960, 112, 4, 200, "bf16"),     # split form on padded rows
+    (1, 2, 5, 33, 8, 1, 5, "f32"),
+    (40, 8, 64, 192, 80, 4, 64, "bf16"),      # whole-head form on padded rows
+    (3, 4, 30, 70, 40, "all", 20, "bf16"),    # every head
 ]
 
 
@@ -356,14 +372,17 @@ def score_form(B, H, Nt, N, hd, nh, dt):
 
 @pytest.mark.parametrize("B,H,Nt,N,hd,nh,budget,dt", HEAD_EDGE)
 def test_head_aware_edges(B, H, Nt, N, hd, nh, budget, dt):
-    _say(f"[head-edge] B={B} H={H} Nt={Nt} N={N} hd={hd} nh={nh} budget={budget} {dt} "
-         f"({score_form(B, H, Nt, N, hd, nh, dt)})")
+    form = score_form(B, H, Nt, N, (hd + 31) // 32 * 32, H if nh == "all" else nh, dt)
+    _say(f"[head-edge] B={B} H={H} Nt={Nt} N={N} hd={hd} nh={nh} budget={budget} {dt} ({form})")
     rng = np.random.default_rng(B * 1000 + N)
     q = (rng.standard_normal((B, H, Nt, hd)) * 1.5).astype(np.float32)
     k = (rng.standard_normal((B, H, N, hd)) * 1.5).astype(np.float32)
     if dt == "bf16":
         q, k = W.bf16_round(q), W.bf16_round(k)
-    heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
+    if nh == "all":
+        heads = np.tile(np.arange(H, dtype=np.int32), (B, 1))
+    else:
+        heads = np.stack([rng.permutation(H)[:nh] for _ in range(B)]).astype(np.int32)
     kept, v = run_head(q, k, heads, dt, budget)
     _, ref_v = oracle.head_aware(q, k, heads, budget)
     assert rel_err(v, ref_v) <= TOL[dt]

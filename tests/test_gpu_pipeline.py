@@ -143,6 +143,8 @@ EDGE = [
     (8, 576, 64, 512, 8, 128, 4, 192, 64, "bf16", False),   # LLaVA-like token counts, batch
     (8, 2000, 16, 64, 2, 128, 1, 600, 50, "bf16", False),   # full-k Gram tiles
     (32, 100, 16, 64, 8, 128, 4, 50, 10, "bf16", False),    # whole-head score form
+    (1, 300, 20, 520, 8, 80, 3, 100, 30, "bf16", False),    # padded widths: separate launches
+    (2, 150, 10, 72, 4, 40, 2, 60, 12, "f32", False),
 ]
 
 

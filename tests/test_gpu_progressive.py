@@ -144,6 +144,7 @@ PROG_EDGE = [
     (1, 90, 7, 128, 4, 128, 40, 1, 40, 1, "f32", True),       # budget2 = budget1, budget3 = 1
     (3, 200, 33, 512, 6, 128, 64, 6, 20, 20, "bf16", False),   # every head visual, N3 = N2
     (1, 1200, 100, 1024, 16, 128, 400, 6, 130, 65, "bf16", True),
+    (2, 250, 24, 520, 8, 72, 80, 4, 30, 12, "bf16", True),   # padded widths
 ]
 
 

@@ -81,6 +81,9 @@ VIS_EDGE = [
     (1, 4, 16, 300, 256, 2, "f32"),     # widest head
     (2, 5, 40, 1500, 96, 2, "f32"),     # many chunks of keys
     (1, 40, 128, 1152, 128, 6, "bf16"),
+    (2, 8, 33, 150, 72, 3, "bf16"),     # head widths padded to a multiple of 32
+    (1, 6, 20, 90, 112, 2, "f32"),
+    (2, 4, 16, 64, 8, 1, "bf16"),
 ]
 
 
