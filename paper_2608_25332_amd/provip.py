@@ -256,6 +256,12 @@ def pv_prune_dedup(vis: torch.Tensor, anchors: torch.Tensor, budget: int, *,
                                       _stream(dev), merge_stream.cuda_stream,
                                       selected.cuda_event, merged_done.cuda_event)
         _check("pv_prune_dedup_split", rc, lib)
+        # the merge stream reads vis, kept and the workspace and writes assign
+        # and merged after this call returns: keep the caching allocator from
+        # handing any of them to another allocation until that work is done
+        for t in (vis, anchors, kept, score, assign, merged, workspace):
+            if t is not None:
+                t.record_stream(merge_stream)
         return {"kept": kept, "score": score, "assign": assign, "merged": merged,
                 "n_kernels": None, "kernel_names": [], "workspace": workspace}
     ev, nev, nm = _events_array(events)
