@@ -75,6 +75,11 @@ def parse():
     ap.add_argument("--per-config", default="3,4,5",
                     help="workload ids measured after the headline for the per_config block "
                          "(empty: none)")
+    ap.add_argument("--gemm-calibration", action="store_true",
+                    help="instead of the step: the pruned x kept Gram of the hi-res and 13B "
+                         "workloads as a library GEMM (torch.bmm, i.e. hipBLASLt, on rows already "
+                         "gathered) beside this library's gram_tile (rows gathered in the kernel, "
+                         "argmax fused); prints its own JSON line")
     ap.add_argument("--score-sweep", action="store_true",
                     help="instead of the step: the head-aware call at the LLaVA-1.5-7B shape over "
                          "a batch sweep, with the selected heads and with all heads; prints its "
@@ -600,6 +605,70 @@ def score_sweep(torch, dev):
             "note": "warm caches; at B=256 with all heads the call reads 537 MB"}
 
 
+def gemm_calibration(torch, dev):
+    """The Gram stage's contraction at the hi-res and 13B shapes (pruned x
+    kept rows, 2 d (N_v - N_1) N_1 flops per sample) done two ways on the
+    same device: torch.bmm on bf16 rows already gathered into contiguous
+    [B, N_v - N_1, d] and [B, d, N_1] operands (the vendor GEMM library), and
+    the dedup call's gram_tile kernel (rows gathered through index lists in
+    the kernel, the row argmax fused), each timed back to back between HIP
+    events.  A reference point for the MFMA fraction the Gram reaches."""
+    from paper_2608_25332_amd import provip as pv
+    from paper_2608_25332_amd import workloads as W
+
+    rows = []
+    for wid in (4, 5):
+        w = W.make_workload(wid, with_kv=False)
+        s = w.spec
+        Mp, N1, d = s.Nv - w.N1, w.N1, s.d
+        flops = 2.0 * s.B * Mp * N1 * d
+        g = torch.Generator(device=dev)
+        g.manual_seed(wid)
+        A = torch.randn((s.B, Mp, d), generator=g, device=dev).to(torch.bfloat16)
+        Bt = torch.randn((s.B, d, N1), generator=g, device=dev).to(torch.bfloat16).contiguous()
+
+        def t_bmm():
+            torch.bmm(A, Bt)
+        t_bmm()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        z = torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(20):
+            t_bmm()
+        z.record()
+        torch.cuda.synchronize()
+        bmm_us = a.elapsed_time(z) * 1000.0 / 20
+        # this library's gram_tile in the dedup call (the kernel's own events)
+        vis = torch.from_numpy(W.bf16_bits(w.vis).view(np.int16)).view(torch.bfloat16).to(dev)
+        anc = torch.from_numpy(W.bf16_bits(w.anchors).view(np.int16)).view(torch.bfloat16).to(dev)
+        out = pv.pv_prune_dedup(vis, anc, w.N1, want_merged=False)
+        ws = out["workspace"]
+        samples = []
+        for _ in range(5):
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(Step.DEDUP_EVENTS)]
+            for e in ev:
+                e.record()
+            r = pv.pv_prune_dedup(vis, anc, w.N1, want_merged=False, out=out, workspace=ws,
+                                  events=ev, reps=20)
+            torch.cuda.synchronize()
+            i = r["kernel_names"].index("gram_tile")
+            samples.append(ev[i].elapsed_time(ev[i + 1]) * 1000.0 / 20)
+        gt_us = float(np.median(samples))
+        rows.append({"workload": s.name, "B": s.B, "M": Mp, "N": N1, "K": d, "flops": flops,
+                     "torch_bmm_us": bmm_us,
+                     "torch_bmm_frac_bf16_peak": flops / (bmm_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS,
+                     "gram_tile_us": gt_us,
+                     "gram_tile_frac_bf16_peak": flops / (gt_us * 1e-6) / 1e12 / BF16_PEAK_TFLOPS})
+        print(f"[gemm-calibration] {s.name}: torch.bmm {bmm_us:.1f} us, gram_tile {gt_us:.1f} us",
+              file=sys.stderr, flush=True)
+        del A, Bt, vis, anc, out, ws
+    return {"gemm_calibration": rows, "torch": torch.__version__,
+            "note": "torch.bmm on contiguous bf16 operands (rows already gathered); gram_tile "
+                    "gathers its rows through index lists and fuses the row argmax",
+            "csrc_digest": csrc_digest()}
+
+
 def visual_heads_timing(torch, step, n_vis=6):
     """Visual-head identification (all H heads of the N1 kept keys, the
     paper's N_vis = 6) at the step's shape: the call from graph replays and
@@ -976,6 +1045,9 @@ def main():
     torch.cuda.set_device(dev)
     if args.score_sweep:
         print(json.dumps(score_sweep(torch, dev)), flush=True)
+        return
+    if args.gemm_calibration:
+        print(json.dumps(gemm_calibration(torch, dev)), flush=True)
         return
     w = W.make_workload(args.workload)
     s = w.spec
