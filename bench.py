@@ -602,7 +602,8 @@ def score_sweep(torch, dev):
         del out, ws
     return {"score_sweep": rows, "shape": {"H": H, "Nt": Nt, "N": N, "hd": hd, "N2": N2,
                                            "dtype": "bf16"},
-            "note": "warm caches; at B=256 with all heads the call reads 537 MB"}
+            "note": "warm caches; at B=256 with all heads the call reads 537 MB",
+            "csrc_digest": csrc_digest()}
 
 
 def gemm_calibration(torch, dev):
