@@ -606,6 +606,49 @@ def score_sweep(torch, dev):
             "csrc_digest": csrc_digest()}
 
 
+def measured_peaks(torch, dev):
+    """The two published peaks the rooflines divide by, re-measured on this
+    device (the fractions in this line stay against the published figures):
+    HBM as the rate of the runtime's device copy of 1 GiB (bytes read +
+    bytes written over the copy's time), and bf16 matrix throughput as the
+    rate of the vendor GEMM (torch.matmul) on 8192^3, each the best of a few
+    back-to-back batches between HIP events."""
+    n = 1 << 30
+    src = torch.empty(n, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    ka = torch.randn((8192, 8192), device=dev).to(torch.bfloat16)
+    kb = torch.randn((8192, 8192), device=dev).to(torch.bfloat16)
+    kc = torch.matmul(ka, kb)
+    torch.cuda.synchronize()
+
+    def best_ms(fn, reps, tries=5):
+        best = float("inf")
+        for _ in range(tries):
+            a = torch.cuda.Event(enable_timing=True)
+            z = torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fn()
+            z.record()
+            torch.cuda.synchronize()
+            best = min(best, a.elapsed_time(z) / reps)
+        return best
+
+    copy_ms = best_ms(lambda: dst.copy_(src), 10)
+    gemm_ms = best_ms(lambda: torch.matmul(ka, kb, out=kc), 5)
+    hbm = 2.0 * n / (copy_ms * 1e-3) / 1e9
+    tflops = 2.0 * 8192 ** 3 / (gemm_ms * 1e-3) / 1e12
+    del src, dst, ka, kb, kc
+    torch.cuda.synchronize()
+    return {"hbm_copy_GBs": hbm, "hbm_copy_frac_of_published": hbm / HBM_PEAK_GBS,
+            "bf16_gemm_8192_TFLOPs": tflops,
+            "bf16_gemm_frac_of_published": tflops / BF16_PEAK_TFLOPS,
+            "published": {"hbm_GBs": HBM_PEAK_GBS, "bf16_TFLOPs": BF16_PEAK_TFLOPS},
+            "note": "rooflines use the published peaks; these are the device copy and the "
+                    "vendor GEMM on this box"}
+
+
 def gemm_calibration(torch, dev):
     """The Gram stage's contraction at the hi-res and 13B shapes (pruned x
     kept rows, 2 d (N_v - N_1) N_1 flops per sample) done two ways on the
@@ -1142,6 +1185,7 @@ def main():
         "critical_text": crit_text,
         # the method's whole progressive schedule in one call
         "progressive": prog,
+        "measured_peaks": measured_peaks(torch, dev),
         "csrc_digest": csrc_digest(),
     }
     if args.cpu_seconds > 0:
