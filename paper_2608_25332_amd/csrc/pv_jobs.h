@@ -168,7 +168,7 @@ __device__ __forceinline__ void gram_reduce_row(const ReduceJob &j, int m, int b
 // Rows of gram_reduce_row per carried workgroup (one per wave of 256).
 constexpr int kReduceRowsPerBlock = 4;
 
-// ---- head-aware score: v and the top-N_2 (Eq. v, Sec. 4.2) ---------------
+// ---- head-aware score: v and the top-N_2 (Eq. v, Sec. 4.4) ---------------
 constexpr int kSelU = 16;
 
 struct SelectJob {
@@ -181,36 +181,59 @@ struct SelectJob {
     int nblocks;           // samples carried by another launch; 0: none
 };
 
-// Workgroup of NT threads, sample b: v[j] = inv_norm x the partials of column
-// j added in part order, then the top-budget of v (lower index first among
-// equal scores), ascending.
+// inv_norm x the partials of column j added in part order, loaded in blocks
+// of kSelU with clamped addresses (all loads of a block in flight).
+template <int NT, int EMAX>
+__device__ __forceinline__ float select_sum(const SelectJob &sj, const float *pb, int j) {
+    const int N = sj.N, nparts = sj.nparts;
+    float s = 0.f;
+    for (int t0 = 0; t0 < nparts; t0 += kSelU) {
+        float v[kSelU];
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u) v[u] = pb[(size_t)min(t0 + u, nparts - 1) * N + j];
+#pragma unroll
+        for (int u = 0; u < kSelU; ++u)
+            if (t0 + u < nparts) s += v[u];
+    }
+    return s * sj.inv_norm;
+}
+
+// Workgroup of NT threads, sample b: v[j] = select_sum for every column, then
+// the top-budget of v (lower index first among equal scores), ascending.
 template <int NT, int EMAX>
 __device__ __forceinline__ void score_select_block(const SelectJob &sj, int b) {
     __shared__ TopkSmem sm;
     const int N = sj.N, nparts = sj.nparts;
     const float *pb = sj.partial + (size_t)b * nparts * N;
     float *vb = sj.v + (size_t)b * N;
-    const int E = topk_per_thread(N, NT), j0 = threadIdx.x * E;
+    const int E = topk_per_thread(N, NT), t = threadIdx.x;
     uint32_t key[EMAX];
+    if constexpr (EMAX == 1) {
+        key[0] = 0u;
+        if (E == 1 && t < N) {
+            const float s = select_sum<NT, EMAX>(sj, pb, t);
+            vb[t] = s;
+            key[0] = order_key(s);
+        }
+    } else {
+        // the sums with the columns spread over the lanes (each load of a
+        // part then covers contiguous columns), handed to block_topk's
+        // ownership (E consecutive columns per thread) through LDS
+        __shared__ float vs[EMAX * NT];
 #pragma unroll
-    for (int e = 0; e < EMAX; ++e) {
-        const int j = j0 + e;
-        key[e] = 0u;
-        if (e < E && j < N) {
-            // partials in blocks of kSelU with clamped addresses (all loads of a
-            // block in flight), added in part order
-            float s = 0.f;
-            for (int t0 = 0; t0 < nparts; t0 += kSelU) {
-                float v[kSelU];
-#pragma unroll
-                for (int u = 0; u < kSelU; ++u) v[u] = pb[(size_t)min(t0 + u, nparts - 1) * N + j];
-#pragma unroll
-                for (int u = 0; u < kSelU; ++u)
-                    if (t0 + u < nparts) s += v[u];
+        for (int e = 0; e < EMAX; ++e) {
+            const int j = t + e * NT;
+            if (e < E && j < N) {
+                const float s = select_sum<NT, EMAX>(sj, pb, j);
+                vb[j] = s;
+                vs[j] = s;
             }
-            s *= sj.inv_norm;
-            vb[j] = s;
-            key[e] = order_key(s);
+        }
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < EMAX; ++e) {
+            const int j = t * E + e;
+            key[e] = (e < E && j < N) ? order_key(vs[j]) : 0u;
         }
     }
     block_topk<NT, EMAX>(key, N, sj.budget, sj.kept + (size_t)b * sj.budget, nullptr, nullptr, sm);
