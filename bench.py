@@ -203,15 +203,16 @@ STAGE_OF = {
 
 
 # kernel of the shared-launch step (pv_prune_pipeline_timed's name) -> the
-# two kernels of the separate step whose work it does
-SHARED_PARTS = {"gram_partial+gather_kv1": ("gram_partial", "gather_kv1"),
-                "score_partial+gram_reduce": ("score_partial", "gram_reduce"),
-                "merge+score_select": ("merge", "score_select")}
+# kernels of the separate step whose work it does
+SHARED_PARTS = {"gram_partial+score_partial": ("gram_partial", "score_partial"),
+                "gram_reduce+score_select+gather_kv1": ("gram_reduce", "score_select",
+                                                        "gather_kv1"),
+                "merge+gather_hkv2": ("merge", "gather_hkv2")}
 # kernel name in bench.py -> the name rocprofv3 reports (without "_kernel" and
 # template arguments), which keys the committed counter summaries
-PROFILED_NAME = {"gram_partial+gather_kv1": "gram_partial_gather",
-                 "score_partial+gram_reduce": "score_partial_reduce",
-                 "merge+score_select": "merge", "gather_kv1": "gather", "gather_hkv2": "gather"}
+PROFILED_NAME = {"gram_partial+score_partial": "gram_score",
+                 "gram_reduce+score_select+gather_kv1": "reduce_select_gather",
+                 "merge+gather_hkv2": "merge", "gather_kv1": "gather", "gather_hkv2": "gather"}
 
 
 def algorithmic(w):
@@ -256,10 +257,13 @@ def algorithmic(w):
         # read + write the hidden, K and V rows of the N2 kept tokens
         "gather_hkv2": dict(bytes=2 * B * N2 * (d + 2 * H * hd) * e, flops=0.0),
     }
-    # kernels of the shared-launch step: each carries the work of two
-    for a, b in SHARED_PARTS.values():
-        kern[a + "+" + b] = dict(bytes=kern[a]["bytes"] + kern[b]["bytes"],
-                                 flops=kern[a]["flops"] + kern[b]["flops"])
+    # kernels of the shared-launch step: each does the work of its parts
+    for parts in SHARED_PARTS.values():
+        kern["+".join(parts)] = dict(bytes=sum(kern[p]["bytes"] for p in parts),
+                                     flops=sum(kern[p]["flops"] for p in parts))
+    # the merge writes the kept slots' rows to their compacted places itself:
+    # the compaction reads no merged row
+    kern["merge+gather_hkv2"]["bytes"] -= B * N2 * d * e
     stage = {
         "cosine": dict(bytes=B * (Nv + Nt) * d * e + B * Nv * 4, flops=2.0 * B * Nt * Nv * d),
         "select": kern["select"],

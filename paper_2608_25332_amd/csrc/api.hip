@@ -949,13 +949,14 @@ PV_API int pv_prune_gather(const void *src, void *dst, const int32_t *idx, int B
 namespace {
 
 struct PipeSizes {
-    size_t dedup, head, total;
+    size_t dedup, head, slots, total;
 };
 
 PipeSizes pipe_sizes(int B, int Nv, int Nt, int d, int H, int hd, int esz, int N1, int n_heads) {
     const size_t D = round_up(dedup_total_bytes(B, Nv, Nt, d, esz, N1, false, false, true));
-    const size_t Hh = head_total_bytes(B, H, Nt, N1, hd, esz, n_heads, false);
-    return PipeSizes{D, Hh, D + Hh};
+    const size_t Hh = round_up(head_total_bytes(B, H, Nt, N1, hd, esz, n_heads, false));
+    const size_t S = round_up((size_t)B * N1 * sizeof(int32_t));  // each slot's place among the N_2
+    return PipeSizes{D, Hh, S, D + Hh + S + kAlign};
 }
 
 pv_gather_desc kv_desc(const void *src, void *dst, int H, int n_src, int k, int64_t row) {
@@ -1002,22 +1003,26 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
                                   kv_desc(v_full, v1, H, Nv, N1, row_kv)};
     pv_gather_desc g2[3] = {kv_desc(merged, hidden2, 1, N1, N2, row_h),
                             kv_desc(k1, k2, H, N1, N2, row_kv), kv_desc(v1, v2, H, N1, N2, row_kv)};
-    pv::GatherArgs ga1, ga2;
+    pv::GatherArgs ga1, ga2, ga2kv;
     if ((rc = make_gather(g1, 2, kept1, B, N1, ga1)) != PV_OK) return rc;
     if ((rc = make_gather(g2, 3, kept2, B, N2, ga2)) != PV_OK) return rc;
+    if ((rc = make_gather(g2 + 1, 2, kept2, B, N2, ga2kv)) != PV_OK) return rc;
     hipStream_t st = (hipStream_t)stream;
     Trace tr{events, n_events, names, reps, st};
     if (!tr.handles_ok()) return PV_ERR_NULL;
     char *wsa = (char *)(((uintptr_t)workspace + kAlign - 1) / kAlign * kAlign);
     char *ws_head = wsa + sz.dedup;
+    int32_t *slot_of2 = (int32_t *)(ws_head + sz.head);
 
     const DedupPlan P = plan_dedup(wsa, B, Nv, Nt, d, esz, N1, false, false, true);
     const int dt = (dtype == PV_BF16) ? pv::kBF16 : pv::kF32;
     // the two chains after the top-N_1 share launches when the dedup takes
     // the split-k Gram and the plain merge, and the score its 16-row blocks
+    // with every logit in registers (the same kernels' arithmetic as the
+    // separate calls, so the same bits)
     const bool carry = !force_separate && padded_d(d, esz) == d && padded_hd(hd) == hd &&
                        P.Mp > 0 && !P.gram_big && !P.lists && N1 <= 256 &&
-                       pv::score_can_carry_reduce(dt, hd) &&
+                       pv::gram_score_supported(dt, B, n_heads, N1, hd) &&
                        !pv::score_uses_head_form(dt, B, H, n_heads, Nt, N1, hd) &&
                        !pv::score_uses_split_form(dt, B, H, n_heads, Nt, N1, hd);
     if (!carry) {
@@ -1036,34 +1041,35 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
     if (!launch_front(tr, P, dt, vis, anchors, nullptr, B, Nv, Nt, d, N1, score1, kept1, assign,
                       st))
         return PV_ERR_HIP;
-    // Gram partials + the K/V rows of the kept tokens
-    pv::GatherJob gj;
-    gj.ga = ga1;
-    gj.idx = kept1;
-    gj.k = N1;
-    gj.nblocks = ga1.bstart[ga1.n];
-    if (!tr.launch("gram_partial+gather_kv1", [&] {
-            return pv::launch_gram_partial(dt, vis, B, Nv, d, kept1, N1, P.pruned, P.Mp,
-                                           P.ks_gram, P.gpart, st, &gj);
+    // score blocks on the keys of the kept tokens + Gram partials
+    const int ntm = (P.Mp + pv::kSplitTile - 1) / pv::kSplitTile;
+    const int ntn = (N1 + pv::kSplitTile - 1) / pv::kSplitTile;
+    const pv::GramJob gram{(const char *)vis, B,      Nv,  d * esz,   kept1,  N1,
+                           P.pruned,          P.Mp,   ntm, ntn,       P.ks_gram, P.gpart,
+                           B * P.ks_gram * ntm * ntn};
+    if (!tr.launch("gram_partial+score_partial", [&] {
+            return pv::launch_gram_score(dt, q, k_full, heads, B, H, Nt, N1, Nv, kept1, hd,
+                                         n_heads, Hh.partial, gram, st);
         }))
         return PV_ERR_HIP;
-    // score blocks + the Gram's argmax
+    // the score's top-N_2 + the Gram's argmax + the K/V rows of the N_1 kept
+    const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
     const pv::ReduceJob rj{P.gpart, B, P.Mp, N1, Nv, P.ks_gram, P.invn, P.pruned, kept1, assign,
                            B * ((P.Mp + pv::kReduceRowsPerBlock - 1) / pv::kReduceRowsPerBlock)};
-    if (!tr.launch("score_partial+gram_reduce", [&] {
-            return pv::launch_score_partial(dt, q, k1, heads, nullptr, nullptr, B, H, Nt, N1, hd,
-                                            hd, n_heads, Hh.partial, Hh.stats, st, &rj);
+    const pv::SelectJob sj{Hh.partial, n_heads * Hh.nrb, N1, inv_norm, score2, N2, kept2, B,
+                           slot_of2};
+    const pv::GatherJob gj1{ga1, kept1, N1, ga1.bstart[ga1.n]};
+    if (!tr.launch("gram_reduce+score_select+gather_kv1", [&] {
+            return pv::launch_reduce_select_gather(rj, sj, gj1, st);
         }))
         return PV_ERR_HIP;
-    // merge + the score's top-N_2
-    const float inv_norm = (float)(1.0 / ((double)Nt * (double)n_heads));
-    const pv::SelectJob sj{Hh.partial, n_heads * Hh.nrb, N1, inv_norm, score2, N2, kept2, B};
-    if (!tr.launch("merge+score_select", [&] {
-            return pv::launch_merge(dt, vis, B, Nv, d, N1, assign, merged, st, &sj);
+    // merge, with the merged rows of the N_2 kept slots written to their
+    // compacted places, + K and V of the N_2 kept
+    const pv::MergeCarry mc{slot_of2, (char *)hidden2, N2,
+                            pv::GatherJob{ga2kv, kept2, N2, ga2kv.bstart[ga2kv.n]}};
+    if (!tr.launch("merge+gather_hkv2", [&] {
+            return pv::launch_merge(dt, vis, B, Nv, d, N1, assign, merged, st, &mc);
         }))
-        return PV_ERR_HIP;
-    // merged hidden rows, K and V of the N_2 kept tokens
-    if (!tr.launch("gather_hkv2", [&] { return pv::launch_gather(ga2, kept2, B, N2, st); }))
         return PV_ERR_HIP;
     if (!tr.after_all()) return PV_ERR_HIP;
     if (n_kernels) *n_kernels = tr.launched;

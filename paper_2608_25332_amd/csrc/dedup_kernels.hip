@@ -30,20 +30,6 @@
 
 namespace pv {
 
-// ----------------------------------------------------------------------------
-// Split-k products (the cosine, and the Grams that are too small to fill the
-// chip with full-k tiles).
-//
-// A workgroup owns a 64 x 64 output tile and one k slice of its rows (streamed
-// into LDS, see pv_tile_lds.h); the k slices are added in slice order by the
-// reduce kernels.  Slicing k spreads a B=1 problem over every CU while each
-// CU fetches only a few tens of KB; the price is KS fp32 partial tiles, which
-// stay in L2.
-// ----------------------------------------------------------------------------
-constexpr int kPT = 64;  // tile edge of the split-k products
-template <int DT, int NS>
-using PTile = TileGemmLds<DT, kPT, kPT, 2, 2, NS>;
-
 // cos_partial: 1-D grid over (sample, k slice, anchor tile, token tile) in XCD
 // order (token tiles of one anchor tile and slice are adjacent: they share the
 // anchor rows).  Writes partial dot products part[ks][b][Nt][Nv] and partial
@@ -418,75 +404,13 @@ __global__ __launch_bounds__(kFinNT) void gram_finish_kernel(const float *__rest
     assign[(size_t)b * Nv + pruned[(size_t)b * Mp + m]] = bs;
 }
 
-// gram_partial: 1-D grid over (sample, k slice, kept tile, pruned tile) in
-// XCD order (pruned tiles of one kept tile and slice are adjacent: they share
-// the kept rows).  Writes partial dot products part[ks][b][Mp][N1].
-template <int DT, int NS>
-__device__ __forceinline__ void gram_partial_tile(const char *__restrict__ vis, int B, int Nv,
-                                                  int d_bytes, const int32_t *__restrict__ kept,
-                                                  int N1, const int32_t *__restrict__ pruned,
-                                                  int Mp, int ntm, int ntn, int KS,
-                                                  float *__restrict__ part, int total) {
-    using G = PTile<DT, NS>;
-    __shared__ int32_t rowtok[G::ROWS];
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave / 2, wn = wave % 2;
-    const int tile = xcd_tile(blockIdx.x, total);
-    const int mt = tile % ntm;
-    const int nt = (tile / ntm) % ntn;
-    const int ks = (tile / (ntm * ntn)) % KS;
-    const int b = tile / (ntm * ntn * KS);
-    const int m0 = mt * kPT, n0 = nt * kPT;
-    const int32_t *pr = pruned + (size_t)b * Mp;
-    const int32_t *kp = kept + (size_t)b * N1;
-    for (int r = tid; r < G::ROWS; r += G::NT)
-        rowtok[r] = (r < kPT) ? pr[min(m0 + r, Mp - 1)] : kp[min(n0 + r - kPT, N1 - 1)];
-    __syncthreads();
-    const char *vbase = vis + (size_t)b * Nv * d_bytes;
-    auto row_ptr = [&](int r) -> const char * { return vbase + (size_t)rowtok[r] * d_bytes; };
-    const int nch = d_bytes / G::CHUNK;
-    const int c0 = (int)(((long long)nch * ks) / KS), c1 = (int)(((long long)nch * (ks + 1)) / KS);
-    f32x4_t acc[G::FM][G::FN];
-    float sa[G::FM], sb[G::FN];
-    G::template run<false>(row_ptr, c0, c1, acc, sa, sb);
-    float *pb = part + ((size_t)ks * B + b) * Mp * N1;
-#pragma unroll
-    for (int fm = 0; fm < G::FM; ++fm)
-#pragma unroll
-        for (int fn = 0; fn < G::FN; ++fn) {
-            const int n = n0 + wn * G::SUB_N + fn * 16 + (lane & 15);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int m = m0 + wm * G::SUB_M + fm * 16 + (lane >> 4) * 4 + e;
-                if (m < Mp && n < N1) pb[(size_t)m * N1 + n] = acc[fm][fn][e];
-            }
-        }
-}
-
 template <int DT, int NS>
 __global__ __launch_bounds__(256) void gram_partial_kernel(
     const char *__restrict__ vis, int B, int Nv, int d_bytes, const int32_t *__restrict__ kept,
     int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn, int KS,
     float *__restrict__ part) {
     gram_partial_tile<DT, NS>(vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS, part,
-                              B * KS * ntn * ntm);
-}
-
-// The same with a gather carried by the workgroups past the tiles (a kernel
-// of its own: the job's arguments would slow the plain form down).
-template <int DT, int NS>
-__global__ __launch_bounds__(256) void gram_partial_gather_kernel(
-    const char *__restrict__ vis, int B, int Nv, int d_bytes, const int32_t *__restrict__ kept,
-    int N1, const int32_t *__restrict__ pruned, int Mp, int ntm, int ntn, int KS,
-    float *__restrict__ part, GatherJob gj) {
-    const int total = B * KS * ntn * ntm;
-    if ((int)blockIdx.x >= total) {
-        gather_block(gj.ga, gj.idx, gj.k, blockIdx.x - total);
-        return;
-    }
-    gram_partial_tile<DT, NS>(vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS, part,
-                              total);
+                              B * KS * ntn * ntm, blockIdx.x);
 }
 
 // gram_reduce: grid (ceil(Mp / 2), B), 128 threads, one wave per pruned row
@@ -624,7 +548,8 @@ __device__ __forceinline__ void add16(float (&acc)[DT == kBF16 ? 8 : 4], uint4 v
 template <int DT, int NW>
 __device__ __forceinline__ void merge_finish(float (&acc)[DT == kBF16 ? 8 : 4],
                                              float (&part)[NW][DT == kBF16 ? 8 : 4][64], int wave,
-                                             int lane, int c, int nchunk, int total, char *out) {
+                                             int lane, int c, int nchunk, int total, char *out,
+                                             char *out2 = nullptr) {
     constexpr int EPC = (DT == kBF16) ? 8 : 4;
     if (wave > 0) {
 #pragma unroll
@@ -647,6 +572,7 @@ __device__ __forceinline__ void merge_finish(float (&acc)[DT == kBF16 ? 8 : 4],
             for (int q = 0; q < 4; ++q) w4[q] = __float_as_uint(acc[q] / cntf);
         }
         st16(out + (size_t)c * 16, uint4{w4[0], w4[1], w4[2], w4[3]});
+        if (out2) st16(out2 + (size_t)c * 16, uint4{w4[0], w4[1], w4[2], w4[3]});
     }
 }
 
@@ -655,18 +581,25 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
                                                          int d_bytes,
                                                          const int32_t *__restrict__ assign,
                                                          int N1, char *__restrict__ merged,
-                                                         SelectJob sj) {
+                                                         MergeCarry mc) {
     constexpr int EPC = (DT == kBF16) ? 8 : 4;  // elements per 16-byte chunk
     constexpr int NW = kMergeNT / 64;
     __shared__ int list[kMergeRound];
     __shared__ int wsum[NW];
     __shared__ float part[NW][EPC][64];
     const int bx = blockIdx.x, s = blockIdx.y, b = blockIdx.z;
-    // a carried score selection takes one more row of slots: workgroup
-    // (0, N1, b) runs sample b's, the rest of that row has nothing to do
+    // a carried compaction takes more rows of slots in sample 0's plane of
+    // the grid: workgroup (x, N1 + r, 0) runs its block r * gridDim.x + x
     if (s >= N1) {
-        if (bx == 0 && b < sj.nblocks) score_select_block<kMergeNT, 1>(sj, b);
+        const int g = (s - N1) * (int)gridDim.x + bx;
+        if (b == 0 && g < mc.gj.nblocks) gather_block(mc.gj.ga, mc.gj.idx, mc.gj.k, g);
         return;
+    }
+    // the slot's row among the N_2 kept, when the head-aware top-N_2 kept it
+    char *out2 = nullptr;
+    if (mc.slot_of2) {
+        const int pos = mc.slot_of2[(size_t)b * N1 + s];
+        if (pos >= 0) out2 = mc.hidden2 + ((size_t)b * mc.N2 + pos) * d_bytes;
     }
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -711,7 +644,7 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
         __syncthreads();  // the list is rewritten by the next round
     }
     merge_finish<DT, NW>(acc, part, wave, lane, c, nchunk, total,
-                         merged + ((size_t)b * N1 + s) * d_bytes);
+                         merged + ((size_t)b * N1 + s) * d_bytes, out2);
 }
 
 // ----------------------------------------------------------------------------
@@ -956,11 +889,6 @@ __global__ __launch_bounds__(256) void cos_reduce4_kernel(
 // ----------------------------------------------------------------------------
 // launchers
 // ----------------------------------------------------------------------------
-// Ring depth of the split-k tiles: three 16 KB stages.  Measured: a deeper
-// ring costs more (fewer workgroups fit a CU) than the extra loads in flight
-// gain.
-constexpr int kSplitNS = 3;
-
 template <int DT, int NS, int BT>
 static void cos_partial_go(const void *vis, const void *anchors, int B, int Nv, int Nt,
                            int d_bytes, int KS, float *part, float *ssv, float *ssa,
@@ -1077,32 +1005,20 @@ static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int3
     return hipGetLastError();
 }
 
-template <int DT, int NS>
-static void gram_partial_go(dim3 grid, const void *vis, int B, int Nv, int d_bytes,
-                            const int32_t *kept, int N1, const int32_t *pruned, int Mp, int ntm,
-                            int ntn, int KS, float *part, const GatherJob *gj, hipStream_t st) {
-    if (gj)
-        hipLaunchKernelGGL((gram_partial_gather_kernel<DT, NS>), grid, dim3(256), 0, st,
-                           (const char *)vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS,
-                           part, *gj);
-    else
-        hipLaunchKernelGGL((gram_partial_kernel<DT, NS>), grid, dim3(256), 0, st,
-                           (const char *)vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS,
-                           part);
-}
-
 hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                                int N1, const int32_t *pruned, int Mp, int KS, float *part,
-                               hipStream_t st, const GatherJob *with) {
+                               hipStream_t st) {
     const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
     const int ntm = (Mp + kPT - 1) / kPT, ntn = (N1 + kPT - 1) / kPT;
-    const dim3 grid(B * KS * ntm * ntn + (with ? with->nblocks : 0));
+    const dim3 grid(B * KS * ntm * ntn);
     if (dt == kBF16)
-        gram_partial_go<kBF16, kSplitNS>(grid, vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn,
-                                         KS, part, with, st);
+        hipLaunchKernelGGL((gram_partial_kernel<kBF16, kSplitNS>), grid, dim3(256), 0, st,
+                           (const char *)vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS,
+                           part);
     else
-        gram_partial_go<kF32, kSplitNS>(grid, vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn,
-                                        KS, part, with, st);
+        hipLaunchKernelGGL((gram_partial_kernel<kF32, kSplitNS>), grid, dim3(256), 0, st,
+                           (const char *)vis, B, Nv, d_bytes, kept, N1, pruned, Mp, ntm, ntn, KS,
+                           part);
     return hipGetLastError();
 }
 
@@ -1171,26 +1087,27 @@ hipError_t launch_merge_csr(int dt, const void *vis, int B, int Nv, int d, int N
 }
 
 hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
-                        const int32_t *assign, void *merged, hipStream_t st, const SelectJob *with) {
+                        const int32_t *assign, void *merged, hipStream_t st,
+                        const MergeCarry *with) {
     const int d_bytes = d * ((dt == kBF16) ? 2 : 4);
-    SelectJob sj;
+    MergeCarry mc;
     if (with) {
-        // the carried selection runs on the merge's 256 threads, one key each
-        if (with->N > kMergeNT) return hipErrorInvalidValue;
-        sj = *with;
+        mc = *with;
+        if (mc.slot_of2 && (!mc.hidden2 || mc.N2 < 1)) return hipErrorInvalidValue;
     } else {
-        memset(&sj, 0, sizeof(sj));
+        memset(&mc, 0, sizeof(mc));
     }
     // (measured: the same work on a 1-D grid with the coordinates decoded in
     // the kernel is 15% slower at B = 1)
-    if (sj.nblocks != 0 && sj.nblocks != B) return hipErrorInvalidValue;
-    const dim3 grid((d_bytes / 16 + 63) / 64, N1 + (sj.nblocks ? 1 : 0), B);
+    const int gx = (d_bytes / 16 + 63) / 64;
+    const int extra = (mc.gj.nblocks + gx - 1) / gx;  // rows of slots for the carried blocks
+    const dim3 grid(gx, N1 + extra, B);
     if (dt == kBF16)
         hipLaunchKernelGGL(merge_kernel<kBF16>, grid, dim3(kMergeNT), 0, st, (const char *)vis, Nv,
-                           d * 2, assign, N1, (char *)merged, sj);
+                           d * 2, assign, N1, (char *)merged, mc);
     else
         hipLaunchKernelGGL(merge_kernel<kF32>, grid, dim3(kMergeNT), 0, st, (const char *)vis, Nv,
-                           d * 4, assign, N1, (char *)merged, sj);
+                           d * 4, assign, N1, (char *)merged, mc);
     return hipGetLastError();
 }
 

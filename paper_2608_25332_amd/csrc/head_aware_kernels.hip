@@ -71,21 +71,26 @@ enum HeadSource { kHeadsArg = 0, kHeadsDevice = 1, kHeadsAll = 2 };
 // one pass only, also carrying the sum of squared probabilities of each row,
 // and one number per workgroup: the sum over its rows of the row variance
 // (the head confidence of this row block).
-// Score kernels that can carry the split-k Gram's argmax (ReduceJob): the
-// 256-byte head rows, whose occupancy is set by LDS, so the argmax's
-// registers cost nothing there.
-constexpr bool score_carries_reduce(int nks, bool conf) { return nks == 4 && !conf; }
 
 // One score workgroup; n_score: workgroups of the launch that score.
-template <int DT, int NKS, int MAXC, bool CONF>
+// IDX: key j of the head is row kidx[b][j] of k ([B][H][n_src][hd], the keys
+// of every token; kidx[b] holds N indices), so the score needs no compacted
+// copy of the kept keys; the ring is then `ext_ring` (S::NS * S::STAGE bytes
+// of LDS, shared with the other workgroups of the launch).  N <= 256.
+template <int DT, int NKS, int MAXC, bool CONF, bool IDX = false>
 __device__ __forceinline__ void score_partial_block(
     const char *__restrict__ q, const char *__restrict__ k, const HeadArgs &heads,
     const int32_t *__restrict__ heads_dev, int head_src, const int32_t *__restrict__ row_mask,
     const float *__restrict__ row_lse, int b0, int H, int Nt, int N, int n_heads,
-    float scale_log2e, float *__restrict__ partial, int cols_in_lds, int n_score) {
+    float scale_log2e, float *__restrict__ partial, int cols_in_lds, int n_score,
+    const int32_t *__restrict__ kidx = nullptr, int n_src = 0, char *ext_ring = nullptr) {
     static_assert(!CONF || MAXC == 0, "the confidence needs no second pass");
+    static_assert(!IDX || (!CONF && MAXC > 0 && MAXC * kScoreCK <= 256),
+                  "indexed keys: one pass, at most 256 keys");
     using S = ScoreStage<NKS>;
-    __shared__ __attribute__((aligned(16))) char ring[S::NS][S::STAGE];
+    __shared__ __attribute__((aligned(16))) char own_ring[IDX ? 16 : S::NS * S::STAGE];
+    __shared__ int32_t krow[IDX ? 256 : 1];  // IDX: the source row of every key
+    char *const ring = IDX ? ext_ring : own_ring;
     __shared__ __attribute__((aligned(16))) char qrows[16 * S::RB];
     __shared__ float sm_m[4][16], sm_l[4][16], sm_s[CONF ? 4 : 1][16];
     __shared__ float row_m[16], row_il[16];
@@ -102,7 +107,14 @@ __device__ __forceinline__ void score_partial_block(
     else if (head_src == kHeadsDevice) h = min(max(heads_dev[(size_t)b * n_heads + hi], 0), H - 1);
     else h = heads.h[bl * n_heads + hi];
     const char *qb = q + ((size_t)b * H + h) * Nt * S::RB;
-    const char *kb = k + ((size_t)b * H + h) * N * S::RB;
+    const char *kb = k + ((size_t)b * H + h) * (IDX ? n_src : N) * S::RB;
+    if constexpr (IDX) {
+        // ordinary loads, all retired at the barrier: the ring's loads below
+        // are then the only ones in flight (see the ordering note)
+        for (int j = tid; j < N; j += kScoreNT)
+            krow[j] = min(max(kidx[(size_t)b * N + j], 0), n_src - 1);
+        __syncthreads();
+    }
 
     const int nch = (N + kScoreCK - 1) / kScoreCK;
     uint4 qf[NKS];  // the 16 query rows as MFMA fragments
@@ -117,10 +129,11 @@ __device__ __forceinline__ void score_partial_block(
         sbyte[t] = (slot ^ (r & S::SWZ)) << 4;
     }
     auto issue = [&](int ch) {
-        char *dst = ring[ch % S::NS] + wave * S::IPW * 1024;
+        char *dst = ring + (ch % S::NS) * S::STAGE + wave * S::IPW * 1024;
 #pragma unroll
         for (int t = 0; t < S::IPW; ++t) {
-            const int row = min(ch * kScoreCK + srow[t], N - 1);  // past the end: last key
+            const int key = min(ch * kScoreCK + srow[t], N - 1);  // past the end: last key
+            const int row = IDX ? krow[key] : key;
             lds_dma16(kb + (size_t)row * S::RB + sbyte[t], dst + t * 1024);
         }
     };
@@ -173,7 +186,7 @@ __device__ __forceinline__ void score_partial_block(
         bare_barrier();  // chunk ch is in LDS; chunk ch - 1 has been read
         if (ch >= 1 && ch + S::NS - 1 < nch) issue(ch + S::NS - 1);
         if (ch == 0) read_q();
-        const char *sp = ring[ch % S::NS];
+        const char *sp = ring + (ch % S::NS) * S::STAGE;
         const int r = wave * 16 + (lane & 15);
         uint4 kf[NKS];
 #pragma unroll
@@ -443,29 +456,6 @@ __global__ __launch_bounds__(kScoreNT) void score_partial_kernel(
     score_partial_block<DT, NKS, MAXC, CONF>(q, k, heads, heads_dev, head_src, row_mask, row_lse,
                                              b0, H, Nt, N, n_heads, scale_log2e, partial,
                                              cols_in_lds, gridDim.x);
-}
-
-// The same with the split-k Gram's argmax carried by the workgroups past the
-// score blocks, one pruned row per wave (a kernel of its own: the job slows
-// the plain form down).
-template <int DT, int NKS, int MAXC>
-__global__ __launch_bounds__(kScoreNT) void score_partial_reduce_kernel(
-    const char *__restrict__ q, const char *__restrict__ k, HeadArgs heads,
-    const int32_t *__restrict__ heads_dev, int head_src, const float *__restrict__ row_lse,
-    int b0, int H, int Nt, int N, int n_heads, float scale_log2e, float *__restrict__ partial,
-    int cols_in_lds, ReduceJob rj) {
-    static_assert(kScoreNT / 64 == kReduceRowsPerBlock, "one carried Gram row per wave");
-    const int n_score = (int)gridDim.x - rj.nblocks;
-    if ((int)blockIdx.x >= n_score) {
-        const int v = blockIdx.x - n_score;
-        const int per = (rj.Mp + kReduceRowsPerBlock - 1) / kReduceRowsPerBlock;
-        const int m = (v % per) * kReduceRowsPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-        if (m < rj.Mp) gram_reduce_row<16>(rj, m, v / per, threadIdx.x & 63);
-        return;
-    }
-    score_partial_block<DT, NKS, MAXC, false>(q, k, heads, heads_dev, head_src, nullptr, row_lse,
-                                              b0, H, Nt, N, n_heads, scale_log2e, partial,
-                                              cols_in_lds, n_score);
 }
 
 // ----------------------------------------------------------------------------
@@ -878,7 +868,6 @@ struct ScoreLaunch {
     float *partial;
     hipStream_t st;
     int hd_scale = 0;  // head width of the attention scale (0: the row width)
-    const ReduceJob *rj = nullptr;  // carried by the first launch (score only)
 };
 
 // A host head list travels as a kernel argument of bounded size: a launch
@@ -900,28 +889,11 @@ static hipError_t score_go(const ScoreLaunch &a) {
         for (int i = 0; i < kMaxHeadArgs; ++i)
             ha.h[i] = (a.src == kHeadsArg && i < nb * a.n_heads)
                           ? a.heads_host[(size_t)b0 * a.n_heads + i] : 0;
-        ReduceJob rj;
-        if (a.rj && b0 == 0) {
-            rj = *a.rj;
-        } else {
-            memset(&rj, 0, sizeof(rj));
-        }
-        dim3 grid(nrb * a.n_heads * nb + rj.nblocks);
-        bool carried = false;
-        if constexpr (score_carries_reduce(NKS, CONF)) {
-            if (rj.nblocks > 0) {
-                hipLaunchKernelGGL((score_partial_reduce_kernel<DT, NKS, MAXC>), grid,
-                                   dim3(kScoreNT), in_lds ? cols : 0, a.st, (const char *)a.q,
-                                   (const char *)a.k, ha, a.heads_dev, a.src, a.row_lse, b0, a.H,
-                                   a.Nt, a.N, a.n_heads, a.sl2e, a.partial, in_lds ? 1 : 0, rj);
-                carried = true;
-            }
-        }
-        if (!carried)
-            hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC, CONF>), grid, dim3(kScoreNT),
-                               in_lds ? cols : 0, a.st, (const char *)a.q, (const char *)a.k, ha,
-                               a.heads_dev, a.src, a.row_mask, a.row_lse, b0, a.H, a.Nt, a.N,
-                               a.n_heads, a.sl2e, a.partial, in_lds ? 1 : 0);
+        dim3 grid(nrb * a.n_heads * nb);
+        hipLaunchKernelGGL((score_partial_kernel<DT, NKS, MAXC, CONF>), grid, dim3(kScoreNT),
+                           in_lds ? cols : 0, a.st, (const char *)a.q, (const char *)a.k, ha,
+                           a.heads_dev, a.src, a.row_mask, a.row_lse, b0, a.H, a.Nt, a.N,
+                           a.n_heads, a.sl2e, a.partial, in_lds ? 1 : 0);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -1066,22 +1038,16 @@ int score_parts(int dt, int B, int H, int n_heads, int Nt, int N, int hd) {
     return (Nt + 15) / 16;
 }
 
-bool score_can_carry_reduce(int dt, int hd) {
-    return score_carries_reduce(hd * ((dt == kBF16) ? 2 : 4) / 64, false);
-}
-
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, const float *row_lse, int B, int H,
                                 int Nt, int N, int hd, int hd_scale, int n_heads, float *partial,
-                                float *split_stats, hipStream_t st, const ReduceJob *with) {
+                                float *split_stats, hipStream_t st) {
     ScoreLaunch a{q, k, heads_host, heads_dev, heads_dev ? kHeadsDevice : kHeadsArg, nullptr,
                   row_lse, B, H, Nt, N, n_heads, 0.f, partial, st};
-    a.rj = with;
     a.hd_scale = hd_scale;
     const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
-    if (with && !score_carries_reduce(nks, false)) return hipErrorInvalidValue;
     if (score_uses_split_form(dt, B, H, n_heads, Nt, N, hd)) {
-        if (with || !split_stats) return hipErrorInvalidValue;  // the split form carries nothing
+        if (!split_stats) return hipErrorInvalidValue;
         a.sl2e = scale_log2e_of(a, hd);
         float2 *stats = reinterpret_cast<float2 *>(split_stats);
         if (dt == kBF16)
@@ -1089,7 +1055,6 @@ hipError_t launch_score_partial(int dt, const void *q, const void *k, const int3
         return nks == 2 ? score_split_go<kF32, 2>(a, stats) : score_split_go<kF32, 4>(a, stats);
     }
     if (score_uses_head_form(dt, B, H, n_heads, Nt, N, hd)) {
-        if (with) return hipErrorInvalidValue;  // the whole-head form carries nothing
         a.sl2e = scale_log2e_of(a, hd);
         if (dt == kBF16) return nks == 2 ? score_head_go<kBF16, 2>(a) : score_head_go<kBF16, 4>(a);
         return nks == 2 ? score_head_go<kF32, 2>(a) : score_head_go<kF32, 4>(a);
@@ -1104,6 +1069,110 @@ hipError_t launch_head_conf(int dt, const void *q, const void *k, const int32_t 
                   partial, st};
     a.hd_scale = hd_scale;
     return score_any<true>(dt, hd, a);
+}
+
+// ----------------------------------------------------------------------------
+// The launches of the one-call step that follow the top-N_1 at small batches.
+// The two chains after the selection (nearest kept token -> merge, and
+// score -> top-N_2) share launches, so the step is six dependent launches:
+//   gram_score: the head-aware score blocks, reading the keys of the kept
+//     tokens through the kept list (no compacted copy is needed yet), and the
+//     split-k Gram tiles, both on one LDS ring;
+//   reduce_select_gather: the score's top-N_2 (with each slot's place among
+//     the kept), the Gram's argmax (one pruned row per wave) and the
+//     compaction of K and V to the N_1 kept tokens;
+//   then the merge, which also writes the merged rows of the N_2 kept slots
+//   to their compacted places and carries the compaction of their K and V.
+// ----------------------------------------------------------------------------
+template <int DT, int NKS, int MAXC>
+__global__ __launch_bounds__(kScoreNT) void gram_score_kernel(
+    const char *__restrict__ q, const char *__restrict__ k_full, HeadArgs heads, int H, int Nt,
+    int N, int n_src, const int32_t *__restrict__ kidx, int n_heads, float scale_log2e,
+    float *__restrict__ partial, GramJob gj) {
+    using G = PTile<DT, kSplitNS>;
+    using S = ScoreStage<NKS>;
+    constexpr int RING = G::LDS_BYTES > S::NS * S::STAGE ? G::LDS_BYTES : S::NS * S::STAGE;
+    __shared__ __attribute__((aligned(16))) char ring[RING];
+    // the score blocks first: they are the longer ones
+    const int n_score = (int)gridDim.x - gj.nblocks;
+    if ((int)blockIdx.x >= n_score) {
+        gram_partial_tile<DT, kSplitNS, true>(gj.vis, gj.B, gj.Nv, gj.d_bytes, gj.kept, gj.N1,
+                                              gj.pruned, gj.Mp, gj.ntm, gj.ntn, gj.KS, gj.part,
+                                              gj.nblocks, (int)blockIdx.x - n_score, ring);
+        return;
+    }
+    score_partial_block<DT, NKS, MAXC, false, true>(q, k_full, heads, nullptr, kHeadsArg, nullptr,
+                                                    nullptr, 0, H, Nt, N, n_heads, scale_log2e,
+                                                    partial, 0, n_score, kidx, n_src, ring);
+}
+
+__global__ __launch_bounds__(kScoreNT) void reduce_select_gather_kernel(ReduceJob rj, SelectJob sj,
+                                                                        GatherJob gj) {
+    static_assert(kScoreNT / 64 == kReduceRowsPerBlock, "one Gram row per wave");
+    static_assert(kScoreNT == kGatherNT, "the gather's workgroup size");
+    int blk = blockIdx.x;
+    if (blk < sj.nblocks) {
+        score_select_block<kScoreNT, 1>(sj, blk);
+        return;
+    }
+    blk -= sj.nblocks;
+    if (blk < rj.nblocks) {
+        const int per = (rj.Mp + kReduceRowsPerBlock - 1) / kReduceRowsPerBlock;
+        const int m = (blk % per) * kReduceRowsPerBlock + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        if (m < rj.Mp) gram_reduce_row<16>(rj, m, blk / per, threadIdx.x & 63);
+        return;
+    }
+    blk -= rj.nblocks;
+    if (blk < gj.nblocks) gather_block(gj.ga, gj.idx, gj.k, blk);
+}
+
+bool gram_score_supported(int dt, int B, int n_heads, int N, int hd) {
+    const int nks = hd * ((dt == kBF16) ? 2 : 4) / 64;
+    return nks == 4 && N <= 4 * kScoreCK && (long long)B * n_heads <= kMaxHeadArgs;
+}
+
+template <int DT, int MAXC>
+static void gram_score_go(dim3 grid, const void *q, const void *k_full, const HeadArgs &ha, int H,
+                          int Nt, int N, int n_src, const int32_t *kidx, int n_heads, float sl2e,
+                          float *partial, const GramJob &gj, hipStream_t st) {
+    hipLaunchKernelGGL((gram_score_kernel<DT, 4, MAXC>), grid, dim3(kScoreNT), 0, st,
+                       (const char *)q, (const char *)k_full, ha, H, Nt, N, n_src, kidx, n_heads,
+                       sl2e, partial, gj);
+}
+
+hipError_t launch_gram_score(int dt, const void *q, const void *k_full, const int32_t *heads_host,
+                             int B, int H, int Nt, int N, int n_src, const int32_t *kidx, int hd,
+                             int n_heads, float *partial, const GramJob &gj, hipStream_t st) {
+    if (!gram_score_supported(dt, B, n_heads, N, hd) || N < 1) return hipErrorInvalidValue;
+    HeadArgs ha;
+    for (int i = 0; i < kMaxHeadArgs; ++i) ha.h[i] = i < B * n_heads ? heads_host[i] : 0;
+    const float sl2e = (float)(1.4426950408889634 / sqrt((double)hd));
+    const dim3 grid(((Nt + 15) / 16) * n_heads * B + gj.nblocks);
+    const int nch = (N + kScoreCK - 1) / kScoreCK;
+#define PV_GS_CASE(mc)                                                                            \
+    if (nch <= mc) {                                                                              \
+        if (dt == kBF16)                                                                          \
+            gram_score_go<kBF16, mc>(grid, q, k_full, ha, H, Nt, N, n_src, kidx, n_heads, sl2e,   \
+                                     partial, gj, st);                                            \
+        else                                                                                      \
+            gram_score_go<kF32, mc>(grid, q, k_full, ha, H, Nt, N, n_src, kidx, n_heads, sl2e,    \
+                                    partial, gj, st);                                             \
+        return hipGetLastError();                                                                 \
+    }
+    PV_GS_CASE(1)
+    PV_GS_CASE(2)
+    PV_GS_CASE(4)
+#undef PV_GS_CASE
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_reduce_select_gather(const ReduceJob &rj, const SelectJob &sj,
+                                       const GatherJob &gj, hipStream_t st) {
+    if (sj.nblocks > 0 && sj.N > kScoreNT) return hipErrorInvalidValue;
+    const int blocks = sj.nblocks + rj.nblocks + gj.nblocks;
+    if (blocks < 1) return hipSuccess;
+    hipLaunchKernelGGL(reduce_select_gather_kernel, dim3(blocks), dim3(kScoreNT), 0, st, rj, sj, gj);
+    return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------

@@ -2,17 +2,19 @@
 //
 // At small batches every kernel of the pipeline is a few microseconds, most
 // of it the launch itself, and the two chains that follow the top-N_1
-// selection (nearest kept token -> merge, and K/V of the kept tokens ->
-// head-aware score -> top-N_2) do not depend on each other.  A launch can
-// then carry the next step of the other chain as extra workgroups appended
-// after its own: the gather of the kept rows with the Gram, the Gram's
-// argmax with the score, the score's top-N_2 with the merge.  The bodies
-// below are those steps' workgroup bodies, shared by their own kernels and
-// by the kernels that carry them; a job with nblocks == 0 adds nothing.
+// selection (nearest kept token -> merge, and head-aware score -> top-N_2)
+// do not depend on each other.  Their steps then share launches as extra
+// workgroups of one grid: the score (reading the kept tokens' keys through
+// the kept list) with the Gram tiles; the top-N_2 with the Gram's argmax and
+// the compaction of K/V to the N_1 kept; the final compaction with the
+// merge.  The bodies below are those steps' workgroup bodies, shared by
+// their own kernels and by the kernels that carry them; a job with
+// nblocks == 0 adds nothing.
 #pragma once
 
 #include "pv_device.h"
 #include "pv_launch.h"
+#include "pv_tile_lds.h"
 
 namespace pv {
 
@@ -168,6 +170,100 @@ __device__ __forceinline__ void gram_reduce_row(const ReduceJob &j, int m, int b
 // Rows of gram_reduce_row per carried workgroup (one per wave of 256).
 constexpr int kReduceRowsPerBlock = 4;
 
+// ----------------------------------------------------------------------------
+// Split-k products (the cosine, and the Grams that are too small to fill the
+// chip with full-k tiles).
+//
+// A workgroup owns a 64 x 64 output tile and one k slice of its rows (streamed
+// into LDS, see pv_tile_lds.h); the k slices are added in slice order by the
+// reduce kernels.  Slicing k spreads a B=1 problem over every CU while each
+// CU fetches only a few tens of KB; the price is KS fp32 partial tiles, which
+// stay in L2.
+// ----------------------------------------------------------------------------
+constexpr int kPT = 64;  // tile edge of the split-k products
+template <int DT, int NS>
+using PTile = TileGemmLds<DT, kPT, kPT, 2, 2, NS>;
+// Ring depth of the split-k tiles: three 16 KB stages.  Measured: a deeper
+// ring costs more (fewer workgroups fit a CU) than the extra loads in flight
+// gain.
+constexpr int kSplitNS = 3;
+
+
+// gram_partial: 1-D grid over (sample, k slice, kept tile, pruned tile) in
+// XCD order (pruned tiles of one kept tile and slice are adjacent: they share
+// the kept rows).  Writes partial dot products part[ks][b][Mp][N1].
+// blk: this workgroup's index among the launch's `total` tile workgroups.
+// EXT: the LDS ring is `ext_ring` (PTile::LDS_BYTES, shared with the other
+// workgroups of a launch that carries another step); else its own.
+template <int DT, int NS, bool EXT = false>
+__device__ __forceinline__ void gram_partial_tile(const char *__restrict__ vis, int B, int Nv,
+                                                  int d_bytes, const int32_t *__restrict__ kept,
+                                                  int N1, const int32_t *__restrict__ pruned,
+                                                  int Mp, int ntm, int ntn, int KS,
+                                                  float *__restrict__ part, int total, int blk,
+                                                  char *ext_ring = nullptr) {
+    using G = PTile<DT, NS>;
+    __shared__ int32_t rowtok[G::ROWS];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave / 2, wn = wave % 2;
+    const int tile = xcd_tile(blk, total);
+    const int mt = tile % ntm;
+    const int nt = (tile / ntm) % ntn;
+    const int ks = (tile / (ntm * ntn)) % KS;
+    const int b = tile / (ntm * ntn * KS);
+    const int m0 = mt * kPT, n0 = nt * kPT;
+    const int32_t *pr = pruned + (size_t)b * Mp;
+    const int32_t *kp = kept + (size_t)b * N1;
+    for (int r = tid; r < G::ROWS; r += G::NT)
+        rowtok[r] = (r < kPT) ? pr[min(m0 + r, Mp - 1)] : kp[min(n0 + r - kPT, N1 - 1)];
+    __syncthreads();
+    const char *vbase = vis + (size_t)b * Nv * d_bytes;
+    auto row_ptr = [&](int r) -> const char * { return vbase + (size_t)rowtok[r] * d_bytes; };
+    const int nch = d_bytes / G::CHUNK;
+    const int c0 = (int)(((long long)nch * ks) / KS), c1 = (int)(((long long)nch * (ks + 1)) / KS);
+    f32x4_t acc[G::FM][G::FN];
+    float sa[G::FM], sb[G::FN];
+    if constexpr (EXT) G::template run_in<false>(ext_ring, row_ptr, c0, c1, acc, sa, sb);
+    else G::template run<false>(row_ptr, c0, c1, acc, sa, sb);
+    float *pb = part + ((size_t)ks * B + b) * Mp * N1;
+#pragma unroll
+    for (int fm = 0; fm < G::FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < G::FN; ++fn) {
+            const int n = n0 + wn * G::SUB_N + fn * 16 + (lane & 15);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int m = m0 + wm * G::SUB_M + fm * 16 + (lane >> 4) * 4 + e;
+                if (m < Mp && n < N1) pb[(size_t)m * N1 + n] = acc[fm][fn][e];
+            }
+        }
+}
+
+// The split-k Gram carried by another launch (its tiles after that launch's
+// own workgroups).
+struct GramJob {
+    const char *vis;
+    int B, Nv, d_bytes;
+    const int32_t *kept;    // [B][N1]
+    int N1;
+    const int32_t *pruned;  // [B][Mp]
+    int Mp, ntm, ntn, KS;
+    float *part;            // [KS][B][Mp][N1]
+    int nblocks;            // tile workgroups (B * KS * ntm * ntn); 0: none
+};
+
+// What the merge launch of the one-call step carries besides the merge: the
+// merged rows of the slots the head-aware top-N_2 kept, written straight to
+// their compacted places, and the compaction of K and V to those slots.
+struct MergeCarry {
+    const int32_t *slot_of2;  // [B][N1] position of each slot among the N_2 kept, or -1
+    char *hidden2;            // [B][N2] rows of d_bytes
+    int N2;
+    GatherJob gj;             // K and V of the N_2 kept slots
+};
+
+
 // ---- head-aware score: v and the top-N_2 (Eq. v, Sec. 4.4) ---------------
 constexpr int kSelU = 16;
 
@@ -179,6 +275,7 @@ struct SelectJob {
     int budget;
     int32_t *kept;         // [B][budget]
     int nblocks;           // samples carried by another launch; 0: none
+    int32_t *slot_of;      // [B][N] position of each column in kept, or -1 (may be NULL)
 };
 
 // inv_norm x the partials of column j added in part order, loaded in blocks
@@ -236,7 +333,8 @@ __device__ __forceinline__ void score_select_block(const SelectJob &sj, int b) {
             key[e] = (e < E && j < N) ? order_key(vs[j]) : 0u;
         }
     }
-    block_topk<NT, EMAX>(key, N, sj.budget, sj.kept + (size_t)b * sj.budget, nullptr, nullptr, sm);
+    block_topk<NT, EMAX>(key, N, sj.budget, sj.kept + (size_t)b * sj.budget, nullptr,
+                         sj.slot_of ? sj.slot_of + (size_t)b * N : nullptr, sm);
 }
 
 }  // namespace pv

@@ -10,6 +10,8 @@ namespace pv {
 struct GatherJob;
 struct ReduceJob;
 struct SelectJob;
+struct GramJob;
+struct MergeCarry;
 
 // Element types of the inputs (values of pv_dtype).
 constexpr int kF32 = 0;
@@ -55,10 +57,9 @@ hipError_t launch_center(const float *M, const float *rowsum, const int32_t *row
                          int B, int Nt, int Nv, float *p, hipStream_t st);
 hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kept, int32_t *pruned,
                          int32_t *slot_of, hipStream_t st);
-// with: a gather carried as extra workgroups of the same launch (or NULL).
 hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                                int N1, const int32_t *pruned, int Mp, int KS, float *part,
-                               hipStream_t st, const GatherJob *with = nullptr);
+                               hipStream_t st);
 hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, int KS,
                               const float *invn, const int32_t *pruned, const int32_t *kept,
                               int32_t *assign, hipStream_t st);
@@ -85,10 +86,12 @@ hipError_t launch_merge_csr(int dt, const void *vis, int B, int Nv, int d, int N
 inline bool merge_uses_lists(int B, int N1, int d_bytes) {
     return B > 1 || (long long)((d_bytes / 16 + 63) / 64) * N1 * 4 > d_bytes;
 }
-// with: the score's top-N_2 carried as extra workgroups (N <= 256), or NULL.
+// with: the merged rows of the head-aware top-N_2 written to their compacted
+// places too, and the compaction of K and V to those slots carried as extra
+// workgroups (or NULL).
 hipError_t launch_merge(int dt, const void *vis, int B, int Nv, int d, int N1,
                         const int32_t *assign, void *merged, hipStream_t st,
-                        const SelectJob *with = nullptr);
+                        const MergeCarry *with = nullptr);
 
 // ---- critical text tokens (Sec. 4.2)
 hipError_t launch_text_gram_sum(const float *part, int B, int Nt, int KS, float *G,
@@ -115,12 +118,8 @@ int score_parts(int dt, int B, int H, int n_heads, int Nt, int N, int hd);
 inline size_t score_split_stats_bytes(int B, int n_heads, int Nt, int N) {
     return (size_t)B * n_heads * ((N + 63) / 64) * Nt * 8;
 }
-// Whether the score launch can carry the split-k Gram's argmax (ReduceJob).
-bool score_can_carry_reduce(int dt, int hd);
 // row_lse [B][H][Nt] (may be NULL): log-sum-exp of each row's scaled logits
 // over the non-visual keys, which join the softmax normaliser.
-// with: the split-k Gram's argmax carried as extra workgroups of the first
-// launch (or NULL); not with the whole-head form.
 // split_stats: workspace of score_split_stats_bytes (used by the split form).
 // hd: the width of the q and k rows (a multiple of 32); hd_scale: the head
 // width of the attention scale 1 / sqrt(hd_scale) (the rows may be padded
@@ -128,8 +127,7 @@ bool score_can_carry_reduce(int dt, int hd);
 hipError_t launch_score_partial(int dt, const void *q, const void *k, const int32_t *heads_host,
                                 const int32_t *heads_dev, const float *row_lse, int B, int H,
                                 int Nt, int N, int hd, int hd_scale, int n_heads, float *partial,
-                                float *split_stats, hipStream_t st,
-                                const ReduceJob *with = nullptr);
+                                float *split_stats, hipStream_t st);
 // Head confidence of every head, per 16-row block: partial[b][h][rb].
 // row_mask as for launch_center: the rows summed into the confidence.
 // row_lse as for launch_score_partial (may be NULL): the variance is then
@@ -141,6 +139,18 @@ hipError_t launch_conf_select(const float *partial, int B, int H, int Nt, float 
                               int32_t *heads, hipStream_t st);
 hipError_t launch_score_select(const float *partial, int B, int nparts, int N, float inv_norm,
                                float *v, int budget, int32_t *kept, hipStream_t st);
+// The one-call step after the top-N_1 at small batches (see
+// head_aware_kernels.hip): the score on the keys of the kept tokens read
+// through kidx ([B][N] rows of k_full, [B][H][n_src][hd]) beside the split-k
+// Gram's tiles, then the score's top-N_2, the Gram's argmax and the
+// compaction of K and V to the N_1 kept in one launch.  The score runs one
+// 16-row block per workgroup with every logit in registers.
+bool gram_score_supported(int dt, int B, int n_heads, int N, int hd);
+hipError_t launch_gram_score(int dt, const void *q, const void *k_full, const int32_t *heads_host,
+                             int B, int H, int Nt, int N, int n_src, const int32_t *kidx, int hd,
+                             int n_heads, float *partial, const GramJob &gj, hipStream_t st);
+hipError_t launch_reduce_select_gather(const ReduceJob &rj, const SelectJob &sj,
+                                       const GatherJob &gj, hipStream_t st);
 
 // ---- compaction (Sec. 4.1)
 constexpr int kMaxGather = 4;

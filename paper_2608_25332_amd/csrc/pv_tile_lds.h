@@ -105,7 +105,17 @@ struct TileGemmLds {
     __device__ __forceinline__ static void run(RowPtr row_ptr, int c_begin, int c_end,
                                                f32x4_t (&acc)[FM][FN], float (&ssa)[FM],
                                                float (&ssb)[FN]) {
-        __shared__ __attribute__((aligned(16))) char ring[NSTAGE][STAGE_BYTES];
+        __shared__ __attribute__((aligned(16))) char ring[LDS_BYTES];
+        run_in<WANT_SS>(ring, row_ptr, c_begin, c_end, acc, ssa, ssb);
+    }
+
+    // The same on a ring the caller provides (LDS_BYTES of LDS, 16-byte
+    // aligned), for kernels whose other workgroups use the same LDS for
+    // something else.
+    template <bool WANT_SS, typename RowPtr>
+    __device__ __forceinline__ static void run_in(char *ring, RowPtr row_ptr, int c_begin,
+                                                  int c_end, f32x4_t (&acc)[FM][FN],
+                                                  float (&ssa)[FM], float (&ssb)[FN]) {
         const int lane = threadIdx.x & 63;
         const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
         const int wm = wave / WN, wn = wave % WN;
@@ -130,7 +140,7 @@ struct TileGemmLds {
         }
         // chunk i (relative to c_begin) goes to stage i % NSTAGE
         auto issue = [&](int i) {
-            char *dst = ring[i % NSTAGE] + wave * IPW * 1024;
+            char *dst = ring + (i % NSTAGE) * STAGE_BYTES + wave * IPW * 1024;
 #pragma unroll
             for (int q = 0; q < IPW; ++q)
                 lds_dma16(src[q] + (size_t)i * CHUNK, dst + q * 1024);
@@ -149,7 +159,7 @@ struct TileGemmLds {
             else wait_vmcnt<0>();
             bare_barrier();  // all of chunk i is in LDS; chunk i - 1 has been read
             if (i + NSTAGE - 1 < nc) issue(i + NSTAGE - 1);
-            const char *sp = ring[i % NSTAGE];
+            const char *sp = ring + (i % NSTAGE) * STAGE_BYTES;
             // both 64-byte windows of the chunk are read up front: the
             // second window's reads are in flight while the first window's
             // MFMAs run

@@ -202,8 +202,9 @@ def test_pipeline_timed_reps_leave_results_unchanged(wid):
     torch.cuda.synchronize()
     _assert_same(got, ref)
     if wid == 2:
-        assert got["kernel_names"] == ["cos_full", "center", "select", "gram_partial+gather_kv1",
-                                       "score_partial+gram_reduce", "merge+score_select",
-                                       "gather_hkv2"]
+        assert got["kernel_names"] == ["cos_full", "center", "select",
+                                       "gram_partial+score_partial",
+                                       "gram_reduce+score_select+gather_kv1",
+                                       "merge+gather_hkv2"]
     else:  # B = 16: member-list merge, separate launches
         assert got["n_kernels"] == 0
