@@ -1,8 +1,10 @@
 """The whole pruning step in one call (pv_prune_pipeline).
 
 Where the shapes allow it, the two chains that follow the top-N_1 selection
-share launches (the K/V compaction rides in the Gram's launch, the Gram's
-argmax in the score's, the score's top-N_2 in the merge's).  Every output
+share launches (the score, on the kept tokens' keys read through the kept
+list, rides with the Gram tiles; the top-N_2, the Gram's argmax and the K/V
+compaction share the next launch; the merge writes the kept slots' hidden
+rows and carries the final K/V compaction).  Every output
 must equal, bit for bit, the same step with every kernel in its own launch
 (pv_prune_pipeline_separate, which is the four calls made one after another),
 and the step must match the oracle as the separate calls do.
@@ -128,8 +130,11 @@ def test_pipeline_against_oracle(wid):
 # whether the step must take them
 EDGE = [
     (1, 100, 5, 512, 2, 128, 1, 37, 5, "bf16", True),       # ragged tiles, one head
-    (1, 300, 20, 512, 8, 128, 3, 256, 100, "bf16", True),   # N1 = 256: the widest merge-carried top-k
+    (1, 300, 20, 512, 8, 128, 3, 256, 100, "bf16", True),   # N1 = 256: the widest carried top-k (four key chunks)
     (1, 300, 20, 512, 8, 128, 3, 257, 100, "bf16", False),  # N1 = 257: member-list merge
+    (1, 300, 20, 512, 8, 128, 3, 100, 30, "bf16", True),    # two key chunks in the shared score
+    (1, 300, 20, 512, 8, 128, 3, 100, 100, "bf16", True),   # N2 = N1: every slot's row compacted
+    (1, 130, 7, 512, 8, 128, 8, 65, 64, "bf16", True),      # 65 keys: one past a chunk, all heads
     (1, 64, 16, 512, 4, 64, 2, 64, 10, "bf16", False),      # N1 = Nv: nothing pruned, no Gram
     (1, 90, 16, 512, 4, 64, 2, 40, 7, "bf16", False),       # 128-byte head rows
     (1, 90, 16, 256, 4, 64, 2, 40, 7, "f32", True),         # 256-byte fp32 head rows
