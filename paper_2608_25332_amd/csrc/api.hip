@@ -106,6 +106,7 @@ struct DedupPlan {
     int Mp;
     bool gram_big;                 // full-k 128x128 tiles (operands streamed into LDS)
     int ks_gram, ntn;              // split-k slices (small) / column tiles (big)
+    bool gram_wide;                // split-k Gram on the wide tiles
     // workspace
     bool lists;                    // merge reads bucketed member lists
     float *cpart, *ssv, *ssa, *M, *rowsum, *invn, *p, *gpart, *best_val;
@@ -136,6 +137,27 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
         const long long t = n_tiles(Mp1, budget, B, T);
         if (t * P.ks_gram > 256 && t * P.ks_gram < 512 && 256 / t >= 1) P.ks_gram = (int)(256 / t);
         else if (t * P.ks_gram > 768 && t * P.ks_gram < 1536 && 768 / t >= 1) P.ks_gram = (int)(768 / t);
+    }
+    // The wide split-k tiles (two workgroups per CU, a whole round of them)
+    // when they load fewer bytes on the busiest CU: a CU streams about the
+    // same bytes per second whatever its tiles, so the CU with the most bytes
+    // to load sets the kernel's time.
+    P.gram_wide = false;
+    if (!P.gram_big) {
+        const long long tw = (long long)((Mp1 + pv::kGramWideM - 1) / pv::kGramWideM) *
+                             ((budget + pv::kGramWideN - 1) / pv::kGramWideN) * B;
+        const int ksw = pick_slices(tw, P.nch, 512, true);
+        // row chunks the busiest CU loads (workgroups go round-robin to the
+        // 256 CUs)
+        auto busiest = [&](long long tiles, int ks, int rows) {
+            return (double)((tiles * ks + 255) / 256) * rows * ((double)P.nch / ks);
+        };
+        const double sq = busiest(n_tiles(Mp1, budget, B, T), P.ks_gram, 2 * T);
+        const double wd = busiest(tw, ksw, pv::kGramWideM + pv::kGramWideN);
+        if (wd < 0.8 * sq) {
+            P.gram_wide = true;
+            P.ks_gram = ksw;
+        }
     }
     P.ntn = P.gram_big ? (budget + pv::kGramTileN - 1) / pv::kGramTileN : 1;
     Carve c(ws);
@@ -308,7 +330,7 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
         } else {
             if (!tr.launch("gram_partial", [&] {
                     return pv::launch_gram_partial(dt, vis_k, B, Nv, dp, kept, budget, P.pruned,
-                                                   P.Mp, P.ks_gram, P.gpart, sm);
+                                                   P.Mp, P.ks_gram, P.gpart, P.gram_wide, sm);
                 }))
                 return PV_ERR_HIP;
             if (!tr.launch("gram_reduce", [&] {
@@ -1021,7 +1043,7 @@ int pipeline_impl(const void *vis, const void *anchors, const void *q, const voi
     // with every logit in registers (the same kernels' arithmetic as the
     // separate calls, so the same bits)
     const bool carry = !force_separate && padded_d(d, esz) == d && padded_hd(hd) == hd &&
-                       P.Mp > 0 && !P.gram_big && !P.lists && N1 <= 256 &&
+                       P.Mp > 0 && !P.gram_big && !P.gram_wide && !P.lists && N1 <= 256 &&
                        pv::gram_score_supported(dt, B, n_heads, N1, hd) &&
                        !pv::score_uses_head_form(dt, B, H, n_heads, Nt, N1, hd) &&
                        !pv::score_uses_split_form(dt, B, H, n_heads, Nt, N1, hd);

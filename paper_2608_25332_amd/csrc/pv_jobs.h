@@ -193,16 +193,17 @@ constexpr int kSplitNS = 3;
 // XCD order (pruned tiles of one kept tile and slice are adjacent: they share
 // the kept rows).  Writes partial dot products part[ks][b][Mp][N1].
 // blk: this workgroup's index among the launch's `total` tile workgroups.
-// EXT: the LDS ring is `ext_ring` (PTile::LDS_BYTES, shared with the other
-// workgroups of a launch that carries another step); else its own.
-template <int DT, int NS, bool EXT = false>
+// EXT: the LDS ring is `ext_ring` (the tile's LDS_BYTES, shared with the
+// other workgroups of a launch that carries another step); else its own.
+// Tiles of BM pruned x BN kept rows (four waves of BM/2 x BN/2).
+template <int DT, int NS, bool EXT = false, int BM = kPT, int BN = kPT>
 __device__ __forceinline__ void gram_partial_tile(const char *__restrict__ vis, int B, int Nv,
                                                   int d_bytes, const int32_t *__restrict__ kept,
                                                   int N1, const int32_t *__restrict__ pruned,
                                                   int Mp, int ntm, int ntn, int KS,
                                                   float *__restrict__ part, int total, int blk,
                                                   char *ext_ring = nullptr) {
-    using G = PTile<DT, NS>;
+    using G = TileGemmLds<DT, BM, BN, 2, 2, NS>;
     __shared__ int32_t rowtok[G::ROWS];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -212,11 +213,11 @@ __device__ __forceinline__ void gram_partial_tile(const char *__restrict__ vis, 
     const int nt = (tile / ntm) % ntn;
     const int ks = (tile / (ntm * ntn)) % KS;
     const int b = tile / (ntm * ntn * KS);
-    const int m0 = mt * kPT, n0 = nt * kPT;
+    const int m0 = mt * BM, n0 = nt * BN;
     const int32_t *pr = pruned + (size_t)b * Mp;
     const int32_t *kp = kept + (size_t)b * N1;
     for (int r = tid; r < G::ROWS; r += G::NT)
-        rowtok[r] = (r < kPT) ? pr[min(m0 + r, Mp - 1)] : kp[min(n0 + r - kPT, N1 - 1)];
+        rowtok[r] = (r < BM) ? pr[min(m0 + r, Mp - 1)] : kp[min(n0 + r - BM, N1 - 1)];
     __syncthreads();
     const char *vbase = vis + (size_t)b * Nv * d_bytes;
     auto row_ptr = [&](int r) -> const char * { return vbase + (size_t)rowtok[r] * d_bytes; };

@@ -57,9 +57,13 @@ hipError_t launch_center(const float *M, const float *rowsum, const int32_t *row
                          int B, int Nt, int Nv, float *p, hipStream_t st);
 hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kept, int32_t *pruned,
                          int32_t *slot_of, hipStream_t st);
+// The split-k Gram's partial dot products part[KS][B][Mp][N1], on kSplitTile
+// square tiles (three workgroups per CU) or, with `wide`, on kGramWideM x
+// kGramWideN tiles (two per CU, each row loaded once for more outputs).
+constexpr int kGramWideM = 128, kGramWideN = 96;
 hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                                int N1, const int32_t *pruned, int Mp, int KS, float *part,
-                               hipStream_t st);
+                               bool wide, hipStream_t st);
 hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, int KS,
                               const float *invn, const int32_t *pruned, const int32_t *kept,
                               int32_t *assign, hipStream_t st);

@@ -181,6 +181,9 @@ DEDUP_EDGE = [
     (8, 1000, 130, 256, 300, "bf16"),
     (2, 1500, 100, 2048, 400, "bf16"),
     (1, 1200, 70, 2048, 300, "f32"),
+    # wide split-k Gram tiles (128 x 96), ragged in both directions (three
+    # cases above take them too: 64 x 200, 2 x 1500 and the fp32 1 x 1200)
+    (12, 500, 64, 4096, 150, "bf16"),
     # full-k Gram tiles: one kept tile (slot written directly), and two kept
     # tiles in fp32 (per-tile candidates merged by gram_finish)
     (128, 300, 4, 64, 100, "bf16"),

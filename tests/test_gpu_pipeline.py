@@ -140,6 +140,7 @@ EDGE = [
     (1, 90, 16, 256, 4, 64, 2, 40, 7, "f32", True),         # 256-byte fp32 head rows
     (1, 500, 130, 512, 8, 128, 4, 200, 50, "bf16", True),   # nine 16-row score blocks
     (1, 1500, 100, 512, 8, 128, 4, 250, 60, "bf16", True),  # many pruned rows
+    (1, 1500, 20, 2048, 8, 128, 2, 250, 60, "bf16", False),  # wide split-k Gram tiles
     (1, 40, 3, 64, 1, 128, 1, 1, 1, "bf16", True),          # budgets of one
     (1, 200, 8, 64, 2, 128, 2, 100, 9, "bf16", False),      # member-list merge (narrow rows)
     (1, 1300, 16, 64, 2, 128, 1, 1024, 50, "bf16", False),  # N1 = 1024

@@ -78,7 +78,7 @@ def check(sc2: np.ndarray, k: int, r: dict):
 
 KINDS = ["normal", "ties", "equal", "two", "signed_zero", "lowbit", "packed", "negative", "wide",
          "ascending", "descending"]
-SIZES = [1, 2, 63, 64, 65, 192, 576, 1024, 1025, 2880, 4096, 4097]
+SIZES = [1, 2, 63, 64, 65, 192, 576, 1024, 1025, 2880, 4096, 4097, 4608, 5120, 5121]
 
 
 @pytest.mark.parametrize("n", SIZES)
