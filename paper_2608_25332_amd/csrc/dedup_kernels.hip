@@ -651,11 +651,11 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
 // Member lists for large inputs, where every merge workgroup scanning the whole
 // assignment would cost more than the rows it adds.
 //
-// bucket: grid (ceil(N1 / 256), B), 512 threads.  Lists the members of the
+// bucket: grid (ceil(N1 / 256), B), 512 or 1024 threads.  Lists the members of the
 // 256 slots [256 g, 256 g + 256) in ascending token order: mcount[b][s],
 // mstart[b][s] (offset in the sample's list region) and the lists themselves
-// in mlist[b][g * Nv ...].  The assignment is staged in LDS; the eight waves
-// take eight consecutive token segments and sweep them twice, 64 tokens per
+// in mlist[b][g * Nv ...].  The assignment is staged in LDS; the waves take
+// consecutive token segments and sweep them twice, 64 tokens per
 // step: per-slot counts, then placement at offsets that keep the segments in
 // order.  Within a step, the lanes that hold the same slot are found with one
 // ballot per bit of the slot offset (the lanes whose offsets agree on every
@@ -665,8 +665,9 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
 constexpr int kBucketBits = 8;
 constexpr int kBucketSlots = 1 << kBucketBits;
 static_assert(kBucketSlots == kBucketSlotsPerGroup, "slots per bucket group");
-constexpr int kBucketNT = 512;
-constexpr int kBucketW = kBucketNT / 64;
+// threads: 512, or 1024 from kBucketWideNv tokens (measured: 16 waves sweep
+// the longer assignments faster, 8 cost less on short ones)
+constexpr int kBucketWideNv = 2048;
 
 // Lanes whose value v agrees with this lane's on the low kBucketBits bits,
 // among the lanes in `act`.
@@ -681,12 +682,14 @@ __device__ __forceinline__ unsigned long long same_slot_lanes(int v, unsigned lo
     return same;
 }
 
+template <int kBucketNT>
 __global__ __launch_bounds__(kBucketNT) void bucket_kernel(const int32_t *__restrict__ assign,
                                                            int Nv, int N1,
                                                            int32_t *__restrict__ mcount,
                                                            int32_t *__restrict__ mstart,
                                                            int32_t *__restrict__ mlist) {
     extern __shared__ int32_t sa[];  // [Nv] the sample's assignment
+    constexpr int kBucketW = kBucketNT / 64;
     __shared__ int cur[kBucketW][kBucketSlots];
     __shared__ int wsum[kBucketW];
     const int g = blockIdx.x, b = blockIdx.y, tid = threadIdx.x, lane = tid & 63;
@@ -1080,8 +1083,12 @@ hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, i
 hipError_t launch_bucket(const int32_t *assign, int B, int Nv, int N1, int32_t *mcount,
                          int32_t *mstart, int32_t *mlist, hipStream_t st) {
     const dim3 grid((N1 + kBucketSlots - 1) / kBucketSlots, B);
-    hipLaunchKernelGGL(bucket_kernel, grid, dim3(kBucketNT), (size_t)Nv * sizeof(int32_t), st,
-                       assign, Nv, N1, mcount, mstart, mlist);
+    if (Nv >= kBucketWideNv)
+        hipLaunchKernelGGL(bucket_kernel<1024>, grid, dim3(1024), (size_t)Nv * sizeof(int32_t), st,
+                           assign, Nv, N1, mcount, mstart, mlist);
+    else
+        hipLaunchKernelGGL(bucket_kernel<512>, grid, dim3(512), (size_t)Nv * sizeof(int32_t), st,
+                           assign, Nv, N1, mcount, mstart, mlist);
     return hipGetLastError();
 }
 
