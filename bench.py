@@ -210,6 +210,7 @@ SHARED_PARTS = {"gram_partial+score_partial": ("gram_partial", "score_partial"),
                 "merge+gather_hkv2": ("merge", "gather_hkv2")}
 # kernel name in bench.py -> the name rocprofv3 reports (without "_kernel" and
 # template arguments), which keys the committed counter summaries
+PROFILED_ALT = {"merge": ["merge_csr"], "cos_reduce": ["cos_reduce4"]}
 PROFILED_NAME = {"gram_partial+score_partial": "gram_score",
                  "gram_reduce+score_select+gather_kv1": "reduce_select_gather",
                  "merge+gather_hkv2": "merge", "gather_kv1": "gather", "gather_hkv2": "gather"}
@@ -423,7 +424,11 @@ def load_traffic(workload, kernel):
         return None
     if rec.get("csrc_digest") != csrc_digest():
         return None
-    k = rec.get("kernels", {}).get(PROFILED_NAME.get(kernel, kernel))
+    kernels = rec.get("kernels", {})
+    # the same call runs another kernel at some shapes (member-list merge,
+    # four-token slice reduction)
+    names = [PROFILED_NAME.get(kernel, kernel)] + PROFILED_ALT.get(kernel, [])
+    k = next((kernels[n] for n in names if n in kernels), None)
     if not k:
         return None
     return float(k["fetch_bytes"]) + float(k["write_bytes"])
