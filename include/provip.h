@@ -437,12 +437,15 @@ int pv_visual_heads_masked_timed(const void *q, const void *k, const int32_t *ro
  *   4. the compaction of merged, k1 and v1 to the budget2 kept tokens
  *      -> hidden2 [B][budget2][d], k2, v2 [B][H][budget2][hd].
  * Every output is the bit-for-bit result of the four calls made one after
- * another.  Where the shapes allow it (the split-k Gram and the plain merge
- * of the dedup, the 16-row score blocks, 256-byte head rows, budget1 <= 256),
- * the two independent chains that follow the top-budget1 selection share
- * launches: the K/V compaction rides in the Gram's launch, the Gram's argmax
- * in the score's, and the score's top-budget2 in the merge's, which takes
- * three kernel boundaries off the step.  All pointers are DEVICE memory,
+ * another.  Where the shapes allow it (the split-k Gram on its square tiles
+ * and the plain merge of the dedup, the 16-row score blocks, 256-byte head
+ * rows, budget1 <= 256, B * n_heads <= 512), the two independent chains that
+ * follow the top-budget1 selection share launches: the score, reading the
+ * kept tokens' keys from k_full through kept1, rides in the Gram's launch;
+ * the score's top-budget2, the Gram's argmax and the compaction to k1 and v1
+ * share the next; and the merge writes the merged rows of the budget2 kept
+ * slots to hidden2 itself and carries the compaction to k2 and v2.  The step
+ * is then six launches instead of ten.  All pointers are DEVICE memory,
  * contiguous, 16-byte aligned and required (none may be NULL); heads_host is
  * HOST memory.  Errors as for the calls it combines.
  * ---------------------------------------------------------------------- */
@@ -459,9 +462,9 @@ int pv_prune_pipeline(const void *vis, const void *anchors, const void *q, const
 /* The step with an event recorded around each of its launches, as the other
  * *_timed calls do (profiling only).  Where the launches are shared, the
  * kernel names are "cos_full" (or "cos_partial", "cos_reduce"), "center",
- * "select", "gram_partial+gather_kv1", "score_partial+gram_reduce",
- * "merge+score_select" and "gather_hkv2"; where they are not, the step runs
- * once without events and *n_kernels is 0. */
+ * "select", "gram_partial+score_partial",
+ * "gram_reduce+score_select+gather_kv1" and "merge+gather_hkv2"; where they
+ * are not, the step runs once without events and *n_kernels is 0. */
 int pv_prune_pipeline_timed(const void *vis, const void *anchors, const void *q,
                             const void *k_full, const void *v_full, const int32_t *heads_host,
                             int n_heads, int B, int Nv, int Nt, int d, int H, int hd, int dtype,
