@@ -316,8 +316,11 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     if (need_assign && P.Mp > 0) {
         if (P.gram_big) {
             if (!tr.launch("gram_tile", [&] {
+                    // on the second stream of the split call the Gram shares the chip
+                    // with the caller's work: the deeper-prefetch form
                     return pv::launch_gram_tile(dt, vis_k, B, Nv, dp, kept, budget, P.pruned, P.Mp,
-                                                P.invn, P.best_val, P.best_slot, asg, sm);
+                                                P.invn, P.best_val, P.best_slot, asg,
+                                                fork != nullptr, sm);
                 }))
                 return PV_ERR_HIP;
             if (P.ntn > 1) {

@@ -462,7 +462,13 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
 
     f32x4_t acc[G::FM][G::FN];
     float ssa[G::FM], ssb[G::FN];
-    G::template run<false>(row_ptr, 0, d_bytes / G::CHUNK, acc, ssa, ssb);
+    if constexpr (NS == 3) {
+        // one workgroup per CU with the loads two chunks ahead (run_ahead)
+        __shared__ __attribute__((aligned(16))) char ring[G::LDS_BYTES];
+        G::run_ahead(ring, row_ptr, 0, d_bytes / G::CHUNK, acc);
+    } else {
+        G::template run<false>(row_ptr, 0, d_bytes / G::CHUNK, acc, ssa, ssb);
+    }
 
 #pragma unroll
     for (int fm = 0; fm < G::FM; ++fm) {
@@ -1002,12 +1008,20 @@ hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kep
 template <int DT>
 static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int32_t *kept, int N1,
                                const int32_t *pruned, int Mp, const float *invn, float *best_val,
-                               int32_t *best_slot, int32_t *assign, hipStream_t st) {
+                               int32_t *best_slot, int32_t *assign, bool ahead, hipStream_t st) {
     const int esz = (DT == kBF16) ? 2 : 4;
-    const int ntm = (Mp + kGramTileM - 1) / kGramTileM, ntn = (N1 + kGramTileN - 1) / kGramTileN;
-    hipLaunchKernelGGL((gram_tile_kernel<DT, kGramTileM, kGramTileN, 2, 2, 2>),
-                       dim3(B * ntm * ntn), dim3(256), 0, st, (const char *)vis, Nv, d * esz, kept,
-                       N1, pruned, Mp, invn, ntm, ntn, best_val, best_slot, assign);
+    const int ntn = (N1 + kGramTileN - 1) / kGramTileN;
+    if (ahead) {
+        const int ntm = (Mp + kGramAheadM - 1) / kGramAheadM;
+        hipLaunchKernelGGL((gram_tile_kernel<DT, kGramAheadM, kGramTileN, 4, 2, 3>),
+                           dim3(B * ntm * ntn), dim3(512), 0, st, (const char *)vis, Nv, d * esz,
+                           kept, N1, pruned, Mp, invn, ntm, ntn, best_val, best_slot, assign);
+    } else {
+        const int ntm = (Mp + kGramTileM - 1) / kGramTileM;
+        hipLaunchKernelGGL((gram_tile_kernel<DT, kGramTileM, kGramTileN, 2, 2, 2>),
+                           dim3(B * ntm * ntn), dim3(256), 0, st, (const char *)vis, Nv, d * esz,
+                           kept, N1, pruned, Mp, invn, ntm, ntn, best_val, best_slot, assign);
+    }
     return hipGetLastError();
 }
 
@@ -1065,10 +1079,13 @@ hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, 
 
 hipError_t launch_gram_tile(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                             int N1, const int32_t *pruned, int Mp, const float *invn,
-                            float *best_val, int32_t *best_slot, int32_t *assign, hipStream_t st) {
+                            float *best_val, int32_t *best_slot, int32_t *assign, bool ahead,
+                            hipStream_t st) {
     if (dt == kBF16)
-        return gram_tile_go<kBF16>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
-    return gram_tile_go<kF32>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot, assign, st);
+        return gram_tile_go<kBF16>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot,
+                                   assign, ahead, st);
+    return gram_tile_go<kF32>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot,
+                              assign, ahead, st);
 }
 
 hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, int B, int ntn,

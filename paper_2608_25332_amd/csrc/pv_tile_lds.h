@@ -206,6 +206,102 @@ struct TileGemmLds {
         bare_barrier();  // the stages may be reused by a later call
     }
 
+    // Software-pipelined product for one workgroup per CU (three stages): the
+    // fragments of chunk i + 1 are read into a second register set while
+    // chunk i's MFMAs issue, and the direct-to-LDS loads run two chunks ahead
+    // of the fragment reads (a stage is free again once its fragments are in
+    // registers, so three stages hold two chunks in flight and one being
+    // read).  Per chunk i: wait for this wave's fragment reads of chunk i and
+    // for its loads of chunk i + 1; one barrier (chunk i + 1 is in LDS, every
+    // wave holds chunk i in registers); the loads of chunk i + 3 into chunk
+    // i's stage; the fragment reads of chunk i + 1; chunk i's MFMAs.
+    template <typename RowPtr>
+    __device__ __forceinline__ static void run_ahead(char *ring, RowPtr row_ptr, int c_begin,
+                                                     int c_end, f32x4_t (&acc)[FM][FN]) {
+        static_assert(NSTAGE == 3, "two chunks in flight and one being read");
+        const int lane = threadIdx.x & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int wm = wave / WN, wn = wave % WN;
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+            for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        const int nc = c_end - c_begin;
+        if (nc <= 0) return;
+        const char *src[IPW];
+#pragma unroll
+        for (int q = 0; q < IPW; ++q) {
+            const int pos = (wave * IPW + q) * 64 + lane;
+            const int r = pos >> 3, slot = pos & 7;
+            src[q] = row_ptr(r) + (size_t)c_begin * CHUNK + ((slot ^ (r & 7)) << 4);
+        }
+        auto issue = [&](int i) {
+            char *dst = ring + (i % NSTAGE) * STAGE_BYTES + wave * IPW * 1024;
+#pragma unroll
+            for (int q = 0; q < IPW; ++q)
+                lds_dma16(src[q] + (size_t)i * CHUNK, dst + q * 1024);
+        };
+        const int a_row = wm * SUB_M + (lane & 15);
+        const int b_row = BM + wn * SUB_N + (lane & 15);
+        const int kq = lane >> 4;
+        auto read = [&](int i, uint4(&af)[2][FM], uint4(&bf)[2][FN]) {
+            const char *sp = ring + (i % NSTAGE) * STAGE_BYTES;
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+                const int piece = s * 4 + kq;
+#pragma unroll
+                for (int f = 0; f < FM; ++f) {
+                    const int r = a_row + f * 16;
+                    af[s][f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
+                }
+#pragma unroll
+                for (int f = 0; f < FN; ++f) {
+                    const int r = b_row + f * 16;
+                    bf[s][f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
+                }
+            }
+        };
+        auto step = [&](int i, uint4(&af)[2][FM], uint4(&bf)[2][FN], uint4(&na)[2][FM],
+                        uint4(&nb)[2][FN]) {
+            lds_wait();  // this wave's fragments of chunk i
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+#pragma unroll
+                for (int f = 0; f < FM; ++f) lds_after_wait(af[s][f]);
+#pragma unroll
+                for (int f = 0; f < FN; ++f) lds_after_wait(bf[s][f]);
+            }
+            // this wave's loads of chunk i + 1 (those of chunk i + 2 may fly on)
+            if (i + 2 < nc) wait_vmcnt<IPW>();
+            else wait_vmcnt<0>();
+            bare_barrier();  // chunk i + 1 in LDS; chunk i's stage read by every wave
+            if (i + 3 < nc) issue(i + 3);
+            if (i + 1 < nc) read(i + 1, na, nb);
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int f = 0; f < FM; ++f)
+#pragma unroll
+                    for (int g = 0; g < FN; ++g)
+                        acc[f][g] = mma16<DT>(af[s][f], bf[s][g], acc[f][g]);
+        };
+        // prologue: chunks 0, 1 and 2 in flight; chunk 0 read into registers
+#pragma unroll
+        for (int p = 0; p < NSTAGE; ++p)
+            if (p < nc) issue(p);
+        if (nc >= 3) wait_vmcnt<2 * IPW>();
+        else if (nc == 2) wait_vmcnt<IPW>();
+        else wait_vmcnt<0>();
+        bare_barrier();
+        uint4 fa0[2][FM], fb0[2][FN], fa1[2][FM], fb1[2][FN];
+        read(0, fa0, fb0);
+        for (int i = 0; i < nc; i += 2) {
+            step(i, fa0, fb0, fa1, fb1);
+            if (i + 1 < nc) step(i + 1, fa1, fb1, fa0, fb0);
+        }
+        bare_barrier();  // the stages may be reused by a later call
+    }
+
     // Sum of squares of row (lane & 15) of a fragment block: combines the four
     // 16-byte quarters held by lanes l, l+16, l+32, l+48 in a fixed order.
     __device__ __forceinline__ static float row_sumsq(float partial) {

@@ -139,7 +139,7 @@ def test_timed_reps_leave_results_unchanged():
         assert torch.equal(h1[k], h2[k]), k
 
 
-@pytest.mark.parametrize("wid", [1, 2, 4])
+@pytest.mark.parametrize("wid", [1, 2, 4, 5])
 def test_dedup_split_matches_single_stream(wid):
     """pv_prune_dedup_split (merge branch on a second stream) gives the bits
     of pv_prune_dedup once merged_done has completed."""
@@ -158,6 +158,49 @@ def test_dedup_split_matches_single_stream(wid):
     torch.cuda.synchronize()
     for k in ("kept", "score", "assign", "merged"):
         assert torch.equal(a[k], b[k]), k
+
+
+# full-k Gram shapes for the split call, whose Gram takes the 256-row tiles
+# with loads two chunks ahead: one chunk (d = 64 bf16), one kept tile, two
+# kept tiles in fp32, padded rows, ragged tiles in both directions
+SPLIT_EDGE = [
+    (128, 300, 4, 64, 100, "bf16"),
+    (64, 600, 4, 128, 200, "f32"),
+    (64, 600, 4, 1000, 200, "bf16"),
+    (8, 1700, 16, 256, 500, "bf16"),
+    (16, 900, 8, 384, 300, "bf16"),
+]
+
+
+@pytest.mark.parametrize("B,Nv,Nt,d,budget,dt", SPLIT_EDGE)
+def test_dedup_split_edges(B, Nv, Nt, d, budget, dt):
+    """The split call's Gram against the single-stream call (same bits) and
+    its assignment against the oracle on every pruned row of the first and
+    last sample."""
+    from paper_2608_25332_amd import provip
+    _say(f"[dedup-split-edge] B={B} Nv={Nv} Nt={Nt} d={d} budget={budget} {dt}")
+    rng = np.random.default_rng(Nv * 11 + d)
+    vis = rng.standard_normal((B, Nv, d)).astype(np.float32)
+    anc = rng.standard_normal((B, Nt, d)).astype(np.float32)
+    if dt == "bf16":
+        vis, anc = W.bf16_round(vis), W.bf16_round(anc)
+    dv, da = to_dev(vis, dt), to_dev(anc, dt)
+    a = provip.pv_prune_dedup(dv, da, budget)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    sel, done = torch.cuda.Event(), torch.cuda.Event()
+    sel.record()
+    done.record()
+    b = provip.pv_prune_dedup(dv, da, budget, split=(side, sel, done))
+    torch.cuda.current_stream().wait_event(done)
+    torch.cuda.synchronize()
+    for k in ("kept", "score", "assign", "merged"):
+        assert torch.equal(a[k], b[k]), k
+    kept_all, assign_all = to_host(b["kept"]), to_host(b["assign"])
+    for bb in sorted({0, B - 1}):
+        kept = kept_all[bb]
+        pruned = np.setdiff1d(np.arange(Nv), kept)
+        check_assign_rows(assign_all[bb], vis[bb], kept, pruned, dt)
 
 
 DEDUP_EDGE = [
