@@ -127,7 +127,7 @@ DedupPlan plan_dedup(void *ws, int B, int Nv, int Nt, int d, int esz, int budget
     P.njt = P.cos_full ? pv::cos_full_row_tiles(Nv) : pv::cos_row_tiles(Nv);
     P.Mp = Nv - budget;
     const int Mp1 = P.Mp > 0 ? P.Mp : 1;
-    P.gram_big = (long long)((Mp1 + pv::kGramBigM - 1) / pv::kGramBigM) *
+    P.gram_big = (long long)((Mp1 + pv::kGramTileM - 1) / pv::kGramTileM) *
                      ((budget + pv::kGramTileN - 1) / pv::kGramTileN) * B >= 128;
     P.ks_gram = P.gram_big ? 1 : pick_slices(n_tiles(Mp1, budget, B, T), P.nch);
     {
@@ -316,11 +316,8 @@ int dedup_impl(const void *vis, const void *anchors, int B, int Nv, int Nt, int 
     if (need_assign && P.Mp > 0) {
         if (P.gram_big) {
             if (!tr.launch("gram_tile", [&] {
-                    // on the second stream of the split call the Gram shares the chip
-                    // with the caller's work: the deeper-prefetch form
                     return pv::launch_gram_tile(dt, vis_k, B, Nv, dp, kept, budget, P.pruned, P.Mp,
-                                                P.invn, P.best_val, P.best_slot, asg,
-                                                fork != nullptr, sm);
+                                                P.invn, P.best_val, P.best_slot, asg, sm);
                 }))
                 return PV_ERR_HIP;
             if (P.ntn > 1) {

@@ -424,20 +424,23 @@ __global__ __launch_bounds__(128) void gram_reduce_kernel(ReduceJob j) {
 
 // gram_tile: the large, MFMA-bound Grams.  1-D grid over (sample, pruned
 // tile, kept tile) in XCD order (the kept tiles of one pruned tile are
-// adjacent, so they share its rows in one L2); 128 x 128 tiles with the
-// operands streamed straight into LDS (TileGemmLds), four waves of 64 x 64.
-// The ring is two stages of 32 KB, so two workgroups share a CU: with one
-// chunk in flight per workgroup, the chunk latency of one is covered by the
-// MFMAs of the other (measured: 20% faster than one 256 x 128 workgroup of
-// eight waves per CU, whose waves all meet at every chunk's barrier).
+// adjacent, so they share its rows in one L2); 256 x 128 tiles with the
+// operands streamed straight into LDS (TileGemmLds::run_pc): eight matrix
+// waves of 64 x 64 that only read fragments and multiply, NP producer waves
+// that issue every load, a three-stage ring of 48 KB stages, one workgroup
+// per CU.  A matrix wave that issued its own loads waited for the CU's load
+// path to take them, between its MFMAs (measured: 29% of its time with
+// 128 x 128 tiles); with the producers the Gram also keeps its pace when
+// another stream's copies share the CU's load path.
 // Writes the best (cosine, slot) of every pruned row within this kept tile,
 // or the slot itself when there is only one kept tile.
-template <int DT, int BM, int BN, int WM, int WN, int NS>
-__global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
+template <int DT, int BM, int BN, int WM, int WN, int NS, int NP>
+__global__ __launch_bounds__(64 * (WM * WN + NP)) void gram_tile_kernel(
     const char *__restrict__ vis, int Nv, int d_bytes, const int32_t *__restrict__ kept, int N1,
     const int32_t *__restrict__ pruned, int Mp, const float *__restrict__ invn, int ntm, int ntn,
     float *__restrict__ best_val, int32_t *__restrict__ best_slot, int32_t *__restrict__ assign) {
     using G = TileGemmLds<DT, BM, BN, WM, WN, NS>;
+    constexpr int NTT = G::NT + 64 * NP;  // matrix waves, then producer waves
     __shared__ int32_t rowtok[G::ROWS];
     __shared__ float rowinv[G::ROWS];
     __shared__ float red_v[WN][BM];
@@ -451,7 +454,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
     const int32_t *pr = pruned + (size_t)b * Mp;
     const int32_t *kp = kept + (size_t)b * N1;
 
-    for (int r = tid; r < G::ROWS; r += G::NT) {
+    for (int r = tid; r < G::ROWS; r += NTT) {
         const int tok = (r < BM) ? pr[min(m0 + r, Mp - 1)] : kp[min(n0 + r - BM, N1 - 1)];
         rowtok[r] = tok;
         rowinv[r] = invn[(size_t)b * Nv + tok];
@@ -461,42 +464,39 @@ __global__ __launch_bounds__(64 * WM * WN) void gram_tile_kernel(
     auto row_ptr = [&](int r) -> const char * { return vbase + (size_t)rowtok[r] * d_bytes; };
 
     f32x4_t acc[G::FM][G::FN];
-    float ssa[G::FM], ssb[G::FN];
-    if constexpr (NS == 3) {
-        // one workgroup per CU with the loads two chunks ahead (run_ahead)
-        __shared__ __attribute__((aligned(16))) char ring[G::LDS_BYTES];
-        G::run_ahead(ring, row_ptr, 0, d_bytes / G::CHUNK, acc);
-    } else {
-        G::template run<false>(row_ptr, 0, d_bytes / G::CHUNK, acc, ssa, ssb);
-    }
+    __shared__ __attribute__((aligned(16))) char ring[G::LDS_BYTES];
+    G::template run_pc<NP>(ring, row_ptr, 0, d_bytes / G::CHUNK, acc);
 
+    // producer waves hold no products
+    if (__builtin_amdgcn_readfirstlane(wave) < WM * WN) {
 #pragma unroll
-    for (int fm = 0; fm < G::FM; ++fm) {
+        for (int fm = 0; fm < G::FM; ++fm) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = wm * G::SUB_M + fm * 16 + (lane >> 4) * 4 + i;
-            const float ia = rowinv[r];
-            float bv = -INFINITY;
-            int bs = 0x7FFFFFFF;
+            for (int i = 0; i < 4; ++i) {
+                const int r = wm * G::SUB_M + fm * 16 + (lane >> 4) * 4 + i;
+                const float ia = rowinv[r];
+                float bv = -INFINITY;
+                int bs = 0x7FFFFFFF;
 #pragma unroll
-            for (int fn = 0; fn < G::FN; ++fn) {
-                const int c = wn * G::SUB_N + fn * 16 + (lane & 15);
-                const int slot = n0 + c;
-                const float cs = acc[fm][fn][i] * ia * rowinv[BM + c];
-                if (slot < N1 && better(cs, slot, bv, bs)) {
-                    bv = cs;
-                    bs = slot;
+                for (int fn = 0; fn < G::FN; ++fn) {
+                    const int c = wn * G::SUB_N + fn * 16 + (lane & 15);
+                    const int slot = n0 + c;
+                    const float cs = acc[fm][fn][i] * ia * rowinv[BM + c];
+                    if (slot < N1 && better(cs, slot, bv, bs)) {
+                        bv = cs;
+                        bs = slot;
+                    }
                 }
-            }
-            row16_best(bv, bs);
-            if ((lane & 15) == 0) {
-                red_v[wn][r] = bv;
-                red_s[wn][r] = bs;
+                row16_best(bv, bs);
+                if ((lane & 15) == 0) {
+                    red_v[wn][r] = bv;
+                    red_s[wn][r] = bs;
+                }
             }
         }
     }
     __syncthreads();
-    for (int r = tid; r < BM; r += G::NT) {
+    for (int r = tid; r < BM; r += NTT) {
         float bv = red_v[0][r];
         int bs = red_s[0][r];
 #pragma unroll
@@ -1008,20 +1008,14 @@ hipError_t launch_select(const float *p, int B, int Nv, int budget, int32_t *kep
 template <int DT>
 static hipError_t gram_tile_go(const void *vis, int B, int Nv, int d, const int32_t *kept, int N1,
                                const int32_t *pruned, int Mp, const float *invn, float *best_val,
-                               int32_t *best_slot, int32_t *assign, bool ahead, hipStream_t st) {
+                               int32_t *best_slot, int32_t *assign, hipStream_t st) {
     const int esz = (DT == kBF16) ? 2 : 4;
     const int ntn = (N1 + kGramTileN - 1) / kGramTileN;
-    if (ahead) {
-        const int ntm = (Mp + kGramAheadM - 1) / kGramAheadM;
-        hipLaunchKernelGGL((gram_tile_kernel<DT, kGramAheadM, kGramTileN, 4, 2, 3>),
-                           dim3(B * ntm * ntn), dim3(512), 0, st, (const char *)vis, Nv, d * esz,
-                           kept, N1, pruned, Mp, invn, ntm, ntn, best_val, best_slot, assign);
-    } else {
-        const int ntm = (Mp + kGramTileM - 1) / kGramTileM;
-        hipLaunchKernelGGL((gram_tile_kernel<DT, kGramTileM, kGramTileN, 2, 2, 2>),
-                           dim3(B * ntm * ntn), dim3(256), 0, st, (const char *)vis, Nv, d * esz,
-                           kept, N1, pruned, Mp, invn, ntm, ntn, best_val, best_slot, assign);
-    }
+    const int ntm = (Mp + kGramTileM - 1) / kGramTileM;
+    hipLaunchKernelGGL((gram_tile_kernel<DT, kGramTileM, kGramTileN, 4, 2, 3, kGramProducers>),
+                       dim3(B * ntm * ntn), dim3(64 * (8 + kGramProducers)), 0, st,
+                       (const char *)vis, Nv, d * esz, kept, N1, pruned, Mp, invn, ntm, ntn,
+                       best_val, best_slot, assign);
     return hipGetLastError();
 }
 
@@ -1079,13 +1073,12 @@ hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, 
 
 hipError_t launch_gram_tile(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                             int N1, const int32_t *pruned, int Mp, const float *invn,
-                            float *best_val, int32_t *best_slot, int32_t *assign, bool ahead,
-                            hipStream_t st) {
+                            float *best_val, int32_t *best_slot, int32_t *assign, hipStream_t st) {
     if (dt == kBF16)
         return gram_tile_go<kBF16>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot,
-                                   assign, ahead, st);
+                                   assign, st);
     return gram_tile_go<kF32>(vis, B, Nv, d, kept, N1, pruned, Mp, invn, best_val, best_slot,
-                              assign, ahead, st);
+                              assign, st);
 }
 
 hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, int B, int ntn,

@@ -67,20 +67,15 @@ hipError_t launch_gram_partial(int dt, const void *vis, int B, int Nv, int d, co
 hipError_t launch_gram_reduce(const float *part, int B, int Mp, int N1, int Nv, int KS,
                               const float *invn, const int32_t *pruned, const int32_t *kept,
                               int32_t *assign, hipStream_t st);
-// Tile of the full-k Gram (pruned rows x kept rows) used for large inputs.
-// The full-k form is chosen when the product holds at least 128 blocks of
-// kGramBigM x kGramTileN (enough work to keep every CU busy without split-k).
-constexpr int kGramTileM = 128, kGramTileN = 128, kGramBigM = 256;
-// ahead: kGramAheadM x kGramTileN tiles, one workgroup of eight waves per CU
-// with its loads two chunks ahead of the fragment reads (for a Gram that
-// shares the chip with other work on another stream: the deeper prefetch
-// keeps its pace under the others' memory traffic); else kGramTileM x
-// kGramTileN tiles, two workgroups per CU (faster with the chip to itself).
-constexpr int kGramAheadM = 256;
+// Tile of the full-k Gram (pruned rows x kept rows) used for large inputs:
+// kGramTileM x kGramTileN, one workgroup per CU of eight matrix waves and
+// kGramProducers producer waves that issue the loads.  The full-k form is
+// chosen when the product holds at least 128 such tiles (enough work to keep
+// every CU busy without split-k).
+constexpr int kGramTileM = 256, kGramTileN = 128, kGramProducers = 4;
 hipError_t launch_gram_tile(int dt, const void *vis, int B, int Nv, int d, const int32_t *kept,
                             int N1, const int32_t *pruned, int Mp, const float *invn,
-                            float *best_val, int32_t *best_slot, int32_t *assign, bool ahead,
-                            hipStream_t st);
+                            float *best_val, int32_t *best_slot, int32_t *assign, hipStream_t st);
 hipError_t launch_gram_finish(const float *best_val, const int32_t *best_slot, int B, int ntn,
                               int Mp, int Nv, const int32_t *pruned, int32_t *assign,
                               hipStream_t st);

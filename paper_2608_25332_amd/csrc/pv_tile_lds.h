@@ -18,9 +18,10 @@
 //
 // The stages form one ring; chunk i of the range goes to stage i % NSTAGE.
 //
-// Ordering.  Before a stage is read, every wave waits for its own loads of
-// that stage (vmcnt), then all waves meet at a bare barrier: a __syncthreads
-// fence would also wait for the younger loads still in flight.  The fragment
+// Ordering.  Before a stage is read, every wave that loaded part of it waits
+// for its own loads of that stage (vmcnt; in run_pc only the producer waves
+// load), then all waves meet at a bare barrier: a __syncthreads fence would
+// also wait for the younger loads still in flight.  The fragment
 // reads are issued as inline assembly: the compiler cannot tell that they do
 // not touch the stages still being filled and would otherwise drain every
 // load in flight before each read.  Their completion is awaited explicitly
@@ -206,98 +207,110 @@ struct TileGemmLds {
         bare_barrier();  // the stages may be reused by a later call
     }
 
-    // Software-pipelined product for one workgroup per CU (three stages): the
-    // fragments of chunk i + 1 are read into a second register set while
-    // chunk i's MFMAs issue, and the direct-to-LDS loads run two chunks ahead
-    // of the fragment reads (a stage is free again once its fragments are in
-    // registers, so three stages hold two chunks in flight and one being
-    // read).  Per chunk i: wait for this wave's fragment reads of chunk i and
-    // for its loads of chunk i + 1; one barrier (chunk i + 1 is in LDS, every
-    // wave holds chunk i in registers); the loads of chunk i + 3 into chunk
-    // i's stage; the fragment reads of chunk i + 1; chunk i's MFMAs.
-    template <typename RowPtr>
-    __device__ __forceinline__ static void run_ahead(char *ring, RowPtr row_ptr, int c_begin,
-                                                     int c_end, f32x4_t (&acc)[FM][FN]) {
+    // The same product with NP producer waves after the NW matrix waves
+    // (blockDim = 64 (NW + NP)) and a three-stage ring.  The producers issue
+    // every direct-to-LDS load, so a matrix wave never waits for the CU's load
+    // path to take one (about 16 clocks per 1 KB instruction, shared by the
+    // CU); the matrix waves read fragments one 64-byte window ahead of their
+    // MFMAs: window 1 of chunk i while window 0's MFMAs issue, window 0 of
+    // chunk i + 1 while window 1's issue.
+    //
+    // Barrier j (j = 0 .. nc) closes the reads of chunk j - 1 and opens chunk
+    // j: before it the producers wait for their loads of chunk j, and after it
+    // they load chunk j + 2 into chunk j - 1's stage (chunks 0 .. 2 are loaded
+    // up front).  A matrix wave meets barrier j + 1 after its last read of
+    // chunk j and before its first read of chunk j + 1.  Both sides pass
+    // nc + 2 barriers.  acc is meaningful in the matrix waves only.
+    template <int NP, typename RowPtr>
+    __device__ __forceinline__ static void run_pc(char *ring, RowPtr row_ptr, int c_begin, int c_end,
+                                                  f32x4_t (&acc)[FM][FN]) {
         static_assert(NSTAGE == 3, "two chunks in flight and one being read");
+        constexpr int IPP = ROWS * 8 / 64 / NP;  // load instructions per producer wave per stage
+        static_assert(NP >= 1 && ROWS * 8 % (64 * NP) == 0, "stage rows must split over the producers");
+        static_assert(IPP * 2 < 64, "loads in flight exceed the wait counter");
         const int lane = threadIdx.x & 63;
         const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-        const int wm = wave / WN, wn = wave % WN;
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
             for (int j = 0; j < FN; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
         const int nc = c_end - c_begin;
         if (nc <= 0) return;
-        const char *src[IPW];
+        if (wave >= NW) {
+            const int pw = wave - NW;
+            const char *src[IPP];
 #pragma unroll
-        for (int q = 0; q < IPW; ++q) {
-            const int pos = (wave * IPW + q) * 64 + lane;
-            const int r = pos >> 3, slot = pos & 7;
-            src[q] = row_ptr(r) + (size_t)c_begin * CHUNK + ((slot ^ (r & 7)) << 4);
-        }
-        auto issue = [&](int i) {
-            char *dst = ring + (i % NSTAGE) * STAGE_BYTES + wave * IPW * 1024;
+            for (int q = 0; q < IPP; ++q) {
+                const int pos = (pw * IPP + q) * 64 + lane;
+                const int r = pos >> 3, slot = pos & 7;
+                src[q] = row_ptr(r) + (size_t)c_begin * CHUNK + ((slot ^ (r & 7)) << 4);
+            }
+            auto issue = [&](int i) {
+                char *dst = ring + (i % NSTAGE) * STAGE_BYTES + pw * IPP * 1024;
 #pragma unroll
-            for (int q = 0; q < IPW; ++q)
-                lds_dma16(src[q] + (size_t)i * CHUNK, dst + q * 1024);
-        };
-        const int a_row = wm * SUB_M + (lane & 15);
-        const int b_row = BM + wn * SUB_N + (lane & 15);
-        const int kq = lane >> 4;
-        auto read = [&](int i, uint4(&af)[2][FM], uint4(&bf)[2][FN]) {
-            const char *sp = ring + (i % NSTAGE) * STAGE_BYTES;
-#pragma unroll
-            for (int s = 0; s < 2; ++s) {
+                for (int q = 0; q < IPP; ++q)
+                    lds_dma16(src[q] + (size_t)i * CHUNK, dst + q * 1024);
+            };
+            issue(0);
+            if (nc > 1) issue(1);
+            if (nc > 2) issue(2);
+            // chunk 0 landed (chunks 1 and 2 may still fly)
+            if (nc > 2) wait_vmcnt<2 * IPP>();
+            else if (nc == 2) wait_vmcnt<IPP>();
+            else wait_vmcnt<0>();
+            bare_barrier();  // barrier 0
+            for (int i = 0; i < nc; ++i) {
+                // chunk i + 1 landed (chunk i + 2 may still fly)
+                if (i + 2 < nc) wait_vmcnt<IPP>();
+                else wait_vmcnt<0>();
+                bare_barrier();  // barrier i + 1: chunk i's stage is free
+                if (i + 3 < nc) issue(i + 3);
+            }
+        } else {
+            const int wm = wave / WN, wn = wave % WN;
+            const int a_row = wm * SUB_M + (lane & 15);
+            const int b_row = BM + wn * SUB_N + (lane & 15);
+            const int kq = lane >> 4;
+            auto read_w = [&](int i, int s, uint4(&a)[FM], uint4(&b)[FN]) {
+                const char *sp = ring + (i % NSTAGE) * STAGE_BYTES;
                 const int piece = s * 4 + kq;
 #pragma unroll
                 for (int f = 0; f < FM; ++f) {
                     const int r = a_row + f * 16;
-                    af[s][f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
+                    a[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
                 }
 #pragma unroll
                 for (int f = 0; f < FN; ++f) {
                     const int r = b_row + f * 16;
-                    bf[s][f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
+                    b[f] = lds_read16(sp + r * CHUNK + ((piece ^ (r & 7)) << 4));
                 }
-            }
-        };
-        auto step = [&](int i, uint4(&af)[2][FM], uint4(&bf)[2][FN], uint4(&na)[2][FM],
-                        uint4(&nb)[2][FN]) {
-            lds_wait();  // this wave's fragments of chunk i
-#pragma unroll
-            for (int s = 0; s < 2; ++s) {
-#pragma unroll
-                for (int f = 0; f < FM; ++f) lds_after_wait(af[s][f]);
-#pragma unroll
-                for (int f = 0; f < FN; ++f) lds_after_wait(bf[s][f]);
-            }
-            // this wave's loads of chunk i + 1 (those of chunk i + 2 may fly on)
-            if (i + 2 < nc) wait_vmcnt<IPW>();
-            else wait_vmcnt<0>();
-            bare_barrier();  // chunk i + 1 in LDS; chunk i's stage read by every wave
-            if (i + 3 < nc) issue(i + 3);
-            if (i + 1 < nc) read(i + 1, na, nb);
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
+            };
+            auto mma_w = [&](uint4(&a)[FM], uint4(&b)[FN]) {
 #pragma unroll
                 for (int f = 0; f < FM; ++f)
 #pragma unroll
-                    for (int g = 0; g < FN; ++g)
-                        acc[f][g] = mma16<DT>(af[s][f], bf[s][g], acc[f][g]);
-        };
-        // prologue: chunks 0, 1 and 2 in flight; chunk 0 read into registers
+                    for (int g = 0; g < FN; ++g) acc[f][g] = mma16<DT>(a[f], b[g], acc[f][g]);
+            };
+            uint4 a0[FM], b0[FN], a1[FM], b1[FN];
+            bare_barrier();  // barrier 0
+            read_w(0, 0, a0, b0);
+            for (int i = 0; i < nc; ++i) {
+                read_w(i, 1, a1, b1);
+                lds_wait_n<(FM + FN <= 15 ? FM + FN : 0)>();  // window 0 of chunk i
 #pragma unroll
-        for (int p = 0; p < NSTAGE; ++p)
-            if (p < nc) issue(p);
-        if (nc >= 3) wait_vmcnt<2 * IPW>();
-        else if (nc == 2) wait_vmcnt<IPW>();
-        else wait_vmcnt<0>();
-        bare_barrier();
-        uint4 fa0[2][FM], fb0[2][FN], fa1[2][FM], fb1[2][FN];
-        read(0, fa0, fb0);
-        for (int i = 0; i < nc; i += 2) {
-            step(i, fa0, fb0, fa1, fb1);
-            if (i + 1 < nc) step(i + 1, fa1, fb1, fa0, fb0);
+                for (int f = 0; f < FM; ++f) lds_after_wait(a0[f]);
+#pragma unroll
+                for (int f = 0; f < FN; ++f) lds_after_wait(b0[f]);
+                mma_w(a0, b0);
+                lds_wait();  // window 1 of chunk i: every read of chunk i done
+#pragma unroll
+                for (int f = 0; f < FM; ++f) lds_after_wait(a1[f]);
+#pragma unroll
+                for (int f = 0; f < FN; ++f) lds_after_wait(b1[f]);
+                bare_barrier();  // barrier i + 1
+                if (i + 1 < nc) read_w(i + 1, 0, a0, b0);
+                mma_w(a1, b1);
+            }
         }
         bare_barrier();  // the stages may be reused by a later call
     }

@@ -228,9 +228,12 @@ DEDUP_EDGE = [
     # cases above take them too: 64 x 200, 2 x 1500 and the fp32 1 x 1200)
     (12, 500, 64, 4096, 150, "bf16"),
     # full-k Gram tiles: one kept tile (slot written directly), and two kept
-    # tiles in fp32 (per-tile candidates merged by gram_finish)
+    # tiles in fp32 (per-tile candidates merged by gram_finish); one, two and
+    # three 128-byte chunks per row (the load ring's short starts)
     (128, 300, 4, 64, 100, "bf16"),
     (64, 600, 4, 128, 200, "f32"),
+    (128, 300, 4, 128, 100, "bf16"),
+    (128, 300, 4, 192, 100, "bf16"),
     # split-k cosine on 128 x 128 tiles at the boundary (65 anchors, 512 tokens)
     (16, 512, 65, 2048, 100, "bf16"),
     # four-token slice reduction at its smallest (8 tokens, many anchors)
