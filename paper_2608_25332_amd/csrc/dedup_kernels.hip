@@ -465,7 +465,9 @@ __global__ __launch_bounds__(64 * (WM * WN + NP)) void gram_tile_kernel(
 
     f32x4_t acc[G::FM][G::FN];
     __shared__ __attribute__((aligned(16))) char ring[G::LDS_BYTES];
-    G::template run_pc<NP>(ring, row_ptr, 0, d_bytes / G::CHUNK, acc);
+    // matrix waves past the last pruned row or kept slot of an edge tile skip
+    // their MFMAs (the epilogue ignores those rows and slots)
+    G::template run_pc<NP>(ring, row_ptr, 0, d_bytes / G::CHUNK, acc, Mp - m0, N1 - n0);
 
     // producer waves hold no products
     if (__builtin_amdgcn_readfirstlane(wave) < WM * WN) {

@@ -221,9 +221,14 @@ struct TileGemmLds {
     // up front).  A matrix wave meets barrier j + 1 after its last read of
     // chunk j and before its first read of chunk j + 1.  Both sides pass
     // nc + 2 barriers.  acc is meaningful in the matrix waves only.
+    //
+    // m_valid / n_valid: the A / B rows that count (the rest are padding the
+    // caller clamps to valid rows); a matrix wave whose A rows or B rows all
+    // lie past them keeps only the barriers and returns zero products.
     template <int NP, typename RowPtr>
     __device__ __forceinline__ static void run_pc(char *ring, RowPtr row_ptr, int c_begin, int c_end,
-                                                  f32x4_t (&acc)[FM][FN]) {
+                                                  f32x4_t (&acc)[FM][FN], int m_valid = BM,
+                                                  int n_valid = BN) {
         static_assert(NSTAGE == 3, "two chunks in flight and one being read");
         constexpr int IPP = ROWS * 8 / 64 / NP;  // load instructions per producer wave per stage
         static_assert(NP >= 1 && ROWS * 8 % (64 * NP) == 0, "stage rows must split over the producers");
@@ -268,6 +273,12 @@ struct TileGemmLds {
             }
         } else {
             const int wm = wave / WN, wn = wave % WN;
+            if (wm * SUB_M >= m_valid || wn * SUB_N >= n_valid) {
+                bare_barrier();  // barrier 0
+                for (int i = 0; i < nc; ++i) bare_barrier();
+                bare_barrier();
+                return;
+            }
             const int a_row = wm * SUB_M + (lane & 15);
             const int b_row = BM + wn * SUB_N + (lane & 15);
             const int kq = lane >> 4;
