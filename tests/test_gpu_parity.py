@@ -234,6 +234,11 @@ DEDUP_EDGE = [
     (64, 600, 4, 128, 200, "f32"),
     (128, 300, 4, 128, 100, "bf16"),
     (128, 300, 4, 192, 100, "bf16"),
+    # full-k Gram edge tiles where whole matrix waves lie past the last pruned
+    # row (136 of 256) and the last kept slot (64 of 128): they skip their
+    # MFMAs
+    (128, 200, 4, 128, 64, "bf16"),
+    (128, 200, 4, 64, 64, "f32"),
     # split-k cosine on 128 x 128 tiles at the boundary (65 anchors, 512 tokens)
     (16, 512, 65, 2048, 100, "bf16"),
     # four-token slice reduction at its smallest (8 tokens, many anchors)
