@@ -664,11 +664,13 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
 // mstart[b][s] (offset in the sample's list region) and the lists themselves
 // in mlist[b][g * Nv ...].  The assignment is staged in LDS; the waves take
 // consecutive token segments and sweep them twice, 64 tokens per
-// step: per-slot counts, then placement at offsets that keep the segments in
-// order.  Within a step, the lanes that hold the same slot are found with one
-// ballot per bit of the slot offset (the lanes whose offsets agree on every
-// bit), so a step costs the same whatever the number of distinct slots in it;
-// the lowest such lane updates the wave's counter of that slot.
+// step: per-slot counts (integer atomics on the wave's counters in LDS), then
+// placement at offsets that keep the segments in order.  In the placement the
+// lanes of a step that hold the same slot are found with one ballot per bit
+// of the slot offset (the lanes whose offsets agree on every bit), so a step
+// costs the same whatever the number of distinct slots in it; each lane takes
+// the next places in lane order and the lowest such lane advances the wave's
+// counter of that slot.
 // ----------------------------------------------------------------------------
 constexpr int kBucketBits = 8;
 constexpr int kBucketSlots = 1 << kBucketBits;
@@ -724,13 +726,12 @@ __global__ __launch_bounds__(kBucketNT) void bucket_kernel(const int32_t *__rest
     const int t0 = min(wave * seg, Nv), t1 = min(t0 + seg, Nv);
     int *wc = cur[wave];
 
-    // pass 1: this wave's count of every slot
+    // pass 1: this wave's count of every slot (integer atomics in LDS: the
+    // counts do not depend on their order)
     for (int c0 = t0; c0 < t1; c0 += 64) {
         const int j = c0 + lane;
         const int v = (j < t1) ? sa[j] - s0 : -1;
-        const bool rel = v >= 0 && v < kBucketSlots;
-        const unsigned long long same = same_slot_lanes(v, __ballot(rel));
-        if (rel && (same & lt) == 0ull) wc[v] += __popcll(same);
+        if (v >= 0 && v < kBucketSlots) atomicAdd(&wc[v], 1);
     }
     __syncthreads();
     // slot totals and offsets; then each wave's first position per slot
