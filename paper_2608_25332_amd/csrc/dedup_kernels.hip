@@ -770,10 +770,18 @@ __global__ __launch_bounds__(kBucketNT) void bucket_kernel(const int32_t *__rest
 }
 
 // merge_csr: as merge, with the member list read from the bucket output and
-// CPL 16-byte chunks per lane (a column block of 64 * CPL chunks): every
-// workgroup keeps CPL x kMergeU x 4 member chunks in flight per lane group.
-// The list entries are read where they are (they are the same for every lane
-// of a wave), so the chain per workgroup is count/offset, list, rows.
+// CPL 16-byte chunks per lane (a column block of 64 * CPL chunks).  The list
+// entries are read where they are (they are the same for every lane of a
+// wave), so the chain per workgroup is count/offset, list, rows.  Wave w adds
+// members w, w + 4, ... in list order.  Most slots hold a few members, one
+// or two per wave, and take them one row after the other; a slot with more
+// than kMergeFew members keeps kMergeHeavyU rows per wave in flight, so the
+// few slots with a hundred members or more do not set the kernel's end.
+// (Measured: loading repeats of the last member in place of the missing ones,
+// or several rows per wave in every slot, costs the light slots more than it
+// saves.)
+constexpr int kMergeFew = 8;
+constexpr int kMergeHeavyU = 4;
 template <int DT, int CPL>
 __global__ __launch_bounds__(kMergeNT) void merge_csr_kernel(
     const char *__restrict__ vis, int Nv, int d_bytes, const int32_t *__restrict__ mcount,
@@ -798,19 +806,35 @@ __global__ __launch_bounds__(kMergeNT) void merge_csr_kernel(
     for (int t = 0; t < CPL; ++t)
 #pragma unroll
         for (int e = 0; e < EPC; ++e) acc[t][e] = 0.f;
-    for (int m0 = wave; m0 < total; m0 += NW * kMergeU) {
-        uint4 v[kMergeU][CPL];
+    if (total > kMergeFew) {
+        // kMergeHeavyU rows in flight per wave; a member past the list loads
+        // nothing and adds zero (acc starts at +0, so adding +0 changes no bit)
+        for (int m0 = wave; m0 < total; m0 += NW * kMergeHeavyU) {
+            uint4 v[kMergeHeavyU][CPL];
 #pragma unroll
-        for (int u = 0; u < kMergeU; ++u) {
-            const char *row = vb + (size_t)lst[min(m0 + u * NW, total - 1)] * d_bytes;
+            for (int u = 0; u < kMergeHeavyU; ++u) {
+                const char *row = vb + (size_t)lst[min(m0 + u * NW, total - 1)] * d_bytes;
+                if (m0 + u * NW < total) {
 #pragma unroll
-            for (int t = 0; t < CPL; ++t) v[u][t] = ld16(row + (size_t)min(cc[t], nchunk - 1) * 16);
+                    for (int t = 0; t < CPL; ++t)
+                        v[u][t] = ld16(row + (size_t)min(cc[t], nchunk - 1) * 16);
+                } else {
+#pragma unroll
+                    for (int t = 0; t < CPL; ++t) v[u][t] = uint4{0u, 0u, 0u, 0u};
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kMergeHeavyU; ++u)
+#pragma unroll
+                for (int t = 0; t < CPL; ++t) add16<DT>(acc[t], v[u][t]);
         }
+    } else {
+        // at most kMergeFew / NW members per wave, one row after the other
+        for (int m = wave; m < total; m += NW) {
+            const char *row = vb + (size_t)lst[m] * d_bytes;
 #pragma unroll
-        for (int u = 0; u < kMergeU; ++u) {
-            if (m0 + u * NW >= total) break;
-#pragma unroll
-            for (int t = 0; t < CPL; ++t) add16<DT>(acc[t], v[u][t]);
+            for (int t = 0; t < CPL; ++t)
+                add16<DT>(acc[t], ld16(row + (size_t)min(cc[t], nchunk - 1) * 16));
         }
     }
     char *out = merged + ((size_t)b * N1 + s) * d_bytes;
