@@ -46,7 +46,9 @@ __device__ __forceinline__ void gather_block(const GatherArgs &ga, const int32_t
     char *d0 = g.dst + b * g.db + gr * g.dg;
     const int32_t *ib = idx + (size_t)b * k;
     uint4 v[kGatherIT];
-    int rr[kGatherIT], cc[kGatherIT];
+    int rr[kGatherIT], cc[kGatherIT], jj[kGatherIT];
+    // the row indices first, then every piece's load: a piece load issued
+    // between two index loads would be waited for with the next index
 #pragma unroll
     for (int it = 0; it < kGatherIT; ++it) {
         const int e = (sub * kGatherIT + it) * kGatherNT + threadIdx.x;
@@ -54,9 +56,14 @@ __device__ __forceinline__ void gather_block(const GatherArgs &ga, const int32_t
         const int r = ec / g.cpr, c = ec - r * g.cpr;
         rr[it] = e < ppp ? r : -1;
         cc[it] = c;
-        const int j = ib[r];
+        jj[it] = ib[r];
+    }
+    wait_vmcnt<0>();
+#pragma unroll
+    for (int it = 0; it < kGatherIT; ++it) {
+        const int j = jj[it];
         v[it] = uint4{0u, 0u, 0u, 0u};
-        if (j >= 0 && j < g.n_src) v[it] = ld16(s0 + (int64_t)j * g.sr + (int64_t)c * 16);
+        if (j >= 0 && j < g.n_src) v[it] = ld16(s0 + (int64_t)j * g.sr + (int64_t)cc[it] * 16);
     }
 #pragma unroll
     for (int it = 0; it < kGatherIT; ++it)
