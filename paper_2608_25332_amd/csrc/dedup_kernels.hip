@@ -380,8 +380,12 @@ __global__ __launch_bounds__(NT) void select_kernel(const float *__restrict__ p,
 // order of `better` (higher cosine, then lower slot).
 // ----------------------------------------------------------------------------
 // gram_finish: grid (ceil(Mp / 256), B).  Best column tile of every pruned
-// row, combined in tile order with the total order above.
+// row, combined in tile order with the total order above.  The candidates of
+// kFinU tiles are loaded at once (a loop that compares each one as it arrives
+// waits for every load in turn); past the last tile the last one repeats,
+// which cannot change a maximum under a total order.
 constexpr int kFinNT = 256;
+constexpr int kFinU = 16;
 
 __global__ __launch_bounds__(kFinNT) void gram_finish_kernel(const float *__restrict__ best_val,
                                                              const int32_t *__restrict__ best_slot,
@@ -391,17 +395,26 @@ __global__ __launch_bounds__(kFinNT) void gram_finish_kernel(const float *__rest
     const int b = blockIdx.y;
     const int m = blockIdx.x * kFinNT + threadIdx.x;
     if (m >= Mp) return;
+    const int tok = pruned[(size_t)b * Mp + m];
     float bv = -INFINITY;
     int bs = 0x7FFFFFFF;
-    for (int t = 0; t < ntn; ++t) {
-        const float v = best_val[((size_t)b * ntn + t) * Mp + m];
-        const int s = best_slot[((size_t)b * ntn + t) * Mp + m];
-        if (better(v, s, bv, bs)) {
-            bv = v;
-            bs = s;
+    for (int t0 = 0; t0 < ntn; t0 += kFinU) {
+        float v[kFinU];
+        int s[kFinU];
+#pragma unroll
+        for (int u = 0; u < kFinU; ++u) {
+            const size_t at = ((size_t)b * ntn + min(t0 + u, ntn - 1)) * Mp + m;
+            v[u] = best_val[at];
+            s[u] = best_slot[at];
         }
+#pragma unroll
+        for (int u = 0; u < kFinU; ++u)
+            if (better(v[u], s[u], bv, bs)) {
+                bv = v[u];
+                bs = s[u];
+            }
     }
-    assign[(size_t)b * Nv + pruned[(size_t)b * Mp + m]] = bs;
+    assign[(size_t)b * Nv + tok] = bs;
 }
 
 template <int DT, int NS, int BM, int BN>
