@@ -227,6 +227,11 @@ DEDUP_EDGE = [
     # wide split-k Gram tiles (128 x 96), ragged in both directions (three
     # cases above take them too: 64 x 200, 2 x 1500 and the fp32 1 x 1200)
     (12, 500, 64, 4096, 150, "bf16"),
+    # member-list merge: 10-37 members in every slot (the many-member path,
+    # four rows per wave in flight, ragged last rounds), then 2-16 members
+    # (both paths in one launch)
+    (2, 400, 8, 256, 20, "f32"),
+    (3, 401, 8, 192, 50, "bf16"),
     # full-k Gram tiles: one kept tile (slot written directly), and two kept
     # tiles in fp32 (per-tile candidates merged by gram_finish); one, two and
     # three 128-byte chunks per row (the load ring's short starts)
