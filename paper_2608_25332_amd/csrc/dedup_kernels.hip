@@ -537,8 +537,9 @@ __global__ __launch_bounds__(64 * (WM * WN + NP)) void gram_tile_kernel(
 // one slot s and one 1 KB column block (16 bytes per lane).  The members of s
 // (the tokens whose assignment is s, the kept token itself included) are
 // listed in ascending token order with one block scan per round of 4096
-// tokens; the four waves then take every fourth member, so a slot with many
-// members keeps 4 x kMergeU rows in flight instead of a serial chain, and the
+// tokens; the four waves then take every fourth member, each wave one row
+// after the other (the slots of the inputs this form serves hold a few
+// members each; loading a wave's members together measured slower), and the
 // column split spreads one slot's bytes over several CUs.  Each wave adds its
 // members in list order (fp32) and the four partial sums are combined in wave
 // order, so the result does not depend on timing.
@@ -546,7 +547,6 @@ __global__ __launch_bounds__(64 * (WM * WN + NP)) void gram_tile_kernel(
 constexpr int kMergeNT = 256;
 constexpr int kMergeRound = 4096;                  // tokens listed per round
 constexpr int kMergeTPT = kMergeRound / kMergeNT;  // tokens per thread per round
-constexpr int kMergeU = 8;                         // member rows in flight per wave
 
 // Adds the elements of one 16-byte chunk to acc (fp32).
 template <int DT>
@@ -650,17 +650,7 @@ __global__ __launch_bounds__(kMergeNT) void merge_kernel(const char *__restrict_
         for (int e = 0; e < kMergeTPT; ++e)
             if (e < tpt && t0 + e < rend && a[e] == s) list[w++] = t0 + e;
         __syncthreads();
-        for (int m0 = wave; m0 < cnt; m0 += NW * kMergeU) {
-            uint4 v[kMergeU];
-#pragma unroll
-            for (int u = 0; u < kMergeU; ++u)
-                v[u] = ld16(col + (size_t)list[min(m0 + u * NW, cnt - 1)] * d_bytes);
-#pragma unroll
-            for (int u = 0; u < kMergeU; ++u) {
-                if (m0 + u * NW >= cnt) break;
-                add16<DT>(acc, v[u]);
-            }
-        }
+        for (int m = wave; m < cnt; m += NW) add16<DT>(acc, ld16(col + (size_t)list[m] * d_bytes));
         total += cnt;
         __syncthreads();  // the list is rewritten by the next round
     }
